@@ -1,0 +1,122 @@
+/*
+ * atsi.h -- C ABI of the block-int4 quantised-linear hot path with host
+ * streaming (tensor-granularity placement, ATSInfer, arxiv 2607.10183).
+ *
+ * The unit of placement is one weight tensor (Sec. 4.3.2: each tensor i has a
+ * size s_i and a backend/placement b_i).  A tensor is read either from HBM
+ * (the GPU resident region, Sec. 4.2.1) or from pinned host memory (CPU
+ * pinned-memory storage, Sec. 4.2.1); a host tensor is copied into a GPU
+ * temporary buffer ("slot") on a transfer stream and consumed on a compute
+ * stream, with events ordering the two (Sec. 4.2.2).  All compute runs on the
+ * GPU: every host tensor is promoted for each use (the all-GPU runtime
+ * assignment of Sec. 4.4.1), and the engine hides the copies behind compute.
+ *
+ * Weight format (the paper uses INT4 weights without fixing a layout, Sec. 5.1):
+ *   codes  uint8 [N][K/2]  -- row n = output feature n; byte j of a row holds
+ *                             input 2j in its low nibble and 2j+1 in its high
+ *                             nibble, each as u = q + 8 with q in [-8, 7];
+ *   scales uint16[N][K/32] -- IEEE fp16 bit patterns, one per 32 inputs;
+ *   weight w[n][k] = scale[n][k/32] * q[n][k].
+ * Activations are fp16 row-major [M][K]; outputs fp16 row-major [M][N],
+ * accumulated in fp32 and rounded to nearest-even once.  Dequantised weights
+ * must be finite in fp16 (|scale| * 8 <= 65504).
+ *
+ * Ownership: the caller owns every buffer (weights in HBM, pinned host
+ * weights, activations, the workspace); the library keeps borrowed pointers
+ * until atsi_destroy and itself allocates only host bookkeeping and HIP
+ * events.  Device pointers must be 16-byte aligned.
+ *
+ * Streams: calls only enqueue work on the compute stream (and copies on the
+ * transfer stream); they return before the GPU finishes.  Inputs must stay
+ * valid until atsi_sync returns.
+ *
+ * Errors: every call validates its arguments before any HIP call and returns
+ * a status; atsi_last_error(ctx) gives a message.  Failures reported by the
+ * HIP runtime are latched and returned by the next call and by atsi_sync.
+ * No C++ exception crosses this boundary.  A context is not thread-safe.
+ */
+#ifndef ATSI_H
+#define ATSI_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  ATSI_OK = 0,
+  ATSI_E_INVALID = 1,        /* null or malformed argument */
+  ATSI_E_SHAPE = 2,          /* unsupported shape (K % 32, group != 32, M range) */
+  ATSI_E_UNKNOWN_TENSOR = 3, /* tensor id not registered */
+  ATSI_E_NO_COPY = 4,        /* placement points at a location with no copy */
+  ATSI_E_WORKSPACE = 5,      /* workspace too small for slots or scratch */
+  ATSI_E_HIP = 6,            /* HIP runtime error (also: no GPU present) */
+  ATSI_E_STATE = 7           /* call not valid in the current state */
+} atsi_status;
+
+typedef struct atsi_ctx atsi_ctx;
+typedef int32_t atsi_tid;
+
+/* Create a context on `device`.
+ * compute_stream, transfer_stream: distinct, non-null hipStream_t handles
+ *   (the paper's compute stream and transfer stream, Sec. 4.2.2).
+ * workspace: device buffer of workspace_bytes, carved into n_slots temporary
+ *   buffers for streamed tensors (Sec. 4.2.1, GPU temporary buffers) and a
+ *   scratch region for intermediate activations; 256-byte aligned.
+ * n_slots: number of temporary buffers, 2..64.
+ * On a machine without a usable GPU this returns ATSI_E_HIP and *out = NULL. */
+atsi_status atsi_create(int device, void* compute_stream, void* transfer_stream,
+                        void* workspace, size_t workspace_bytes, int n_slots,
+                        atsi_ctx** out);
+
+/* Drain both streams and free the context (events, host bookkeeping). */
+atsi_status atsi_destroy(atsi_ctx* ctx);
+
+/* Message of the last failure on ctx (or of the last failed atsi_create when
+ * ctx is NULL).  Valid until the next call on the same context. */
+const char* atsi_last_error(const atsi_ctx* ctx);
+
+/* One block-int4 weight tensor: K inputs, N outputs, group must be 32 and
+ * K % 32 == 0.  dev_* point at an HBM copy, host_* at a pinned host copy;
+ * either pair may be NULL, not both.  The tensor starts HBM-resident when it
+ * has an HBM copy, host-resident otherwise. */
+typedef struct {
+  int64_t K, N;
+  int32_t group;
+  const uint8_t* dev_codes;
+  const uint16_t* dev_scales;
+  const uint8_t* host_codes;
+  const uint16_t* host_scales;
+} atsi_qtensor;
+
+/* Register a tensor (its size s_i and locations, Sec. 4.3.2); ids count from 0. */
+atsi_status atsi_tensor_register(atsi_ctx* ctx, const atsi_qtensor* t, atsi_tid* out);
+
+/* Set the placement of tensors 0..n-1 (Sec. 4.3.2, b_i): host_mask[i] = 1
+ * reads tensor i from pinned host memory through a temporary buffer, 0 from
+ * HBM.  n must equal the number of registered tensors.  Re-lays out the
+ * temporary buffers (each sized for the largest host tensor); fails with
+ * ATSI_E_WORKSPACE if n_slots of them do not fit.  Drains the streams. */
+atsi_status atsi_set_placement(atsi_ctx* ctx, const uint8_t* host_mask, int32_t n);
+
+/* y[M][N] = x[M][K] . W^T for tensor w (fp16 in and out, fp32 accumulation).
+ * Decode sizes (M <= 4) run a dequantising GEMV that streams the codes once;
+ * larger M runs a dequantise-into-LDS fp16 MFMA GEMM (prefill, Sec. 2.2 and
+ * the chunked prefill of Sec. 5.1).  A host-resident w is first copied into a
+ * temporary buffer on the transfer stream (Sec. 4.2.2).  1 <= M <= 65536. */
+atsi_status atsi_linear(atsi_ctx* ctx, atsi_tid w, const void* x_f16, int64_t M, void* y_f16);
+
+/* Wait for both streams; returns the first latched asynchronous error. */
+atsi_status atsi_sync(atsi_ctx* ctx);
+
+/* Test export: the signed codes q[N][K] (int8, device buffer) of tensor w as
+ * the library reads them, from wherever w currently lives. */
+atsi_status atsi_debug_unpack(atsi_ctx* ctx, atsi_tid w, int8_t* q_out);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ATSI_H */

@@ -1,0 +1,108 @@
+"""Thin ctypes binding of libatsi.so: the C ABI in include/atsi.h, same names.
+
+Argument marshalling only: every step of the hot path runs in the library's
+HIP kernels.  Functions raise AtsiError when the library returns a non-OK
+status.  Pointers are plain integers (torch: ``tensor.data_ptr()``; streams:
+``torch.cuda.Stream().cuda_stream``).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libatsi.so")
+
+STATUS = {0: "ATSI_OK", 1: "ATSI_E_INVALID", 2: "ATSI_E_SHAPE", 3: "ATSI_E_UNKNOWN_TENSOR",
+          4: "ATSI_E_NO_COPY", 5: "ATSI_E_WORKSPACE", 6: "ATSI_E_HIP", 7: "ATSI_E_STATE"}
+
+
+class AtsiError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS.get(status, status)}: {message}")
+        self.status = status
+
+
+class atsi_qtensor(ctypes.Structure):
+    _fields_ = [("K", ctypes.c_int64), ("N", ctypes.c_int64), ("group", ctypes.c_int32),
+                ("dev_codes", ctypes.c_void_p), ("dev_scales", ctypes.c_void_p),
+                ("host_codes", ctypes.c_void_p), ("host_scales", ctypes.c_void_p)]
+
+
+_P = ctypes.c_void_p
+_SIGS = {
+    "atsi_create": ([ctypes.c_int, _P, _P, _P, ctypes.c_size_t, ctypes.c_int, ctypes.POINTER(_P)], ctypes.c_int),
+    "atsi_destroy": ([_P], ctypes.c_int),
+    "atsi_last_error": ([_P], ctypes.c_char_p),
+    "atsi_tensor_register": ([_P, ctypes.POINTER(atsi_qtensor), ctypes.POINTER(ctypes.c_int32)], ctypes.c_int),
+    "atsi_set_placement": ([_P, _P, ctypes.c_int32], ctypes.c_int),
+    "atsi_linear": ([_P, ctypes.c_int32, _P, ctypes.c_int64, _P], ctypes.c_int),
+    "atsi_sync": ([_P], ctypes.c_int),
+    "atsi_debug_unpack": ([_P, ctypes.c_int32, _P], ctypes.c_int),
+}
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library; raises ImportError (never falls back) when it is not built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is not built: run `python -m paper_2607_10183_amd.build` "
+                              "(there is no CPU fallback)")
+        l = ctypes.CDLL(LIB_PATH)
+        for name, (args, res) in _SIGS.items():
+            f = getattr(l, name)
+            f.argtypes = args
+            f.restype = res
+        _lib = l
+    return _lib
+
+
+def _check(ctx, status: int) -> None:
+    if status != 0:
+        msg = lib().atsi_last_error(ctx)
+        raise AtsiError(status, msg.decode() if msg else "")
+
+
+def atsi_create(device: int, compute_stream: int, transfer_stream: int, workspace: int,
+                workspace_bytes: int, n_slots: int) -> int:
+    out = _P()
+    _check(None, lib().atsi_create(device, compute_stream, transfer_stream, workspace, workspace_bytes,
+                                   n_slots, ctypes.byref(out)))
+    return out.value
+
+
+def atsi_destroy(ctx: int) -> None:
+    _check(ctx, lib().atsi_destroy(ctx))
+
+
+def atsi_last_error(ctx: int | None) -> str:
+    m = lib().atsi_last_error(ctx)
+    return m.decode() if m else ""
+
+
+def atsi_tensor_register(ctx: int, K: int, N: int, dev_codes: int = 0, dev_scales: int = 0,
+                         host_codes: int = 0, host_scales: int = 0, group: int = 32) -> int:
+    d = atsi_qtensor(K, N, group, dev_codes or None, dev_scales or None, host_codes or None, host_scales or None)
+    out = ctypes.c_int32()
+    _check(ctx, lib().atsi_tensor_register(ctx, ctypes.byref(d), ctypes.byref(out)))
+    return out.value
+
+
+def atsi_set_placement(ctx: int, host_mask) -> None:
+    arr = (ctypes.c_uint8 * len(host_mask))(*[int(v) for v in host_mask])
+    _check(ctx, lib().atsi_set_placement(ctx, ctypes.cast(arr, _P), len(host_mask)))
+
+
+def atsi_linear(ctx: int, w: int, x: int, M: int, y: int) -> None:
+    _check(ctx, lib().atsi_linear(ctx, w, x, M, y))
+
+
+def atsi_sync(ctx: int) -> None:
+    _check(ctx, lib().atsi_sync(ctx))
+
+
+def atsi_debug_unpack(ctx: int, w: int, q_out: int) -> None:
+    _check(ctx, lib().atsi_debug_unpack(ctx, w, q_out))

@@ -1,0 +1,236 @@
+// Prefill-path dequantising GEMM for block-int4 weights on CDNA4 (gfx950).
+//
+// Prefill runs a whole chunk of tokens through each linear (Sec. 2.2, chunked
+// prefill in Sec. 5.1), a dense contraction, so it runs on the matrix cores:
+//   * a 256-thread workgroup owns a BM x BN output tile; its four waves own
+//     (BM/WM) x (BN/WN) sub-tiles built from 32x32x16 fp16 MFMAs with fp32
+//     accumulators;
+//   * per K step of 64 (two scale groups) the activation tile is copied to LDS
+//     and the weight tile is dequantised into LDS as fp16: nibble -> 1024 + u
+//     by mantissa OR, minus 1032 (exact), times the group scale (one rounding);
+//     activations stay fp16, so the only operand rounding is w = RNE16(s * q);
+//   * the next K step's global loads are issued before the current step's
+//     MFMAs (register double-buffering) and LDS is double-buffered;
+//   * LDS rows are padded by 16 bytes so the 16-byte fragment reads of a
+//     wavefront hit distinct banks;
+//   * workgroup ids are remapped so that the M tiles sharing one weight tile
+//     run on the same XCD and reuse it from that XCD's L2.
+#include "common.h"
+
+namespace atsi {
+namespace {
+
+constexpr int kBlock = 256;
+constexpr int BK = 64;           // K per LDS stage = two scale groups
+constexpr int LDSP = BK + 8;     // padded LDS row length in halves
+constexpr uint32_t kMagic = 0x64006400u;
+
+typedef _Float16 half8_t __attribute__((ext_vector_type(8)));
+typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
+typedef float float16_t __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ uint32_t pk_sub_mul(uint32_t t, half2_t off, half2_t s) {
+  half2_t v = __builtin_bit_cast(half2_t, t);
+  v = (v - off) * s;  // q exactly, then one rounding of s * q
+  return __builtin_bit_cast(uint32_t, v);
+}
+
+// Dequantise one group (16 code bytes) into 32 fp16 weights in natural k order.
+__device__ __forceinline__ void dequant_group(const uint4& cw, uint16_t sbits, uint4 (&out)[4]) {
+  const _Float16 s = __builtin_bit_cast(_Float16, sbits);
+  const half2_t s2 = {s, s};
+  const half2_t off = {(_Float16)1032.0f, (_Float16)1032.0f};
+  const uint32_t w4[4] = {cw.x, cw.y, cw.z, cw.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t w = w4[i];
+    const uint32_t t0 = pk_sub_mul((w & 0x000F000Fu) | kMagic, off, s2);          // (k0, k4)
+    const uint32_t t1 = pk_sub_mul(((w >> 4) & 0x000F000Fu) | kMagic, off, s2);   // (k1, k5)
+    const uint32_t t2 = pk_sub_mul(((w >> 8) & 0x000F000Fu) | kMagic, off, s2);   // (k2, k6)
+    const uint32_t t3 = pk_sub_mul(((w >> 12) & 0x000F000Fu) | kMagic, off, s2);  // (k3, k7)
+    out[i].x = __builtin_amdgcn_perm(t1, t0, 0x05040100u);  // (k0, k1)
+    out[i].y = __builtin_amdgcn_perm(t3, t2, 0x05040100u);  // (k2, k3)
+    out[i].z = __builtin_amdgcn_perm(t1, t0, 0x07060302u);  // (k4, k5)
+    out[i].w = __builtin_amdgcn_perm(t3, t2, 0x07060302u);  // (k6, k7)
+  }
+}
+
+template <int BM, int BN, int WM, int WN>
+__global__ __launch_bounds__(kBlock, 2) void q4_gemm_kernel(QView w, const __half* __restrict__ x, int M,
+                                                            __half* __restrict__ y, int ldy, int ep,
+                                                            const __half* res, int tiles_m, int tiles_n) {
+  static_assert(WM * WN == 4, "four waves");
+  constexpr int SM = BM / WM, SN = BN / WN;  // wave sub-tile
+  constexpr int FM = SM / 32, FN = SN / 32;  // 32x32 fragments per wave
+  static_assert(FM >= 1 && FN >= 1, "sub-tile at least 32x32");
+  // global -> register staging per thread
+  constexpr int XV = BM * BK / 8 / kBlock;   // uint4 of activations per thread
+  constexpr int WG = (BN * 2 + kBlock - 1) / kBlock;  // weight groups per thread (BN rows x 2 groups)
+  static_assert(XV >= 1 && (BM * BK / 8) % kBlock == 0, "activation tile must split evenly");
+
+  __shared__ __attribute__((aligned(16))) _Float16 As[2][BM * LDSP];
+  __shared__ __attribute__((aligned(16))) _Float16 Bs[2][BN * LDSP];
+
+  // XCD-aware tile order: consecutive ids land on different XCDs (8-way
+  // round robin); give each XCD a contiguous run of tiles, M fastest.
+  const int ntiles = tiles_m * tiles_n;
+  int bid = blockIdx.x;
+  if ((ntiles & 7) == 0) bid = (bid & 7) * (ntiles >> 3) + (bid >> 3);
+  const int tm = bid % tiles_m, tn = bid / tiles_m;
+  const int m0 = tm * BM, n0 = tn * BN;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+  const int K = w.K;
+  const int ngrp = K / 32;
+  const int nk = (K + BK - 1) / BK;
+
+  uint4 xr[XV];
+  uint4 cr[WG];
+  uint16_t sr[WG];
+
+  auto gload = [&](int kt) {
+    const int k0 = kt * BK;
+#pragma unroll
+    for (int i = 0; i < XV; ++i) {
+      const int idx = tid + i * kBlock;    // 8-half chunk index within the tile
+      const int r = idx / (BK / 8), cchunk = idx % (BK / 8);
+      const int m = m0 + r, k = k0 + cchunk * 8;
+      if (m < M && k < K)
+        xr[i] = *reinterpret_cast<const uint4*>(x + (size_t)m * K + k);
+      else
+        xr[i] = make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < WG; ++i) {
+      const int idx = tid + i * kBlock;
+      if (idx >= BN * 2) break;
+      const int r = idx >> 1, g = (k0 >> 5) + (idx & 1);
+      const int n = n0 + r;
+      if (n < w.N && g < ngrp) {
+        cr[i] = *reinterpret_cast<const uint4*>(w.codes + (size_t)n * (K / 2) + (size_t)g * 16);
+        sr[i] = w.scales[(size_t)n * ngrp + g];
+      } else {
+        cr[i] = make_uint4(0x88888888u, 0x88888888u, 0x88888888u, 0x88888888u);  // q = 0
+        sr[i] = 0;
+      }
+    }
+  };
+  auto lstore = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < XV; ++i) {
+      const int idx = tid + i * kBlock;
+      const int r = idx / (BK / 8), cchunk = idx % (BK / 8);
+      *reinterpret_cast<uint4*>(&As[buf][r * LDSP + cchunk * 8]) = xr[i];
+    }
+#pragma unroll
+    for (int i = 0; i < WG; ++i) {
+      const int idx = tid + i * kBlock;
+      if (idx >= BN * 2) break;
+      const int r = idx >> 1, gl = idx & 1;
+      uint4 o[4];
+      dequant_group(cr[i], sr[i], o);
+      uint4* dst = reinterpret_cast<uint4*>(&Bs[buf][r * LDSP + gl * 32]);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) dst[j] = o[j];
+    }
+  };
+
+  float16_t acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+  gload(0);
+  lstore(0);
+  __syncthreads();
+
+  const int frow = lane & 31, fk = (lane >> 5) * 8;
+  for (int kt = 0; kt < nk; ++kt) {
+    const int buf = kt & 1;
+    if (kt + 1 < nk) gload(kt + 1);
+#pragma unroll
+    for (int ks = 0; ks < BK / 16; ++ks) {
+      half8_t a[FM], b[FN];
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+        a[i] = *reinterpret_cast<const half8_t*>(&As[buf][(wm * SM + i * 32 + frow) * LDSP + ks * 16 + fk]);
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        b[j] = *reinterpret_cast<const half8_t*>(&Bs[buf][(wn * SN + j * 32 + frow) * LDSP + ks * 16 + fk]);
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+    if (kt + 1 < nk) {
+      lstore(buf ^ 1);
+      __syncthreads();
+    }
+  }
+
+  // D layout of a 32x32 MFMA block: lane l holds column l % 32; accumulator v
+  // holds row 8 * (v / 4) + 4 * (l / 32) + v % 4.
+  const int col = lane & 31, rq = (lane >> 5) * 4;
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int n = n0 + wn * SN + j * 32 + col;
+      if (n >= w.N) continue;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int m = m0 + wm * SM + i * 32 + 8 * (v >> 2) + rq + (v & 3);
+        if (m < M) {
+          const size_t at = (size_t)m * ldy + n;
+          float o = acc[i][j][v];
+          if (ep == kResidual) o += __half2float(res[at]);
+          y[at] = __float2half_rn(o);
+        }
+      }
+    }
+}
+
+template <int BM, int BN, int WM, int WN>
+hipError_t launch_tile(const QView& w, const __half* x, int M, __half* y, int ldy, Epilogue ep, const __half* res,
+                       hipStream_t s) {
+  const int tm = (M + BM - 1) / BM, tn = (w.N + BN - 1) / BN;
+  hipLaunchKernelGGL((q4_gemm_kernel<BM, BN, WM, WN>), dim3(tm * tn), dim3(kBlock), 0, s, w, x, M, y, ldy, (int)ep,
+                     res, tm, tn);
+  return hipGetLastError();
+}
+
+// unpack kernel for the debug export: q[n][k] = nibble - 8
+__global__ void unpack_kernel(QView w, int8_t* q) {
+  const size_t total = (size_t)w.N * (w.K / 2);
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (size_t)gridDim.x * blockDim.x) {
+    const uint8_t b = w.codes[i];
+    q[2 * i] = (int8_t)((b & 0xF) - 8);
+    q[2 * i + 1] = (int8_t)((b >> 4) - 8);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_gemm(const QView& w, const __half* x, int M, __half* y, int ldy, Epilogue ep, const __half* res,
+                       hipStream_t s) {
+  // Prefer 128x128 tiles; fall back to narrower tiles when the grid would
+  // leave most of the 256 CUs idle.
+  const long t128 = (long)((M + 127) / 128) * ((w.N + 127) / 128);
+  if (M <= 64) return launch_tile<64, 64, 2, 2>(w, x, M, y, ldy, ep, res, s);
+  if (t128 >= 256) return launch_tile<128, 128, 2, 2>(w, x, M, y, ldy, ep, res, s);
+  return launch_tile<128, 64, 2, 2>(w, x, M, y, ldy, ep, res, s);
+}
+
+hipError_t launch_unpack(const QView& w, int8_t* q, hipStream_t s) {
+  const size_t total = (size_t)w.N * (w.K / 2);
+  const int blocks = (int)std::min<size_t>((total + 255) / 256, 4096);
+  hipLaunchKernelGGL(unpack_kernel, dim3(blocks), dim3(256), 0, s, w, q);
+  return hipGetLastError();
+}
+
+}  // namespace atsi

@@ -1,0 +1,179 @@
+// Decode-path dequantising GEMV for block-int4 weights on CDNA4 (gfx950).
+//
+// y[m][n] = sum_g s[n][g] * sum_{k in g} q[n][k] * x[m][k] for M <= 4 tokens.
+// Decode reads every weight byte once per token (the memory-bound phase,
+// Sec. 2.2), so the kernel is organised around streaming the packed codes at
+// HBM rate:
+//   * a wavefront owns RW consecutive rows; lane l handles groups l, l+64, ...
+//     of every row, so one 128-bit load per lane covers one whole group of 32
+//     inputs and a wave instruction reads 1 KiB contiguous from a row;
+//   * nibbles become fp16 values 1024 + u by OR-ing them into the mantissa of
+//     0x6400 (two per 32-bit register), then v_dot2_f32_f16 multiplies two of
+//     them by two activations and accumulates in fp32;
+//   * the +1032 offset of (1024 + u) against q = u - 8 is removed once per
+//     group with the group sum of x, computed once per chunk and reused by the
+//     RW rows; the group partial is scaled by its fp16 scale in fp32;
+//   * activations are read once per wave and permuted in registers to the
+//     (k, k+4) pairing the nibble extraction yields;
+//   * lanes reduce across the wavefront with DPP/shuffles; one lane per
+//     (row, token) rounds to fp16 once.
+#include "common.h"
+
+namespace atsi {
+namespace {
+
+constexpr int kWave = 64;
+constexpr int kBlock = 256;
+constexpr uint32_t kMagic = 0x64006400u;  // fp16 1024.0 in both halves
+
+typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
+  return __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, a), __builtin_bit_cast(half2_t, b), c, false);
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+  return v;
+}
+
+// x pairs of one 32-input group in nibble order, plus the group sum.
+template <int MT>
+struct XChunk {
+  uint32_t p[MT][16];
+  float sum[MT];
+};
+
+template <int MT>
+__device__ __forceinline__ void load_x(XChunk<MT>& xc, const __half* __restrict__ x, int K, int M, int c) {
+#pragma unroll
+  for (int m = 0; m < MT; ++m) {
+    if (m < M) {
+      const uint4* src = reinterpret_cast<const uint4*>(x + (size_t)m * K + (size_t)c * kGroup);
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {       // 8 inputs per 16 bytes
+        uint4 d = src[b];
+        xc.p[m][4 * b + 0] = __builtin_amdgcn_perm(d.z, d.x, 0x05040100u);  // (x0, x4)
+        xc.p[m][4 * b + 1] = __builtin_amdgcn_perm(d.z, d.x, 0x07060302u);  // (x1, x5)
+        xc.p[m][4 * b + 2] = __builtin_amdgcn_perm(d.w, d.y, 0x05040100u);  // (x2, x6)
+        xc.p[m][4 * b + 3] = __builtin_amdgcn_perm(d.w, d.y, 0x07060302u);  // (x3, x7)
+      }
+      float s = 0.f;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) s = dot2(xc.p[m][i], 0x3C003C00u, s);  // (1.0, 1.0)
+      xc.sum[m] = s;
+    } else {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) xc.p[m][i] = 0u;
+      xc.sum[m] = 0.f;
+    }
+  }
+}
+
+// sum_k (1024 + u_k) x_k over one group, per token.
+template <int MT>
+__device__ __forceinline__ void group_dot(const uint4& cw, const XChunk<MT>& xc, float (&part)[MT]) {
+#pragma unroll
+  for (int m = 0; m < MT; ++m) part[m] = 0.f;
+  const uint32_t w4[4] = {cw.x, cw.y, cw.z, cw.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t w = w4[i];
+    const uint32_t t0 = (w & 0x000F000Fu) | kMagic;          // inputs 8i+0, 8i+4
+    const uint32_t t1 = ((w >> 4) & 0x000F000Fu) | kMagic;   // 8i+1, 8i+5
+    const uint32_t t2 = ((w >> 8) & 0x000F000Fu) | kMagic;   // 8i+2, 8i+6
+    const uint32_t t3 = ((w >> 12) & 0x000F000Fu) | kMagic;  // 8i+3, 8i+7
+#pragma unroll
+    for (int m = 0; m < MT; ++m) {
+      float a = part[m];
+      a = dot2(t0, xc.p[m][4 * i + 0], a);
+      a = dot2(t1, xc.p[m][4 * i + 1], a);
+      a = dot2(t2, xc.p[m][4 * i + 2], a);
+      a = dot2(t3, xc.p[m][4 * i + 3], a);
+      part[m] = a;
+    }
+  }
+}
+
+template <int MT, int RW>
+__global__ __launch_bounds__(kBlock) void q4_gemv_kernel(QView w, const __half* __restrict__ x, int M,
+                                                          __half* __restrict__ y, int ldy, int ep,
+                                                          const __half* res) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = threadIdx.x / kWave;
+  const int row0 = (blockIdx.x * (kBlock / kWave) + wave) * RW;
+  if (row0 >= w.N) return;
+  const int K = w.K;
+  const int nchunk = K / kGroup;
+  const size_t rbytes = (size_t)K / 2;
+
+  float acc[RW][MT];
+#pragma unroll
+  for (int r = 0; r < RW; ++r)
+#pragma unroll
+    for (int m = 0; m < MT; ++m) acc[r][m] = 0.f;
+
+  for (int c = lane; c < nchunk; c += kWave) {
+    uint4 cw[RW];
+    float sc[RW];
+#pragma unroll
+    for (int r = 0; r < RW; ++r) {
+      const int row = min(row0 + r, w.N - 1);  // clamped rows are computed, never stored
+      cw[r] = *reinterpret_cast<const uint4*>(w.codes + (size_t)row * rbytes + (size_t)c * 16);
+      sc[r] = __half2float(__ushort_as_half(w.scales[(size_t)row * nchunk + c]));
+    }
+    XChunk<MT> xc;
+    load_x<MT>(xc, x, K, M, c);
+#pragma unroll
+    for (int r = 0; r < RW; ++r) {
+      float part[MT];
+      group_dot<MT>(cw[r], xc, part);
+#pragma unroll
+      for (int m = 0; m < MT; ++m) acc[r][m] = fmaf(sc[r], part[m] - 1032.f * xc.sum[m], acc[r][m]);
+    }
+  }
+
+#pragma unroll
+  for (int r = 0; r < RW; ++r)
+#pragma unroll
+    for (int m = 0; m < MT; ++m) {
+      const float v = wave_sum(acc[r][m]);
+      const int row = row0 + r;
+      if (lane == r * MT + m && row < w.N && m < M) {
+        float o = v;
+        const size_t at = (size_t)m * ldy + row;
+        if (ep == kResidual) o += __half2float(res[at]);
+        y[at] = __float2half_rn(o);
+      }
+    }
+}
+
+template <int MT, int RW>
+hipError_t launch_mt_rw(const QView& w, const __half* x, int M, __half* y, int ldy, Epilogue ep,
+                        const __half* res, hipStream_t s) {
+  const int rows_per_block = (kBlock / kWave) * RW;
+  const int blocks = (w.N + rows_per_block - 1) / rows_per_block;
+  hipLaunchKernelGGL((q4_gemv_kernel<MT, RW>), dim3(blocks), dim3(kBlock), 0, s, w, x, M, y, ldy, (int)ep, res);
+  return hipGetLastError();
+}
+
+template <int MT>
+hipError_t launch_mt(const QView& w, const __half* x, int M, __half* y, int ldy, Epilogue ep, const __half* res,
+                     hipStream_t s) {
+  // Pick rows per wave so the grid has at least ~2 blocks per CU when N allows.
+  if (w.N >= 8192) return launch_mt_rw<MT, 4>(w, x, M, y, ldy, ep, res, s);
+  if (w.N >= 4096) return launch_mt_rw<MT, 2>(w, x, M, y, ldy, ep, res, s);
+  return launch_mt_rw<MT, 1>(w, x, M, y, ldy, ep, res, s);
+}
+
+}  // namespace
+
+hipError_t launch_gemv(const QView& w, const __half* x, int M, __half* y, int ldy, Epilogue ep,
+                       const __half* res, hipStream_t s) {
+  if (M == 1) return launch_mt<1>(w, x, M, y, ldy, ep, res, s);
+  if (M == 2) return launch_mt<2>(w, x, M, y, ldy, ep, res, s);
+  return launch_mt<4>(w, x, M, y, ldy, ep, res, s);
+}
+
+}  // namespace atsi

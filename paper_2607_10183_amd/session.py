@@ -1,0 +1,119 @@
+"""Device-memory and stream plumbing around the C ABI, using PyTorch.
+
+PyTorch only allocates (HBM tensors, pinned host tensors, the workspace) and
+creates the two streams; all compute goes through libatsi.so.
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from . import atsi
+
+
+class Session:
+    """One atsi context on one GPU with its own compute and transfer streams."""
+
+    def __init__(self, workspace_bytes: int = 1 << 30, n_slots: int = 4, device: int = 0):
+        if not torch.cuda.is_available():
+            raise RuntimeError("no GPU visible to torch; the atsi library has no CPU path")
+        self.device = torch.device("cuda", device)
+        self.cs = torch.cuda.Stream(device=self.device)
+        self.ts = torch.cuda.Stream(device=self.device)
+        self.ws = torch.empty(workspace_bytes, dtype=torch.uint8, device=self.device)
+        self.ctx = atsi.atsi_create(device, self.cs.cuda_stream, self.ts.cuda_stream, self.ws.data_ptr(),
+                                    workspace_bytes, n_slots)
+        self._keep: list = []
+        self.shapes: list[tuple[int, int]] = []
+        self.placement: list[int] = []  # current host mask, mirrors the library's
+
+    # ---------------------------------------------------------------- tensors
+    def register(self, codes: np.ndarray, scales: np.ndarray, hbm: bool = True, host: bool = False) -> int:
+        """Register a block-int4 tensor (codes uint8[N][K/2], scales fp16[N][K/32])
+        with an HBM copy and/or a pinned host copy."""
+        N, kb = codes.shape
+        K = 2 * kb
+        sbits = np.ascontiguousarray(scales, dtype=np.float16).view(np.uint16)
+        dc = ds = hc = hs = 0
+        if hbm:
+            tc = torch.from_numpy(np.ascontiguousarray(codes)).to(self.device)
+            tsc = torch.from_numpy(sbits.view(np.int16)).to(self.device)
+            self._keep += [tc, tsc]
+            dc, ds = tc.data_ptr(), tsc.data_ptr()
+        if host:
+            pc = torch.from_numpy(np.ascontiguousarray(codes)).pin_memory()
+            ps = torch.from_numpy(sbits.view(np.int16)).pin_memory()
+            self._keep += [pc, ps]
+            hc, hs = pc.data_ptr(), ps.data_ptr()
+        torch.cuda.synchronize(self.device)
+        tid = atsi.atsi_tensor_register(self.ctx, K, N, dc, ds, hc, hs)
+        self.shapes.append((K, N))
+        self.placement.append(0 if hbm else 1)
+        return tid
+
+    def register_device(self, codes_t: torch.Tensor, scales_t: torch.Tensor,
+                        host_codes: torch.Tensor | None = None, host_scales: torch.Tensor | None = None) -> int:
+        """Register tensors already in memory (device uint8/int16, optional pinned host copies)."""
+        N, kb = codes_t.shape
+        self._keep += [codes_t, scales_t] + [t for t in (host_codes, host_scales) if t is not None]
+        tid = atsi.atsi_tensor_register(self.ctx, 2 * kb, N, codes_t.data_ptr(), scales_t.data_ptr(),
+                                        host_codes.data_ptr() if host_codes is not None else 0,
+                                        host_scales.data_ptr() if host_scales is not None else 0)
+        self.shapes.append((2 * kb, N))
+        self.placement.append(0)
+        return tid
+
+    def set_placement(self, host_mask) -> None:
+        mask = [int(v) for v in host_mask]
+        atsi.atsi_set_placement(self.ctx, mask)
+        self.placement = mask
+
+    def place(self, tid: int, host: bool) -> None:
+        """Move one tensor between HBM and host, keeping the others where they are."""
+        mask = list(self.placement)
+        mask[tid] = int(host)
+        self.set_placement(mask)
+
+    # ---------------------------------------------------------------- compute
+    def linear(self, tid: int, x: torch.Tensor, y: torch.Tensor | None = None) -> torch.Tensor:
+        K, N = self.shapes[tid]
+        assert x.dtype == torch.float16 and x.is_contiguous() and x.shape[-1] == K
+        M = x.numel() // K
+        if y is None:
+            with torch.cuda.stream(self.cs):
+                y = torch.empty((M, N), dtype=torch.float16, device=self.device)
+        self._wait_torch()
+        atsi.atsi_linear(self.ctx, tid, x.data_ptr(), M, y.data_ptr())
+        self._torch_waits()
+        return y
+
+    def unpack(self, tid: int) -> torch.Tensor:
+        K, N = self.shapes[tid]
+        with torch.cuda.stream(self.cs):
+            q = torch.empty((N, K), dtype=torch.int8, device=self.device)
+        self._wait_torch()
+        atsi.atsi_debug_unpack(self.ctx, tid, q.data_ptr())
+        self._torch_waits()
+        return q
+
+    def _wait_torch(self) -> None:
+        # work torch queued on its current stream (uploads, allocations) precedes ours
+        self.cs.wait_stream(torch.cuda.current_stream(self.device))
+
+    def _torch_waits(self) -> None:
+        # results are safe to consume on torch's current stream
+        torch.cuda.current_stream(self.device).wait_stream(self.cs)
+
+    def sync(self) -> None:
+        atsi.atsi_sync(self.ctx)
+
+    def close(self) -> None:
+        if self.ctx:
+            atsi.atsi_destroy(self.ctx)
+            self.ctx = 0
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()

@@ -1,0 +1,110 @@
+"""GPU parity of the quantised linear layer (decode GEMV and prefill GEMM)
+against the fp64 oracle, through the C ABI."""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from tests.parity import bits16, check
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def sess():
+    from paper_2607_10183_amd.session import Session
+    s = Session(workspace_bytes=512 << 20, n_slots=4)
+    yield s
+    s.close()
+
+
+def _x(seed, uid, M, K, exact=False):
+    import torch
+    xn = synth.exact_activations(seed, uid, M, K) if exact else synth.activations(seed, uid, M, K)
+    return xn, torch.from_numpy(xn).cuda()
+
+
+@pytest.mark.parametrize("host", [False, True])
+def test_unpack_bitexact(sess, host):
+    K, N = 4096, 300
+    codes = synth.int4_codes(61, 1, N, K)
+    scales = synth.group_scales(61, 1, N, K)
+    tid = sess.register(codes, scales, hbm=not host, host=host)
+    q = sess.unpack(tid)
+    sess.sync()
+    assert np.array_equal(q.cpu().numpy(), oracle.unpack_codes(codes))
+
+
+EXACT_SHAPES = [  # (K, N, M): GEMV for M <= 4, GEMM above; ragged N and M
+    (32, 7, 1), (96, 33, 3), (768, 2048, 1), (4096, 1000, 4), (14336, 257, 2), (4096, 4096, 1),
+    (4096, 1000, 5), (768, 300, 64), (4096, 520, 100), (14336, 130, 512), (2048, 4096, 16), (96, 65, 129),
+]
+
+
+@pytest.mark.parametrize("K,N,M", EXACT_SHAPES)
+def test_exact_arithmetic_bitexact(sess, K, N, M):
+    """Scales 2^-6 and activations in {-4..4}/4 make every fp32 partial sum
+    exact, so the fp16 output must equal the nearest-even rounding of the exact
+    result, bit for bit."""
+    codes = synth.int4_codes(62, K * 7 + N, N, K)
+    scales = synth.exact_scales(N, K)
+    xn, x = _x(62, M, M, K, exact=True)
+    tid = sess.register(codes, scales)
+    y = sess.linear(tid, x)
+    sess.sync()
+    ref, _ = oracle.linear(xn, codes, scales)
+    assert np.array_equal(bits16(y), bits16(ref))
+
+
+RANDOM_SHAPES = [  # linear4096 (decode 1, batch 16) and the dense-layer tensors
+    (4096, 4096, 1), (4096, 4096, 16), (4096, 1024, 1), (4096, 14336, 1), (14336, 4096, 1),
+    (4096, 4096, 2), (4096, 1024, 4), (4096, 1024, 512), (4096, 14336, 512), (14336, 4096, 512),
+    (4096, 4096, 3), (2048, 768, 37),
+]
+
+
+@pytest.mark.parametrize("K,N,M", RANDOM_SHAPES)
+def test_random_parity(sess, K, N, M):
+    codes = synth.int4_codes(63, K + N, N, K)
+    scales = synth.group_scales(63, K + N, N, K)
+    xn, x = _x(63, M, M, K)
+    tid = sess.register(codes, scales)
+    y = sess.linear(tid, x).cpu().numpy()
+    sess.sync()
+    rows = np.arange(N) if N * M <= 4096 * 512 else synth.permutation(63, 9, N)[:2048]
+    ref, zeta = oracle.linear(xn, codes[rows], scales[rows])
+    check(y[:, rows], ref, zeta, name=f"linear K={K} N={N} M={M}")
+
+
+@pytest.mark.parametrize("M", [1, 3, 16, 200])
+def test_scaling_by_two_and_determinism(sess, M):
+    import torch
+    K, N = 4096, 777
+    codes = synth.int4_codes(64, 1, N, K)
+    scales = synth.group_scales(64, 1, N, K)
+    xn, x = _x(64, M, M, K)
+    tid = sess.register(codes, scales)
+    y1 = sess.linear(tid, x)
+    y2 = sess.linear(tid, (2 * x).contiguous())
+    y3 = sess.linear(tid, x)
+    sess.sync()
+    assert torch.equal(y1, y3)
+    assert np.array_equal(bits16(y2), bits16((2 * y1.float()).half()))
+
+
+@pytest.mark.parametrize("M", [1, 4, 64, 512])
+def test_placement_invariance(sess, M):
+    """HBM-resident and host-streamed reads of the same tensor give bit-identical outputs."""
+    import torch
+    K, N = 4096, 1024
+    codes = synth.int4_codes(65, M, N, K)
+    scales = synth.group_scales(65, M, N, K)
+    xn, x = _x(65, M, M, K)
+    tid = sess.register(codes, scales, hbm=True, host=True)
+    y_hbm = sess.linear(tid, x)
+    sess.place(tid, True)
+    y_host = [sess.linear(tid, x) for _ in range(3)]
+    sess.sync()
+    sess.place(tid, False)
+    for yh in y_host:
+        assert torch.equal(y_hbm, yh)
