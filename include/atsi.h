@@ -108,6 +108,43 @@ atsi_status atsi_set_placement(atsi_ctx* ctx, const uint8_t* host_mask, int32_t 
  * temporary buffer on the transfer stream (Sec. 4.2.2).  1 <= M <= 65536. */
 atsi_status atsi_linear(atsi_ctx* ctx, atsi_tid w, const void* x_f16, int64_t M, void* y_f16);
 
+/* Dense SwiGLU feed-forward block (the FFN of a decoder layer):
+ *   y = (silu(x Wg) * (x Wu)) Wd,  silu(z) = z / (1 + exp(-z)),
+ * gate and up are H x I tensors, down is I x H.  gate and up run in one
+ * launch with the SwiGLU product fused; the intermediate (fp16, M x I) lives
+ * in the workspace's scratch region (ATSI_E_WORKSPACE if it does not fit).
+ * y must not alias x. */
+atsi_status atsi_ffn_swiglu(atsi_ctx* ctx, atsi_tid gate, atsi_tid up, atsi_tid down,
+                            const void* x_f16, int64_t M, void* y_f16);
+
+/* One pre-norm decoder layer whose projections are all quantised tensors. */
+typedef struct {
+  int32_t n_heads, n_kv_heads, head_dim; /* grouped-query heads; n_heads % n_kv_heads == 0 */
+  float eps;                             /* RMS-norm epsilon (unit gain) */
+  atsi_tid q, k, v, o, gate, up, down;   /* Q/K/V: H x heads*dim, O: heads*dim x H, FFN as above */
+} atsi_dense_layer;
+
+/* h <- h + attn(rms(h)) Wo;  h <- h + FFN(rms(h)), in place on h[M][H].
+ * Attention is evaluated at context length 1 (each token attends only to
+ * itself, so query head i outputs the value of KV head i / (n_heads /
+ * n_kv_heads)); the Q and K projections are still computed and written to
+ * q_out[M][n_heads*dim] and k_out[M][n_kv_heads*dim] when those are non-NULL
+ * (device buffers), else to scratch.  rms(v) = v / sqrt(mean(v^2) + eps).
+ * Four launches: fused RMS-norm + Q/K/V, O + residual, fused RMS-norm +
+ * gate/up + SwiGLU, down + residual.  Streamed tensors of the layer are
+ * queued for copy at entry so their transfers overlap earlier launches. */
+atsi_status atsi_decoder_layer(atsi_ctx* ctx, const atsi_dense_layer* layer, void* h_f16, int64_t M,
+                               void* q_out_f16, void* k_out_f16);
+
+/* Execution order of tensors, repeated cyclically (the execution plan of a
+ * round, Sec. 4.2.2): the engine copies upcoming host-resident tensors into
+ * free temporary buffers as soon as one frees up, up to n_slots - 1 ahead, so
+ * weight transfers start as early as dependencies allow.  n = 0 clears it. */
+atsi_status atsi_set_schedule(atsi_ctx* ctx, const atsi_tid* order, int32_t n);
+
+/* Queue an early copy of a host-resident tensor (no-op for HBM tensors). */
+atsi_status atsi_prefetch(atsi_ctx* ctx, atsi_tid w);
+
 /* Wait for both streams; returns the first latched asynchronous error. */
 atsi_status atsi_sync(atsi_ctx* ctx);
 

@@ -29,6 +29,12 @@ class atsi_qtensor(ctypes.Structure):
                 ("host_codes", ctypes.c_void_p), ("host_scales", ctypes.c_void_p)]
 
 
+class atsi_dense_layer(ctypes.Structure):
+    _fields_ = [("n_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("eps", ctypes.c_float), ("q", ctypes.c_int32), ("k", ctypes.c_int32), ("v", ctypes.c_int32),
+                ("o", ctypes.c_int32), ("gate", ctypes.c_int32), ("up", ctypes.c_int32), ("down", ctypes.c_int32)]
+
+
 _P = ctypes.c_void_p
 _SIGS = {
     "atsi_create": ([ctypes.c_int, _P, _P, _P, ctypes.c_size_t, ctypes.c_int, ctypes.POINTER(_P)], ctypes.c_int),
@@ -37,6 +43,10 @@ _SIGS = {
     "atsi_tensor_register": ([_P, ctypes.POINTER(atsi_qtensor), ctypes.POINTER(ctypes.c_int32)], ctypes.c_int),
     "atsi_set_placement": ([_P, _P, ctypes.c_int32], ctypes.c_int),
     "atsi_linear": ([_P, ctypes.c_int32, _P, ctypes.c_int64, _P], ctypes.c_int),
+    "atsi_ffn_swiglu": ([_P, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _P, ctypes.c_int64, _P], ctypes.c_int),
+    "atsi_decoder_layer": ([_P, ctypes.POINTER(atsi_dense_layer), _P, ctypes.c_int64, _P, _P], ctypes.c_int),
+    "atsi_set_schedule": ([_P, _P, ctypes.c_int32], ctypes.c_int),
+    "atsi_prefetch": ([_P, ctypes.c_int32], ctypes.c_int),
     "atsi_sync": ([_P], ctypes.c_int),
     "atsi_debug_unpack": ([_P, ctypes.c_int32, _P], ctypes.c_int),
 }
@@ -98,6 +108,23 @@ def atsi_set_placement(ctx: int, host_mask) -> None:
 
 def atsi_linear(ctx: int, w: int, x: int, M: int, y: int) -> None:
     _check(ctx, lib().atsi_linear(ctx, w, x, M, y))
+
+
+def atsi_ffn_swiglu(ctx: int, gate: int, up: int, down: int, x: int, M: int, y: int) -> None:
+    _check(ctx, lib().atsi_ffn_swiglu(ctx, gate, up, down, x, M, y))
+
+
+def atsi_decoder_layer(ctx: int, layer: atsi_dense_layer, h: int, M: int, q_out: int = 0, k_out: int = 0) -> None:
+    _check(ctx, lib().atsi_decoder_layer(ctx, ctypes.byref(layer), h, M, q_out or None, k_out or None))
+
+
+def atsi_set_schedule(ctx: int, order) -> None:
+    arr = (ctypes.c_int32 * max(1, len(order)))(*[int(t) for t in order])
+    _check(ctx, lib().atsi_set_schedule(ctx, ctypes.cast(arr, _P), len(order)))
+
+
+def atsi_prefetch(ctx: int, w: int) -> None:
+    _check(ctx, lib().atsi_prefetch(ctx, w))
 
 
 def atsi_sync(ctx: int) -> None:

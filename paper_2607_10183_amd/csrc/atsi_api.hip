@@ -13,6 +13,7 @@
 // ahead of compute by up to n_slots - 1 tensors.
 #include <algorithm>
 #include <cstdarg>
+#include <deque>
 #include <cstdio>
 #include <cstring>
 #include <new>
@@ -67,8 +68,9 @@ struct atsi_ctx {
   std::vector<Slot> slots;
   size_t slot_bytes = 0;
   size_t scratch_off = 0;
-  std::vector<atsi_tid> schedule;
-  size_t sched_pos = 0;     // next schedule position whose host tensor is not yet prefetched
+  std::vector<atsi_tid> schedule;  // execution order of tensors, repeated cyclically
+  size_t sched_pos = 0;            // next schedule position not yet queued
+  std::deque<atsi_tid> queue;      // host tensors to copy ahead, in consumption order
   uint64_t clock = 0;
   std::string err;
   atsi_status latched = ATSI_OK;
@@ -141,18 +143,33 @@ atsi_status layout_slots(atsi_ctx* c) {
   }
   c->scratch_off = align_up((size_t)c->n_slots * need);
   c->sched_pos = 0;
+  c->queue.clear();
   return ATSI_OK;
 }
 
-// Issue the H2D copy of host tensor `tid` into a reusable slot; returns its index.
-atsi_status issue_copy(atsi_ctx* c, atsi_tid tid, int* slot_out) {
+// Issue the H2D copy of host tensor `tid` into a reusable slot; returns its
+// index.  Slots in `pinned` (held by the launch being assembled) are never
+// taken.  When every other slot holds a prefetched copy, the copy furthest in
+// the future is dropped and its tensor queued again.
+atsi_status issue_copy(atsi_ctx* c, atsi_tid tid, int* slot_out, const std::vector<int>& pinned = {}) {
+  auto is_pinned = [&](int i) { return std::find(pinned.begin(), pinned.end(), i) != pinned.end(); };
   int best = -1;
   for (int i = 0; i < c->n_slots; ++i) {
     const Slot& s = c->slots[i];
-    if (s.armed) continue;
+    if (s.armed || is_pinned(i)) continue;
     if (best < 0 || s.last < c->slots[best].last) best = i;
   }
-  if (best < 0) return fail(c, ATSI_E_STATE, "all %d slots hold prefetched tensors not yet consumed", c->n_slots);
+  if (best < 0) {
+    for (int i = 0; i < c->n_slots; ++i) {
+      const Slot& s = c->slots[i];
+      if (is_pinned(i)) continue;
+      if (best < 0 || s.seq > c->slots[best].seq) best = i;
+    }
+    if (best < 0)
+      return fail(c, ATSI_E_STATE, "one launch needs more streamed tensors than the %d slots", c->n_slots);
+    c->queue.push_front(c->slots[best].tid);
+    c->slots[best].armed = false;
+  }
   Slot& s = c->slots[best];
   const Tensor& t = c->tensors[tid];
   if (s.free_recorded) HIP_TRY(c, hipStreamWaitEvent(c->ts, s.free, 0));
@@ -168,15 +185,22 @@ atsi_status issue_copy(atsi_ctx* c, atsi_tid tid, int* slot_out) {
   return ATSI_OK;
 }
 
-// Keep the transfer stream ahead: prefetch the next host tensors of the schedule.
+// Keep the transfer stream ahead of compute: copy queued (or scheduled) host
+// tensors into free slots, leaving one slot for on-demand copies.
 atsi_status topup(atsi_ctx* c) {
-  if (c->schedule.empty()) return ATSI_OK;
   int armed = 0;
   for (const Slot& s : c->slots) armed += s.armed ? 1 : 0;
   size_t guard = 0;
-  while (armed < c->n_slots - 1 && guard++ < c->schedule.size()) {
-    atsi_tid t = c->schedule[c->sched_pos % c->schedule.size()];
-    c->sched_pos++;
+  while (armed < c->n_slots - 1) {
+    if (c->queue.empty()) {
+      if (c->schedule.empty() || guard++ >= c->schedule.size()) break;
+      atsi_tid t = c->schedule[c->sched_pos % c->schedule.size()];
+      c->sched_pos++;
+      if (c->tensors[t].on_host) c->queue.push_back(t);
+      continue;
+    }
+    atsi_tid t = c->queue.front();
+    c->queue.pop_front();
     if (!c->tensors[t].on_host) continue;
     int si;
     atsi_status st = issue_copy(c, t, &si);
@@ -187,13 +211,27 @@ atsi_status topup(atsi_ctx* c) {
   return ATSI_OK;
 }
 
-// Resolve where tensor `tid` is read from for the next kernel; for a host
-// tensor this makes the compute stream wait for its copy.  *slot = -1 for HBM.
-atsi_status acquire(atsi_ctx* c, atsi_tid tid, QView* v, int* slot) {
+// Without a schedule, a multi-tensor call queues its own host tensors so their
+// copies start before the first of them is needed.
+atsi_status prefetch_call(atsi_ctx* c, const atsi_tid* tids, int n) {
+  if (!c->schedule.empty()) return topup(c);
+  for (int i = 0; i < n; ++i) {
+    const atsi_tid t = tids[i];
+    if (!c->tensors[t].on_host) continue;
+    bool have = std::find(c->queue.begin(), c->queue.end(), t) != c->queue.end();
+    for (const Slot& s : c->slots) have = have || (s.armed && s.tid == t);
+    if (!have) c->queue.push_back(t);
+  }
+  return topup(c);
+}
+
+// Resolve where tensor `tid` is read from for the launch being assembled;
+// for a host tensor the compute stream waits for its copy.  The slot index is
+// appended to `held` (HBM tensors hold none).
+atsi_status acquire(atsi_ctx* c, atsi_tid tid, QView* v, std::vector<int>& held) {
   const Tensor& t = c->tensors[tid];
   v->K = (int)t.K;
   v->N = (int)t.N;
-  *slot = -1;
   if (!t.on_host) {
     v->codes = t.dcodes;
     v->scales = t.dscales;
@@ -202,33 +240,80 @@ atsi_status acquire(atsi_ctx* c, atsi_tid tid, QView* v, int* slot) {
   int si = -1;
   for (int i = 0; i < c->n_slots; ++i) {
     const Slot& s = c->slots[i];
-    if (s.armed && s.tid == tid && (si < 0 || s.seq < c->slots[si].seq)) si = i;
+    if (s.armed && s.tid == tid && std::find(held.begin(), held.end(), i) == held.end() &&
+        (si < 0 || s.seq < c->slots[si].seq))
+      si = i;
   }
   if (si < 0) {
-    atsi_status st = issue_copy(c, tid, &si);
+    auto q = std::find(c->queue.begin(), c->queue.end(), tid);
+    if (q != c->queue.end()) c->queue.erase(q);
+    atsi_status st = issue_copy(c, tid, &si, held);
     if (st) return st;
   }
   Slot& s = c->slots[si];
   HIP_TRY(c, hipStreamWaitEvent(c->cs, s.ready, 0));
   v->codes = reinterpret_cast<const uint8_t*>(s.base);
   v->scales = reinterpret_cast<const uint16_t*>(s.base + align_up(t.codes_bytes()));
-  *slot = si;
+  held.push_back(si);
   return ATSI_OK;
 }
 
-// After the consumer kernel of a slot has been enqueued.
-atsi_status release(atsi_ctx* c, int slot) {
-  if (slot < 0) return ATSI_OK;
-  Slot& s = c->slots[slot];
-  HIP_TRY(c, hipEventRecord(s.free, c->cs));
-  s.free_recorded = true;
-  s.armed = false;
-  s.last = ++c->clock;
+// After the consumer kernel of the held slots has been enqueued.
+atsi_status release(atsi_ctx* c, std::vector<int>& held) {
+  for (int si : held) {
+    Slot& s = c->slots[si];
+    HIP_TRY(c, hipEventRecord(s.free, c->cs));
+    s.free_recorded = true;
+    s.armed = false;
+    s.last = ++c->clock;
+  }
+  held.clear();
   return topup(c);
 }
 
-atsi_status launched(atsi_ctx* c, hipError_t e, const char* what) {
-  if (e != hipSuccess) return hip_fail(c, e, what);
+
+// Bump allocator over the scratch region of the workspace (after the slots).
+struct Scratch {
+  atsi_ctx* c;
+  size_t off;
+  explicit Scratch(atsi_ctx* ctx) : c(ctx), off(ctx->scratch_off) {}
+  __half* take(size_t elems, size_t elem_bytes = 2) {
+    size_t need = align_up(elems * elem_bytes);
+    if (off + need > c->ws_bytes) return nullptr;
+    char* p = c->ws + off;
+    off += need;
+    return reinterpret_cast<__half*>(p);
+  }
+};
+
+// Acquire the tensors of a fused launch (segment order; SwiGLU: gate, up),
+// launch the GEMV (M <= 4) or the GEMM, release the slots.
+atsi_status run_op(atsi_ctx* c, LinOp& op, const atsi_tid* tids, int ntids) {
+  std::vector<int> held;
+  for (int i = 0; i < ntids; ++i) {
+    QView v;
+    atsi_status st = acquire(c, tids[i], &v, held);
+    if (st) return st;
+    if (op.swiglu) {
+      if (i == 0) op.seg[0].w = v; else op.seg[0].w2 = v;
+    } else {
+      op.seg[i].w = v;
+    }
+  }
+  const bool gemv = op.M <= 4;
+  hipError_t e = gemv ? launch_gemv(op, c->cs) : launch_gemm(op, c->cs);
+  if (e != hipSuccess) return hip_fail(c, e, gemv ? "q4 gemv launch" : "q4 gemm launch");
+  return release(c, held);
+}
+
+atsi_status check_act(atsi_ctx* c, const void* p, const char* what) {
+  if (!p) return fail(c, ATSI_E_INVALID, "%s is NULL", what);
+  if (!aligned16(p)) return fail(c, ATSI_E_INVALID, "%s must be 16-byte aligned", what);
+  return ATSI_OK;
+}
+
+atsi_status check_m(atsi_ctx* c, int64_t M) {
+  if (M < 1 || M > 65536) return fail(c, ATSI_E_SHAPE, "M=%lld outside 1..65536", (long long)M);
   return ATSI_OK;
 }
 
@@ -357,24 +442,122 @@ atsi_status atsi_set_placement(atsi_ctx* c, const uint8_t* host_mask, int32_t n)
 
 atsi_status atsi_linear(atsi_ctx* c, atsi_tid w, const void* x, int64_t M, void* y) {
   if (!c) return ATSI_E_INVALID;
-  if (!x || !y) return fail(c, ATSI_E_INVALID, "x or y is NULL");
-  if (!aligned16(x) || !aligned16(y)) return fail(c, ATSI_E_INVALID, "x and y must be 16-byte aligned");
-  if (M < 1 || M > 65536) return fail(c, ATSI_E_SHAPE, "M=%lld outside 1..65536", (long long)M);
+  atsi_status st;
+  if ((st = check_act(c, x, "x")) || (st = check_act(c, y, "y")) || (st = check_m(c, M)) || (st = check_tid(c, w)))
+    return st;
+  if ((st = enter(c))) return st;
+  const Tensor& t = c->tensors[w];
+  QView v{nullptr, nullptr, (int)t.K, (int)t.N};
+  LinOp op = plain_op(v, (const __half*)x, (int)M, (__half*)y);
+  return run_op(c, op, &w, 1);
+}
+
+atsi_status atsi_ffn_swiglu(atsi_ctx* c, atsi_tid gate, atsi_tid up, atsi_tid down, const void* x, int64_t M,
+                            void* y) {
+  if (!c) return ATSI_E_INVALID;
+  atsi_status st;
+  if ((st = check_act(c, x, "x")) || (st = check_act(c, y, "y")) || (st = check_m(c, M)) ||
+      (st = check_tid(c, gate)) || (st = check_tid(c, up)) || (st = check_tid(c, down)))
+    return st;
+  const Tensor &tg = c->tensors[gate], &tu = c->tensors[up], &td = c->tensors[down];
+  if (tg.K != tu.K || tg.N != tu.N || td.K != tg.N || td.N != tg.K)
+    return fail(c, ATSI_E_SHAPE, "SwiGLU shapes: gate/up must be H x I and down I x H");
+  if (x == y) return fail(c, ATSI_E_INVALID, "y must not alias x");
+  if ((st = enter(c))) return st;
+  Scratch sc(c);
+  __half* h = sc.take((size_t)M * tg.N);
+  if (!h) return fail(c, ATSI_E_WORKSPACE, "scratch too small for the %lld x %lld SwiGLU activation",
+                      (long long)M, (long long)tg.N);
+  const atsi_tid order[3] = {gate, up, down};
+  if ((st = prefetch_call(c, order, 3))) return st;
+  // gate/up with the SwiGLU product fused: h = silu(x Wg) * (x Wu)
+  LinOp gu = plain_op(QView{nullptr, nullptr, (int)tg.K, (int)tg.N}, (const __half*)x, (int)M, h);
+  gu.swiglu = 1;
+  if ((st = run_op(c, gu, order, 2))) return st;
+  // down: y = h Wd
+  LinOp dn = plain_op(QView{nullptr, nullptr, (int)td.K, (int)td.N}, h, (int)M, (__half*)y);
+  return run_op(c, dn, &order[2], 1);
+}
+
+atsi_status atsi_decoder_layer(atsi_ctx* c, const atsi_dense_layer* L, void* h, int64_t M, void* q_out,
+                               void* k_out) {
+  if (!c) return ATSI_E_INVALID;
+  if (!L) return fail(c, ATSI_E_INVALID, "layer descriptor is NULL");
+  atsi_status st;
+  if ((st = check_act(c, h, "h")) || (st = check_m(c, M))) return st;
+  if ((q_out && !aligned16(q_out)) || (k_out && !aligned16(k_out)))
+    return fail(c, ATSI_E_INVALID, "q_out / k_out must be 16-byte aligned");
+  const atsi_tid ids[7] = {L->q, L->k, L->v, L->o, L->gate, L->up, L->down};
+  for (atsi_tid t : ids)
+    if ((st = check_tid(c, t))) return st;
+  const Tensor &tq = c->tensors[L->q], &tk = c->tensors[L->k], &tv = c->tensors[L->v], &to = c->tensors[L->o];
+  const Tensor &tg = c->tensors[L->gate], &tu = c->tensors[L->up], &td = c->tensors[L->down];
+  const int64_t H = tq.K;
+  if (L->n_heads < 1 || L->n_kv_heads < 1 || L->head_dim < 1 || L->n_heads % L->n_kv_heads != 0 ||
+      !(L->eps >= 0.f))
+    return fail(c, ATSI_E_SHAPE, "heads %d / kv heads %d / head_dim %d / eps invalid", L->n_heads, L->n_kv_heads,
+                L->head_dim);
+  const int64_t Hq = (int64_t)L->n_heads * L->head_dim, Hkv = (int64_t)L->n_kv_heads * L->head_dim;
+  if (tq.N != Hq || tk.K != H || tv.K != H || tk.N != Hkv || tv.N != Hkv || to.K != Hq || to.N != H ||
+      tg.K != H || tu.K != H || tg.N != tu.N || td.K != tg.N || td.N != H)
+    return fail(c, ATSI_E_SHAPE, "decoder layer tensor shapes do not match hidden %lld, heads %d x %d",
+                (long long)H, L->n_heads, L->head_dim);
+  if ((st = enter(c))) return st;
+  Scratch sc(c);
+  __half* qb = q_out ? (__half*)q_out : sc.take((size_t)M * Hq);
+  __half* kb = k_out ? (__half*)k_out : sc.take((size_t)M * Hkv);
+  __half* oin = sc.take((size_t)M * Hq);
+  __half* hf = sc.take((size_t)M * tg.N);
+  if (!qb || !kb || !oin || !hf) return fail(c, ATSI_E_WORKSPACE, "scratch too small for a %lld-token layer", (long long)M);
+  if ((st = prefetch_call(c, ids, 7))) return st;
+  __half* hh = (__half*)h;
+  const int Mi = (int)M;
+  const float eps = L->eps;
+
+  // 1. q, k, v = rms(h) Wq, Wk, Wv in one launch; v goes straight to the
+  //    attention output of every query head of its group (context length 1)
+  LinOp a{};
+  a.nseg = 3;
+  a.x = hh; a.M = Mi; a.K = (int)H; a.norm = 1; a.eps = eps; a.head_dim = L->head_dim;
+  a.seg[0] = Seg{QView{}, QView{}, qb, (int)Hq, 1};
+  a.seg[1] = Seg{QView{}, QView{}, kb, (int)Hkv, 1};
+  a.seg[2] = Seg{QView{}, QView{}, oin, (int)Hq, L->n_heads / L->n_kv_heads};
+  if ((st = run_op(c, a, ids, 3))) return st;
+  // 2. h = h + attn Wo
+  LinOp o = plain_op(QView{nullptr, nullptr, (int)to.K, (int)to.N}, oin, Mi, hh);
+  o.res = hh;
+  if ((st = run_op(c, o, &ids[3], 1))) return st;
+  // 3. f = silu(rms(h) Wg) * (rms(h) Wu)
+  LinOp gu = plain_op(QView{nullptr, nullptr, (int)tg.K, (int)tg.N}, hh, Mi, hf);
+  gu.swiglu = 1; gu.norm = 1; gu.eps = eps;
+  if ((st = run_op(c, gu, &ids[4], 2))) return st;
+  // 4. h = h + f Wd
+  LinOp dn = plain_op(QView{nullptr, nullptr, (int)td.K, (int)td.N}, hf, Mi, hh);
+  dn.res = hh;
+  return run_op(c, dn, &ids[6], 1);
+}
+
+atsi_status atsi_set_schedule(atsi_ctx* c, const atsi_tid* order, int32_t n) {
+  if (!c) return ATSI_E_INVALID;
+  if (n < 0 || (n > 0 && !order)) return fail(c, ATSI_E_INVALID, "schedule of length %d with NULL order", n);
+  for (int32_t i = 0; i < n; ++i) {
+    atsi_status st = check_tid(c, order[i]);
+    if (st) return st;
+  }
+  c->schedule.assign(order, order + n);
+  c->sched_pos = 0;
+  c->queue.clear();
+  return ATSI_OK;
+}
+
+atsi_status atsi_prefetch(atsi_ctx* c, atsi_tid w) {
+  if (!c) return ATSI_E_INVALID;
   atsi_status st = check_tid(c, w);
   if (st) return st;
-  st = enter(c);
-  if (st) return st;
-  QView v;
-  int slot;
-  st = acquire(c, w, &v, &slot);
-  if (st) return st;
-  const __half* xh = (const __half*)x;
-  __half* yh = (__half*)y;
-  hipError_t e = (M <= 4) ? launch_gemv(v, xh, (int)M, yh, v.N, kStore, nullptr, c->cs)
-                          : launch_gemm(v, xh, (int)M, yh, v.N, kStore, nullptr, c->cs);
-  st = launched(c, e, M <= 4 ? "q4 gemv launch" : "q4 gemm launch");
-  if (st) return st;
-  return release(c, slot);
+  if ((st = enter(c))) return st;
+  if (!c->tensors[w].on_host) return ATSI_OK;
+  c->queue.push_back(w);
+  return topup(c);
 }
 
 atsi_status atsi_sync(atsi_ctx* c) {
@@ -395,15 +578,13 @@ atsi_status atsi_debug_unpack(atsi_ctx* c, atsi_tid w, int8_t* q_out) {
   if (!q_out) return fail(c, ATSI_E_INVALID, "q_out is NULL");
   atsi_status st = check_tid(c, w);
   if (st) return st;
-  st = enter(c);
-  if (st) return st;
+  if ((st = enter(c))) return st;
   QView v;
-  int slot;
-  st = acquire(c, w, &v, &slot);
-  if (st) return st;
-  st = launched(c, launch_unpack(v, q_out, c->cs), "unpack launch");
-  if (st) return st;
-  return release(c, slot);
+  std::vector<int> held;
+  if ((st = acquire(c, w, &v, held))) return st;
+  hipError_t e = launch_unpack(v, q_out, c->cs);
+  if (e != hipSuccess) return hip_fail(c, e, "unpack launch");
+  return release(c, held);
 }
 
 }  // extern "C"

@@ -8,6 +8,7 @@
 namespace atsi {
 
 constexpr int kGroup = 32;  // inputs per fp16 scale
+constexpr int kMaxSeg = 3;  // tensors fused into one launch
 
 // Location of one block-int4 tensor as a kernel sees it.
 struct QView {
@@ -17,17 +18,50 @@ struct QView {
   int N;
 };
 
-// Epilogues of the linear kernels.
-enum Epilogue : int {
-  kStore = 0,        // y = acc
-  kResidual = 1,     // y = acc + res (res may alias y)
+// One output segment of a fused launch: a tensor (or a gate/up pair), where
+// its outputs go and how they are laid out.
+struct Seg {
+  QView w;       // the tensor (gate for SwiGLU)
+  QView w2;      // up tensor for SwiGLU, unused otherwise
+  __half* y;     // output [M][ldy]
+  int ldy;
+  int expand;    // >1: output row n = (j, d) of a KV head is written to
+                 // query heads j*expand .. j*expand+expand-1 (context-length-1
+                 // attention of grouped-query heads); 1: plain
+};
+
+// A fused linear launch over up to kMaxSeg tensors sharing one input x.
+struct LinOp {
+  Seg seg[kMaxSeg];
+  int nseg;
+  const __half* x;   // [M][K], K common to all segments
+  int M;
+  int K;
+  int swiglu;        // 1: segment 0 is a (gate, up) pair, output silu(g) * u
+  int norm;          // 1: input is RMS-normalised (unit gain) before the product
+  float eps;
+  const __half* res; // residual added to segment 0's output (may alias its y)
+  int head_dim;      // granularity of `expand`
 };
 
 // ---- launchers (each returns hipGetLastError() of its launch) ----
-hipError_t launch_gemv(const QView& w, const __half* x, int M, __half* y, int ldy,
-                       Epilogue ep, const __half* res, hipStream_t s);
-hipError_t launch_gemm(const QView& w, const __half* x, int M, __half* y, int ldy,
-                       Epilogue ep, const __half* res, hipStream_t s);
+hipError_t launch_gemv(const LinOp& op, hipStream_t s);
+hipError_t launch_gemm(const LinOp& op, hipStream_t s);
 hipError_t launch_unpack(const QView& w, int8_t* q, hipStream_t s);
+
+// single-tensor helpers
+inline LinOp plain_op(const QView& w, const __half* x, int M, __half* y) {
+  LinOp op{};
+  op.seg[0].w = w;
+  op.seg[0].y = y;
+  op.seg[0].ldy = w.N;
+  op.seg[0].expand = 1;
+  op.nseg = 1;
+  op.x = x;
+  op.M = M;
+  op.K = w.K;
+  op.head_dim = 1;
+  return op;
+}
 
 }  // namespace atsi

@@ -15,6 +15,13 @@
 //     wavefront hit distinct banks;
 //   * workgroup ids are remapped so that the M tiles sharing one weight tile
 //     run on the same XCD and reuse it from that XCD's L2.
+// Like the GEMV, one launch covers several tensors sharing an input and fuses
+// RMS normalisation (row sums of squares gathered while staging activations,
+// applied to the fp32 accumulators), SwiGLU (the B tile interleaves 32-row
+// blocks of gate and up so one lane holds g and u of the same output), the
+// residual add and grouped-query head expansion.
+#include <algorithm>
+
 #include "common.h"
 
 namespace atsi {
@@ -55,40 +62,57 @@ __device__ __forceinline__ void dequant_group(const uint4& cw, uint16_t sbits, u
   }
 }
 
-template <int BM, int BN, int WM, int WN>
-__global__ __launch_bounds__(kBlock, 2) void q4_gemm_kernel(QView w, const __half* __restrict__ x, int M,
-                                                            __half* __restrict__ y, int ldy, int ep,
-                                                            const __half* res, int tiles_m, int tiles_n) {
+__device__ __forceinline__ float silu_f(float g) { return g / (1.f + expf(-g)); }
+
+struct TileMap {
+  int end[kMaxSeg];    // cumulative tile counts per segment
+  int tiles_n[kMaxSeg];
+  int tiles_m;
+  int total;
+};
+
+template <int BM, int BN, int WM, int WN, bool SWI>
+__global__ __launch_bounds__(kBlock, 2) void q4_gemm_kernel(LinOp op, TileMap tm_) {
   static_assert(WM * WN == 4, "four waves");
   constexpr int SM = BM / WM, SN = BN / WN;  // wave sub-tile
   constexpr int FM = SM / 32, FN = SN / 32;  // 32x32 fragments per wave
   static_assert(FM >= 1 && FN >= 1, "sub-tile at least 32x32");
-  // global -> register staging per thread
-  constexpr int XV = BM * BK / 8 / kBlock;   // uint4 of activations per thread
+  static_assert(!SWI || (SN % 64) == 0, "SwiGLU pairs gate/up fragments inside a wave");
+  constexpr int XV = BM * BK / 8 / kBlock;            // uint4 of activations per thread
   constexpr int WG = (BN * 2 + kBlock - 1) / kBlock;  // weight groups per thread (BN rows x 2 groups)
   static_assert(XV >= 1 && (BM * BK / 8) % kBlock == 0, "activation tile must split evenly");
+  constexpr int NOUT = SWI ? BN / 2 : BN;             // output columns per tile
 
   __shared__ __attribute__((aligned(16))) _Float16 As[2][BM * LDSP];
   __shared__ __attribute__((aligned(16))) _Float16 Bs[2][BN * LDSP];
+  __shared__ float rowinv[BM];
 
   // XCD-aware tile order: consecutive ids land on different XCDs (8-way
   // round robin); give each XCD a contiguous run of tiles, M fastest.
-  const int ntiles = tiles_m * tiles_n;
   int bid = blockIdx.x;
-  if ((ntiles & 7) == 0) bid = (bid & 7) * (ntiles >> 3) + (bid >> 3);
-  const int tm = bid % tiles_m, tn = bid / tiles_m;
-  const int m0 = tm * BM, n0 = tn * BN;
+  if ((tm_.total & 7) == 0) bid = (bid & 7) * (tm_.total >> 3) + (bid >> 3);
+  int s = 0;
+  while (s < op.nseg - 1 && bid >= tm_.end[s]) ++s;
+  const int local = bid - (s ? tm_.end[s - 1] : 0);
+  const int tmi = local % tm_.tiles_m, tni = local / tm_.tiles_m;
+  const Seg& sg = op.seg[s];
+  const QView w = sg.w, w2 = sg.w2;
+  const int m0 = tmi * BM, n0 = tni * NOUT;
+  const int M = op.M;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
-  const int K = w.K;
+  const int K = op.K;
   const int ngrp = K / 32;
   const int nk = (K + BK - 1) / BK;
 
   uint4 xr[XV];
   uint4 cr[WG];
   uint16_t sr[WG];
+  float sq[XV];
+#pragma unroll
+  for (int i = 0; i < XV; ++i) sq[i] = 0.f;
 
   auto gload = [&](int kt) {
     const int k0 = kt * BK;
@@ -98,7 +122,7 @@ __global__ __launch_bounds__(kBlock, 2) void q4_gemm_kernel(QView w, const __hal
       const int r = idx / (BK / 8), cchunk = idx % (BK / 8);
       const int m = m0 + r, k = k0 + cchunk * 8;
       if (m < M && k < K)
-        xr[i] = *reinterpret_cast<const uint4*>(x + (size_t)m * K + k);
+        xr[i] = *reinterpret_cast<const uint4*>(op.x + (size_t)m * K + k);
       else
         xr[i] = make_uint4(0, 0, 0, 0);
     }
@@ -106,11 +130,19 @@ __global__ __launch_bounds__(kBlock, 2) void q4_gemm_kernel(QView w, const __hal
     for (int i = 0; i < WG; ++i) {
       const int idx = tid + i * kBlock;
       if (idx >= BN * 2) break;
-      const int r = idx >> 1, g = (k0 >> 5) + (idx & 1);
-      const int n = n0 + r;
+      const int br = idx >> 1, g = (k0 >> 5) + (idx & 1);
+      int n;
+      const QView* src = &w;
+      if constexpr (SWI) {
+        const int b32 = br >> 5;
+        n = n0 + (b32 >> 1) * 32 + (br & 31);
+        if (b32 & 1) src = &w2;
+      } else {
+        n = n0 + br;
+      }
       if (n < w.N && g < ngrp) {
-        cr[i] = *reinterpret_cast<const uint4*>(w.codes + (size_t)n * (K / 2) + (size_t)g * 16);
-        sr[i] = w.scales[(size_t)n * ngrp + g];
+        cr[i] = *reinterpret_cast<const uint4*>(src->codes + (size_t)n * (K / 2) + (size_t)g * 16);
+        sr[i] = src->scales[(size_t)n * ngrp + g];
       } else {
         cr[i] = make_uint4(0x88888888u, 0x88888888u, 0x88888888u, 0x88888888u);  // q = 0
         sr[i] = 0;
@@ -123,6 +155,16 @@ __global__ __launch_bounds__(kBlock, 2) void q4_gemm_kernel(QView w, const __hal
       const int idx = tid + i * kBlock;
       const int r = idx / (BK / 8), cchunk = idx % (BK / 8);
       *reinterpret_cast<uint4*>(&As[buf][r * LDSP + cchunk * 8]) = xr[i];
+      if (op.norm) {
+        const half2_t* h = reinterpret_cast<const half2_t*>(&xr[i]);
+        float q = sq[i];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const float a = (float)h[j][0], b = (float)h[j][1];
+          q = fmaf(a, a, fmaf(b, b, q));
+        }
+        sq[i] = q;
+      }
     }
 #pragma unroll
     for (int i = 0; i < WG; ++i) {
@@ -173,6 +215,20 @@ __global__ __launch_bounds__(kBlock, 2) void q4_gemm_kernel(QView w, const __hal
     }
   }
 
+  // fused RMS normalisation: 1 / sqrt(mean(x^2) + eps) per row of the tile
+  if (op.norm) {
+#pragma unroll
+    for (int i = 0; i < XV; ++i) {
+      float q = sq[i];
+      q += __shfl_xor(q, 1, 64);
+      q += __shfl_xor(q, 2, 64);
+      q += __shfl_xor(q, 4, 64);
+      const int idx = tid + i * kBlock;
+      if ((idx % (BK / 8)) == 0) rowinv[idx / (BK / 8)] = 1.f / sqrtf(q / (float)K + op.eps);
+    }
+    __syncthreads();
+  }
+
   // D layout of a 32x32 MFMA block: lane l holds column l % 32; accumulator v
   // holds row 8 * (v / 4) + 4 * (l / 32) + v % 4.
   const int col = lane & 31, rq = (lane >> 5) * 4;
@@ -180,27 +236,46 @@ __global__ __launch_bounds__(kBlock, 2) void q4_gemm_kernel(QView w, const __hal
   for (int i = 0; i < FM; ++i)
 #pragma unroll
     for (int j = 0; j < FN; ++j) {
-      const int n = n0 + wn * SN + j * 32 + col;
+      if (SWI && (j & 1)) continue;
+      int n;
+      if constexpr (SWI) n = n0 + ((wn * SN / 32 + j) >> 1) * 32 + col;
+      else n = n0 + wn * SN + j * 32 + col;
       if (n >= w.N) continue;
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        const int m = m0 + wm * SM + i * 32 + 8 * (v >> 2) + rq + (v & 3);
-        if (m < M) {
-          const size_t at = (size_t)m * ldy + n;
-          float o = acc[i][j][v];
-          if (ep == kResidual) o += __half2float(res[at]);
-          y[at] = __float2half_rn(o);
+        const int ml = wm * SM + i * 32 + 8 * (v >> 2) + rq + (v & 3);
+        const int m = m0 + ml;
+        if (m >= M) continue;
+        const float sc = op.norm ? rowinv[ml] : 1.f;
+        float o = acc[i][j][v] * sc;
+        if constexpr (SWI) o = silu_f(o) * (acc[i][j + 1][v] * sc);
+        if (sg.expand > 1) {
+          const int hd = op.head_dim, jh = n / hd, d = n % hd;
+          const __half h = __float2half_rn(o);
+          for (int g = 0; g < sg.expand; ++g)
+            sg.y[(size_t)m * sg.ldy + (size_t)(jh * sg.expand + g) * hd + d] = h;
+        } else {
+          const size_t at = (size_t)m * sg.ldy + n;
+          if (op.res && s == 0) o += __half2float(op.res[at]);
+          sg.y[at] = __float2half_rn(o);
         }
       }
     }
 }
 
-template <int BM, int BN, int WM, int WN>
-hipError_t launch_tile(const QView& w, const __half* x, int M, __half* y, int ldy, Epilogue ep, const __half* res,
-                       hipStream_t s) {
-  const int tm = (M + BM - 1) / BM, tn = (w.N + BN - 1) / BN;
-  hipLaunchKernelGGL((q4_gemm_kernel<BM, BN, WM, WN>), dim3(tm * tn), dim3(kBlock), 0, s, w, x, M, y, ldy, (int)ep,
-                     res, tm, tn);
+template <int BM, int BN, int WM, int WN, bool SWI>
+hipError_t launch_tile(const LinOp& op, hipStream_t st) {
+  constexpr int NOUT = SWI ? BN / 2 : BN;
+  TileMap tm{};
+  tm.tiles_m = (op.M + BM - 1) / BM;
+  int total = 0;
+  for (int s = 0; s < op.nseg; ++s) {
+    tm.tiles_n[s] = (op.seg[s].w.N + NOUT - 1) / NOUT;
+    total += tm.tiles_m * tm.tiles_n[s];
+    tm.end[s] = total;
+  }
+  tm.total = total;
+  hipLaunchKernelGGL((q4_gemm_kernel<BM, BN, WM, WN, SWI>), dim3(total), dim3(kBlock), 0, st, op, tm);
   return hipGetLastError();
 }
 
@@ -216,14 +291,19 @@ __global__ void unpack_kernel(QView w, int8_t* q) {
 
 }  // namespace
 
-hipError_t launch_gemm(const QView& w, const __half* x, int M, __half* y, int ldy, Epilogue ep, const __half* res,
-                       hipStream_t s) {
-  // Prefer 128x128 tiles; fall back to narrower tiles when the grid would
-  // leave most of the 256 CUs idle.
-  const long t128 = (long)((M + 127) / 128) * ((w.N + 127) / 128);
-  if (M <= 64) return launch_tile<64, 64, 2, 2>(w, x, M, y, ldy, ep, res, s);
-  if (t128 >= 256) return launch_tile<128, 128, 2, 2>(w, x, M, y, ldy, ep, res, s);
-  return launch_tile<128, 64, 2, 2>(w, x, M, y, ldy, ep, res, s);
+hipError_t launch_gemm(const LinOp& op, hipStream_t st) {
+  long n = 0;
+  for (int s = 0; s < op.nseg; ++s) n += op.seg[s].w.N;
+  if (op.swiglu) {
+    if (op.M <= 64) return launch_tile<64, 128, 2, 2, true>(op, st);
+    return launch_tile<128, 128, 2, 2, true>(op, st);
+  }
+  // Prefer 128x128 tiles; narrower tiles when the grid would leave most of
+  // the 256 CUs idle.
+  const long t128 = (long)((op.M + 127) / 128) * ((n + 127) / 128);
+  if (op.M <= 64) return launch_tile<64, 64, 2, 2, false>(op, st);
+  if (t128 >= 256) return launch_tile<128, 128, 2, 2, false>(op, st);
+  return launch_tile<128, 64, 2, 2, false>(op, st);
 }
 
 hipError_t launch_unpack(const QView& w, int8_t* q, hipStream_t s) {

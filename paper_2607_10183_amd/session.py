@@ -87,6 +87,32 @@ class Session:
         self._torch_waits()
         return y
 
+    def ffn(self, gate: int, up: int, down: int, x: torch.Tensor, y: torch.Tensor | None = None) -> torch.Tensor:
+        H, I = self.shapes[gate]
+        M = x.numel() // H
+        if y is None:
+            with torch.cuda.stream(self.cs):
+                y = torch.empty((M, H), dtype=torch.float16, device=self.device)
+        self._wait_torch()
+        atsi.atsi_ffn_swiglu(self.ctx, gate, up, down, x.data_ptr(), M, y.data_ptr())
+        self._torch_waits()
+        return y
+
+    def decoder_layer(self, tids: dict, h: torch.Tensor, n_heads: int, n_kv: int, head_dim: int,
+                      eps: float = 1e-6, q_out: torch.Tensor | None = None, k_out: torch.Tensor | None = None):
+        """In-place pre-norm decoder layer on h[M][H]; tids maps q,k,v,o,gate,up,down to tensor ids."""
+        L = atsi.atsi_dense_layer(n_heads, n_kv, head_dim, eps, *[tids[r] for r in
+                                                                  ("q", "k", "v", "o", "gate", "up", "down")])
+        M = h.shape[0]
+        self._wait_torch()
+        atsi.atsi_decoder_layer(self.ctx, L, h.data_ptr(), M, q_out.data_ptr() if q_out is not None else 0,
+                                k_out.data_ptr() if k_out is not None else 0)
+        self._torch_waits()
+        return h
+
+    def set_schedule(self, order) -> None:
+        atsi.atsi_set_schedule(self.ctx, list(order))
+
     def unpack(self, tid: int) -> torch.Tensor:
         K, N = self.shapes[tid]
         with torch.cuda.stream(self.cs):
