@@ -145,6 +145,55 @@ atsi_status atsi_set_schedule(atsi_ctx* ctx, const atsi_tid* order, int32_t n);
 /* Queue an early copy of a host-resident tensor (no-op for HBM tensors). */
 atsi_status atsi_prefetch(atsi_ctx* ctx, atsi_tid w);
 
+/* A routed mixture-of-experts layer of SwiGLU experts. */
+typedef struct {
+  int32_t n_experts;          /* E, a multiple of 16, at most 128 */
+  int32_t top_k;              /* experts per token, 1..16, <= E */
+  int64_t hidden, inter;      /* H and I, multiples of 32 */
+  const void* router_w_f16;   /* device fp16 [H][E] (not quantised) */
+  const float* router_bias;   /* device fp32 [E], or NULL */
+  const atsi_tid* gate;       /* host arrays of E tensor ids: gate/up are H x I, */
+  const atsi_tid* up;         /*   down is I x H */
+  const atsi_tid* down;
+} atsi_moe;
+
+/* Optional device buffers that receive the routing (each may be NULL):
+ * logits fp32 [M][E]; idx int32 [M][k] and p fp32 [M][k] (slot j in order of
+ * logit descending, expert id ascending); counts int32 [E]; offsets int32
+ * [E+1] (exclusive prefix sum of counts); perm int32 [M*k] (pair ids k*t + j
+ * ordered by expert, then token); inv_perm int32 [M*k] (inverse of perm). */
+typedef struct {
+  float* logits;
+  int32_t* idx;
+  float* p;
+  int32_t* counts;
+  int32_t* offsets;
+  int32_t* perm;
+  int32_t* inv_perm;
+} atsi_moe_debug;
+
+/* y[t] = sum_j p[t][j] * FFN_{idx[t][j]}(x[t]) for x, y fp16 [M][H].
+ * Router logits l = x W_r + b are accumulated in fp32; each token keeps the
+ * top_k experts by (logit descending, expert id ascending) and p is the
+ * softmax over the kept logits (the full softmax renormalised over them).
+ * Pairs are bucketed by expert; each expert FFN runs on its own tokens only
+ * and only routed experts are read.  An expert with any host-resident tensor
+ * is streamed after routing resolves (Sec. 4.2.2: expert transfers wait for
+ * routing and move only selected experts): the host reads the per-expert
+ * counts back (one event wait), copies the active host experts heaviest
+ * first into temporary buffers (n_slots >= 3 needed) while the HBM-resident
+ * experts already run.  Expert outputs are kept in fp16 before the fp32
+ * combine.  1 <= M <= 65536.  dbg may be NULL. */
+atsi_status atsi_moe_ffn(atsi_ctx* ctx, const atsi_moe* moe, const void* x_f16, int64_t M, void* y_f16,
+                         const atsi_moe_debug* dbg);
+
+/* Token-to-expert bucketing alone (the same kernel atsi_moe_ffn uses), from
+ * device idx int32 [M][k] with ids in [0, n_experts): counts [E], offsets
+ * [E+1], perm [M*k], inv_perm [M*k] as in atsi_moe_debug.  Out-of-range ids
+ * are skipped (memory-safe, results then unspecified). */
+atsi_status atsi_moe_bucket(atsi_ctx* ctx, const int32_t* idx, int64_t M, int32_t k, int32_t n_experts,
+                            int32_t* counts, int32_t* offsets, int32_t* perm, int32_t* inv_perm);
+
 /* Wait for both streams; returns the first latched asynchronous error. */
 atsi_status atsi_sync(atsi_ctx* ctx);
 

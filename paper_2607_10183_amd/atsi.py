@@ -35,6 +35,17 @@ class atsi_dense_layer(ctypes.Structure):
                 ("o", ctypes.c_int32), ("gate", ctypes.c_int32), ("up", ctypes.c_int32), ("down", ctypes.c_int32)]
 
 
+class atsi_moe(ctypes.Structure):
+    _fields_ = [("n_experts", ctypes.c_int32), ("top_k", ctypes.c_int32), ("hidden", ctypes.c_int64),
+                ("inter", ctypes.c_int64), ("router_w_f16", ctypes.c_void_p), ("router_bias", ctypes.c_void_p),
+                ("gate", ctypes.POINTER(ctypes.c_int32)), ("up", ctypes.POINTER(ctypes.c_int32)),
+                ("down", ctypes.POINTER(ctypes.c_int32))]
+
+
+class atsi_moe_debug(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in ("logits", "idx", "p", "counts", "offsets", "perm", "inv_perm")]
+
+
 _P = ctypes.c_void_p
 _SIGS = {
     "atsi_create": ([ctypes.c_int, _P, _P, _P, ctypes.c_size_t, ctypes.c_int, ctypes.POINTER(_P)], ctypes.c_int),
@@ -45,6 +56,9 @@ _SIGS = {
     "atsi_linear": ([_P, ctypes.c_int32, _P, ctypes.c_int64, _P], ctypes.c_int),
     "atsi_ffn_swiglu": ([_P, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _P, ctypes.c_int64, _P], ctypes.c_int),
     "atsi_decoder_layer": ([_P, ctypes.POINTER(atsi_dense_layer), _P, ctypes.c_int64, _P, _P], ctypes.c_int),
+    "atsi_moe_ffn": ([_P, ctypes.POINTER(atsi_moe), _P, ctypes.c_int64, _P, ctypes.POINTER(atsi_moe_debug)],
+                     ctypes.c_int),
+    "atsi_moe_bucket": ([_P, _P, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, _P, _P, _P, _P], ctypes.c_int),
     "atsi_set_schedule": ([_P, _P, ctypes.c_int32], ctypes.c_int),
     "atsi_prefetch": ([_P, ctypes.c_int32], ctypes.c_int),
     "atsi_sync": ([_P], ctypes.c_int),
@@ -116,6 +130,15 @@ def atsi_ffn_swiglu(ctx: int, gate: int, up: int, down: int, x: int, M: int, y: 
 
 def atsi_decoder_layer(ctx: int, layer: atsi_dense_layer, h: int, M: int, q_out: int = 0, k_out: int = 0) -> None:
     _check(ctx, lib().atsi_decoder_layer(ctx, ctypes.byref(layer), h, M, q_out or None, k_out or None))
+
+
+def atsi_moe_ffn(ctx: int, moe: atsi_moe, x: int, M: int, y: int, dbg: atsi_moe_debug | None = None) -> None:
+    _check(ctx, lib().atsi_moe_ffn(ctx, ctypes.byref(moe), x, M, y, ctypes.byref(dbg) if dbg is not None else None))
+
+
+def atsi_moe_bucket(ctx: int, idx: int, M: int, k: int, n_experts: int, counts: int, offsets: int, perm: int,
+                    inv_perm: int) -> None:
+    _check(ctx, lib().atsi_moe_bucket(ctx, idx, M, k, n_experts, counts, offsets, perm, inv_perm))
 
 
 def atsi_set_schedule(ctx: int, order) -> None:

@@ -22,6 +22,7 @@
 
 #include "../../include/atsi.h"
 #include "common.h"
+#include "moe.h"
 
 using namespace atsi;
 
@@ -72,6 +73,18 @@ struct atsi_ctx {
   size_t sched_pos = 0;            // next schedule position not yet queued
   std::deque<atsi_tid> queue;      // host tensors to copy ahead, in consumption order
   uint64_t clock = 0;
+  // MoE expert tables, stacked down from the top of the workspace
+  struct MoeTable {
+    std::vector<atsi_tid> key;  // gate ids, up ids, down ids
+    size_t off = 0;             // ExpertW[E] then uint8 resident[E]
+    uint64_t version = ~0ull;   // placement version it was written for
+    int n_streamed = 0;         // experts with a host-resident tensor
+  };
+  std::vector<MoeTable> tables;
+  size_t table_floor = 0;       // lowest byte used by tables (ws_bytes if none)
+  uint64_t placement_version = 0;
+  int32_t* pinned = nullptr;    // pinned host copy of per-expert counts
+  hipEvent_t counts_ev = nullptr;
   std::string err;
   atsi_status latched = ATSI_OK;
   std::string latched_msg;
@@ -128,8 +141,9 @@ atsi_status layout_slots(atsi_ctx* c) {
   size_t need = 0;
   for (const Tensor& t : c->tensors)
     if (t.on_host) need = std::max(need, t.slot_need());
-  if (need > 0 && (size_t)c->n_slots * need > c->ws_bytes)
-    return fail(c, ATSI_E_WORKSPACE, "workspace %zu B < %d slots x %zu B", c->ws_bytes, c->n_slots, need);
+  if (need > 0 && (size_t)c->n_slots * need > c->table_floor)
+    return fail(c, ATSI_E_WORKSPACE, "workspace %zu B (%zu B free of expert tables) < %d slots x %zu B",
+                c->ws_bytes, c->table_floor, c->n_slots, need);
   HIP_TRY(c, hipStreamSynchronize(c->cs));
   HIP_TRY(c, hipStreamSynchronize(c->ts));
   c->slot_bytes = need;
@@ -279,12 +293,61 @@ struct Scratch {
   explicit Scratch(atsi_ctx* ctx) : c(ctx), off(ctx->scratch_off) {}
   __half* take(size_t elems, size_t elem_bytes = 2) {
     size_t need = align_up(elems * elem_bytes);
-    if (off + need > c->ws_bytes) return nullptr;
+    if (off + need > c->table_floor) return nullptr;
     char* p = c->ws + off;
     off += need;
     return reinterpret_cast<__half*>(p);
   }
 };
+
+// Device table of expert weights for one MoE layer, cached at the top of the
+// workspace and rewritten (by kernel, no host staging) when placement changes.
+atsi_status get_table(atsi_ctx* c, const atsi_moe* m, atsi_ctx::MoeTable** out) {
+  const int E = m->n_experts;
+  std::vector<atsi_tid> key(3 * E);
+  for (int e = 0; e < E; ++e) {
+    key[e] = m->gate[e];
+    key[E + e] = m->up[e];
+    key[2 * E + e] = m->down[e];
+  }
+  atsi_ctx::MoeTable* tb = nullptr;
+  for (auto& t : c->tables)
+    if (t.key == key) tb = &t;
+  if (!tb) {
+    const size_t need = align_up((size_t)E * sizeof(ExpertW)) + align_up((size_t)E);
+    if (c->table_floor < need || c->table_floor - need < c->scratch_off)
+      return fail(c, ATSI_E_WORKSPACE, "no workspace left for a %d-expert table", E);
+    c->table_floor -= need;
+    c->tables.push_back(atsi_ctx::MoeTable{key, c->table_floor, ~0ull, 0});
+    tb = &c->tables.back();
+  }
+  if (tb->version != c->placement_version) {
+    ExpertW* dev = reinterpret_cast<ExpertW*>(c->ws + tb->off);
+    uint8_t* res = reinterpret_cast<uint8_t*>(c->ws + tb->off + align_up((size_t)E * sizeof(ExpertW)));
+    tb->n_streamed = 0;
+    for (int e0 = 0; e0 < E; e0 += 16) {
+      const int n = std::min(16, E - e0);
+      ExpertW w[16];
+      uint8_t r[16];
+      for (int i = 0; i < n; ++i) {
+        const Tensor* ts[3] = {&c->tensors[m->gate[e0 + i]], &c->tensors[m->up[e0 + i]], &c->tensors[m->down[e0 + i]]};
+        QView* qv[3] = {&w[i].gate, &w[i].up, &w[i].down};
+        bool resident = true;
+        for (int j = 0; j < 3; ++j) {
+          *qv[j] = QView{ts[j]->dcodes, ts[j]->dscales, (int)ts[j]->K, (int)ts[j]->N};
+          resident = resident && !ts[j]->on_host;
+        }
+        r[i] = resident ? 1 : 0;
+        tb->n_streamed += resident ? 0 : 1;
+      }
+      hipError_t e = launch_table_patch(dev, res, e0, n, w, r, c->cs);
+      if (e != hipSuccess) return hip_fail(c, e, "expert table patch");
+    }
+    tb->version = c->placement_version;
+  }
+  *out = tb;
+  return ATSI_OK;
+}
 
 // Acquire the tensors of a fused launch (segment order; SwiGLU: gate, up),
 // launch the GEMV (M <= 4) or the GEMM, release the slots.
@@ -346,7 +409,14 @@ atsi_status atsi_create(int device, void* compute_stream, void* transfer_stream,
   c->ws = (char*)workspace;
   c->ws_bytes = workspace_bytes;
   c->n_slots = n_slots;
+  c->table_floor = workspace_bytes / kAlign * kAlign;
   c->slots.resize(n_slots);
+  if (hipHostMalloc((void**)&c->pinned, kMaxExperts * sizeof(int32_t), hipHostMallocDefault) != hipSuccess ||
+      hipEventCreateWithFlags(&c->counts_ev, hipEventDisableTiming) != hipSuccess) {
+    fail(nullptr, ATSI_E_HIP, "pinned staging or event allocation failed");
+    atsi_destroy(c);
+    return ATSI_E_HIP;
+  }
   for (Slot& s : c->slots) {
     if (hipEventCreateWithFlags(&s.ready, hipEventDisableTiming) != hipSuccess ||
         hipEventCreateWithFlags(&s.free, hipEventDisableTiming) != hipSuccess) {
@@ -368,6 +438,8 @@ atsi_status atsi_destroy(atsi_ctx* c) {
     if (s.ready) hipEventDestroy(s.ready);
     if (s.free) hipEventDestroy(s.free);
   }
+  if (c->counts_ev) hipEventDestroy(c->counts_ev);
+  if (c->pinned) hipHostFree(c->pinned);
   delete c;
   return ATSI_OK;
 }
@@ -437,6 +509,7 @@ atsi_status atsi_set_placement(atsi_ctx* c, const uint8_t* host_mask, int32_t n)
     for (int32_t i = 0; i < n; ++i) c->tensors[i].on_host = old[i];
     return st;
   }
+  ++c->placement_version;
   return ATSI_OK;
 }
 
@@ -535,6 +608,148 @@ atsi_status atsi_decoder_layer(atsi_ctx* c, const atsi_dense_layer* L, void* h, 
   LinOp dn = plain_op(QView{nullptr, nullptr, (int)td.K, (int)td.N}, hf, Mi, hh);
   dn.res = hh;
   return run_op(c, dn, &ids[6], 1);
+}
+
+atsi_status atsi_moe_bucket(atsi_ctx* c, const int32_t* idx, int64_t M, int32_t k, int32_t E, int32_t* counts,
+                            int32_t* offsets, int32_t* perm, int32_t* inv_perm) {
+  if (!c) return ATSI_E_INVALID;
+  if (!idx || !counts || !offsets || !perm || !inv_perm) return fail(c, ATSI_E_INVALID, "NULL buffer");
+  if (E < 1 || E > kMaxExperts || k < 1 || k > kMaxTopK || k > E || M < 1 || M > 65536)
+    return fail(c, ATSI_E_SHAPE, "bucket: E=%d k=%d M=%lld out of range", E, k, (long long)M);
+  atsi_status st = enter(c);
+  if (st) return st;
+  Scratch sc(c);
+  int32_t* order = (int32_t*)sc.take(E, 4);
+  int32_t* tiles = (int32_t*)sc.take(2 * ((size_t)M * k + E + 1), 4);
+  int32_t* nt = (int32_t*)sc.take(1, 4);
+  if (!order || !tiles || !nt) return fail(c, ATSI_E_WORKSPACE, "scratch too small for bucketing");
+  hipError_t e = launch_bucket(idx, (int)M, k, E, nullptr, 1, counts, offsets, perm, inv_perm, order, tiles, nt, c->cs);
+  if (e != hipSuccess) return hip_fail(c, e, "bucket launch");
+  return ATSI_OK;
+}
+
+atsi_status atsi_moe_ffn(atsi_ctx* c, const atsi_moe* m, const void* x, int64_t M, void* y,
+                         const atsi_moe_debug* dbg) {
+  if (!c) return ATSI_E_INVALID;
+  if (!m) return fail(c, ATSI_E_INVALID, "moe descriptor is NULL");
+  atsi_status st;
+  if ((st = check_act(c, x, "x")) || (st = check_act(c, y, "y")) || (st = check_m(c, M))) return st;
+  const int E = m->n_experts, k = m->top_k;
+  if (E < 16 || E > kMaxExperts || E % 16 != 0 || k < 1 || k > kMaxTopK || k > E)
+    return fail(c, ATSI_E_SHAPE, "n_experts %d (multiple of 16, <= %d) / top_k %d (1..16) unsupported", E,
+                kMaxExperts, k);
+  if (m->hidden < 32 || m->hidden % 32 || m->inter < 32 || m->inter % 32)
+    return fail(c, ATSI_E_SHAPE, "hidden %lld / inter %lld must be positive multiples of 32", (long long)m->hidden,
+                (long long)m->inter);
+  if (!m->router_w_f16 || !aligned16(m->router_w_f16) || !m->gate || !m->up || !m->down)
+    return fail(c, ATSI_E_INVALID, "router weights (16-byte aligned) and expert id arrays are required");
+  if (x == y) return fail(c, ATSI_E_INVALID, "y must not alias x");
+  const int H = (int)m->hidden, I = (int)m->inter;
+  for (int e = 0; e < E; ++e) {
+    if ((st = check_tid(c, m->gate[e])) || (st = check_tid(c, m->up[e])) || (st = check_tid(c, m->down[e]))) return st;
+    const Tensor &g = c->tensors[m->gate[e]], &u = c->tensors[m->up[e]], &d = c->tensors[m->down[e]];
+    if (g.K != H || g.N != I || u.K != H || u.N != I || d.K != I || d.N != H)
+      return fail(c, ATSI_E_SHAPE, "expert %d: gate/up must be %d x %d and down %d x %d", e, H, I, I, H);
+  }
+  if ((st = enter(c))) return st;
+  atsi_ctx::MoeTable* tb;
+  if ((st = get_table(c, m, &tb))) return st;
+  const int Mi = (int)M, Mk = Mi * k;
+  const bool gemv = Mi <= 4;
+  const int bm = expert_tile_rows(gemv);
+  Scratch sc(c);
+  float* part = (float*)sc.take(router_partial_floats(Mi, H, E), 4);
+  int32_t* idx = dbg && dbg->idx ? dbg->idx : (int32_t*)sc.take(Mk, 4);
+  float* p = dbg && dbg->p ? dbg->p : (float*)sc.take(Mk, 4);
+  int32_t* counts = dbg && dbg->counts ? dbg->counts : (int32_t*)sc.take(E, 4);
+  int32_t* offsets = dbg && dbg->offsets ? dbg->offsets : (int32_t*)sc.take(E + 1, 4);
+  int32_t* perm = dbg && dbg->perm ? dbg->perm : (int32_t*)sc.take(Mk, 4);
+  int32_t* inv = dbg && dbg->inv_perm ? dbg->inv_perm : (int32_t*)sc.take(Mk, 4);
+  int32_t* order = (int32_t*)sc.take(E, 4);
+  int32_t* tiles = (int32_t*)sc.take(2 * ((size_t)Mk / bm + E + 1), 4);
+  int32_t* ntiles = (int32_t*)sc.take(1, 4);
+  __half* h = sc.take((size_t)Mk * I);
+  __half* out = sc.take((size_t)Mk * H);
+  if (!part || !idx || !p || !counts || !offsets || !perm || !inv || !order || !tiles || !ntiles || !h || !out)
+    return fail(c, ATSI_E_WORKSPACE, "scratch too small for a %d-token MoE layer", Mi);
+  const ExpertW* table = reinterpret_cast<const ExpertW*>(c->ws + tb->off);
+  const uint8_t* resident = reinterpret_cast<const uint8_t*>(c->ws + tb->off + align_up((size_t)E * sizeof(ExpertW)));
+
+  hipError_t e = launch_router((const __half*)x, (const __half*)m->router_w_f16, m->router_bias, Mi, H, E, k, part,
+                               idx, p, dbg ? dbg->logits : nullptr, c->cs);
+  if (e != hipSuccess) return hip_fail(c, e, "router launch");
+  e = launch_bucket(idx, Mi, k, E, resident, bm, counts, offsets, perm, inv, order, tiles, ntiles, c->cs);
+  if (e != hipSuccess) return hip_fail(c, e, "bucket launch");
+  if (tb->n_streamed > 0) {
+    HIP_TRY(c, hipMemcpyAsync(c->pinned, counts, E * sizeof(int32_t), hipMemcpyDeviceToHost, c->cs));
+    HIP_TRY(c, hipEventRecord(c->counts_ev, c->cs));
+  }
+  MoeArgs a{};
+  a.table = table;
+  a.tiles = tiles;
+  a.n_tiles = ntiles;
+  a.counts = counts;
+  a.offsets = offsets;
+  a.perm = perm;
+  a.x = (const __half*)x;
+  a.h = h;
+  a.out = out;
+  a.k = k;
+  a.H = H;
+  a.I = I;
+  // HBM-resident experts first: they run while the host learns which
+  // streamed experts are needed.
+  const int bound = bm == 1 ? Mk : Mk / bm + std::min(E, Mk);
+  if ((e = launch_expert_gateup(a, bound, gemv, c->cs)) != hipSuccess) return hip_fail(c, e, "expert gate/up launch");
+  if ((e = launch_expert_down(a, bound, gemv, c->cs)) != hipSuccess) return hip_fail(c, e, "expert down launch");
+
+  if (tb->n_streamed > 0) {
+    HIP_TRY(c, hipEventSynchronize(c->counts_ev));
+    std::vector<int> act;
+    for (int ex = 0; ex < E; ++ex) {
+      const Tensor &g = c->tensors[m->gate[ex]], &u = c->tensors[m->up[ex]], &d = c->tensors[m->down[ex]];
+      if ((g.on_host || u.on_host || d.on_host) && c->pinned[ex] > 0) act.push_back(ex);
+    }
+    std::stable_sort(act.begin(), act.end(), [&](int l, int r) { return c->pinned[l] > c->pinned[r]; });
+    for (int ex : act)
+      for (const atsi_tid t : {m->gate[ex], m->up[ex], m->down[ex]})
+        if (c->tensors[t].on_host) c->queue.push_back(t);
+    if ((st = topup(c))) return st;
+    const int B = std::max(1, std::min(kBatchExp, c->n_slots / 3));
+    for (size_t b0 = 0; b0 < act.size(); b0 += B) {
+      std::vector<int> held;
+      MoeArgs ba = a;
+      ba.nb = 0;
+      const int nbx = (int)std::min<size_t>(B, act.size() - b0);
+      for (int b = 0; b < nbx; ++b) {
+        const int ex = act[b0 + b];
+        ba.bexp[b] = ex;
+        if ((st = acquire(c, m->gate[ex], &ba.bw[b].gate, held)) || (st = acquire(c, m->up[ex], &ba.bw[b].up, held)) ||
+            (st = acquire(c, m->down[ex], &ba.bw[b].down, held)))
+          return st;
+      }
+      auto flush = [&]() -> atsi_status {
+        if (ba.nb == 0) return ATSI_OK;
+        hipError_t fe = launch_expert_gateup(ba, ba.nb, gemv, c->cs);
+        if (fe == hipSuccess) fe = launch_expert_down(ba, ba.nb, gemv, c->cs);
+        if (fe != hipSuccess) return hip_fail(c, fe, "streamed expert launch");
+        ba.nb = 0;
+        return ATSI_OK;
+      };
+      for (int b = 0; b < nbx; ++b) {
+        const int cnt = c->pinned[act[b0 + b]];
+        for (int r0 = 0; r0 < cnt; r0 += bm) {
+          if (ba.nb == kBatchTiles && (st = flush())) return st;
+          ba.btiles[ba.nb++] = make_int2(b, r0);
+        }
+      }
+      if ((st = flush())) return st;
+      if ((st = release(c, held))) return st;
+    }
+  }
+  e = launch_combine(out, p, Mi, k, H, (__half*)y, c->cs);
+  if (e != hipSuccess) return hip_fail(c, e, "combine launch");
+  return ATSI_OK;
 }
 
 atsi_status atsi_set_schedule(atsi_ctx* c, const atsi_tid* order, int32_t n) {

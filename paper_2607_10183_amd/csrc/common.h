@@ -44,6 +44,8 @@ struct LinOp {
   int head_dim;      // granularity of `expand`
 };
 
+__device__ __forceinline__ float silu_f(float g) { return g / (1.f + expf(-g)); }
+
 // ---- launchers (each returns hipGetLastError() of its launch) ----
 hipError_t launch_gemv(const LinOp& op, hipStream_t s);
 hipError_t launch_gemm(const LinOp& op, hipStream_t s);

@@ -1,0 +1,61 @@
+// Internal definitions of the MoE path: routing, bucketing, grouped expert
+// kernels and the combine.
+#pragma once
+
+#include "common.h"
+
+namespace atsi {
+
+constexpr int kMaxExperts = 128;   // experts per layer handled by one launch
+constexpr int kMaxTopK = 16;
+constexpr int kBatchExp = 4;       // streamed experts per batch launch
+constexpr int kBatchTiles = 64;    // row tiles per batch launch
+
+// The three weight tensors of one SwiGLU expert.
+struct ExpertW {
+  QView gate, up, down;
+};
+
+// One grouped-expert launch.  A "tile" is (expert, first row) over the rows
+// of that expert's bucket (rows offsets[e] .. offsets[e+1] of the routed
+// pairs ordered by expert); rows hold pair ids k*t + j.
+struct MoeArgs {
+  const ExpertW* table;        // device table indexed by expert id (resident launches)
+  const int32_t* tiles;        // device list of (expert, row0) (resident launches)
+  const int32_t* n_tiles;      // device count of that list
+  int nb;                      // > 0: batch launch over btiles with weights bw
+  int2 btiles[kBatchTiles];    // (index into bexp/bw, row0)
+  int bexp[kBatchExp];
+  ExpertW bw[kBatchExp];
+  const int32_t* counts;
+  const int32_t* offsets;
+  const int32_t* perm;
+  const __half* x;             // tokens [M][H]
+  __half* h;                   // SwiGLU activations [M*k][I], row = bucket position
+  __half* out;                 // expert outputs [M*k][H], row = pair id
+  int k, H, I;
+};
+
+// router: logits = x W_r + b (fp32 accumulation), top-k with renormalised softmax
+hipError_t launch_router(const __half* x, const __half* wr, const float* bias, int M, int H, int E, int k,
+                         float* part, int32_t* idx, float* p, float* logits, hipStream_t s);
+size_t router_partial_floats(int M, int H, int E);
+
+// bucketing (single workgroup): counts, offsets, perm, inv_perm, heavy-first
+// expert order and the row tiles (of bm_rows) of experts with resident[e] != 0
+hipError_t launch_bucket(const int32_t* idx, int M, int k, int E, const uint8_t* resident, int bm_rows,
+                         int32_t* counts, int32_t* offsets, int32_t* perm, int32_t* inv_perm, int32_t* order,
+                         int32_t* tiles, int32_t* n_tiles, hipStream_t s);
+
+// rows per tile of the grouped expert kernels (1 on the GEMV path)
+int expert_tile_rows(bool gemv);
+// grouped SwiGLU gate/up and grouped down; tile_bound = grid size in tiles
+hipError_t launch_expert_gateup(const MoeArgs& a, int tile_bound, bool gemv, hipStream_t s);
+hipError_t launch_expert_down(const MoeArgs& a, int tile_bound, bool gemv, hipStream_t s);
+// y[t] = sum_j p[t][j] * out[k*t + j] (fp32, slot order) -> fp16
+hipError_t launch_combine(const __half* out, const float* p, int M, int k, int H, __half* y, hipStream_t s);
+// write table entries e0 .. e0+n-1 (n <= 16) and their residency flags
+hipError_t launch_table_patch(ExpertW* table, uint8_t* resident, int e0, int n, const ExpertW* w, const uint8_t* r,
+                              hipStream_t s);
+
+}  // namespace atsi

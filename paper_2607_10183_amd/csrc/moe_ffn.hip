@@ -1,0 +1,263 @@
+// Grouped SwiGLU expert FFN and the weighted combine.
+//
+// Routed pairs are bucketed by expert (moe_route.hip), so each expert sees a
+// contiguous run of rows; its tokens are gathered row by row straight from
+// the token matrix.  Work is a list of row tiles (expert, first row), ordered
+// heavy-first: the expert with the most tokens starts first, so the Zipf head
+// does not finish last.  Only experts some token selected are ever read.
+//   gate/up : h[i] = silu(x[t] Wg_e) * (x[t] Wu_e) for bucket row i of pair
+//             (t, j), on the MFMA tile (prefill) or a GEMV (decode);
+//   down    : out[k*t + j] = h[i] Wd_e, stored by pair id (fp16);
+//   combine : y[t] = sum_j p[t][j] * out[k*t + j] in fp32, slot order, one
+//             rounding to fp16 -- no atomics, so results are deterministic.
+// A launch reads expert weights either from the device table (HBM-resident
+// experts) or, for a batch of experts streamed into temporary buffers, from
+// its own arguments.
+#include "moe.h"
+#include "q4_gemm_core.h"
+#include "q4_gemv_core.h"
+
+namespace atsi {
+namespace {
+
+__device__ __forceinline__ bool fetch_tile(const MoeArgs& a, int tix, int& e, int& row0, ExpertW& w) {
+  if (a.nb > 0) {
+    if (tix >= a.nb) return false;
+    const int2 t = a.btiles[tix];
+    e = a.bexp[t.x];
+    row0 = t.y;
+    w = a.bw[t.x];
+    return true;
+  }
+  if (tix >= *a.n_tiles) return false;
+  e = a.tiles[2 * tix];
+  row0 = a.tiles[2 * tix + 1];
+  w = a.table[e];
+  return true;
+}
+
+constexpr int EBM = 64;   // rows per expert tile on the MFMA path
+constexpr int EBN = 128;
+
+// ---------------------------------------------------------------- MFMA path
+
+__global__ __launch_bounds__(kGemmBlock, 2) void expert_gateup_gemm(MoeArgs a, int tile_bound) {
+  using Core = GemmCore<EBM, EBN, 2, 2, true>;
+  __shared__ __attribute__((aligned(16))) Core::Smem sm;
+  const int tix = blockIdx.x % tile_bound, tn = blockIdx.x / tile_bound;
+  int e, row0;
+  ExpertW w;
+  if (!fetch_tile(a, tix, e, row0, w)) return;
+  const int cnt = a.counts[e], base = a.offsets[e] + row0;
+  const int rows = min(EBM, cnt - row0);
+  const int n0 = tn * Core::NOUT;
+  const __half* arow[Core::XV];
+#pragma unroll
+  for (int i = 0; i < Core::XV; ++i) {
+    const int r = Core::xrow(i);
+    arow[i] = r < rows ? a.x + (size_t)(a.perm[base + r] / a.k) * a.H : nullptr;
+  }
+  g_float16_t acc[Core::FM][Core::FN];
+  Core::run(sm, arow, w.gate, w.up, n0, a.H, false, 0.f, acc);
+#pragma unroll
+  for (int i = 0; i < Core::FM; ++i)
+#pragma unroll
+    for (int j = 0; j < Core::FN; j += 2) {
+      const int n = n0 + Core::frag_col(j);
+      if (n >= a.I) continue;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int r = Core::frag_row(i, v);
+        if (r < rows) a.h[(size_t)(base + r) * a.I + n] = __float2half_rn(silu_f(acc[i][j][v]) * acc[i][j + 1][v]);
+      }
+    }
+}
+
+__global__ __launch_bounds__(kGemmBlock, 2) void expert_down_gemm(MoeArgs a, int tile_bound) {
+  using Core = GemmCore<EBM, EBN, 2, 2, false>;
+  __shared__ __attribute__((aligned(16))) Core::Smem sm;
+  const int tix = blockIdx.x % tile_bound, tn = blockIdx.x / tile_bound;
+  int e, row0;
+  ExpertW w;
+  if (!fetch_tile(a, tix, e, row0, w)) return;
+  const int cnt = a.counts[e], base = a.offsets[e] + row0;
+  const int rows = min(EBM, cnt - row0);
+  const int n0 = tn * Core::NOUT;
+  const __half* arow[Core::XV];
+#pragma unroll
+  for (int i = 0; i < Core::XV; ++i) {
+    const int r = Core::xrow(i);
+    arow[i] = r < rows ? a.h + (size_t)(base + r) * a.I : nullptr;
+  }
+  g_float16_t acc[Core::FM][Core::FN];
+  Core::run(sm, arow, w.down, w.down, n0, a.I, false, 0.f, acc);
+#pragma unroll
+  for (int i = 0; i < Core::FM; ++i)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int r = Core::frag_row(i, v);
+      if (r >= rows) continue;
+      const size_t prow = (size_t)a.perm[base + r] * a.H;
+#pragma unroll
+      for (int j = 0; j < Core::FN; ++j) {
+        const int n = n0 + Core::frag_col(j);
+        if (n < a.H) a.out[prow + n] = __float2half_rn(acc[i][j][v]);
+      }
+    }
+}
+
+// ---------------------------------------------------------------- GEMV path (one row per tile)
+
+template <int RW, bool DOWN>
+__global__ __launch_bounds__(gemv::kBlock) void expert_gemv(MoeArgs a, int tile_bound) {
+  using namespace gemv;
+  const int tix = blockIdx.x % tile_bound, nb = blockIdx.x / tile_bound;
+  int e, row0;
+  ExpertW w;
+  if (!fetch_tile(a, tix, e, row0, w)) return;
+  const int i = a.offsets[e] + row0;
+  const int pr = a.perm[i];
+  const QView w1 = DOWN ? w.down : w.gate;
+  const QView w2 = w.up;
+  const int K = DOWN ? a.I : a.H, N = DOWN ? a.H : a.I;
+  const __half* xr = DOWN ? a.h + (size_t)i * a.I : a.x + (size_t)(pr / a.k) * a.H;
+
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+  const int n0 = (nb * (kBlock / kWave) + wave) * RW;
+  if (n0 >= N) return;
+  const int nchunk = K / kGroup;
+  const size_t rbytes = (size_t)K / 2;
+  float acc[RW], acc2[RW], sq[1] = {0.f};
+#pragma unroll
+  for (int r = 0; r < RW; ++r) acc[r] = acc2[r] = 0.f;
+  for (int c = lane; c < nchunk; c += kWave) {
+    uint4 cw[RW], cw2[RW];
+    float sc[RW], sc2[RW];
+#pragma unroll
+    for (int r = 0; r < RW; ++r) {
+      const int row = min(n0 + r, N - 1);
+      cw[r] = *reinterpret_cast<const uint4*>(w1.codes + (size_t)row * rbytes + (size_t)c * 16);
+      sc[r] = __half2float(__ushort_as_half(w1.scales[(size_t)row * nchunk + c]));
+      if (!DOWN) {
+        cw2[r] = *reinterpret_cast<const uint4*>(w2.codes + (size_t)row * rbytes + (size_t)c * 16);
+        sc2[r] = __half2float(__ushort_as_half(w2.scales[(size_t)row * nchunk + c]));
+      }
+    }
+    XChunk<1> xc;
+    load_x<1>(xc, xr, K, 1, c, false, sq);
+#pragma unroll
+    for (int r = 0; r < RW; ++r) {
+      float part[1];
+      group_dot<1>(cw[r], xc, part);
+      acc[r] = fmaf(sc[r], part[0] - 1032.f * xc.sum[0], acc[r]);
+      if (!DOWN) {
+        group_dot<1>(cw2[r], xc, part);
+        acc2[r] = fmaf(sc2[r], part[0] - 1032.f * xc.sum[0], acc2[r]);
+      }
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < RW; ++r) {
+    const float g = wave_sum(acc[r]);
+    const float u = DOWN ? 0.f : wave_sum(acc2[r]);
+    const int n = n0 + r;
+    if (lane == r && n < N) {
+      if (DOWN)
+        a.out[(size_t)pr * a.H + n] = __float2half_rn(g);
+      else
+        a.h[(size_t)i * a.I + n] = __float2half_rn(silu_f(g) * u);
+    }
+  }
+}
+
+constexpr int kGemvRW = 2;
+
+// ---------------------------------------------------------------- combine, table patch
+
+__global__ void combine_kernel(const __half* __restrict__ out, const float* __restrict__ p, int M, int k, int H,
+                               __half* __restrict__ y) {
+  const int c8 = H / 8;
+  const size_t total = (size_t)M * c8;
+  for (size_t q = (size_t)blockIdx.x * blockDim.x + threadIdx.x; q < total; q += (size_t)gridDim.x * blockDim.x) {
+    const int t = (int)(q / c8), c = (int)(q % c8);
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < k; ++j) {
+      const float pj = p[(size_t)t * k + j];
+      const uint4 v = *reinterpret_cast<const uint4*>(out + ((size_t)t * k + j) * H + (size_t)c * 8);
+      const __half* hv = reinterpret_cast<const __half*>(&v);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) acc[i] = fmaf(pj, __half2float(hv[i]), acc[i]);
+    }
+    uint4 o;
+    __half* ho = reinterpret_cast<__half*>(&o);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) ho[i] = __float2half_rn(acc[i]);
+    *reinterpret_cast<uint4*>(y + (size_t)t * H + (size_t)c * 8) = o;
+  }
+}
+
+struct TablePatch {
+  int e0, n;
+  ExpertW w[16];
+  uint8_t r[16];
+};
+
+__global__ void table_patch_kernel(ExpertW* table, uint8_t* resident, TablePatch tp) {
+  const int i = threadIdx.x;
+  if (i < tp.n) {
+    table[tp.e0 + i] = tp.w[i];
+    resident[tp.e0 + i] = tp.r[i];
+  }
+}
+
+}  // namespace
+
+int expert_tile_rows(bool gemv) { return gemv ? 1 : EBM; }
+
+hipError_t launch_expert_gateup(const MoeArgs& a, int tile_bound, bool gemv, hipStream_t s) {
+  if (tile_bound <= 0) return hipSuccess;
+  if (gemv) {
+    const int nblk = (a.I + 4 * kGemvRW - 1) / (4 * kGemvRW);
+    hipLaunchKernelGGL((expert_gemv<kGemvRW, false>), dim3(tile_bound * nblk), dim3(gemv::kBlock), 0, s, a,
+                       tile_bound);
+  } else {
+    const int tn = (a.I + EBN / 2 - 1) / (EBN / 2);
+    hipLaunchKernelGGL(expert_gateup_gemm, dim3(tile_bound * tn), dim3(kGemmBlock), 0, s, a, tile_bound);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_expert_down(const MoeArgs& a, int tile_bound, bool gemv, hipStream_t s) {
+  if (tile_bound <= 0) return hipSuccess;
+  if (gemv) {
+    const int nblk = (a.H + 4 * kGemvRW - 1) / (4 * kGemvRW);
+    hipLaunchKernelGGL((expert_gemv<kGemvRW, true>), dim3(tile_bound * nblk), dim3(gemv::kBlock), 0, s, a,
+                       tile_bound);
+  } else {
+    const int tn = (a.H + EBN - 1) / EBN;
+    hipLaunchKernelGGL(expert_down_gemm, dim3(tile_bound * tn), dim3(kGemmBlock), 0, s, a, tile_bound);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_combine(const __half* out, const float* p, int M, int k, int H, __half* y, hipStream_t s) {
+  const size_t total = (size_t)M * (H / 8);
+  const int blocks = (int)std::min<size_t>((total + 255) / 256, 2048);
+  hipLaunchKernelGGL(combine_kernel, dim3(blocks), dim3(256), 0, s, out, p, M, k, H, y);
+  return hipGetLastError();
+}
+
+hipError_t launch_table_patch(ExpertW* table, uint8_t* resident, int e0, int n, const ExpertW* w, const uint8_t* r,
+                              hipStream_t s) {
+  TablePatch tp{};
+  tp.e0 = e0;
+  tp.n = n;
+  for (int i = 0; i < n; ++i) {
+    tp.w[i] = w[i];
+    tp.r[i] = r[i];
+  }
+  hipLaunchKernelGGL(table_patch_kernel, dim3(1), dim3(64), 0, s, table, resident, tp);
+  return hipGetLastError();
+}
+
+}  // namespace atsi

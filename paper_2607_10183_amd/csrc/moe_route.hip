@@ -1,0 +1,271 @@
+// MoE routing on CDNA4: router logits, top-k selection with renormalised
+// softmax weights, and deterministic token-to-expert bucketing.
+//
+// The paper moves a MoE layer's expert weights only after routing is known
+// and only for the experts the current tokens selected (Sec. 4.2.2; Sec.
+// 4.4.1 counts only activated experts); these kernels produce that routing.
+//
+//   router_partial  logits of a 16-token tile for all experts over one K
+//                   slice, on 16x16x32 fp16 MFMAs; the router slice is staged
+//                   through LDS transposed so each lane reads 8 consecutive
+//                   inputs of one expert; fp32 partials per slice.
+//   router_topk     one wavefront per token: sums the K-slice partials in a
+//                   fixed order, adds the bias, selects the top k by (logit
+//                   descending, expert id ascending) with k wave-wide argmax
+//                   rounds, and writes the softmax over the selected logits.
+//   bucket          one workgroup: per-expert counts (LDS integer atomics),
+//                   exclusive scan, then a stable scatter of pair ids k*t + j
+//                   ordered by (expert, token): each 64-token chunk builds a
+//                   64-bit token mask per expert, a pair's rank is the
+//                   popcount of the lower lanes' bits plus the counts of the
+//                   earlier chunks.  Results do not depend on atomics order.
+//                   Also ranks experts heavy-first and lists the row tiles of
+//                   the HBM-resident experts for the grouped expert GEMM.
+#include "moe.h"
+
+namespace atsi {
+namespace {
+
+typedef _Float16 half8_t __attribute__((ext_vector_type(8)));
+typedef float float4_t __attribute__((ext_vector_type(4)));
+
+constexpr int kRT = 16;  // tokens per router tile
+
+// grid: (ceil(M/16), n_split); block 256 = 4 waves x 32 experts (E <= 128).
+// Requires E % 16 == 0, E <= 128, ks % 32 == 0.
+__global__ __launch_bounds__(256) void router_partial_kernel(const __half* __restrict__ x, const __half* __restrict__ wr,
+                                                             int M, int H, int E, int ks, float* __restrict__ part) {
+  __shared__ __attribute__((aligned(16))) _Float16 Bt[128 * (32 + 8)];  // [expert][k] of one 32-k step
+  const int t0 = blockIdx.x * kRT;
+  const int k_begin = blockIdx.y * ks;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int tr = lane & 15, kq = (lane >> 4) * 8;
+  float4_t acc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+  for (int k0 = k_begin; k0 < k_begin + ks; k0 += 32) {
+    // stage W_r[k0 .. k0+31][0 .. E) transposed: thread -> (k = tid / 16, 8 experts)
+    __syncthreads();
+    {
+      const int kk = threadIdx.x >> 4, e8 = (threadIdx.x & 15) * 8;
+      if (e8 < E) {
+        const uint4 v = *reinterpret_cast<const uint4*>(wr + (size_t)(k0 + kk) * E + e8);
+        const _Float16* hv = reinterpret_cast<const _Float16*>(&v);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) Bt[(e8 + i) * 40 + kk] = hv[i];
+      }
+      if (kk + 16 < 32) {
+        const int k2 = kk + 16;
+        if (e8 < E) {
+          const uint4 v = *reinterpret_cast<const uint4*>(wr + (size_t)(k0 + k2) * E + e8);
+          const _Float16* hv = reinterpret_cast<const _Float16*>(&v);
+#pragma unroll
+          for (int i = 0; i < 8; ++i) Bt[(e8 + i) * 40 + k2] = hv[i];
+        }
+      }
+    }
+    __syncthreads();
+    half8_t a;
+    const int t = t0 + tr;
+    if (t < M)
+      a = *reinterpret_cast<const half8_t*>(x + (size_t)t * H + k0 + kq);
+    else
+      a = half8_t{0, 0, 0, 0, 0, 0, 0, 0};
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) {
+      const int e = wave * 32 + nb * 16 + tr;
+      if (wave * 32 + nb * 16 < E) {
+        const half8_t b = *reinterpret_cast<const half8_t*>(&Bt[e * 40 + kq]);
+        acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, acc[nb], 0, 0, 0);
+      }
+    }
+  }
+  // 16x16 D layout: lane l holds column l % 16, rows 4 * (l / 16) + i
+#pragma unroll
+  for (int nb = 0; nb < 2; ++nb) {
+    const int e = wave * 32 + nb * 16 + (lane & 15);
+    if (wave * 32 + nb * 16 >= E) continue;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int t = t0 + 4 * (lane >> 4) + i;
+      if (t < M) part[((size_t)blockIdx.y * M + t) * E + e] = acc[nb][i];
+    }
+  }
+}
+
+// one wave per token; E <= 128 (two candidates per lane)
+__global__ __launch_bounds__(256) void router_topk_kernel(const float* __restrict__ part, int n_split,
+                                                          const float* __restrict__ bias, int M, int E, int k,
+                                                          int32_t* __restrict__ idx, float* __restrict__ p,
+                                                          float* __restrict__ logits_out) {
+  const int lane = threadIdx.x & 63;
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= M) return;
+  float v[2];
+  int id[2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int e = lane + 64 * h;
+    id[h] = e;
+    if (e < E) {
+      float s = 0.f;
+      for (int sp = 0; sp < n_split; ++sp) s += part[((size_t)sp * M + t) * E + e];
+      if (bias) s += bias[e];
+      v[h] = s;
+      if (logits_out) logits_out[(size_t)t * E + e] = s;
+    } else {
+      v[h] = -INFINITY;
+    }
+  }
+  float sel_v[16];
+  int sel_i[16];
+  for (int j = 0; j < k; ++j) {
+    // best of this lane: larger value, then lower id
+    float bv = v[0];
+    int bi = id[0];
+    if (v[1] > bv || (v[1] == bv && id[1] < bi)) { bv = v[1]; bi = id[1]; }
+    if (bi >= E) bi = 0x7fffffff;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const float ov = __shfl_xor(bv, o, 64);
+      const int oi = __shfl_xor(bi, o, 64);
+      if (ov > bv || (ov == bv && oi < bi)) { bv = ov; bi = oi; }
+    }
+    sel_v[j] = bv;
+    sel_i[j] = bi;
+    if (bi == id[0]) v[0] = -INFINITY, id[0] = 0x7fffffff;
+    if (bi == id[1]) v[1] = -INFINITY, id[1] = 0x7fffffff;
+  }
+  if (lane == 0) {
+    float den = 0.f;
+    for (int j = 0; j < k; ++j) den += expf(sel_v[j] - sel_v[0]);
+    for (int j = 0; j < k; ++j) {
+      idx[(size_t)t * k + j] = sel_i[j];
+      p[(size_t)t * k + j] = expf(sel_v[j] - sel_v[0]) / den;
+    }
+  }
+}
+
+// Single workgroup of 1024 threads.  Up to 16 chunks of 64 tokens are ranked
+// per pass; masks live in LDS.
+__global__ __launch_bounds__(1024) void bucket_kernel(const int32_t* __restrict__ idx, int M, int k, int E,
+                                                      const uint8_t* __restrict__ resident, int bm_rows,
+                                                      int32_t* __restrict__ counts, int32_t* __restrict__ offsets,
+                                                      int32_t* __restrict__ perm, int32_t* __restrict__ inv_perm,
+                                                      int32_t* __restrict__ order, int32_t* __restrict__ tiles,
+                                                      int32_t* __restrict__ n_tiles) {
+  __shared__ int cnt[kMaxExperts];
+  __shared__ int base[kMaxExperts];
+  __shared__ unsigned long long mask[16][kMaxExperts];
+  __shared__ int pre[16][kMaxExperts];
+  __shared__ int tstart[kMaxExperts + 1];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int pairs = M * k;
+  for (int e = tid; e < E; e += blockDim.x) cnt[e] = 0;
+  __syncthreads();
+  for (int i = tid; i < pairs; i += blockDim.x) {
+    const int e = idx[i];
+    if ((unsigned)e < (unsigned)E) atomicAdd(&cnt[e], 1);
+  }
+  __syncthreads();
+  if (tid == 0) {
+    int run = 0;
+    for (int e = 0; e < E; ++e) {
+      offsets[e] = run;
+      base[e] = run;
+      counts[e] = cnt[e];
+      run += cnt[e];
+    }
+    offsets[E] = run;
+  }
+  __syncthreads();
+  // stable scatter, 16 chunks of 64 tokens per pass
+  for (int c0 = 0; c0 * 64 < M; c0 += 16) {
+    for (int i = tid; i < 16 * E; i += blockDim.x) mask[i / E][i % E] = 0ull;
+    __syncthreads();
+    const int t = (c0 + wave) * 64 + lane;
+    if (t < M)
+      for (int j = 0; j < k; ++j) {
+        const int e = idx[(size_t)t * k + j];
+        if ((unsigned)e < (unsigned)E) atomicOr(&mask[wave][e], 1ull << lane);
+      }
+    __syncthreads();
+    for (int e = tid; e < E; e += blockDim.x) {
+      int run = base[e];
+      for (int c = 0; c < 16; ++c) {
+        pre[c][e] = run;
+        run += __popcll(mask[c][e]);
+      }
+      base[e] = run;
+    }
+    __syncthreads();
+    if (t < M) {
+      const unsigned long long below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+      for (int j = 0; j < k; ++j) {
+        const int e = idx[(size_t)t * k + j];
+        if ((unsigned)e >= (unsigned)E) continue;
+        const int pos = pre[wave][e] + __popcll(mask[wave][e] & below);
+        perm[pos] = t * k + j;
+        inv_perm[t * k + j] = pos;
+      }
+    }
+    __syncthreads();
+  }
+  // heavy-first expert order: (count descending, id ascending)
+  for (int e = tid; e < E; e += blockDim.x) {
+    int r = 0;
+    for (int f = 0; f < E; ++f) r += (cnt[f] > cnt[e]) || (cnt[f] == cnt[e] && f < e);
+    order[r] = e;
+  }
+  __syncthreads();
+  // row tiles of resident experts in heavy-first order: tile -> (expert, first row)
+  if (tid == 0) {
+    int run = 0;
+    for (int r = 0; r < E; ++r) {
+      const int e = order[r];
+      tstart[r] = run;
+      if (resident == nullptr || resident[e]) run += (cnt[e] + bm_rows - 1) / bm_rows;
+    }
+    tstart[E] = run;
+    *n_tiles = run;
+  }
+  __syncthreads();
+  for (int r = tid; r < E; r += blockDim.x) {
+    const int e = order[r];
+    const int nt = tstart[r + 1] - tstart[r];
+    for (int i = 0; i < nt; ++i) {
+      tiles[2 * (tstart[r] + i)] = e;
+      tiles[2 * (tstart[r] + i) + 1] = i * bm_rows;
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_router(const __half* x, const __half* wr, const float* bias, int M, int H, int E, int k,
+                         float* part, int32_t* idx, float* p, float* logits, hipStream_t s) {
+  // K slice per workgroup: enough workgroups to cover the chip, slices of >= 64
+  const int tiles = (M + kRT - 1) / kRT;
+  int ks = H;
+  while (ks > 64 && (long)tiles * (H / ks) < 512 && (ks / 2) % 32 == 0 && H % (ks / 2) == 0) ks /= 2;
+  const int n_split = H / ks;
+  hipLaunchKernelGGL(router_partial_kernel, dim3(tiles, n_split), dim3(256), 0, s, x, wr, M, H, E, ks, part);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(router_topk_kernel, dim3((M + 3) / 4), dim3(256), 0, s, part, n_split, bias, M, E, k, idx, p,
+                     logits);
+  return hipGetLastError();
+}
+
+size_t router_partial_floats(int M, int H, int E) {
+  // upper bound of n_split * M * E (n_split <= H / 64)
+  return (size_t)(H / 64 + 1) * M * E;
+}
+
+hipError_t launch_bucket(const int32_t* idx, int M, int k, int E, const uint8_t* resident, int bm_rows,
+                         int32_t* counts, int32_t* offsets, int32_t* perm, int32_t* inv_perm, int32_t* order,
+                         int32_t* tiles, int32_t* n_tiles, hipStream_t s) {
+  hipLaunchKernelGGL(bucket_kernel, dim3(1), dim3(1024), 0, s, idx, M, k, E, resident, bm_rows, counts, offsets, perm,
+                     inv_perm, order, tiles, n_tiles);
+  return hipGetLastError();
+}
+
+}  // namespace atsi

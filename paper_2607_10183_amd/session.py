@@ -110,6 +110,24 @@ class Session:
         self._torch_waits()
         return h
 
+    def moe_layer(self, router_w: torch.Tensor, gate, up, down, top_k: int,
+                  router_bias: torch.Tensor | None = None) -> "MoELayer":
+        return MoELayer(self, router_w, gate, up, down, top_k, router_bias)
+
+    def moe_bucket(self, idx: torch.Tensor, n_experts: int):
+        """Bucket device idx int32 [M][k]; returns (counts, offsets, perm, inv_perm)."""
+        M, k = idx.shape
+        with torch.cuda.stream(self.cs):
+            counts = torch.empty(n_experts, dtype=torch.int32, device=self.device)
+            offsets = torch.empty(n_experts + 1, dtype=torch.int32, device=self.device)
+            perm = torch.empty(M * k, dtype=torch.int32, device=self.device)
+            inv = torch.empty(M * k, dtype=torch.int32, device=self.device)
+        self._wait_torch()
+        atsi.atsi_moe_bucket(self.ctx, idx.data_ptr(), M, k, n_experts, counts.data_ptr(), offsets.data_ptr(),
+                             perm.data_ptr(), inv.data_ptr())
+        self._torch_waits()
+        return counts, offsets, perm, inv
+
     def set_schedule(self, order) -> None:
         atsi.atsi_set_schedule(self.ctx, list(order))
 
@@ -143,3 +161,46 @@ class Session:
 
     def __exit__(self, *exc):
         self.close()
+
+
+class MoELayer:
+    """Keeps an atsi_moe descriptor (and what it points at) alive."""
+
+    def __init__(self, sess: Session, router_w: torch.Tensor, gate, up, down, top_k: int,
+                 router_bias: torch.Tensor | None = None):
+        import ctypes
+        E = len(gate)
+        H, I = sess.shapes[gate[0]]
+        assert router_w.dtype == torch.float16 and tuple(router_w.shape) == (H, E)
+        self.sess = sess
+        self.E, self.H, self.I, self.k = E, H, I, top_k
+        self._ids = [(ctypes.c_int32 * E)(*[int(t) for t in ids]) for ids in (gate, up, down)]
+        self._keep = [router_w, router_bias]
+        self.desc = atsi.atsi_moe(E, top_k, H, I, router_w.data_ptr(),
+                                  router_bias.data_ptr() if router_bias is not None else None,
+                                  ctypes.cast(self._ids[0], ctypes.POINTER(ctypes.c_int32)),
+                                  ctypes.cast(self._ids[1], ctypes.POINTER(ctypes.c_int32)),
+                                  ctypes.cast(self._ids[2], ctypes.POINTER(ctypes.c_int32)))
+
+    def __call__(self, x: torch.Tensor, y: torch.Tensor | None = None, debug: bool = False):
+        s = self.sess
+        M = x.shape[0]
+        dbg = None
+        out = {}
+        with torch.cuda.stream(s.cs):
+            if y is None:
+                y = torch.empty((M, self.H), dtype=torch.float16, device=s.device)
+            if debug:
+                out = {"logits": torch.empty((M, self.E), dtype=torch.float32, device=s.device),
+                       "idx": torch.empty((M, self.k), dtype=torch.int32, device=s.device),
+                       "p": torch.empty((M, self.k), dtype=torch.float32, device=s.device),
+                       "counts": torch.empty(self.E, dtype=torch.int32, device=s.device),
+                       "offsets": torch.empty(self.E + 1, dtype=torch.int32, device=s.device),
+                       "perm": torch.empty(M * self.k, dtype=torch.int32, device=s.device),
+                       "inv_perm": torch.empty(M * self.k, dtype=torch.int32, device=s.device)}
+                dbg = atsi.atsi_moe_debug(*[out[n].data_ptr() for n in
+                                            ("logits", "idx", "p", "counts", "offsets", "perm", "inv_perm")])
+        s._wait_torch()
+        atsi.atsi_moe_ffn(s.ctx, self.desc, x.data_ptr(), M, y.data_ptr(), dbg)
+        s._torch_waits()
+        return (y, out) if debug else y

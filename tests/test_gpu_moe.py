@@ -1,0 +1,161 @@
+"""GPU parity of MoE routing, bucketing and the routed expert FFN against the
+fp64 oracle, plus placement invariance with streamed experts."""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from synth import configs
+from tests.parity import check
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def sess():
+    from paper_2607_10183_amd.session import Session
+    s = Session(workspace_bytes=2 << 30, n_slots=16)
+    yield s
+    s.close()
+
+
+def _dev(a):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def _random_idx(seed, M, k, E):
+    return np.stack([synth.permutation(seed, 5000 + t, E)[:k] for t in range(M)]).astype(np.int32)
+
+
+@pytest.mark.parametrize("M,k,E", [(1, 8, 128), (37, 4, 16), (512, 8, 128), (2048, 8, 128), (3000, 8, 128),
+                                   (64, 16, 64)])
+def test_bucket_bitexact(sess, M, k, E):
+    idx = _random_idx(81, M, k, E)
+    outs = sess.moe_bucket(_dev(idx), E)
+    sess.sync()
+    for got, ref in zip(outs, oracle.bucket(idx, E)):
+        assert np.array_equal(got.cpu().numpy(), ref)
+
+
+def test_bucket_special_cases(sess):
+    # every token picks expert 5 first; experts 1..4 stay empty
+    M, k, E = 200, 4, 32
+    idx = np.tile(np.array([[5, 0, 9, 31]], np.int32), (M, 1))
+    outs = sess.moe_bucket(_dev(idx), E)
+    sess.sync()
+    for got, ref in zip(outs, oracle.bucket(idx, E)):
+        assert np.array_equal(got.cpu().numpy(), ref)
+
+
+def _logit_bound(zeta_ref, H):
+    """Worst-case error of an fp32 sum of H exact fp16 products (any order),
+    plus the bias add: (H + 64) * 2^-24 * sum |terms|."""
+    return (H + 64) * 2.0 ** -24 * zeta_ref.max(axis=1)
+
+
+def _route_decided(logits_ref, bound, k):
+    """Tokens whose top-k set (and full order) the fp32 GPU logits cannot flip:
+    consecutive gaps of the sorted oracle logits exceed twice the error bound."""
+    srt = -np.sort(-logits_ref, axis=1)
+    gaps = srt[:, :-1] - srt[:, 1:]
+    boundary = gaps[:, k - 1] > 2 * bound
+    order = np.all(gaps[:, :k] > 2 * bound[:, None], axis=1)
+    return boundary, order
+
+
+def _experts(seed, E, H, I):
+    return [((synth.int4_codes(seed, 10 * e + 1, I, H), synth.group_scales(seed, 10 * e + 1, I, H)),
+             (synth.int4_codes(seed, 10 * e + 2, I, H), synth.group_scales(seed, 10 * e + 2, I, H)),
+             (synth.int4_codes(seed, 10 * e + 3, H, I), synth.group_scales(seed, 10 * e + 3, H, I)))
+            for e in range(E)]
+
+
+class _Setup:
+    def __init__(self, sess, seed, E, H, I, k, host=False):
+        import torch
+        self.E, self.H, self.I, self.k = E, H, I, k
+        self.experts = _experts(seed, E, H, I)
+        self.wr = synth.router_weights(seed, 2, H, E)
+        # a seeded skew so some experts draw many tokens and some none
+        self.bias = (np.linspace(1.5, -1.5, E)[synth.permutation(seed, 3, E)]).astype(np.float32)
+        self.tids = [[sess.register(*self.experts[e][j], hbm=True, host=host) for e in range(E)] for j in range(3)]
+        self.layer = sess.moe_layer(_dev(self.wr), *self.tids, top_k=k, router_bias=torch.from_numpy(self.bias).cuda())
+
+
+def _check_moe(y, dbg, st, xn, name):
+    ref, zeta, aux = oracle.moe_ffn(xn, st.wr, st.bias.astype(np.float64), st.experts, st.k)
+    lg = dbg["logits"].cpu().numpy().astype(np.float64)
+    check(lg, aux["logits"], aux["logit_zeta"], name=f"{name} logits")
+    bound = _logit_bound(aux["logit_zeta"], st.H)
+    boundary, order = _route_decided(aux["logits"], bound, st.k)
+    n = len(boundary)
+    assert boundary.sum() >= min(n - 1, 0.75 * n), f"{name}: too many near-tied routing decisions"
+    idx = dbg["idx"].cpu().numpy()
+    # every selection is a valid top-k of the oracle logits within the bound
+    kth = -np.sort(-aux["logits"], axis=1)[:, st.k - 1]
+    chosen = np.take_along_axis(aux["logits"], idx.astype(np.int64), axis=1)
+    assert np.all(chosen >= (kth - 2 * bound)[:, None]), f"{name}: a selection is not a valid top-k"
+    p = dbg["p"].cpu().numpy().astype(np.float64)
+    for t in range(xn.shape[0]):
+        if order[t]:
+            assert list(idx[t]) == list(aux["idx"][t]), f"{name}: token {t} routed differently"
+        elif boundary[t]:
+            assert set(idx[t]) == set(aux["idx"][t])
+    assert np.all(np.abs(p.sum(axis=1) - 1) <= 1e-6)
+    pz = oracle.softmax_weight_zeta(aux["p"], np.take_along_axis(aux["logit_zeta"], aux["idx"].astype(np.int64), 1))
+    sel = order
+    check(p[sel], aux["p"][sel], pz[sel], name=f"{name} weights")
+    check(y.cpu().numpy()[boundary], ref[boundary], zeta[boundary], name=f"{name} output")
+    # bucketing of the GPU's own routing is exactly the oracle's bucketing of it
+    for key, refv in zip(("counts", "offsets", "perm", "inv_perm"), oracle.bucket(idx, st.E)):
+        assert np.array_equal(dbg[key].cpu().numpy(), refv), f"{name}: {key}"
+
+
+@pytest.mark.parametrize("M", [1, 3, 50])
+def test_moe_small_parity(sess, M):
+    st = _Setup(sess, 82, E=16, H=256, I=96, k=4)
+    xn = synth.activations(82, 100 + M, M, st.H)
+    y, dbg = st.layer(_dev(xn), debug=True)
+    sess.sync()
+    _check_moe(y, dbg, st, xn, f"moe small M={M}")
+
+
+@pytest.fixture(scope="module")
+def cfg4(sess):
+    shp = configs.MOE_LAYER.moe
+    return _Setup(sess, configs.MOE_LAYER.seed, E=shp.n_experts, H=shp.hidden, I=shp.inter, k=shp.top_k, host=True)
+
+
+@pytest.mark.parametrize("M", [1, 4, 512])
+def test_moe_layer_parity(sess, cfg4, M):
+    xn = synth.activations(configs.MOE_LAYER.seed, 200 + M, M, cfg4.H)
+    y, dbg = cfg4.layer(_dev(xn), debug=True)
+    sess.sync()
+    _check_moe(y, dbg, cfg4, xn, f"moe_layer M={M}")
+
+
+@pytest.mark.parametrize("M", [1, 512])
+def test_moe_placement_invariance(sess, cfg4, M):
+    """HBM-resident experts, the seeded 40 % host mask and all experts on host
+    give bit-identical outputs."""
+    import torch
+    xn = synth.activations(configs.MOE_LAYER.seed, 300 + M, M, cfg4.H)
+    x = _dev(xn)
+    all_ids = [t for ids in cfg4.tids for t in ids]
+    host_exp = configs.moe_host_experts()
+    outs = []
+    for mode in ("hbm", "mask", "host", "hbm"):
+        mask = list(sess.placement)
+        for j in range(3):
+            for e in range(cfg4.E):
+                mask[cfg4.tids[j][e]] = {"hbm": 0, "host": 1, "mask": int(host_exp[e])}[mode]
+        sess.set_placement(mask)
+        outs.append(cfg4.layer(x))
+    sess.sync()
+    mask = list(sess.placement)
+    for t in all_ids:
+        mask[t] = 0
+    sess.set_placement(mask)
+    for o in outs[1:]:
+        assert torch.equal(outs[0], o)
