@@ -1,22 +1,26 @@
 #!/usr/bin/env python3
 """Benchmark of the block-int4 quantised-linear hot path on one MI355X.
 
-Workload: one 8B-shaped dense decoder layer (hidden 4096, 32 query / 8 KV heads
-of 128, SwiGLU 14336; seven int4 g32 tensors, 122.7 MB), synthetic weights
-and activations from the seeded generator.
+Headline workload: one 8B-shaped dense decoder layer (hidden 4096, 32 query /
+8 KV heads of 128, SwiGLU 14336; seven int4 g32 tensors, 122.7 MB), seeded
+synthetic weights and activations.
 
-  value            decode weight GB/s: layer bytes / decode-step time, batch 1,
-                   all tensors HBM-resident (inputs resident before timing),
-                   rotating over copies of the layer so the 256 MB MALL cannot
-                   serve the weights; steps are replayed from a HIP graph.
-  prefill          tokens/s of a 512-token prefill pass over the same layer.
-  streamed         the same decode step with the seeded placement mask (three
-                   of the seven tensors read from pinned host memory through
-                   the streaming engine), PCIe-inclusive.
-  roofline         dominant decode kernel (the 4096 x 14336 GEMV) against
-                   8 TB/s; roofline_prefill: the 512 x 4096 x 14336 GEMM
-                   against 2.5 PFLOP/s fp16 MFMA.
-  cpu_baseline     the fp64 oracle on the host cores, on a bounded sample.
+  value             decode weight GB/s = layer bytes / decode-step time for a
+                    batch-1 pass of the whole layer (4 fused launches), all
+                    tensors HBM-resident before timing, replayed from a HIP
+                    graph over rotating copies of the layer (so the 256 MB
+                    MALL cannot serve the weights).
+  prefill           tokens/s of a 512-token pass of the same layer.
+  streamed          decode and prefill with the seeded placement mask (3 of 7
+                    tensors in pinned host memory, copied on the transfer
+                    stream); PCIe-inclusive, never the headline value.
+  moe               30B-A3B-shaped MoE layer (128 experts, top-8, capped-Zipf
+                    routing): decode and 512-token prefill, all-HBM and with
+                    51 experts on host.
+  roofline          dominant decode kernel (GEMV over the 4096 x 14336 gate
+                    tensor) against 8 TB/s; roofline_prefill: the 512 x 4096 x
+                    14336 GEMM against 2.5 PFLOP/s fp16 MFMA.
+  cpu_baseline      the fp64 oracle's decode step on the host cores.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
 """
@@ -42,13 +46,46 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
+class Timer:
+    """HIP-event timing on the compute stream the library launches on."""
+
+    def __init__(self, stream):
+        import torch
+        self.s = stream
+        self.a = torch.cuda.Event(enable_timing=True)
+        self.b = torch.cuda.Event(enable_timing=True)
+
+    def run(self, fn, n: int) -> float:
+        """Seconds per call of fn over n calls."""
+        import torch
+        torch.cuda.synchronize()
+        with torch.cuda.stream(self.s):
+            self.a.record(self.s)
+            for _ in range(n):
+                fn()
+            self.b.record(self.s)
+        torch.cuda.synchronize()
+        return self.a.elapsed_time(self.b) * 1e-3 / n
+
+
+def graph_of(stream, fn):
+    import torch
+    fn()  # warm (allocations, table writes) outside capture
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=stream, capture_error_mode="relaxed"):
+        fn()
+    return g
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--copies", type=int, default=5, help="layer copies rotated to defeat the MALL")
+    ap.add_argument("--copies", type=int, default=5, help="dense-layer copies rotated to defeat the MALL")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-moe", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     args = ap.parse_args()
     if args.gpus != 1:
@@ -60,6 +97,7 @@ def main() -> int:
 
     import synth
     from synth import configs
+    from paper_2607_10183_amd import atsi
     from paper_2607_10183_amd.session import Session
 
     wl = configs.DENSE_LAYER
@@ -67,143 +105,108 @@ def main() -> int:
     roles = configs.ROLES
     dev = torch.device("cuda", 0)
     R = args.copies
+    sess = Session(workspace_bytes=2 << 30, n_slots=16)
+    cs = sess.cs
+    timer = Timer(cs)
 
-    log("generating weights")
-    host_np = {}
+    # ------------------------------------------------------------ dense layer weights
+    log("generating dense-layer weights")
+    W = {}
     for r in roles:
         K, N = shape.kn(r)
         uid = configs.dense_uid(0, r)
-        host_np[r] = (synth.int4_codes(wl.seed, uid, N, K), synth.group_scales(wl.seed, uid, N, K))
+        W[r] = (synth.int4_codes(wl.seed, uid, N, K), synth.group_scales(wl.seed, uid, N, K))
     layer_bytes = shape.layer_bytes()
-
-    sess = Session(workspace_bytes=1 << 30, n_slots=4)
-    tids = []  # tids[copy][role]
-    for c in range(R):
-        row = {}
-        for r in roles:
-            codes, scales = host_np[r]
-            row[r] = sess.register(codes, scales, hbm=True, host=(c == 0))
-        tids.append(row)
-    torch.cuda.synchronize()
-
-    H, I = shape.hidden, shape.inter
-    xs = {r: torch.from_numpy(synth.activations(wl.seed, 50 + i, 512, shape.kn(r)[0])).to(dev)
-          for i, r in enumerate(roles)}
-    ys = {r: torch.empty((512, shape.kn(r)[1]), dtype=torch.float16, device=dev) for r in roles}
-    from paper_2607_10183_amd import atsi
-
-    def step(copy: int, M: int) -> None:
-        for r in roles:
-            atsi.atsi_linear(sess.ctx, tids[copy][r], xs[r].data_ptr(), M, ys[r].data_ptr())
-
-    cs = sess.cs
+    tids = [{r: sess.register(*W[r], hbm=True, host=(c == 0)) for r in roles} for c in range(R)]
+    descs = [atsi.atsi_dense_layer(shape.n_heads, shape.n_kv, shape.head_dim, 1e-6,
+                                   *[t[r] for r in ("q", "k", "v", "o", "gate", "up", "down")]) for t in tids]
+    Mp = wl.prefill_m
+    h1 = torch.from_numpy(synth.activations(wl.seed, 1, 1, shape.hidden)).to(dev)
+    hp = torch.from_numpy(synth.activations(wl.seed, 2, Mp, shape.hidden)).to(dev)
     cs.wait_stream(torch.cuda.current_stream())
 
-    # ------------------------------------------------------------ decode, HBM-resident, graph
-    log("decode: capturing graph")
+    def layer(c, h, M):
+        atsi.atsi_decoder_layer(sess.ctx, descs[c], h.data_ptr(), M, 0, 0)
+
+    # ------------------------------------------------------------ decode, HBM-resident (value)
     reps = 4
-    g = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(g, stream=cs, capture_error_mode="relaxed"):
+
+    def decode_round():
         for _ in range(reps):
             for c in range(R):
-                step(c, 1)
-    steps_per_replay = reps * R
-    n_replay = max(1, args.steps // steps_per_replay)
-    n_warm = max(1, args.warmup // steps_per_replay)
-    with torch.cuda.stream(cs):
-        for _ in range(n_warm):
-            g.replay()
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    with torch.cuda.stream(cs):
-        e0.record(cs)
-        for _ in range(n_replay):
-            g.replay()
-        e1.record(cs)
-    torch.cuda.synchronize()
-    steps_timed = n_replay * steps_per_replay
-    decode_ms = e0.elapsed_time(e1) / steps_timed
-    decode_gbs = layer_bytes / (decode_ms * 1e-3) / 1e9
-    log(f"decode step {decode_ms * 1e3:.2f} us  -> {decode_gbs:.1f} GB/s over {steps_timed} steps")
+                layer(c, h1, 1)
 
-    # ------------------------------------------------------------ dominant decode kernel
-    def time_kernel(role: str, M: int, launches_per_copy: int, n_outer: int):
-        gk = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(gk, stream=cs, capture_error_mode="relaxed"):
-            for _ in range(launches_per_copy):
-                for c in range(R):
-                    atsi.atsi_linear(sess.ctx, tids[c][role], xs[role].data_ptr(), M, ys[role].data_ptr())
-        with torch.cuda.stream(cs):
-            gk.replay()
-        torch.cuda.synchronize()
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        with torch.cuda.stream(cs):
-            a.record(cs)
-            for _ in range(n_outer):
-                gk.replay()
-            b.record(cs)
-        torch.cuda.synchronize()
-        return a.elapsed_time(b) * 1e-3 / (n_outer * launches_per_copy * R)
+    g = graph_of(cs, decode_round)
+    per_replay = reps * R
+    n_replay = max(1, args.steps // per_replay)
+    n_warm = max(1, args.warmup // per_replay)
+    timer.run(g.replay, n_warm)
+    decode_s = timer.run(g.replay, n_replay) / per_replay
+    steps_timed = n_replay * per_replay
+    decode_gbs = layer_bytes / decode_s / 1e9
+    log(f"decode layer {decode_s * 1e6:.2f} us -> {decode_gbs:.1f} GB/s ({steps_timed} steps)")
 
+    # ------------------------------------------------------------ dominant kernels
+    xs = {r: torch.from_numpy(synth.activations(wl.seed, 50 + i, Mp, shape.kn(r)[0])).to(dev)
+          for i, r in enumerate(roles)}
+    yg = torch.empty((Mp, shape.inter), dtype=torch.float16, device=dev)
+    cs.wait_stream(torch.cuda.current_stream())
     K_g, N_g = shape.kn("gate")
+
+    def gate_round(M, n):
+        def f():
+            for _ in range(n):
+                for c in range(R):
+                    atsi.atsi_linear(sess.ctx, tids[c]["gate"], xs["gate"].data_ptr(), M, yg.data_ptr())
+        return f
+
+    gk = graph_of(cs, gate_round(1, 8))
+    t_gemv = timer.run(gk.replay, 10) / (8 * R)
     gemv_bytes = configs.qbytes(K_g, N_g)
-    t_gemv = time_kernel("gate", 1, 8, 10)
     gemv_gbs = gemv_bytes / t_gemv / 1e9
     log(f"gate GEMV {t_gemv * 1e6:.2f} us -> {gemv_gbs:.1f} GB/s")
-
-    # ------------------------------------------------------------ prefill 512
-    Mp = wl.prefill_m
-    with torch.cuda.stream(cs):
-        step(0, Mp)
-    torch.cuda.synchronize()
-    n_pf = max(2, min(20, args.steps // 10))
-    with torch.cuda.stream(cs):
-        e0.record(cs)
-        for i in range(n_pf):
-            step(i % R, Mp)
-        e1.record(cs)
-    torch.cuda.synchronize()
-    prefill_ms = e0.elapsed_time(e1) / n_pf
-    prefill_tps = Mp / (prefill_ms * 1e-3)
-    prefill_flops = sum(2.0 * Mp * shape.kn(r)[0] * shape.kn(r)[1] for r in roles)
-    log(f"prefill step {prefill_ms:.3f} ms -> {prefill_tps:.0f} tok/s, "
-        f"{prefill_flops / (prefill_ms * 1e-3) / 1e12:.1f} TFLOP/s")
-    t_gemm = time_kernel("gate", Mp, 1, 4)
+    gm = graph_of(cs, gate_round(Mp, 1))
+    t_gemm = timer.run(gm.replay, 4) / R
     gemm_flops = 2.0 * Mp * K_g * N_g
     gemm_tfs = gemm_flops / t_gemm / 1e12
     log(f"gate GEMM {t_gemm * 1e6:.1f} us -> {gemm_tfs:.1f} TFLOP/s")
 
-    # ------------------------------------------------------------ streamed decode (placement mask)
-    mask_roles = configs.dense_layer_host_mask()
-    host_roles = [r for r, m in zip(roles, mask_roles) if m]
-    full_mask = [0] * len(sess.shapes)
-    for r in host_roles:
-        full_mask[tids[0][r]] = 1
-    sess.set_placement(full_mask)
-    host_bytes = sum(configs.qbytes(*shape.kn(r)) for r in host_roles)
-    with torch.cuda.stream(cs):
-        for _ in range(3):
-            step(0, 1)
-    torch.cuda.synchronize()
-    n_st = max(5, min(50, args.steps // 4))
-    t0 = time.perf_counter()
-    with torch.cuda.stream(cs):
-        e0.record(cs)
-        for _ in range(n_st):
-            step(0, 1)
-        e1.record(cs)
-    sess.sync()
-    torch.cuda.synchronize()
-    streamed_ms = e0.elapsed_time(e1) / n_st
-    wall_streamed = (time.perf_counter() - t0) / n_st
-    sess.set_placement([0] * len(sess.shapes))
-    log(f"streamed decode step {streamed_ms:.3f} ms ({host_roles} on host, {host_bytes / 1e6:.1f} MB) -> "
-        f"PCIe {host_bytes / (streamed_ms * 1e-3) / 1e9:.1f} GB/s")
+    # ------------------------------------------------------------ prefill 512, HBM-resident
+    pf_state = {"i": 0}
 
-    # ------------------------------------------------------------ CPU baseline (the oracle)
+    def prefill_once():
+        layer(pf_state["i"] % R, hp, Mp)
+        pf_state["i"] += 1
+
+    timer.run(prefill_once, 2)
+    prefill_s = timer.run(prefill_once, max(4, min(20, args.steps // 10)))
+    prefill_flops = sum(2.0 * Mp * shape.kn(r)[0] * shape.kn(r)[1] for r in roles)
+    prefill_tps = Mp / prefill_s
+    log(f"prefill layer {prefill_s * 1e3:.3f} ms -> {prefill_tps:.0f} tok/s, "
+        f"{prefill_flops / prefill_s / 1e12:.1f} TFLOP/s")
+
+    # ------------------------------------------------------------ streamed placement (PCIe-inclusive)
+    host_roles = [r for r, m in zip(roles, configs.dense_layer_host_mask()) if m]
+    mask = [0] * len(sess.shapes)
+    for r in host_roles:
+        mask[tids[0][r]] = 1
+    sess.set_placement(mask)
+    sess.set_schedule([tids[0][r] for r in ("q", "k", "v", "o", "gate", "up", "down")])
+    host_bytes = sum(configs.qbytes(*shape.kn(r)) for r in host_roles)
+    timer.run(lambda: layer(0, h1, 1), 3)
+    st_dec = timer.run(lambda: layer(0, h1, 1), max(5, min(40, args.steps // 5)))
+    timer.run(lambda: layer(0, hp, Mp), 1)
+    st_pf = timer.run(lambda: layer(0, hp, Mp), 5)
+    sess.set_schedule([])
+    sess.set_placement([0] * len(sess.shapes))
+    log(f"streamed decode {st_dec * 1e3:.3f} ms, prefill {st_pf * 1e3:.3f} ms ({host_roles} on host, "
+        f"{host_bytes / 1e6:.1f} MB) -> PCIe {host_bytes / st_dec / 1e9:.1f} GB/s")
+
+    moe = None if args.no_moe else bench_moe(sess, timer, args)
+
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(host_np, shape, roles, args.cpu_seconds, layer_bytes)
+        cpu = cpu_baseline(W, shape, args.cpu_seconds, layer_bytes)
         log(f"cpu baseline {cpu}")
 
     out = {
@@ -212,36 +215,39 @@ def main() -> int:
         "unit": "GB/s",
         "n_gpus": 1,
         "steps": steps_timed,
-        "warmup": n_warm * steps_per_replay,
-        "ms_per_step": round(decode_ms, 6),
+        "warmup": n_warm * per_replay,
+        "ms_per_step": round(decode_s * 1e3, 6),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "f16",
         "data": "synthetic",
         "config": {
-            "workload": "dense_layer: one 8B-shaped decoder layer's seven block-int4 g32 projections "
-                        "(Q 4096x4096, K/V 4096x1024, O 4096x4096, gate/up 4096x14336, down 14336x4096)",
+            "workload": "dense_layer: one 8B-shaped decoder layer, block-int4 g32 weights (Q 4096x4096, "
+                        "K/V 4096x1024, O 4096x4096, gate/up 4096x14336, down 14336x4096; 122.7 MB), "
+                        "RMS-norm, context-length-1 GQA, SwiGLU, residuals",
             "decode_batch": 1, "prefill_tokens": Mp, "layer_bytes": layer_bytes,
-            "placement": "all HBM-resident for value; seeded mask with 3 host tensors for 'streamed'",
+            "placement": "all HBM-resident for value; seeded mask (3 of 7 tensors on host) under 'streamed'",
             "mall_rotation_copies": R,
         },
         "pct_hbm_peak": round(100 * decode_gbs / HBM_PEAK_GBS, 2),
         "prefill_tokens_per_s": round(prefill_tps, 1),
-        "prefill_ms_per_step": round(prefill_ms, 4),
-        "prefill_pct_mfma": round(100 * prefill_flops / (prefill_ms * 1e-3) / 1e12 / MFMA_F16_PEAK_TFLOPS, 2),
+        "prefill_ms_per_step": round(prefill_s * 1e3, 4),
+        "prefill_pct_mfma": round(100 * prefill_flops / prefill_s / 1e12 / MFMA_F16_PEAK_TFLOPS, 2),
         "roofline": {"bound": "hbm", "achieved": round(gemv_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(gemv_gbs / HBM_PEAK_GBS, 4), "traffic": None,
-                     "kernel": "q4_gemv_kernel<1,4> on the 4096x14336 gate tensor, batch 1",
+                     "kernel": "q4_gemv_kernel<1,4,false>: 4096x14336 gate tensor, batch 1",
                      "bytes_per_launch": gemv_bytes, "avg_us": round(t_gemv * 1e6, 3)},
         "roofline_prefill": {"bound": "mfma", "achieved": round(gemm_tfs, 1), "peak": MFMA_F16_PEAK_TFLOPS,
                              "unit": "TFLOP/s", "frac": round(gemm_tfs / MFMA_F16_PEAK_TFLOPS, 4), "traffic": None,
-                             "kernel": "q4_gemm_kernel<128,128> on the 4096x14336 gate tensor, 512 tokens",
+                             "kernel": "q4_gemm_kernel<128,128,2,2,false>: 4096x14336 gate tensor, 512 tokens",
                              "flops_per_launch": gemm_flops, "avg_us": round(t_gemm * 1e6, 2)},
-        "streamed": {"host_tensors": host_roles, "host_bytes": host_bytes, "ms_per_step": round(streamed_ms, 4),
-                     "weight_GBps_pcie_inclusive": round(layer_bytes / (streamed_ms * 1e-3) / 1e9, 2),
-                     "pcie_GBps": round(host_bytes / (streamed_ms * 1e-3) / 1e9, 2),
-                     "host_wall_ms_per_step": round(wall_streamed * 1e3, 4)},
+        "streamed": {"host_tensors": host_roles, "host_bytes": host_bytes,
+                     "decode_ms": round(st_dec * 1e3, 4), "prefill_ms": round(st_pf * 1e3, 4),
+                     "decode_weight_GBps_pcie_inclusive": round(layer_bytes / st_dec / 1e9, 2),
+                     "decode_pcie_GBps": round(host_bytes / st_dec / 1e9, 2),
+                     "prefill_tokens_per_s": round(Mp / st_pf, 1)},
+        "moe": moe,
         "cpu_baseline": cpu,
     }
     sess.close()
@@ -249,28 +255,104 @@ def main() -> int:
     return 0
 
 
-def cpu_baseline(host_np, shape, roles, budget_s, layer_bytes):
-    """Time the fp64 oracle on the same decode step (7 tensors, batch 1)."""
+def bench_moe(sess, timer, args):
+    """30B-A3B-shaped MoE layer: decode (batch 1) and 512-token prefill."""
+    import torch
+
+    import synth
+    from synth import configs
+    from synth.calibrate_router_bias import load_bias
+    from paper_2607_10183_amd import atsi
+
+    wl = configs.MOE_LAYER
+    shp = wl.moe
+    E, H, I, k = shp.n_experts, shp.hidden, shp.inter, shp.top_k
+    dev = torch.device("cuda", 0)
+    log("generating MoE weights")
+    tids = [[], [], []]
+    for e in range(E):
+        for j, (n, kk) in enumerate(((I, H), (I, H), (H, I))):
+            uid = configs.expert_uid(0, e, ("gate", "up", "down")[j])
+            tids[j].append(sess.register(synth.int4_codes(wl.seed, uid, n, kk), synth.group_scales(wl.seed, uid, n, kk),
+                                         hbm=True, host=True))
+    wr = torch.from_numpy(synth.router_weights(wl.seed, configs.router_uid(0), H, E)).to(dev)
+    bias = torch.from_numpy(load_bias()).to(dev)
+    moe_l = sess.moe_layer(wr, *tids, top_k=k, router_bias=bias)
+
+    def layer(x, y):
+        atsi.atsi_moe_ffn(sess.ctx, moe_l.desc, x.data_ptr(), x.shape[0], y.data_ptr(), None)
+
+    n_tok = 64
+    xd = torch.from_numpy(synth.activations(wl.seed, 7, n_tok, H)).to(dev)
+    xp = torch.from_numpy(synth.activations(wl.seed, 8, wl.prefill_m, H)).to(dev)
+    yd = torch.empty((n_tok, H), dtype=torch.float16, device=dev)
+    yp = torch.empty((wl.prefill_m, H), dtype=torch.float16, device=dev)
+    sess.cs.wait_stream(torch.cuda.current_stream())
+    expert_bytes = shp.expert_bytes()
+
+    def decode_all():  # 64 different tokens, one at a time
+        for t in range(n_tok):
+            layer(xd[t:t + 1], yd[t:t + 1])
+
+    # routed bytes actually touched per decode token (8 distinct experts)
+    routed_bytes = k * expert_bytes
+    g = graph_of(sess.cs, decode_all)
+    timer.run(g.replay, 2)
+    dec_s = timer.run(g.replay, 5) / n_tok
+    timer.run(lambda: layer(xp, yp), 2)
+    pf_s = timer.run(lambda: layer(xp, yp), 10)
+    pf_flops = 2.0 * wl.prefill_m * k * 3 * H * I
+    log(f"moe decode {dec_s * 1e6:.1f} us/token ({routed_bytes / dec_s / 1e9:.0f} GB/s routed), "
+        f"prefill {pf_s * 1e3:.3f} ms -> {wl.prefill_m / pf_s:.0f} tok/s, {pf_flops / pf_s / 1e12:.1f} TFLOP/s")
+
+    host_exp = configs.moe_host_experts()
+    mask = list(sess.placement)
+    for j in range(3):
+        for e in range(E):
+            mask[tids[j][e]] = int(host_exp[e])
+    sess.set_placement(mask)
+    layer(xd[0:1], yd[0:1])
+    st_dec = timer.run(lambda: [layer(xd[t:t + 1], yd[t:t + 1]) for t in range(16)], 2) / 16
+    layer(xp, yp)
+    st_pf = timer.run(lambda: layer(xp, yp), 3)
+    for j in range(3):
+        for e in range(E):
+            mask[tids[j][e]] = 0
+    sess.set_placement(mask)
+    host_bytes_pf = int(host_exp.sum()) * expert_bytes
+    log(f"moe streamed decode {st_dec * 1e3:.3f} ms/token, prefill {st_pf * 1e3:.2f} ms "
+        f"({host_bytes_pf / st_pf / 1e9:.1f} GB/s PCIe if all 51 host experts are active)")
+    return {"workload": "moe_layer: 128 experts of SwiGLU 768 over hidden 2048, top-8, capped Zipf(1.1) loads",
+            "decode_us_per_token": round(dec_s * 1e6, 2),
+            "decode_routed_GBps": round(routed_bytes / dec_s / 1e9, 1),
+            "prefill_tokens_per_s": round(wl.prefill_m / pf_s, 1),
+            "prefill_ms": round(pf_s * 1e3, 4),
+            "prefill_TFLOPs": round(pf_flops / pf_s / 1e12, 2),
+            "streamed_40pct_host": {"decode_ms_per_token": round(st_dec * 1e3, 4),
+                                    "prefill_ms": round(st_pf * 1e3, 3),
+                                    "prefill_pcie_GBps_if_all_active": round(host_bytes_pf / st_pf / 1e9, 2)}}
+
+
+def cpu_baseline(W, shape, budget_s, layer_bytes):
+    """The fp64 oracle's decode step of the same layer (batch 1), timed on the host."""
     import oracle
     import synth
     try:
         from threadpoolctl import threadpool_info
-        blas_threads = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] or [1])
+        blas = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] or [1])
     except Exception:  # pragma: no cover
-        blas_threads = 1
-    x = {r: synth.activations(1002, 90 + i, 1, shape.kn(r)[0]) for i, r in enumerate(roles)}
+        blas = 1
+    h = synth.activations(1002, 1, 1, shape.hidden)
     n = 0
     t0 = time.perf_counter()
     while True:
-        for r in roles:
-            oracle.linear(x[r], *host_np[r])
+        oracle.decoder_layer(h, W, shape.n_heads, shape.n_kv, shape.head_dim, 1e-6)
         n += 1
         if time.perf_counter() - t0 >= budget_s:
             break
     dt = (time.perf_counter() - t0) / n
-    return {"value": round(layer_bytes / dt / 1e9, 4), "unit": "GB/s", "cores": int(blas_threads),
-            "kind": "oracle",
-            "sample": f"{n} decode steps of the dense layer (7 tensors, batch 1, fp64 dequant + matmul), "
+    return {"value": round(layer_bytes / dt / 1e9, 4), "unit": "GB/s", "cores": int(blas), "kind": "oracle",
+            "sample": f"{n} batch-1 decode steps of the dense layer (fp64 dequant + BLAS matmul), "
                       f"{dt:.2f} s per step",
             "host_cpus": len(os.sched_getaffinity(0))}
 

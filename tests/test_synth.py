@@ -47,3 +47,20 @@ def test_placement_recipes():
     m4 = configs.moe_host_experts()
     assert m4.sum() == 51
     assert shape.layer_bytes() == 122_683_392
+
+
+def test_router_bias_reproduces_capped_zipf_out_of_sample():
+    """The fitted bias gives the capped Zipf(1.1) expert loads on fresh logits
+    (within 15 % per expert at 65,536 tokens)."""
+    from synth.calibrate_router_bias import capped_zipf, load_bias
+    import json, os
+    b = load_bias().astype(np.float64)
+    d = json.load(open(os.path.join(os.path.dirname(synth.__file__), "router_bias_e128_k8.json")))
+    rank = np.array(d["rank"])
+    target = capped_zipf(128, 8)[rank]
+    assert abs(target.sum() - 8) < 1e-9 and target.max() == 1.0
+    T = 65536
+    z = synth.normal(synth.stream_key(777, 1, 7), T * 128).reshape(T, 128)
+    sel = np.argpartition(-(z + b), 7, axis=1)[:, :8]
+    frac = np.bincount(sel.ravel(), minlength=128) / T
+    assert np.all(np.abs(frac - target) <= 0.15 * target)
