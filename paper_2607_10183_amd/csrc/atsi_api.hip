@@ -40,13 +40,23 @@ struct Tensor {
   bool on_host = false;
   size_t codes_bytes() const { return (size_t)(K / 2) * (size_t)N; }
   size_t scales_bytes() const { return (size_t)(K / kGroup) * (size_t)N * 2; }
-  size_t slot_need() const { return align_up(codes_bytes()) + align_up(scales_bytes()); }
+  size_t bytes() const { return codes_bytes() + scales_bytes(); }
+  // a slot holds the codes followed directly by the scales (16-byte aligned:
+  // K/2 * N is a multiple of 16), the same layout as a contiguous host copy
+  size_t slot_need() const { return align_up(bytes()); }
+  bool host_contiguous() const { return hcodes && hcodes + codes_bytes() == reinterpret_cast<const uint8_t*>(hscales); }
 };
 
+// Each slot owns two events; slots filled by one copy share its ready event
+// and slots released by one launch share its free event.  Both streams run in
+// order, so waiting on a later recording of a shared event only waits longer,
+// never too little.
 struct Slot {
   char* base = nullptr;
-  hipEvent_t ready = nullptr;
-  hipEvent_t free = nullptr;
+  hipEvent_t ready = nullptr;      // owned
+  hipEvent_t free = nullptr;       // owned
+  hipEvent_t ready_ev = nullptr;   // event marking this slot's copy done
+  hipEvent_t free_ev = nullptr;    // event marking this slot's last consumer done
   bool free_recorded = false;
   int tid = -1;         // tensor whose copy the slot holds or receives
   bool armed = false;   // copy issued ahead of its consumer, not yet consumed
@@ -161,11 +171,30 @@ atsi_status layout_slots(atsi_ctx* c) {
   return ATSI_OK;
 }
 
-// Issue the H2D copy of host tensor `tid` into a reusable slot; returns its
-// index.  Slots in `pinned` (held by the launch being assembled) are never
-// taken.  When every other slot holds a prefetched copy, the copy furthest in
-// the future is dropped and its tensor queued again.
-atsi_status issue_copy(atsi_ctx* c, atsi_tid tid, int* slot_out, const std::vector<int>& pinned = {}) {
+// Copy host tensor t into slot s: one copy when its host codes and scales are
+// contiguous (small copies cost far more than their bytes), else two.
+atsi_status copy_into(atsi_ctx* c, const Tensor& t, Slot& s) {
+  if (s.free_recorded) HIP_TRY(c, hipStreamWaitEvent(c->ts, s.free_ev, 0));
+  if (t.host_contiguous()) {
+    HIP_TRY(c, hipMemcpyAsync(s.base, t.hcodes, t.bytes(), hipMemcpyHostToDevice, c->ts));
+  } else {
+    HIP_TRY(c, hipMemcpyAsync(s.base, t.hcodes, t.codes_bytes(), hipMemcpyHostToDevice, c->ts));
+    HIP_TRY(c, hipMemcpyAsync(s.base + t.codes_bytes(), t.hscales, t.scales_bytes(), hipMemcpyHostToDevice, c->ts));
+  }
+  return ATSI_OK;
+}
+
+void arm(atsi_ctx* c, Slot& s, atsi_tid tid) {
+  s.tid = tid;
+  s.armed = true;
+  s.seq = ++c->clock;
+  s.last = s.seq;
+}
+
+// Pick a reusable slot (never one in `pinned`).  When every other slot holds a
+// prefetched copy, the copy furthest in the future is dropped and its tensor
+// queued again.
+atsi_status pick_slot(atsi_ctx* c, const std::vector<int>& pinned, int* out) {
   auto is_pinned = [&](int i) { return std::find(pinned.begin(), pinned.end(), i) != pinned.end(); };
   int best = -1;
   for (int i = 0; i < c->n_slots; ++i) {
@@ -184,19 +213,72 @@ atsi_status issue_copy(atsi_ctx* c, atsi_tid tid, int* slot_out, const std::vect
     c->queue.push_front(c->slots[best].tid);
     c->slots[best].armed = false;
   }
+  *out = best;
+  return ATSI_OK;
+}
+
+// Issue the H2D copy of host tensor `tid` into a reusable slot; returns its index.
+atsi_status issue_copy(atsi_ctx* c, atsi_tid tid, int* slot_out, const std::vector<int>& pinned = {}) {
+  int best;
+  atsi_status st = pick_slot(c, pinned, &best);
+  if (st) return st;
   Slot& s = c->slots[best];
-  const Tensor& t = c->tensors[tid];
-  if (s.free_recorded) HIP_TRY(c, hipStreamWaitEvent(c->ts, s.free, 0));
-  HIP_TRY(c, hipMemcpyAsync(s.base, t.hcodes, t.codes_bytes(), hipMemcpyHostToDevice, c->ts));
-  HIP_TRY(c, hipMemcpyAsync(s.base + align_up(t.codes_bytes()), t.hscales, t.scales_bytes(),
-                            hipMemcpyHostToDevice, c->ts));
+  if ((st = copy_into(c, c->tensors[tid], s))) return st;
   HIP_TRY(c, hipEventRecord(s.ready, c->ts));
-  s.tid = tid;
-  s.armed = true;
-  s.seq = ++c->clock;
-  s.last = s.seq;
+  s.ready_ev = s.ready;
+  arm(c, s, tid);
   *slot_out = best;
   return ATSI_OK;
+}
+
+// Tensors registered back to back in one host buffer, each exactly one slot in
+// size, can move with a single copy into adjacent free slots (an expert's
+// gate, up and down, for instance).  Returns false when that is not possible.
+bool run_candidate(atsi_ctx* c, const atsi_tid* tids, int n) {
+  if (n < 2) return false;
+  for (int i = 0; i < n; ++i) {
+    const Tensor& t = c->tensors[tids[i]];
+    if (!t.on_host || !t.host_contiguous() || t.bytes() != c->slot_bytes) return false;
+    if (i && c->tensors[tids[i - 1]].hcodes + c->slot_bytes != t.hcodes) return false;
+  }
+  return true;
+}
+
+bool issue_run(atsi_ctx* c, const atsi_tid* tids, int n, const std::vector<int>& pinned, atsi_status* st) {
+  *st = ATSI_OK;
+  if (!run_candidate(c, tids, n)) return false;
+  // runs use slot-aligned groups (first slot a multiple of n) so they never
+  // fragment each other
+  int first = -1;
+  for (int j = 0; j + n <= c->n_slots && first < 0; j += n) {
+    bool ok = true;
+    for (int i = 0; i < n && ok; ++i) {
+      const Slot& s = c->slots[j + i];
+      ok = !s.armed && std::find(pinned.begin(), pinned.end(), j + i) == pinned.end();
+    }
+    if (ok) first = j;
+  }
+  if (first < 0) return false;
+  for (int i = 0; i < n; ++i) {
+    Slot& s = c->slots[first + i];
+    bool seen = false;
+    for (int j = 0; j < i; ++j) seen = seen || (c->slots[first + j].free_recorded && c->slots[first + j].free_ev == s.free_ev);
+    if (s.free_recorded && !seen) {
+      hipError_t e = hipStreamWaitEvent(c->ts, s.free_ev, 0);
+      if (e != hipSuccess) { *st = hip_fail(c, e, "hipStreamWaitEvent"); return true; }
+    }
+  }
+  hipError_t e = hipMemcpyAsync(c->slots[first].base, c->tensors[tids[0]].hcodes, (size_t)n * c->slot_bytes,
+                                hipMemcpyHostToDevice, c->ts);
+  if (e != hipSuccess) { *st = hip_fail(c, e, "hipMemcpyAsync"); return true; }
+  e = hipEventRecord(c->slots[first].ready, c->ts);
+  if (e != hipSuccess) { *st = hip_fail(c, e, "hipEventRecord"); return true; }
+  for (int i = 0; i < n; ++i) {
+    Slot& s = c->slots[first + i];
+    s.ready_ev = c->slots[first].ready;
+    arm(c, s, tids[i]);
+  }
+  return true;
 }
 
 // Keep the transfer stream ahead of compute: copy queued (or scheduled) host
@@ -212,6 +294,19 @@ atsi_status topup(atsi_ctx* c) {
       c->sched_pos++;
       if (c->tensors[t].on_host) c->queue.push_back(t);
       continue;
+    }
+    if (c->queue.size() >= 3) {
+      const atsi_tid run[3] = {c->queue[0], c->queue[1], c->queue[2]};
+      if (run_candidate(c, run, 3)) {
+        // an expert moves as one copy or waits for three aligned free slots
+        atsi_status st;
+        if (armed + 3 > c->n_slots - 1 || !issue_run(c, run, 3, {}, &st)) break;
+        if (st) return st;
+        c->queue.erase(c->queue.begin(), c->queue.begin() + 3);
+        armed += 3;
+        guard = 0;
+        continue;
+      }
     }
     atsi_tid t = c->queue.front();
     c->queue.pop_front();
@@ -265,21 +360,25 @@ atsi_status acquire(atsi_ctx* c, atsi_tid tid, QView* v, std::vector<int>& held)
     if (st) return st;
   }
   Slot& s = c->slots[si];
-  HIP_TRY(c, hipStreamWaitEvent(c->cs, s.ready, 0));
+  HIP_TRY(c, hipStreamWaitEvent(c->cs, s.ready_ev, 0));
   v->codes = reinterpret_cast<const uint8_t*>(s.base);
-  v->scales = reinterpret_cast<const uint16_t*>(s.base + align_up(t.codes_bytes()));
+  v->scales = reinterpret_cast<const uint16_t*>(s.base + t.codes_bytes());
   held.push_back(si);
   return ATSI_OK;
 }
 
 // After the consumer kernel of the held slots has been enqueued.
 atsi_status release(atsi_ctx* c, std::vector<int>& held) {
-  for (int si : held) {
-    Slot& s = c->slots[si];
-    HIP_TRY(c, hipEventRecord(s.free, c->cs));
-    s.free_recorded = true;
-    s.armed = false;
-    s.last = ++c->clock;
+  if (!held.empty()) {
+    hipEvent_t ev = c->slots[held[0]].free;
+    HIP_TRY(c, hipEventRecord(ev, c->cs));
+    for (int si : held) {
+      Slot& s = c->slots[si];
+      s.free_ev = ev;
+      s.free_recorded = true;
+      s.armed = false;
+      s.last = ++c->clock;
+    }
   }
   held.clear();
   return topup(c);
@@ -363,7 +462,7 @@ atsi_status run_op(atsi_ctx* c, LinOp& op, const atsi_tid* tids, int ntids) {
       op.seg[i].w = v;
     }
   }
-  const bool gemv = op.M <= 4;
+  const bool gemv = gemv_supported(op.M, op.K);
   hipError_t e = gemv ? launch_gemv(op, c->cs) : launch_gemm(op, c->cs);
   if (e != hipSuccess) return hip_fail(c, e, gemv ? "q4 gemv launch" : "q4 gemm launch");
   return release(c, held);

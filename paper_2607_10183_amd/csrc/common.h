@@ -47,6 +47,9 @@ struct LinOp {
 __device__ __forceinline__ float silu_f(float g) { return g / (1.f + expf(-g)); }
 
 // ---- launchers (each returns hipGetLastError() of its launch) ----
+constexpr size_t kGemvMaxLds = 64 * 1024;  // activations staged per GEMV workgroup
+// decode GEMV handles 1 <= M <= 4 when its staged activations fit in LDS
+bool gemv_supported(int M, int K);
 hipError_t launch_gemv(const LinOp& op, hipStream_t s);
 hipError_t launch_gemm(const LinOp& op, hipStream_t s);
 hipError_t launch_unpack(const QView& w, int8_t* q, hipStream_t s);

@@ -111,6 +111,8 @@ __global__ __launch_bounds__(kGemmBlock, 2) void expert_down_gemm(MoeArgs a, int
 template <int RW, bool DOWN>
 __global__ __launch_bounds__(gemv::kBlock) void expert_gemv(MoeArgs a, int tile_bound) {
   using namespace gemv;
+  constexpr int CH = 2;
+  constexpr int R2 = DOWN ? 1 : RW;
   const int tix = blockIdx.x % tile_bound, nb = blockIdx.x / tile_bound;
   int e, row0;
   ExpertW w;
@@ -127,39 +129,48 @@ __global__ __launch_bounds__(gemv::kBlock) void expert_gemv(MoeArgs a, int tile_
   if (n0 >= N) return;
   const int nchunk = K / kGroup;
   const size_t rbytes = (size_t)K / 2;
-  float acc[RW], acc2[RW], sq[1] = {0.f};
+  float acc[RW], acc2[R2], sq = 0.f;
 #pragma unroll
-  for (int r = 0; r < RW; ++r) acc[r] = acc2[r] = 0.f;
-  for (int c = lane; c < nchunk; c += kWave) {
-    uint4 cw[RW], cw2[RW];
-    float sc[RW], sc2[RW];
+  for (int r = 0; r < RW; ++r) acc[r] = 0.f;
 #pragma unroll
-    for (int r = 0; r < RW; ++r) {
-      const int row = min(n0 + r, N - 1);
-      cw[r] = *reinterpret_cast<const uint4*>(w1.codes + (size_t)row * rbytes + (size_t)c * 16);
-      sc[r] = __half2float(__ushort_as_half(w1.scales[(size_t)row * nchunk + c]));
-      if (!DOWN) {
-        cw2[r] = *reinterpret_cast<const uint4*>(w2.codes + (size_t)row * rbytes + (size_t)c * 16);
-        sc2[r] = __half2float(__ushort_as_half(w2.scales[(size_t)row * nchunk + c]));
+  for (int r = 0; r < R2; ++r) acc2[r] = 0.f;
+  for (int c0 = lane; c0 < nchunk; c0 += kWave * CH) {
+    uint4 cw[CH][RW], cw2[CH][R2];
+    uint16_t sc[CH][RW], sc2[CH][R2];
+    XRaw xv[CH];
+#pragma unroll
+    for (int h = 0; h < CH; ++h) {
+      const int c = c0 + h * kWave;
+      if (c >= nchunk) continue;
+#pragma unroll
+      for (int r = 0; r < RW; ++r) {
+        const int row = min(n0 + r, N - 1);
+        cw[h][r] = *reinterpret_cast<const uint4*>(w1.codes + (size_t)row * rbytes + (size_t)c * 16);
+        sc[h][r] = w1.scales[(size_t)row * nchunk + c];
+        if constexpr (!DOWN) {
+          cw2[h][r] = *reinterpret_cast<const uint4*>(w2.codes + (size_t)row * rbytes + (size_t)c * 16);
+          sc2[h][r] = w2.scales[(size_t)row * nchunk + c];
+        }
       }
+      load_xraw(xv[h], xr, c);
     }
-    XChunk<1> xc;
-    load_x<1>(xc, xr, K, 1, c, false, sq);
 #pragma unroll
-    for (int r = 0; r < RW; ++r) {
-      float part[1];
-      group_dot<1>(cw[r], xc, part);
-      acc[r] = fmaf(sc[r], part[0] - 1032.f * xc.sum[0], acc[r]);
-      if (!DOWN) {
-        group_dot<1>(cw2[r], xc, part);
-        acc2[r] = fmaf(sc2[r], part[0] - 1032.f * xc.sum[0], acc2[r]);
+    for (int h = 0; h < CH; ++h) {
+      if (c0 + h * kWave >= nchunk) break;
+      XGroup g;
+      prep_x(g, xv[h], false, sq);
+#pragma unroll
+      for (int r = 0; r < RW; ++r) {
+        acc[r] = fmaf(__half2float(__ushort_as_half(sc[h][r])), group_dot(cw[h][r], g), acc[r]);
+        if constexpr (!DOWN) acc2[r] = fmaf(__half2float(__ushort_as_half(sc2[h][r])), group_dot(cw2[h][r], g), acc2[r]);
       }
     }
   }
 #pragma unroll
   for (int r = 0; r < RW; ++r) {
     const float g = wave_sum(acc[r]);
-    const float u = DOWN ? 0.f : wave_sum(acc2[r]);
+    float u = 0.f;
+    if constexpr (!DOWN) u = wave_sum(acc2[r]);
     const int n = n0 + r;
     if (lane == r && n < N) {
       if (DOWN)
@@ -181,12 +192,22 @@ __global__ void combine_kernel(const __half* __restrict__ out, const float* __re
   for (size_t q = (size_t)blockIdx.x * blockDim.x + threadIdx.x; q < total; q += (size_t)gridDim.x * blockDim.x) {
     const int t = (int)(q / c8), c = (int)(q % c8);
     float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    for (int j = 0; j < k; ++j) {
-      const float pj = p[(size_t)t * k + j];
-      const uint4 v = *reinterpret_cast<const uint4*>(out + ((size_t)t * k + j) * H + (size_t)c * 8);
-      const __half* hv = reinterpret_cast<const __half*>(&v);
+    for (int j0 = 0; j0 < k; j0 += 8) {  // loads of 8 slots first, then the fixed-order sum
+      float pj[8];
+      uint4 v[8];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) acc[i] = fmaf(pj, __half2float(hv[i]), acc[i]);
+      for (int j = 0; j < 8; ++j)
+        if (j0 + j < k) {
+          pj[j] = p[(size_t)t * k + j0 + j];
+          v[j] = *reinterpret_cast<const uint4*>(out + ((size_t)t * k + j0 + j) * H + (size_t)c * 8);
+        }
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        if (j0 + j < k) {
+          const __half* hv = reinterpret_cast<const __half*>(&v[j]);
+#pragma unroll
+          for (int i = 0; i < 8; ++i) acc[i] = fmaf(pj[j], __half2float(hv[i]), acc[i]);
+        }
     }
     uint4 o;
     __half* ho = reinterpret_cast<__half*>(&o);

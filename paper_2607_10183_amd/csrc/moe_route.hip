@@ -107,6 +107,7 @@ __global__ __launch_bounds__(256) void router_topk_kernel(const float* __restric
     id[h] = e;
     if (e < E) {
       float s = 0.f;
+#pragma unroll 8
       for (int sp = 0; sp < n_split; ++sp) s += part[((size_t)sp * M + t) * E + e];
       if (bias) s += bias[e];
       v[h] = s;
@@ -146,6 +147,30 @@ __global__ __launch_bounds__(256) void router_topk_kernel(const float* __restric
 
 // Single workgroup of 1024 threads.  Up to 16 chunks of 64 tokens are ranked
 // per pass; masks live in LDS.
+// Exclusive prefix sum of v over experts 0..E-1 (E <= 128) by wave 0: lane l
+// owns experts 2l and 2l+1.  Returns the total; out[e] = sum_{f < e} v[f].
+__device__ int scan128(const int* v, int* out, int E) {
+  const int lane = threadIdx.x & 63;
+  int total = 0;
+  if (threadIdx.x < 64) {
+    const int a = (2 * lane < E) ? v[2 * lane] : 0;
+    const int b = (2 * lane + 1 < E) ? v[2 * lane + 1] : 0;
+    int incl = a + b;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int t = __shfl_up(incl, o, 64);
+      if (lane >= o) incl += t;
+    }
+    const int excl = incl - a - b;
+    if (2 * lane < E) out[2 * lane] = excl;
+    if (2 * lane + 1 < E) out[2 * lane + 1] = excl + a;
+    total = __shfl(incl, 63, 64);
+  }
+  return total;
+}
+
+// Single workgroup of 1024 threads.  Up to 16 chunks of 64 tokens are ranked
+// per pass; masks live in LDS.
 __global__ __launch_bounds__(1024) void bucket_kernel(const int32_t* __restrict__ idx, int M, int k, int E,
                                                       const uint8_t* __restrict__ resident, int bm_rows,
                                                       int32_t* __restrict__ counts, int32_t* __restrict__ offsets,
@@ -156,7 +181,9 @@ __global__ __launch_bounds__(1024) void bucket_kernel(const int32_t* __restrict_
   __shared__ int base[kMaxExperts];
   __shared__ unsigned long long mask[16][kMaxExperts];
   __shared__ int pre[16][kMaxExperts];
-  __shared__ int tstart[kMaxExperts + 1];
+  __shared__ int ord[kMaxExperts];
+  __shared__ int ntile[kMaxExperts];   // tiles of the expert at rank r
+  __shared__ int tstart[kMaxExperts];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int pairs = M * k;
   for (int e = tid; e < E; e += blockDim.x) cnt[e] = 0;
@@ -166,17 +193,13 @@ __global__ __launch_bounds__(1024) void bucket_kernel(const int32_t* __restrict_
     if ((unsigned)e < (unsigned)E) atomicAdd(&cnt[e], 1);
   }
   __syncthreads();
-  if (tid == 0) {
-    int run = 0;
-    for (int e = 0; e < E; ++e) {
-      offsets[e] = run;
-      base[e] = run;
-      counts[e] = cnt[e];
-      run += cnt[e];
-    }
-    offsets[E] = run;
-  }
+  const int total = scan128(cnt, base, E);
   __syncthreads();
+  for (int e = tid; e < E; e += blockDim.x) {
+    offsets[e] = base[e];
+    counts[e] = cnt[e];
+  }
+  if (tid == 0) offsets[E] = total;
   // stable scatter, 16 chunks of 64 tokens per pass
   for (int c0 = 0; c0 * 64 < M; c0 += 16) {
     for (int i = tid; i < 16 * E; i += blockDim.x) mask[i / E][i % E] = 0ull;
@@ -213,25 +236,22 @@ __global__ __launch_bounds__(1024) void bucket_kernel(const int32_t* __restrict_
   for (int e = tid; e < E; e += blockDim.x) {
     int r = 0;
     for (int f = 0; f < E; ++f) r += (cnt[f] > cnt[e]) || (cnt[f] == cnt[e] && f < e);
+    ord[r] = e;
     order[r] = e;
   }
   __syncthreads();
   // row tiles of resident experts in heavy-first order: tile -> (expert, first row)
-  if (tid == 0) {
-    int run = 0;
-    for (int r = 0; r < E; ++r) {
-      const int e = order[r];
-      tstart[r] = run;
-      if (resident == nullptr || resident[e]) run += (cnt[e] + bm_rows - 1) / bm_rows;
-    }
-    tstart[E] = run;
-    *n_tiles = run;
+  for (int r = tid; r < E; r += blockDim.x) {
+    const int e = ord[r];
+    ntile[r] = (resident == nullptr || resident[e]) ? (cnt[e] + bm_rows - 1) / bm_rows : 0;
   }
   __syncthreads();
-  for (int r = tid; r < E; r += blockDim.x) {
-    const int e = order[r];
-    const int nt = tstart[r + 1] - tstart[r];
-    for (int i = 0; i < nt; ++i) {
+  const int nt = scan128(ntile, tstart, E);
+  if (tid == 0) *n_tiles = nt;
+  __syncthreads();
+  for (int r = wave; r < E; r += blockDim.x / 64) {
+    const int e = ord[r];
+    for (int i = lane; i < ntile[r]; i += 64) {
       tiles[2 * (tstart[r] + i)] = e;
       tiles[2 * (tstart[r] + i) + 1] = i * bm_rows;
     }

@@ -1,9 +1,21 @@
 // Building blocks of the dequantising GEMV, shared by the dense decode kernel
-// and the grouped expert kernels: a lane streams one 32-input group (16 code
-// bytes, one 128-bit load) per step, turns nibbles into fp16 1024 + u by
-// OR-ing them into the mantissa of 0x6400, multiplies pairs against
-// activations with v_dot2_f32_f16 (fp32 accumulation), removes the 1032 offset
-// with the group sum of x, and scales by the group's fp16 scale in fp32.
+// and the grouped expert kernels.
+//
+// A lane owns one 32-input group of a row per step: one 128-bit load of 16
+// code bytes plus its fp16 scale.  Per 32-bit word (8 nibbles, inputs
+// k0..k7, k0 in the low nibble) the nibbles become fp16 values by OR-ing them
+// into the mantissa of 1024.0 (0x6400):
+//   A = (w & 0x000F000F) | 0x6400_6400  ->  (1024 + u0,  1024 + u4)
+//   B = (w & 0x00F000F0) | 0x6400_6400  ->  (1024 + 16 u1, 1024 + 16 u5)
+//   C, D the same on w >> 8             ->  inputs (2, 6) and (3, 7)
+// so four ALU ops cover eight weights.  v_dot2_f32_f16 multiplies each pair
+// with the matching activation pair and accumulates in fp32 (all products are
+// exact: 11-bit by 11-bit).  With S_e, S_o the even- and odd-input sums and
+// X_e, X_o the matching activation sums, the group's exact partial is
+//   sum_k q_k x_k = S_e - 1032 X_e + S_o / 16 - 72 X_o      (q = u - 8),
+// and it is scaled by the group's fp16 scale in fp32.  Activations are
+// permuted once per group to the (k, k+4) pairing, and X_e, X_o are shared by
+// every row of the wave.
 #pragma once
 
 #include "common.h"
@@ -14,6 +26,7 @@ namespace gemv {
 constexpr int kWave = 64;
 constexpr int kBlock = 256;
 constexpr uint32_t kMagic = 0x64006400u;  // fp16 1024.0 in both halves
+constexpr uint32_t kOnes = 0x3C003C00u;   // fp16 (1.0, 1.0)
 
 typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
 
@@ -27,71 +40,66 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
-// x pairs of one 32-input group in nibble order, plus the group sum.
-template <int MT>
-struct XChunk {
-  uint32_t p[MT][16];
-  float sum[MT];
+// Activations of one 32-input group: 16 pairs in nibble order and the
+// correction 1032 X_e + 72 X_o.
+struct XGroup {
+  uint32_t p[16];
+  float corr;
 };
 
-template <int MT>
-__device__ __forceinline__ void load_x(XChunk<MT>& xc, const __half* __restrict__ x, int K, int M, int c,
-                                       bool norm, float (&sq)[MT]) {
+// Raw activation bytes of one group (64 B).
+struct XRaw {
+  uint4 d[4];
+};
+
+__device__ __forceinline__ void load_xraw(XRaw& r, const __half* __restrict__ xrow, int c) {
+  const uint4* src = reinterpret_cast<const uint4*>(xrow + (size_t)c * kGroup);
 #pragma unroll
-  for (int m = 0; m < MT; ++m) {
-    if (m < M) {
-      const uint4* src = reinterpret_cast<const uint4*>(x + (size_t)m * K + (size_t)c * kGroup);
+  for (int b = 0; b < 4; ++b) r.d[b] = src[b];
+}
+
+// Permute to (k, k+4) pairs and form the correction; optionally add the sum of
+// squares (for a fused RMS norm).
+__device__ __forceinline__ void prep_x(XGroup& g, const XRaw& r, bool want_sq, float& sq) {
+  float xe = 0.f, xo = 0.f;
 #pragma unroll
-      for (int b = 0; b < 4; ++b) {       // 8 inputs per 16 bytes
-        uint4 d = src[b];
-        xc.p[m][4 * b + 0] = __builtin_amdgcn_perm(d.z, d.x, 0x05040100u);  // (x0, x4)
-        xc.p[m][4 * b + 1] = __builtin_amdgcn_perm(d.z, d.x, 0x07060302u);  // (x1, x5)
-        xc.p[m][4 * b + 2] = __builtin_amdgcn_perm(d.w, d.y, 0x05040100u);  // (x2, x6)
-        xc.p[m][4 * b + 3] = __builtin_amdgcn_perm(d.w, d.y, 0x07060302u);  // (x3, x7)
-      }
-      float s = 0.f;
+  for (int b = 0; b < 4; ++b) {  // 8 inputs per 16 bytes
+    const uint4 d = r.d[b];
+    g.p[4 * b + 0] = __builtin_amdgcn_perm(d.z, d.x, 0x05040100u);  // (x0, x4)
+    g.p[4 * b + 1] = __builtin_amdgcn_perm(d.z, d.x, 0x07060302u);  // (x1, x5)
+    g.p[4 * b + 2] = __builtin_amdgcn_perm(d.w, d.y, 0x05040100u);  // (x2, x6)
+    g.p[4 * b + 3] = __builtin_amdgcn_perm(d.w, d.y, 0x07060302u);  // (x3, x7)
+    xe = dot2(g.p[4 * b + 0], kOnes, xe);
+    xo = dot2(g.p[4 * b + 1], kOnes, xo);
+    xe = dot2(g.p[4 * b + 2], kOnes, xe);
+    xo = dot2(g.p[4 * b + 3], kOnes, xo);
+  }
+  g.corr = fmaf(1032.f, xe, 72.f * xo);
+  if (want_sq) {
 #pragma unroll
-      for (int i = 0; i < 16; ++i) s = dot2(xc.p[m][i], 0x3C003C00u, s);  // (1.0, 1.0)
-      xc.sum[m] = s;
-      if (norm) {
-        float q = sq[m];
-#pragma unroll
-        for (int i = 0; i < 16; ++i) q = dot2(xc.p[m][i], xc.p[m][i], q);
-        sq[m] = q;
-      }
-    } else {
-#pragma unroll
-      for (int i = 0; i < 16; ++i) xc.p[m][i] = 0u;
-      xc.sum[m] = 0.f;
-    }
+    for (int i = 0; i < 16; ++i) sq = dot2(g.p[i], g.p[i], sq);
   }
 }
 
-// sum_k (1024 + u_k) x_k over one group, per token.
-template <int MT>
-__device__ __forceinline__ void group_dot(const uint4& cw, const XChunk<MT>& xc, float (&part)[MT]) {
-#pragma unroll
-  for (int m = 0; m < MT; ++m) part[m] = 0.f;
+// sum_k q_k x_k over one group (exact products, fp32 sums).
+__device__ __forceinline__ float group_dot(const uint4& cw, const XGroup& g) {
+  float se = 0.f, so = 0.f;
   const uint32_t w4[4] = {cw.x, cw.y, cw.z, cw.w};
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const uint32_t w = w4[i];
-    const uint32_t t0 = (w & 0x000F000Fu) | kMagic;          // inputs 8i+0, 8i+4
-    const uint32_t t1 = ((w >> 4) & 0x000F000Fu) | kMagic;   // 8i+1, 8i+5
-    const uint32_t t2 = ((w >> 8) & 0x000F000Fu) | kMagic;   // 8i+2, 8i+6
-    const uint32_t t3 = ((w >> 12) & 0x000F000Fu) | kMagic;  // 8i+3, 8i+7
-#pragma unroll
-    for (int m = 0; m < MT; ++m) {
-      float a = part[m];
-      a = dot2(t0, xc.p[m][4 * i + 0], a);
-      a = dot2(t1, xc.p[m][4 * i + 1], a);
-      a = dot2(t2, xc.p[m][4 * i + 2], a);
-      a = dot2(t3, xc.p[m][4 * i + 3], a);
-      part[m] = a;
-    }
+    const uint32_t w8 = w >> 8;
+    const uint32_t a = (w & 0x000F000Fu) | kMagic;   // inputs 8i+0, 8i+4
+    const uint32_t b = (w & 0x00F000F0u) | kMagic;   // 8i+1, 8i+5 (x16)
+    const uint32_t c = (w8 & 0x000F000Fu) | kMagic;  // 8i+2, 8i+6
+    const uint32_t d = (w8 & 0x00F000F0u) | kMagic;  // 8i+3, 8i+7 (x16)
+    se = dot2(a, g.p[4 * i + 0], se);
+    so = dot2(b, g.p[4 * i + 1], so);
+    se = dot2(c, g.p[4 * i + 2], se);
+    so = dot2(d, g.p[4 * i + 3], so);
   }
+  return fmaf(so, 0.0625f, se - g.corr);
 }
-
 
 }  // namespace gemv
 }  // namespace atsi

@@ -41,15 +41,53 @@ class Session:
             self._keep += [tc, tsc]
             dc, ds = tc.data_ptr(), tsc.data_ptr()
         if host:
-            pc = torch.from_numpy(np.ascontiguousarray(codes)).pin_memory()
-            ps = torch.from_numpy(sbits.view(np.int16)).pin_memory()
-            self._keep += [pc, ps]
-            hc, hs = pc.data_ptr(), ps.data_ptr()
+            # codes then scales in one pinned buffer: the engine moves it with one copy
+            buf = torch.empty(codes.nbytes + sbits.nbytes, dtype=torch.uint8).pin_memory()
+            self._fill_host(buf, 0, codes, sbits)
+            self._keep.append(buf)
+            hc, hs = buf.data_ptr(), buf.data_ptr() + codes.nbytes
         torch.cuda.synchronize(self.device)
         tid = atsi.atsi_tensor_register(self.ctx, K, N, dc, ds, hc, hs)
         self.shapes.append((K, N))
         self.placement.append(0 if hbm else 1)
         return tid
+
+    @staticmethod
+    def _fill_host(buf: torch.Tensor, off: int, codes: np.ndarray, sbits: np.ndarray) -> None:
+        nb = buf.numpy()
+        nb[off:off + codes.nbytes] = np.ascontiguousarray(codes).reshape(-1).view(np.uint8)
+        nb[off + codes.nbytes:off + codes.nbytes + sbits.nbytes] = np.ascontiguousarray(sbits).reshape(-1).view(np.uint8)
+
+    def register_group(self, tensors, hbm: bool = True, host: bool = True) -> list[int]:
+        """Register several tensors whose host copies sit back to back in one
+        pinned buffer (e.g. an expert's gate, up and down), so a streamed group
+        can move with a single copy."""
+        sb = [np.ascontiguousarray(sc, dtype=np.float16).view(np.uint16) for _, sc in tensors]
+        sizes = [c.nbytes + s.nbytes for (c, _), s in zip(tensors, sb)]
+        buf = torch.empty(sum(sizes), dtype=torch.uint8).pin_memory() if host else None
+        tids, off = [], 0
+        for (codes, _), sbits, size in zip(tensors, sb, sizes):
+            N, kb = codes.shape
+            dc = ds = hc = hs = 0
+            if hbm:
+                tc = torch.from_numpy(np.ascontiguousarray(codes)).to(self.device)
+                tsc = torch.from_numpy(sbits.view(np.int16)).to(self.device)
+                self._keep += [tc, tsc]
+                dc, ds = tc.data_ptr(), tsc.data_ptr()
+            if host:
+                self._fill_host(buf, off, codes, sbits)
+                hc, hs = buf.data_ptr() + off, buf.data_ptr() + off + codes.nbytes
+            off += size
+            tids.append((2 * kb, N, dc, ds, hc, hs))
+        if buf is not None:
+            self._keep.append(buf)
+        torch.cuda.synchronize(self.device)
+        out = []
+        for K, N, dc, ds, hc, hs in tids:
+            out.append(atsi.atsi_tensor_register(self.ctx, K, N, dc, ds, hc, hs))
+            self.shapes.append((K, N))
+            self.placement.append(0 if hbm else 1)
+        return out
 
     def register_device(self, codes_t: torch.Tensor, scales_t: torch.Tensor,
                         host_codes: torch.Tensor | None = None, host_scales: torch.Tensor | None = None) -> int:

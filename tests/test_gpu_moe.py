@@ -79,7 +79,8 @@ class _Setup:
         self.wr = synth.router_weights(seed, 2, H, E)
         # a seeded skew so some experts draw many tokens and some none
         self.bias = (np.linspace(1.5, -1.5, E)[synth.permutation(seed, 3, E)]).astype(np.float32)
-        self.tids = [[sess.register(*self.experts[e][j], hbm=True, host=host) for e in range(E)] for j in range(3)]
+        groups = [sess.register_group(self.experts[e], hbm=True, host=host) for e in range(E)]
+        self.tids = [[groups[e][j] for e in range(E)] for j in range(3)]
         self.layer = sess.moe_layer(_dev(self.wr), *self.tids, top_k=k, router_bias=torch.from_numpy(self.bias).cuda())
 
 
