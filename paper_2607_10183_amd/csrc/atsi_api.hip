@@ -3,14 +3,16 @@
 //
 // Streaming engine (Sec. 4.2.1-4.2.2 of the paper): host-resident tensors are
 // copied from pinned memory into GPU temporary buffers ("slots") on the
-// transfer stream and consumed on the compute stream.  Per slot two events
-// order the streams: `ready` (recorded on the transfer stream after the copy,
+// transfer stream and consumed on the compute stream.  Two kinds of events
+// order the work: `ready` (recorded on the transfer stream after a copy,
 // waited on by the compute stream before the consumer) and `free` (recorded
-// on the compute stream after the consumer, waited on by the transfer stream
-// before the slot is overwritten), so a slot is never reused early.  Copies
-// start as early as a free slot allows: an explicit prefetch, or the schedule
-// (the execution order of tensors) lets the engine run the transfer stream
-// ahead of compute by up to n_slots - 1 tensors.
+// on the compute stream after the consumer; the host checks it before the
+// slot receives another copy), so a slot is never overwritten while read.
+// Copies start as soon as a free slot allows: an explicit prefetch, or the
+// schedule (the execution order of tensors) lets the transfer stream run
+// ahead of compute by up to n_slots - 1 tensors.  A call that needs a copy
+// while every slot is still being read waits on the host for the oldest
+// reader to finish.
 #include <algorithm>
 #include <cstdarg>
 #include <deque>
@@ -47,21 +49,23 @@ struct Tensor {
   bool host_contiguous() const { return hcodes && hcodes + codes_bytes() == reinterpret_cast<const uint8_t*>(hscales); }
 };
 
-// Each slot owns two events; slots filled by one copy share its ready event
-// and slots released by one launch share its free event.  Both streams run in
-// order, so waiting on a later recording of a shared event only waits longer,
-// never too little.
+// A slot is free (may receive a copy now), armed (a copy of `tid` has been
+// issued into it and not consumed yet) or pending (its consumer is enqueued
+// on the compute stream; it turns free once that launch's `free` event has
+// completed).  Slots filled by one copy share its ready event and slots read
+// by one launch share its free event.
 struct Slot {
   char* base = nullptr;
-  hipEvent_t ready = nullptr;      // owned
-  hipEvent_t free = nullptr;       // owned
-  hipEvent_t ready_ev = nullptr;   // event marking this slot's copy done
-  hipEvent_t free_ev = nullptr;    // event marking this slot's last consumer done
-  bool free_recorded = false;
+  hipEvent_t ready = nullptr;     // owned
+  hipEvent_t free = nullptr;      // owned
+  hipEvent_t ready_ev = nullptr;  // event of the copy that fills the slot
+  hipEvent_t free_ev = nullptr;   // event of the launch that last read the slot
+  bool armed = false;
+  bool pending = false;
   int tid = -1;         // tensor whose copy the slot holds or receives
-  bool armed = false;   // copy issued ahead of its consumer, not yet consumed
   uint64_t seq = 0;     // issue order of the armed copy
   uint64_t last = 0;    // last use (issue or consume), for round-robin reuse
+  bool usable() const { return !armed && !pending; }
 };
 
 thread_local std::string g_create_error;
@@ -82,6 +86,7 @@ struct atsi_ctx {
   std::vector<atsi_tid> schedule;  // execution order of tensors, repeated cyclically
   size_t sched_pos = 0;            // next schedule position not yet queued
   std::deque<atsi_tid> queue;      // host tensors to copy ahead, in consumption order
+  std::deque<int> pending;         // pending slots in release order
   uint64_t clock = 0;
   // MoE expert tables, stacked down from the top of the workspace
   struct MoeTable {
@@ -160,21 +165,47 @@ atsi_status layout_slots(atsi_ctx* c) {
   for (int i = 0; i < c->n_slots; ++i) {
     Slot& s = c->slots[i];
     s.base = c->ws + (size_t)i * need;
-    s.free_recorded = false;
-    s.tid = -1;
     s.armed = false;
+    s.pending = false;
+    s.tid = -1;
     s.last = 0;
   }
   c->scratch_off = align_up((size_t)c->n_slots * need);
   c->sched_pos = 0;
   c->queue.clear();
+  c->pending.clear();
   return ATSI_OK;
 }
 
-// Copy host tensor t into slot s: one copy when its host codes and scales are
-// contiguous (small copies cost far more than their bytes), else two.
+// Turn pending slots whose readers have finished back into free ones.  The
+// compute stream completes launches in release order, so the scan stops at
+// the first unfinished one.  With `block`, wait for the oldest pending launch
+// first.  Reuse is decided here, on the host, rather than by making the
+// transfer stream wait for compute-stream events: on ROCm such cross-stream
+// waits in front of DMA copies have stalled the enqueueing thread for
+// milliseconds.
+atsi_status retire(atsi_ctx* c, bool block) {
+  while (!c->pending.empty()) {
+    const hipEvent_t ev = c->slots[c->pending.front()].free_ev;
+    hipError_t e = hipEventQuery(ev);
+    if (e == hipErrorNotReady) {
+      if (!block) break;
+      e = hipEventSynchronize(ev);
+      block = false;
+    }
+    if (e != hipSuccess) return hip_fail(c, e, "free-event wait");
+    while (!c->pending.empty() && c->slots[c->pending.front()].free_ev == ev) {
+      c->slots[c->pending.front()].pending = false;
+      c->pending.pop_front();
+    }
+  }
+  return ATSI_OK;
+}
+
+// Copy host tensor t into slot s on the transfer stream: one copy when its
+// host codes and scales are contiguous (small copies cost far more than their
+// bytes), else two.  The slot must be free.
 atsi_status copy_into(atsi_ctx* c, const Tensor& t, Slot& s) {
-  if (s.free_recorded) HIP_TRY(c, hipStreamWaitEvent(c->ts, s.free_ev, 0));
   if (t.host_contiguous()) {
     HIP_TRY(c, hipMemcpyAsync(s.base, t.hcodes, t.bytes(), hipMemcpyHostToDevice, c->ts));
   } else {
@@ -184,56 +215,79 @@ atsi_status copy_into(atsi_ctx* c, const Tensor& t, Slot& s) {
   return ATSI_OK;
 }
 
-void arm(atsi_ctx* c, Slot& s, atsi_tid tid) {
+void arm(atsi_ctx* c, Slot& s, atsi_tid tid, hipEvent_t ready) {
   s.tid = tid;
   s.armed = true;
+  s.ready_ev = ready;
   s.seq = ++c->clock;
   s.last = s.seq;
 }
 
-// Pick a reusable slot (never one in `pinned`).  When every other slot holds a
-// prefetched copy, the copy furthest in the future is dropped and its tensor
-// queued again.
-atsi_status pick_slot(atsi_ctx* c, const std::vector<int>& pinned, int* out) {
-  auto is_pinned = [&](int i) { return std::find(pinned.begin(), pinned.end(), i) != pinned.end(); };
-  int best = -1;
-  for (int i = 0; i < c->n_slots; ++i) {
-    const Slot& s = c->slots[i];
-    if (s.armed || is_pinned(i)) continue;
-    if (best < 0 || s.last < c->slots[best].last) best = i;
-  }
-  if (best < 0) {
+bool held_by(const std::vector<int>& held, int i) { return std::find(held.begin(), held.end(), i) != held.end(); }
+
+// Pick a slot for a new copy (never one in `held`).  Prefers the least
+// recently used free slot.  Without `block`, returns -1 when none is free
+// yet; with it, waits for pending slots and, when every other slot holds a
+// prefetched copy, drops the copy furthest in the future and queues its
+// tensor again.
+atsi_status pick_slot(atsi_ctx* c, const std::vector<int>& held, bool block, int* out) {
+  atsi_status st;
+  for (;;) {
+    int best = -1;
     for (int i = 0; i < c->n_slots; ++i) {
       const Slot& s = c->slots[i];
-      if (is_pinned(i)) continue;
-      if (best < 0 || s.seq > c->slots[best].seq) best = i;
+      if (s.usable() && !held_by(held, i) && (best < 0 || s.last < c->slots[best].last)) best = i;
+    }
+    if (best >= 0) {
+      *out = best;
+      return ATSI_OK;
+    }
+    const size_t before = c->pending.size();
+    if (before > 0) {
+      if ((st = retire(c, false))) return st;
+      if (c->pending.size() < before) continue;
+      if (!block) {
+        *out = -1;
+        return ATSI_OK;
+      }
+      if ((st = retire(c, true))) return st;
+      continue;
+    }
+    if (!block) {
+      *out = -1;
+      return ATSI_OK;
+    }
+    for (int i = 0; i < c->n_slots; ++i) {
+      const Slot& s = c->slots[i];
+      if (s.armed && !held_by(held, i) && (best < 0 || s.seq > c->slots[best].seq)) best = i;
     }
     if (best < 0)
       return fail(c, ATSI_E_STATE, "one launch needs more streamed tensors than the %d slots", c->n_slots);
     c->queue.push_front(c->slots[best].tid);
     c->slots[best].armed = false;
+    *out = best;
+    return ATSI_OK;
   }
-  *out = best;
-  return ATSI_OK;
 }
 
-// Issue the H2D copy of host tensor `tid` into a reusable slot; returns its index.
-atsi_status issue_copy(atsi_ctx* c, atsi_tid tid, int* slot_out, const std::vector<int>& pinned = {}) {
-  int best;
-  atsi_status st = pick_slot(c, pinned, &best);
+// Issue the H2D copy of host tensor `tid` into a slot; *slot_out is -1 when
+// `block` is false and no slot is free.
+atsi_status issue_copy(atsi_ctx* c, atsi_tid tid, bool block, const std::vector<int>& held, int* slot_out) {
+  int si;
+  atsi_status st = pick_slot(c, held, block, &si);
   if (st) return st;
-  Slot& s = c->slots[best];
+  *slot_out = si;
+  if (si < 0) return ATSI_OK;
+  Slot& s = c->slots[si];
   if ((st = copy_into(c, c->tensors[tid], s))) return st;
   HIP_TRY(c, hipEventRecord(s.ready, c->ts));
-  s.ready_ev = s.ready;
-  arm(c, s, tid);
-  *slot_out = best;
+  arm(c, s, tid, s.ready);
   return ATSI_OK;
 }
 
 // Tensors registered back to back in one host buffer, each exactly one slot in
 // size, can move with a single copy into adjacent free slots (an expert's
-// gate, up and down, for instance).  Returns false when that is not possible.
+// gate, up and down, for instance).
 bool run_candidate(atsi_ctx* c, const atsi_tid* tids, int n) {
   if (n < 2) return false;
   for (int i = 0; i < n; ++i) {
@@ -244,49 +298,45 @@ bool run_candidate(atsi_ctx* c, const atsi_tid* tids, int n) {
   return true;
 }
 
-bool issue_run(atsi_ctx* c, const atsi_tid* tids, int n, const std::vector<int>& pinned, atsi_status* st) {
-  *st = ATSI_OK;
-  if (!run_candidate(c, tids, n)) return false;
-  // runs use slot-aligned groups (first slot a multiple of n) so they never
-  // fragment each other
-  int first = -1;
-  for (int j = 0; j + n <= c->n_slots && first < 0; j += n) {
+// First slot of n adjacent free slots, in slot-aligned groups (first slot a
+// multiple of n) so that runs never fragment each other; -1 if none.
+int find_run(atsi_ctx* c, int n) {
+  for (int j = 0; j + n <= c->n_slots; j += n) {
     bool ok = true;
-    for (int i = 0; i < n && ok; ++i) {
-      const Slot& s = c->slots[j + i];
-      ok = !s.armed && std::find(pinned.begin(), pinned.end(), j + i) == pinned.end();
-    }
-    if (ok) first = j;
+    for (int i = 0; i < n && ok; ++i) ok = c->slots[j + i].usable();
+    if (ok) return j;
   }
-  if (first < 0) return false;
-  for (int i = 0; i < n; ++i) {
-    Slot& s = c->slots[first + i];
-    bool seen = false;
-    for (int j = 0; j < i; ++j) seen = seen || (c->slots[first + j].free_recorded && c->slots[first + j].free_ev == s.free_ev);
-    if (s.free_recorded && !seen) {
-      hipError_t e = hipStreamWaitEvent(c->ts, s.free_ev, 0);
-      if (e != hipSuccess) { *st = hip_fail(c, e, "hipStreamWaitEvent"); return true; }
-    }
-  }
-  hipError_t e = hipMemcpyAsync(c->slots[first].base, c->tensors[tids[0]].hcodes, (size_t)n * c->slot_bytes,
-                                hipMemcpyHostToDevice, c->ts);
-  if (e != hipSuccess) { *st = hip_fail(c, e, "hipMemcpyAsync"); return true; }
-  e = hipEventRecord(c->slots[first].ready, c->ts);
-  if (e != hipSuccess) { *st = hip_fail(c, e, "hipEventRecord"); return true; }
-  for (int i = 0; i < n; ++i) {
-    Slot& s = c->slots[first + i];
-    s.ready_ev = c->slots[first].ready;
-    arm(c, s, tids[i]);
-  }
-  return true;
+  return -1;
 }
 
-// Keep the transfer stream ahead of compute: copy queued (or scheduled) host
-// tensors into free slots, leaving one slot for on-demand copies.
+// Copy a run (see run_candidate) with one hipMemcpyAsync.  *issued is false
+// when no aligned group of free slots exists (after retiring what finished).
+atsi_status issue_run(atsi_ctx* c, const atsi_tid* tids, int n, bool* issued) {
+  *issued = false;
+  int first = find_run(c, n);
+  if (first < 0) {
+    atsi_status st = retire(c, false);
+    if (st) return st;
+    first = find_run(c, n);
+  }
+  if (first < 0) return ATSI_OK;
+  Slot& s0 = c->slots[first];
+  HIP_TRY(c, hipMemcpyAsync(s0.base, c->tensors[tids[0]].hcodes, (size_t)n * c->slot_bytes, hipMemcpyHostToDevice,
+                            c->ts));
+  HIP_TRY(c, hipEventRecord(s0.ready, c->ts));
+  for (int i = 0; i < n; ++i) arm(c, c->slots[first + i], tids[i], s0.ready);
+  *issued = true;
+  return ATSI_OK;
+}
+
+// Keep the transfer stream ahead of compute without waiting: copy queued (or
+// scheduled) host tensors into free slots, leaving one slot for on-demand
+// copies.
 atsi_status topup(atsi_ctx* c) {
   int armed = 0;
   for (const Slot& s : c->slots) armed += s.armed ? 1 : 0;
   size_t guard = 0;
+  atsi_status st;
   while (armed < c->n_slots - 1) {
     if (c->queue.empty()) {
       if (c->schedule.empty() || guard++ >= c->schedule.size()) break;
@@ -299,21 +349,25 @@ atsi_status topup(atsi_ctx* c) {
       const atsi_tid run[3] = {c->queue[0], c->queue[1], c->queue[2]};
       if (run_candidate(c, run, 3)) {
         // an expert moves as one copy or waits for three aligned free slots
-        atsi_status st;
-        if (armed + 3 > c->n_slots - 1 || !issue_run(c, run, 3, {}, &st)) break;
-        if (st) return st;
+        bool issued = false;
+        if (armed + 3 > c->n_slots - 1) break;
+        if ((st = issue_run(c, run, 3, &issued))) return st;
+        if (!issued) break;
         c->queue.erase(c->queue.begin(), c->queue.begin() + 3);
         armed += 3;
         guard = 0;
         continue;
       }
     }
-    atsi_tid t = c->queue.front();
-    c->queue.pop_front();
-    if (!c->tensors[t].on_host) continue;
+    const atsi_tid t = c->queue.front();
+    if (!c->tensors[t].on_host) {
+      c->queue.pop_front();
+      continue;
+    }
     int si;
-    atsi_status st = issue_copy(c, t, &si);
-    if (st) return st;
+    if ((st = issue_copy(c, t, false, {}, &si))) return st;
+    if (si < 0) break;
+    c->queue.pop_front();
     ++armed;
     guard = 0;
   }
@@ -334,9 +388,19 @@ atsi_status prefetch_call(atsi_ctx* c, const atsi_tid* tids, int n) {
   return topup(c);
 }
 
+int armed_slot(atsi_ctx* c, atsi_tid tid, const std::vector<int>& held) {
+  int si = -1;
+  for (int i = 0; i < c->n_slots; ++i) {
+    const Slot& s = c->slots[i];
+    if (s.armed && s.tid == tid && !held_by(held, i) && (si < 0 || s.seq < c->slots[si].seq)) si = i;
+  }
+  return si;
+}
+
 // Resolve where tensor `tid` is read from for the launch being assembled;
 // for a host tensor the compute stream waits for its copy.  The slot index is
-// appended to `held` (HBM tensors hold none).
+// appended to `held` (HBM tensors hold none).  A queued tensor is copied in
+// queue order, waiting for slots to free up as needed.
 atsi_status acquire(atsi_ctx* c, atsi_tid tid, QView* v, std::vector<int>& held) {
   const Tensor& t = c->tensors[tid];
   v->K = (int)t.K;
@@ -346,44 +410,45 @@ atsi_status acquire(atsi_ctx* c, atsi_tid tid, QView* v, std::vector<int>& held)
     v->scales = t.dscales;
     return ATSI_OK;
   }
-  int si = -1;
-  for (int i = 0; i < c->n_slots; ++i) {
-    const Slot& s = c->slots[i];
-    if (s.armed && s.tid == tid && std::find(held.begin(), held.end(), i) == held.end() &&
-        (si < 0 || s.seq < c->slots[si].seq))
-      si = i;
+  atsi_status st;
+  int si = armed_slot(c, tid, held);
+  while (si < 0 && std::find(c->queue.begin(), c->queue.end(), tid) != c->queue.end()) {
+    if ((st = topup(c))) return st;
+    if ((si = armed_slot(c, tid, held)) >= 0 || c->pending.empty()) break;
+    if ((st = retire(c, true))) return st;
   }
   if (si < 0) {
     auto q = std::find(c->queue.begin(), c->queue.end(), tid);
     if (q != c->queue.end()) c->queue.erase(q);
-    atsi_status st = issue_copy(c, tid, &si, held);
-    if (st) return st;
+    if ((st = issue_copy(c, tid, true, held, &si))) return st;
   }
   Slot& s = c->slots[si];
-  HIP_TRY(c, hipStreamWaitEvent(c->cs, s.ready_ev, 0));
+  bool waited = false;
+  for (int h : held) waited = waited || c->slots[h].ready_ev == s.ready_ev;
+  if (!waited) HIP_TRY(c, hipStreamWaitEvent(c->cs, s.ready_ev, 0));
   v->codes = reinterpret_cast<const uint8_t*>(s.base);
   v->scales = reinterpret_cast<const uint16_t*>(s.base + t.codes_bytes());
   held.push_back(si);
   return ATSI_OK;
 }
 
-// After the consumer kernel of the held slots has been enqueued.
+// After the consumer launch of the held slots has been enqueued.
 atsi_status release(atsi_ctx* c, std::vector<int>& held) {
   if (!held.empty()) {
-    hipEvent_t ev = c->slots[held[0]].free;
+    const hipEvent_t ev = c->slots[held[0]].free;
     HIP_TRY(c, hipEventRecord(ev, c->cs));
     for (int si : held) {
       Slot& s = c->slots[si];
       s.free_ev = ev;
-      s.free_recorded = true;
       s.armed = false;
+      s.pending = true;
       s.last = ++c->clock;
+      c->pending.push_back(si);
     }
   }
   held.clear();
   return topup(c);
 }
-
 
 // Bump allocator over the scratch region of the workspace (after the slots).
 struct Scratch {
@@ -530,9 +595,9 @@ atsi_status atsi_create(int device, void* compute_stream, void* transfer_stream,
 
 atsi_status atsi_destroy(atsi_ctx* c) {
   if (!c) return ATSI_E_INVALID;
-  hipSetDevice(c->device);
-  if (c->cs) hipStreamSynchronize(c->cs);
-  if (c->ts) hipStreamSynchronize(c->ts);
+  (void)hipSetDevice(c->device);
+  if (c->cs) (void)hipStreamSynchronize(c->cs);
+  if (c->ts) (void)hipStreamSynchronize(c->ts);
   for (Slot& s : c->slots) {
     if (s.ready) hipEventDestroy(s.ready);
     if (s.free) hipEventDestroy(s.free);
