@@ -24,6 +24,7 @@
 
 #include "../../include/atsi.h"
 #include "common.h"
+#include "layer.h"
 #include "moe.h"
 
 using namespace atsi;
@@ -31,6 +32,9 @@ using namespace atsi;
 namespace {
 
 constexpr size_t kAlign = 256;
+// The single-launch decode layer (q4_layer.hip) is not enabled yet: it has not
+// passed its GPU tests.  Decoder layers run as four fused launches.
+constexpr bool kFusedDecodeLayer = false;
 inline size_t align_up(size_t v, size_t a = kAlign) { return (v + a - 1) / a * a; }
 
 struct Tensor {
@@ -98,6 +102,8 @@ struct atsi_ctx {
   std::vector<MoeTable> tables;
   size_t table_floor = 0;       // lowest byte used by tables (ws_bytes if none)
   uint64_t placement_version = 0;
+  unsigned* layer_bar = nullptr;  // barrier words of the fused decode layer (top of the workspace)
+  bool layer_launched = false;    // a fused layer ran since the last atsi_sync
   int32_t* pinned = nullptr;    // pinned host copy of per-expert counts
   hipEvent_t counts_ev = nullptr;
   std::string err;
@@ -574,6 +580,13 @@ atsi_status atsi_create(int device, void* compute_stream, void* transfer_stream,
   c->ws_bytes = workspace_bytes;
   c->n_slots = n_slots;
   c->table_floor = workspace_bytes / kAlign * kAlign;
+  const size_t bar_bytes = align_up(kLayerBarrierWords * sizeof(unsigned));
+  if (c->table_floor < bar_bytes) {
+    delete c;
+    return fail(nullptr, ATSI_E_WORKSPACE, "workspace of %zu B is too small", workspace_bytes);
+  }
+  c->table_floor -= bar_bytes;
+  c->layer_bar = reinterpret_cast<unsigned*>(c->ws + c->table_floor);
   c->slots.resize(n_slots);
   if (hipHostMalloc((void**)&c->pinned, kMaxExperts * sizeof(int32_t), hipHostMallocDefault) != hipSuccess ||
       hipEventCreateWithFlags(&c->counts_ev, hipEventDisableTiming) != hipSuccess) {
@@ -588,6 +601,12 @@ atsi_status atsi_create(int device, void* compute_stream, void* transfer_stream,
       atsi_destroy(c);
       return ATSI_E_HIP;
     }
+  }
+  // the fused decode layer's barrier starts from zeroed words and leaves them so
+  if (hipMemsetAsync(c->layer_bar, 0, bar_bytes, c->cs) != hipSuccess || hipStreamSynchronize(c->cs) != hipSuccess) {
+    fail(nullptr, ATSI_E_HIP, "clearing the workspace barrier words failed");
+    atsi_destroy(c);
+    return ATSI_E_HIP;
   }
   *out = c;
   return ATSI_OK;
@@ -746,10 +765,42 @@ atsi_status atsi_decoder_layer(atsi_ctx* c, const atsi_dense_layer* L, void* h, 
   __half* oin = sc.take((size_t)M * Hq);
   __half* hf = sc.take((size_t)M * tg.N);
   if (!qb || !kb || !oin || !hf) return fail(c, ATSI_E_WORKSPACE, "scratch too small for a %lld-token layer", (long long)M);
-  if ((st = prefetch_call(c, ids, 7))) return st;
   __half* hh = (__half*)h;
   const int Mi = (int)M;
   const float eps = L->eps;
+  bool resident = true;
+  for (atsi_tid t : ids) resident = resident && !c->tensors[t].on_host;
+  if (kFusedDecodeLayer && Mi == 1 && resident) {
+    // batch-1 decode with every weight in HBM: one fused launch
+    LayerArgs la{};
+    for (int i = 0; i < kLayerTensors; ++i) {
+      const Tensor& t = c->tensors[ids[i]];
+      la.w[i] = QView{t.dcodes, t.dscales, (int)t.K, (int)t.N};
+    }
+    la.h = hh;
+    la.q_out = qb;
+    la.k_out = kb;
+    la.oin = oin;
+    la.hf = hf;
+    la.H = (int)H;
+    la.Hq = (int)Hq;
+    la.Hkv = (int)Hkv;
+    la.I = (int)tg.N;
+    la.head_dim = L->head_dim;
+    la.expand = L->n_heads / L->n_kv_heads;
+    la.eps = eps;
+    la.bar = c->layer_bar;
+    if (la.expand <= 64) {
+      hipError_t e = launch_decode_layer(la, c->cs);
+      if (e == hipSuccess) {
+        c->layer_launched = true;
+        return ATSI_OK;
+      }
+      if (e != hipErrorInvalidConfiguration) return hip_fail(c, e, "fused decode layer launch");
+      (void)hipGetLastError();  // shape outside the fused kernel: four launches below
+    }
+  }
+  if ((st = prefetch_call(c, ids, 7))) return st;
 
   // 1. q, k, v = rms(h) Wq, Wk, Wv in one launch; v goes straight to the
   //    attention output of every query head of its group (context length 1)
@@ -945,6 +996,18 @@ atsi_status atsi_sync(atsi_ctx* c) {
   if (e == hipSuccess) e = hipStreamSynchronize(c->ts);
   if (e == hipSuccess) e = hipStreamSynchronize(c->cs);
   if (e != hipSuccess) hip_fail(c, e, "stream synchronize");
+  if (e == hipSuccess && c->layer_launched) {
+    // a grid barrier of the fused decode layer that timed out leaves a flag
+    unsigned flag = 0;
+    e = hipMemcpy(&flag, c->layer_bar + kLayerBarrierErrWord, sizeof flag, hipMemcpyDeviceToHost);
+    if (e != hipSuccess) {
+      hip_fail(c, e, "reading the fused-layer barrier flag");
+    } else if (flag) {
+      (void)hipMemset(c->layer_bar, 0, kLayerBarrierWords * sizeof(unsigned));
+      hip_fail(c, hipErrorLaunchTimeOut, "fused decode layer: a grid barrier timed out");
+    }
+    c->layer_launched = false;
+  }
   if (c->latched != ATSI_OK) {
     c->err = c->latched_msg;
     return c->latched;
