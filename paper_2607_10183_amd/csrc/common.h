@@ -46,6 +46,19 @@ struct LinOp {
 
 __device__ __forceinline__ float silu_f(float g) { return g / (1.f + expf(-g)); }
 
+// Loads through the global address space.  Pointers read from memory (expert
+// tables, step tables) are otherwise generic, and a generic load also counts
+// against the LDS wait counter: every LDS wait would then drain the loads in
+// flight.
+typedef unsigned u32x4_g __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 ldg16(const void* p) {
+  const u32x4_g v = *reinterpret_cast<const __attribute__((address_space(1))) u32x4_g*>(reinterpret_cast<uintptr_t>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ uint16_t ldg2(const uint16_t* p) {
+  return *reinterpret_cast<const __attribute__((address_space(1))) uint16_t*>(reinterpret_cast<uintptr_t>(p));
+}
+
 // ---- launchers (each returns hipGetLastError() of its launch) ----
 constexpr size_t kGemvMaxLds = 64 * 1024;  // activations staged per GEMV workgroup
 // decode GEMV handles 1 <= M <= 4 when its staged activations fit in LDS

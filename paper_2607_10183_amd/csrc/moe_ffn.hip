@@ -58,7 +58,7 @@ __global__ __launch_bounds__(kGemmBlock, 2) void expert_gateup_gemm(MoeArgs a, i
     arow[i] = r < rows ? a.x + (size_t)(a.perm[base + r] / a.k) * a.H : nullptr;
   }
   g_float16_t acc[Core::FM][Core::FN];
-  Core::run(sm, arow, w.gate, w.up, n0, a.H, false, 0.f, acc);
+  Core::run(sm, arow, a.x, w.gate, w.up, n0, a.H, 0.f, acc);
 #pragma unroll
   for (int i = 0; i < Core::FM; ++i)
 #pragma unroll
@@ -90,7 +90,7 @@ __global__ __launch_bounds__(kGemmBlock, 2) void expert_down_gemm(MoeArgs a, int
     arow[i] = r < rows ? a.h + (size_t)(base + r) * a.I : nullptr;
   }
   g_float16_t acc[Core::FM][Core::FN];
-  Core::run(sm, arow, w.down, w.down, n0, a.I, false, 0.f, acc);
+  Core::run(sm, arow, a.h, w.down, w.down, n0, a.I, 0.f, acc);
 #pragma unroll
   for (int i = 0; i < Core::FM; ++i)
 #pragma unroll
@@ -145,11 +145,11 @@ __global__ __launch_bounds__(gemv::kBlock) void expert_gemv(MoeArgs a, int tile_
 #pragma unroll
       for (int r = 0; r < RW; ++r) {
         const int row = min(n0 + r, N - 1);
-        cw[h][r] = *reinterpret_cast<const uint4*>(w1.codes + (size_t)row * rbytes + (size_t)c * 16);
-        sc[h][r] = w1.scales[(size_t)row * nchunk + c];
+        cw[h][r] = ldg16(w1.codes + (size_t)row * rbytes + (size_t)c * 16);
+        sc[h][r] = ldg2(w1.scales + (size_t)row * nchunk + c);
         if constexpr (!DOWN) {
-          cw2[h][r] = *reinterpret_cast<const uint4*>(w2.codes + (size_t)row * rbytes + (size_t)c * 16);
-          sc2[h][r] = w2.scales[(size_t)row * nchunk + c];
+          cw2[h][r] = ldg16(w2.codes + (size_t)row * rbytes + (size_t)c * 16);
+          sc2[h][r] = ldg2(w2.scales + (size_t)row * nchunk + c);
         }
       }
       load_xraw(xv[h], xr, c);

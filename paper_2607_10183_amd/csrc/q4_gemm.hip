@@ -21,9 +21,9 @@ struct TileMap {
   int total;
 };
 
-template <int BM, int BN, int WM, int WN, bool SWI>
+template <int BM, int BN, int WM, int WN, bool SWI, bool NORM>
 __global__ __launch_bounds__(kGemmBlock, 2) void q4_gemm_kernel(LinOp op, TileMap tm_) {
-  using Core = GemmCore<BM, BN, WM, WN, SWI>;
+  using Core = GemmCore<BM, BN, WM, WN, SWI, NORM>;
   __shared__ __attribute__((aligned(16))) typename Core::Smem sm;
 
   // XCD-aware order: consecutive ids go to different XCDs (8-way round
@@ -45,7 +45,7 @@ __global__ __launch_bounds__(kGemmBlock, 2) void q4_gemm_kernel(LinOp op, TileMa
     arow[i] = m < M ? op.x + (size_t)m * K : nullptr;
   }
   g_float16_t acc[Core::FM][Core::FN];
-  Core::run(sm, arow, sg.w, sg.w2, n0, K, op.norm != 0, op.eps, acc);
+  Core::run(sm, arow, op.x, sg.w, sg.w2, n0, K, op.eps, acc);
 
 #pragma unroll
   for (int i = 0; i < Core::FM; ++i)
@@ -59,7 +59,7 @@ __global__ __launch_bounds__(kGemmBlock, 2) void q4_gemm_kernel(LinOp op, TileMa
         const int ml = Core::frag_row(i, v);
         const int m = m0 + ml;
         if (m >= M) continue;
-        const float sc = op.norm ? sm.rowinv[ml] : 1.f;
+        const float sc = NORM ? sm.rowinv[ml] : 1.f;
         float o = acc[i][j][v] * sc;
         if constexpr (SWI) o = silu_f(o) * (acc[i][j + 1][v] * sc);
         if (sg.expand > 1) {
@@ -75,8 +75,8 @@ __global__ __launch_bounds__(kGemmBlock, 2) void q4_gemm_kernel(LinOp op, TileMa
     }
 }
 
-template <int BM, int BN, int WM, int WN, bool SWI>
-hipError_t launch_tile(const LinOp& op, hipStream_t st) {
+template <int BM, int BN, int WM, int WN, bool SWI, bool NORM>
+hipError_t launch_tile_n(const LinOp& op, hipStream_t st) {
   constexpr int NOUT = GemmCore<BM, BN, WM, WN, SWI>::NOUT;
   TileMap tm{};
   tm.tiles_m = (op.M + BM - 1) / BM;
@@ -86,8 +86,13 @@ hipError_t launch_tile(const LinOp& op, hipStream_t st) {
     tm.end[s] = total;
   }
   tm.total = total;
-  hipLaunchKernelGGL((q4_gemm_kernel<BM, BN, WM, WN, SWI>), dim3(total), dim3(kGemmBlock), 0, st, op, tm);
+  hipLaunchKernelGGL((q4_gemm_kernel<BM, BN, WM, WN, SWI, NORM>), dim3(total), dim3(kGemmBlock), 0, st, op, tm);
   return hipGetLastError();
+}
+
+template <int BM, int BN, int WM, int WN, bool SWI>
+hipError_t launch_tile(const LinOp& op, hipStream_t st) {
+  return op.norm ? launch_tile_n<BM, BN, WM, WN, SWI, true>(op, st) : launch_tile_n<BM, BN, WM, WN, SWI, false>(op, st);
 }
 
 // unpack kernel for the debug export: q[n][k] = nibble - 8

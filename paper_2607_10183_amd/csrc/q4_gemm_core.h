@@ -8,15 +8,17 @@
 //     and the weight tile is dequantised into LDS as fp16: nibble -> 1024 + u
 //     by mantissa OR, minus 1032 (exact), times the group scale (one rounding);
 //     activations stay fp16, so the only operand rounding is w = RNE16(s * q);
-//   * the next K step's global loads are issued before the current step's
-//     MFMAs (register double-buffering) and LDS is double-buffered;
+//   * global loads run two K steps ahead of the MFMAs through two register
+//     stages, and LDS is double-buffered; loads past the last K step repeat
+//     it, so every iteration issues the same loads and the compiler's wait
+//     counts stay exact;
 //   * LDS rows are padded by 16 bytes so the 16-byte fragment reads of a
 //     wavefront hit distinct banks;
 //   * activation rows come from per-thread row pointers, so a tile can gather
 //     its rows (tokens routed to one expert) from anywhere;
 //   * with SWI the B tile interleaves 32-row blocks of two tensors (gate, up)
 //     so one lane ends up holding g and u of the same output;
-//   * with norm the row sums of squares are gathered while staging the
+//   * with NORM the row sums of squares are gathered while staging the
 //     activations and 1/rms per row lands in LDS for the epilogue.
 #pragma once
 
@@ -31,6 +33,7 @@ typedef float g_float16_t __attribute__((ext_vector_type(16)));
 constexpr int kGemmBlock = 256;
 constexpr int kBK = 64;          // K per LDS stage = two scale groups
 constexpr int kLDSP = kBK + 8;   // padded LDS row length in halves
+constexpr int kPre = 2;          // register stages of global loads in flight
 
 __device__ __forceinline__ uint32_t pk_sub_mul(uint32_t t, g_half2_t off, g_half2_t s) {
   g_half2_t v = __builtin_bit_cast(g_half2_t, t);
@@ -60,7 +63,7 @@ __device__ __forceinline__ void dequant_group(const uint4& cw, uint16_t sbits, u
 }
 
 
-template <int BM, int BN, int WM, int WN, bool SWI>
+template <int BM, int BN, int WM, int WN, bool SWI, bool NORM = false>
 struct GemmCore {
   static_assert(WM * WN == 4, "four waves");
   static constexpr int SM = BM / WM, SN = BN / WN;  // wave sub-tile
@@ -82,37 +85,44 @@ struct GemmCore {
   __device__ static int xrow(int i) { return (threadIdx.x + i * kGemmBlock) / (kBK / 8); }
 
   // arow[i]: pointer to activation row xrow(i) (K halves), or nullptr for a row
-  // outside the tile.  Weight rows n0 .. (n0 + NOUT) of w (and w2).
-  __device__ static void run(Smem& sm, const __half* const (&arow)[XV], const QView& w, const QView& w2, int n0,
-                             int K, bool norm, float eps, g_float16_t (&acc)[FM][FN]) {
+  // outside the tile; safe: any readable 16-byte activation chunk.  Weight
+  // rows n0 .. (n0 + NOUT) of w (and w2).
+  __device__ static void run(Smem& sm, const __half* const (&arow)[XV], const __half* safe, const QView& w,
+                             const QView& w2, int n0, int K, float eps, g_float16_t (&acc)[FM][FN]) {
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int wm = wave / WN, wn = wave % WN;
     const int ngrp = K / 32;
     const int nk = (K + kBK - 1) / kBK;
 
-    uint4 xr[XV];
-    uint4 cr[WG];
-    uint16_t sr[WG];
+    uint4 xr[kPre][XV];
+    uint4 cr[kPre][WG];
+    uint16_t sr[kPre][WG];
+    uint32_t sok[kPre][WG];  // 0xFFFF for a group inside the tensor, else 0
     float sq[XV];
 #pragma unroll
     for (int i = 0; i < XV; ++i) sq[i] = 0.f;
 
-    auto gload = [&](int kt) {
-      const int k0 = kt * kBK;
+    // global loads of K step kt (clamped to the last one) into stage st
+    auto gload = [&](int st, int kt) {
+      const int k0 = (kt < nk ? kt : nk - 1) * kBK;
 #pragma unroll
       for (int i = 0; i < XV; ++i) {
+        // loads are unconditional (rows outside the tile read `safe`, K past
+        // the end its last chunk) and zeroed afterwards, so that every lane
+        // issues the same loads
         const int cchunk = (tid + i * kGemmBlock) % (kBK / 8);
         const int k = k0 + cchunk * 8;
-        if (arow[i] != nullptr && k < K)
-          xr[i] = *reinterpret_cast<const uint4*>(arow[i] + k);
-        else
-          xr[i] = make_uint4(0, 0, 0, 0);
+        const bool ok = arow[i] != nullptr && k < K;
+        const __half* p = arow[i] != nullptr ? arow[i] + (k < K ? k : K - 8) : safe;
+        const uint4 v = ldg16(p);
+        xr[st][i] = ok ? v : make_uint4(0, 0, 0, 0);
       }
 #pragma unroll
       for (int i = 0; i < WG; ++i) {
-        const int idx = tid + i * kGemmBlock;
-        if (idx >= BN * 2) break;
+        // every thread loads (threads past the tile repeat its last group);
+        // groups outside the tensor get scale 0 when dequantised
+        const int idx = min(tid + i * kGemmBlock, BN * 2 - 1);
         const int br = idx >> 1, g = (k0 >> 5) + (idx & 1);
         int n;
         const QView* src = &w;
@@ -123,39 +133,40 @@ struct GemmCore {
         } else {
           n = n0 + br;
         }
-        if (n < w.N && g < ngrp) {
-          cr[i] = *reinterpret_cast<const uint4*>(src->codes + (size_t)n * (K / 2) + (size_t)g * 16);
-          sr[i] = src->scales[(size_t)n * ngrp + g];
-        } else {
-          cr[i] = make_uint4(0x88888888u, 0x88888888u, 0x88888888u, 0x88888888u);  // q = 0
-          sr[i] = 0;
-        }
+        const int nc = n < w.N ? n : w.N - 1, gc = g < ngrp ? g : ngrp - 1;
+        cr[st][i] = ldg16(src->codes + (size_t)nc * (K / 2) + (size_t)gc * 16);
+        sr[st][i] = ldg2(src->scales + (size_t)nc * ngrp + gc);
+        sok[st][i] = n < w.N && g < ngrp ? 0xFFFFu : 0u;
       }
     };
-    auto lstore = [&](int buf) {
+    // stage st into LDS buffer buf (activations as they are, weights
+    // dequantised); sq gathers row sums of squares once per K step
+    auto lstore = [&](int st, int buf, float count) {
 #pragma unroll
       for (int i = 0; i < XV; ++i) {
         const int idx = tid + i * kGemmBlock;
         const int r = idx / (kBK / 8), cchunk = idx % (kBK / 8);
-        *reinterpret_cast<uint4*>(&sm.As[buf][r * kLDSP + cchunk * 8]) = xr[i];
-        if (norm) {
-          const g_half2_t* h = reinterpret_cast<const g_half2_t*>(&xr[i]);
-          float q = sq[i];
+        *reinterpret_cast<uint4*>(&sm.As[buf][r * kLDSP + cchunk * 8]) = xr[st][i];
+        if constexpr (NORM) {
+          const g_half2_t* h = reinterpret_cast<const g_half2_t*>(&xr[st][i]);
+          float q = 0.f;
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
             const float a = (float)h[j][0], b = (float)h[j][1];
             q = fmaf(a, a, fmaf(b, b, q));
           }
-          sq[i] = q;
+          sq[i] = fmaf(count, q, sq[i]);  // count 0 for a repeated K step
         }
       }
 #pragma unroll
       for (int i = 0; i < WG; ++i) {
         const int idx = tid + i * kGemmBlock;
-        if (idx >= BN * 2) break;
+        if constexpr ((BN * 2) % kGemmBlock != 0) {
+          if (idx >= BN * 2) break;
+        }
         const int r = idx >> 1, gl = idx & 1;
         uint4 o[4];
-        dequant_group(cr[i], sr[i], o);
+        dequant_group(cr[st][i], (uint16_t)(sr[st][i] & sok[st][i]), o);  // scale 0: weights 0
         uint4* dst = reinterpret_cast<uint4*>(&sm.Bs[buf][r * kLDSP + gl * 32]);
 #pragma unroll
         for (int j = 0; j < 4; ++j) dst[j] = o[j];
@@ -169,14 +180,18 @@ struct GemmCore {
 #pragma unroll
         for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-    gload(0);
-    lstore(0);
+    // stage s and LDS buffer s hold K steps s, s + 2, s + 4, ...  The steady
+    // state is one basic block per K step (MFMAs on one LDS buffer, the next
+    // step's dequantisation into the other, the refill loads), so the
+    // scheduler can overlap the dequantising VALU work with the MFMAs.
+    gload(0, 0);
+    gload(1, 1);
+    lstore(0, 0, 1.f);
+    gload(0, 2);
     __syncthreads();
 
     const int frow = lane & 31, fk = (lane >> 5) * 8;
-    for (int kt = 0; kt < nk; ++kt) {
-      const int buf = kt & 1;
-      if (kt + 1 < nk) gload(kt + 1);
+    auto mfma_step = [&](int buf) {
 #pragma unroll
       for (int ks = 0; ks < kBK / 16; ++ks) {
         g_half8_t a[FM], b[FN];
@@ -192,13 +207,24 @@ struct GemmCore {
           for (int j = 0; j < FN; ++j)
             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a[i], b[j], acc[i][j], 0, 0, 0);
       }
-      if (kt + 1 < nk) {
-        lstore(buf ^ 1);
-        __syncthreads();
-      }
+    };
+    // K step kt on buffer st: MFMAs, stage st ^ 1 (K step kt + 1) into LDS,
+    // refill stage st ^ 1 with K step kt + 3 (clamped, so every step issues
+    // the same loads and the compiler waits for exactly one stage)
+    int kt = 0;
+    for (; kt + 2 <= nk; kt += 2) {
+      mfma_step(0);
+      lstore(1, 1, kt + 1 < nk ? 1.f : 0.f);
+      gload(1, kt + 3);
+      __syncthreads();
+      mfma_step(1);
+      lstore(0, 0, kt + 2 < nk ? 1.f : 0.f);
+      gload(0, kt + 4);
+      __syncthreads();
     }
+    if (kt < nk) mfma_step(0);
 
-    if (norm) {
+    if constexpr (NORM) {
 #pragma unroll
       for (int i = 0; i < XV; ++i) {
         float q = sq[i];
