@@ -17,12 +17,18 @@ synthetic weights and activations.
   moe               30B-A3B-shaped MoE layer (128 experts, top-8, capped-Zipf
                     routing): decode and 512-token prefill, all-HBM and with
                     51 experts on host.
-  roofline          dominant decode kernel (GEMV over the 4096 x 14336 gate
-                    tensor) against 8 TB/s; roofline_prefill: the 512 x 4096 x
-                    14336 GEMM against 2.5 PFLOP/s fp16 MFMA.
+  roofline          the dominant decode kernel, the fused SwiGLU gate/up GEMV
+                    (two 4096 x 14336 tensors, 66.1 MB per launch), against
+                    8 TB/s; roofline_prefill: the fused gate/up GEMM at 512
+                    tokens against 2.5 PFLOP/s fp16 MFMA.  Both are timed
+                    alone (atsi_swiglu_gate_up) with HIP events; their HBM
+                    traffic comes from the committed counter profile when the
+                    kernel sources still match it.
   cpu_baseline      the fp64 oracle's decode step on the host cores.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
+       python bench.py --roofline-only   (the two roofline kernels and a
+                                          256 MiB copy; for counter runs)
 """
 from __future__ import annotations
 
@@ -68,6 +74,33 @@ class Timer:
         return self.a.elapsed_time(self.b) * 1e-3 / n
 
 
+def kernel_hash(kind: str) -> str:
+    """sha256 of the sources a roofline kernel is built from."""
+    import hashlib
+    csrc = os.path.join(ROOT, "paper_2607_10183_amd", "csrc")
+    files = {"q4_gemv": ("common.h", "q4_gemv_core.h", "q4_gemv.hip"),
+             "q4_gemm": ("common.h", "q4_gemm_core.h", "q4_gemm.hip")}[kind]
+    h = hashlib.sha256()
+    for f in files:
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(key: str, kind: str):
+    """HBM bytes per launch from the committed FETCH_SIZE / WRITE_SIZE profile
+    (profiles/traffic.json), or None when the kernel sources changed since."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    try:
+        with open(path) as fh:
+            rec = json.load(fh)[key]
+    except (OSError, KeyError, ValueError):
+        return None
+    if rec.get("source_sha256_16") != kernel_hash(kind):
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
 def graph_of(stream, fn):
     import torch
     fn()  # warm (allocations, table writes) outside capture
@@ -87,10 +120,11 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-moe", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--roofline-only", action="store_true",
+                    help="run only the roofline kernels and a 256 MiB copy (for rocprofv3 --pmc)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
-              "(sharding is described in DESIGN.md, not implemented)", file=sys.stderr)
+        print("bench.py runs on exactly one GPU: the library has no multi-GPU path", file=sys.stderr)
         return 2
 
     import torch
@@ -129,30 +163,64 @@ def main() -> int:
         atsi.atsi_decoder_layer(sess.ctx, descs[c], h.data_ptr(), M, 0, 0)
 
     # ------------------------------------------------------------ decode, HBM-resident (value)
-    reps = 4
+    decode_s = steps_timed = n_warm = per_replay = decode_gbs = 0
+    if not args.roofline_only:
+        reps = 4
 
-    def decode_round():
-        for _ in range(reps):
-            for c in range(R):
-                layer(c, h1, 1)
+        def decode_round():
+            for _ in range(reps):
+                for c in range(R):
+                    layer(c, h1, 1)
 
-    g = graph_of(cs, decode_round)
-    per_replay = reps * R
-    n_replay = max(1, args.steps // per_replay)
-    n_warm = max(1, args.warmup // per_replay)
-    timer.run(g.replay, n_warm)
-    decode_s = timer.run(g.replay, n_replay) / per_replay
-    steps_timed = n_replay * per_replay
-    decode_gbs = layer_bytes / decode_s / 1e9
-    log(f"decode layer {decode_s * 1e6:.2f} us -> {decode_gbs:.1f} GB/s ({steps_timed} steps)")
+        g = graph_of(cs, decode_round)
+        per_replay = reps * R
+        n_replay = max(1, args.steps // per_replay)
+        n_warm = max(1, args.warmup // per_replay)
+        timer.run(g.replay, n_warm)
+        decode_s = timer.run(g.replay, n_replay) / per_replay
+        steps_timed = n_replay * per_replay
+        decode_gbs = layer_bytes / decode_s / 1e9
+        log(f"decode layer {decode_s * 1e6:.2f} us -> {decode_gbs:.1f} GB/s ({steps_timed} steps)")
 
     # ------------------------------------------------------------ dominant kernels
     xs = {r: torch.from_numpy(synth.activations(wl.seed, 50 + i, Mp, shape.kn(r)[0])).to(dev)
           for i, r in enumerate(roles)}
+    hg = torch.empty((Mp, shape.inter), dtype=torch.float16, device=dev)
     yg = torch.empty((Mp, shape.inter), dtype=torch.float16, device=dev)
     cs.wait_stream(torch.cuda.current_stream())
     K_g, N_g = shape.kn("gate")
 
+    def gate_up_round(M, n):
+        def f():
+            for _ in range(n):
+                for c in range(R):
+                    atsi.atsi_swiglu_gate_up(sess.ctx, tids[c]["gate"], tids[c]["up"], xs["gate"].data_ptr(), M,
+                                             hg.data_ptr())
+        return f
+
+    gk = graph_of(cs, gate_up_round(1, 8))
+    t_gemv = timer.run(gk.replay, 10) / (8 * R)
+    gemv_bytes = 2 * configs.qbytes(K_g, N_g)
+    gemv_gbs = gemv_bytes / t_gemv / 1e9
+    log(f"gate/up GEMV {t_gemv * 1e6:.2f} us -> {gemv_gbs:.1f} GB/s")
+    gm = graph_of(cs, gate_up_round(Mp, 1))
+    t_gemm = timer.run(gm.replay, 4) / R
+    gemm_flops = 2.0 * 2.0 * Mp * K_g * N_g
+    gemm_tfs = gemm_flops / t_gemm / 1e12
+    log(f"gate/up GEMM {t_gemm * 1e6:.1f} us -> {gemm_tfs:.1f} TFLOP/s")
+    if args.roofline_only:
+        # copy of known size: calibrates the FETCH_SIZE / WRITE_SIZE counters
+        src = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        sess.close()
+        print(json.dumps({"roofline_only": True, "gate_up_gemv_us": round(t_gemv * 1e6, 3),
+                          "gate_up_gemm_us": round(t_gemm * 1e6, 2), "copy_bytes": 256 << 20}), flush=True)
+        return 0
+
+    # the standalone gate GEMV / GEMM (same kernels as the q, k, v, o launches)
     def gate_round(M, n):
         def f():
             for _ in range(n):
@@ -160,16 +228,9 @@ def main() -> int:
                     atsi.atsi_linear(sess.ctx, tids[c]["gate"], xs["gate"].data_ptr(), M, yg.data_ptr())
         return f
 
-    gk = graph_of(cs, gate_round(1, 8))
-    t_gemv = timer.run(gk.replay, 10) / (8 * R)
-    gemv_bytes = configs.qbytes(K_g, N_g)
-    gemv_gbs = gemv_bytes / t_gemv / 1e9
-    log(f"gate GEMV {t_gemv * 1e6:.2f} us -> {gemv_gbs:.1f} GB/s")
-    gm = graph_of(cs, gate_round(Mp, 1))
-    t_gemm = timer.run(gm.replay, 4) / R
-    gemm_flops = 2.0 * Mp * K_g * N_g
-    gemm_tfs = gemm_flops / t_gemm / 1e12
-    log(f"gate GEMM {t_gemm * 1e6:.1f} us -> {gemm_tfs:.1f} TFLOP/s")
+    g1 = graph_of(cs, gate_round(1, 8))
+    t_gate1 = timer.run(g1.replay, 10) / (8 * R)
+    log(f"gate GEMV {t_gate1 * 1e6:.2f} us -> {configs.qbytes(K_g, N_g) / t_gate1 / 1e9:.1f} GB/s")
 
     # ------------------------------------------------------------ prefill 512, HBM-resident
     pf_state = {"i": 0}
@@ -248,13 +309,17 @@ def main() -> int:
         "prefill_ms_per_step": round(prefill_s * 1e3, 4),
         "prefill_pct_mfma": round(100 * prefill_flops / prefill_s / 1e12 / MFMA_F16_PEAK_TFLOPS, 2),
         "roofline": {"bound": "hbm", "achieved": round(gemv_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(gemv_gbs / HBM_PEAK_GBS, 4), "traffic": None,
-                     "kernel": "q4_gemv_kernel<1,4,false>: 4096x14336 gate tensor, batch 1",
+                     "frac": round(gemv_gbs / HBM_PEAK_GBS, 4),
+                     "traffic": measured_traffic("gemv_gate_up", "q4_gemv"),
+                     "kernel": "q4_gemv_kernel<1,1,2,true,1>: SwiGLU gate/up, two 4096x14336 tensors, batch 1",
                      "bytes_per_launch": gemv_bytes, "avg_us": round(t_gemv * 1e6, 3)},
         "roofline_prefill": {"bound": "mfma", "achieved": round(gemm_tfs, 1), "peak": MFMA_F16_PEAK_TFLOPS,
-                             "unit": "TFLOP/s", "frac": round(gemm_tfs / MFMA_F16_PEAK_TFLOPS, 4), "traffic": None,
-                             "kernel": "q4_gemm_kernel<128,128,2,2,false>: 4096x14336 gate tensor, 512 tokens",
+                             "unit": "TFLOP/s", "frac": round(gemm_tfs / MFMA_F16_PEAK_TFLOPS, 4),
+                             "traffic": measured_traffic("gemm_gate_up", "q4_gemm"),
+                             "kernel": "q4_gemm_kernel<128,128,2,2,true,false>: SwiGLU gate/up, two 4096x14336 "
+                                       "tensors, 512 tokens",
                              "flops_per_launch": gemm_flops, "avg_us": round(t_gemm * 1e6, 2)},
+        "gate_gemv_us": round(t_gate1 * 1e6, 3),
         "pcie_h2d_ceiling_GBps": round(h2d_gbs, 2),
         "streamed": {"host_tensors": host_roles, "host_bytes": host_bytes,
                      "decode_ms": round(st_dec * 1e3, 4), "prefill_ms": round(st_pf * 1e3, 4),
@@ -373,5 +438,88 @@ def cpu_baseline(W, shape, budget_s, layer_bytes):
             "host_cpus": len(os.sched_getaffinity(0))}
 
 
+def summarize(trace_dir: str, fetch_dir: str, write_dir: str, commands: dict) -> None:
+    """Write profiles/kernels_dense_layer_moe_layer.md (per-kernel durations of a
+    full bench run) and profiles/traffic.json + .md (HBM bytes per launch of
+    the two roofline kernels from FETCH_SIZE / WRITE_SIZE, scaled by what the
+    same counters read for a 256 MiB device copy) from rocprofv3 CSV output."""
+    import csv
+    import glob
+
+    def one(pattern):
+        hits = glob.glob(os.path.join(pattern))
+        if not hits:
+            raise FileNotFoundError(pattern)
+        return hits[0]
+
+    prof = os.path.join(ROOT, "profiles")
+    stats = list(csv.DictReader(open(one(os.path.join(trace_dir, "*kernel_stats.csv")))))
+    lines = ["# Kernel durations: dense_layer + moe_layer bench run", "",
+             "Command (from the repository root, on one MI355X):", "",
+             "    " + commands["trace"], "",
+             "| kernel | calls | avg us | min us | max us | share |", "|---|---|---|---|---|---|"]
+    for r in sorted(stats, key=lambda r: -float(r["TotalDurationNs"]))[:24]:
+        lines.append(f"| `{r['Name'][:110]}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
+                     f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} | {float(r['Percentage']):.1f}% |")
+    with open(os.path.join(prof, "kernels_dense_layer_moe_layer.md"), "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+
+    def counter(dirname, name):
+        per = {}
+        for r in csv.DictReader(open(one(os.path.join(dirname, "*counter_collection.csv")))):
+            if r["Counter_Name"] != name:
+                continue
+            per.setdefault(r["Kernel_Name"], {}).setdefault(r["Dispatch_Id"], 0.0)
+            per[r["Kernel_Name"]][r["Dispatch_Id"]] += float(r["Counter_Value"])
+        return {k: sorted(v.values()) for k, v in per.items()}
+
+    def pick(per, needle):
+        ks = [k for k in per if needle in k]
+        if not ks:
+            raise KeyError(needle)
+        vals = per[ks[0]]
+        return ks[0], vals[len(vals) // 2]  # median over dispatches, KiB
+
+    fetch, write = counter(fetch_dir, "FETCH_SIZE"), counter(write_dir, "WRITE_SIZE")
+    copy_bytes = 256 << 20
+    # the device-to-device copy runs as the runtime's copy kernel; its three
+    # 256 MiB dispatches are the largest ones
+    f_copy = sorted(fetch["__amd_rocclr_copyBuffer"])[-2]
+    w_copy = sorted(write["__amd_rocclr_copyBuffer"])[-2]
+    f_scale, w_scale = copy_bytes / (f_copy * 1024), copy_bytes / (w_copy * 1024)
+    out = {"calibration": {"copy_bytes": copy_bytes, "fetch_kib": f_copy, "write_kib": w_copy,
+                           "fetch_scale": round(f_scale, 4), "write_scale": round(w_scale, 4)}}
+    md = ["# HBM traffic of the roofline kernels (FETCH_SIZE, WRITE_SIZE)", "",
+          "Commands (from the repository root, one counter per run):", "",
+          "    " + commands["fetch"], "    " + commands["write"], "",
+          f"Calibration: a {copy_bytes >> 20} MiB device copy reads {f_copy:.0f} KiB (FETCH_SIZE) and writes "
+          f"{w_copy:.0f} KiB (WRITE_SIZE) per dispatch; scale factors {f_scale:.4f} and {w_scale:.4f}.", "",
+          "| kernel | FETCH KiB | WRITE KiB | HBM bytes per launch (scaled) | algorithmic bytes |",
+          "|---|---|---|---|---|"]
+    for key, needle, kind, algo in (("gemv_gate_up", "q4_gemv_kernel<1, 1, 2, true, 1>", "q4_gemv", 66060288),
+                                    ("gemm_gate_up", "q4_gemm_kernel<128, 128, 2, 2, true, false>", "q4_gemm",
+                                     66060288 + 2 * 512 * 4096 + 2 * 512 * 14336)):
+        kname, f = pick(fetch, needle)
+        _, w = pick(write, needle)
+        bytes_ = int(round(f * 1024 * f_scale + w * 1024 * w_scale))
+        out[key] = {"kernel": kname, "fetch_kib": f, "write_kib": w, "hbm_bytes_per_launch": bytes_,
+                    "algorithmic_bytes": algo, "source_sha256_16": kernel_hash(kind)}
+        md.append(f"| `{kname[:90]}` | {f:.0f} | {w:.0f} | {bytes_} | {algo} |")
+    with open(os.path.join(prof, "traffic.json"), "w") as fh:
+        json.dump(out, fh, indent=1)
+    with open(os.path.join(prof, "traffic.md"), "w") as fh:
+        fh.write("\n".join(md) + "\n")
+
+
 if __name__ == "__main__":
+    if len(sys.argv) > 1 and sys.argv[1] == "--summarize":
+        # bench.py --summarize TRACE_DIR FETCH_DIR WRITE_DIR
+        summarize(sys.argv[2], sys.argv[3], sys.argv[4], {
+            "trace": "rocprofv3 --kernel-trace --stats -f csv -d gpurun_out/prof_trace -o bench -- "
+                     "python -u bench.py --no-cpu-baseline",
+            "fetch": "rocprofv3 --pmc FETCH_SIZE -f csv -d gpurun_out/prof_fetch -o f -- "
+                     "python -u bench.py --roofline-only",
+            "write": "rocprofv3 --pmc WRITE_SIZE -f csv -d gpurun_out/prof_write -o w -- "
+                     "python -u bench.py --roofline-only"})
+        sys.exit(0)
     sys.exit(main())

@@ -117,6 +117,15 @@ atsi_status atsi_linear(atsi_ctx* ctx, atsi_tid w, const void* x_f16, int64_t M,
 atsi_status atsi_ffn_swiglu(atsi_ctx* ctx, atsi_tid gate, atsi_tid up, atsi_tid down,
                             const void* x_f16, int64_t M, void* y_f16);
 
+/* The gate/up half of a SwiGLU FFN as one launch:
+ *   h[M][I] = silu(x Wg) * (x Wu)   (fp32 accumulation, one fp16 rounding),
+ * gate and up H x I, x fp16 [M][H], h fp16 [M][I] (caller-owned device
+ * memory, must not alias x).  The kernel atsi_ffn_swiglu and the decoder
+ * layers run for their first half, exposed on its own so that it can be
+ * checked and timed alone. */
+atsi_status atsi_swiglu_gate_up(atsi_ctx* ctx, atsi_tid gate, atsi_tid up, const void* x_f16, int64_t M,
+                                void* h_f16);
+
 /* One pre-norm decoder layer whose projections are all quantised tensors. */
 typedef struct {
   int32_t n_heads, n_kv_heads, head_dim; /* grouped-query heads; n_heads % n_kv_heads == 0 */

@@ -55,6 +55,7 @@ _SIGS = {
     "atsi_set_placement": ([_P, _P, ctypes.c_int32], ctypes.c_int),
     "atsi_linear": ([_P, ctypes.c_int32, _P, ctypes.c_int64, _P], ctypes.c_int),
     "atsi_ffn_swiglu": ([_P, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _P, ctypes.c_int64, _P], ctypes.c_int),
+    "atsi_swiglu_gate_up": ([_P, ctypes.c_int32, ctypes.c_int32, _P, ctypes.c_int64, _P], ctypes.c_int),
     "atsi_decoder_layer": ([_P, ctypes.POINTER(atsi_dense_layer), _P, ctypes.c_int64, _P, _P], ctypes.c_int),
     "atsi_moe_ffn": ([_P, ctypes.POINTER(atsi_moe), _P, ctypes.c_int64, _P, ctypes.POINTER(atsi_moe_debug)],
                      ctypes.c_int),
@@ -126,6 +127,10 @@ def atsi_linear(ctx: int, w: int, x: int, M: int, y: int) -> None:
 
 def atsi_ffn_swiglu(ctx: int, gate: int, up: int, down: int, x: int, M: int, y: int) -> None:
     _check(ctx, lib().atsi_ffn_swiglu(ctx, gate, up, down, x, M, y))
+
+
+def atsi_swiglu_gate_up(ctx: int, gate: int, up: int, x: int, M: int, h: int) -> None:
+    _check(ctx, lib().atsi_swiglu_gate_up(ctx, gate, up, x, M, h))
 
 
 def atsi_decoder_layer(ctx: int, layer: atsi_dense_layer, h: int, M: int, q_out: int = 0, k_out: int = 0) -> None:

@@ -735,6 +735,23 @@ atsi_status atsi_ffn_swiglu(atsi_ctx* c, atsi_tid gate, atsi_tid up, atsi_tid do
   return run_op(c, dn, &order[2], 1);
 }
 
+atsi_status atsi_swiglu_gate_up(atsi_ctx* c, atsi_tid gate, atsi_tid up, const void* x, int64_t M, void* h) {
+  if (!c) return ATSI_E_INVALID;
+  atsi_status st;
+  if ((st = check_act(c, x, "x")) || (st = check_act(c, h, "h")) || (st = check_m(c, M)) ||
+      (st = check_tid(c, gate)) || (st = check_tid(c, up)))
+    return st;
+  const Tensor &tg = c->tensors[gate], &tu = c->tensors[up];
+  if (tg.K != tu.K || tg.N != tu.N) return fail(c, ATSI_E_SHAPE, "gate and up must have the same shape");
+  if (x == h) return fail(c, ATSI_E_INVALID, "h must not alias x");
+  if ((st = enter(c))) return st;
+  const atsi_tid order[2] = {gate, up};
+  if ((st = prefetch_call(c, order, 2))) return st;
+  LinOp gu = plain_op(QView{nullptr, nullptr, (int)tg.K, (int)tg.N}, (const __half*)x, (int)M, (__half*)h);
+  gu.swiglu = 1;
+  return run_op(c, gu, order, 2);
+}
+
 atsi_status atsi_decoder_layer(atsi_ctx* c, const atsi_dense_layer* L, void* h, int64_t M, void* q_out,
                                void* k_out) {
   if (!c) return ATSI_E_INVALID;

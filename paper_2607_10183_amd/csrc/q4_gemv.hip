@@ -13,7 +13,9 @@
 //   * steps alternate between two register buffers: the next step's codes and
 //     scales are loaded (unconditionally, rows and groups clamped, so the
 //     compiler counts outstanding loads exactly) before the current step is
-//     computed, keeping a step of loads in flight per wave;
+//     computed, keeping a step of loads in flight per wave; steps per wave
+//     are a compile-time constant, so no load is issued past a wave's last
+//     step (those rows belong to the next workgroup and would be read twice);
 //   * arithmetic per group: four ALU ops make eight fp16 weights-plus-offset
 //     values, v_dot2_f32_f16 accumulates exact products in fp32, one FMA
 //     removes the offset and one applies the fp16 scale (q4_gemv_core.h);
@@ -110,8 +112,8 @@ __device__ __forceinline__ void load_step(Step<RW, CPL, SWI>& st, const QView& w
 #pragma unroll
       for (int j = 0; j < CPL; ++j) {
         const int c = min(lane + j * kWave, nchunk - 1);  // groups past the row end are not used
-        st.c[t][r][j] = *reinterpret_cast<const uint4*>(cr + (size_t)c * 16);
-        st.s[t][r][j] = sr[c];
+        st.c[t][r][j] = ldg16(cr + (size_t)c * 16);
+        st.s[t][r][j] = ldg2(sr + c);
       }
     }
   }
@@ -188,7 +190,7 @@ __device__ __forceinline__ void compute_step(const Step<RW, CPL, SWI>& cur, cons
     }
 }
 
-template <int MT, int RW, int CPL, bool SWI>
+template <int MT, int RW, int CPL, bool SWI, int SPW>
 __global__ __launch_bounds__(kBlock) void q4_gemv_kernel(LinOp op, BlockMap bm) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   int s = 0;
@@ -203,13 +205,12 @@ __global__ __launch_bounds__(kBlock) void q4_gemv_kernel(LinOp op, BlockMap bm) 
   const int wave = threadIdx.x / kWave;
   constexpr int NW = kBlock / kWave;
   const int blk_row0 = local * bm.rows_per_block;
-  const int spw = bm.rows_per_block / (NW * RW);  // steps per wave
   // step i of this wave covers rows blk_row0 + (i * NW + wave) * RW + [0, RW)
   auto step_row = [&](int i) { return blk_row0 + (i * NW + wave) * RW; };
 
   // weight loads of the first step go out before the activations are staged
-  Step<RW, CPL, SWI> A, B;
-  load_step(A, w, w2, step_row(0), lane, nchunk);
+  Step<RW, CPL, SWI> buf[2];
+  load_step(buf[0], w, w2, step_row(0), lane, nchunk);
 
   GemvCtx<MT> gc;
   stage_x<MT>(smem, op.x, K, M, op.norm != 0, gc.inv_r, op.eps);
@@ -218,20 +219,18 @@ __global__ __launch_bounds__(kBlock) void q4_gemv_kernel(LinOp op, BlockMap bm) 
   gc.nchunk = nchunk;
   gc.lane = lane;
 
-  for (int i = 0; i < spw; i += 2) {
-    if (step_row(i) >= w.N) break;
-    load_step(B, w, w2, step_row(i + 1), lane, nchunk);  // past the end: clamped, harmless
-    compute_step(A, gc, op, sg, s, step_row(i), M, w.N);
-    if (i + 1 >= spw || step_row(i + 1) >= w.N) break;
-    load_step(A, w, w2, step_row(i + 2), lane, nchunk);
-    compute_step(B, gc, op, sg, s, step_row(i + 1), M, w.N);
+  // the next step's loads go out before the current step is computed
+#pragma unroll
+  for (int i = 0; i < SPW; ++i) {
+    if (i + 1 < SPW) load_step(buf[(i + 1) & 1], w, w2, step_row(i + 1), lane, nchunk);
+    if (step_row(i) < w.N) compute_step(buf[i & 1], gc, op, sg, s, step_row(i), M, w.N);
   }
 }
 
-template <int MT, int RW, int CPL, bool SWI>
-hipError_t launch_cfg(const LinOp& op, int spw, hipStream_t st) {
+template <int MT, int RW, int CPL, bool SWI, int SPW>
+hipError_t launch_cfg(const LinOp& op, hipStream_t st) {
   BlockMap bm{};
-  bm.rows_per_block = (kBlock / kWave) * RW * spw;
+  bm.rows_per_block = (kBlock / kWave) * RW * SPW;
   int total = 0;
   for (int s = 0; s < op.nseg; ++s) {
     total += (op.seg[s].w.N + bm.rows_per_block - 1) / bm.rows_per_block;
@@ -240,22 +239,26 @@ hipError_t launch_cfg(const LinOp& op, int spw, hipStream_t st) {
   const int nchunk = op.K / kGroup;
   const size_t lds = (size_t)4 * MT * nchunk * 16 + (size_t)MT * nchunk * 4;
   if (lds > kGemvMaxLds) return hipErrorInvalidValue;  // callers check gemv_supported()
-  hipLaunchKernelGGL((q4_gemv_kernel<MT, RW, CPL, SWI>), dim3(total), dim3(kBlock), lds, st, op, bm);
+  hipLaunchKernelGGL((q4_gemv_kernel<MT, RW, CPL, SWI, SPW>), dim3(total), dim3(kBlock), lds, st, op, bm);
   return hipGetLastError();
 }
 
-// Groups per lane (CPL) follow K; one row per step.  Steps per wave were
-// chosen by measurement on MI355X: two (four for the fused gate/up pair of a
-// wide FFN) pipeline well while keeping enough workgroups per CU.
+template <int MT, int RW, int CPL, bool SWI>
+hipError_t launch_spw(const LinOp& op, int spw, hipStream_t st) {
+  if (spw >= 2) return launch_cfg<MT, RW, CPL, SWI, 2>(op, st);
+  return launch_cfg<MT, RW, CPL, SWI, 1>(op, st);
+}
+
+// Groups per lane (CPL) follow K; one row per step.
 template <int MT, bool SWI>
 hipError_t launch_mt(const LinOp& op, int spw, hipStream_t st) {
   const int nchunk = op.K / kGroup;
-  if (nchunk <= 64) return launch_cfg<MT, 1, 1, SWI>(op, spw, st);
-  if (nchunk <= 128) return launch_cfg<MT, 1, 2, SWI>(op, spw, st);
-  if (nchunk <= 256) return launch_cfg<MT, 1, 4, SWI>(op, spw, st);
-  if (nchunk <= 448) return launch_cfg<MT, 1, 7, SWI>(op, spw, st);
-  if (nchunk <= 512) return launch_cfg<MT, 1, 8, SWI>(op, spw, st);
-  return launch_cfg<MT, 1, 16, SWI>(op, spw, st);
+  if (nchunk <= 64) return launch_spw<MT, 1, 1, SWI>(op, spw, st);
+  if (nchunk <= 128) return launch_spw<MT, 1, 2, SWI>(op, spw, st);
+  if (nchunk <= 256) return launch_spw<MT, 1, 4, SWI>(op, spw, st);
+  if (nchunk <= 448) return launch_spw<MT, 1, 7, SWI>(op, spw, st);
+  if (nchunk <= 512) return launch_spw<MT, 1, 8, SWI>(op, spw, st);
+  return launch_spw<MT, 1, 16, SWI>(op, spw, st);
 }
 
 template <bool SWI>
@@ -265,10 +268,13 @@ hipError_t launch_sw(const LinOp& op, int spw, hipStream_t st) {
   return launch_mt<4, SWI>(op, spw, st);
 }
 
+// Steps per wave, measured on MI355X (batch 1): two for plain tensors of
+// 2048+ rows; one for the fused gate/up pair (each step already covers a row
+// of both tensors) and for small tensors, where the grid would be too small.
 int default_spw(const LinOp& op) {
   int n = 0;
   for (int s = 0; s < op.nseg; ++s) n += op.seg[s].w.N;
-  if (op.swiglu && n >= 8192) return 4;
+  if (op.swiglu) return 1;
   return n >= 2048 ? 2 : 1;
 }
 

@@ -136,6 +136,18 @@ class Session:
         self._torch_waits()
         return y
 
+    def gate_up(self, gate: int, up: int, x: torch.Tensor, h: torch.Tensor | None = None) -> torch.Tensor:
+        """h = silu(x Wg) * (x Wu), one launch."""
+        H, I = self.shapes[gate]
+        M = x.numel() // H
+        if h is None:
+            with torch.cuda.stream(self.cs):
+                h = torch.empty((M, I), dtype=torch.float16, device=self.device)
+        self._wait_torch()
+        atsi.atsi_swiglu_gate_up(self.ctx, gate, up, x.data_ptr(), M, h.data_ptr())
+        self._torch_waits()
+        return h
+
     def decoder_layer(self, tids: dict, h: torch.Tensor, n_heads: int, n_kv: int, head_dim: int,
                       eps: float = 1e-6, q_out: torch.Tensor | None = None, k_out: torch.Tensor | None = None):
         """In-place pre-norm decoder layer on h[M][H]; tids maps q,k,v,o,gate,up,down to tensor ids."""

@@ -42,6 +42,22 @@ def test_ffn_swiglu_parity(sess, H, I, M):
     check(y, ref, zeta, name=f"ffn H={H} I={I} M={M}")
 
 
+@pytest.mark.parametrize("H,I,M", [(256, 96, 1), (4096, 14336, 1), (4096, 14336, 3), (512, 160, 77),
+                                   (4096, 14336, 512)])
+def test_swiglu_gate_up_parity(sess, H, I, M):
+    """h = silu(x Wg) * (x Wu) from the fused launch against the oracle."""
+    gate, up = _qt(75, H + 1, I, H), _qt(75, H + 2, I, H)
+    tg = sess.register(*gate)
+    tu = sess.register(*up)
+    xn = synth.activations(75, M, M, H)
+    h = sess.gate_up(tg, tu, _dev(xn)).cpu().numpy()
+    sess.sync()
+    g, zg = oracle.linear(xn, *gate)
+    u, zu = oracle.linear(xn, *up)
+    ref, zeta = oracle.swiglu(g, u, zg, zu)
+    check(h, ref, zeta, name=f"gate/up H={H} I={I} M={M}")
+
+
 def _layer_weights(shape, seed, layer=0):
     return {r: _qt(seed, configs.dense_uid(layer, r), shape.kn(r)[1], shape.kn(r)[0]) for r in configs.ROLES}
 
