@@ -117,6 +117,12 @@ atsi_status atsi_linear(atsi_ctx* ctx, atsi_tid w, const void* x_f16, int64_t M,
 atsi_status atsi_ffn_swiglu(atsi_ctx* ctx, atsi_tid gate, atsi_tid up, atsi_tid down,
                             const void* x_f16, int64_t M, void* y_f16);
 
+/* RMS normalisation with unit gain: y[t] = x[t] / sqrt(mean_k x[t][k]^2 + eps)
+ * for fp16 x, y [M][H] (device, 16-byte aligned, H % 8 == 0), fp32
+ * arithmetic and one fp16 rounding; y may alias x.  The glue between the
+ * layers of a stack whose hidden state is renormalised after every layer. */
+atsi_status atsi_rmsnorm(atsi_ctx* ctx, const void* x_f16, int64_t M, int64_t H, float eps, void* y_f16);
+
 /* The gate/up half of a SwiGLU FFN as one launch:
  *   h[M][I] = silu(x Wg) * (x Wu)   (fp32 accumulation, one fp16 rounding),
  * gate and up H x I, x fp16 [M][H], h fp16 [M][I] (caller-owned device
@@ -131,9 +137,15 @@ typedef struct {
   int32_t n_heads, n_kv_heads, head_dim; /* grouped-query heads; n_heads % n_kv_heads == 0 */
   float eps;                             /* RMS-norm epsilon (unit gain) */
   atsi_tid q, k, v, o, gate, up, down;   /* Q/K/V: H x heads*dim, O: heads*dim x H, FFN as above */
+  int32_t renorm_out;                    /* 1: h_out = rms(h + attn + FFN) (see below), 0: plain */
 } atsi_dense_layer;
 
 /* h <- h + attn(rms(h)) Wo;  h <- h + FFN(rms(h)), in place on h[M][H].
+ * With layer->renorm_out = 1 the layer's output is renormalised as well,
+ * h <- rms(h + FFN(rms(h))), for stacks whose hidden state is renormalised
+ * between layers: the residual sum is kept in fp32 (the FFN output of a
+ * layer alone can approach the fp16 range) and only the normalised state is
+ * rounded to fp16 (one more launch).
  * Attention is evaluated at context length 1 (each token attends only to
  * itself, so query head i outputs the value of KV head i / (n_heads /
  * n_kv_heads)); the Q and K projections are still computed and written to
@@ -195,6 +207,26 @@ typedef struct {
  * combine.  1 <= M <= 65536.  dbg may be NULL. */
 atsi_status atsi_moe_ffn(atsi_ctx* ctx, const atsi_moe* moe, const void* x_f16, int64_t M, void* y_f16,
                          const atsi_moe_debug* dbg);
+
+/* One pre-norm decoder layer whose FFN is the routed MoE above (the layers
+ * of the MoE models of Sec. 5, e.g. a 235B-A22B stack):
+ *   q, k, v = rms(h) Wq, Wk, Wv;  h += attn Wo   (as atsi_decoder_layer)
+ *   h += MoE(rms(h))                              (as atsi_moe_ffn)
+ * with rms(v) = v / sqrt(mean(v^2) + eps).  The norm is not materialised:
+ * its per-token factor scales the router logits (before the bias) and the
+ * expert gate/up products in fp32, and the combine adds the residual, so h
+ * (fp16 [M][hidden], device) is updated in place.  q_out / k_out as in
+ * atsi_decoder_layer; dbg as in atsi_moe_ffn.  moe->hidden must equal the
+ * attention hidden size. */
+typedef struct {
+  int32_t n_heads, n_kv_heads, head_dim;
+  float eps;
+  atsi_tid q, k, v, o;
+  const atsi_moe* moe;
+} atsi_moe_layer;
+
+atsi_status atsi_moe_decoder_layer(atsi_ctx* ctx, const atsi_moe_layer* layer, void* h_f16, int64_t M,
+                                   void* q_out_f16, void* k_out_f16, const atsi_moe_debug* dbg);
 
 /* Token-to-expert bucketing alone (the same kernel atsi_moe_ffn uses), from
  * device idx int32 [M][k] with ids in [0, n_experts): counts [E], offsets

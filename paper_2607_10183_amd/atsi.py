@@ -32,7 +32,8 @@ class atsi_qtensor(ctypes.Structure):
 class atsi_dense_layer(ctypes.Structure):
     _fields_ = [("n_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
                 ("eps", ctypes.c_float), ("q", ctypes.c_int32), ("k", ctypes.c_int32), ("v", ctypes.c_int32),
-                ("o", ctypes.c_int32), ("gate", ctypes.c_int32), ("up", ctypes.c_int32), ("down", ctypes.c_int32)]
+                ("o", ctypes.c_int32), ("gate", ctypes.c_int32), ("up", ctypes.c_int32), ("down", ctypes.c_int32),
+                ("renorm_out", ctypes.c_int32)]
 
 
 class atsi_moe(ctypes.Structure):
@@ -46,6 +47,12 @@ class atsi_moe_debug(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in ("logits", "idx", "p", "counts", "offsets", "perm", "inv_perm")]
 
 
+class atsi_moe_layer(ctypes.Structure):
+    _fields_ = [("n_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("eps", ctypes.c_float), ("q", ctypes.c_int32), ("k", ctypes.c_int32), ("v", ctypes.c_int32),
+                ("o", ctypes.c_int32), ("moe", ctypes.POINTER(atsi_moe))]
+
+
 _P = ctypes.c_void_p
 _SIGS = {
     "atsi_create": ([ctypes.c_int, _P, _P, _P, ctypes.c_size_t, ctypes.c_int, ctypes.POINTER(_P)], ctypes.c_int),
@@ -56,9 +63,12 @@ _SIGS = {
     "atsi_linear": ([_P, ctypes.c_int32, _P, ctypes.c_int64, _P], ctypes.c_int),
     "atsi_ffn_swiglu": ([_P, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _P, ctypes.c_int64, _P], ctypes.c_int),
     "atsi_swiglu_gate_up": ([_P, ctypes.c_int32, ctypes.c_int32, _P, ctypes.c_int64, _P], ctypes.c_int),
+    "atsi_rmsnorm": ([_P, _P, ctypes.c_int64, ctypes.c_int64, ctypes.c_float, _P], ctypes.c_int),
     "atsi_decoder_layer": ([_P, ctypes.POINTER(atsi_dense_layer), _P, ctypes.c_int64, _P, _P], ctypes.c_int),
     "atsi_moe_ffn": ([_P, ctypes.POINTER(atsi_moe), _P, ctypes.c_int64, _P, ctypes.POINTER(atsi_moe_debug)],
                      ctypes.c_int),
+    "atsi_moe_decoder_layer": ([_P, ctypes.POINTER(atsi_moe_layer), _P, ctypes.c_int64, _P, _P,
+                                ctypes.POINTER(atsi_moe_debug)], ctypes.c_int),
     "atsi_moe_bucket": ([_P, _P, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, _P, _P, _P, _P], ctypes.c_int),
     "atsi_set_schedule": ([_P, _P, ctypes.c_int32], ctypes.c_int),
     "atsi_prefetch": ([_P, ctypes.c_int32], ctypes.c_int),
@@ -129,6 +139,10 @@ def atsi_ffn_swiglu(ctx: int, gate: int, up: int, down: int, x: int, M: int, y: 
     _check(ctx, lib().atsi_ffn_swiglu(ctx, gate, up, down, x, M, y))
 
 
+def atsi_rmsnorm(ctx: int, x: int, M: int, H: int, eps: float, y: int) -> None:
+    _check(ctx, lib().atsi_rmsnorm(ctx, x, M, H, eps, y))
+
+
 def atsi_swiglu_gate_up(ctx: int, gate: int, up: int, x: int, M: int, h: int) -> None:
     _check(ctx, lib().atsi_swiglu_gate_up(ctx, gate, up, x, M, h))
 
@@ -139,6 +153,12 @@ def atsi_decoder_layer(ctx: int, layer: atsi_dense_layer, h: int, M: int, q_out:
 
 def atsi_moe_ffn(ctx: int, moe: atsi_moe, x: int, M: int, y: int, dbg: atsi_moe_debug | None = None) -> None:
     _check(ctx, lib().atsi_moe_ffn(ctx, ctypes.byref(moe), x, M, y, ctypes.byref(dbg) if dbg is not None else None))
+
+
+def atsi_moe_decoder_layer(ctx: int, layer: atsi_moe_layer, h: int, M: int, q_out: int = 0, k_out: int = 0,
+                           dbg: atsi_moe_debug | None = None) -> None:
+    _check(ctx, lib().atsi_moe_decoder_layer(ctx, ctypes.byref(layer), h, M, q_out or None, k_out or None,
+                                              ctypes.byref(dbg) if dbg is not None else None))
 
 
 def atsi_moe_bucket(ctx: int, idx: int, M: int, k: int, n_experts: int, counts: int, offsets: int, perm: int,

@@ -550,6 +550,173 @@ atsi_status check_m(atsi_ctx* c, int64_t M) {
   return ATSI_OK;
 }
 
+// Attention half of a pre-norm decoder layer (tensors ids[0..3] = q, k, v, o):
+//   1. q, k, v = rms(h) Wq, Wk, Wv in one launch; v goes straight to the
+//      attention output of every query head of its group (context length 1);
+//   2. h = h + attn Wo.
+atsi_status run_attention(atsi_ctx* c, const atsi_tid* ids, int n_heads, int n_kv, int head_dim, float eps,
+                          __half* hh, int Mi, __half* qb, __half* kb, __half* oin) {
+  const Tensor &tq = c->tensors[ids[0]], &tk = c->tensors[ids[1]], &to = c->tensors[ids[3]];
+  atsi_status st;
+  LinOp a{};
+  a.nseg = 3;
+  a.x = hh; a.M = Mi; a.K = (int)tq.K; a.norm = 1; a.eps = eps; a.head_dim = head_dim;
+  a.seg[0] = Seg{QView{}, QView{}, qb, (int)tq.N, 1};
+  a.seg[1] = Seg{QView{}, QView{}, kb, (int)tk.N, 1};
+  a.seg[2] = Seg{QView{}, QView{}, oin, (int)tq.N, n_heads / n_kv};
+  if ((st = run_op(c, a, ids, 3))) return st;
+  LinOp o = plain_op(QView{nullptr, nullptr, (int)to.K, (int)to.N}, oin, Mi, hh);
+  o.res = hh;
+  return run_op(c, o, &ids[3], 1);
+}
+
+// Shapes of the attention tensors of a layer with hidden H.
+atsi_status check_attention(atsi_ctx* c, const atsi_tid* ids, int n_heads, int n_kv, int head_dim, float eps) {
+  atsi_status st;
+  for (int i = 0; i < 4; ++i)
+    if ((st = check_tid(c, ids[i]))) return st;
+  if (n_heads < 1 || n_kv < 1 || head_dim < 1 || n_heads % n_kv != 0 || !(eps >= 0.f))
+    return fail(c, ATSI_E_SHAPE, "heads %d / kv heads %d / head_dim %d / eps invalid", n_heads, n_kv, head_dim);
+  const Tensor &tq = c->tensors[ids[0]], &tk = c->tensors[ids[1]], &tv = c->tensors[ids[2]], &to = c->tensors[ids[3]];
+  const int64_t H = tq.K, Hq = (int64_t)n_heads * head_dim, Hkv = (int64_t)n_kv * head_dim;
+  if (tq.N != Hq || tk.K != H || tv.K != H || tk.N != Hkv || tv.N != Hkv || to.K != Hq || to.N != H)
+    return fail(c, ATSI_E_SHAPE, "attention tensor shapes do not match hidden %lld, heads %d x %d", (long long)H,
+                n_heads, head_dim);
+  return ATSI_OK;
+}
+
+// Validate an MoE descriptor and its experts' shapes.
+atsi_status check_moe(atsi_ctx* c, const atsi_moe* m) {
+  if (!m) return fail(c, ATSI_E_INVALID, "moe descriptor is NULL");
+  const int E = m->n_experts, k = m->top_k;
+  if (E < 16 || E > kMaxExperts || E % 16 != 0 || k < 1 || k > kMaxTopK || k > E)
+    return fail(c, ATSI_E_SHAPE, "n_experts %d (multiple of 16, <= %d) / top_k %d (1..16) unsupported", E,
+                kMaxExperts, k);
+  if (m->hidden < 32 || m->hidden % 32 || m->inter < 32 || m->inter % 32)
+    return fail(c, ATSI_E_SHAPE, "hidden %lld / inter %lld must be positive multiples of 32", (long long)m->hidden,
+                (long long)m->inter);
+  if (!m->router_w_f16 || !aligned16(m->router_w_f16) || !m->gate || !m->up || !m->down)
+    return fail(c, ATSI_E_INVALID, "router weights (16-byte aligned) and expert id arrays are required");
+  const int H = (int)m->hidden, I = (int)m->inter;
+  atsi_status st;
+  for (int e = 0; e < E; ++e) {
+    if ((st = check_tid(c, m->gate[e])) || (st = check_tid(c, m->up[e])) || (st = check_tid(c, m->down[e]))) return st;
+    const Tensor &g = c->tensors[m->gate[e]], &u = c->tensors[m->up[e]], &d = c->tensors[m->down[e]];
+    if (g.K != H || g.N != I || u.K != H || u.N != I || d.K != I || d.N != H)
+      return fail(c, ATSI_E_SHAPE, "expert %d: gate/up must be %d x %d and down %d x %d", e, H, I, I, H);
+  }
+  return ATSI_OK;
+}
+
+// The routed MoE FFN (validated descriptor): y = sum_j p_j FFN_{e_j}(x) for
+// each token, plus res when res is given (y may then alias res but not x);
+// with inv_r the input is x * inv_r[t] per token, the factor applied to the
+// router logits and the expert gate/up products.
+atsi_status run_moe(atsi_ctx* c, const atsi_moe* m, const __half* x, int Mi, __half* y, const atsi_moe_debug* dbg,
+                    const float* inv_r, const __half* res, Scratch& sc) {
+  atsi_status st;
+  atsi_ctx::MoeTable* tb;
+  if ((st = get_table(c, m, &tb))) return st;
+  const int E = m->n_experts, k = m->top_k;
+  const int H = (int)m->hidden, I = (int)m->inter;
+  const int Mk = Mi * k;
+  const bool gemv = Mi <= 4;
+  const int bm = expert_tile_rows(gemv);
+  float* part = (float*)sc.take(router_partial_floats(Mi, H, E), 4);
+  int32_t* idx = dbg && dbg->idx ? dbg->idx : (int32_t*)sc.take(Mk, 4);
+  float* p = dbg && dbg->p ? dbg->p : (float*)sc.take(Mk, 4);
+  int32_t* counts = dbg && dbg->counts ? dbg->counts : (int32_t*)sc.take(E, 4);
+  int32_t* offsets = dbg && dbg->offsets ? dbg->offsets : (int32_t*)sc.take(E + 1, 4);
+  int32_t* perm = dbg && dbg->perm ? dbg->perm : (int32_t*)sc.take(Mk, 4);
+  int32_t* inv = dbg && dbg->inv_perm ? dbg->inv_perm : (int32_t*)sc.take(Mk, 4);
+  int32_t* order = (int32_t*)sc.take(E, 4);
+  int32_t* tiles = (int32_t*)sc.take(2 * ((size_t)Mk / bm + E + 1), 4);
+  int32_t* ntiles = (int32_t*)sc.take(1, 4);
+  __half* h = sc.take((size_t)Mk * I);
+  __half* out = sc.take((size_t)Mk * H);
+  if (!part || !idx || !p || !counts || !offsets || !perm || !inv || !order || !tiles || !ntiles || !h || !out)
+    return fail(c, ATSI_E_WORKSPACE, "scratch too small for a %d-token MoE layer", Mi);
+  const ExpertW* table = reinterpret_cast<const ExpertW*>(c->ws + tb->off);
+  const uint8_t* resident = reinterpret_cast<const uint8_t*>(c->ws + tb->off + align_up((size_t)E * sizeof(ExpertW)));
+
+  hipError_t e = launch_router(x, inv_r, (const __half*)m->router_w_f16, m->router_bias, Mi, H, E, k, part, idx, p,
+                               dbg ? dbg->logits : nullptr, c->cs);
+  if (e != hipSuccess) return hip_fail(c, e, "router launch");
+  e = launch_bucket(idx, Mi, k, E, resident, bm, counts, offsets, perm, inv, order, tiles, ntiles, c->cs);
+  if (e != hipSuccess) return hip_fail(c, e, "bucket launch");
+  if (tb->n_streamed > 0) {
+    HIP_TRY(c, hipMemcpyAsync(c->pinned, counts, E * sizeof(int32_t), hipMemcpyDeviceToHost, c->cs));
+    HIP_TRY(c, hipEventRecord(c->counts_ev, c->cs));
+  }
+  MoeArgs a{};
+  a.table = table;
+  a.tiles = tiles;
+  a.n_tiles = ntiles;
+  a.counts = counts;
+  a.offsets = offsets;
+  a.perm = perm;
+  a.x = x;
+  a.h = h;
+  a.out = out;
+  a.inv_r = inv_r;
+  a.k = k;
+  a.H = H;
+  a.I = I;
+  // HBM-resident experts first: they run while the host learns which
+  // streamed experts are needed.
+  const int bound = bm == 1 ? Mk : Mk / bm + std::min(E, Mk);
+  if ((e = launch_expert_gateup(a, bound, gemv, c->cs)) != hipSuccess) return hip_fail(c, e, "expert gate/up launch");
+  if ((e = launch_expert_down(a, bound, gemv, c->cs)) != hipSuccess) return hip_fail(c, e, "expert down launch");
+
+  if (tb->n_streamed > 0) {
+    HIP_TRY(c, hipEventSynchronize(c->counts_ev));
+    std::vector<int> act;
+    for (int ex = 0; ex < E; ++ex) {
+      const Tensor &g = c->tensors[m->gate[ex]], &u = c->tensors[m->up[ex]], &d = c->tensors[m->down[ex]];
+      if ((g.on_host || u.on_host || d.on_host) && c->pinned[ex] > 0) act.push_back(ex);
+    }
+    std::stable_sort(act.begin(), act.end(), [&](int l, int r) { return c->pinned[l] > c->pinned[r]; });
+    for (int ex : act)
+      for (const atsi_tid t : {m->gate[ex], m->up[ex], m->down[ex]})
+        if (c->tensors[t].on_host) c->queue.push_back(t);
+    if ((st = topup(c))) return st;
+    const int B = std::max(1, std::min(kBatchExp, c->n_slots / 3));
+    for (size_t b0 = 0; b0 < act.size(); b0 += B) {
+      std::vector<int> held;
+      MoeArgs ba = a;
+      ba.nb = 0;
+      const int nbx = (int)std::min<size_t>(B, act.size() - b0);
+      for (int b = 0; b < nbx; ++b) {
+        const int ex = act[b0 + b];
+        ba.bexp[b] = ex;
+        if ((st = acquire(c, m->gate[ex], &ba.bw[b].gate, held)) || (st = acquire(c, m->up[ex], &ba.bw[b].up, held)) ||
+            (st = acquire(c, m->down[ex], &ba.bw[b].down, held)))
+          return st;
+      }
+      auto flush = [&]() -> atsi_status {
+        if (ba.nb == 0) return ATSI_OK;
+        hipError_t fe = launch_expert_gateup(ba, ba.nb, gemv, c->cs);
+        if (fe == hipSuccess) fe = launch_expert_down(ba, ba.nb, gemv, c->cs);
+        if (fe != hipSuccess) return hip_fail(c, fe, "streamed expert launch");
+        ba.nb = 0;
+        return ATSI_OK;
+      };
+      for (int b = 0; b < nbx; ++b) {
+        const int cnt = c->pinned[act[b0 + b]];
+        for (int r0 = 0; r0 < cnt; r0 += bm) {
+          if (ba.nb == kBatchTiles && (st = flush())) return st;
+          ba.btiles[ba.nb++] = make_int2(b, r0);
+        }
+      }
+      if ((st = flush())) return st;
+      if ((st = release(c, held))) return st;
+    }
+  }
+  e = launch_combine(out, p, Mi, k, H, res, y, c->cs);
+  if (e != hipSuccess) return hip_fail(c, e, "combine launch");
+  return ATSI_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -618,11 +785,11 @@ atsi_status atsi_destroy(atsi_ctx* c) {
   if (c->cs) (void)hipStreamSynchronize(c->cs);
   if (c->ts) (void)hipStreamSynchronize(c->ts);
   for (Slot& s : c->slots) {
-    if (s.ready) hipEventDestroy(s.ready);
-    if (s.free) hipEventDestroy(s.free);
+    if (s.ready) (void)hipEventDestroy(s.ready);
+    if (s.free) (void)hipEventDestroy(s.free);
   }
-  if (c->counts_ev) hipEventDestroy(c->counts_ev);
-  if (c->pinned) hipHostFree(c->pinned);
+  if (c->counts_ev) (void)hipEventDestroy(c->counts_ev);
+  if (c->pinned) (void)hipHostFree(c->pinned);
   delete c;
   return ATSI_OK;
 }
@@ -763,31 +930,28 @@ atsi_status atsi_decoder_layer(atsi_ctx* c, const atsi_dense_layer* L, void* h, 
   const atsi_tid ids[7] = {L->q, L->k, L->v, L->o, L->gate, L->up, L->down};
   for (atsi_tid t : ids)
     if ((st = check_tid(c, t))) return st;
-  const Tensor &tq = c->tensors[L->q], &tk = c->tensors[L->k], &tv = c->tensors[L->v], &to = c->tensors[L->o];
+  if ((st = check_attention(c, ids, L->n_heads, L->n_kv_heads, L->head_dim, L->eps))) return st;
+  const Tensor &tq = c->tensors[L->q];
   const Tensor &tg = c->tensors[L->gate], &tu = c->tensors[L->up], &td = c->tensors[L->down];
   const int64_t H = tq.K;
-  if (L->n_heads < 1 || L->n_kv_heads < 1 || L->head_dim < 1 || L->n_heads % L->n_kv_heads != 0 ||
-      !(L->eps >= 0.f))
-    return fail(c, ATSI_E_SHAPE, "heads %d / kv heads %d / head_dim %d / eps invalid", L->n_heads, L->n_kv_heads,
-                L->head_dim);
   const int64_t Hq = (int64_t)L->n_heads * L->head_dim, Hkv = (int64_t)L->n_kv_heads * L->head_dim;
-  if (tq.N != Hq || tk.K != H || tv.K != H || tk.N != Hkv || tv.N != Hkv || to.K != Hq || to.N != H ||
-      tg.K != H || tu.K != H || tg.N != tu.N || td.K != tg.N || td.N != H)
-    return fail(c, ATSI_E_SHAPE, "decoder layer tensor shapes do not match hidden %lld, heads %d x %d",
-                (long long)H, L->n_heads, L->head_dim);
+  if (tg.K != H || tu.K != H || tg.N != tu.N || td.K != tg.N || td.N != H)
+    return fail(c, ATSI_E_SHAPE, "decoder layer FFN shapes do not match hidden %lld", (long long)H);
   if ((st = enter(c))) return st;
   Scratch sc(c);
   __half* qb = q_out ? (__half*)q_out : sc.take((size_t)M * Hq);
   __half* kb = k_out ? (__half*)k_out : sc.take((size_t)M * Hkv);
   __half* oin = sc.take((size_t)M * Hq);
   __half* hf = sc.take((size_t)M * tg.N);
-  if (!qb || !kb || !oin || !hf) return fail(c, ATSI_E_WORKSPACE, "scratch too small for a %lld-token layer", (long long)M);
+  float* y32 = L->renorm_out ? (float*)sc.take((size_t)M * H, 4) : nullptr;
+  if (!qb || !kb || !oin || !hf || (L->renorm_out && !y32))
+    return fail(c, ATSI_E_WORKSPACE, "scratch too small for a %lld-token layer", (long long)M);
   __half* hh = (__half*)h;
   const int Mi = (int)M;
   const float eps = L->eps;
   bool resident = true;
   for (atsi_tid t : ids) resident = resident && !c->tensors[t].on_host;
-  if (kFusedDecodeLayer && Mi == 1 && resident) {
+  if (kFusedDecodeLayer && Mi == 1 && resident && !L->renorm_out) {
     // batch-1 decode with every weight in HBM: one fused launch
     LayerArgs la{};
     for (int i = 0; i < kLayerTensors; ++i) {
@@ -818,28 +982,67 @@ atsi_status atsi_decoder_layer(atsi_ctx* c, const atsi_dense_layer* L, void* h, 
     }
   }
   if ((st = prefetch_call(c, ids, 7))) return st;
-
-  // 1. q, k, v = rms(h) Wq, Wk, Wv in one launch; v goes straight to the
-  //    attention output of every query head of its group (context length 1)
-  LinOp a{};
-  a.nseg = 3;
-  a.x = hh; a.M = Mi; a.K = (int)H; a.norm = 1; a.eps = eps; a.head_dim = L->head_dim;
-  a.seg[0] = Seg{QView{}, QView{}, qb, (int)Hq, 1};
-  a.seg[1] = Seg{QView{}, QView{}, kb, (int)Hkv, 1};
-  a.seg[2] = Seg{QView{}, QView{}, oin, (int)Hq, L->n_heads / L->n_kv_heads};
-  if ((st = run_op(c, a, ids, 3))) return st;
-  // 2. h = h + attn Wo
-  LinOp o = plain_op(QView{nullptr, nullptr, (int)to.K, (int)to.N}, oin, Mi, hh);
-  o.res = hh;
-  if ((st = run_op(c, o, &ids[3], 1))) return st;
+  if ((st = run_attention(c, ids, L->n_heads, L->n_kv_heads, L->head_dim, eps, hh, Mi, qb, kb, oin))) return st;
   // 3. f = silu(rms(h) Wg) * (rms(h) Wu)
   LinOp gu = plain_op(QView{nullptr, nullptr, (int)tg.K, (int)tg.N}, hh, Mi, hf);
   gu.swiglu = 1; gu.norm = 1; gu.eps = eps;
   if ((st = run_op(c, gu, &ids[4], 2))) return st;
-  // 4. h = h + f Wd
+  // 4. h = h + f Wd (in fp32 and renormalised when asked)
   LinOp dn = plain_op(QView{nullptr, nullptr, (int)td.K, (int)td.N}, hf, Mi, hh);
   dn.res = hh;
-  return run_op(c, dn, &ids[6], 1);
+  dn.y32 = y32;
+  if ((st = run_op(c, dn, &ids[6], 1))) return st;
+  if (y32) {
+    hipError_t e = launch_rmsnorm32(y32, Mi, (int)H, eps, hh, c->cs);
+    if (e != hipSuccess) return hip_fail(c, e, "rmsnorm launch");
+  }
+  return ATSI_OK;
+}
+
+atsi_status atsi_moe_decoder_layer(atsi_ctx* c, const atsi_moe_layer* L, void* h, int64_t M, void* q_out,
+                                   void* k_out, const atsi_moe_debug* dbg) {
+  if (!c) return ATSI_E_INVALID;
+  if (!L) return fail(c, ATSI_E_INVALID, "layer descriptor is NULL");
+  atsi_status st;
+  if ((st = check_act(c, h, "h")) || (st = check_m(c, M))) return st;
+  if ((q_out && !aligned16(q_out)) || (k_out && !aligned16(k_out)))
+    return fail(c, ATSI_E_INVALID, "q_out / k_out must be 16-byte aligned");
+  const atsi_tid ids[4] = {L->q, L->k, L->v, L->o};
+  if ((st = check_attention(c, ids, L->n_heads, L->n_kv_heads, L->head_dim, L->eps)) || (st = check_moe(c, L->moe)))
+    return st;
+  const int64_t H = c->tensors[L->q].K, Hq = c->tensors[L->q].N, Hkv = c->tensors[L->k].N;
+  if (L->moe->hidden != H) return fail(c, ATSI_E_SHAPE, "MoE hidden %lld != attention hidden %lld",
+                                       (long long)L->moe->hidden, (long long)H);
+  if ((st = enter(c))) return st;
+  Scratch sc(c);
+  __half* qb = q_out ? (__half*)q_out : sc.take((size_t)M * Hq);
+  __half* kb = k_out ? (__half*)k_out : sc.take((size_t)M * Hkv);
+  __half* oin = sc.take((size_t)M * Hq);
+  float* inv_r = (float*)sc.take(M, 4);
+  if (!qb || !kb || !oin || !inv_r)
+    return fail(c, ATSI_E_WORKSPACE, "scratch too small for a %lld-token layer", (long long)M);
+  __half* hh = (__half*)h;
+  const int Mi = (int)M;
+  // expert copies wait for routing; the attention tensors can start now
+  if ((st = prefetch_call(c, ids, 4))) return st;
+  if ((st = run_attention(c, ids, L->n_heads, L->n_kv_heads, L->head_dim, L->eps, hh, Mi, qb, kb, oin))) return st;
+  // h = h + MoE(rms(h)): the norm is a per-token factor on the router logits
+  // and the expert gate/up products, the residual is added by the combine
+  hipError_t e = launch_rms_inv(hh, Mi, (int)H, L->eps, inv_r, c->cs);
+  if (e != hipSuccess) return hip_fail(c, e, "rms launch");
+  return run_moe(c, L->moe, hh, Mi, hh, dbg, inv_r, hh, sc);
+}
+
+atsi_status atsi_rmsnorm(atsi_ctx* c, const void* x, int64_t M, int64_t H, float eps, void* y) {
+  if (!c) return ATSI_E_INVALID;
+  atsi_status st;
+  if ((st = check_act(c, x, "x")) || (st = check_act(c, y, "y")) || (st = check_m(c, M))) return st;
+  if (H < 8 || H % 8 != 0 || H > (1 << 20) || !(eps >= 0.f))
+    return fail(c, ATSI_E_SHAPE, "hidden %lld must be a positive multiple of 8 (eps >= 0)", (long long)H);
+  if ((st = enter(c))) return st;
+  hipError_t e = launch_rmsnorm((const __half*)x, (int)M, (int)H, eps, (__half*)y, c->cs);
+  if (e != hipSuccess) return hip_fail(c, e, "rmsnorm launch");
+  return ATSI_OK;
 }
 
 atsi_status atsi_moe_bucket(atsi_ctx* c, const int32_t* idx, int64_t M, int32_t k, int32_t E, int32_t* counts,
@@ -863,125 +1066,13 @@ atsi_status atsi_moe_bucket(atsi_ctx* c, const int32_t* idx, int64_t M, int32_t 
 atsi_status atsi_moe_ffn(atsi_ctx* c, const atsi_moe* m, const void* x, int64_t M, void* y,
                          const atsi_moe_debug* dbg) {
   if (!c) return ATSI_E_INVALID;
-  if (!m) return fail(c, ATSI_E_INVALID, "moe descriptor is NULL");
   atsi_status st;
-  if ((st = check_act(c, x, "x")) || (st = check_act(c, y, "y")) || (st = check_m(c, M))) return st;
-  const int E = m->n_experts, k = m->top_k;
-  if (E < 16 || E > kMaxExperts || E % 16 != 0 || k < 1 || k > kMaxTopK || k > E)
-    return fail(c, ATSI_E_SHAPE, "n_experts %d (multiple of 16, <= %d) / top_k %d (1..16) unsupported", E,
-                kMaxExperts, k);
-  if (m->hidden < 32 || m->hidden % 32 || m->inter < 32 || m->inter % 32)
-    return fail(c, ATSI_E_SHAPE, "hidden %lld / inter %lld must be positive multiples of 32", (long long)m->hidden,
-                (long long)m->inter);
-  if (!m->router_w_f16 || !aligned16(m->router_w_f16) || !m->gate || !m->up || !m->down)
-    return fail(c, ATSI_E_INVALID, "router weights (16-byte aligned) and expert id arrays are required");
+  if ((st = check_act(c, x, "x")) || (st = check_act(c, y, "y")) || (st = check_m(c, M)) || (st = check_moe(c, m)))
+    return st;
   if (x == y) return fail(c, ATSI_E_INVALID, "y must not alias x");
-  const int H = (int)m->hidden, I = (int)m->inter;
-  for (int e = 0; e < E; ++e) {
-    if ((st = check_tid(c, m->gate[e])) || (st = check_tid(c, m->up[e])) || (st = check_tid(c, m->down[e]))) return st;
-    const Tensor &g = c->tensors[m->gate[e]], &u = c->tensors[m->up[e]], &d = c->tensors[m->down[e]];
-    if (g.K != H || g.N != I || u.K != H || u.N != I || d.K != I || d.N != H)
-      return fail(c, ATSI_E_SHAPE, "expert %d: gate/up must be %d x %d and down %d x %d", e, H, I, I, H);
-  }
   if ((st = enter(c))) return st;
-  atsi_ctx::MoeTable* tb;
-  if ((st = get_table(c, m, &tb))) return st;
-  const int Mi = (int)M, Mk = Mi * k;
-  const bool gemv = Mi <= 4;
-  const int bm = expert_tile_rows(gemv);
   Scratch sc(c);
-  float* part = (float*)sc.take(router_partial_floats(Mi, H, E), 4);
-  int32_t* idx = dbg && dbg->idx ? dbg->idx : (int32_t*)sc.take(Mk, 4);
-  float* p = dbg && dbg->p ? dbg->p : (float*)sc.take(Mk, 4);
-  int32_t* counts = dbg && dbg->counts ? dbg->counts : (int32_t*)sc.take(E, 4);
-  int32_t* offsets = dbg && dbg->offsets ? dbg->offsets : (int32_t*)sc.take(E + 1, 4);
-  int32_t* perm = dbg && dbg->perm ? dbg->perm : (int32_t*)sc.take(Mk, 4);
-  int32_t* inv = dbg && dbg->inv_perm ? dbg->inv_perm : (int32_t*)sc.take(Mk, 4);
-  int32_t* order = (int32_t*)sc.take(E, 4);
-  int32_t* tiles = (int32_t*)sc.take(2 * ((size_t)Mk / bm + E + 1), 4);
-  int32_t* ntiles = (int32_t*)sc.take(1, 4);
-  __half* h = sc.take((size_t)Mk * I);
-  __half* out = sc.take((size_t)Mk * H);
-  if (!part || !idx || !p || !counts || !offsets || !perm || !inv || !order || !tiles || !ntiles || !h || !out)
-    return fail(c, ATSI_E_WORKSPACE, "scratch too small for a %d-token MoE layer", Mi);
-  const ExpertW* table = reinterpret_cast<const ExpertW*>(c->ws + tb->off);
-  const uint8_t* resident = reinterpret_cast<const uint8_t*>(c->ws + tb->off + align_up((size_t)E * sizeof(ExpertW)));
-
-  hipError_t e = launch_router((const __half*)x, (const __half*)m->router_w_f16, m->router_bias, Mi, H, E, k, part,
-                               idx, p, dbg ? dbg->logits : nullptr, c->cs);
-  if (e != hipSuccess) return hip_fail(c, e, "router launch");
-  e = launch_bucket(idx, Mi, k, E, resident, bm, counts, offsets, perm, inv, order, tiles, ntiles, c->cs);
-  if (e != hipSuccess) return hip_fail(c, e, "bucket launch");
-  if (tb->n_streamed > 0) {
-    HIP_TRY(c, hipMemcpyAsync(c->pinned, counts, E * sizeof(int32_t), hipMemcpyDeviceToHost, c->cs));
-    HIP_TRY(c, hipEventRecord(c->counts_ev, c->cs));
-  }
-  MoeArgs a{};
-  a.table = table;
-  a.tiles = tiles;
-  a.n_tiles = ntiles;
-  a.counts = counts;
-  a.offsets = offsets;
-  a.perm = perm;
-  a.x = (const __half*)x;
-  a.h = h;
-  a.out = out;
-  a.k = k;
-  a.H = H;
-  a.I = I;
-  // HBM-resident experts first: they run while the host learns which
-  // streamed experts are needed.
-  const int bound = bm == 1 ? Mk : Mk / bm + std::min(E, Mk);
-  if ((e = launch_expert_gateup(a, bound, gemv, c->cs)) != hipSuccess) return hip_fail(c, e, "expert gate/up launch");
-  if ((e = launch_expert_down(a, bound, gemv, c->cs)) != hipSuccess) return hip_fail(c, e, "expert down launch");
-
-  if (tb->n_streamed > 0) {
-    HIP_TRY(c, hipEventSynchronize(c->counts_ev));
-    std::vector<int> act;
-    for (int ex = 0; ex < E; ++ex) {
-      const Tensor &g = c->tensors[m->gate[ex]], &u = c->tensors[m->up[ex]], &d = c->tensors[m->down[ex]];
-      if ((g.on_host || u.on_host || d.on_host) && c->pinned[ex] > 0) act.push_back(ex);
-    }
-    std::stable_sort(act.begin(), act.end(), [&](int l, int r) { return c->pinned[l] > c->pinned[r]; });
-    for (int ex : act)
-      for (const atsi_tid t : {m->gate[ex], m->up[ex], m->down[ex]})
-        if (c->tensors[t].on_host) c->queue.push_back(t);
-    if ((st = topup(c))) return st;
-    const int B = std::max(1, std::min(kBatchExp, c->n_slots / 3));
-    for (size_t b0 = 0; b0 < act.size(); b0 += B) {
-      std::vector<int> held;
-      MoeArgs ba = a;
-      ba.nb = 0;
-      const int nbx = (int)std::min<size_t>(B, act.size() - b0);
-      for (int b = 0; b < nbx; ++b) {
-        const int ex = act[b0 + b];
-        ba.bexp[b] = ex;
-        if ((st = acquire(c, m->gate[ex], &ba.bw[b].gate, held)) || (st = acquire(c, m->up[ex], &ba.bw[b].up, held)) ||
-            (st = acquire(c, m->down[ex], &ba.bw[b].down, held)))
-          return st;
-      }
-      auto flush = [&]() -> atsi_status {
-        if (ba.nb == 0) return ATSI_OK;
-        hipError_t fe = launch_expert_gateup(ba, ba.nb, gemv, c->cs);
-        if (fe == hipSuccess) fe = launch_expert_down(ba, ba.nb, gemv, c->cs);
-        if (fe != hipSuccess) return hip_fail(c, fe, "streamed expert launch");
-        ba.nb = 0;
-        return ATSI_OK;
-      };
-      for (int b = 0; b < nbx; ++b) {
-        const int cnt = c->pinned[act[b0 + b]];
-        for (int r0 = 0; r0 < cnt; r0 += bm) {
-          if (ba.nb == kBatchTiles && (st = flush())) return st;
-          ba.btiles[ba.nb++] = make_int2(b, r0);
-        }
-      }
-      if ((st = flush())) return st;
-      if ((st = release(c, held))) return st;
-    }
-  }
-  e = launch_combine(out, p, Mi, k, H, (__half*)y, c->cs);
-  if (e != hipSuccess) return hip_fail(c, e, "combine launch");
-  return ATSI_OK;
+  return run_moe(c, m, (const __half*)x, (int)M, (__half*)y, dbg, nullptr, nullptr, sc);
 }
 
 atsi_status atsi_set_schedule(atsi_ctx* c, const atsi_tid* order, int32_t n) {

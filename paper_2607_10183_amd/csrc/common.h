@@ -41,6 +41,7 @@ struct LinOp {
   int norm;          // 1: input is RMS-normalised (unit gain) before the product
   float eps;
   const __half* res; // residual added to segment 0's output (may alias its y)
+  float* y32;        // non-null: segment 0's output goes here in fp32 instead of y
   int head_dim;      // granularity of `expand`
 };
 

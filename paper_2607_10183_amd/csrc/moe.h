@@ -33,12 +33,18 @@ struct MoeArgs {
   const __half* x;             // tokens [M][H]
   __half* h;                   // SwiGLU activations [M*k][I], row = bucket position
   __half* out;                 // expert outputs [M*k][H], row = pair id
+  const float* inv_r;          // per-token RMS-norm factor of x, or nullptr
   int k, H, I;
 };
 
 // router: logits = x W_r + b (fp32 accumulation), top-k with renormalised softmax
-hipError_t launch_router(const __half* x, const __half* wr, const float* bias, int M, int H, int E, int k,
-                         float* part, int32_t* idx, float* p, float* logits, hipStream_t s);
+hipError_t launch_router(const __half* x, const float* inv_r, const __half* wr, const float* bias, int M, int H,
+                         int E, int k, float* part, int32_t* idx, float* p, float* logits, hipStream_t s);
+// inv_r[t] = 1 / sqrt(mean_k x[t][k]^2 + eps) (fp32)
+hipError_t launch_rms_inv(const __half* x, int M, int H, float eps, float* inv_r, hipStream_t s);
+// y[t] = x[t] * inv_r[t] in fp16 (y may alias x)
+hipError_t launch_rmsnorm(const __half* x, int M, int H, float eps, __half* y, hipStream_t s);
+hipError_t launch_rmsnorm32(const float* x, int M, int H, float eps, __half* y, hipStream_t s);
 size_t router_partial_floats(int M, int H, int E);
 
 // bucketing (single workgroup): counts, offsets, perm, inv_perm, heavy-first
@@ -53,7 +59,8 @@ int expert_tile_rows(bool gemv);
 hipError_t launch_expert_gateup(const MoeArgs& a, int tile_bound, bool gemv, hipStream_t s);
 hipError_t launch_expert_down(const MoeArgs& a, int tile_bound, bool gemv, hipStream_t s);
 // y[t] = sum_j p[t][j] * out[k*t + j] (fp32, slot order) -> fp16
-hipError_t launch_combine(const __half* out, const float* p, int M, int k, int H, __half* y, hipStream_t s);
+hipError_t launch_combine(const __half* out, const float* p, int M, int k, int H, const __half* res, __half* y,
+                          hipStream_t s);
 // write table entries e0 .. e0+n-1 (n <= 16) and their residency flags
 hipError_t launch_table_patch(ExpertW* table, uint8_t* resident, int e0, int n, const ExpertW* w, const uint8_t* r,
                               hipStream_t s);

@@ -68,7 +68,11 @@ __global__ __launch_bounds__(kGemmBlock, 2) void expert_gateup_gemm(MoeArgs a, i
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int r = Core::frag_row(i, v);
-        if (r < rows) a.h[(size_t)(base + r) * a.I + n] = __float2half_rn(silu_f(acc[i][j][v]) * acc[i][j + 1][v]);
+        if (r < rows) {
+          // RMS-normalised input: scale both products by the token's factor
+          const float sc = a.inv_r ? a.inv_r[a.perm[base + r] / a.k] : 1.f;
+          a.h[(size_t)(base + r) * a.I + n] = __float2half_rn(silu_f(acc[i][j][v] * sc) * (acc[i][j + 1][v] * sc));
+        }
       }
     }
 }
@@ -166,11 +170,12 @@ __global__ __launch_bounds__(gemv::kBlock) void expert_gemv(MoeArgs a, int tile_
       }
     }
   }
+  const float sc = (!DOWN && a.inv_r) ? a.inv_r[pr / a.k] : 1.f;  // RMS-normalised input
 #pragma unroll
   for (int r = 0; r < RW; ++r) {
-    const float g = wave_sum(acc[r]);
+    const float g = wave_sum(acc[r]) * sc;
     float u = 0.f;
-    if constexpr (!DOWN) u = wave_sum(acc2[r]);
+    if constexpr (!DOWN) u = wave_sum(acc2[r]) * sc;
     const int n = n0 + r;
     if (lane == r && n < N) {
       if (DOWN)
@@ -186,7 +191,7 @@ constexpr int kGemvRW = 2;
 // ---------------------------------------------------------------- combine, table patch
 
 __global__ void combine_kernel(const __half* __restrict__ out, const float* __restrict__ p, int M, int k, int H,
-                               __half* __restrict__ y) {
+                               const __half* res, __half* y) {
   const int c8 = H / 8;
   const size_t total = (size_t)M * c8;
   for (size_t q = (size_t)blockIdx.x * blockDim.x + threadIdx.x; q < total; q += (size_t)gridDim.x * blockDim.x) {
@@ -208,6 +213,12 @@ __global__ void combine_kernel(const __half* __restrict__ out, const float* __re
 #pragma unroll
           for (int i = 0; i < 8; ++i) acc[i] = fmaf(pj[j], __half2float(hv[i]), acc[i]);
         }
+    }
+    if (res) {  // y = res + sum (y may alias res: each element is read, then written, by one thread)
+      const uint4 rv = *reinterpret_cast<const uint4*>(res + (size_t)t * H + (size_t)c * 8);
+      const __half* hr = reinterpret_cast<const __half*>(&rv);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) acc[i] += __half2float(hr[i]);
     }
     uint4 o;
     __half* ho = reinterpret_cast<__half*>(&o);
@@ -261,10 +272,11 @@ hipError_t launch_expert_down(const MoeArgs& a, int tile_bound, bool gemv, hipSt
   return hipGetLastError();
 }
 
-hipError_t launch_combine(const __half* out, const float* p, int M, int k, int H, __half* y, hipStream_t s) {
+hipError_t launch_combine(const __half* out, const float* p, int M, int k, int H, const __half* res, __half* y,
+                          hipStream_t s) {
   const size_t total = (size_t)M * (H / 8);
   const int blocks = (int)std::min<size_t>((total + 255) / 256, 2048);
-  hipLaunchKernelGGL(combine_kernel, dim3(blocks), dim3(256), 0, s, out, p, M, k, H, y);
+  hipLaunchKernelGGL(combine_kernel, dim3(blocks), dim3(256), 0, s, out, p, M, k, H, res, y);
   return hipGetLastError();
 }
 

@@ -93,6 +93,7 @@ __global__ __launch_bounds__(256) void router_partial_kernel(const __half* __res
 
 // one wave per token; E <= 128 (two candidates per lane)
 __global__ __launch_bounds__(256) void router_topk_kernel(const float* __restrict__ part, int n_split,
+                                                          const float* __restrict__ inv_r,
                                                           const float* __restrict__ bias, int M, int E, int k,
                                                           int32_t* __restrict__ idx, float* __restrict__ p,
                                                           float* __restrict__ logits_out) {
@@ -109,6 +110,7 @@ __global__ __launch_bounds__(256) void router_topk_kernel(const float* __restric
       float s = 0.f;
 #pragma unroll 8
       for (int sp = 0; sp < n_split; ++sp) s += part[((size_t)sp * M + t) * E + e];
+      if (inv_r) s *= inv_r[t];  // RMS-normalised input: scale the product once
       if (bias) s += bias[e];
       v[h] = s;
       if (logits_out) logits_out[(size_t)t * E + e] = s;
@@ -258,10 +260,101 @@ __global__ __launch_bounds__(1024) void bucket_kernel(const int32_t* __restrict_
   }
 }
 
+// one wavefront per token: inv_r[t] = 1 / sqrt(mean(x[t]^2) + eps)
+__global__ __launch_bounds__(256) void rms_inv_kernel(const __half* __restrict__ x, int M, int H, float eps,
+                                                      float* __restrict__ inv_r) {
+  const int lane = threadIdx.x & 63;
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= M) return;
+  float q = 0.f;
+  for (int c = lane * 8; c < H; c += 64 * 8) {
+    const uint4 v = *reinterpret_cast<const uint4*>(x + (size_t)t * H + c);
+    const __half* hv = reinterpret_cast<const __half*>(&v);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const float f = __half2float(hv[i]);
+      q = fmaf(f, f, q);
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) q += __shfl_xor(q, o, 64);
+  if (lane == 0) inv_r[t] = 1.f / sqrtf(q / (float)H + eps);
+}
+
+// one wavefront per token: y[t] = x[t] * inv_r (one fp16 rounding); y may alias x
+__global__ __launch_bounds__(256) void rmsnorm_kernel(const __half* x, int M, int H, float eps, __half* y) {
+  const int lane = threadIdx.x & 63;
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= M) return;
+  float q = 0.f;
+  for (int c = lane * 8; c < H; c += 64 * 8) {
+    const uint4 v = *reinterpret_cast<const uint4*>(x + (size_t)t * H + c);
+    const __half* hv = reinterpret_cast<const __half*>(&v);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const float f = __half2float(hv[i]);
+      q = fmaf(f, f, q);
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) q += __shfl_xor(q, o, 64);
+  const float inv = 1.f / sqrtf(q / (float)H + eps);
+  for (int c = lane * 8; c < H; c += 64 * 8) {
+    const uint4 v = *reinterpret_cast<const uint4*>(x + (size_t)t * H + c);
+    const __half* hv = reinterpret_cast<const __half*>(&v);
+    uint4 o;
+    __half* ho = reinterpret_cast<__half*>(&o);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) ho[i] = __float2half_rn(__half2float(hv[i]) * inv);
+    *reinterpret_cast<uint4*>(y + (size_t)t * H + c) = o;
+  }
+}
+
+// the same from an fp32 input (a residual sum that may exceed the fp16 range)
+__global__ __launch_bounds__(256) void rmsnorm32_kernel(const float* __restrict__ x, int M, int H, float eps,
+                                                        __half* __restrict__ y) {
+  const int lane = threadIdx.x & 63;
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= M) return;
+  float q = 0.f;
+  for (int c = lane * 4; c < H; c += 64 * 4) {
+    const float4 v = *reinterpret_cast<const float4*>(x + (size_t)t * H + c);
+    q = fmaf(v.x, v.x, q);
+    q = fmaf(v.y, v.y, q);
+    q = fmaf(v.z, v.z, q);
+    q = fmaf(v.w, v.w, q);
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) q += __shfl_xor(q, o, 64);
+  const float inv = 1.f / sqrtf(q / (float)H + eps);
+  for (int c = lane * 4; c < H; c += 64 * 4) {
+    const float4 v = *reinterpret_cast<const float4*>(x + (size_t)t * H + c);
+    y[(size_t)t * H + c] = __float2half_rn(v.x * inv);
+    y[(size_t)t * H + c + 1] = __float2half_rn(v.y * inv);
+    y[(size_t)t * H + c + 2] = __float2half_rn(v.z * inv);
+    y[(size_t)t * H + c + 3] = __float2half_rn(v.w * inv);
+  }
+}
+
 }  // namespace
 
-hipError_t launch_router(const __half* x, const __half* wr, const float* bias, int M, int H, int E, int k,
-                         float* part, int32_t* idx, float* p, float* logits, hipStream_t s) {
+hipError_t launch_rmsnorm32(const float* x, int M, int H, float eps, __half* y, hipStream_t s) {
+  hipLaunchKernelGGL(rmsnorm32_kernel, dim3((M + 3) / 4), dim3(256), 0, s, x, M, H, eps, y);
+  return hipGetLastError();
+}
+
+hipError_t launch_rmsnorm(const __half* x, int M, int H, float eps, __half* y, hipStream_t s) {
+  hipLaunchKernelGGL(rmsnorm_kernel, dim3((M + 3) / 4), dim3(256), 0, s, x, M, H, eps, y);
+  return hipGetLastError();
+}
+
+hipError_t launch_rms_inv(const __half* x, int M, int H, float eps, float* inv_r, hipStream_t s) {
+  hipLaunchKernelGGL(rms_inv_kernel, dim3((M + 3) / 4), dim3(256), 0, s, x, M, H, eps, inv_r);
+  return hipGetLastError();
+}
+
+hipError_t launch_router(const __half* x, const float* inv_r, const __half* wr, const float* bias, int M, int H,
+                         int E, int k, float* part, int32_t* idx, float* p, float* logits, hipStream_t s) {
   // K slice per workgroup: enough workgroups to cover the chip, slices of >= 64
   const int tiles = (M + kRT - 1) / kRT;
   int ks = H;
@@ -270,8 +363,8 @@ hipError_t launch_router(const __half* x, const __half* wr, const float* bias, i
   hipLaunchKernelGGL(router_partial_kernel, dim3(tiles, n_split), dim3(256), 0, s, x, wr, M, H, E, ks, part);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(router_topk_kernel, dim3((M + 3) / 4), dim3(256), 0, s, part, n_split, bias, M, E, k, idx, p,
-                     logits);
+  hipLaunchKernelGGL(router_topk_kernel, dim3((M + 3) / 4), dim3(256), 0, s, part, n_split, inv_r, bias, M, E, k,
+                     idx, p, logits);
   return hipGetLastError();
 }
 

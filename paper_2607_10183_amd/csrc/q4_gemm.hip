@@ -69,7 +69,10 @@ __global__ __launch_bounds__(kGemmBlock, 2) void q4_gemm_kernel(LinOp op, TileMa
         } else {
           const size_t at = (size_t)m * sg.ldy + n;
           if (op.res && s == 0) o += __half2float(op.res[at]);
-          sg.y[at] = __float2half_rn(o);
+          if (op.y32 && s == 0)
+            op.y32[at] = o;
+          else
+            sg.y[at] = __float2half_rn(o);
         }
       }
     }

@@ -184,7 +184,10 @@ __device__ __forceinline__ void compute_step(const Step<RW, CPL, SWI>& cur, cons
         } else {
           const size_t at = (size_t)m * sg.ldy + row;
           if (op.res && s == 0) v += __half2float(op.res[at]);
-          sg.y[at] = __float2half_rn(v);
+          if (op.y32 && s == 0)
+            op.y32[at] = v;
+          else
+            sg.y[at] = __float2half_rn(v);
         }
       }
     }

@@ -136,6 +136,17 @@ class Session:
         self._torch_waits()
         return y
 
+    def rmsnorm(self, x: torch.Tensor, eps: float = 1e-6, y: torch.Tensor | None = None) -> torch.Tensor:
+        """y = x / rms(x) per row (unit gain); in place when y is x."""
+        M, H = x.shape
+        if y is None:
+            with torch.cuda.stream(self.cs):
+                y = torch.empty_like(x)
+        self._wait_torch()
+        atsi.atsi_rmsnorm(self.ctx, x.data_ptr(), M, H, eps, y.data_ptr())
+        self._torch_waits()
+        return y
+
     def gate_up(self, gate: int, up: int, x: torch.Tensor, h: torch.Tensor | None = None) -> torch.Tensor:
         """h = silu(x Wg) * (x Wu), one launch."""
         H, I = self.shapes[gate]
@@ -149,10 +160,13 @@ class Session:
         return h
 
     def decoder_layer(self, tids: dict, h: torch.Tensor, n_heads: int, n_kv: int, head_dim: int,
-                      eps: float = 1e-6, q_out: torch.Tensor | None = None, k_out: torch.Tensor | None = None):
-        """In-place pre-norm decoder layer on h[M][H]; tids maps q,k,v,o,gate,up,down to tensor ids."""
+                      eps: float = 1e-6, q_out: torch.Tensor | None = None, k_out: torch.Tensor | None = None,
+                      renorm_out: bool = False):
+        """In-place pre-norm decoder layer on h[M][H]; tids maps q,k,v,o,gate,up,down to tensor ids.
+        renorm_out: the output is renormalised (h <- rms(h + FFN)), as between the layers of a stack."""
         L = atsi.atsi_dense_layer(n_heads, n_kv, head_dim, eps, *[tids[r] for r in
-                                                                  ("q", "k", "v", "o", "gate", "up", "down")])
+                                                                  ("q", "k", "v", "o", "gate", "up", "down")],
+                                  int(renorm_out))
         M = h.shape[0]
         self._wait_torch()
         atsi.atsi_decoder_layer(self.ctx, L, h.data_ptr(), M, q_out.data_ptr() if q_out is not None else 0,
@@ -254,3 +268,39 @@ class MoELayer:
         atsi.atsi_moe_ffn(s.ctx, self.desc, x.data_ptr(), M, y.data_ptr(), dbg)
         s._torch_waits()
         return (y, out) if debug else y
+
+    def _debug_buffers(self, M: int):
+        s = self.sess
+        with torch.cuda.stream(s.cs):
+            out = {"logits": torch.empty((M, self.E), dtype=torch.float32, device=s.device),
+                   "idx": torch.empty((M, self.k), dtype=torch.int32, device=s.device),
+                   "p": torch.empty((M, self.k), dtype=torch.float32, device=s.device),
+                   "counts": torch.empty(self.E, dtype=torch.int32, device=s.device),
+                   "offsets": torch.empty(self.E + 1, dtype=torch.int32, device=s.device),
+                   "perm": torch.empty(M * self.k, dtype=torch.int32, device=s.device),
+                   "inv_perm": torch.empty(M * self.k, dtype=torch.int32, device=s.device)}
+        dbg = atsi.atsi_moe_debug(*[out[n].data_ptr() for n in
+                                    ("logits", "idx", "p", "counts", "offsets", "perm", "inv_perm")])
+        return out, dbg
+
+
+class MoEDecoderLayer:
+    """Attention (q, k, v, o tensor ids) plus an MoELayer as the FFN."""
+
+    def __init__(self, moe: MoELayer, q: int, k: int, v: int, o: int, n_heads: int, n_kv: int, head_dim: int,
+                 eps: float = 1e-6):
+        self.moe = moe
+        self.desc = atsi.atsi_moe_layer(n_heads, n_kv, head_dim, eps, q, k, v, o,
+                                        __import__("ctypes").pointer(moe.desc))
+
+    def __call__(self, h: torch.Tensor, q_out: torch.Tensor | None = None, k_out: torch.Tensor | None = None,
+                 debug: bool = False):
+        """Updates h (fp16 [M][hidden]) in place; returns the routing buffers when debug."""
+        s = self.moe.sess
+        M = h.shape[0]
+        out, dbg = self.moe._debug_buffers(M) if debug else ({}, None)
+        s._wait_torch()
+        atsi.atsi_moe_decoder_layer(s.ctx, self.desc, h.data_ptr(), M, q_out.data_ptr() if q_out is not None else 0,
+                                    k_out.data_ptr() if k_out is not None else 0, dbg)
+        s._torch_waits()
+        return out if debug else None

@@ -145,3 +145,16 @@ def test_schedule_prefetch_across_layers(sess):
     sess.set_placement(base)
     for o in outs:
         assert torch.equal(o, ref)
+
+
+@pytest.mark.parametrize("M,H", [(1, 256), (8, 4096), (77, 2048)])
+def test_rmsnorm_parity(sess, M, H):
+    """The between-layer renormalisation against the oracle, in place."""
+    xn = synth.activations(76, M, M, H) * 7.0
+    x = _dev(xn.astype(np.float16))
+    sess.rmsnorm(x, 1e-6, x)
+    sess.sync()
+    ref, zeta = oracle.rmsnorm(xn.astype(np.float16).astype(np.float64), 1e-6)
+    # the output is rounded to fp16: near zero its quantum is the subnormal
+    # spacing, so the magnitude gets the smallest normal fp16 as a floor
+    check(x.cpu().numpy(), ref, zeta + 2.0 ** -14, name=f"rmsnorm M={M} H={H}")
