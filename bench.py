@@ -24,6 +24,12 @@ synthetic weights and activations.
                     alone (atsi_swiglu_gate_up) with HIP events; their HBM
                     traffic comes from the committed counter profile when the
                     kernel sources still match it.
+  stacks            dense_stack: 32 such layers as a decode loop of 8
+                    sequences (hidden state renormalised after every layer),
+                    all-HBM and with 30 % of the bytes streamed; moe_stack:
+                    one 235B-A22B-shaped MoE decoder layer at decode and
+                    2048-token prefill, all-HBM and with 40 % of its experts
+                    streamed (94-layer figures = 94 x the layer).
   cpu_baseline      the fp64 oracle's decode step on the host cores.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
@@ -119,6 +125,7 @@ def main() -> int:
     ap.add_argument("--copies", type=int, default=5, help="dense-layer copies rotated to defeat the MALL")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-moe", action="store_true")
+    ap.add_argument("--no-stacks", action="store_true", help="skip the dense-stack and MoE-stack lines")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--roofline-only", action="store_true",
                     help="run only the roofline kernels and a 256 MiB copy (for rocprofv3 --pmc)")
@@ -277,6 +284,11 @@ def main() -> int:
         f"{host_bytes / 1e6:.1f} MB) -> PCIe {host_bytes / st_dec / 1e9:.1f} GB/s")
 
     moe = None if args.no_moe else bench_moe(sess, timer, args)
+    stacks = None
+    if not args.no_stacks:
+        sess.close()
+        stacks = {"dense_stack": bench_dense_stack(timer_cls=Timer, h2d_gbs=h2d_gbs),
+                  "moe_stack": bench_moe_stack(timer_cls=Timer)}
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -329,9 +341,11 @@ def main() -> int:
                      "prefill_exposed_ms": round(max(0.0, st_pf - prefill_s) * 1e3, 4),
                      "prefill_tokens_per_s": round(Mp / st_pf, 1)},
         "moe": moe,
+        "stacks": stacks,
         "cpu_baseline": cpu,
     }
-    sess.close()
+    if args.no_stacks:
+        sess.close()
     print(json.dumps(out), flush=True)
     return 0
 
@@ -412,6 +426,152 @@ def bench_moe(sess, timer, args):
             "streamed_40pct_host": {"decode_ms_per_token": round(st_dec * 1e3, 4),
                                     "prefill_ms": round(st_pf * 1e3, 3),
                                     "prefill_pcie_GBps_if_all_active": round(host_bytes_pf / st_pf / 1e9, 2)}}
+
+
+def bench_dense_stack(timer_cls, h2d_gbs, steps=6):
+    """32 8B-shaped layers, a decode loop over 8 sequences (hidden state
+    renormalised after every layer), 30 % of the int4 bytes on host by
+    seeded score, streamed each step with schedule-driven prefetch."""
+    import torch
+
+    import synth
+    from synth import configs
+    from paper_2607_10183_amd.session import Session
+
+    wl = configs.DENSE_STACK
+    shape = wl.dense
+    mask = configs.dense_stack_host_mask()
+    log("generating dense-stack weights (32 layers)")
+    sess = Session(workspace_bytes=2 << 30, n_slots=24)
+    timer = timer_cls(sess.cs)
+    tids = []
+    for layer in range(wl.n_layers):
+        t = {}
+        for j, r in enumerate(configs.ROLES):
+            K, N = shape.kn(r)
+            uid = configs.dense_uid(layer, r)
+            t[r] = sess.register(synth.int4_codes(wl.seed, uid, N, K), synth.group_scales(wl.seed, uid, N, K),
+                                 hbm=True, host=bool(mask[layer, j]))
+        tids.append(t)
+    total_bytes = wl.n_layers * shape.layer_bytes()
+    host_bytes = sum(configs.qbytes(*shape.kn(configs.ROLES[j])) for layer in range(wl.n_layers)
+                     for j in range(len(configs.ROLES)) if mask[layer, j])
+    h = torch.from_numpy(synth.activations(wl.seed, 1, wl.decode_m, shape.hidden)).cuda()
+    sess.cs.wait_stream(torch.cuda.current_stream())
+
+    def step():
+        for layer in range(wl.n_layers):
+            sess.decoder_layer(tids[layer], h, shape.n_heads, shape.n_kv, shape.head_dim, 1e-6, renorm_out=True)
+
+    # all weights in HBM
+    timer.run(step, 1)
+    t_hbm = timer.run(step, steps)
+    # the seeded 30 % mask, streamed with the schedule (execution order)
+    pl = [0] * len(sess.shapes)
+    for layer in range(wl.n_layers):
+        for j, r in enumerate(configs.ROLES):
+            pl[tids[layer][r]] = int(mask[layer, j])
+    sess.set_placement(pl)
+    sess.set_schedule([tids[layer][r] for layer in range(wl.n_layers) for r in configs.ROLES])
+    timer.run(step, 1)
+    t_st = timer.run(step, steps)
+    sess.close()
+    m = wl.decode_m
+    log(f"dense stack: decode step {t_hbm * 1e3:.2f} ms all-HBM ({total_bytes / t_hbm / 1e9:.0f} GB/s), "
+        f"{t_st * 1e3:.2f} ms with {host_bytes / 1e9:.2f} GB on host ({host_bytes / t_st / 1e9:.1f} GB/s PCIe)")
+    return {"workload": "dense_stack: 32 8B-shaped layers, decode loop of 8 sequences, hidden state renormalised "
+                        "after every layer, 30 % of the int4 bytes on host by seeded score",
+            "layers": wl.n_layers, "sequences": m, "steps_timed": steps,
+            "total_bytes": total_bytes, "host_bytes": host_bytes,
+            "all_hbm": {"ms_per_step": round(t_hbm * 1e3, 3), "tokens_per_s": round(m / t_hbm, 1),
+                        "weight_GBps": round(total_bytes / t_hbm / 1e9, 1)},
+            "streamed": {"ms_per_step": round(t_st * 1e3, 3), "tokens_per_s": round(m / t_st, 1),
+                         "weight_GBps_pcie_inclusive": round(total_bytes / t_st / 1e9, 1),
+                         "pcie_GBps": round(host_bytes / t_st / 1e9, 2),
+                         "pct_of_h2d_ceiling": round(100 * host_bytes / t_st / 1e9 / h2d_gbs, 1),
+                         "tokens_per_s_256_steps": round(m / t_st, 1)}}
+
+
+def bench_moe_stack(timer_cls):
+    """One 235B-A22B-shaped layer (attention 64 / 4 heads of 128 over hidden
+    4096, 128 experts of SwiGLU 1536, top-8), timed at decode (batch 1) and
+    prefill (2048 tokens), all-HBM and with 40 % of its experts on host;
+    the 94-layer figures are 94 x one layer."""
+    import torch
+
+    import synth
+    from synth import configs
+    from synth.calibrate_router_bias import load_bias
+    from paper_2607_10183_amd.session import MoEDecoderLayer, Session
+
+    wl = configs.MOE_STACK
+    ds, ms = wl.dense, wl.moe
+    H, E, I, k = ms.hidden, ms.n_experts, ms.inter, ms.top_k
+    layer = 0
+    log("generating one MoE-stack layer")
+    sess = Session(workspace_bytes=3 << 30, n_slots=24)
+    timer = timer_cls(sess.cs)
+    a = {r: sess.register(synth.int4_codes(wl.seed, configs.dense_uid(layer, r), ds.kn(r)[1], ds.kn(r)[0]),
+                          synth.group_scales(wl.seed, configs.dense_uid(layer, r), ds.kn(r)[1], ds.kn(r)[0]))
+         for r in ("q", "k", "v", "o")}
+    tids = [[], [], []]
+    for e in range(E):
+        group = []
+        for p, (n, kk) in zip(("gate", "up", "down"), ((I, H), (I, H), (H, I))):
+            uid = configs.expert_uid(layer, e, p)
+            group.append((synth.int4_codes(wl.seed, uid, n, kk), synth.group_scales(wl.seed, uid, n, kk)))
+        for j, t in enumerate(sess.register_group(group, hbm=True, host=True)):
+            tids[j].append(t)
+    wr = torch.from_numpy(synth.router_weights(wl.seed, configs.router_uid(layer), H, E)).cuda()
+    moe = sess.moe_layer(wr, *tids, top_k=k, router_bias=torch.from_numpy(load_bias()).cuda())
+    L = MoEDecoderLayer(moe, a["q"], a["k"], a["v"], a["o"], ds.n_heads, ds.n_kv, ds.head_dim, 1e-6)
+    hd = torch.from_numpy(synth.activations(wl.seed, 1, 32, H)).cuda()
+    hp = torch.from_numpy(synth.activations(wl.seed, 2, wl.prefill_m, H)).cuda()
+    sess.cs.wait_stream(torch.cuda.current_stream())
+    attn_bytes = sum(configs.qbytes(*ds.kn(r)) for r in ("q", "k", "v", "o"))
+    expert_bytes = 3 * configs.qbytes(H, I)
+
+    def measure():
+        def dec():
+            for t in range(32):
+                L(hd[t:t + 1])
+        timer.run(dec, 1)
+        t_dec = timer.run(dec, 2) / 32
+        timer.run(lambda: L(hp), 1)
+        t_pf = timer.run(lambda: L(hp), 3)
+        return t_dec, t_pf
+
+    d_hbm, p_hbm = measure()
+    host_exp = configs.moe_host_experts(frac=0.40, seed=wl.seed, layer=layer)
+    pl = list(sess.placement)
+    for j in range(3):
+        for e in range(E):
+            pl[tids[j][e]] = int(host_exp[e])
+    sess.set_placement(pl)
+    d_st, p_st = measure()
+    # experts the prefill actually routes to, and how many of those are on host
+    dbg = L(torch.from_numpy(synth.activations(wl.seed, 2, wl.prefill_m, H)).cuda(), debug=True)
+    sess.sync()
+    counts = dbg["counts"].cpu().numpy()
+    n_act = int((counts > 0).sum())
+    n_host_act = int(((counts > 0) & (host_exp > 0)).sum())
+    sess.close()
+    pf_flops = 2.0 * wl.prefill_m * (attn_bytes * 16 / 9 + k * expert_bytes * 16 / 9)  # 2 M K N per weight
+    log(f"moe stack layer: decode {d_hbm * 1e3:.3f} ms ({d_st * 1e3:.3f} streamed), prefill {p_hbm * 1e3:.2f} ms "
+        f"({p_st * 1e3:.2f} streamed, {n_host_act} of {n_act} active experts on host -> "
+        f"{n_host_act * expert_bytes / p_st / 1e9:.1f} GB/s PCIe); x94: {94 * d_hbm * 1e3:.1f} ms/token all-HBM")
+    return {"workload": "moe_stack: one 235B-A22B-shaped layer (attention 64/4 heads of 128, hidden 4096, "
+                        "128 experts of SwiGLU 1536, top-8, capped-Zipf routing); 94-layer figures are 94 x the layer",
+            "all_hbm": {"decode_ms_per_layer": round(d_hbm * 1e3, 4), "prefill_ms_per_layer": round(p_hbm * 1e3, 3),
+                        "decode_tokens_per_s_94_layers": round(1.0 / (94 * d_hbm), 2),
+                        "prefill_tokens_per_s_94_layers": round(wl.prefill_m / (94 * p_hbm), 1),
+                        "prefill_TFLOPs": round(pf_flops / p_hbm / 1e12, 1)},
+            "prefill_active_experts": n_act, "prefill_active_host_experts": n_host_act,
+            "streamed_40pct_experts": {"decode_ms_per_layer": round(d_st * 1e3, 4),
+                                       "prefill_ms_per_layer": round(p_st * 1e3, 3),
+                                       "prefill_pcie_GBps": round(n_host_act * expert_bytes / p_st / 1e9, 2),
+                                       "decode_tokens_per_s_94_layers": round(1.0 / (94 * d_st), 2),
+                                       "prefill_tokens_per_s_94_layers": round(wl.prefill_m / (94 * p_st), 1)}}
 
 
 def cpu_baseline(W, shape, budget_s, layer_bytes):

@@ -533,9 +533,28 @@ atsi_status run_op(atsi_ctx* c, LinOp& op, const atsi_tid* tids, int ntids) {
       op.seg[i].w = v;
     }
   }
-  const bool gemv = gemv_supported(op.M, op.K);
-  hipError_t e = gemv ? launch_gemv(op, c->cs) : launch_gemm(op, c->cs);
-  if (e != hipSuccess) return hip_fail(c, e, gemv ? "q4 gemv launch" : "q4 gemm launch");
+  // decode sizes: up to 4 tokens run as GEMV launches of at most
+  // gemv_tokens(K) tokens each, up to 16 on the matrix cores with the codes
+  // read once; larger batches run the MFMA GEMM
+  const int mt = gemv_tokens(op.K);
+  if (op.M < kSkinnyMinTokens && mt > 0) {
+    for (int m0 = 0; m0 < op.M; m0 += mt) {
+      LinOp sub = op;
+      sub.M = std::min(mt, op.M - m0);
+      sub.x = op.x + (size_t)m0 * op.K;
+      for (int s = 0; s < op.nseg; ++s) sub.seg[s].y = op.seg[s].y + (size_t)m0 * op.seg[s].ldy;
+      if (op.res) sub.res = op.res + (size_t)m0 * op.seg[0].ldy;
+      if (op.y32) sub.y32 = op.y32 + (size_t)m0 * op.seg[0].ldy;
+      hipError_t e = launch_gemv(sub, c->cs);
+      if (e != hipSuccess) return hip_fail(c, e, "q4 gemv launch");
+    }
+  } else if (op.M <= kSkinnyMaxTokens && skinny_supported(op)) {
+    hipError_t e = launch_skinny(op, c->cs);
+    if (e != hipSuccess) return hip_fail(c, e, "q4 batched-decode launch");
+  } else {
+    hipError_t e = launch_gemm(op, c->cs);
+    if (e != hipSuccess) return hip_fail(c, e, "q4 gemm launch");
+  }
   return release(c, held);
 }
 

@@ -61,10 +61,20 @@ __device__ __forceinline__ uint16_t ldg2(const uint16_t* p) {
 }
 
 // ---- launchers (each returns hipGetLastError() of its launch) ----
-constexpr size_t kGemvMaxLds = 64 * 1024;  // activations staged per GEMV workgroup
-// decode GEMV handles 1 <= M <= 4 when its staged activations fit in LDS
-bool gemv_supported(int M, int K);
+// LDS one workgroup may use on the current device (160 KiB on gfx950)
+size_t lds_limit();
+// Tokens one decode-GEMV launch takes for inputs K wide: 4, 2 or 1, the most
+// whose staged activations fit in LDS (0 if not even one does).  Calls with
+// up to 4 tokens run as GEMV launches of at most that many tokens.
+int gemv_tokens(int K);
+constexpr int kGemvMaxTokens = 4;
 hipError_t launch_gemv(const LinOp& op, hipStream_t s);
+// batched decode on the matrix cores: 1 <= M <= kSkinnyMaxTokens, any K
+// divisible by 32, tensors below 2 GiB
+constexpr int kSkinnyMaxTokens = 16;
+constexpr int kSkinnyMinTokens = 5;  // fewer tokens go to the GEMV
+bool skinny_supported(const LinOp& op);
+hipError_t launch_skinny(const LinOp& op, hipStream_t s);
 hipError_t launch_gemm(const LinOp& op, hipStream_t s);
 hipError_t launch_unpack(const QView& w, int8_t* q, hipStream_t s);
 

@@ -176,20 +176,7 @@ __device__ __forceinline__ void compute_step(const Step<RW, CPL, SWI>& cur, cons
         v = silu_f(v) * u;
       }
       const int row = row0 + r;
-      if (lane == r * MT + m && row < N && m < M) {
-        if (sg.expand > 1) {
-          const int hd = op.head_dim, jh = row / hd, d = row % hd;
-          const __half o = __float2half_rn(v);
-          for (int g = 0; g < sg.expand; ++g) sg.y[(size_t)m * sg.ldy + (size_t)(jh * sg.expand + g) * hd + d] = o;
-        } else {
-          const size_t at = (size_t)m * sg.ldy + row;
-          if (op.res && s == 0) v += __half2float(op.res[at]);
-          if (op.y32 && s == 0)
-            op.y32[at] = v;
-          else
-            sg.y[at] = __float2half_rn(v);
-        }
-      }
+      if (lane == r * MT + m && row < N && m < M) emit_out(op, sg, s, m, row, v);
     }
 }
 
@@ -241,7 +228,9 @@ hipError_t launch_cfg(const LinOp& op, hipStream_t st) {
   }
   const int nchunk = op.K / kGroup;
   const size_t lds = (size_t)4 * MT * nchunk * 16 + (size_t)MT * nchunk * 4;
-  if (lds > kGemvMaxLds) return hipErrorInvalidValue;  // callers check gemv_supported()
+  // HIP admits dynamic LDS up to the device's per-workgroup limit without a
+  // function attribute
+  if (lds > lds_limit()) return hipErrorInvalidValue;  // callers check gemv_tokens()
   hipLaunchKernelGGL((q4_gemv_kernel<MT, RW, CPL, SWI, SPW>), dim3(total), dim3(kBlock), lds, st, op, bm);
   return hipGetLastError();
 }
@@ -283,9 +272,25 @@ int default_spw(const LinOp& op) {
 
 }  // namespace
 
-bool gemv_supported(int M, int K) {
-  const int mt = M == 1 ? 1 : (M == 2 ? 2 : 4);
-  return M >= 1 && M <= 4 && (size_t)mt * (K / kGroup) * 68 <= kGemvMaxLds;
+size_t lds_limit() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 64 * 1024;
+  if (!cached[dev]) {
+    int v = 0;
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess || v <= 0)
+      v = 64 * 1024;
+    cached[dev] = v;
+  }
+  return (size_t)cached[dev];
+}
+
+int gemv_tokens(int K) {
+  const size_t per_token = (size_t)(K / kGroup) * 68;
+  const size_t lim = lds_limit();
+  for (int mt = kGemvMaxTokens; mt >= 1; mt /= 2)
+    if (mt * per_token <= lim) return mt;
+  return 0;
 }
 
 hipError_t launch_gemv(const LinOp& op, hipStream_t st) {

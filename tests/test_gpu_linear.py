@@ -35,9 +35,11 @@ def test_unpack_bitexact(sess, host):
     assert np.array_equal(q.cpu().numpy(), oracle.unpack_codes(codes))
 
 
-EXACT_SHAPES = [  # (K, N, M): GEMV for M <= 4, GEMM above; ragged N and M
+EXACT_SHAPES = [  # (K, N, M): GEMV launches for M <= 8 (8 tokens per launch up to K = 8192, chunks
+    # of fewer tokens for wider inputs), GEMM above; ragged N and M
     (32, 7, 1), (96, 33, 3), (768, 2048, 1), (4096, 1000, 4), (14336, 257, 2), (4096, 4096, 1),
     (4096, 1000, 5), (768, 300, 64), (4096, 520, 100), (14336, 130, 512), (2048, 4096, 16), (96, 65, 129),
+    (4096, 700, 8), (8192, 300, 7), (14336, 257, 8), (14336, 130, 6), (256, 96, 8),
 ]
 
 
@@ -59,7 +61,7 @@ def test_exact_arithmetic_bitexact(sess, K, N, M):
 RANDOM_SHAPES = [  # linear4096 (decode 1, batch 16) and the dense-layer tensors
     (4096, 4096, 1), (4096, 4096, 16), (4096, 1024, 1), (4096, 14336, 1), (14336, 4096, 1),
     (4096, 4096, 2), (4096, 1024, 4), (4096, 1024, 512), (4096, 14336, 512), (14336, 4096, 512),
-    (4096, 4096, 3), (2048, 768, 37),
+    (4096, 4096, 3), (2048, 768, 37), (4096, 14336, 8), (14336, 4096, 8), (4096, 6144, 5),
 ]
 
 
