@@ -102,11 +102,11 @@ atsi_status atsi_tensor_register(atsi_ctx* ctx, const atsi_qtensor* t, atsi_tid*
 atsi_status atsi_set_placement(atsi_ctx* ctx, const uint8_t* host_mask, int32_t n);
 
 /* y[M][N] = x[M][K] . W^T for tensor w (fp16 in and out, fp32 accumulation).
- * Decode sizes run kernels that read the codes once per launch: M <= 4 a
- * dequantising GEMV (up to 4 tokens per launch, fewer for inputs too wide for
- * the device's LDS), 5 <= M <= 16 a batched-decode kernel on the matrix cores;
- * larger M runs a dequantise-into-LDS fp16 MFMA GEMM (prefill, Sec. 2.2 and
- * the chunked prefill of Sec. 5.1).  A
+ * Decode sizes run kernels that read the codes once per launch: M = 1 a
+ * dequantising GEMV, 2 <= M <= 16 a batched-decode kernel on the matrix cores
+ * (for K not a multiple of 128, M <= 4 runs GEMV launches instead); larger M
+ * runs a dequantise-into-LDS fp16 MFMA GEMM (prefill, Sec. 2.2 and the
+ * chunked prefill of Sec. 5.1).  A
  * host-resident w is first copied into a temporary buffer on the transfer
  * stream (Sec. 4.2.2).  1 <= M <= 65536. */
 atsi_status atsi_linear(atsi_ctx* ctx, atsi_tid w, const void* x_f16, int64_t M, void* y_f16);

@@ -533,11 +533,13 @@ atsi_status run_op(atsi_ctx* c, LinOp& op, const atsi_tid* tids, int ntids) {
       op.seg[i].w = v;
     }
   }
-  // decode sizes: up to 4 tokens run as GEMV launches of at most
-  // gemv_tokens(K) tokens each, up to 16 on the matrix cores with the codes
-  // read once; larger batches run the MFMA GEMM
+  // decode sizes: one token runs the GEMV, 2 to 16 the batched-decode kernel
+  // on the matrix cores (both read the codes once); where that kernel does
+  // not apply (K not a multiple of 128), up to 4 tokens run as GEMV launches
+  // of at most gemv_tokens(K) tokens each; larger batches run the MFMA GEMM
   const int mt = gemv_tokens(op.K);
-  if (op.M < kSkinnyMinTokens && mt > 0) {
+  const bool skinny = op.M >= kSkinnyMinTokens && op.M <= kSkinnyMaxTokens && skinny_supported(op);
+  if (!skinny && op.M <= kGemvMaxTokens && mt > 0) {
     for (int m0 = 0; m0 < op.M; m0 += mt) {
       LinOp sub = op;
       sub.M = std::min(mt, op.M - m0);
@@ -548,7 +550,7 @@ atsi_status run_op(atsi_ctx* c, LinOp& op, const atsi_tid* tids, int ntids) {
       hipError_t e = launch_gemv(sub, c->cs);
       if (e != hipSuccess) return hip_fail(c, e, "q4 gemv launch");
     }
-  } else if (op.M <= kSkinnyMaxTokens && skinny_supported(op)) {
+  } else if (skinny) {
     hipError_t e = launch_skinny(op, c->cs);
     if (e != hipSuccess) return hip_fail(c, e, "q4 batched-decode launch");
   } else {

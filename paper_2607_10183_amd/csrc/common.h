@@ -69,10 +69,10 @@ size_t lds_limit();
 int gemv_tokens(int K);
 constexpr int kGemvMaxTokens = 4;
 hipError_t launch_gemv(const LinOp& op, hipStream_t s);
-// batched decode on the matrix cores: 1 <= M <= kSkinnyMaxTokens, any K
-// divisible by 32, tensors below 2 GiB
+// batched decode on the matrix cores: 1 <= M <= kSkinnyMaxTokens, K
+// divisible by 128, tensors below 2 GiB
 constexpr int kSkinnyMaxTokens = 16;
-constexpr int kSkinnyMinTokens = 5;  // fewer tokens go to the GEMV
+constexpr int kSkinnyMinTokens = 2;  // a single token goes to the GEMV
 bool skinny_supported(const LinOp& op);
 hipError_t launch_skinny(const LinOp& op, hipStream_t s);
 hipError_t launch_gemm(const LinOp& op, hipStream_t s);

@@ -18,10 +18,15 @@
 //   * the (k, k+4) pair order that nibble extraction yields is matched by
 //     permuting the activations of each lane's 8 inputs the same way;
 //   * a workgroup owns 16 weight rows; its waves split K into contiguous
-//     stretches of groups, each wave keeping D - 1 groups of loads in flight,
-//     and their partial sums meet in LDS;
+//     stretches, each wave keeping D - 1 steps of four groups in flight, and
+//     their partial sums meet in LDS;
+//   * the MFMA operand layout puts four different rows (or tokens) in every
+//     four consecutive lanes, which defeats load coalescing (each lane's
+//     access becomes a cache access of its own), so the loads use a layout
+//     where four consecutive lanes read one contiguous run and each wave
+//     restages the data through its own slice of LDS;
 //   * all loads are buffer loads whose out-of-range lanes read zeros: rows
-//     past N, tokens past M and groups past K need no clamping or branches;
+//     past N, tokens past M and steps past K need no clamping or branches;
 //   * a fused RMS norm takes the per-token sum of squares from one more MFMA
 //     per group (the activations times themselves; the diagonal of the
 //     product is what is kept).
@@ -96,17 +101,37 @@ __device__ __forceinline__ h8_t perm_x(u4_t d) {
   return __builtin_bit_cast(h8_t, r);
 }
 
-// Loads of one group for one lane.
-template <bool SWI>
-struct GroupLd {
-  uint32_t c[SWI ? 2 : 1];  // code word of its row (gate and up for SwiGLU)
-  uint16_t s[SWI ? 2 : 1];  // the row's scale of the group
-  u4_t x;                   // its token's 8 activations
+// One step is four consecutive groups (128 inputs) of the wave's 16 rows.
+// Global loads are laid out for coalescing, four consecutive lanes reading
+// one contiguous run, and each wave restages them through its own LDS into
+// the MFMA lanes' layout (lane n + 16 c takes row n, 8-input chunk c):
+//   codes   lane l: row l/4, group l%4 of the step, 16 bytes;
+//   scales  lane l: row l/4, group l%4, 2 bytes;
+//   x       lane l of load i: token l/16 + 4 i, 16 bytes (chunk l%16) of the
+//           step's 128 inputs, permuted to the codes' pair order on the way.
+constexpr int kCStride = 80;   // LDS bytes per row of staged codes (64 + pad)
+constexpr int kXStride = 272;  // LDS bytes per token of staged x (256 + pad)
+
+template <bool SWI, int MX>
+struct StepLd {
+  u4_t c[SWI ? 2 : 1];      // 16 code bytes (gate and up for SwiGLU)
+  uint32_t s[SWI ? 2 : 1];  // one scale in the low half
+  u4_t x[MX];               // 8 activations of a token
 };
 
-template <int NW, int D, bool SWI, bool NORM>
+template <bool SWI, int MX>
+struct WaveLds {
+  static constexpr int NT = SWI ? 2 : 1;
+  static constexpr int XR = 4 * MX + 1;  // staged tokens and a zero row
+  __attribute__((aligned(16))) uint8_t codes[NT][16 * kCStride];
+  __attribute__((aligned(16))) uint8_t x[XR * kXStride];
+  __attribute__((aligned(16))) uint16_t sc[NT][16 * 4];
+};
+
+template <int NW, int D, int MX, bool SWI, bool NORM>
 __global__ __launch_bounds__(NW * 64) void q4_skinny_kernel(LinOp op, SkinnyMap bm) {
   constexpr int NT = SWI ? 2 : 1;
+  __shared__ WaveLds<SWI, MX> wl[NW];
   __shared__ f4_t red[NT][NW][64];
   __shared__ float sq[NW][16];
   __shared__ float inv_r[16];
@@ -116,9 +141,10 @@ __global__ __launch_bounds__(NW * 64) void q4_skinny_kernel(LinOp op, SkinnyMap 
   const Seg& sg = op.seg[s];
   const int K = op.K, G = K / kGroup, M = op.M, N = sg.w.N;
   const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform: group offsets stay scalar
-  const int j = lane & 15, kb = lane >> 4;  // B column (weight row) / A row (token); 8-input chunk
-  const int row = local * kRows + j;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform: step offsets stay scalar
+  const int j = lane & 15, kb = lane >> 4;  // MFMA roles: B column (row) / A row (token); 8-input chunk
+  const int row0 = local * kRows;
+  WaveLds<SWI, MX>& L = wl[wave];
 
   __amdgpu_buffer_rsrc_t rc[NT], rs[NT];
   rc[0] = rsrc(sg.w.codes, (uint32_t)((size_t)N * K / 2));
@@ -128,78 +154,102 @@ __global__ __launch_bounds__(NW * 64) void q4_skinny_kernel(LinOp op, SkinnyMap 
     rs[1] = rsrc(sg.w2.scales, (uint32_t)((size_t)N * G * 2));
   }
   const __amdgpu_buffer_rsrc_t rx = rsrc(op.x, (uint32_t)((size_t)M * K * 2));
-  const uint32_t oc = (uint32_t)row * (uint32_t)(K / 2) + (uint32_t)kb * 4;
-  const uint32_t os = (uint32_t)row * (uint32_t)G * 2;
-  const uint32_t ox = ((uint32_t)j * (uint32_t)K + (uint32_t)kb * 8) * 2;
+  // load roles: codes/scales row lr, group lg of the step; x token xm + 4 i, chunk xc
+  const int lr = lane >> 2, lg = lane & 3, xm = lane >> 4, xc = lane & 15;
+  const uint32_t oc = (uint32_t)(row0 + lr) * (uint32_t)(K / 2) + (uint32_t)lg * 16;  // + 64 per step
+  const uint32_t os = ((uint32_t)(row0 + lr) * (uint32_t)G + (uint32_t)lg) * 2;     // + 8 per step
+  const uint32_t ox = ((uint32_t)xm * (uint32_t)K + (uint32_t)xc * 8) * 2;           // + 256 per step
 
-  // Wave w owns groups [w * ngw, (w + 1) * ngw): at any moment the waves of a
-  // workgroup read different stretches of their rows, so the requests in
-  // flight spread over the HBM channels (waves taking interleaved groups all
-  // hit the same few bytes of rows 2 KiB apart, and the channels behind
-  // those addresses).  Past the wave's last group every offset is out of
-  // range: the load reads zeros and moves no data.
-  const int ngw = (G + NW - 1) / NW;
-  const int g0 = wave * ngw, g1 = min(g0 + ngw, G);
-  auto load = [&](GroupLd<SWI>& b, int i) {
-    const int g = g0 + i;
-    const bool ok = g < g1;
-    const uint32_t gc = ok ? (uint32_t)g * 16 : kOob, gs = ok ? (uint32_t)g * 2 : kOob,
-                   gx = ok ? (uint32_t)g * 64 : kOob;
+  // wave w owns steps [s0, s1) of ceil(G / 4): a contiguous stretch of its
+  // rows, so the waves of a workgroup read different parts of them at once
+  const int nstep = G / 4;  // K % 128 == 0
+  const int spw = (nstep + NW - 1) / NW;
+  const int s0 = wave * spw, s1 = min(s0 + spw, nstep);
+  auto load = [&](StepLd<SWI, MX>& b, int st) {
+    const bool ok = st < s1;  // uniform; past the stretch every load reads zeros
+    const uint32_t dc = ok ? (uint32_t)st * 64 : kOob, ds = ok ? (uint32_t)st * 8 : kOob,
+                   dx = ok ? (uint32_t)st * 256 : kOob;
+#pragma unroll
+    for (int t = 0; t < NT; ++t) b.c[t] = __builtin_amdgcn_raw_buffer_load_b128(rc[t], oc + dc, 0, 0);
+#pragma unroll
+    for (int t = 0; t < NT; ++t) b.s[t] = __builtin_amdgcn_raw_buffer_load_b16(rs[t], os + ds, 0, 0);
+#pragma unroll
+    for (int i = 0; i < MX; ++i)
+      b.x[i] = __builtin_amdgcn_raw_buffer_load_b128(rx, ox + (uint32_t)i * 4 * K * 2 + dx, 0, 0);
+  };
+  // staging writes: codes at [row][group] 16 B, scales [row][group], x [token][128 inputs]
+  auto stage = [&](const StepLd<SWI, MX>& b) {
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
-      b.c[t] = __builtin_amdgcn_raw_buffer_load_b32(rc[t], oc + gc, 0, 0);
-      b.s[t] = __builtin_amdgcn_raw_buffer_load_b16(rs[t], os + gs, 0, 0);
+      *reinterpret_cast<u4_t*>(&L.codes[t][lr * kCStride + lg * 16]) = b.c[t];
+      L.sc[t][lr * 4 + lg] = (uint16_t)b.s[t];
     }
-    b.x = __builtin_amdgcn_raw_buffer_load_b128(rx, ox + gx, 0, 0);
-  };
-
-  // Software pipeline, one region per group with nothing moved across
-  // regions: region i computes group i's MFMA, applies the previous group's
-  // scale (its MFMA has finished by then), and refills the buffer it used
-  // with group i + D.  Loads keep one order, so each region waits for its own
-  // group's loads only and D - 1 groups stay in flight.
-  const int nit = (ngw + D - 1) / D;
-  const UnpackK uk = unpack_consts();
-  GroupLd<SWI> buf[D];
 #pragma unroll
-  for (int d = 0; d < D; ++d) {
-    load(buf[d], d);
-    __builtin_amdgcn_sched_barrier(0);
-  }
+    for (int i = 0; i < MX; ++i) {
+      *reinterpret_cast<h8_t*>(&L.x[(xm + 4 * i) * kXStride + xc * 16]) = perm_x(b.x[i]);
+    }
+  };
+  // the zero row: A rows past the staged tokens read it
+  if (lane < kXStride / 16)
+    *reinterpret_cast<u4_t*>(&L.x[4 * MX * kXStride + lane * 16]) = u4_t{0u, 0u, 0u, 0u};
+  const int arow = j < 4 * MX ? j : 4 * MX;
+  const uint8_t* xa = &L.x[arow * kXStride + kb * 16];   // + 64 per group
+  const UnpackK uk = unpack_consts();
 
   const f4_t zero = {0.f, 0.f, 0.f, 0.f};
-  f4_t acc[NT], prev[NT], gram = zero;
-  float prev_s[NT];
+  f4_t acc[NT], gram = zero;
 #pragma unroll
-  for (int t = 0; t < NT; ++t) {
-    acc[t] = zero;
-    prev[t] = zero;
-    prev_s[t] = 0.f;
+  for (int t = 0; t < NT; ++t) acc[t] = zero;
+  // compute one staged step: four MFMAs per tensor, each one group
+  // (all LDS reads of the step go out before the first MFMA needs one)
+  auto compute = [&]() {
+    uint2 sv[NT];
+    u4_t xa4[4];
+    uint32_t w4[NT][4];
+#pragma unroll
+    for (int g = 0; g < 4; ++g) xa4[g] = *reinterpret_cast<const u4_t*>(xa + g * 64);
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+#pragma unroll
+      for (int g = 0; g < 4; ++g)
+        w4[t][g] = *reinterpret_cast<const uint32_t*>(&L.codes[t][j * kCStride + g * 16 + kb * 4]);
+      sv[t] = *reinterpret_cast<const uint2*>(&L.sc[t][j * 4]);
+    }
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const h8_t a = __builtin_bit_cast(h8_t, xa4[g]);
+      if constexpr (NORM) gram = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, a, gram, 0, 0, 0);
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        const f4_t p = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, unpack_q(w4[t][g], uk), zero, 0, 0, 0);
+        const uint32_t pair = g < 2 ? sv[t].x : sv[t].y;
+        const float sc = __half2float(__ushort_as_half((uint16_t)((g & 1) ? pair >> 16 : pair)));
+#pragma unroll
+        for (int v = 0; v < 4; ++v) acc[t][v] = fmaf(sc, p[v], acc[t][v]);
+      }
+    }
+  };
+
+  // Software pipeline over steps, one region per step with nothing moved
+  // across regions: stage step st from its registers into LDS, refill those
+  // registers with step st + D, compute step st.  Loads keep one order, so
+  // each region waits for its own step only and D - 1 steps stay in flight.
+  StepLd<SWI, MX> buf[D];
+#pragma unroll
+  for (int d = 0; d < D; ++d) {
+    load(buf[d], s0 + d);
+    __builtin_amdgcn_sched_barrier(0);
   }
+  const int nit = (spw + D - 1) / D;
   for (int it = 0; it < nit; ++it) {
 #pragma unroll
     for (int d = 0; d < D; ++d) {
-      GroupLd<SWI>& b = buf[d];
-      const h8_t a = perm_x(b.x);
-      if constexpr (NORM) gram = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, a, gram, 0, 0, 0);
-      f4_t p[NT];
-#pragma unroll
-      for (int t = 0; t < NT; ++t) p[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, unpack_q(b.c[t], uk), zero, 0, 0, 0);
-#pragma unroll
-      for (int t = 0; t < NT; ++t) {
-#pragma unroll
-        for (int v = 0; v < 4; ++v) acc[t][v] = fmaf(prev_s[t], prev[t][v], acc[t][v]);
-        prev[t] = p[t];
-        prev_s[t] = __half2float(__ushort_as_half(b.s[t]));
-      }
-      load(b, (it + 1) * D + d);
+      stage(buf[d]);
+      load(buf[d], s0 + (it + 1) * D + d);
+      compute();
       __builtin_amdgcn_sched_barrier(0);
     }
   }
-#pragma unroll
-  for (int t = 0; t < NT; ++t)
-#pragma unroll
-    for (int v = 0; v < 4; ++v) acc[t][v] = fmaf(prev_s[t], prev[t][v], acc[t][v]);
 
   // partial sums of the waves meet in LDS; D[m][n] sits in lane n + 16 (m / 4), item m % 4
 #pragma unroll
@@ -217,6 +267,7 @@ __global__ __launch_bounds__(NW * 64) void q4_skinny_kernel(LinOp op, SkinnyMap 
     }
     __syncthreads();
   }
+  const int row = row0 + j;
   if (wave != 0 || row >= N) return;
   f4_t v[NT];
 #pragma unroll
@@ -236,7 +287,7 @@ __global__ __launch_bounds__(NW * 64) void q4_skinny_kernel(LinOp op, SkinnyMap 
   }
 }
 
-template <int NW, int D, bool SWI, bool NORM>
+template <int NW, int D, int MX, bool SWI, bool NORM>
 hipError_t launch_cfg(const LinOp& op, hipStream_t st) {
   SkinnyMap bm{};
   int total = 0;
@@ -244,19 +295,28 @@ hipError_t launch_cfg(const LinOp& op, hipStream_t st) {
     total += (op.seg[s].w.N + kRows - 1) / kRows;
     bm.end[s] = total;
   }
-  hipLaunchKernelGGL((q4_skinny_kernel<NW, D, SWI, NORM>), dim3(total), dim3(NW * 64), 0, st, op, bm);
+  hipLaunchKernelGGL((q4_skinny_kernel<NW, D, MX, SWI, NORM>), dim3(total), dim3(NW * 64), 0, st, op, bm);
   return hipGetLastError();
+}
+
+template <int MX, bool SWI>
+hipError_t launch_mx(const LinOp& op, hipStream_t st) {
+  // eight waves, two steps of loads in flight while a step is computed:
+  // the fastest of 4 / 8 waves and 2 / 3 / 4 steps measured on MI355X
+  return op.norm ? launch_cfg<8, 2, MX, SWI, true>(op, st) : launch_cfg<8, 2, MX, SWI, false>(op, st);
 }
 
 template <bool SWI>
 hipError_t launch_sw(const LinOp& op, hipStream_t st) {
-  return op.norm ? launch_cfg<8, 8, SWI, true>(op, st) : launch_cfg<8, 8, SWI, false>(op, st);
+  if (op.M <= 4) return launch_mx<1, SWI>(op, st);
+  if (op.M <= 8) return launch_mx<2, SWI>(op, st);
+  return launch_mx<4, SWI>(op, st);
 }
 
 }  // namespace
 
 bool skinny_supported(const LinOp& op) {
-  if (op.M < 1 || op.M > kSkinnyMaxTokens || op.K % kGroup) return false;
+  if (op.M < 1 || op.M > kSkinnyMaxTokens || op.K % (4 * kGroup)) return false;
   // 32-bit buffer offsets
   if ((size_t)op.M * op.K * 2 >= kOob) return false;
   for (int s = 0; s < op.nseg; ++s) {

@@ -35,11 +35,12 @@ def test_unpack_bitexact(sess, host):
     assert np.array_equal(q.cpu().numpy(), oracle.unpack_codes(codes))
 
 
-EXACT_SHAPES = [  # (K, N, M): GEMV launches for M <= 8 (8 tokens per launch up to K = 8192, chunks
-    # of fewer tokens for wider inputs), GEMM above; ragged N and M
+EXACT_SHAPES = [  # (K, N, M): GEMV for M = 1, the batched-decode kernel for 2 <= M <= 16 when
+    # K % 128 == 0 (else GEMV launches up to M = 4, GEMM above), GEMM for larger M; ragged N and M
     (32, 7, 1), (96, 33, 3), (768, 2048, 1), (4096, 1000, 4), (14336, 257, 2), (4096, 4096, 1),
     (4096, 1000, 5), (768, 300, 64), (4096, 520, 100), (14336, 130, 512), (2048, 4096, 16), (96, 65, 129),
     (4096, 700, 8), (8192, 300, 7), (14336, 257, 8), (14336, 130, 6), (256, 96, 8),
+    (160, 70, 2), (224, 50, 4), (96, 40, 6), (128, 20, 16), (384, 17, 3),
 ]
 
 
