@@ -80,6 +80,14 @@ class Timer:
         return self.a.elapsed_time(self.b) * 1e-3 / n
 
 
+def h2d_timed(sess, timer, fn, n: int):
+    """(seconds per call, host-to-device bytes the engine copied per call) of
+    fn over n timed calls; the bytes come from the library's own counters."""
+    sess.stats(reset=True)
+    t = timer.run(fn, n)
+    return t, sess.stats(reset=True)["h2d_bytes"] / n
+
+
 def kernel_hash(kind: str) -> str:
     """sha256 of the sources a roofline kernel is built from."""
     import hashlib
@@ -166,6 +174,8 @@ def main() -> int:
     hp = torch.from_numpy(synth.activations(wl.seed, 2, Mp, shape.hidden)).to(dev)
     cs.wait_stream(torch.cuda.current_stream())
 
+    # a dense layer does the same work whatever h holds, so timed calls keep
+    # updating h in place (the MoE stack below restores its inputs instead)
     def layer(c, h, M):
         atsi.atsi_decoder_layer(sess.ctx, descs[c], h.data_ptr(), M, 0, 0)
 
@@ -274,14 +284,15 @@ def main() -> int:
     sess.set_placement(mask)
     sess.set_schedule(order)
     n_sd = 40
-    st_dec = timer.run(lambda: layer(0, h1, 1), n_sd)
+    st_dec, h2d_dec = h2d_timed(sess, timer, lambda: layer(0, h1, 1), n_sd)
     sess.set_placement(mask)
     sess.set_schedule(order)
-    st_pf = timer.run(lambda: layer(0, hp, Mp), 10)
+    st_pf, h2d_pf = h2d_timed(sess, timer, lambda: layer(0, hp, Mp), 10)
     sess.set_schedule([])
     sess.set_placement([0] * len(sess.shapes))
     log(f"streamed decode {st_dec * 1e3:.3f} ms, prefill {st_pf * 1e3:.3f} ms ({host_roles} on host, "
-        f"{host_bytes / 1e6:.1f} MB) -> PCIe {host_bytes / st_dec / 1e9:.1f} GB/s")
+        f"{host_bytes / 1e6:.1f} MB; copied per call {h2d_dec / 1e6:.1f} / {h2d_pf / 1e6:.1f} MB) -> PCIe "
+        f"{h2d_dec / st_dec / 1e9:.1f} GB/s")
 
     moe = None if args.no_moe else bench_moe(sess, timer, args)
     stacks = None
@@ -336,8 +347,9 @@ def main() -> int:
         "streamed": {"host_tensors": host_roles, "host_bytes": host_bytes,
                      "decode_ms": round(st_dec * 1e3, 4), "prefill_ms": round(st_pf * 1e3, 4),
                      "decode_weight_GBps_pcie_inclusive": round(layer_bytes / st_dec / 1e9, 2),
-                     "decode_pcie_GBps": round(host_bytes / st_dec / 1e9, 2),
-                     "decode_pct_of_h2d_ceiling": round(100 * host_bytes / st_dec / 1e9 / h2d_gbs, 1),
+                     "decode_h2d_bytes_per_call": int(h2d_dec), "prefill_h2d_bytes_per_call": int(h2d_pf),
+                     "decode_pcie_GBps": round(h2d_dec / st_dec / 1e9, 2),
+                     "decode_pct_of_h2d_ceiling": round(100 * h2d_dec / st_dec / 1e9 / h2d_gbs, 1),
                      "prefill_exposed_ms": round(max(0.0, st_pf - prefill_s) * 1e3, 4),
                      "prefill_tokens_per_s": round(Mp / st_pf, 1)},
         "moe": moe,
@@ -408,15 +420,15 @@ def bench_moe(sess, timer, args):
         for e in range(E):
             mask[tids[j][e]] = int(host_exp[e])
     sess.set_placement(mask)
-    st_dec = timer.run(lambda: [layer(xd[t:t + 1], yd[t:t + 1]) for t in range(32)], 1) / 32
-    st_pf = timer.run(lambda: layer(xp, yp), 3)
+    st_dec, h2d_dec = h2d_timed(sess, timer, lambda: [layer(xd[t:t + 1], yd[t:t + 1]) for t in range(32)], 1)
+    st_dec, h2d_dec = st_dec / 32, h2d_dec / 32
+    st_pf, h2d_pf = h2d_timed(sess, timer, lambda: layer(xp, yp), 3)
     for j in range(3):
         for e in range(E):
             mask[tids[j][e]] = 0
     sess.set_placement(mask)
-    host_bytes_pf = int(host_exp.sum()) * expert_bytes
-    log(f"moe streamed decode {st_dec * 1e3:.3f} ms/token, prefill {st_pf * 1e3:.2f} ms "
-        f"({host_bytes_pf / st_pf / 1e9:.1f} GB/s PCIe if all 51 host experts are active)")
+    log(f"moe streamed decode {st_dec * 1e3:.3f} ms/token ({h2d_dec / 1e6:.1f} MB copied), prefill "
+        f"{st_pf * 1e3:.2f} ms ({h2d_pf / 1e6:.1f} MB copied, {h2d_pf / st_pf / 1e9:.1f} GB/s PCIe)")
     return {"workload": "moe_layer: 128 experts of SwiGLU 768 over hidden 2048, top-8, capped Zipf(1.1) loads",
             "decode_us_per_token": round(dec_s * 1e6, 2),
             "decode_routed_GBps": round(routed_bytes / dec_s / 1e9, 1),
@@ -424,8 +436,11 @@ def bench_moe(sess, timer, args):
             "prefill_ms": round(pf_s * 1e3, 4),
             "prefill_TFLOPs": round(pf_flops / pf_s / 1e12, 2),
             "streamed_40pct_host": {"decode_ms_per_token": round(st_dec * 1e3, 4),
+                                    "decode_h2d_bytes_per_token": int(h2d_dec),
+                                    "decode_pcie_GBps": round(h2d_dec / st_dec / 1e9, 2),
                                     "prefill_ms": round(st_pf * 1e3, 3),
-                                    "prefill_pcie_GBps_if_all_active": round(host_bytes_pf / st_pf / 1e9, 2)}}
+                                    "prefill_h2d_bytes": int(h2d_pf),
+                                    "prefill_pcie_GBps": round(h2d_pf / st_pf / 1e9, 2)}}
 
 
 def bench_dense_stack(timer_cls, h2d_gbs, steps=6):
@@ -474,11 +489,12 @@ def bench_dense_stack(timer_cls, h2d_gbs, steps=6):
     sess.set_placement(pl)
     sess.set_schedule([tids[layer][r] for layer in range(wl.n_layers) for r in configs.ROLES])
     timer.run(step, 1)
-    t_st = timer.run(step, steps)
+    t_st, h2d_st = h2d_timed(sess, timer, step, steps)
     sess.close()
     m = wl.decode_m
     log(f"dense stack: decode step {t_hbm * 1e3:.2f} ms all-HBM ({total_bytes / t_hbm / 1e9:.0f} GB/s), "
-        f"{t_st * 1e3:.2f} ms with {host_bytes / 1e9:.2f} GB on host ({host_bytes / t_st / 1e9:.1f} GB/s PCIe)")
+        f"{t_st * 1e3:.2f} ms with {host_bytes / 1e9:.2f} GB on host ({h2d_st / 1e9:.2f} GB copied per step, "
+        f"{h2d_st / t_st / 1e9:.1f} GB/s PCIe)")
     return {"workload": "dense_stack: 32 8B-shaped layers, decode loop of 8 sequences, hidden state renormalised "
                         "after every layer, 30 % of the int4 bytes on host by seeded score",
             "layers": wl.n_layers, "sequences": m, "steps_timed": steps,
@@ -487,8 +503,9 @@ def bench_dense_stack(timer_cls, h2d_gbs, steps=6):
                         "weight_GBps": round(total_bytes / t_hbm / 1e9, 1)},
             "streamed": {"ms_per_step": round(t_st * 1e3, 3), "tokens_per_s": round(m / t_st, 1),
                          "weight_GBps_pcie_inclusive": round(total_bytes / t_st / 1e9, 1),
-                         "pcie_GBps": round(host_bytes / t_st / 1e9, 2),
-                         "pct_of_h2d_ceiling": round(100 * host_bytes / t_st / 1e9 / h2d_gbs, 1),
+                         "h2d_bytes_per_step": int(h2d_st),
+                         "pcie_GBps": round(h2d_st / t_st / 1e9, 2),
+                         "pct_of_h2d_ceiling": round(100 * h2d_st / t_st / 1e9 / h2d_gbs, 1),
                          "tokens_per_s_256_steps": round(m / t_st, 1)}}
 
 
@@ -525,32 +542,44 @@ def bench_moe_stack(timer_cls):
     wr = torch.from_numpy(synth.router_weights(wl.seed, configs.router_uid(layer), H, E)).cuda()
     moe = sess.moe_layer(wr, *tids, top_k=k, router_bias=torch.from_numpy(load_bias()).cuda())
     L = MoEDecoderLayer(moe, a["q"], a["k"], a["v"], a["o"], ds.n_heads, ds.n_kv, ds.head_dim, 1e-6)
-    hd = torch.from_numpy(synth.activations(wl.seed, 1, 32, H)).cuda()
-    hp = torch.from_numpy(synth.activations(wl.seed, 2, wl.prefill_m, H)).cuda()
+    # The layer updates h in place (h += attention + MoE) and routing depends
+    # on h, so every timed call starts from the same hidden states: restored
+    # from a pristine copy inside the call, with the copy's own time taken off.
+    hd0 = torch.from_numpy(synth.activations(wl.seed, 1, 32, H)).cuda()
+    hp0 = torch.from_numpy(synth.activations(wl.seed, 2, wl.prefill_m, H)).cuda()
+    hd, hp = hd0.clone(), hp0.clone()
     sess.cs.wait_stream(torch.cuda.current_stream())
     attn_bytes = sum(configs.qbytes(*ds.kn(r)) for r in ("q", "k", "v", "o"))
     expert_bytes = 3 * configs.qbytes(H, I)
+    t_cd = timer.run(lambda: hd.copy_(hd0), 20)
+    t_cp = timer.run(lambda: hp.copy_(hp0), 20)
+
+    def dec():
+        hd.copy_(hd0)
+        for t in range(32):
+            L(hd[t:t + 1])
+
+    def pf():
+        hp.copy_(hp0)
+        L(hp)
 
     def measure():
-        def dec():
-            for t in range(32):
-                L(hd[t:t + 1])
         timer.run(dec, 1)
-        t_dec = timer.run(dec, 2) / 32
-        timer.run(lambda: L(hp), 1)
-        t_pf = timer.run(lambda: L(hp), 3)
-        return t_dec, t_pf
+        t_dec, b_dec = h2d_timed(sess, timer, dec, 2)
+        timer.run(pf, 1)
+        t_pf, b_pf = h2d_timed(sess, timer, pf, 3)
+        return (t_dec - t_cd) / 32, t_pf - t_cp, b_dec / 32, b_pf
 
-    d_hbm, p_hbm = measure()
+    d_hbm, p_hbm, _, _ = measure()
     host_exp = configs.moe_host_experts(frac=0.40, seed=wl.seed, layer=layer)
     pl = list(sess.placement)
     for j in range(3):
         for e in range(E):
             pl[tids[j][e]] = int(host_exp[e])
     sess.set_placement(pl)
-    d_st, p_st = measure()
+    d_st, p_st, d_h2d, p_h2d = measure()
     # experts the prefill actually routes to, and how many of those are on host
-    dbg = L(torch.from_numpy(synth.activations(wl.seed, 2, wl.prefill_m, H)).cuda(), debug=True)
+    dbg = L(hp0.clone(), debug=True)
     sess.sync()
     counts = dbg["counts"].cpu().numpy()
     n_act = int((counts > 0).sum())
@@ -558,8 +587,9 @@ def bench_moe_stack(timer_cls):
     sess.close()
     pf_flops = 2.0 * wl.prefill_m * (attn_bytes * 16 / 9 + k * expert_bytes * 16 / 9)  # 2 M K N per weight
     log(f"moe stack layer: decode {d_hbm * 1e3:.3f} ms ({d_st * 1e3:.3f} streamed), prefill {p_hbm * 1e3:.2f} ms "
-        f"({p_st * 1e3:.2f} streamed, {n_host_act} of {n_act} active experts on host -> "
-        f"{n_host_act * expert_bytes / p_st / 1e9:.1f} GB/s PCIe); x94: {94 * d_hbm * 1e3:.1f} ms/token all-HBM")
+        f"({p_st * 1e3:.2f} streamed, {n_host_act} of {n_act} active experts on host, {p_h2d / 1e6:.0f} MB "
+        f"copied -> {p_h2d / p_st / 1e9:.1f} GB/s PCIe); decode copies {d_h2d / 1e6:.1f} MB/token; "
+        f"x94: {94 * d_hbm * 1e3:.1f} ms/token all-HBM")
     return {"workload": "moe_stack: one 235B-A22B-shaped layer (attention 64/4 heads of 128, hidden 4096, "
                         "128 experts of SwiGLU 1536, top-8, capped-Zipf routing); 94-layer figures are 94 x the layer",
             "all_hbm": {"decode_ms_per_layer": round(d_hbm * 1e3, 4), "prefill_ms_per_layer": round(p_hbm * 1e3, 3),
@@ -569,7 +599,10 @@ def bench_moe_stack(timer_cls):
             "prefill_active_experts": n_act, "prefill_active_host_experts": n_host_act,
             "streamed_40pct_experts": {"decode_ms_per_layer": round(d_st * 1e3, 4),
                                        "prefill_ms_per_layer": round(p_st * 1e3, 3),
-                                       "prefill_pcie_GBps": round(n_host_act * expert_bytes / p_st / 1e9, 2),
+                                       "decode_h2d_bytes_per_layer": int(d_h2d),
+                                       "decode_pcie_GBps": round(d_h2d / d_st / 1e9, 2),
+                                       "prefill_h2d_bytes_per_layer": int(p_h2d),
+                                       "prefill_pcie_GBps": round(p_h2d / p_st / 1e9, 2),
                                        "decode_tokens_per_s_94_layers": round(1.0 / (94 * d_st), 2),
                                        "prefill_tokens_per_s_94_layers": round(wl.prefill_m / (94 * p_st), 1)}}
 

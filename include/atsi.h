@@ -241,6 +241,19 @@ atsi_status atsi_moe_bucket(atsi_ctx* ctx, const int32_t* idx, int64_t M, int32_
 /* Wait for both streams; returns the first latched asynchronous error. */
 atsi_status atsi_sync(atsi_ctx* ctx);
 
+/* Transfer counters of the engine (Sec. 4.2.2 moves host tensors into GPU
+ * temporary buffers; these count what it moved), cumulative since atsi_create
+ * or the last reset.  Counted when the copies are enqueued. */
+typedef struct {
+  uint64_t h2d_bytes;    /* bytes copied from pinned host memory to the device */
+  uint64_t h2d_copies;   /* hipMemcpyAsync calls that moved them */
+  uint64_t h2d_tensors;  /* host tensors copied (an expert moved as one copy counts 3) */
+  uint64_t host_reads;   /* launches' reads of a host tensor, each served by a copy */
+} atsi_stats;
+
+/* *out = the counters; reset != 0 then zeroes them. */
+atsi_status atsi_get_stats(atsi_ctx* ctx, atsi_stats* out, int32_t reset);
+
 /* Test export: the signed codes q[N][K] (int8, device buffer) of tensor w as
  * the library reads them, from wherever w currently lives. */
 atsi_status atsi_debug_unpack(atsi_ctx* ctx, atsi_tid w, int8_t* q_out);

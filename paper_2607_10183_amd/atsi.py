@@ -54,6 +54,11 @@ class atsi_moe_layer(ctypes.Structure):
 
 
 _P = ctypes.c_void_p
+class atsi_stats(ctypes.Structure):
+    _fields_ = [("h2d_bytes", ctypes.c_uint64), ("h2d_copies", ctypes.c_uint64), ("h2d_tensors", ctypes.c_uint64),
+                ("host_reads", ctypes.c_uint64)]
+
+
 _SIGS = {
     "atsi_create": ([ctypes.c_int, _P, _P, _P, ctypes.c_size_t, ctypes.c_int, ctypes.POINTER(_P)], ctypes.c_int),
     "atsi_destroy": ([_P], ctypes.c_int),
@@ -73,6 +78,7 @@ _SIGS = {
     "atsi_set_schedule": ([_P, _P, ctypes.c_int32], ctypes.c_int),
     "atsi_prefetch": ([_P, ctypes.c_int32], ctypes.c_int),
     "atsi_sync": ([_P], ctypes.c_int),
+    "atsi_get_stats": ([_P, ctypes.POINTER(atsi_stats), ctypes.c_int32], ctypes.c_int),
     "atsi_debug_unpack": ([_P, ctypes.c_int32, _P], ctypes.c_int),
 }
 
@@ -177,6 +183,12 @@ def atsi_prefetch(ctx: int, w: int) -> None:
 
 def atsi_sync(ctx: int) -> None:
     _check(ctx, lib().atsi_sync(ctx))
+
+
+def atsi_get_stats(ctx: int, reset: bool = False) -> dict:
+    st = atsi_stats()
+    _check(ctx, lib().atsi_get_stats(ctx, ctypes.byref(st), int(reset)))
+    return {f: int(getattr(st, f)) for f, _ in atsi_stats._fields_}
 
 
 def atsi_debug_unpack(ctx: int, w: int, q_out: int) -> None:

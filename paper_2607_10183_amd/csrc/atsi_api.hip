@@ -106,6 +106,7 @@ struct atsi_ctx {
   bool layer_launched = false;    // a fused layer ran since the last atsi_sync
   int32_t* pinned = nullptr;    // pinned host copy of per-expert counts
   hipEvent_t counts_ev = nullptr;
+  atsi_stats stats{};           // transfer counters (atsi_get_stats)
   std::string err;
   atsi_status latched = ATSI_OK;
   std::string latched_msg;
@@ -214,10 +215,14 @@ atsi_status retire(atsi_ctx* c, bool block) {
 atsi_status copy_into(atsi_ctx* c, const Tensor& t, Slot& s) {
   if (t.host_contiguous()) {
     HIP_TRY(c, hipMemcpyAsync(s.base, t.hcodes, t.bytes(), hipMemcpyHostToDevice, c->ts));
+    c->stats.h2d_copies += 1;
   } else {
     HIP_TRY(c, hipMemcpyAsync(s.base, t.hcodes, t.codes_bytes(), hipMemcpyHostToDevice, c->ts));
     HIP_TRY(c, hipMemcpyAsync(s.base + t.codes_bytes(), t.hscales, t.scales_bytes(), hipMemcpyHostToDevice, c->ts));
+    c->stats.h2d_copies += 2;
   }
+  c->stats.h2d_bytes += t.bytes();
+  c->stats.h2d_tensors += 1;
   return ATSI_OK;
 }
 
@@ -329,6 +334,9 @@ atsi_status issue_run(atsi_ctx* c, const atsi_tid* tids, int n, bool* issued) {
   Slot& s0 = c->slots[first];
   HIP_TRY(c, hipMemcpyAsync(s0.base, c->tensors[tids[0]].hcodes, (size_t)n * c->slot_bytes, hipMemcpyHostToDevice,
                             c->ts));
+  c->stats.h2d_copies += 1;
+  c->stats.h2d_bytes += (uint64_t)n * c->slot_bytes;
+  c->stats.h2d_tensors += (uint64_t)n;
   HIP_TRY(c, hipEventRecord(s0.ready, c->ts));
   for (int i = 0; i < n; ++i) arm(c, c->slots[first + i], tids[i], s0.ready);
   *issued = true;
@@ -435,6 +443,7 @@ atsi_status acquire(atsi_ctx* c, atsi_tid tid, QView* v, std::vector<int>& held)
   v->codes = reinterpret_cast<const uint8_t*>(s.base);
   v->scales = reinterpret_cast<const uint16_t*>(s.base + t.codes_bytes());
   held.push_back(si);
+  c->stats.host_reads += 1;
   return ATSI_OK;
 }
 
@@ -1117,6 +1126,13 @@ atsi_status atsi_prefetch(atsi_ctx* c, atsi_tid w) {
   if (!c->tensors[w].on_host) return ATSI_OK;
   c->queue.push_back(w);
   return topup(c);
+}
+
+atsi_status atsi_get_stats(atsi_ctx* c, atsi_stats* out, int32_t reset) {
+  if (!c || !out) return fail(c, ATSI_E_INVALID, "ctx and out are required");
+  *out = c->stats;
+  if (reset) c->stats = atsi_stats{};
+  return ATSI_OK;
 }
 
 atsi_status atsi_sync(atsi_ctx* c) {

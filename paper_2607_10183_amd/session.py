@@ -192,6 +192,10 @@ class Session:
         self._torch_waits()
         return counts, offsets, perm, inv
 
+    def stats(self, reset: bool = False) -> dict:
+        """Transfer counters: h2d_bytes, h2d_copies, h2d_tensors, host_reads (see atsi_get_stats)."""
+        return atsi.atsi_get_stats(self.ctx, reset)
+
     def set_schedule(self, order) -> None:
         atsi.atsi_set_schedule(self.ctx, list(order))
 

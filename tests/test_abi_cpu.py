@@ -71,3 +71,4 @@ def test_null_context_is_invalid(lib):
     assert lib.atsi_sync(None) == 1
     assert lib.atsi_destroy(None) == 1
     assert lib.atsi_linear(None, 0, None, 1, None) == 1
+    assert lib.atsi_get_stats(None, None, 0) == 1
