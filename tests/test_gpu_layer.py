@@ -86,6 +86,24 @@ def test_decoder_layer_parity(sess, shape, M):
     check(k_out.cpu().numpy(), kr, zk, name="k projection")
 
 
+@pytest.mark.skip(reason="the single-launch cooperative decode layer (csrc/q4_layer.hip) is switched off "
+                         "(kFusedDecodeLayer = false): two GPU runs of this case faulted with an illegal address; "
+                         "two causes were shown on the CPU and fixed (a read past the per-wave step table, and the "
+                         "low address word read back from LDS sign-extended), and the path stays off until a run "
+                         "of this test passes")
+def test_fused_decode_layer_parity(sess):
+    """Batch-1 all-resident decode layer through the fused launch, against the oracle."""
+    shape = configs.DenseShape()
+    W = _layer_weights(shape, 77)
+    tids = {r: sess.register(*W[r]) for r in configs.ROLES}
+    hn = synth.activations(77, 1, 1, shape.hidden)
+    h = _dev(hn)
+    sess.decoder_layer(tids, h, shape.n_heads, shape.n_kv, shape.head_dim, 1e-6)
+    sess.sync()
+    ref, zeta, _ = oracle.decoder_layer(hn, W, shape.n_heads, shape.n_kv, shape.head_dim, 1e-6)
+    check(h.cpu().numpy(), ref, zeta, name="fused decode layer")
+
+
 @pytest.mark.parametrize("M", [1, 512])
 def test_layer_placement_invariance(sess, M):
     """All-HBM, the seeded mask and all-host placements give bit-identical layers."""
