@@ -334,7 +334,7 @@ def main() -> int:
         "roofline": {"bound": "hbm", "achieved": round(gemv_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(gemv_gbs / HBM_PEAK_GBS, 4),
                      "traffic": measured_traffic("gemv_gate_up", "q4_gemv"),
-                     "kernel": "q4_gemv_kernel<1,1,2,true,1>: SwiGLU gate/up, two 4096x14336 tensors, batch 1",
+                     "kernel": "q4_gemv1_kernel<7,true,4>: SwiGLU gate/up, two 4096x14336 tensors, batch 1",
                      "bytes_per_launch": gemv_bytes, "avg_us": round(t_gemv * 1e6, 3)},
         "roofline_prefill": {"bound": "mfma", "achieved": round(gemm_tfs, 1), "peak": MFMA_F16_PEAK_TFLOPS,
                              "unit": "TFLOP/s", "frac": round(gemm_tfs / MFMA_F16_PEAK_TFLOPS, 4),
@@ -689,7 +689,7 @@ def summarize(trace_dir: str, fetch_dir: str, write_dir: str, commands: dict) ->
           f"{w_copy:.0f} KiB (WRITE_SIZE) per dispatch; scale factors {f_scale:.4f} and {w_scale:.4f}.", "",
           "| kernel | FETCH KiB | WRITE KiB | HBM bytes per launch (scaled) | algorithmic bytes |",
           "|---|---|---|---|---|"]
-    for key, needle, kind, algo in (("gemv_gate_up", "q4_gemv_kernel<1, 1, 2, true, 1>", "q4_gemv", 66060288),
+    for key, needle, kind, algo in (("gemv_gate_up", "q4_gemv1_kernel<7, true, 4>", "q4_gemv", 66060288),
                                     ("gemm_gate_up", "q4_gemm_kernel<128, 128, 2, 2, true, false>", "q4_gemm",
                                      66060288 + 2 * 512 * 4096 + 2 * 512 * 14336)):
         kname, f = pick(fetch, needle)

@@ -1,30 +1,40 @@
 // Decode-path dequantising GEMV for block-int4 weights on CDNA4 (gfx950).
 //
-// y[m][n] = sum_g s[n][g] * sum_{k in g} q[n][k] * x[m][k] for M <= 4 tokens.
-// Decode reads every weight byte once per token (the memory-bound phase,
-// Sec. 2.2), so the kernel is built to keep HBM busy:
-//   * the first step's weight loads are issued before anything else; then the
-//     workgroup stages its activations once in LDS, already permuted to the
-//     (k, k+4) pairs the nibble extraction yields, with each group's offset
-//     correction (and, for a fused RMS norm, the sum of squares);
-//   * a wavefront walks SPW steps of RW rows; lane l handles groups l, l+64, ...
-//     of a row, so one 128-bit load covers one 32-input group and a wave
-//     instruction reads 1 KiB contiguous from a row;
-//   * steps alternate between two register buffers: the next step's codes and
-//     scales are loaded (unconditionally, rows and groups clamped, so the
-//     compiler counts outstanding loads exactly) before the current step is
-//     computed, keeping a step of loads in flight per wave; steps per wave
-//     are a compile-time constant, so no load is issued past a wave's last
-//     step (those rows belong to the next workgroup and would be read twice);
-//   * arithmetic per group: four ALU ops make eight fp16 weights-plus-offset
-//     values, v_dot2_f32_f16 accumulates exact products in fp32, one FMA
-//     removes the offset and one applies the fp16 scale (q4_gemv_core.h);
-//   * lanes reduce across the wavefront with shuffles; one lane per
-//     (row, token) rounds to fp16 once.
+// y[m][n] = sum_g s[n][g] * sum_{k in g} q[n][k] * x[m][k].  Decode reads
+// every weight byte once per token (the memory-bound phase, Sec. 2.2), so
+// both kernels here are built to keep HBM busy while the arithmetic hides
+// under the loads.
+//
+// One token (q4_gemv1_kernel):
+//   * a workgroup of S x P waves owns R = P x C consecutive rows; wave (s, p)
+//     takes K-slice s (groups 64 s .. 64 s + 63, one group per lane, so one
+//     128-bit load per lane reads 1 KiB of a row contiguously) of rows
+//     r0 + p + P i, i < C; the P waves of a slice read neighbouring rows;
+//   * the workgroup stages the activations once in LDS, already permuted to
+//     the (k, k+4) pairs the nibble extraction yields, with each group's
+//     offset correction (and the sum of squares for a fused RMS norm); each
+//     lane then keeps its one group in registers for all C rows;
+//   * the first D - 1 rows' loads are issued before the staging, and each row
+//     refills the register buffer consumed by the previous one, so D - 1 rows
+//     stay in flight per wave; loads are non-temporal buffer loads whose
+//     out-of-range lanes (rows past N, groups past K) read zeros;
+//   * per group: four ALU ops make eight fp16 weight-plus-offset values,
+//     v_dot2_f32_f16 accumulates exact products in fp32, one FMA removes the
+//     offset and one applies the fp16 scale (q4_gemv_core.h);
+//   * a lane carries one partial per (row, tensor); after the last row the
+//     wave sums all of them at once with a transposed butterfly (permlane32
+//     and permlane16 swaps, then DPP inside rows of 16 lanes), and the S
+//     slices meet in LDS, where one thread per row applies the epilogue.
+// Up to 4 tokens (q4_gemv_kernel, used where the batched-decode kernel does
+// not apply): a wavefront walks rows with lane l on groups l, l+64, ..., the
+// activations staged in LDS per token and read back per row.
 // One launch can cover several tensors that read the same input (Q, K and V;
 // the gate/up pair of a SwiGLU FFN) and fuses the RMS normalisation of the
 // input, the SwiGLU product, the residual add and the grouped-query head
 // expansion of a context-length-1 attention into the epilogue.
+#include <algorithm>
+#include <cmath>
+
 #include "q4_gemv_core.h"
 
 namespace atsi {
@@ -270,6 +280,208 @@ int default_spw(const LinOp& op) {
   return n >= 2048 ? 2 : 1;
 }
 
+// ---------------------------------------------------------------- one token
+
+constexpr uint32_t kOobOff = 0x80000000u;  // an offset past every buffer here
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), 0, (int)bytes, 0x00020000);
+}
+
+constexpr int kNtBits = 2;  // cache policy of the weight loads: non-temporal
+
+struct Gemv1Map {
+  int end[kMaxSeg];  // cumulative workgroup counts per segment
+  int S;             // K slices (waves per row)
+  int P;             // row partitions
+};
+
+constexpr int pad_pow2(int v) { return v <= 4 ? 4 : (v <= 8 ? 8 : 16); }
+
+template <int C, bool SWI, int D>
+__global__ __launch_bounds__(1024) void q4_gemv1_kernel(LinOp op, Gemv1Map m) {
+  constexpr int NT = SWI ? 2 : 1;
+  constexpr int V = pad_pow2(NT * C);
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  __shared__ float sq_wave[16];
+  int sgi = 0;
+  while (sgi < op.nseg - 1 && (int)blockIdx.x >= m.end[sgi]) ++sgi;
+  const int local = (int)blockIdx.x - (sgi ? m.end[sgi - 1] : 0);
+  const Seg& sg = op.seg[sgi];
+  const int K = op.K, G = K / kGroup, N = sg.w.N;
+  const int S = m.S, P = m.P;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
+  const int s = wave % S, p = wave / S;
+  const int r0 = local * P * C;
+  const int g = 64 * s + lane;
+  const bool gok = g < G;
+
+  __amdgpu_buffer_rsrc_t rc[NT], rs[NT];
+  rc[0] = buf_rsrc(sg.w.codes, (uint32_t)((size_t)N * K / 2));
+  rs[0] = buf_rsrc(sg.w.scales, (uint32_t)((size_t)N * G * 2));
+  if constexpr (SWI) {
+    rc[1] = buf_rsrc(sg.w2.codes, (uint32_t)((size_t)N * K / 2));
+    rs[1] = buf_rsrc(sg.w2.scales, (uint32_t)((size_t)N * G * 2));
+  }
+  struct Ld {
+    u32x4_g c[NT];
+    uint32_t s[NT];
+  };
+  // row i of this wave (rows past the block or the tensor read zeros)
+  auto load = [&](Ld& b, int i) {
+    const int row = i < C ? r0 + p + P * i : N;
+    const uint32_t co = gok ? (uint32_t)row * (uint32_t)(K / 2) + (uint32_t)g * 16 : kOobOff;
+    const uint32_t so = gok ? ((uint32_t)row * (uint32_t)G + (uint32_t)g) * 2 : kOobOff;
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      b.c[t] = __builtin_bit_cast(u32x4_g, __builtin_amdgcn_raw_buffer_load_b128(rc[t], co, 0, kNtBits));
+      b.s[t] = __builtin_amdgcn_raw_buffer_load_b16(rs[t], so, 0, kNtBits);
+    }
+  };
+  Ld buf[D];
+#pragma unroll
+  for (int d = 0; d < D - 1; ++d) load(buf[d], d);
+
+  // activations: [group][16 pairs + correction], then the slice partials [S][P][V]
+  uint32_t* xs = reinterpret_cast<uint32_t*>(smem);
+  float* red = reinterpret_cast<float*>(smem + (size_t)G * 68);
+  float sq = 0.f;
+  for (int c = threadIdx.x; c < G; c += S * P * kWave) {
+    XRaw r;
+    XGroup gx;
+    load_xraw(r, op.x, c);
+    prep_x(gx, r, op.norm != 0, sq);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) xs[c * 17 + i] = gx.p[i];
+    xs[c * 17 + 16] = __float_as_uint(gx.corr);
+  }
+  if (op.norm) {
+    const float t = wave_total(sq);
+    if (lane == 0) sq_wave[wave] = t;
+  }
+  __syncthreads();
+  float inv_r = 1.f;
+  if (op.norm) {
+    float t = 0.f;
+    for (int w = 0; w < S * P; ++w) t += sq_wave[w];
+    inv_r = 1.f / sqrtf(t / (float)K + op.eps);
+  }
+  XGroup xg;
+  {
+    const int c = gok ? g : 0;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) xg.p[i] = xs[c * 17 + i];
+    xg.corr = __uint_as_float(xs[c * 17 + 16]);
+  }
+  const UnpackMasks um = unpack_masks();
+
+  float part[V];
+#pragma unroll
+  for (int i = 0; i < V; ++i) part[i] = 0.f;
+#pragma unroll
+  for (int i = 0; i < C; ++i) {
+    load(buf[(i + D - 1) % D], i + D - 1);
+    const Ld& cur = buf[i % D];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      const float sc = gok ? __half2float(__ushort_as_half((uint16_t)cur.s[t])) : 0.f;
+      const uint4 cw = make_uint4(cur.c[t].x, cur.c[t].y, cur.c[t].z, cur.c[t].w);
+      part[t * C + i] = sc * group_dot_m(cw, xg, um);
+    }
+  }
+  transpose_reduce<V>(part);
+  if ((lane & 15) == 0) {
+    const int rr = lane >> 4;
+#pragma unroll
+    for (int i = 0; i < V / 4; ++i) red[(s * P + p) * V + i + (V / 4) * (rr & 1) + (V / 2) * (rr >> 1)] = part[i];
+  }
+  __syncthreads();
+  const int tid = threadIdx.x;
+  if (tid < P * C) {
+    const int pp = tid % P, i = tid / P;
+    const int row = r0 + pp + P * i;
+    float a[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      float sum = 0.f;
+      for (int ss = 0; ss < S; ++ss) sum += red[(ss * P + pp) * V + t * C + i];
+      a[t] = sum * inv_r;
+    }
+    float v = a[0];
+    if constexpr (SWI) v = silu_f(a[0]) * a[NT - 1];
+    if (row < N) emit_out(op, sg, sgi, 0, row, v);
+  }
+}
+
+// Rows per wave C (compile time) and row partitions P for a batch-1 launch:
+// about two workgroups per CU over all segments (256 CUs), at most 16 waves
+// per workgroup.  Measured on MI355X: 7 rows per wave with 4 partitions for
+// the 4096 x 14336 gate/up pair, 4 x 2 for 4096 x 4096 and 14336 x 4096,
+// 2 x 2 for 4096 x 1024.
+struct Gemv1Shape {
+  int C, P;
+};
+Gemv1Shape gemv1_shape(long rows, int S) {
+  const int pmax = std::max(1, 16 / S);
+  const double target = std::max(4.0, (double)rows / 512.0);
+  const int cs[4] = {7, 4, 8, 2};  // ties go to the earlier entry
+  Gemv1Shape best{2, 1};
+  double berr = 1e30;
+  for (int ci = 0; ci < 4; ++ci)
+    for (int P = 1; P <= pmax; ++P) {
+      const double err = std::fabs(cs[ci] * P - target) / target + (cs[ci] * P > 2 * target ? 1.0 : 0.0);
+      if (err < berr - 1e-9) {
+        berr = err;
+        best = Gemv1Shape{cs[ci], P};
+      }
+    }
+  return best;
+}
+
+template <int C, bool SWI, int D>
+hipError_t launch_gemv1_cfg(const LinOp& op, int S, int P, hipStream_t st) {
+  Gemv1Map m{};
+  m.S = S;
+  m.P = P;
+  int total = 0;
+  for (int s = 0; s < op.nseg; ++s) {
+    total += (op.seg[s].w.N + P * C - 1) / (P * C);
+    m.end[s] = total;
+  }
+  constexpr int V = pad_pow2((SWI ? 2 : 1) * C);
+  const size_t lds = (size_t)(op.K / kGroup) * 68 + (size_t)S * P * V * 4;
+  if (lds > lds_limit()) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((q4_gemv1_kernel<C, SWI, D>), dim3(total), dim3(S * P * kWave), lds, st, op, m);
+  return hipGetLastError();
+}
+
+template <bool SWI>
+hipError_t launch_gemv1(const LinOp& op, hipStream_t st) {
+  const int G = op.K / kGroup;
+  const int S = (G + 63) / 64;
+  long rows = 0;
+  for (int s = 0; s < op.nseg; ++s) rows += op.seg[s].w.N;
+  const Gemv1Shape sh = gemv1_shape(rows, S);
+  switch (sh.C) {
+    case 8: return launch_gemv1_cfg<8, SWI, 4>(op, S, sh.P, st);
+    case 7: return launch_gemv1_cfg<7, SWI, 4>(op, S, sh.P, st);
+    case 4: return launch_gemv1_cfg<4, SWI, 3>(op, S, sh.P, st);
+    default: return launch_gemv1_cfg<2, SWI, 3>(op, S, sh.P, st);
+  }
+}
+
+// One-token launches need 32-bit buffer offsets and at most 16 slices.
+bool gemv1_supported(const LinOp& op) {
+  if (op.M != 1 || op.K % kGroup || op.K / kGroup > 16 * 64) return false;
+  for (int s = 0; s < op.nseg; ++s) {
+    const QView* v[2] = {&op.seg[s].w, &op.seg[s].w2};
+    for (int t = 0; t < (op.swiglu ? 2 : 1); ++t)
+      if ((size_t)v[t]->N * v[t]->K / 2 + (size_t)v[t]->K >= kOobOff) return false;
+  }
+  return true;
+}
+
 }  // namespace
 
 size_t lds_limit() {
@@ -294,6 +506,7 @@ int gemv_tokens(int K) {
 }
 
 hipError_t launch_gemv(const LinOp& op, hipStream_t st) {
+  if (gemv1_supported(op)) return op.swiglu ? launch_gemv1<true>(op, st) : launch_gemv1<false>(op, st);
   const int spw = default_spw(op);
   return op.swiglu ? launch_sw<true>(op, spw, st) : launch_sw<false>(op, spw, st);
 }

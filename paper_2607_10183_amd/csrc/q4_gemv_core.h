@@ -40,6 +40,51 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
+// Cross-lane sums on the DPP and permlane paths (no LDS traffic).
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, ROW_MASK, 0xF, false));
+}
+// Sum over each row of 16 lanes, left in every lane of the row.
+__device__ __forceinline__ float row16_sum(float v) {
+  v += dpp_f<0xB1, 0xF>(v);   // quad_perm [1,0,3,2]
+  v += dpp_f<0x4E, 0xF>(v);   // quad_perm [2,3,0,1]
+  v += dpp_f<0x141, 0xF>(v);  // row_half_mirror
+  v += dpp_f<0x140, 0xF>(v);  // row_mirror
+  return v;
+}
+// Sum over the wave, returned in every lane.
+__device__ __forceinline__ float wave_total(float v) {
+  v = row16_sum(v);
+  v += dpp_f<0x142, 0xA>(v);  // row_bcast:15 into rows 1 and 3
+  v += dpp_f<0x143, 0xC>(v);  // row_bcast:31 into rows 2 and 3
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
+}
+
+// Sums V per-lane values over the wave at once.  Two butterfly levels swap
+// half the values between lane halves (permlane32) and row pairs (permlane16),
+// so each level halves the count of values a lane carries; the last V/4
+// values are summed inside each row of 16.  On return v[i] (i < V/4), in
+// every lane of row r, holds the total of value i + (V/4)(r & 1) + (V/2)(r >> 1).
+template <int V>
+__device__ __forceinline__ void transpose_reduce(float (&v)[V]) {
+  static_assert(V >= 4 && (V & (V - 1)) == 0, "a power of two, at least 4");
+#if defined(__HIP_DEVICE_COMPILE__)
+#pragma unroll
+  for (int i = 0; i < V / 2; ++i) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v[i]), __float_as_uint(v[i + V / 2]), false, false);
+    v[i] = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+  }
+#pragma unroll
+  for (int i = 0; i < V / 4; ++i) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v[i]), __float_as_uint(v[i + V / 4]), false, false);
+    v[i] = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+  }
+#endif
+#pragma unroll
+  for (int i = 0; i < V / 4; ++i) v[i] = row16_sum(v[i]);
+}
+
 // Activations of one 32-input group: 16 pairs in nibble order and the
 // correction 1032 X_e + 72 X_o.
 struct XGroup {
@@ -95,6 +140,50 @@ __device__ __forceinline__ float group_dot(const uint4& cw, const XGroup& g) {
     const uint32_t d = (w8 & 0x00F000F0u) | kMagic;  // 8i+3, 8i+7 (x16)
     se = dot2(a, g.p[4 * i + 0], se);
     so = dot2(b, g.p[4 * i + 1], so);
+    se = dot2(c, g.p[4 * i + 2], se);
+    so = dot2(d, g.p[4 * i + 3], so);
+  }
+  return fmaf(so, 0.0625f, se - g.corr);
+}
+
+// Unpack masks held in scalar registers and the 1024.0 pattern in a vector
+// register, so that each mask-and-or is one v_and_or_b32 (its VOP3 encoding
+// takes no literal constant and reads at most one scalar register).
+struct UnpackMasks {
+  uint32_t lo, hi, magic;
+};
+__device__ __forceinline__ UnpackMasks unpack_masks() {
+  uint32_t lo, hi, mg;
+  asm volatile("s_mov_b32 %0, %1" : "=s"(lo) : "i"(0x000F000Fu));
+  asm volatile("s_mov_b32 %0, %1" : "=s"(hi) : "i"(0x00F000F0u));
+  asm volatile("v_mov_b32 %0, %1" : "=v"(mg) : "i"(kMagic));
+  return UnpackMasks{lo, hi, mg};
+}
+// v_dot2_f32_f16 with a zero addend (saves zeroing an accumulator)
+__device__ __forceinline__ float dot2_0(uint32_t a, uint32_t b) {
+  float r;
+  asm("v_dot2_f32_f16 %0, %1, %2, 0" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+// group_dot with the masks in registers (same arithmetic and order)
+__device__ __forceinline__ float group_dot_m(const uint4& cw, const XGroup& g, const UnpackMasks& k) {
+  float se = 0.f, so = 0.f;
+  const uint32_t w4[4] = {cw.x, cw.y, cw.z, cw.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t w = w4[i];
+    const uint32_t w8 = w >> 8;
+    const uint32_t a = (w & k.lo) | k.magic;
+    const uint32_t b = (w & k.hi) | k.magic;
+    const uint32_t c = (w8 & k.lo) | k.magic;
+    const uint32_t d = (w8 & k.hi) | k.magic;
+    if (i == 0) {
+      se = dot2_0(a, g.p[0]);
+      so = dot2_0(b, g.p[1]);
+    } else {
+      se = dot2(a, g.p[4 * i + 0], se);
+      so = dot2(b, g.p[4 * i + 1], so);
+    }
     se = dot2(c, g.p[4 * i + 2], se);
     so = dot2(d, g.p[4 * i + 3], so);
   }
