@@ -103,6 +103,7 @@ struct atsi_ctx {
   size_t table_floor = 0;       // lowest byte used by tables (ws_bytes if none)
   uint64_t placement_version = 0;
   unsigned* layer_bar = nullptr;  // barrier words of the fused decode layer (top of the workspace)
+  float* row_inv = nullptr;       // per-row 1/rms for normalised prefill GEMMs (below the barrier words)
   bool layer_launched = false;    // a fused layer ran since the last atsi_sync
   int32_t* pinned = nullptr;    // pinned host copy of per-expert counts
   hipEvent_t counts_ev = nullptr;
@@ -546,6 +547,13 @@ atsi_status run_op(atsi_ctx* c, LinOp& op, const atsi_tid* tids, int ntids) {
   // on the matrix cores (both read the codes once); where that kernel does
   // not apply (K not a multiple of 128), up to 4 tokens run as GEMV launches
   // of at most gemv_tokens(K) tokens each; larger batches run the MFMA GEMM
+  // a normalised prefill GEMM on 512-row tiles reads 1/rms per row from a
+  // small pass over x (its main loop has no registers to spare for the sums)
+  if (op.norm && c->row_inv && gemm_wide_wanted(op)) {
+    hipError_t e = launch_rms_inv(op.x, op.M, op.K, op.eps, c->row_inv, c->cs);
+    if (e != hipSuccess) return hip_fail(c, e, "row rms launch");
+    op.rinv = c->row_inv;
+  }
   const int mt = gemv_tokens(op.K);
   const bool skinny = op.M >= kSkinnyMinTokens && op.M <= kSkinnyMaxTokens && skinny_supported(op);
   if (!skinny && op.M <= kGemvMaxTokens && mt > 0) {
@@ -576,7 +584,7 @@ atsi_status check_act(atsi_ctx* c, const void* p, const char* what) {
 }
 
 atsi_status check_m(atsi_ctx* c, int64_t M) {
-  if (M < 1 || M > 65536) return fail(c, ATSI_E_SHAPE, "M=%lld outside 1..65536", (long long)M);
+  if (M < 1 || M > kMaxCallRows) return fail(c, ATSI_E_SHAPE, "M=%lld outside 1..%d", (long long)M, kMaxCallRows);
   return ATSI_OK;
 }
 
@@ -784,6 +792,13 @@ atsi_status atsi_create(int device, void* compute_stream, void* transfer_stream,
   }
   c->table_floor -= bar_bytes;
   c->layer_bar = reinterpret_cast<unsigned*>(c->ws + c->table_floor);
+  // one float per activation row of the largest call (M <= 65536); left out of
+  // small workspaces, where normalised prefill GEMMs keep the 128-row tiles
+  const size_t rinv_bytes = align_up((size_t)kMaxCallRows * sizeof(float));
+  if (c->table_floor >= 2 * rinv_bytes) {
+    c->table_floor -= rinv_bytes;
+    c->row_inv = reinterpret_cast<float*>(c->ws + c->table_floor);
+  }
   c->slots.resize(n_slots);
   if (hipHostMalloc((void**)&c->pinned, kMaxExperts * sizeof(int32_t), hipHostMallocDefault) != hipSuccess ||
       hipEventCreateWithFlags(&c->counts_ev, hipEventDisableTiming) != hipSuccess) {

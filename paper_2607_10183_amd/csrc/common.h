@@ -8,6 +8,7 @@
 namespace atsi {
 
 constexpr int kGroup = 32;  // inputs per fp16 scale
+constexpr int kMaxCallRows = 65536;  // activation rows (tokens) one call may take
 constexpr int kMaxSeg = 3;  // tensors fused into one launch
 
 // Location of one block-int4 tensor as a kernel sees it.
@@ -43,6 +44,7 @@ struct LinOp {
   const __half* res; // residual added to segment 0's output (may alias its y)
   float* y32;        // non-null: segment 0's output goes here in fp32 instead of y
   int head_dim;      // granularity of `expand`
+  const float* rinv; // norm: per-row 1 / rms of x precomputed (the 512-row GEMM needs it), or null
 };
 
 __device__ __forceinline__ float silu_f(float g) { return g / (1.f + expf(-g)); }
@@ -76,6 +78,17 @@ constexpr int kSkinnyMinTokens = 2;  // a single token goes to the GEMV
 bool skinny_supported(const LinOp& op);
 hipError_t launch_skinny(const LinOp& op, hipStream_t s);
 hipError_t launch_gemm(const LinOp& op, hipStream_t s);
+// 512-row-tile prefill GEMM: tiles one launch would have, and whether its
+// buffer offsets fit 32 bits
+int gemm_wide_tiles(const LinOp& op);
+bool gemm_wide_supported(const LinOp& op);
+hipError_t launch_gemm_wide(const LinOp& op, hipStream_t s);
+constexpr int kWideMinTiles = 192;  // three quarters of the 256 CUs
+// the prefill GEMM takes 512-row tiles when at least 256 rows come in and the
+// launch still has a tile for most CUs
+inline bool gemm_wide_wanted(const LinOp& op) {
+  return op.M >= 256 && gemm_wide_tiles(op) >= kWideMinTiles && gemm_wide_supported(op);
+}
 hipError_t launch_unpack(const QView& w, int8_t* q, hipStream_t s);
 
 // single-tensor helpers

@@ -65,8 +65,14 @@ def _layer_weights(shape, seed, layer=0):
 SMALL = configs.DenseShape(hidden=256, n_heads=4, n_kv=2, head_dim=64, inter=96)
 
 
+# attention of the 235B-A22B-shaped layer (64 query heads, 4 KV heads of 128) with a
+# small FFN: at 2048 tokens its fused Q/K/V launch takes 512-row tiles with the
+# norm and the grouped-query expansion
+WIDE_ATTN = configs.DenseShape(hidden=4096, n_heads=64, n_kv=4, head_dim=128, inter=128)
+
+
 @pytest.mark.parametrize("shape,M", [(SMALL, 1), (SMALL, 2), (SMALL, 5), (SMALL, 64),
-                                     (configs.DenseShape(), 1), (configs.DenseShape(), 512)])
+                                     (configs.DenseShape(), 1), (configs.DenseShape(), 512), (WIDE_ATTN, 2048)])
 def test_decoder_layer_parity(sess, shape, M):
     import torch
     W = _layer_weights(shape, 72)

@@ -35,12 +35,27 @@ def test_unpack_bitexact(sess, host):
     assert np.array_equal(q.cpu().numpy(), oracle.unpack_codes(codes))
 
 
+def assert_doubles(y2, y1):
+    """y(2x) is 2 y(x) bit for bit wherever the fp16 output is normal: every
+    product and fp32 partial sum scales exactly, and so does the final
+    rounding in the normal range.  In the subnormal output range the rounding
+    grid is absolute (2^-24), so there the two may differ by one step."""
+    a = np.ascontiguousarray(y2.detach().cpu().numpy())
+    b = (2 * y1.float()).half().cpu().numpy()
+    normal = np.abs(y1.float().cpu().numpy()) >= 2.0 ** -13
+    assert np.array_equal(a.view(np.uint16)[normal], b.view(np.uint16)[normal])
+    assert np.all(np.abs(a[~normal].astype(np.float64) - b[~normal].astype(np.float64)) <= 2.0 ** -24)
+
+
 EXACT_SHAPES = [  # (K, N, M): GEMV for M = 1, the batched-decode kernel for 2 <= M <= 16 when
     # K % 128 == 0 (else GEMV launches up to M = 4, GEMM above), GEMM for larger M; ragged N and M
     (32, 7, 1), (96, 33, 3), (768, 2048, 1), (4096, 1000, 4), (14336, 257, 2), (4096, 4096, 1),
     (4096, 1000, 5), (768, 300, 64), (4096, 520, 100), (14336, 130, 512), (2048, 4096, 16), (96, 65, 129),
     (4096, 700, 8), (8192, 300, 7), (14336, 257, 8), (14336, 130, 6), (256, 96, 8),
     (160, 70, 2), (224, 50, 4), (96, 40, 6), (128, 20, 16), (384, 17, 3),
+    # 512-row-tile prefill GEMM (taken from 256 rows and 192 tiles of 128 outputs):
+    # ragged M, a K step left half full, two row tiles
+    (96, 24576, 300), (64, 24576, 520),
 ]
 
 
@@ -63,6 +78,7 @@ RANDOM_SHAPES = [  # linear4096 (decode 1, batch 16) and the dense-layer tensors
     (4096, 4096, 1), (4096, 4096, 16), (4096, 1024, 1), (4096, 14336, 1), (14336, 4096, 1),
     (4096, 4096, 2), (4096, 1024, 4), (4096, 1024, 512), (4096, 14336, 512), (14336, 4096, 512),
     (4096, 4096, 3), (2048, 768, 37), (4096, 14336, 8), (14336, 4096, 8), (4096, 6144, 5),
+    (512, 24576, 600), (4096, 24576, 257),  # 512-row-tile GEMM
 ]
 
 
@@ -92,7 +108,24 @@ def test_scaling_by_two_and_determinism(sess, M):
     y3 = sess.linear(tid, x)
     sess.sync()
     assert torch.equal(y1, y3)
-    assert np.array_equal(bits16(y2), bits16((2 * y1.float()).half()))
+    assert_doubles(y2, y1)
+
+
+def test_wide_gemm_scaling_by_two_and_determinism(sess):
+    """The 512-row-tile GEMM: y(2x) equals 2 y(x) (exact products, sums scaled
+    exactly) and repeated calls are bit-identical."""
+    import torch
+    K, N, M = 128, 24576, 300
+    codes = synth.int4_codes(66, 1, N, K)
+    scales = synth.group_scales(66, 1, N, K)
+    xn, x = _x(66, M, M, K)
+    tid = sess.register(codes, scales)
+    y1 = sess.linear(tid, x)
+    y2 = sess.linear(tid, (2 * x).contiguous())
+    y3 = sess.linear(tid, x)
+    sess.sync()
+    assert torch.equal(y1, y3)
+    assert_doubles(y2, y1)
 
 
 @pytest.mark.parametrize("M", [1, 4, 64, 512])
