@@ -234,37 +234,108 @@ __global__ __launch_bounds__(kThreads, 1) void q4_gemm_wide_kernel(LinOp op, Wid
     step(s + 3, 3);
   }
 
-  // D of a 32x32 block: lane l holds column l % 32, item v row 8 (v/4) + 4 (l/32) + v % 4
+  // D of a 32x32 block: lane l holds column l % 32, item v row 8 (v/4) + 4 (l/32) + v % 4.
+  auto out_at = [&](int i, int v, int j, int& m, int& n, float& o) {
+    const int ml = kRows * wave + 32 * i + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+    m = m0 + ml;
+    n = SWI ? n0 + 32 * (j >> 1) + (lane & 31) : n0 + 32 * j + (lane & 31);
+    const float sc = NORM ? (m < M ? op.rinv[m] : 0.f) : 1.f;
+    o = acc[i][j][v] * sc;
+    if constexpr (SWI) o = silu_fast(o) * (acc[i][j + 1][v] * sc);
+  };
+  if (sg.expand > 1) {
+    // grouped-query expansion: each output goes to several query heads
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
+    for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int ml = kRows * wave + 32 * i + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-      const int m = m0 + ml;
-      if (m >= M) continue;
-      const float sc = NORM ? op.rinv[m] : 1.f;
+      for (int v = 0; v < 16; ++v)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        if (SWI && (j & 1)) continue;
-        const int n = SWI ? n0 + 32 * (j >> 1) + (lane & 31) : n0 + 32 * j + (lane & 31);
-        if (n >= N) continue;
-        float o = acc[i][j][v] * sc;
-        if constexpr (SWI) o = silu_fast(o) * (acc[i][j + 1][v] * sc);
-        if (sg.expand > 1) {
+        for (int j = 0; j < 4; ++j) {
+          if (SWI && (j & 1)) continue;
+          int m, n;
+          float o;
+          out_at(i, v, j, m, n, o);
+          if (m >= M || n >= N) continue;
           const int hd = op.head_dim, jh = n / hd, d = n % hd;
           const __half h = __float2half_rn(o);
           for (int e = 0; e < sg.expand; ++e) sg.y[(size_t)m * sg.ldy + (size_t)(jh * sg.expand + e) * hd + d] = h;
+        }
+    return;
+  }
+  // Otherwise restage 8 rows at a time through the wave's own LDS rows (free
+  // now) as fp32, so that each lane adds the residual and rounds 8 or 16
+  // consecutive outputs of one row and stores them in one or two 16-byte
+  // stores instead of one 2-byte store per output.
+  constexpr int W = NOUT;                      // outputs per tile row
+  constexpr int PER = W / 8;                   // outputs per lane per pass (8 lanes per row)
+  float* stage = reinterpret_cast<float*>(Aw);  // [8][W] fp32 (4 KiB of the wave's 9 KiB)
+  const bool full_cols = n0 + W <= N && (sg.ldy % 8) == 0;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+#pragma unroll
+      for (int vv = 0; vv < 4; ++vv)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          if (SWI && (j & 1)) continue;
+          int m, n;
+          float o;
+          out_at(i, 4 * q + vv, j, m, n, o);
+          stage[(4 * (lane >> 5) + vv) * W + (n - n0)] = o;
+        }
+      // row 8 q + (l/8) of this block, outputs PER * (l % 8) .. +PER
+      const int rl = lane >> 3, c0 = PER * (lane & 7);
+      const int m = m0 + kRows * wave + 32 * i + 8 * q + rl;
+      float o[PER];
+#pragma unroll
+      for (int e = 0; e < PER; e += 4) {
+        const float4 t = *reinterpret_cast<const float4*>(&stage[rl * W + c0 + e]);
+        o[e] = t.x;
+        o[e + 1] = t.y;
+        o[e + 2] = t.z;
+        o[e + 3] = t.w;
+      }
+      if (m < M) {
+        const size_t at = (size_t)m * sg.ldy + n0 + c0;
+        if (full_cols) {
+          if (op.res && sgi == 0) {
+#pragma unroll
+            for (int e = 0; e < PER; e += 8) {
+              const uint4 r = *reinterpret_cast<const uint4*>(op.res + at + e);
+              const __half* rh = reinterpret_cast<const __half*>(&r);
+#pragma unroll
+              for (int t = 0; t < 8; ++t) o[e + t] += __half2float(rh[t]);
+            }
+          }
+          if (op.y32 && sgi == 0) {
+#pragma unroll
+            for (int e = 0; e < PER; e += 4)
+              *reinterpret_cast<float4*>(op.y32 + at + e) = make_float4(o[e], o[e + 1], o[e + 2], o[e + 3]);
+          } else {
+#pragma unroll
+            for (int e = 0; e < PER; e += 8) {
+              uint4 w;
+              __half* wh = reinterpret_cast<__half*>(&w);
+#pragma unroll
+              for (int t = 0; t < 8; ++t) wh[t] = __float2half_rn(o[e + t]);
+              *reinterpret_cast<uint4*>(sg.y + at + e) = w;
+            }
+          }
         } else {
-          const size_t at = (size_t)m * sg.ldy + n;
-          if (op.res && sgi == 0) o += __half2float(op.res[at]);
-          if (op.y32 && sgi == 0)
-            op.y32[at] = o;
-          else
-            sg.y[at] = __float2half_rn(o);
+#pragma unroll
+          for (int e = 0; e < PER; ++e) {
+            if (n0 + c0 + e >= N) break;
+            float v = o[e];
+            if (op.res && sgi == 0) v += __half2float(op.res[at + e]);
+            if (op.y32 && sgi == 0)
+              op.y32[at + e] = v;
+            else
+              sg.y[at + e] = __float2half_rn(v);
+          }
         }
       }
     }
-  }
 }
 
 template <bool SWI, bool NORM>
