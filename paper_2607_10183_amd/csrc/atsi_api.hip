@@ -543,10 +543,6 @@ atsi_status run_op(atsi_ctx* c, LinOp& op, const atsi_tid* tids, int ntids) {
       op.seg[i].w = v;
     }
   }
-  // decode sizes: one token runs the GEMV, 2 to 16 the batched-decode kernel
-  // on the matrix cores (both read the codes once); where that kernel does
-  // not apply (K not a multiple of 128), up to 4 tokens run as GEMV launches
-  // of at most gemv_tokens(K) tokens each; larger batches run the MFMA GEMM
   // a normalised prefill GEMM on 512-row tiles reads 1/rms per row from a
   // small pass over x (its main loop has no registers to spare for the sums)
   if (op.norm && c->row_inv && gemm_wide_wanted(op)) {
@@ -554,6 +550,10 @@ atsi_status run_op(atsi_ctx* c, LinOp& op, const atsi_tid* tids, int ntids) {
     if (e != hipSuccess) return hip_fail(c, e, "row rms launch");
     op.rinv = c->row_inv;
   }
+  // decode sizes: one token runs the GEMV, 2 to 16 the batched-decode kernel
+  // on the matrix cores (both read the codes once); where that kernel does
+  // not apply (K not a multiple of 128), up to 4 tokens run as GEMV launches
+  // of at most gemv_tokens(K) tokens each; larger batches run the MFMA GEMM
   const int mt = gemv_tokens(op.K);
   const bool skinny = op.M >= kSkinnyMinTokens && op.M <= kSkinnyMaxTokens && skinny_supported(op);
   if (!skinny && op.M <= kGemvMaxTokens && mt > 0) {
