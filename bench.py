@@ -339,7 +339,7 @@ def main() -> int:
         "roofline_prefill": {"bound": "mfma", "achieved": round(gemm_tfs, 1), "peak": MFMA_F16_PEAK_TFLOPS,
                              "unit": "TFLOP/s", "frac": round(gemm_tfs / MFMA_F16_PEAK_TFLOPS, 4),
                              "traffic": measured_traffic("gemm_gate_up", "q4_gemm"),
-                             "kernel": "q4_gemm_wide_kernel<true,false>: SwiGLU gate/up, two 4096x14336 "
+                             "kernel": "q4_gemm_wide_kernel<true,false,false>: SwiGLU gate/up, two 4096x14336 "
                                        "tensors, 512 tokens",
                              "flops_per_launch": gemm_flops, "avg_us": round(t_gemm * 1e6, 2)},
         "gate_gemv_us": round(t_gate1 * 1e6, 3),
@@ -690,7 +690,7 @@ def summarize(trace_dir: str, fetch_dir: str, write_dir: str, commands: dict) ->
           "| kernel | FETCH KiB | WRITE KiB | HBM bytes per launch (scaled) | algorithmic bytes |",
           "|---|---|---|---|---|"]
     for key, needle, kind, algo in (("gemv_gate_up", "q4_gemv1_kernel<7, true, 4>", "q4_gemv", 66060288),
-                                    ("gemm_gate_up", "q4_gemm_wide_kernel<true, false>", "q4_gemm",
+                                    ("gemm_gate_up", "q4_gemm_wide_kernel<true, false, false>", "q4_gemm",
                                      66060288 + 2 * 512 * 4096 + 2 * 512 * 14336)):
         kname, f = pick(fetch, needle)
         _, w = pick(write, needle)

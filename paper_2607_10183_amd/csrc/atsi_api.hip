@@ -87,6 +87,7 @@ struct atsi_ctx {
   std::vector<Slot> slots;
   size_t slot_bytes = 0;
   size_t scratch_off = 0;
+  size_t scratch_top = 0;  // end of the scratch the current call has taken
   std::vector<atsi_tid> schedule;  // execution order of tensors, repeated cyclically
   size_t sched_pos = 0;            // next schedule position not yet queued
   std::deque<atsi_tid> queue;      // host tensors to copy ahead, in consumption order
@@ -148,6 +149,7 @@ atsi_status enter(atsi_ctx* c) {
   }
   hipError_t e = hipSetDevice(c->device);
   if (e != hipSuccess) return hip_fail(c, e, "hipSetDevice");
+  c->scratch_top = c->scratch_off;
   return ATSI_OK;
 }
 
@@ -476,6 +478,7 @@ struct Scratch {
     if (off + need > c->table_floor) return nullptr;
     char* p = c->ws + off;
     off += need;
+    c->scratch_top = std::max(c->scratch_top, off);
     return reinterpret_cast<__half*>(p);
   }
 };
@@ -543,12 +546,29 @@ atsi_status run_op(atsi_ctx* c, LinOp& op, const atsi_tid* tids, int ntids) {
       op.seg[i].w = v;
     }
   }
-  // a normalised prefill GEMM on 512-row tiles reads 1/rms per row from a
-  // small pass over x (its main loop has no registers to spare for the sums)
-  if (op.norm && c->row_inv && gemm_wide_wanted(op)) {
-    hipError_t e = launch_rms_inv(op.x, op.M, op.K, op.eps, c->row_inv, c->cs);
-    if (e != hipSuccess) return hip_fail(c, e, "row rms launch");
-    op.rinv = c->row_inv;
+  // Prefill on 512-row tiles (each weight dequantised once per 512 rows).  A
+  // normalised input needs 1/rms per row from a small pass over x (the main
+  // loop has no registers to spare for the sums); a launch with K ranges
+  // needs their fp32 partial sums above the scratch this call has taken,
+  // which nothing else uses until its reduction has run on the stream.
+  int wide = (op.norm && !c->row_inv) ? 0 : gemm_wide_splits(op);
+  float* part = nullptr;
+  if (wide > 1) {
+    const size_t at = align_up(c->scratch_top), need = gemm_wide_part_bytes(op, wide);
+    if (at + need <= c->table_floor)
+      part = reinterpret_cast<float*>(c->ws + at);
+    else
+      wide = 0;
+  }
+  if (wide) {
+    if (op.norm) {
+      hipError_t e = launch_rms_inv(op.x, op.M, op.K, op.eps, c->row_inv, c->cs);
+      if (e != hipSuccess) return hip_fail(c, e, "row rms launch");
+      op.rinv = c->row_inv;
+    }
+    hipError_t e = launch_gemm_wide(op, wide, part, c->cs);
+    if (e != hipSuccess) return hip_fail(c, e, "q4 wide gemm launch");
+    return release(c, held);
   }
   // decode sizes: one token runs the GEMV, 2 to 16 the batched-decode kernel
   // on the matrix cores (both read the codes once); where that kernel does

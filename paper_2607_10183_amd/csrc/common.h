@@ -49,6 +49,23 @@ struct LinOp {
 
 __device__ __forceinline__ float silu_f(float g) { return g / (1.f + expf(-g)); }
 
+// Epilogue of one output v of row `row` (output n) of token m in segment s:
+// grouped-query expansion, or residual add (segment 0), then fp32 or fp16.
+__device__ __forceinline__ void emit_out(const LinOp& op, const Seg& sg, int s, int m, int row, float v) {
+  if (sg.expand > 1) {
+    const int hd = op.head_dim, jh = row / hd, d = row % hd;
+    const __half o = __float2half_rn(v);
+    for (int g = 0; g < sg.expand; ++g) sg.y[(size_t)m * sg.ldy + (size_t)(jh * sg.expand + g) * hd + d] = o;
+    return;
+  }
+  const size_t at = (size_t)m * sg.ldy + row;
+  if (op.res && s == 0) v += __half2float(op.res[at]);
+  if (op.y32 && s == 0)
+    op.y32[at] = v;
+  else
+    sg.y[at] = __float2half_rn(v);
+}
+
 // Loads through the global address space.  Pointers read from memory (expert
 // tables, step tables) are otherwise generic, and a generic load also counts
 // against the LDS wait counter: every LDS wait would then drain the loads in
@@ -78,17 +95,16 @@ constexpr int kSkinnyMinTokens = 2;  // a single token goes to the GEMV
 bool skinny_supported(const LinOp& op);
 hipError_t launch_skinny(const LinOp& op, hipStream_t s);
 hipError_t launch_gemm(const LinOp& op, hipStream_t s);
-// 512-row-tile prefill GEMM: tiles one launch would have, and whether its
-// buffer offsets fit 32 bits
-int gemm_wide_tiles(const LinOp& op);
-bool gemm_wide_supported(const LinOp& op);
-hipError_t launch_gemm_wide(const LinOp& op, hipStream_t s);
+// 512-row-tile prefill GEMM.  K ranges per output tile: 1 when the launch
+// has a tile for most CUs, up to 8 (fp32 partial sums, reduced by a second
+// kernel in a fixed order) when it does not, 0 when the 512-row tiles do not
+// apply (fewer than 256 rows, too little K to split, offsets beyond 32 bits).
 constexpr int kWideMinTiles = 192;  // three quarters of the 256 CUs
-// the prefill GEMM takes 512-row tiles when at least 256 rows come in and the
-// launch still has a tile for most CUs
-inline bool gemm_wide_wanted(const LinOp& op) {
-  return op.M >= 256 && gemm_wide_tiles(op) >= kWideMinTiles && gemm_wide_supported(op);
-}
+constexpr int kWideMaxSplits = 8;
+int gemm_wide_splits(const LinOp& op);
+// bytes of fp32 partial sums a launch with `splits` K ranges needs (0 for 1)
+size_t gemm_wide_part_bytes(const LinOp& op, int splits);
+hipError_t launch_gemm_wide(const LinOp& op, int splits, float* part, hipStream_t s);
 hipError_t launch_unpack(const QView& w, int8_t* q, hipStream_t s);
 
 // single-tensor helpers

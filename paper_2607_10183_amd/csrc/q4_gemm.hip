@@ -111,9 +111,6 @@ __global__ void unpack_kernel(QView w, int8_t* q) {
 }  // namespace
 
 hipError_t launch_gemm(const LinOp& op, hipStream_t st) {
-  // 512-row tiles dequantise each weight once per 512 rows; they pay off when
-  // the launch still has a tile for most CUs
-  if (gemm_wide_wanted(op) && (!op.norm || op.rinv)) return launch_gemm_wide(op, st);
   long n = 0;
   for (int s = 0; s < op.nseg; ++s) n += op.seg[s].w.N;
   if (op.swiglu) {

@@ -23,7 +23,11 @@
 //   * each 16-deep substep is one fenced phase: the next substep's fragment
 //     reads, this substep's 8 MFMAs, then a slice of the dequantisation,
 //     activation staging and code loads, which runs under the MFMAs;
-//   * workgroup ids are remapped so each XCD takes a contiguous run of tiles.
+//   * workgroup ids are remapped so each XCD takes a contiguous run of tiles;
+//   * where the output has too few tiles to occupy the CUs (the O and down
+//     projections of a 512-token chunk have 32), K is split into up to 8
+//     ranges: each workgroup writes its raw fp32 sums for one range, and a
+//     second kernel adds the ranges in order and applies the epilogue.
 // One launch covers up to three tensors sharing the input, and fuses RMS
 // normalisation of the input (rows scaled by precomputed 1/rms values, so the
 // main loop carries no sums of squares), the SwiGLU product, the residual add
@@ -78,19 +82,30 @@ __device__ __forceinline__ float silu_fast(float g) { return g * __builtin_amdgc
 struct WideMap {
   int end[kMaxSeg];  // cumulative tile counts per segment
   int tiles_m;
-  int total;
+  int total;         // output tiles
+  int splits;        // K ranges per tile (workgroups = total * splits)
+  int tiles_n;       // tile columns over all segments (partial rows hold tiles_n * kBN floats)
 };
 
-template <bool SWI, bool NORM>
-__global__ __launch_bounds__(kThreads, 1) void q4_gemm_wide_kernel(LinOp op, WideMap tm) {
+// K steps of range r out of `splits` over nk steps
+__device__ __forceinline__ int range_begin(int r, int nk, int splits) { return (int)(((long)r * nk) / splits); }
+
+// SPLIT: write the raw sums of K range blockIdx / total to part[range][m][tile column]
+// (NORM is then applied by the reduction).
+template <bool SWI, bool NORM, bool SPLIT>
+__global__ __launch_bounds__(kThreads, 1) void q4_gemm_wide_kernel(LinOp op, WideMap tm, float* __restrict__ part) {
   constexpr int NOUT = SWI ? kBN / 2 : kBN;
   __shared__ __attribute__((aligned(16))) _Float16 Bs[2][kBN * kPitch];
   __shared__ __attribute__((aligned(16))) _Float16 As[8 * kRows * kPitch];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int nwg = tm.total * tm.splits;
   int bid = blockIdx.x;
-  if ((tm.total & 7) == 0) bid = (bid & 7) * (tm.total >> 3) + (bid >> 3);
+  if ((nwg & 7) == 0) bid = (bid & 7) * (nwg >> 3) + (bid >> 3);
+  // range-major order: the workgroups of one XCD share a K range of the activations
+  const int range = bid / tm.total;
+  bid -= range * tm.total;
   int sgi = 0;
   while (sgi < op.nseg - 1 && bid >= tm.end[sgi]) ++sgi;
   const int local = bid - (sgi ? tm.end[sgi - 1] : 0);
@@ -98,15 +113,20 @@ __global__ __launch_bounds__(kThreads, 1) void q4_gemm_wide_kernel(LinOp op, Wid
   const Seg& sg = op.seg[sgi];
   const int M = op.M, K = op.K, N = sg.w.N, G = K / kGroup;
   const int m0 = tmi * kBM, n0 = tni * NOUT;
-  const int nk = (K + kBK - 1) / kBK;
+  const int nk_all = (K + kBK - 1) / kBK;
+  const int kb = range_begin(range, nk_all, tm.splits);
+  const int nk = range_begin(range + 1, nk_all, tm.splits) - kb;  // steps of this range
+  // the buffers start at the range; inputs past klim (the range's end, or K) read zeros
+  const int klim = min(K - kb * kBK, nk * kBK), glim = klim / kGroup;
+  const size_t ka = (size_t)kb * kBK;
 
-  const __amdgpu_buffer_rsrc_t ra = rsrc(op.x, (uint32_t)((size_t)M * K * 2));
+  const __amdgpu_buffer_rsrc_t ra = rsrc(op.x + ka, (uint32_t)(((size_t)M * K - ka) * 2));
   __amdgpu_buffer_rsrc_t rc[2], rs[2];
-  rc[0] = rsrc(sg.w.codes, (uint32_t)((size_t)N * K / 2));
-  rs[0] = rsrc(sg.w.scales, (uint32_t)((size_t)N * G * 2));
+  rc[0] = rsrc(sg.w.codes + ka / 2, (uint32_t)((size_t)N * K / 2 - ka / 2));
+  rs[0] = rsrc(sg.w.scales + ka / kGroup, (uint32_t)(((size_t)N * G - ka / kGroup) * 2));
   if constexpr (SWI) {
-    rc[1] = rsrc(sg.w2.codes, (uint32_t)((size_t)N * K / 2));
-    rs[1] = rsrc(sg.w2.scales, (uint32_t)((size_t)N * G * 2));
+    rc[1] = rsrc(sg.w2.codes + ka / 2, (uint32_t)((size_t)N * K / 2 - ka / 2));
+    rs[1] = rsrc(sg.w2.scales + ka / kGroup, (uint32_t)(((size_t)N * G - ka / kGroup) * 2));
   } else {
     rc[1] = rc[0];
     rs[1] = rs[0];
@@ -121,7 +141,7 @@ __global__ __launch_bounds__(kThreads, 1) void q4_gemm_wide_kernel(LinOp op, Wid
     for (int r = 0; r < 8; ++r) {
       const int row = m0 + kRows * wave + 8 * r + (lane >> 3);
       const int k = kt * kBK + 8 * (lane & 7);
-      const uint32_t off = (row < M && k < K) ? ((uint32_t)row * (uint32_t)K + (uint32_t)k) * 2 : kOob;
+      const uint32_t off = (row < M && k < klim) ? ((uint32_t)row * (uint32_t)K + (uint32_t)k) * 2 : kOob;
       ax[r] = __builtin_bit_cast(w_u4_t, __builtin_amdgcn_raw_buffer_load_b128(ra, off, 0, 0));
     }
   };
@@ -149,7 +169,7 @@ __global__ __launch_bounds__(kThreads, 1) void q4_gemm_wide_kernel(LinOp op, Wid
   };
   auto load_b = [&](BCode& b, int kt) {
     const int gg = 2 * kt + bg;
-    const bool ok = bn < N && gg < G;
+    const bool ok = bn < N && gg < glim;
     const uint32_t co = ok ? (uint32_t)bn * (uint32_t)(K / 2) + (uint32_t)gg * 16 + 8u * bh : kOob;
     const uint32_t so = ok ? ((uint32_t)bn * (uint32_t)G + (uint32_t)gg) * 2 : kOob;
     const auto v = __builtin_amdgcn_raw_buffer_load_b64(rc[bt], co, 0, 2);
@@ -188,11 +208,11 @@ __global__ __launch_bounds__(kThreads, 1) void q4_gemm_wide_kernel(LinOp op, Wid
   dq_store(ring[0], 0, 1);
   __syncthreads();
 
-  // Step s (ring slot rq = s % kRing at compile time): MFMAs on weight buffer
+  // Step s of the range (ring slot rq = s % kRing at compile time): MFMAs on weight buffer
   // s % 2; step s + 1's weights are dequantised into the other buffer, the
   // codes of step s + kRing - 1 are loaded into the slot step s - 1 used, and
   // step s + 1's activations are staged once this step's fragments are read.
-  // Steps past the end read zeros (out-of-range buffer loads) and add zeros.
+  // Steps past the range read zeros (out-of-range buffer loads) and add zeros.
   auto step = [&](int s, int rq) {
     const int buf = s & 1;
     w_h8_t bf[2][4], af[2][2];
@@ -235,6 +255,32 @@ __global__ __launch_bounds__(kThreads, 1) void q4_gemm_wide_kernel(LinOp op, Wid
   }
 
   // D of a 32x32 block: lane l holds column l % 32, item v row 8 (v/4) + 4 (l/32) + v % 4.
+  if constexpr (SPLIT) {
+    // raw sums, restaged 8 rows at a time through the wave's LDS rows so that
+    // each lane writes 16 consecutive floats of one row
+    float* stage = reinterpret_cast<float*>(Aw);  // [8][kBN] fp32
+    const size_t pc = (size_t)tm.tiles_n * kBN;
+    const int tcol = ((sgi ? tm.end[sgi - 1] : 0) / tm.tiles_m + tni) * kBN;
+    float* dst = part + (size_t)range * M * pc + tcol;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+#pragma unroll
+        for (int vv = 0; vv < 4; ++vv)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) stage[(4 * (lane >> 5) + vv) * kBN + 32 * j + (lane & 31)] = acc[i][j][4 * q + vv];
+        const int rl = lane >> 3, c0 = 16 * (lane & 7);
+        const int m = m0 + kRows * wave + 32 * i + 8 * q + rl;
+        if (m < M) {
+#pragma unroll
+          for (int e = 0; e < 16; e += 4)
+            *reinterpret_cast<float4*>(dst + (size_t)m * pc + c0 + e) =
+                *reinterpret_cast<const float4*>(&stage[rl * kBN + c0 + e]);
+        }
+      }
+    return;
+  }
   auto out_at = [&](int i, int v, int j, int& m, int& n, float& o) {
     const int ml = kRows * wave + 32 * i + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
     m = m0 + ml;
@@ -338,23 +384,73 @@ __global__ __launch_bounds__(kThreads, 1) void q4_gemm_wide_kernel(LinOp op, Wid
     }
 }
 
+// Sum of the K ranges of a split launch, in range order, then the epilogue of
+// the single-range kernel: one thread per output.
 template <bool SWI, bool NORM>
-hipError_t launch_wide(const LinOp& op, const WideMap& tm, hipStream_t st) {
-  hipLaunchKernelGGL((q4_gemm_wide_kernel<SWI, NORM>), dim3(tm.total), dim3(kThreads), 0, st, op, tm);
+__global__ __launch_bounds__(256) void wide_reduce_kernel(LinOp op, WideMap tm, const float* __restrict__ part) {
+  constexpr int NOUT = SWI ? kBN / 2 : kBN;
+  const long idx = (long)blockIdx.x * 256 + threadIdx.x;
+  const long total = (long)op.M * tm.tiles_n * NOUT;
+  if (idx >= total) return;
+  const int o = (int)(idx % NOUT);
+  const long rest = idx / NOUT;
+  const int T = (int)(rest % tm.tiles_n), m = (int)(rest / tm.tiles_n);
+  int sgi = 0;
+  while (sgi < op.nseg - 1 && T >= tm.end[sgi] / tm.tiles_m) ++sgi;
+  const int tni = T - (sgi ? tm.end[sgi - 1] / tm.tiles_m : 0);
+  const Seg& sg = op.seg[sgi];
+  const int n = tni * NOUT + o;
+  if (n >= sg.w.N) return;
+  const size_t pc = (size_t)tm.tiles_n * kBN;
+  const int col = T * kBN + (SWI ? 64 * (o >> 5) + (o & 31) : o);
+  const float* p = part + (size_t)m * pc + col;
+  const size_t stride = (size_t)op.M * pc;
+  float g = 0.f, u = 0.f;
+  for (int r = 0; r < tm.splits; ++r) {
+    g += p[r * stride];
+    if constexpr (SWI) u += p[r * stride + 32];
+  }
+  const float sc = NORM ? op.rinv[m] : 1.f;
+  float v = g * sc;
+  if constexpr (SWI) v = silu_fast(v) * (u * sc);
+  emit_out(op, sg, sgi, m, n, v);
+}
+
+template <bool SWI, bool NORM>
+hipError_t launch_wide(const LinOp& op, const WideMap& tm, float* part, hipStream_t st) {
+  if (tm.splits == 1) {
+    hipLaunchKernelGGL((q4_gemm_wide_kernel<SWI, NORM, false>), dim3(tm.total), dim3(kThreads), 0, st, op, tm,
+                       nullptr);
+    return hipGetLastError();
+  }
+  hipLaunchKernelGGL((q4_gemm_wide_kernel<SWI, false, true>), dim3(tm.total * tm.splits), dim3(kThreads), 0, st, op,
+                     tm, part);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const long outs = (long)op.M * tm.tiles_n * (SWI ? kBN / 2 : kBN);
+  hipLaunchKernelGGL((wide_reduce_kernel<SWI, NORM>), dim3((unsigned)((outs + 255) / 256)), dim3(256), 0, st, op, tm,
+                     part);
   return hipGetLastError();
 }
 
-}  // namespace
-
-int gemm_wide_tiles(const LinOp& op) {
+WideMap wide_map(const LinOp& op, int splits) {
   const int nout = op.swiglu ? kBN / 2 : kBN;
-  const int tiles_m = (op.M + kBM - 1) / kBM;
-  int total = 0;
-  for (int s = 0; s < op.nseg; ++s) total += tiles_m * ((op.seg[s].w.N + nout - 1) / nout);
-  return total;
+  WideMap tm{};
+  tm.tiles_m = (op.M + kBM - 1) / kBM;
+  int total = 0, tn = 0;
+  for (int s = 0; s < op.nseg; ++s) {
+    const int t = (op.seg[s].w.N + nout - 1) / nout;
+    tn += t;
+    total += tm.tiles_m * t;
+    tm.end[s] = total;
+  }
+  tm.total = total;
+  tm.tiles_n = tn;
+  tm.splits = splits;
+  return tm;
 }
 
-bool gemm_wide_supported(const LinOp& op) {
+bool wide_offsets_ok(const LinOp& op) {
   // 32-bit buffer offsets for the activations and every tensor
   if ((size_t)op.M * op.K * 2 >= kOob) return false;
   for (int s = 0; s < op.nseg; ++s) {
@@ -365,19 +461,33 @@ bool gemm_wide_supported(const LinOp& op) {
   return true;
 }
 
-hipError_t launch_gemm_wide(const LinOp& op, hipStream_t st) {
-  if (!gemm_wide_supported(op)) return hipErrorInvalidValue;
-  const int nout = op.swiglu ? kBN / 2 : kBN;
-  WideMap tm{};
-  tm.tiles_m = (op.M + kBM - 1) / kBM;
-  int total = 0;
-  for (int s = 0; s < op.nseg; ++s) {
-    total += tm.tiles_m * ((op.seg[s].w.N + nout - 1) / nout);
-    tm.end[s] = total;
-  }
-  tm.total = total;
-  if (op.swiglu) return op.norm ? launch_wide<true, true>(op, tm, st) : launch_wide<true, false>(op, tm, st);
-  return op.norm ? launch_wide<false, true>(op, tm, st) : launch_wide<false, false>(op, tm, st);
+}  // namespace
+
+// One range when the tiles fill three quarters of the CUs; otherwise the
+// fewest ranges that do, keeping at least 8 K steps (512 inputs) per range.
+int gemm_wide_splits(const LinOp& op) {
+  if (op.M < 256 || !wide_offsets_ok(op)) return 0;
+  const int tiles = wide_map(op, 1).total;
+  if (tiles >= kWideMinTiles) return 1;
+  const int nk = (op.K + kBK - 1) / kBK;
+  const int want = (kWideMinTiles + tiles - 1) / tiles;
+  const int splits = std::min(std::min(want, kWideMaxSplits), nk / 8);
+  return splits >= 2 ? splits : 0;
+}
+
+size_t gemm_wide_part_bytes(const LinOp& op, int splits) {
+  if (splits <= 1) return 0;
+  return (size_t)splits * op.M * wide_map(op, splits).tiles_n * kBN * sizeof(float);
+}
+
+hipError_t launch_gemm_wide(const LinOp& op, int splits, float* part, hipStream_t st) {
+  if (splits < 1 || splits > kWideMaxSplits || !wide_offsets_ok(op) || (splits > 1 && !part) ||
+      (op.norm && !op.rinv))
+    return hipErrorInvalidValue;
+  const WideMap tm = wide_map(op, splits);
+  if (op.swiglu)
+    return op.norm ? launch_wide<true, true>(op, tm, part, st) : launch_wide<true, false>(op, tm, part, st);
+  return op.norm ? launch_wide<false, true>(op, tm, part, st) : launch_wide<false, false>(op, tm, part, st);
 }
 
 }  // namespace atsi

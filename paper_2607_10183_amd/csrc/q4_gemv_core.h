@@ -194,20 +194,6 @@ __device__ __forceinline__ float group_dot_m(const uint4& cw, const XGroup& g, c
 // to every query head of a grouped-query KV head, or with the residual added
 // (segment 0) and kept in fp32 when the launch asks for it, else rounded to
 // fp16 once.
-__device__ __forceinline__ void emit_out(const LinOp& op, const Seg& sg, int s, int m, int row, float v) {
-  if (sg.expand > 1) {
-    const int hd = op.head_dim, jh = row / hd, d = row % hd;
-    const __half o = __float2half_rn(v);
-    for (int g = 0; g < sg.expand; ++g) sg.y[(size_t)m * sg.ldy + (size_t)(jh * sg.expand + g) * hd + d] = o;
-    return;
-  }
-  const size_t at = (size_t)m * sg.ldy + row;
-  if (op.res && s == 0) v += __half2float(op.res[at]);
-  if (op.y32 && s == 0)
-    op.y32[at] = v;
-  else
-    sg.y[at] = __float2half_rn(v);
-}
 
 }  // namespace gemv
 }  // namespace atsi

@@ -29,7 +29,7 @@ def _dev(xn):
 
 
 @pytest.mark.parametrize("H,I,M", [(256, 96, 1), (256, 96, 3), (512, 160, 77), (4096, 14336, 1),
-                                   (4096, 14336, 4), (4096, 14336, 512), (2048, 768, 100)])
+                                   (4096, 14336, 4), (4096, 14336, 512), (2048, 768, 100), (2048, 768, 512)])
 def test_ffn_swiglu_parity(sess, H, I, M):
     gate, up, down = _qt(71, H + 1, I, H), _qt(71, H + 2, I, H), _qt(71, H + 3, H, I)
     tg = sess.register(*gate)
@@ -43,7 +43,7 @@ def test_ffn_swiglu_parity(sess, H, I, M):
 
 
 @pytest.mark.parametrize("H,I,M", [(256, 96, 1), (4096, 14336, 1), (4096, 14336, 3), (512, 160, 77),
-                                   (4096, 14336, 512)])
+                                   (4096, 14336, 512), (4096, 1024, 512), (2048, 768, 300)])
 def test_swiglu_gate_up_parity(sess, H, I, M):
     """h = silu(x Wg) * (x Wu) from the fused launch against the oracle."""
     gate, up = _qt(75, H + 1, I, H), _qt(75, H + 2, I, H)

@@ -56,6 +56,10 @@ EXACT_SHAPES = [  # (K, N, M): GEMV for M = 1, the batched-decode kernel for 2 <
     # 512-row-tile prefill GEMM (taken from 256 rows and 192 tiles of 128 outputs):
     # ragged M, a K step left half full, two row tiles
     (96, 24576, 300), (64, 24576, 520),
+    # the same with K split into ranges (fewer than 192 tiles): 6 ranges of the
+    # 4096 x 4096 tile grid, 8 ranges with a half-full last step and ragged N,
+    # two row tiles, and 8 ranges over 14336 inputs (the ragged N = 130 above)
+    (4096, 4096, 512), (4128, 600, 512), (8192, 1000, 700),
 ]
 
 
@@ -111,11 +115,12 @@ def test_scaling_by_two_and_determinism(sess, M):
     assert_doubles(y2, y1)
 
 
-def test_wide_gemm_scaling_by_two_and_determinism(sess):
-    """The 512-row-tile GEMM: y(2x) equals 2 y(x) (exact products, sums scaled
-    exactly) and repeated calls are bit-identical."""
+@pytest.mark.parametrize("K,N,M", [(128, 24576, 300), (4096, 4096, 512)])
+def test_wide_gemm_scaling_by_two_and_determinism(sess, K, N, M):
+    """The 512-row-tile GEMM, with one K range and with six: y(2x) equals
+    2 y(x) (exact products, sums scaled exactly) and repeated calls are
+    bit-identical (the ranges are added in a fixed order)."""
     import torch
-    K, N, M = 128, 24576, 300
     codes = synth.int4_codes(66, 1, N, K)
     scales = synth.group_scales(66, 1, N, K)
     xn, x = _x(66, M, M, K)
