@@ -700,8 +700,14 @@ atsi_status run_moe(atsi_ctx* c, const atsi_moe* m, const __half* x, int Mi, __h
   hipError_t e = launch_router(x, inv_r, (const __half*)m->router_w_f16, m->router_bias, Mi, H, E, k, part, idx, p,
                                dbg ? dbg->logits : nullptr, c->cs);
   if (e != hipSuccess) return hip_fail(c, e, "router launch");
-  e = launch_bucket(idx, Mi, k, E, resident, bm, counts, offsets, perm, inv, order, tiles, ntiles, c->cs);
-  if (e != hipSuccess) return hip_fail(c, e, "bucket launch");
+  // decode with every expert resident: the expert launches index routed pairs
+  // directly, and the bucketing only runs when the caller asks for its output
+  const bool by_pair = gemv && tb->n_streamed == 0;
+  const bool want_buckets = dbg && (dbg->counts || dbg->offsets || dbg->perm || dbg->inv_perm);
+  if (!by_pair || want_buckets) {
+    e = launch_bucket(idx, Mi, k, E, resident, bm, counts, offsets, perm, inv, order, tiles, ntiles, c->cs);
+    if (e != hipSuccess) return hip_fail(c, e, "bucket launch");
+  }
   if (tb->n_streamed > 0) {
     HIP_TRY(c, hipMemcpyAsync(c->pinned, counts, E * sizeof(int32_t), hipMemcpyDeviceToHost, c->cs));
     HIP_TRY(c, hipEventRecord(c->counts_ev, c->cs));
@@ -720,6 +726,11 @@ atsi_status run_moe(atsi_ctx* c, const atsi_moe* m, const __half* x, int Mi, __h
   a.k = k;
   a.H = H;
   a.I = I;
+  if (by_pair) {
+    a.pair_expert = idx;
+    a.n_pairs = Mk;
+    a.n_experts = E;
+  }
   // HBM-resident experts first: they run while the host learns which
   // streamed experts are needed.
   const int bound = bm == 1 ? Mk : Mk / bm + std::min(E, Mk);

@@ -35,6 +35,12 @@ struct MoeArgs {
   __half* out;                 // expert outputs [M*k][H], row = pair id
   const float* inv_r;          // per-token RMS-norm factor of x, or nullptr
   int k, H, I;
+  // decode with every expert HBM-resident (GEMV path only): tile t is routed
+  // pair t, whose expert is pair_expert[t]; its rows in h and out are t, so no
+  // bucketing sits between routing and the expert loads
+  const int32_t* pair_expert;
+  int n_pairs;
+  int n_experts;               // table entries (a pair naming another expert is skipped)
 };
 
 // router: logits = x W_r + b (fp32 accumulation), top-k with renormalised softmax

@@ -6,7 +6,8 @@
 // heavy-first: the expert with the most tokens starts first, so the Zipf head
 // does not finish last.  Only experts some token selected are ever read.
 //   gate/up : h[i] = silu(x[t] Wg_e) * (x[t] Wu_e) for bucket row i of pair
-//             (t, j), on the MFMA tile (prefill) or a GEMV (decode);
+//             (t, j), on the MFMA tile (prefill) or a GEMV (decode; with
+//             every expert resident the row is the pair id itself);
 //   down    : out[k*t + j] = h[i] Wd_e, stored by pair id (fp16);
 //   combine : y[t] = sum_j p[t][j] * out[k*t + j] in fp32, slot order, one
 //             rounding to fp16 -- no atomics, so results are deterministic.
@@ -33,6 +34,25 @@ __device__ __forceinline__ bool fetch_tile(const MoeArgs& a, int tix, int& e, in
   e = a.tiles[2 * tix];
   row0 = a.tiles[2 * tix + 1];
   w = a.table[e];
+  return true;
+}
+
+// GEMV tile: the h row i and pair id pr it computes, and the expert's weights.
+// Pair-indexed launches read one table entry per tile; bucketed ones follow
+// the tile list, the bucket offsets and the permutation.
+__device__ __forceinline__ bool fetch_row(const MoeArgs& a, int tix, int& i, int& pr, ExpertW& w) {
+  if (a.pair_expert) {
+    if (tix >= a.n_pairs) return false;
+    const int e = a.pair_expert[tix];
+    if ((unsigned)e >= (unsigned)a.n_experts) return false;
+    w = a.table[e];
+    i = pr = tix;
+    return true;
+  }
+  int e, row0;
+  if (!fetch_tile(a, tix, e, row0, w)) return false;
+  i = a.offsets[e] + row0;
+  pr = a.perm[i];
   return true;
 }
 
@@ -118,11 +138,9 @@ __global__ __launch_bounds__(gemv::kBlock) void expert_gemv(MoeArgs a, int tile_
   constexpr int CH = 2;
   constexpr int R2 = DOWN ? 1 : RW;
   const int tix = blockIdx.x % tile_bound, nb = blockIdx.x / tile_bound;
-  int e, row0;
+  int i, pr;
   ExpertW w;
-  if (!fetch_tile(a, tix, e, row0, w)) return;
-  const int i = a.offsets[e] + row0;
-  const int pr = a.perm[i];
+  if (!fetch_row(a, tix, i, pr, w)) return;
   const QView w1 = DOWN ? w.down : w.gate;
   const QView w2 = w.up;
   const int K = DOWN ? a.I : a.H, N = DOWN ? a.H : a.I;

@@ -100,16 +100,29 @@ __global__ __launch_bounds__(256) void router_topk_kernel(const float* __restric
   const int lane = threadIdx.x & 63;
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= M) return;
-  float v[2];
-  int id[2];
+  float v[2] = {0.f, 0.f};
+  int id[2] = {lane, lane + 64};
+  // the K-slice partials, 16 slices of both experts per round of loads (the
+  // partials come from other XCDs' writes, a memory round trip each), added
+  // in slice order
+  for (int sp0 = 0; sp0 < n_split; sp0 += 16) {
+    float pv[2][16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j)
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+        pv[h][j] = (sp0 + j < n_split && id[h] < E) ? part[((size_t)(sp0 + j) * M + t) * E + id[h]] : 0.f;
+#pragma unroll
+    for (int j = 0; j < 16; ++j)
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+        if (sp0 + j < n_split) v[h] += pv[h][j];
+  }
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
-    const int e = lane + 64 * h;
-    id[h] = e;
+    const int e = id[h];
     if (e < E) {
-      float s = 0.f;
-#pragma unroll 8
-      for (int sp = 0; sp < n_split; ++sp) s += part[((size_t)sp * M + t) * E + e];
+      float s = v[h];
       if (inv_r) s *= inv_r[t];  // RMS-normalised input: scale the product once
       if (bias) s += bias[e];
       v[h] = s;
@@ -236,8 +249,15 @@ __global__ __launch_bounds__(1024) void bucket_kernel(const int32_t* __restrict_
   }
   // heavy-first expert order: (count descending, id ascending)
   for (int e = tid; e < E; e += blockDim.x) {
+    const int ce = cnt[e];
     int r = 0;
-    for (int f = 0; f < E; ++f) r += (cnt[f] > cnt[e]) || (cnt[f] == cnt[e] && f < e);
+    for (int f0 = 0; f0 < E; f0 += 16) {  // E is a multiple of 16
+      int cf[16];
+#pragma unroll
+      for (int j = 0; j < 16; ++j) cf[j] = cnt[f0 + j];
+#pragma unroll
+      for (int j = 0; j < 16; ++j) r += (cf[j] > ce) || (cf[j] == ce && f0 + j < e);
+    }
     ord[r] = e;
     order[r] = e;
   }

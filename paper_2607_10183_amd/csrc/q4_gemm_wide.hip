@@ -385,15 +385,17 @@ __global__ __launch_bounds__(kThreads, 1) void q4_gemm_wide_kernel(LinOp op, Wid
 }
 
 // Sum of the K ranges of a split launch, in range order, then the epilogue of
-// the single-range kernel: one thread per output.
+// the single-range kernel: one thread per 4 consecutive outputs of a row
+// (16-byte loads of each range's partial sums).
 template <bool SWI, bool NORM>
 __global__ __launch_bounds__(256) void wide_reduce_kernel(LinOp op, WideMap tm, const float* __restrict__ part) {
   constexpr int NOUT = SWI ? kBN / 2 : kBN;
+  constexpr int Q = NOUT / 4;  // quads per tile row
   const long idx = (long)blockIdx.x * 256 + threadIdx.x;
-  const long total = (long)op.M * tm.tiles_n * NOUT;
+  const long total = (long)op.M * tm.tiles_n * Q;
   if (idx >= total) return;
-  const int o = (int)(idx % NOUT);
-  const long rest = idx / NOUT;
+  const int o = 4 * (int)(idx % Q);
+  const long rest = idx / Q;
   const int T = (int)(rest % tm.tiles_n), m = (int)(rest / tm.tiles_n);
   int sgi = 0;
   while (sgi < op.nseg - 1 && T >= tm.end[sgi] / tm.tiles_m) ++sgi;
@@ -402,18 +404,24 @@ __global__ __launch_bounds__(256) void wide_reduce_kernel(LinOp op, WideMap tm, 
   const int n = tni * NOUT + o;
   if (n >= sg.w.N) return;
   const size_t pc = (size_t)tm.tiles_n * kBN;
-  const int col = T * kBN + (SWI ? 64 * (o >> 5) + (o & 31) : o);
+  const int col = T * kBN + (SWI ? 64 * (o >> 5) + (o & 31) : o);  // 4 columns in one 32-column chunk
   const float* p = part + (size_t)m * pc + col;
   const size_t stride = (size_t)op.M * pc;
-  float g = 0.f, u = 0.f;
+  typedef float f4_t __attribute__((ext_vector_type(4)));
+  f4_t g = {0.f, 0.f, 0.f, 0.f}, u = g;
   for (int r = 0; r < tm.splits; ++r) {
-    g += p[r * stride];
-    if constexpr (SWI) u += p[r * stride + 32];
+    g += __builtin_nontemporal_load(reinterpret_cast<const f4_t*>(p + r * stride));
+    if constexpr (SWI) u += __builtin_nontemporal_load(reinterpret_cast<const f4_t*>(p + r * stride + 32));
   }
   const float sc = NORM ? op.rinv[m] : 1.f;
-  float v = g * sc;
-  if constexpr (SWI) v = silu_fast(v) * (u * sc);
-  emit_out(op, sg, sgi, m, n, v);
+  const float gv[4] = {g.x, g.y, g.z, g.w}, uv[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    if (n + e >= sg.w.N) break;
+    float v = gv[e] * sc;
+    if constexpr (SWI) v = silu_fast(v) * (uv[e] * sc);
+    emit_out(op, sg, sgi, m, n + e, v);
+  }
 }
 
 template <bool SWI, bool NORM>
@@ -427,8 +435,8 @@ hipError_t launch_wide(const LinOp& op, const WideMap& tm, float* part, hipStrea
                      tm, part);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const long outs = (long)op.M * tm.tiles_n * (SWI ? kBN / 2 : kBN);
-  hipLaunchKernelGGL((wide_reduce_kernel<SWI, NORM>), dim3((unsigned)((outs + 255) / 256)), dim3(256), 0, st, op, tm,
+  const long quads = (long)op.M * tm.tiles_n * (SWI ? kBN / 8 : kBN / 4);
+  hipLaunchKernelGGL((wide_reduce_kernel<SWI, NORM>), dim3((unsigned)((quads + 255) / 256)), dim3(256), 0, st, op, tm,
                      part);
   return hipGetLastError();
 }

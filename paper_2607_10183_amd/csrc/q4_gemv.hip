@@ -302,6 +302,7 @@ template <int C, bool SWI, int D>
 __global__ __launch_bounds__(1024) void q4_gemv1_kernel(LinOp op, Gemv1Map m) {
   constexpr int NT = SWI ? 2 : 1;
   constexpr int V = pad_pow2(NT * C);
+  static_assert(NT * C <= V, "one partial per row and tensor: at most 16 per lane");
   extern __shared__ __attribute__((aligned(16))) char smem[];
   __shared__ float sq_wave[16];
   int sgi = 0;
