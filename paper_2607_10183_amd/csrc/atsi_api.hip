@@ -735,6 +735,11 @@ atsi_status run_moe(atsi_ctx* c, const atsi_moe* m, const __half* x, int Mi, __h
   // streamed experts are needed.
   const int bound = bm == 1 ? Mk : Mk / bm + std::min(E, Mk);
   if ((e = launch_expert_gateup(a, bound, gemv, c->cs)) != hipSuccess) return hip_fail(c, e, "expert gate/up launch");
+  if (by_pair) {  // every expert resident: the down launch also combines
+    if ((e = launch_expert_down_combine(a, Mi, p, res, y, c->cs)) != hipSuccess)
+      return hip_fail(c, e, "expert down/combine launch");
+    return ATSI_OK;
+  }
   if ((e = launch_expert_down(a, bound, gemv, c->cs)) != hipSuccess) return hip_fail(c, e, "expert down launch");
 
   if (tb->n_streamed > 0) {

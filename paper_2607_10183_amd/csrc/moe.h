@@ -64,6 +64,11 @@ int expert_tile_rows(bool gemv);
 // grouped SwiGLU gate/up and grouped down; tile_bound = grid size in tiles
 hipError_t launch_expert_gateup(const MoeArgs& a, int tile_bound, bool gemv, hipStream_t s);
 hipError_t launch_expert_down(const MoeArgs& a, int tile_bound, bool gemv, hipStream_t s);
+// pair-indexed decode (a.pair_expert set): the down projections of all k
+// experts of each of the M tokens and the combine, in one launch; the same
+// results as launch_expert_down followed by launch_combine
+hipError_t launch_expert_down_combine(const MoeArgs& a, int M, const float* p, const __half* res, __half* y,
+                                      hipStream_t s);
 // y[t] = sum_j p[t][j] * out[k*t + j] (fp32, slot order) -> fp16
 hipError_t launch_combine(const __half* out, const float* p, int M, int k, int H, const __half* res, __half* y,
                           hipStream_t s);

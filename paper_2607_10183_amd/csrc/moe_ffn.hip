@@ -132,23 +132,15 @@ __global__ __launch_bounds__(kGemmBlock, 2) void expert_down_gemm(MoeArgs a, int
 
 // ---------------------------------------------------------------- GEMV path (one row per tile)
 
-template <int RW, bool DOWN>
-__global__ __launch_bounds__(gemv::kBlock) void expert_gemv(MoeArgs a, int tile_bound) {
+// Sums over the wave of RW rows n0 .. n0 + RW - 1 of w1 (and of w2 when TWO)
+// against one K-wide input row xr: lane l takes groups l, l + 64, ...; rows
+// past N repeat the last row and are discarded by the caller.
+template <int RW, bool TWO>
+__device__ __forceinline__ void expert_rows(const QView& w1, const QView& w2, const __half* xr, int n0, int N, int K,
+                                            int lane, float (&g)[RW], float (&u)[RW]) {
   using namespace gemv;
   constexpr int CH = 2;
-  constexpr int R2 = DOWN ? 1 : RW;
-  const int tix = blockIdx.x % tile_bound, nb = blockIdx.x / tile_bound;
-  int i, pr;
-  ExpertW w;
-  if (!fetch_row(a, tix, i, pr, w)) return;
-  const QView w1 = DOWN ? w.down : w.gate;
-  const QView w2 = w.up;
-  const int K = DOWN ? a.I : a.H, N = DOWN ? a.H : a.I;
-  const __half* xr = DOWN ? a.h + (size_t)i * a.I : a.x + (size_t)(pr / a.k) * a.H;
-
-  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
-  const int n0 = (nb * (kBlock / kWave) + wave) * RW;
-  if (n0 >= N) return;
+  constexpr int R2 = TWO ? RW : 1;
   const int nchunk = K / kGroup;
   const size_t rbytes = (size_t)K / 2;
   float acc[RW], acc2[R2], sq = 0.f;
@@ -169,7 +161,7 @@ __global__ __launch_bounds__(gemv::kBlock) void expert_gemv(MoeArgs a, int tile_
         const int row = min(n0 + r, N - 1);
         cw[h][r] = ldg16(w1.codes + (size_t)row * rbytes + (size_t)c * 16);
         sc[h][r] = ldg2(w1.scales + (size_t)row * nchunk + c);
-        if constexpr (!DOWN) {
+        if constexpr (TWO) {
           cw2[h][r] = ldg16(w2.codes + (size_t)row * rbytes + (size_t)c * 16);
           sc2[h][r] = ldg2(w2.scales + (size_t)row * nchunk + c);
         }
@@ -179,28 +171,91 @@ __global__ __launch_bounds__(gemv::kBlock) void expert_gemv(MoeArgs a, int tile_
 #pragma unroll
     for (int h = 0; h < CH; ++h) {
       if (c0 + h * kWave >= nchunk) break;
-      XGroup g;
-      prep_x(g, xv[h], false, sq);
+      XGroup gx;
+      prep_x(gx, xv[h], false, sq);
 #pragma unroll
       for (int r = 0; r < RW; ++r) {
-        acc[r] = fmaf(__half2float(__ushort_as_half(sc[h][r])), group_dot(cw[h][r], g), acc[r]);
-        if constexpr (!DOWN) acc2[r] = fmaf(__half2float(__ushort_as_half(sc2[h][r])), group_dot(cw2[h][r], g), acc2[r]);
+        acc[r] = fmaf(__half2float(__ushort_as_half(sc[h][r])), group_dot(cw[h][r], gx), acc[r]);
+        if constexpr (TWO) acc2[r] = fmaf(__half2float(__ushort_as_half(sc2[h][r])), group_dot(cw2[h][r], gx), acc2[r]);
       }
     }
   }
+#pragma unroll
+  for (int r = 0; r < RW; ++r) {
+    g[r] = wave_total(acc[r]);
+    u[r] = TWO ? wave_total(acc2[R2 > 1 ? r : 0]) : 0.f;
+  }
+}
+
+template <int RW, bool DOWN>
+__global__ __launch_bounds__(gemv::kBlock) void expert_gemv(MoeArgs a, int tile_bound) {
+  using namespace gemv;
+  const int tix = blockIdx.x % tile_bound, nb = blockIdx.x / tile_bound;
+  int i, pr;
+  ExpertW w;
+  if (!fetch_row(a, tix, i, pr, w)) return;
+  const int K = DOWN ? a.I : a.H, N = DOWN ? a.H : a.I;
+  const __half* xr = DOWN ? a.h + (size_t)i * a.I : a.x + (size_t)(pr / a.k) * a.H;
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+  const int n0 = (nb * (kBlock / kWave) + wave) * RW;
+  if (n0 >= N) return;
+  float g[RW], u[RW];
+  expert_rows<RW, !DOWN>(DOWN ? w.down : w.gate, w.up, xr, n0, N, K, lane, g, u);
   const float sc = (!DOWN && a.inv_r) ? a.inv_r[pr / a.k] : 1.f;  // RMS-normalised input
 #pragma unroll
   for (int r = 0; r < RW; ++r) {
-    const float g = wave_sum(acc[r]) * sc;
-    float u = 0.f;
-    if constexpr (!DOWN) u = wave_sum(acc2[r]) * sc;
     const int n = n0 + r;
     if (lane == r && n < N) {
       if (DOWN)
-        a.out[(size_t)pr * a.H + n] = __float2half_rn(g);
+        a.out[(size_t)pr * a.H + n] = __float2half_rn(g[r] * sc);
       else
-        a.h[(size_t)i * a.I + n] = __float2half_rn(silu_f(g) * u);
+        a.h[(size_t)i * a.I + n] = __float2half_rn(silu_f(g[r] * sc) * (u[r] * sc));
     }
+  }
+}
+
+// Down projection and combine in one launch (decode, every expert resident,
+// pair-indexed h): a workgroup owns kDcRows output rows of one token and
+// computes them for all k routed experts of that token (wave task = expert j,
+// RW rows), rounds each expert output to fp16 as the separate down launch
+// stores it, and sums p_j * out_j in slot order in fp32 plus the residual, as
+// the combine does.  y may alias res: each element is read, then written, by
+// one thread.
+constexpr int kDcRows = 4;
+constexpr int kDcThreads = 1024;
+
+template <int RW>
+__global__ __launch_bounds__(kDcThreads) void expert_down_combine(MoeArgs a, const float* __restrict__ p,
+                                                                  const __half* res, __half* y) {
+  using namespace gemv;
+  static_assert(kDcRows % RW == 0, "whole wave tasks per row block");
+  constexpr int SUB = kDcRows / RW;
+  __shared__ float outs[kMaxTopK][kDcRows];
+  const int t = blockIdx.y, nb = blockIdx.x * kDcRows;
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+  for (int task = wave; task < a.k * SUB; task += kDcThreads / kWave) {
+    const int j = task / SUB, n0 = nb + (task % SUB) * RW;
+    const int pr = t * a.k + j;
+    const int e = a.pair_expert[pr];
+    float g[RW], u[RW];
+    if ((unsigned)e < (unsigned)a.n_experts) {
+      expert_rows<RW, false>(a.table[e].down, a.table[e].down, a.h + (size_t)pr * a.I, n0, a.H, a.I, lane, g, u);
+    } else {
+#pragma unroll
+      for (int r = 0; r < RW; ++r) g[r] = 0.f;
+    }
+    if (lane == 0) {
+#pragma unroll
+      for (int r = 0; r < RW; ++r) outs[j][(task % SUB) * RW + r] = __half2float(__float2half_rn(g[r]));
+    }
+  }
+  __syncthreads();
+  const int n = nb + (int)threadIdx.x;
+  if (threadIdx.x < kDcRows && n < a.H) {
+    float acc = 0.f;
+    for (int j = 0; j < a.k; ++j) acc = fmaf(p[(size_t)t * a.k + j], outs[j][threadIdx.x], acc);
+    if (res) acc += __half2float(res[(size_t)t * a.H + n]);
+    y[(size_t)t * a.H + n] = __float2half_rn(acc);
   }
 }
 
@@ -287,6 +342,14 @@ hipError_t launch_expert_down(const MoeArgs& a, int tile_bound, bool gemv, hipSt
     const int tn = (a.H + EBN - 1) / EBN;
     hipLaunchKernelGGL(expert_down_gemm, dim3(tile_bound * tn), dim3(kGemmBlock), 0, s, a, tile_bound);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_expert_down_combine(const MoeArgs& a, int M, const float* p, const __half* res, __half* y,
+                                      hipStream_t s) {
+  if (!a.pair_expert || M < 1 || a.k > kMaxTopK) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((expert_down_combine<kGemvRW>), dim3((a.H + kDcRows - 1) / kDcRows, M), dim3(kDcThreads), 0, s, a,
+                     p, res, y);
   return hipGetLastError();
 }
 

@@ -12,7 +12,8 @@
 //   router_topk     one wavefront per token: sums the K-slice partials in a
 //                   fixed order, adds the bias, selects the top k by (logit
 //                   descending, expert id ascending) with k wave-wide argmax
-//                   rounds, and writes the softmax over the selected logits.
+//                   rounds (DPP inside rows of 16 lanes, scalar reads across
+//                   rows), and writes the softmax over the selected logits.
 //   bucket          one workgroup: per-expert counts (LDS integer atomics),
 //                   exclusive scan, then a stable scatter of pair ids k*t + j
 //                   ordered by (expert, token): each 64-token chunk builds a
@@ -91,6 +92,41 @@ __global__ __launch_bounds__(256) void router_partial_kernel(const __half* __res
   }
 }
 
+// (value, id) of the best candidate of the wave, by (value descending, id
+// ascending), returned to every lane: DPP steps inside rows of 16 lanes
+// (swap neighbours, swap pairs, mirror within 8, mirror within 16), then the
+// four row results read back as scalars.  Needs all 64 lanes active.
+__device__ __forceinline__ void wave_best(float& v, int& i) {
+  auto better = [](float av, int ai, float bv, int bi) { return av > bv || (av == bv && ai < bi); };
+#define ATSI_BEST_STEP(CTRL)                                                                             \
+  {                                                                                                      \
+    const float ov = __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false)); \
+    const int oi = __builtin_amdgcn_update_dpp(0, i, CTRL, 0xF, 0xF, false);                             \
+    if (better(ov, oi, v, i)) {                                                                          \
+      v = ov;                                                                                            \
+      i = oi;                                                                                            \
+    }                                                                                                    \
+  }
+  ATSI_BEST_STEP(0xB1)   // quad_perm 1,0,3,2
+  ATSI_BEST_STEP(0x4E)   // quad_perm 2,3,0,1
+  ATSI_BEST_STEP(0x141)  // row_half_mirror
+  ATSI_BEST_STEP(0x140)  // row_mirror
+#undef ATSI_BEST_STEP
+  float bv = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
+  int bi = __builtin_amdgcn_readlane(i, 0);
+#pragma unroll
+  for (int r = 1; r < 4; ++r) {
+    const float ov = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16 * r));
+    const int oi = __builtin_amdgcn_readlane(i, 16 * r);
+    if (better(ov, oi, bv, bi)) {
+      bv = ov;
+      bi = oi;
+    }
+  }
+  v = bv;
+  i = bi;
+}
+
 // one wave per token; E <= 128 (two candidates per lane)
 __global__ __launch_bounds__(256) void router_topk_kernel(const float* __restrict__ part, int n_split,
                                                           const float* __restrict__ inv_r,
@@ -102,9 +138,14 @@ __global__ __launch_bounds__(256) void router_topk_kernel(const float* __restric
   if (t >= M) return;
   float v[2] = {0.f, 0.f};
   int id[2] = {lane, lane + 64};
-  // the K-slice partials, 16 slices of both experts per round of loads (the
+  // every global load is issued before the first wait: the norm factor, the
+  // bias, then the K-slice partials, 16 slices of both experts per round (the
   // partials come from other XCDs' writes, a memory round trip each), added
   // in slice order
+  const float rs = inv_r ? inv_r[t] : 1.f;
+  float bv[2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) bv[h] = (bias && id[h] < E) ? bias[id[h]] : 0.f;
   for (int sp0 = 0; sp0 < n_split; sp0 += 16) {
     float pv[2][16];
 #pragma unroll
@@ -123,8 +164,8 @@ __global__ __launch_bounds__(256) void router_topk_kernel(const float* __restric
     const int e = id[h];
     if (e < E) {
       float s = v[h];
-      if (inv_r) s *= inv_r[t];  // RMS-normalised input: scale the product once
-      if (bias) s += bias[e];
+      if (inv_r) s *= rs;  // RMS-normalised input: scale the product once
+      if (bias) s += bv[h];
       v[h] = s;
       if (logits_out) logits_out[(size_t)t * E + e] = s;
     } else {
@@ -139,12 +180,7 @@ __global__ __launch_bounds__(256) void router_topk_kernel(const float* __restric
     int bi = id[0];
     if (v[1] > bv || (v[1] == bv && id[1] < bi)) { bv = v[1]; bi = id[1]; }
     if (bi >= E) bi = 0x7fffffff;
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      const float ov = __shfl_xor(bv, o, 64);
-      const int oi = __shfl_xor(bi, o, 64);
-      if (ov > bv || (ov == bv && oi < bi)) { bv = ov; bi = oi; }
-    }
+    wave_best(bv, bi);
     sel_v[j] = bv;
     sel_i[j] = bi;
     if (bi == id[0]) v[0] = -INFINITY, id[0] = 0x7fffffff;
