@@ -104,6 +104,7 @@ struct atsi_ctx {
   size_t table_floor = 0;       // lowest byte used by tables (ws_bytes if none)
   uint64_t placement_version = 0;
   unsigned* layer_bar = nullptr;  // barrier words of the fused decode layer (top of the workspace)
+  unsigned* route_count = nullptr;  // the router's finished-workgroup count, after the barrier words
   float* row_inv = nullptr;       // per-row 1/rms for normalised prefill GEMMs (below the barrier words)
   bool layer_launched = false;    // a fused layer ran since the last atsi_sync
   int32_t* pinned = nullptr;    // pinned host copy of per-expert counts
@@ -668,10 +669,11 @@ atsi_status check_moe(atsi_ctx* c, const atsi_moe* m) {
 
 // The routed MoE FFN (validated descriptor): y = sum_j p_j FFN_{e_j}(x) for
 // each token, plus res when res is given (y may then alias res but not x);
-// with inv_r the input is x * inv_r[t] per token, the factor applied to the
+// with inv_r the input is x * inv_r[t] per token (make_inv: the factors are
+// computed here into inv_r, with eps), the factor applied to the
 // router logits and the expert gate/up products.
 atsi_status run_moe(atsi_ctx* c, const atsi_moe* m, const __half* x, int Mi, __half* y, const atsi_moe_debug* dbg,
-                    const float* inv_r, const __half* res, Scratch& sc) {
+                    float* inv_r, bool make_inv, float eps, const __half* res, Scratch& sc) {
   atsi_status st;
   atsi_ctx::MoeTable* tb;
   if ((st = get_table(c, m, &tb))) return st;
@@ -697,8 +699,9 @@ atsi_status run_moe(atsi_ctx* c, const atsi_moe* m, const __half* x, int Mi, __h
   const ExpertW* table = reinterpret_cast<const ExpertW*>(c->ws + tb->off);
   const uint8_t* resident = reinterpret_cast<const uint8_t*>(c->ws + tb->off + align_up((size_t)E * sizeof(ExpertW)));
 
-  hipError_t e = launch_router(x, inv_r, (const __half*)m->router_w_f16, m->router_bias, Mi, H, E, k, part, idx, p,
-                               dbg ? dbg->logits : nullptr, c->cs);
+  hipError_t e = launch_router(x, make_inv ? nullptr : inv_r, make_inv ? inv_r : nullptr, eps,
+                               (const __half*)m->router_w_f16, m->router_bias, Mi, H, E, k, part, idx, p,
+                               dbg ? dbg->logits : nullptr, c->route_count, c->cs);
   if (e != hipSuccess) return hip_fail(c, e, "router launch");
   // decode with every expert resident: the expert launches index routed pairs
   // directly, and the bucketing only runs when the caller asks for its output
@@ -821,13 +824,14 @@ atsi_status atsi_create(int device, void* compute_stream, void* transfer_stream,
   c->ws_bytes = workspace_bytes;
   c->n_slots = n_slots;
   c->table_floor = workspace_bytes / kAlign * kAlign;
-  const size_t bar_bytes = align_up(kLayerBarrierWords * sizeof(unsigned));
+  const size_t bar_bytes = align_up((kLayerBarrierWords + 1) * sizeof(unsigned));
   if (c->table_floor < bar_bytes) {
     delete c;
     return fail(nullptr, ATSI_E_WORKSPACE, "workspace of %zu B is too small", workspace_bytes);
   }
   c->table_floor -= bar_bytes;
   c->layer_bar = reinterpret_cast<unsigned*>(c->ws + c->table_floor);
+  c->route_count = c->layer_bar + kLayerBarrierWords;
   // one float per activation row of the largest call (M <= 65536); left out of
   // small workspaces, where normalised prefill GEMMs keep the 128-row tiles
   const size_t rinv_bytes = align_up((size_t)kMaxCallRows * sizeof(float));
@@ -850,7 +854,8 @@ atsi_status atsi_create(int device, void* compute_stream, void* transfer_stream,
       return ATSI_E_HIP;
     }
   }
-  // the fused decode layer's barrier starts from zeroed words and leaves them so
+  // the fused decode layer's barrier and the router's count start from zeroed
+  // words and leave them so
   if (hipMemsetAsync(c->layer_bar, 0, bar_bytes, c->cs) != hipSuccess || hipStreamSynchronize(c->cs) != hipSuccess) {
     fail(nullptr, ATSI_E_HIP, "clearing the workspace barrier words failed");
     atsi_destroy(c);
@@ -1108,10 +1113,9 @@ atsi_status atsi_moe_decoder_layer(atsi_ctx* c, const atsi_moe_layer* L, void* h
   if ((st = prefetch_call(c, ids, 4))) return st;
   if ((st = run_attention(c, ids, L->n_heads, L->n_kv_heads, L->head_dim, L->eps, hh, Mi, qb, kb, oin))) return st;
   // h = h + MoE(rms(h)): the norm is a per-token factor on the router logits
-  // and the expert gate/up products, the residual is added by the combine
-  hipError_t e = launch_rms_inv(hh, Mi, (int)H, L->eps, inv_r, c->cs);
-  if (e != hipSuccess) return hip_fail(c, e, "rms launch");
-  return run_moe(c, L->moe, hh, Mi, hh, dbg, inv_r, hh, sc);
+  // and the expert gate/up products (computed with the routing), the residual
+  // is added by the combine
+  return run_moe(c, L->moe, hh, Mi, hh, dbg, inv_r, true, L->eps, hh, sc);
 }
 
 atsi_status atsi_rmsnorm(atsi_ctx* c, const void* x, int64_t M, int64_t H, float eps, void* y) {
@@ -1153,7 +1157,7 @@ atsi_status atsi_moe_ffn(atsi_ctx* c, const atsi_moe* m, const void* x, int64_t 
   if (x == y) return fail(c, ATSI_E_INVALID, "y must not alias x");
   if ((st = enter(c))) return st;
   Scratch sc(c);
-  return run_moe(c, m, (const __half*)x, (int)M, (__half*)y, dbg, nullptr, nullptr, sc);
+  return run_moe(c, m, (const __half*)x, (int)M, (__half*)y, dbg, nullptr, false, 0.f, nullptr, sc);
 }
 
 atsi_status atsi_set_schedule(atsi_ctx* c, const atsi_tid* order, int32_t n) {

@@ -43,9 +43,13 @@ struct MoeArgs {
   int n_experts;               // table entries (a pair naming another expert is skipped)
 };
 
-// router: logits = x W_r + b (fp32 accumulation), top-k with renormalised softmax
-hipError_t launch_router(const __half* x, const float* inv_r, const __half* wr, const float* bias, int M, int H,
-                         int E, int k, float* part, int32_t* idx, float* p, float* logits, hipStream_t s);
+// router: logits = x W_r + b (fp32 accumulation), top-k with renormalised
+// softmax.  Per-token norm factors: given (inv_r), computed here (inv_r_out,
+// with eps), or none.  counter: a word that is zero between launches (the
+// launch leaves it so); with it, up to 16 tokens are routed in one launch.
+hipError_t launch_router(const __half* x, const float* inv_r, float* inv_r_out, float eps, const __half* wr,
+                         const float* bias, int M, int H, int E, int k, float* part, int32_t* idx, float* p,
+                         float* logits, unsigned* counter, hipStream_t s);
 // inv_r[t] = 1 / sqrt(mean_k x[t][k]^2 + eps) (fp32)
 hipError_t launch_rms_inv(const __half* x, int M, int H, float eps, float* inv_r, hipStream_t s);
 // y[t] = x[t] * inv_r[t] in fp16 (y may alias x)

@@ -9,6 +9,10 @@
 //                   slice, on 16x16x32 fp16 MFMAs; the router slice is staged
 //                   through LDS transposed so each lane reads 8 consecutive
 //                   inputs of one expert; fp32 partials per slice.
+//                   A launch of at most 16 tokens routes them in its last
+//                   workgroup to finish (release/acquire fences around a
+//                   counter that the last one resets), and computes the
+//                   tokens' RMS-norm factors there when asked.
 //   router_topk     one wavefront per token: sums the K-slice partials in a
 //                   fixed order, adds the bias, selects the top k by (logit
 //                   descending, expert id ascending) with k wave-wide argmax
@@ -32,10 +36,114 @@ typedef float float4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kRT = 16;  // tokens per router tile
 
+// 1 / sqrt(mean(x[t]^2) + eps) for one token, computed by one wavefront and
+// returned to every lane (the same arithmetic for every caller)
+__device__ __forceinline__ float token_inv_rms(const __half* __restrict__ x, int t, int H, float eps) {
+  const int lane = threadIdx.x & 63;
+  float q = 0.f;
+  for (int c = lane * 8; c < H; c += 64 * 8) {
+    const uint4 v = *reinterpret_cast<const uint4*>(x + (size_t)t * H + c);
+    const __half* hv = reinterpret_cast<const __half*>(&v);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const float f = __half2float(hv[i]);
+      q = fmaf(f, f, q);
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) q += __shfl_xor(q, o, 64);
+  return 1.f / sqrtf(q / (float)H + eps);
+}
+
+__device__ __forceinline__ void wave_best(float& v, int& i);
+
+// Routing of token t by one wavefront (E <= 128, two candidates per lane):
+// the K-slice partial logits summed in slice order, times the norm factor rs
+// when norm is set, plus the bias; the top k by (logit descending, expert id
+// ascending) in k argmax rounds; the softmax over the selected logits.
+__device__ __forceinline__ void route_token(const float* __restrict__ part, int n_split, int M, int t, bool norm,
+                                            float rs, const float* __restrict__ bias, int E, int k,
+                                            int32_t* __restrict__ idx, float* __restrict__ p,
+                                            float* __restrict__ logits_out) {
+  const int lane = threadIdx.x & 63;
+  float v[2] = {0.f, 0.f};
+  int id[2] = {lane, lane + 64};
+  // every global load is issued before the first wait: the bias, then the
+  // K-slice partials, 16 slices of both experts per round (the partials come
+  // from other XCDs' writes, a memory round trip each), added in slice order
+  float bv[2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) bv[h] = (bias && id[h] < E) ? bias[id[h]] : 0.f;
+  for (int sp0 = 0; sp0 < n_split; sp0 += 16) {
+    float pv[2][16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j)
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+        pv[h][j] = (sp0 + j < n_split && id[h] < E) ? part[((size_t)(sp0 + j) * M + t) * E + id[h]] : 0.f;
+#pragma unroll
+    for (int j = 0; j < 16; ++j)
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+        if (sp0 + j < n_split) v[h] += pv[h][j];
+  }
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int e = id[h];
+    if (e < E) {
+      float s = v[h];
+      if (norm) s *= rs;  // RMS-normalised input: scale the product once
+      if (bias) s += bv[h];
+      v[h] = s;
+      if (logits_out) logits_out[(size_t)t * E + e] = s;
+    } else {
+      v[h] = -INFINITY;
+    }
+  }
+  float sel_v[16];
+  int sel_i[16];
+  for (int j = 0; j < k; ++j) {
+    // best of this lane: larger value, then lower id
+    float bv2 = v[0];
+    int bi = id[0];
+    if (v[1] > bv2 || (v[1] == bv2 && id[1] < bi)) { bv2 = v[1]; bi = id[1]; }
+    if (bi >= E) bi = 0x7fffffff;
+    wave_best(bv2, bi);
+    sel_v[j] = bv2;
+    sel_i[j] = bi;
+    if (bi == id[0]) v[0] = -INFINITY, id[0] = 0x7fffffff;
+    if (bi == id[1]) v[1] = -INFINITY, id[1] = 0x7fffffff;
+  }
+  if (lane == 0) {
+    float den = 0.f;
+    for (int j = 0; j < k; ++j) den += expf(sel_v[j] - sel_v[0]);
+    for (int j = 0; j < k; ++j) {
+      idx[(size_t)t * k + j] = sel_i[j];
+      p[(size_t)t * k + j] = expf(sel_v[j] - sel_v[0]) / den;
+    }
+  }
+}
+
+// Outputs of the routing of one launch: the last workgroup of a single-tile
+// launch (FUSED) routes the tile's tokens itself.
+struct RouteOut {
+  unsigned* counter;        // zero between launches; counts finished workgroups
+  const float* inv_r;       // per-token norm factors given by the caller, or null
+  float* inv_r_out;         // non-null: compute them here (and write them)
+  float eps;
+  const float* bias;
+  int k;
+  int32_t* idx;
+  float* p;
+  float* logits;
+};
+
 // grid: (ceil(M/16), n_split); block 256 = 4 waves x 32 experts (E <= 128).
 // Requires E % 16 == 0, E <= 128, ks % 32 == 0.
+template <bool FUSED>
 __global__ __launch_bounds__(256) void router_partial_kernel(const __half* __restrict__ x, const __half* __restrict__ wr,
-                                                             int M, int H, int E, int ks, float* __restrict__ part) {
+                                                             int M, int H, int E, int ks, float* __restrict__ part,
+                                                             RouteOut ro) {
   __shared__ __attribute__((aligned(16))) _Float16 Bt[128 * (32 + 8)];  // [expert][k] of one 32-k step
   const int t0 = blockIdx.x * kRT;
   const int k_begin = blockIdx.y * ks;
@@ -90,6 +198,30 @@ __global__ __launch_bounds__(256) void router_partial_kernel(const __half* __res
       if (t < M) part[((size_t)blockIdx.y * M + t) * E + e] = acc[nb][i];
     }
   }
+  if constexpr (FUSED) {
+    // The last workgroup to finish routes the tile: every workgroup makes its
+    // partials visible device-wide (release) before it counts itself; the last
+    // one acquires them all, resets the count for the next launch and routes.
+    __shared__ unsigned ticket;
+    __threadfence();
+    if (threadIdx.x == 0) ticket = atomicAdd(ro.counter, 1u);
+    __syncthreads();
+    if (ticket != gridDim.y - 1) return;
+    __threadfence();
+    if (threadIdx.x == 0) atomicExch(ro.counter, 0u);
+    for (int tt = wave; tt < kRT; tt += 4) {
+      const int t = t0 + tt;
+      if (t >= M) break;
+      float rs = 1.f;
+      if (ro.inv_r_out) {
+        rs = token_inv_rms(x, t, H, ro.eps);
+        if (lane == 0) ro.inv_r_out[t] = rs;
+      } else if (ro.inv_r) {
+        rs = ro.inv_r[t];
+      }
+      route_token(part, gridDim.y, M, t, ro.inv_r_out || ro.inv_r, rs, ro.bias, E, ro.k, ro.idx, ro.p, ro.logits);
+    }
+  }
 }
 
 // (value, id) of the best candidate of the wave, by (value descending, id
@@ -133,67 +265,10 @@ __global__ __launch_bounds__(256) void router_topk_kernel(const float* __restric
                                                           const float* __restrict__ bias, int M, int E, int k,
                                                           int32_t* __restrict__ idx, float* __restrict__ p,
                                                           float* __restrict__ logits_out) {
-  const int lane = threadIdx.x & 63;
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= M) return;
-  float v[2] = {0.f, 0.f};
-  int id[2] = {lane, lane + 64};
-  // every global load is issued before the first wait: the norm factor, the
-  // bias, then the K-slice partials, 16 slices of both experts per round (the
-  // partials come from other XCDs' writes, a memory round trip each), added
-  // in slice order
   const float rs = inv_r ? inv_r[t] : 1.f;
-  float bv[2];
-#pragma unroll
-  for (int h = 0; h < 2; ++h) bv[h] = (bias && id[h] < E) ? bias[id[h]] : 0.f;
-  for (int sp0 = 0; sp0 < n_split; sp0 += 16) {
-    float pv[2][16];
-#pragma unroll
-    for (int j = 0; j < 16; ++j)
-#pragma unroll
-      for (int h = 0; h < 2; ++h)
-        pv[h][j] = (sp0 + j < n_split && id[h] < E) ? part[((size_t)(sp0 + j) * M + t) * E + id[h]] : 0.f;
-#pragma unroll
-    for (int j = 0; j < 16; ++j)
-#pragma unroll
-      for (int h = 0; h < 2; ++h)
-        if (sp0 + j < n_split) v[h] += pv[h][j];
-  }
-#pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    const int e = id[h];
-    if (e < E) {
-      float s = v[h];
-      if (inv_r) s *= rs;  // RMS-normalised input: scale the product once
-      if (bias) s += bv[h];
-      v[h] = s;
-      if (logits_out) logits_out[(size_t)t * E + e] = s;
-    } else {
-      v[h] = -INFINITY;
-    }
-  }
-  float sel_v[16];
-  int sel_i[16];
-  for (int j = 0; j < k; ++j) {
-    // best of this lane: larger value, then lower id
-    float bv = v[0];
-    int bi = id[0];
-    if (v[1] > bv || (v[1] == bv && id[1] < bi)) { bv = v[1]; bi = id[1]; }
-    if (bi >= E) bi = 0x7fffffff;
-    wave_best(bv, bi);
-    sel_v[j] = bv;
-    sel_i[j] = bi;
-    if (bi == id[0]) v[0] = -INFINITY, id[0] = 0x7fffffff;
-    if (bi == id[1]) v[1] = -INFINITY, id[1] = 0x7fffffff;
-  }
-  if (lane == 0) {
-    float den = 0.f;
-    for (int j = 0; j < k; ++j) den += expf(sel_v[j] - sel_v[0]);
-    for (int j = 0; j < k; ++j) {
-      idx[(size_t)t * k + j] = sel_i[j];
-      p[(size_t)t * k + j] = expf(sel_v[j] - sel_v[0]) / den;
-    }
-  }
+  route_token(part, n_split, M, t, inv_r != nullptr, rs, bias, E, k, idx, p, logits_out);
 }
 
 // Single workgroup of 1024 threads.  Up to 16 chunks of 64 tokens are ranked
@@ -319,22 +394,10 @@ __global__ __launch_bounds__(1024) void bucket_kernel(const int32_t* __restrict_
 // one wavefront per token: inv_r[t] = 1 / sqrt(mean(x[t]^2) + eps)
 __global__ __launch_bounds__(256) void rms_inv_kernel(const __half* __restrict__ x, int M, int H, float eps,
                                                       float* __restrict__ inv_r) {
-  const int lane = threadIdx.x & 63;
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= M) return;
-  float q = 0.f;
-  for (int c = lane * 8; c < H; c += 64 * 8) {
-    const uint4 v = *reinterpret_cast<const uint4*>(x + (size_t)t * H + c);
-    const __half* hv = reinterpret_cast<const __half*>(&v);
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const float f = __half2float(hv[i]);
-      q = fmaf(f, f, q);
-    }
-  }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) q += __shfl_xor(q, o, 64);
-  if (lane == 0) inv_r[t] = 1.f / sqrtf(q / (float)H + eps);
+  const float r = token_inv_rms(x, t, H, eps);
+  if ((threadIdx.x & 63) == 0) inv_r[t] = r;
 }
 
 // one wavefront per token: y[t] = x[t] * inv_r (one fp16 rounding); y may alias x
@@ -409,14 +472,29 @@ hipError_t launch_rms_inv(const __half* x, int M, int H, float eps, float* inv_r
   return hipGetLastError();
 }
 
-hipError_t launch_router(const __half* x, const float* inv_r, const __half* wr, const float* bias, int M, int H,
-                         int E, int k, float* part, int32_t* idx, float* p, float* logits, hipStream_t s) {
+hipError_t launch_router(const __half* x, const float* inv_r, float* inv_r_out, float eps, const __half* wr,
+                         const float* bias, int M, int H, int E, int k, float* part, int32_t* idx, float* p,
+                         float* logits, unsigned* counter, hipStream_t s) {
   // K slice per workgroup: enough workgroups to cover the chip, slices of >= 64
   const int tiles = (M + kRT - 1) / kRT;
   int ks = H;
   while (ks > 64 && (long)tiles * (H / ks) < 512 && (ks / 2) % 32 == 0 && H % (ks / 2) == 0) ks /= 2;
   const int n_split = H / ks;
-  hipLaunchKernelGGL(router_partial_kernel, dim3(tiles, n_split), dim3(256), 0, s, x, wr, M, H, E, ks, part);
+  RouteOut ro{counter, inv_r, inv_r_out, eps, bias, k, idx, p, logits};
+  if (tiles == 1 && counter) {
+    // one tile: its last workgroup routes (no second launch)
+    hipLaunchKernelGGL(router_partial_kernel<true>, dim3(tiles, n_split), dim3(256), 0, s, x, wr, M, H, E, ks, part,
+                       ro);
+    return hipGetLastError();
+  }
+  if (inv_r_out) {
+    hipLaunchKernelGGL(rms_inv_kernel, dim3((M + 3) / 4), dim3(256), 0, s, x, M, H, eps, inv_r_out);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    inv_r = inv_r_out;
+  }
+  hipLaunchKernelGGL(router_partial_kernel<false>, dim3(tiles, n_split), dim3(256), 0, s, x, wr, M, H, E, ks, part,
+                     ro);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(router_topk_kernel, dim3((M + 3) / 4), dim3(256), 0, s, part, n_split, inv_r, bias, M, E, k,
