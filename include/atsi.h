@@ -254,6 +254,42 @@ typedef struct {
 /* *out = the counters; reset != 0 then zeroes them. */
 atsi_status atsi_get_stats(atsi_ctx* ctx, atsi_stats* out, int32_t reset);
 
+/* ---- Static tensor placement (Sec. 4.3 problem formulation; Alg. 1) ----
+ * Chooses which tensors stay resident in GPU memory.  Host computation only:
+ * no GPU call and no context.  Tensor i is the i-th in execution order:
+ *   size_bytes[i]  its size (finite, >= 0);
+ *   r[i]           latency saved by keeping it on the GPU (t^c - t^g), finite;
+ *   c[i]           cost of a backend switch between tensors i-1 and i (c[0] unused), finite;
+ *   is_expert      nullable; 1 marks an MoE expert tensor (an operator's experts as one tensor).
+ * The result maximises sum_i r[i] [GPU] - sum_{i>=1} c[i] [b_i != b_{i-1}] with
+ * the GPU-resident sizes, rounded up to whole granules, within budget_bytes
+ * rounded down to whole granules (granularity_bytes > 0; the paper uses MB).
+ * With is_expert, Alg. 1's branch applies first: a budget that covers every
+ * non-expert tensor puts them all on the GPU and experts are chosen within
+ * what remains; otherwise every expert stays on the CPU and the non-expert
+ * tensors are chosen within the budget.  Fixed tensors keep their backend
+ * while the choice optimises the whole objective, switches included.
+ * Outputs: on_gpu_out[n] (caller-owned) = 1 for GPU-resident, 0 otherwise
+ * (atsi_set_placement takes the opposite mask: 1 = host); objective_out
+ * (nullable) = the objective of that placement from the unrounded inputs.
+ * Equal-objective ties go to the placement whose backtrack prefers the CPU
+ * predecessor and the fewest units, so results are deterministic.
+ * Errors (message from atsi_last_error(NULL)): ATSI_E_INVALID for NULL
+ * arrays, non-finite values, a negative size or budget, a non-positive
+ * granularity; ATSI_E_SHAPE for n < 1, or when n times the budget units
+ * exceeds 2^31 (use a coarser granularity).  Memory: n * units / 4 bytes. */
+typedef struct {
+  int32_t n;
+  const double* size_bytes;
+  const double* r;
+  const double* c;
+  const uint8_t* is_expert;
+  double budget_bytes;
+  double granularity_bytes;
+} atsi_placement_problem;
+
+atsi_status atsi_solve_placement(const atsi_placement_problem* problem, uint8_t* on_gpu_out, double* objective_out);
+
 /* Test export: the signed codes q[N][K] (int8, device buffer) of tensor w as
  * the library reads them, from wherever w currently lives. */
 atsi_status atsi_debug_unpack(atsi_ctx* ctx, atsi_tid w, int8_t* q_out);

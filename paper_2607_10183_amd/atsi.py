@@ -53,6 +53,12 @@ class atsi_moe_layer(ctypes.Structure):
                 ("o", ctypes.c_int32), ("moe", ctypes.POINTER(atsi_moe))]
 
 
+class atsi_placement_problem(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_int32), ("size_bytes", ctypes.c_void_p), ("r", ctypes.c_void_p),
+                ("c", ctypes.c_void_p), ("is_expert", ctypes.c_void_p), ("budget_bytes", ctypes.c_double),
+                ("granularity_bytes", ctypes.c_double)]
+
+
 _P = ctypes.c_void_p
 class atsi_stats(ctypes.Structure):
     _fields_ = [("h2d_bytes", ctypes.c_uint64), ("h2d_copies", ctypes.c_uint64), ("h2d_tensors", ctypes.c_uint64),
@@ -80,6 +86,8 @@ _SIGS = {
     "atsi_sync": ([_P], ctypes.c_int),
     "atsi_get_stats": ([_P, ctypes.POINTER(atsi_stats), ctypes.c_int32], ctypes.c_int),
     "atsi_debug_unpack": ([_P, ctypes.c_int32, _P], ctypes.c_int),
+    "atsi_solve_placement": ([ctypes.POINTER(atsi_placement_problem), _P, ctypes.POINTER(ctypes.c_double)],
+                             ctypes.c_int),
 }
 
 _lib = None
@@ -193,3 +201,19 @@ def atsi_get_stats(ctx: int, reset: bool = False) -> dict:
 
 def atsi_debug_unpack(ctx: int, w: int, q_out: int) -> None:
     _check(ctx, lib().atsi_debug_unpack(ctx, w, q_out))
+
+
+def atsi_solve_placement(size_bytes, r, c, budget_bytes: float, granularity_bytes: float = float(1 << 20),
+                         is_expert=None):
+    """(on_gpu list of 0/1, objective) of the static placement (host computation)."""
+    n = len(size_bytes)
+    D = ctypes.c_double * n
+    sa, ra, ca = D(*map(float, size_bytes)), D(*map(float, r)), D(*map(float, c))
+    ea = (ctypes.c_uint8 * n)(*[int(v) for v in is_expert]) if is_expert is not None else None
+    prob = atsi_placement_problem(n, ctypes.cast(sa, _P), ctypes.cast(ra, _P), ctypes.cast(ca, _P),
+                                  ctypes.cast(ea, _P) if ea is not None else None, float(budget_bytes),
+                                  float(granularity_bytes))
+    out = (ctypes.c_uint8 * max(n, 1))()
+    obj = ctypes.c_double()
+    _check(None, lib().atsi_solve_placement(ctypes.byref(prob), ctypes.cast(out, _P), ctypes.byref(obj)))
+    return [int(out[i]) for i in range(n)], obj.value

@@ -76,6 +76,11 @@ thread_local std::string g_create_error;
 
 }  // namespace
 
+namespace atsi {
+// the message atsi_last_error(NULL) returns, for calls made without a context
+void set_context_free_error(const char* msg) { g_create_error = msg; }
+}  // namespace atsi
+
 struct atsi_ctx {
   int device = 0;
   hipStream_t cs = nullptr;  // compute stream
