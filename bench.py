@@ -30,6 +30,8 @@ synthetic weights and activations.
                     one 235B-A22B-shaped MoE decoder layer at decode and
                     2048-token prefill, all-HBM and with 40 % of its experts
                     streamed (94-layer figures = 94 x the layer).
+  placement_solver  host time of the static placement solver (Alg. 1) on the
+                    94-layer 235B-A22B-shaped model at 1 MiB granularity.
   cpu_baseline      the fp64 oracle's decode step on the host cores.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
@@ -301,6 +303,9 @@ def main() -> int:
         stacks = {"dense_stack": bench_dense_stack(timer_cls=Timer, h2d_gbs=h2d_gbs),
                   "moe_stack": bench_moe_stack(timer_cls=Timer)}
 
+    placement = bench_placement_solver()
+    log(f"placement solver: {placement}")
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(W, shape, args.cpu_seconds, layer_bytes)
@@ -354,6 +359,7 @@ def main() -> int:
                      "prefill_tokens_per_s": round(Mp / st_pf, 1)},
         "moe": moe,
         "stacks": stacks,
+        "placement_solver": placement,
         "cpu_baseline": cpu,
     }
     if args.no_stacks:
@@ -605,6 +611,33 @@ def bench_moe_stack(timer_cls):
                                        "prefill_pcie_GBps": round(p_h2d / p_st / 1e9, 2),
                                        "decode_tokens_per_s_94_layers": round(1.0 / (94 * d_st), 2),
                                        "prefill_tokens_per_s_94_layers": round(wl.prefill_m / (94 * p_st), 1)}}
+
+
+def bench_placement_solver(reps: int = 3):
+    """Host time of atsi_solve_placement on the 94-layer 235B-A22B-shaped
+    model: per layer q, k, v, o, the router and the gate / up / down expert
+    operators (128 experts each, one tensor per operator), 1 MiB granularity,
+    a budget of half the model's 131.5 GB.  Gains are seeded (each tensor's
+    size over 20 GB/s, times U(0.5, 1.5)); switch costs 20 us."""
+    from paper_2607_10183_amd import atsi
+    layer = [18874368, 1179648, 1179648, 18874368, 1048576, 128 * 3538944, 128 * 3538944, 128 * 3538944]
+    expert_role = [0, 0, 0, 0, 0, 1, 1, 1]
+    s = [float(v) for _ in range(94) for v in layer]
+    expert = [e for _ in range(94) for e in expert_role]
+    rng = np.random.default_rng(2607)
+    r = list(np.array(s) / 2e10 * rng.uniform(0.5, 1.5, len(s)))
+    c = [2e-5] * len(s)
+    budget = 0.5 * sum(s)
+    best = float("inf")
+    for _ in range(reps):
+        t0 = time.perf_counter()
+        b, obj = atsi.atsi_solve_placement(s, r, c, budget, float(1 << 20), expert)
+        best = min(best, time.perf_counter() - t0)
+    units = int((budget - sum(x for x, e in zip(s, expert) if not e)) // (1 << 20))
+    return {"workload": "static placement of the 94-layer 235B-A22B-shaped model (752 tensors), 1 MiB "
+                        "granularity, budget half the model", "tensors": len(s), "budget_units": units,
+            "gpu_resident_bytes": int(sum(x for x, g in zip(s, b) if g)), "objective_s": round(obj, 6),
+            "host_ms": round(best * 1e3, 2)}
 
 
 def cpu_baseline(W, shape, budget_s, layer_bytes):
