@@ -156,7 +156,13 @@ typedef struct {
  * (device buffers), else to scratch.  rms(v) = v / sqrt(mean(v^2) + eps).
  * Four launches: fused RMS-norm + Q/K/V, O + residual, fused RMS-norm +
  * gate/up + SwiGLU, down + residual.  Streamed tensors of the layer are
- * queued for copy at entry so their transfers overlap earlier launches. */
+ * queued for copy at entry so their transfers overlap earlier launches.
+ * A context created with the environment variable ATSI_FUSED_DECODE_LAYER=1
+ * runs a batch-1 layer whose tensors are all HBM-resident, of the 8B shape
+ * (hidden 4096, 32 x 128 query and 8 x 128 KV heads, SwiGLU 14336), on a
+ * 256-CU device, as one persistent launch with grid barriers instead (the
+ * same bits; slower than the four launches on MI355X).  A barrier of that
+ * launch that does not complete is reported by atsi_sync. */
 atsi_status atsi_decoder_layer(atsi_ctx* ctx, const atsi_dense_layer* layer, void* h_f16, int64_t M,
                                void* q_out_f16, void* k_out_f16);
 

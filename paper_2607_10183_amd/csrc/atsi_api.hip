@@ -17,6 +17,7 @@
 #include <cstdarg>
 #include <deque>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <new>
 #include <string>
@@ -32,9 +33,10 @@ using namespace atsi;
 namespace {
 
 constexpr size_t kAlign = 256;
-// The single-launch decode layer (q4_layer.hip) is not enabled yet: it has not
-// passed its GPU tests.  Decoder layers run as four fused launches.
-constexpr bool kFusedDecodeLayer = false;
+// Batch-1 decode of an all-resident 8B-shaped layer can run as one persistent
+// launch (q4_layer.hip, the same bits as the four fused launches).  It is
+// slower on MI355X than the four launches, so a context takes it only when
+// ATSI_FUSED_DECODE_LAYER=1 is set at atsi_create.
 inline size_t align_up(size_t v, size_t a = kAlign) { return (v + a - 1) / a * a; }
 
 struct Tensor {
@@ -112,6 +114,7 @@ struct atsi_ctx {
   unsigned* route_count = nullptr;  // the router's finished-workgroup count, after the barrier words
   float* row_inv = nullptr;       // per-row 1/rms for normalised prefill GEMMs (below the barrier words)
   bool layer_launched = false;    // a fused layer ran since the last atsi_sync
+  bool fused_layer = false;       // batch-1 decode layers take the single persistent launch
   int32_t* pinned = nullptr;    // pinned host copy of per-expert counts
   hipEvent_t counts_ev = nullptr;
   atsi_stats stats{};           // transfer counters (atsi_get_stats)
@@ -828,6 +831,7 @@ atsi_status atsi_create(int device, void* compute_stream, void* transfer_stream,
   c->ws = (char*)workspace;
   c->ws_bytes = workspace_bytes;
   c->n_slots = n_slots;
+  if (const char* f = getenv("ATSI_FUSED_DECODE_LAYER")) c->fused_layer = atoi(f) == 1;
   c->table_floor = workspace_bytes / kAlign * kAlign;
   const size_t bar_bytes = align_up((kLayerBarrierWords + 1) * sizeof(unsigned));
   if (c->table_floor < bar_bytes) {
@@ -1042,7 +1046,7 @@ atsi_status atsi_decoder_layer(atsi_ctx* c, const atsi_dense_layer* L, void* h, 
   const float eps = L->eps;
   bool resident = true;
   for (atsi_tid t : ids) resident = resident && !c->tensors[t].on_host;
-  if (kFusedDecodeLayer && Mi == 1 && resident && !L->renorm_out) {
+  if (c->fused_layer && Mi == 1 && resident && !L->renorm_out) {
     // batch-1 decode with every weight in HBM: one fused launch
     LayerArgs la{};
     for (int i = 0; i < kLayerTensors; ++i) {

@@ -1,4 +1,5 @@
-// Fused batch-1 decode of a dense decoder layer (one cooperative launch).
+// Fused batch-1 decode of an 8B-shaped dense decoder layer (one persistent
+// launch of one workgroup per CU, grid barriers between its four phases).
 #pragma once
 
 #include "common.h"
@@ -13,7 +14,6 @@ enum LayerTensor { kQ = 0, kK, kV, kO, kGate, kUp, kDown, kLayerTensors };
 // flag, which stays set after a barrier that timed out)
 constexpr size_t kLayerBarrierWords = 352;
 constexpr int kLayerBarrierErrWord = 8 * 32 + 64;
-constexpr size_t kLayerMaxLds = 96 * 1024;
 
 struct LayerArgs {
   QView w[kLayerTensors];
@@ -25,12 +25,11 @@ struct LayerArgs {
   unsigned* bar;  // kLayerBarrierWords words of barrier state
   int H, Hq, Hkv, I, head_dim, expand;
   float eps;
-  int rpw[kLayerPhases];  // rows per wavefront, filled by the launcher
 };
 
-// LDS bytes the fused kernel needs per workgroup for `total` steps per wave
-size_t decode_layer_lds(const LayerArgs& a, int total);
-// hipErrorInvalidConfiguration when the layer does not fit the fused kernel
+// hipErrorInvalidConfiguration when the layer is not the shape the fused
+// kernel is built for (hidden 4096, 32 x 128 query and 8 x 128 KV heads,
+// SwiGLU 14336) or the device does not have 256 CUs for one workgroup each
 hipError_t launch_decode_layer(LayerArgs a, hipStream_t s);
 
 }  // namespace atsi

@@ -92,22 +92,56 @@ def test_decoder_layer_parity(sess, shape, M):
     check(k_out.cpu().numpy(), kr, zk, name="k projection")
 
 
-@pytest.mark.skip(reason="the single-launch cooperative decode layer (csrc/q4_layer.hip) is switched off "
-                         "(kFusedDecodeLayer = false): two GPU runs of this case faulted with an illegal address; "
-                         "two causes were shown on the CPU and fixed (a read past the per-wave step table, and the "
-                         "low address word read back from LDS sign-extended), and the path stays off until a run "
-                         "of this test passes")
-def test_fused_decode_layer_parity(sess):
-    """Batch-1 all-resident decode layer through the fused launch, against the oracle."""
+@pytest.fixture(scope="module")
+def fused_sess():
+    """A context created with the single-launch decode layer switched on."""
+    import os
+    from paper_2607_10183_amd.session import Session
+    old = os.environ.get("ATSI_FUSED_DECODE_LAYER")
+    os.environ["ATSI_FUSED_DECODE_LAYER"] = "1"
+    try:
+        s = Session(workspace_bytes=1 << 30, n_slots=4)
+    finally:
+        if old is None:
+            del os.environ["ATSI_FUSED_DECODE_LAYER"]
+        else:
+            os.environ["ATSI_FUSED_DECODE_LAYER"] = old
+    yield s
+    s.close()
+
+
+def test_fused_decode_layer_parity(fused_sess):
+    """Batch-1 all-resident decode layer through the single persistent launch,
+    against the oracle and bit for bit against the four-launch path."""
+    sess = fused_sess
     shape = configs.DenseShape()
     W = _layer_weights(shape, 77)
-    tids = {r: sess.register(*W[r]) for r in configs.ROLES}
+    tids = {r: sess.register(*W[r], hbm=True, host=(r == "down")) for r in configs.ROLES}
     hn = synth.activations(77, 1, 1, shape.hidden)
     h = _dev(hn)
     sess.decoder_layer(tids, h, shape.n_heads, shape.n_kv, shape.head_dim, 1e-6)
     sess.sync()
     ref, zeta, _ = oracle.decoder_layer(hn, W, shape.n_heads, shape.n_kv, shape.head_dim, 1e-6)
     check(h.cpu().numpy(), ref, zeta, name="fused decode layer")
+    # the four-launch path (taken when a tensor is host-resident) does the same
+    # per-row arithmetic: bit-identical residual stream, q and k
+    import torch
+    outs = []
+    for host in (False, True):
+        mask = list(sess.placement)
+        mask[tids["down"]] = int(host)
+        sess.set_placement(mask)
+        hh = _dev(hn)
+        q_out = torch.empty(shape.n_heads * shape.head_dim, dtype=torch.float16, device="cuda")
+        k_out = torch.empty(shape.n_kv * shape.head_dim, dtype=torch.float16, device="cuda")
+        sess.decoder_layer(tids, hh, shape.n_heads, shape.n_kv, shape.head_dim, 1e-6, q_out=q_out, k_out=k_out)
+        sess.sync()
+        outs.append((hh, q_out, k_out))
+    mask = list(sess.placement)
+    mask[tids["down"]] = 0
+    sess.set_placement(mask)
+    for a, b in zip(outs[0], outs[1]):
+        assert torch.equal(a, b)
 
 
 @pytest.mark.parametrize("M", [1, 512])
