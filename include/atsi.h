@@ -244,6 +244,20 @@ atsi_status atsi_moe_decoder_layer(atsi_ctx* ctx, const atsi_moe_layer* layer, v
 atsi_status atsi_moe_bucket(atsi_ctx* ctx, const int32_t* idx, int64_t M, int32_t k, int32_t n_experts,
                             int32_t* counts, int32_t* offsets, int32_t* perm, int32_t* inv_perm);
 
+/* Checking modes of the streaming engine (flags may be combined; 0 = off):
+ *   ATSI_DEBUG_POISON     every temporary slot is filled with 0xFF bytes
+ *                         (codes q = 7, scales fp16 NaN) on the transfer
+ *                         stream right before its copy, so a launch that read
+ *                         a slot before the copy landed would produce NaN;
+ *   ATSI_DEBUG_SERIALIZE  no overlap: each copy waits for every launch already
+ *                         enqueued on the compute stream and completes before
+ *                         the call goes on (host synchronisation).
+ * Outputs must not change with either flag (the engine's ordering is then
+ * checked by comparing outputs).  ATSI_E_INVALID for unknown bits. */
+#define ATSI_DEBUG_POISON 1u
+#define ATSI_DEBUG_SERIALIZE 2u
+atsi_status atsi_set_debug(atsi_ctx* ctx, uint32_t flags);
+
 /* Wait for both streams; returns the first latched asynchronous error. */
 atsi_status atsi_sync(atsi_ctx* ctx);
 

@@ -13,6 +13,9 @@ import os
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libatsi.so")
 
+DEBUG_POISON = 1
+DEBUG_SERIALIZE = 2
+
 STATUS = {0: "ATSI_OK", 1: "ATSI_E_INVALID", 2: "ATSI_E_SHAPE", 3: "ATSI_E_UNKNOWN_TENSOR",
           4: "ATSI_E_NO_COPY", 5: "ATSI_E_WORKSPACE", 6: "ATSI_E_HIP", 7: "ATSI_E_STATE"}
 
@@ -86,6 +89,7 @@ _SIGS = {
     "atsi_sync": ([_P], ctypes.c_int),
     "atsi_get_stats": ([_P, ctypes.POINTER(atsi_stats), ctypes.c_int32], ctypes.c_int),
     "atsi_debug_unpack": ([_P, ctypes.c_int32, _P], ctypes.c_int),
+    "atsi_set_debug": ([_P, ctypes.c_uint32], ctypes.c_int),
     "atsi_solve_placement": ([ctypes.POINTER(atsi_placement_problem), _P, ctypes.POINTER(ctypes.c_double)],
                              ctypes.c_int),
 }
@@ -217,3 +221,7 @@ def atsi_solve_placement(size_bytes, r, c, budget_bytes: float, granularity_byte
     obj = ctypes.c_double()
     _check(None, lib().atsi_solve_placement(ctypes.byref(prob), ctypes.cast(out, _P), ctypes.byref(obj)))
     return [int(out[i]) for i in range(n)], obj.value
+
+
+def atsi_set_debug(ctx: int, flags: int) -> None:
+    _check(ctx, lib().atsi_set_debug(ctx, int(flags)))

@@ -115,6 +115,7 @@ struct atsi_ctx {
   float* row_inv = nullptr;       // per-row 1/rms for normalised prefill GEMMs (below the barrier words)
   bool layer_launched = false;    // a fused layer ran since the last atsi_sync
   bool fused_layer = false;       // batch-1 decode layers take the single persistent launch
+  uint32_t debug = 0;             // ATSI_DEBUG_* flags (atsi_set_debug)
   int32_t* pinned = nullptr;    // pinned host copy of per-expert counts
   hipEvent_t counts_ev = nullptr;
   atsi_stats stats{};           // transfer counters (atsi_get_stats)
@@ -221,10 +222,40 @@ atsi_status retire(atsi_ctx* c, bool block) {
   return ATSI_OK;
 }
 
+// Poison mode: every byte of a slot about to receive a copy becomes 0xFF first
+// (codes q = 7, scales fp16 NaN), on the transfer stream ahead of the copy, so
+// a launch that read the slot before its copy landed would show NaN.  A fill
+// kernel rather than a memset node, so that captured streams stay valid.
+__global__ void poison_kernel(uint4* __restrict__ p, size_t n16) {
+  for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n16; i += (size_t)gridDim.x * 256)
+    p[i] = make_uint4(~0u, ~0u, ~0u, ~0u);
+}
+
+// Before a copy into `bytes` at base (slot-aligned, whole slots): poison it,
+// and in serialise mode let every launch already enqueued finish first.
+atsi_status before_copy(atsi_ctx* c, char* base, size_t bytes) {
+  if (c->debug & ATSI_DEBUG_SERIALIZE) HIP_TRY(c, hipStreamSynchronize(c->cs));
+  if (c->debug & ATSI_DEBUG_POISON) {
+    const size_t n16 = bytes / 16;
+    const unsigned blocks = (unsigned)std::min<size_t>((n16 + 255) / 256, 4096);
+    hipLaunchKernelGGL(poison_kernel, dim3(blocks), dim3(256), 0, c->ts, reinterpret_cast<uint4*>(base), n16);
+    HIP_TRY(c, hipGetLastError());
+  }
+  return ATSI_OK;
+}
+
+// In serialise mode a copy completes before the host goes on.
+atsi_status after_copy(atsi_ctx* c) {
+  if (c->debug & ATSI_DEBUG_SERIALIZE) HIP_TRY(c, hipStreamSynchronize(c->ts));
+  return ATSI_OK;
+}
+
 // Copy host tensor t into slot s on the transfer stream: one copy when its
 // host codes and scales are contiguous (small copies cost far more than their
 // bytes), else two.  The slot must be free.
 atsi_status copy_into(atsi_ctx* c, const Tensor& t, Slot& s) {
+  atsi_status st = before_copy(c, s.base, c->slot_bytes);
+  if (st) return st;
   if (t.host_contiguous()) {
     HIP_TRY(c, hipMemcpyAsync(s.base, t.hcodes, t.bytes(), hipMemcpyHostToDevice, c->ts));
     c->stats.h2d_copies += 1;
@@ -235,7 +266,7 @@ atsi_status copy_into(atsi_ctx* c, const Tensor& t, Slot& s) {
   }
   c->stats.h2d_bytes += t.bytes();
   c->stats.h2d_tensors += 1;
-  return ATSI_OK;
+  return after_copy(c);
 }
 
 void arm(atsi_ctx* c, Slot& s, atsi_tid tid, hipEvent_t ready) {
@@ -344,6 +375,8 @@ atsi_status issue_run(atsi_ctx* c, const atsi_tid* tids, int n, bool* issued) {
   }
   if (first < 0) return ATSI_OK;
   Slot& s0 = c->slots[first];
+  atsi_status st = before_copy(c, s0.base, (size_t)n * c->slot_bytes);
+  if (st) return st;
   HIP_TRY(c, hipMemcpyAsync(s0.base, c->tensors[tids[0]].hcodes, (size_t)n * c->slot_bytes, hipMemcpyHostToDevice,
                             c->ts));
   c->stats.h2d_copies += 1;
@@ -352,7 +385,7 @@ atsi_status issue_run(atsi_ctx* c, const atsi_tid* tids, int n, bool* issued) {
   HIP_TRY(c, hipEventRecord(s0.ready, c->ts));
   for (int i = 0; i < n; ++i) arm(c, c->slots[first + i], tids[i], s0.ready);
   *issued = true;
-  return ATSI_OK;
+  return after_copy(c);
 }
 
 // Keep the transfer stream ahead of compute without waiting: copy queued (or
@@ -1196,6 +1229,14 @@ atsi_status atsi_get_stats(atsi_ctx* c, atsi_stats* out, int32_t reset) {
   if (!c || !out) return fail(c, ATSI_E_INVALID, "ctx and out are required");
   *out = c->stats;
   if (reset) c->stats = atsi_stats{};
+  return ATSI_OK;
+}
+
+atsi_status atsi_set_debug(atsi_ctx* c, uint32_t flags) {
+  if (!c) return ATSI_E_INVALID;
+  if (flags & ~(uint32_t)(ATSI_DEBUG_POISON | ATSI_DEBUG_SERIALIZE))
+    return fail(c, ATSI_E_INVALID, "unknown debug flags 0x%x", flags);
+  c->debug = flags;
   return ATSI_OK;
 }
 

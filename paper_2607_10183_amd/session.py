@@ -101,6 +101,10 @@ class Session:
         self.placement.append(0)
         return tid
 
+    def set_debug(self, poison: bool = False, serialize: bool = False) -> None:
+        """Checking modes of the streaming engine (atsi_set_debug)."""
+        atsi.atsi_set_debug(self.ctx, (atsi.DEBUG_POISON if poison else 0) | (atsi.DEBUG_SERIALIZE if serialize else 0))
+
     def set_placement(self, host_mask) -> None:
         mask = [int(v) for v in host_mask]
         atsi.atsi_set_placement(self.ctx, mask)

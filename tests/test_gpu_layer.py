@@ -172,6 +172,39 @@ def test_layer_placement_invariance(sess, M):
         assert torch.equal(outs[0], o)
 
 
+@pytest.mark.parametrize("M", [1, 512])
+def test_layer_engine_checking_modes(sess, M):
+    """Streamed layers under poisoned slots (a read before its copy landed
+    would give NaN) and with copies serialised against compute give the
+    all-HBM output bit for bit."""
+    import torch
+    shape = configs.DenseShape()
+    W = _layer_weights(shape, 79)
+    tids = {r: sess.register(*W[r], hbm=True, host=True) for r in configs.ROLES}
+    h0 = _dev(synth.activations(79, M, M, shape.hidden))
+
+    def run(mask):
+        base = list(sess.placement)
+        for r, m in zip(configs.ROLES, mask):
+            base[tids[r]] = int(m)
+        sess.set_placement(base)
+        h = h0.clone()
+        sess.decoder_layer(tids, h, shape.n_heads, shape.n_kv, shape.head_dim)
+        sess.sync()
+        return h
+
+    ref = run([0] * 7)
+    try:
+        for poison, serialize in ((True, False), (False, True), (True, True)):
+            sess.set_debug(poison=poison, serialize=serialize)
+            for mask in (list(configs.dense_layer_host_mask()), [1] * 7):
+                out = run(mask)
+                assert torch.equal(ref, out), (poison, serialize, mask)
+    finally:
+        sess.set_debug()
+        run([0] * 7)
+
+
 def test_schedule_prefetch_across_layers(sess):
     """A schedule over two layers (all tensors on host, 4 slots) lets copies run
     ahead across layer boundaries; results equal the HBM-resident run."""

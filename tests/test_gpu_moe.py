@@ -136,6 +136,35 @@ def test_moe_layer_parity(sess, cfg4, M):
     _check_moe(y, dbg, cfg4, xn, f"moe_layer M={M}")
 
 
+@pytest.mark.parametrize("M", [1, 512])
+def test_moe_engine_checking_modes(sess, cfg4, M):
+    """The seeded 40 % host mask under poisoned slots and with serialised
+    copies gives the all-HBM output bit for bit."""
+    import torch
+    xn = synth.activations(configs.MOE_LAYER.seed, 400 + M, M, cfg4.H)
+    x = _dev(xn)
+    host_exp = configs.moe_host_experts()
+
+    def run(mode):
+        mask = list(sess.placement)
+        for j in range(3):
+            for e in range(cfg4.E):
+                mask[cfg4.tids[j][e]] = {"hbm": 0, "mask": int(host_exp[e])}[mode]
+        sess.set_placement(mask)
+        y = cfg4.layer(x)
+        sess.sync()
+        return y
+
+    ref = run("hbm")
+    try:
+        for poison, serialize in ((True, False), (False, True)):
+            sess.set_debug(poison=poison, serialize=serialize)
+            assert torch.equal(ref, run("mask")), (poison, serialize)
+    finally:
+        sess.set_debug()
+        run("hbm")
+
+
 @pytest.mark.parametrize("M", [1, 4, 512])
 def test_moe_placement_invariance(sess, cfg4, M):
     """HBM-resident experts, the seeded 40 % host mask and all experts on host
