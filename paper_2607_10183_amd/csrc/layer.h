@@ -6,7 +6,6 @@
 
 namespace atsi {
 
-constexpr int kLayerPhases = 4;  // q/k/v, o, gate/up, down
 enum LayerTensor { kQ = 0, kK, kV, kO, kGate, kUp, kDown, kLayerTensors };
 
 // barrier words the fused kernel keeps in device memory (zero-initialised

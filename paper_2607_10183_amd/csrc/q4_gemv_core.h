@@ -190,10 +190,5 @@ __device__ __forceinline__ float group_dot_m(const uint4& cw, const XGroup& g, c
   return fmaf(so, 0.0625f, se - g.corr);
 }
 
-// Store output (token m, row `row` of segment s) of a fused launch: written
-// to every query head of a grouped-query KV head, or with the residual added
-// (segment 0) and kept in fp32 when the launch asks for it, else rounded to
-// fp16 once.
-
 }  // namespace gemv
 }  // namespace atsi
