@@ -183,3 +183,21 @@ def test_moe_layer_placement_invariance(sess, stack_layer, M):
     sess.set_placement(mask)
     for o in outs[1:]:
         assert torch.equal(outs[0], o)
+
+
+def _sampled_layers():
+    """The first layer and two seeded layers of the 94 (the last one is the
+    stack_layer fixture above)."""
+    n = configs.MOE_STACK.n_layers
+    perm = [int(i) for i in synth.permutation(configs.MOE_STACK.seed, 97, n) if 0 < i < n - 1]
+    return [0, perm[0], perm[1]]
+
+
+@pytest.mark.parametrize("layer", _sampled_layers())
+def test_moe_stack_sampled_layers(sess, layer):
+    """Layers of the 235B-A22B-shaped stack besides the last: one decode
+    token and a 64-token prefill chunk, all experts HBM-resident."""
+    L = _Layer(sess, configs.MOE_STACK.seed, layer, STACK)
+    for M in (1, 64):
+        _run_and_check(sess, L, M, configs.MOE_STACK.seed, f"moe stack layer {layer} M={M}")
+
