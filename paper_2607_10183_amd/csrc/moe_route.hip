@@ -10,14 +10,18 @@
 //                   through LDS transposed so each lane reads 8 consecutive
 //                   inputs of one expert; fp32 partials per slice.
 //                   A launch of at most 16 tokens routes them in its last
-//                   workgroup to finish (release/acquire fences around a
-//                   counter that the last one resets), and computes the
-//                   tokens' RMS-norm factors there when asked.
+//                   workgroup to finish (partials stored and loaded at agent
+//                   scope around a counter that the last one resets), and computes the
+//                   tokens' RMS-norm factors there when asked, from sums of
+//                   squares each slice's workgroup leaves beside its
+//                   partials; that workgroup's 256 threads fetch every
+//                   partial in one round of loads.
 //   router_topk     one wavefront per token: sums the K-slice partials in a
 //                   fixed order, adds the bias, selects the top k by (logit
-//                   descending, expert id ascending) with k wave-wide argmax
-//                   rounds (DPP inside rows of 16 lanes, scalar reads across
-//                   rows), and writes the softmax over the selected logits.
+//                   descending, expert id ascending) with a pruned bitonic
+//                   network over 64-bit keys (DPP and permlane swaps, no
+//                   data-dependent branches), and writes the softmax over the
+//                   selected logits.
 //   bucket          one workgroup: per-expert counts (LDS integer atomics),
 //                   exclusive scan, then a stable scatter of pair ids k*t + j
 //                   ordered by (expert, token): each 64-token chunk builds a
@@ -35,6 +39,16 @@ typedef _Float16 half8_t __attribute__((ext_vector_type(8)));
 typedef float float4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kRT = 16;  // tokens per router tile
+
+// The partials of a fused launch cross workgroups on other XCDs: they are
+// stored and loaded at agent scope, so no XCD's L2 keeps or serves a stale
+// copy of them and no workgroup has to write back or invalidate its L2.
+__device__ __forceinline__ void st_agent(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float ld_agent(const float* p) {
+  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
 
 // 1 / sqrt(mean(x[t]^2) + eps) for one token, computed by one wavefront and
 // returned to every lane (the same arithmetic for every caller)
@@ -55,22 +69,152 @@ __device__ __forceinline__ float token_inv_rms(const __half* __restrict__ x, int
   return 1.f / sqrtf(q / (float)H + eps);
 }
 
-__device__ __forceinline__ void wave_best(float& v, int& i);
+// Top k of one token's logits by (value descending, expert id ascending), by
+// one wavefront holding experts lane and lane + 64 (-inf past E).  Each
+// candidate is a 64-bit key, larger is better: the logit's bits mapped to an
+// unsigned order in the high word (-0 taken as +0), the complement of the
+// expert id in the low word.  A pruned bitonic network finds the top C (C = 8
+// for k <= 8, else 16) without data-dependent branches: both registers sort
+// their C-lane chunks descending; the elementwise maximum of a descending and
+// an ascending chunk holds the top C of the two and is bitonic, so one merge
+// sorts it; pairing each lane's two keys, then chunks across mirror distances
+// 2C - 1 (up to 63) leaves the top C sorted in lanes 0 .. C - 1.  Lanes j < k
+// write the ids and the softmax over the selected logits (normaliser summed
+// in rank order).
+__device__ __forceinline__ uint64_t topk_key(float v, int id) {
+  unsigned u = __float_as_uint(v + 0.f);
+  u = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return ((uint64_t)u << 32) | (unsigned)~id;
+}
+
+template <int CTRL>
+__device__ __forceinline__ uint64_t dpp64(uint64_t x) {
+  const unsigned lo = (unsigned)__builtin_amdgcn_update_dpp(0, (int)(unsigned)x, CTRL, 0xF, 0xF, false);
+  const unsigned hi = (unsigned)__builtin_amdgcn_update_dpp(0, (int)(unsigned)(x >> 32), CTRL, 0xF, 0xF, false);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+// the key of lane l ^ 16 (W = 16) or l ^ 32 (W = 32): the swap returns the
+// lane's own word and its partner's, the partner's second in the lower half
+template <int W>
+__device__ __forceinline__ uint64_t swap64(uint64_t x, int lane) {
+  const unsigned lo = (unsigned)x, hi = (unsigned)(x >> 32);
+  unsigned plo, phi;
+  if constexpr (W == 16) {
+    const auto a = __builtin_amdgcn_permlane16_swap(lo, lo, false, false);
+    const auto b = __builtin_amdgcn_permlane16_swap(hi, hi, false, false);
+    plo = (lane & 16) ? a[0] : a[1];
+    phi = (lane & 16) ? b[0] : b[1];
+  } else {
+    const auto a = __builtin_amdgcn_permlane32_swap(lo, lo, false, false);
+    const auto b = __builtin_amdgcn_permlane32_swap(hi, hi, false, false);
+    plo = (lane & 32) ? a[0] : a[1];
+    phi = (lane & 32) ? b[0] : b[1];
+  }
+  return ((uint64_t)phi << 32) | plo;
+}
+
+// the key of lane l ^ J
+template <int J>
+__device__ __forceinline__ uint64_t lane_xor(uint64_t x, int lane) {
+  if constexpr (J == 1) return dpp64<0xB1>(x);                  // quad_perm 1,0,3,2
+  else if constexpr (J == 2) return dpp64<0x4E>(x);             // quad_perm 2,3,0,1
+  else if constexpr (J == 3) return dpp64<0x1B>(x);             // quad_perm 3,2,1,0
+  else if constexpr (J == 7) return dpp64<0x141>(x);            // row_half_mirror
+  else if constexpr (J == 15) return dpp64<0x140>(x);           // row_mirror
+  else if constexpr (J == 4) return dpp64<0x1B>(dpp64<0x141>(x));  // (l ^ 7) ^ 3
+  else if constexpr (J == 8) return dpp64<0x141>(dpp64<0x140>(x));  // (l ^ 15) ^ 7
+  else if constexpr (J == 31) return swap64<16>(dpp64<0x140>(x), lane);
+  else if constexpr (J == 63) return swap64<32>(swap64<16>(dpp64<0x140>(x), lane), lane);
+  else static_assert(J == 1, "no cross-lane path for this distance");
+}
+
+// compare-exchange with lane l ^ J: the lane keeps the larger key iff
+// (l & D) == 0
+template <int J, int D>
+__device__ __forceinline__ uint64_t cx(uint64_t x, int lane) {
+  const uint64_t p = lane_xor<J>(x, lane);
+  return ((p > x) == ((lane & D) == 0)) ? p : x;
+}
+
+template <int J>
+__device__ __forceinline__ uint64_t kmax(uint64_t x, int lane) {
+  const uint64_t p = lane_xor<J>(x, lane);
+  return p > x ? p : x;
+}
+
+// sorts a bitonic C-lane chunk descending (half-cleaners C/2 .. 1)
+template <int C>
+__device__ __forceinline__ uint64_t bitonic_merge(uint64_t x, int lane) {
+  if constexpr (C >= 16) x = cx<8, 8>(x, lane);
+  if constexpr (C >= 8) x = cx<4, 4>(x, lane);
+  x = cx<2, 2>(x, lane);
+  return cx<1, 1>(x, lane);
+}
+
+// sorts each C-lane chunk descending: stage s compares mirror partners
+// (l ^ (s - 1)), then merges the halves
+template <int C>
+__device__ __forceinline__ uint64_t chunk_sort(uint64_t x, int lane) {
+  x = cx<1, 1>(x, lane);
+  x = cx<3, 2>(x, lane);
+  x = cx<1, 1>(x, lane);
+  x = cx<7, 4>(x, lane);
+  x = bitonic_merge<4>(x, lane);
+  if constexpr (C == 16) {
+    x = cx<15, 8>(x, lane);
+    x = bitonic_merge<8>(x, lane);
+  }
+  return x;
+}
+
+template <int C>
+__device__ __forceinline__ uint64_t topk_network(uint64_t a, uint64_t b, int lane) {
+  a = chunk_sort<C>(a, lane);
+  b = chunk_sort<C>(b, lane);
+  // lane's two chunks: a descending against b mirrored (ascending)
+  const uint64_t bm = lane_xor<C - 1>(b, lane);
+  a = a > bm ? a : bm;
+  a = bitonic_merge<C>(a, lane);
+  if constexpr (C == 8) {
+    a = bitonic_merge<8>(kmax<15>(a, lane), lane);
+  }
+  a = bitonic_merge<C>(kmax<31>(a, lane), lane);
+  return bitonic_merge<C>(kmax<63>(a, lane), lane);
+}
+
+__device__ __forceinline__ void select_topk(float v0, float v1, int E, int k, int t, int32_t* __restrict__ idx,
+                                            float* __restrict__ p) {
+  const int lane = threadIdx.x & 63;
+  const uint64_t a = lane < E ? topk_key(v0, lane) : 0ull;
+  const uint64_t b = lane + 64 < E ? topk_key(v1, lane + 64) : 0ull;
+  const uint64_t key = k <= 8 ? topk_network<8>(a, b, lane) : topk_network<16>(a, b, lane);
+  const unsigned hi = (unsigned)(key >> 32);
+  const float v = __uint_as_float((hi & 0x80000000u) ? (hi & 0x7fffffffu) : ~hi);
+  const int id = (int)~(unsigned)key;
+  const float v_top = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(v)));  // lane 0: rank 0
+  const float ev = lane < k ? expf(v - v_top) : 0.f;
+  float den = 0.f;
+  for (int j = 0; j < k; ++j) den += __int_as_float(__builtin_amdgcn_readlane(__float_as_int(ev), j));
+  if (lane < k) {
+    idx[(size_t)t * k + lane] = id;
+    p[(size_t)t * k + lane] = ev / den;
+  }
+}
 
 // Routing of token t by one wavefront (E <= 128, two candidates per lane):
 // the K-slice partial logits summed in slice order, times the norm factor rs
-// when norm is set, plus the bias; the top k by (logit descending, expert id
-// ascending) in k argmax rounds; the softmax over the selected logits.
+// when norm is set, plus the bias; then the top k and their softmax.
 __device__ __forceinline__ void route_token(const float* __restrict__ part, int n_split, int M, int t, bool norm,
                                             float rs, const float* __restrict__ bias, int E, int k,
                                             int32_t* __restrict__ idx, float* __restrict__ p,
                                             float* __restrict__ logits_out) {
   const int lane = threadIdx.x & 63;
   float v[2] = {0.f, 0.f};
-  int id[2] = {lane, lane + 64};
+  const int id[2] = {lane, lane + 64};
   // every global load is issued before the first wait: the bias, then the
-  // K-slice partials, 16 slices of both experts per round (the partials come
-  // from other XCDs' writes, a memory round trip each), added in slice order
+  // K-slice partials, 16 slices of both experts per round, added in slice
+  // order
   float bv[2];
 #pragma unroll
   for (int h = 0; h < 2; ++h) bv[h] = (bias && id[h] < E) ? bias[id[h]] : 0.f;
@@ -100,28 +244,7 @@ __device__ __forceinline__ void route_token(const float* __restrict__ part, int 
       v[h] = -INFINITY;
     }
   }
-  float sel_v[16];
-  int sel_i[16];
-  for (int j = 0; j < k; ++j) {
-    // best of this lane: larger value, then lower id
-    float bv2 = v[0];
-    int bi = id[0];
-    if (v[1] > bv2 || (v[1] == bv2 && id[1] < bi)) { bv2 = v[1]; bi = id[1]; }
-    if (bi >= E) bi = 0x7fffffff;
-    wave_best(bv2, bi);
-    sel_v[j] = bv2;
-    sel_i[j] = bi;
-    if (bi == id[0]) v[0] = -INFINITY, id[0] = 0x7fffffff;
-    if (bi == id[1]) v[1] = -INFINITY, id[1] = 0x7fffffff;
-  }
-  if (lane == 0) {
-    float den = 0.f;
-    for (int j = 0; j < k; ++j) den += expf(sel_v[j] - sel_v[0]);
-    for (int j = 0; j < k; ++j) {
-      idx[(size_t)t * k + j] = sel_i[j];
-      p[(size_t)t * k + j] = expf(sel_v[j] - sel_v[0]) / den;
-    }
-  }
+  select_topk(v[0], v[1], E, k, t, idx, p);
 }
 
 // Outputs of the routing of one launch: the last workgroup of a single-tile
@@ -138,52 +261,152 @@ struct RouteOut {
   float* logits;
 };
 
+constexpr int kChunk = 32;  // partials a thread of the routing workgroup fetches per round
+
+// Routing of a whole tile (at most 16 tokens) by the 256 threads of the last
+// workgroup.  Every input is fetched in one round of loads where it fits:
+// g threads per (token, expert) each sum a contiguous run of K slices in
+// slice order and the g runs are added in order; the squares of the inputs
+// (per slice, written by the slices' workgroups) are summed the same way
+// for the norm factor.  Then one wavefront per token selects the top k.
+// pbuf holds at least 2048 floats.
+__device__ void route_tile(const float* __restrict__ part, int n_split, int M, int t0, int H, int E, const RouteOut& ro,
+                           float* pbuf) {
+  __shared__ float lg[kRT * 128];
+  __shared__ float sqb[256];
+  __shared__ float rsq[kRT];
+  const int tid = threadIdx.x;
+  const int Mt = min(kRT, M - t0);
+  const int items = Mt * E;
+  int g = 1;
+  while (2 * g * items <= 256 && 2 * g <= n_split) g *= 2;
+  const int chunk = n_split / g;
+  const float* sq = part + (size_t)n_split * M * E;  // per-slice sums of squares, [slice][token]
+  int g2 = 1;
+  while (n_split / g2 > kChunk) g2 *= 2;
+  const int chunk2 = n_split / g2;
+  const bool make = ro.inv_r_out != nullptr;
+  const bool norm = make || ro.inv_r != nullptr;
+
+  // issued first, consumed last: this thread's squares run, its first
+  // item's bias and the given norm factors
+  // loads are unpredicated (indexes clamped into the run, the extra values
+  // dropped when summing) with 32-bit offsets from the launch's base, so
+  // they issue back to back
+  float qv[kChunk];
+  const bool has_q = make && tid < Mt * g2;
+  if (has_q) {
+    const int t = t0 + tid / g2, s0 = (tid % g2) * chunk2;
+#pragma unroll
+    for (int j = 0; j < kChunk; ++j) qv[j] = ld_agent(sq + (unsigned)(min(s0 + j, s0 + chunk2 - 1) * M + t));
+  }
+  const float b0 = (ro.bias && tid < items) ? ro.bias[tid % E] : 0.f;
+  if (!make && ro.inv_r && tid < Mt) rsq[tid] = ro.inv_r[t0 + tid];
+
+  const unsigned stride = (unsigned)(M * E);
+  for (int w = tid; w < items * g; w += 256) {
+    const int item = w / g, sub = w % g;
+    const unsigned base = (unsigned)((t0 + item / E) * E + item % E);
+    const int end = (sub + 1) * chunk;
+    float s = 0.f;
+    for (int c0 = sub * chunk; c0 < end; c0 += kChunk) {
+      float pv[kChunk];
+#pragma unroll
+      for (int j = 0; j < kChunk; ++j) pv[j] = ld_agent(part + (base + (unsigned)min(c0 + j, end - 1) * stride));
+#pragma unroll
+      for (int j = 0; j < kChunk; ++j)
+        if (c0 + j < end) s += pv[j];
+    }
+    pbuf[w] = s;
+  }
+  if (has_q) {
+    float q = 0.f;
+#pragma unroll
+    for (int j = 0; j < kChunk; ++j)
+      if (j < chunk2) q += qv[j];
+    sqb[tid] = q;
+  }
+  __syncthreads();
+  if (make && tid < Mt) {
+    float q = 0.f;
+    for (int j = 0; j < g2; ++j) q += sqb[tid * g2 + j];
+    const float rs = 1.f / sqrtf(q / (float)H + ro.eps);
+    rsq[tid] = rs;
+    ro.inv_r_out[t0 + tid] = rs;
+  }
+  __syncthreads();
+  for (int item = tid; item < items; item += 256) {
+    const int tt = item / E, e = item % E;
+    float s = 0.f;
+    for (int j = 0; j < g; ++j) s += pbuf[item * g + j];
+    if (norm) s *= rsq[tt];  // RMS-normalised input: scale the product once
+    if (ro.bias) s += item == tid ? b0 : ro.bias[e];
+    lg[item] = s;
+    if (ro.logits) ro.logits[(size_t)(t0 + tt) * E + e] = s;
+  }
+  __syncthreads();
+  const int lane = tid & 63, wave = tid >> 6;
+  for (int tt = wave; tt < Mt; tt += 4) {
+    const float v0 = lane < E ? lg[tt * E + lane] : -INFINITY;
+    const float v1 = lane + 64 < E ? lg[tt * E + lane + 64] : -INFINITY;
+    select_topk(v0, v1, E, ro.k, t0 + tt, ro.idx, ro.p);
+  }
+}
+
 // grid: (ceil(M/16), n_split); block 256 = 4 waves x 32 experts (E <= 128).
-// Requires E % 16 == 0, E <= 128, ks % 32 == 0.
+// Requires E % 16 == 0, E <= 128, ks % 32 == 0.  The global loads of the
+// next 32-input step are issued before the MFMAs of the current one.
 template <bool FUSED>
 __global__ __launch_bounds__(256) void router_partial_kernel(const __half* __restrict__ x, const __half* __restrict__ wr,
                                                              int M, int H, int E, int ks, float* __restrict__ part,
                                                              RouteOut ro) {
   __shared__ __attribute__((aligned(16))) _Float16 Bt[128 * (32 + 8)];  // [expert][k] of one 32-k step
   const int t0 = blockIdx.x * kRT;
-  const int k_begin = blockIdx.y * ks;
+  const int k_begin = blockIdx.y * ks, k_end = k_begin + ks;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int tr = lane & 15, kq = (lane >> 4) * 8;
+  const int kk = threadIdx.x >> 4, e8 = (threadIdx.x & 15) * 8;
+  const bool wl = e8 < E;
+  const int t = t0 + tr;
+  // squares of the slice's inputs, for the norm factors of the fused routing
+  const bool sq = FUSED && ro.inv_r_out && wave == 0;
   float4_t acc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
-  for (int k0 = k_begin; k0 < k_begin + ks; k0 += 32) {
-    // stage W_r[k0 .. k0+31][0 .. E) transposed: thread -> (k = tid / 16, 8 experts)
-    __syncthreads();
-    {
-      const int kk = threadIdx.x >> 4, e8 = (threadIdx.x & 15) * 8;
-      if (e8 < E) {
-        const uint4 v = *reinterpret_cast<const uint4*>(wr + (size_t)(k0 + kk) * E + e8);
-        const _Float16* hv = reinterpret_cast<const _Float16*>(&v);
+  float q = 0.f;
+  uint4 w0 = {0, 0, 0, 0}, w1 = {0, 0, 0, 0};
+  half8_t a = {0, 0, 0, 0, 0, 0, 0, 0};
+  auto fetch = [&](int k0) {
+    // W_r rows k0 + kk and k0 + kk + 16, 8 experts from e8; x[t][k0 + kq ..]
+    if (wl) {
+      w0 = *reinterpret_cast<const uint4*>(wr + (size_t)(k0 + kk) * E + e8);
+      w1 = *reinterpret_cast<const uint4*>(wr + (size_t)(k0 + kk + 16) * E + e8);
+    }
+    if (t < M) a = *reinterpret_cast<const half8_t*>(x + (size_t)t * H + k0 + kq);
+  };
+  fetch(k_begin);
+  for (int k0 = k_begin; k0 < k_end; k0 += 32) {
+    __syncthreads();  // the previous step's reads of Bt are done
+    if (wl) {
+      const _Float16* h0 = reinterpret_cast<const _Float16*>(&w0);
+      const _Float16* h1 = reinterpret_cast<const _Float16*>(&w1);
 #pragma unroll
-        for (int i = 0; i < 8; ++i) Bt[(e8 + i) * 40 + kk] = hv[i];
-      }
-      if (kk + 16 < 32) {
-        const int k2 = kk + 16;
-        if (e8 < E) {
-          const uint4 v = *reinterpret_cast<const uint4*>(wr + (size_t)(k0 + k2) * E + e8);
-          const _Float16* hv = reinterpret_cast<const _Float16*>(&v);
-#pragma unroll
-          for (int i = 0; i < 8; ++i) Bt[(e8 + i) * 40 + k2] = hv[i];
-        }
+      for (int i = 0; i < 8; ++i) {
+        Bt[(e8 + i) * 40 + kk] = h0[i];
+        Bt[(e8 + i) * 40 + kk + 16] = h1[i];
       }
     }
+    const half8_t ac = a;
+    if (k0 + 32 < k_end) fetch(k0 + 32);
     __syncthreads();
-    half8_t a;
-    const int t = t0 + tr;
-    if (t < M)
-      a = *reinterpret_cast<const half8_t*>(x + (size_t)t * H + k0 + kq);
-    else
-      a = half8_t{0, 0, 0, 0, 0, 0, 0, 0};
+    if (sq) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) q = fmaf((float)ac[i], (float)ac[i], q);
+    }
 #pragma unroll
     for (int nb = 0; nb < 2; ++nb) {
       const int e = wave * 32 + nb * 16 + tr;
       if (wave * 32 + nb * 16 < E) {
         const half8_t b = *reinterpret_cast<const half8_t*>(&Bt[e * 40 + kq]);
-        acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, acc[nb], 0, 0, 0);
+        acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ac, b, acc[nb], 0, 0, 0);
       }
     }
   }
@@ -194,69 +417,33 @@ __global__ __launch_bounds__(256) void router_partial_kernel(const __half* __res
     if (wave * 32 + nb * 16 >= E) continue;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int t = t0 + 4 * (lane >> 4) + i;
-      if (t < M) part[((size_t)blockIdx.y * M + t) * E + e] = acc[nb][i];
+      const int tt = t0 + 4 * (lane >> 4) + i;
+      if (tt < M) {
+        float* dst = part + ((size_t)blockIdx.y * M + tt) * E + e;
+        if constexpr (FUSED) st_agent(dst, acc[nb][i]); else *dst = acc[nb][i];
+      }
     }
   }
   if constexpr (FUSED) {
-    // The last workgroup to finish routes the tile: every workgroup makes its
-    // partials visible device-wide (release) before it counts itself; the last
-    // one acquires them all, resets the count for the next launch and routes.
+    if (sq) {
+      // lanes tr, tr + 16, tr + 32, tr + 48 hold token tr's four 8-input groups
+      q += __shfl_xor(q, 16, 64);
+      q += __shfl_xor(q, 32, 64);
+      if (lane < 16 && t < M) st_agent(part + (size_t)gridDim.y * M * E + (size_t)blockIdx.y * M + t, q);
+    }
+    // The last workgroup to finish routes the tile.  Every thread waits until
+    // its agent-scope stores are performed, then one thread counts the
+    // workgroup in; the last one resets the count for the next launch and
+    // reads the partials back at agent scope.
     __shared__ unsigned ticket;
-    __threadfence();
-    if (threadIdx.x == 0) ticket = atomicAdd(ro.counter, 1u);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (threadIdx.x == 0) ticket = __hip_atomic_fetch_add(ro.counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __syncthreads();
     if (ticket != gridDim.y - 1) return;
-    __threadfence();
-    if (threadIdx.x == 0) atomicExch(ro.counter, 0u);
-    for (int tt = wave; tt < kRT; tt += 4) {
-      const int t = t0 + tt;
-      if (t >= M) break;
-      float rs = 1.f;
-      if (ro.inv_r_out) {
-        rs = token_inv_rms(x, t, H, ro.eps);
-        if (lane == 0) ro.inv_r_out[t] = rs;
-      } else if (ro.inv_r) {
-        rs = ro.inv_r[t];
-      }
-      route_token(part, gridDim.y, M, t, ro.inv_r_out || ro.inv_r, rs, ro.bias, E, ro.k, ro.idx, ro.p, ro.logits);
-    }
+    if (threadIdx.x == 0) __hip_atomic_store(ro.counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    route_tile(part, gridDim.y, M, t0, H, E, ro, reinterpret_cast<float*>(Bt));
   }
-}
-
-// (value, id) of the best candidate of the wave, by (value descending, id
-// ascending), returned to every lane: DPP steps inside rows of 16 lanes
-// (swap neighbours, swap pairs, mirror within 8, mirror within 16), then the
-// four row results read back as scalars.  Needs all 64 lanes active.
-__device__ __forceinline__ void wave_best(float& v, int& i) {
-  auto better = [](float av, int ai, float bv, int bi) { return av > bv || (av == bv && ai < bi); };
-#define ATSI_BEST_STEP(CTRL)                                                                             \
-  {                                                                                                      \
-    const float ov = __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false)); \
-    const int oi = __builtin_amdgcn_update_dpp(0, i, CTRL, 0xF, 0xF, false);                             \
-    if (better(ov, oi, v, i)) {                                                                          \
-      v = ov;                                                                                            \
-      i = oi;                                                                                            \
-    }                                                                                                    \
-  }
-  ATSI_BEST_STEP(0xB1)   // quad_perm 1,0,3,2
-  ATSI_BEST_STEP(0x4E)   // quad_perm 2,3,0,1
-  ATSI_BEST_STEP(0x141)  // row_half_mirror
-  ATSI_BEST_STEP(0x140)  // row_mirror
-#undef ATSI_BEST_STEP
-  float bv = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
-  int bi = __builtin_amdgcn_readlane(i, 0);
-#pragma unroll
-  for (int r = 1; r < 4; ++r) {
-    const float ov = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16 * r));
-    const int oi = __builtin_amdgcn_readlane(i, 16 * r);
-    if (better(ov, oi, bv, bi)) {
-      bv = ov;
-      bi = oi;
-    }
-  }
-  v = bv;
-  i = bi;
 }
 
 // one wave per token; E <= 128 (two candidates per lane)
@@ -481,8 +668,9 @@ hipError_t launch_router(const __half* x, const float* inv_r, float* inv_r_out, 
   while (ks > 64 && (long)tiles * (H / ks) < 512 && (ks / 2) % 32 == 0 && H % (ks / 2) == 0) ks /= 2;
   const int n_split = H / ks;
   RouteOut ro{counter, inv_r, inv_r_out, eps, bias, k, idx, p, logits};
-  if (tiles == 1 && counter) {
-    // one tile: its last workgroup routes (no second launch)
+  if (tiles == 1 && counter && n_split <= 512) {
+    // one tile: its last workgroup routes (no second launch); at most 16
+    // threads per token then fetch its squares (32 slices each)
     hipLaunchKernelGGL(router_partial_kernel<true>, dim3(tiles, n_split), dim3(256), 0, s, x, wr, M, H, E, ks, part,
                        ro);
     return hipGetLastError();
@@ -503,8 +691,9 @@ hipError_t launch_router(const __half* x, const float* inv_r, float* inv_r_out, 
 }
 
 size_t router_partial_floats(int M, int H, int E) {
-  // upper bound of n_split * M * E (n_split <= H / 64)
-  return (size_t)(H / 64 + 1) * M * E;
+  // upper bound of n_split * M * (E + 1): the logit partials, then the
+  // squares partials of the fused routing (n_split <= H / 64 + 1)
+  return (size_t)(H / 64 + 1) * M * (E + 1);
 }
 
 hipError_t launch_bucket(const int32_t* idx, int M, int k, int E, const uint8_t* resident, int bm_rows,

@@ -122,6 +122,18 @@ def test_moe_small_parity(sess, M):
     _check_moe(y, dbg, st, xn, f"moe small M={M}")
 
 
+@pytest.mark.parametrize("k,M", [(12, 1), (16, 1), (9, 16), (16, 33), (9, 20)])
+def test_moe_wide_topk_parity(sess, k, M):
+    """More than 8 experts per token: the selection network keeps 16 per
+    chunk; one token routes in the router's last workgroup, 20 and 33 in a
+    second launch."""
+    st = _Setup(sess, 83, E=64, H=256, I=96, k=k)
+    xn = synth.activations(83, 100 + M, M, st.H)
+    y, dbg = st.layer(_dev(xn), debug=True)
+    sess.sync()
+    _check_moe(y, dbg, st, xn, f"moe k={k} M={M}")
+
+
 @pytest.fixture(scope="module")
 def cfg4(sess):
     shp = configs.MOE_LAYER.moe

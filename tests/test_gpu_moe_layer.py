@@ -126,7 +126,7 @@ def _run_and_check(sess, L, M, seed, name):
         assert np.array_equal(dbg[key].cpu().numpy(), refv), f"{name}: {key}"
 
 
-@pytest.mark.parametrize("M", [1, 5, 64])
+@pytest.mark.parametrize("M", [1, 5, 16, 64])
 def test_moe_decoder_layer_small(sess, M):
     L = _Layer(sess, 91, 0, SMALL)
     _run_and_check(sess, L, M, 91, f"moe layer small M={M}")
