@@ -221,7 +221,8 @@ __global__ __launch_bounds__(gemv::kBlock) void expert_gemv(MoeArgs a, int tile_
 // stores it, and sums p_j * out_j in slot order in fp32 plus the residual, as
 // the combine does.  y may alias res: each element is read, then written, by
 // one thread.
-constexpr int kDcRows = 4;
+constexpr int kDcRows = 8;
+constexpr int kDcRW = 4;  // rows per wave task
 constexpr int kDcThreads = 1024;
 
 template <int RW>
@@ -348,7 +349,7 @@ hipError_t launch_expert_down(const MoeArgs& a, int tile_bound, bool gemv, hipSt
 hipError_t launch_expert_down_combine(const MoeArgs& a, int M, const float* p, const __half* res, __half* y,
                                       hipStream_t s) {
   if (!a.pair_expert || M < 1 || a.k > kMaxTopK) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((expert_down_combine<kGemvRW>), dim3((a.H + kDcRows - 1) / kDcRows, M), dim3(kDcThreads), 0, s, a,
+  hipLaunchKernelGGL((expert_down_combine<kDcRW>), dim3((a.H + kDcRows - 1) / kDcRows, M), dim3(kDcThreads), 0, s, a,
                      p, res, y);
   return hipGetLastError();
 }

@@ -202,3 +202,28 @@ def test_moe_placement_invariance(sess, cfg4, M):
     sess.set_placement(mask)
     for o in outs[1:]:
         assert torch.equal(outs[0], o)
+
+
+def test_moe_decode_back_to_back(sess, cfg4):
+    """Distinct single tokens queued back to back (decode with every expert
+    resident) give bit for bit what each gives with a wait after it: the
+    scratch that consecutive calls reuse is not raced."""
+    import torch
+    mask = list(sess.placement)
+    for j in range(3):
+        for e in range(cfg4.E):
+            mask[cfg4.tids[j][e]] = 0
+    sess.set_placement(mask)
+    n = 24
+    x = _dev(synth.activations(configs.MOE_LAYER.seed, 500, n, cfg4.H))
+    ref = torch.empty((n, cfg4.H), dtype=torch.float16, device="cuda")
+    for t in range(n):
+        cfg4.layer(x[t:t + 1], ref[t:t + 1])
+        sess.sync()
+    for rep in range(2):
+        y = torch.zeros_like(ref)
+        for t in range(n):
+            cfg4.layer(x[t:t + 1], y[t:t + 1])
+        sess.sync()
+        bad = (y != ref).any(dim=1).nonzero().flatten().tolist()
+        assert not bad, f"pass {rep}: tokens {bad} differ from their one-at-a-time results"
