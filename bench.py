@@ -429,12 +429,22 @@ def bench_moe(sess, timer, args):
     st_dec, h2d_dec = h2d_timed(sess, timer, lambda: [layer(xd[t:t + 1], yd[t:t + 1]) for t in range(32)], 1)
     st_dec, h2d_dec = st_dec / 32, h2d_dec / 32
     st_pf, h2d_pf = h2d_timed(sess, timer, lambda: layer(xp, yp), 3)
+    # the same placement with the routed host experts read in place (zero-copy):
+    # nothing is copied, the PCIe bytes are those the copy path moves
+    sess.set_zero_copy(True)
+    timer.run(lambda: [layer(xd[t:t + 1], yd[t:t + 1]) for t in range(32)], 1)
+    zc_dec = timer.run(lambda: [layer(xd[t:t + 1], yd[t:t + 1]) for t in range(32)], 1) / 32
+    gz = graph_of(sess.cs, decode_all)
+    timer.run(gz.replay, 1)
+    zc_graph = timer.run(gz.replay, 3) / n_tok
+    sess.set_zero_copy(False)
     for j in range(3):
         for e in range(E):
             mask[tids[j][e]] = 0
     sess.set_placement(mask)
     log(f"moe streamed decode {st_dec * 1e3:.3f} ms/token ({h2d_dec / 1e6:.1f} MB copied), prefill "
-        f"{st_pf * 1e3:.2f} ms ({h2d_pf / 1e6:.1f} MB copied, {h2d_pf / st_pf / 1e9:.1f} GB/s PCIe)")
+        f"{st_pf * 1e3:.2f} ms ({h2d_pf / 1e6:.1f} MB copied, {h2d_pf / st_pf / 1e9:.1f} GB/s PCIe); "
+        f"zero-copy decode {zc_dec * 1e3:.3f} ms/token ({zc_graph * 1e3:.3f} graph-replayed)")
     return {"workload": "moe_layer: 128 experts of SwiGLU 768 over hidden 2048, top-8, capped Zipf(1.1) loads",
             "decode_us_per_token": round(dec_s * 1e6, 2),
             "decode_routed_GBps": round(routed_bytes / dec_s / 1e9, 1),
@@ -446,7 +456,10 @@ def bench_moe(sess, timer, args):
                                     "decode_pcie_GBps": round(h2d_dec / st_dec / 1e9, 2),
                                     "prefill_ms": round(st_pf * 1e3, 3),
                                     "prefill_h2d_bytes": int(h2d_pf),
-                                    "prefill_pcie_GBps": round(h2d_pf / st_pf / 1e9, 2)}}
+                                    "prefill_pcie_GBps": round(h2d_pf / st_pf / 1e9, 2),
+                                    "zero_copy_decode_ms_per_token": round(zc_dec * 1e3, 4),
+                                    "zero_copy_decode_ms_per_token_graph": round(zc_graph * 1e3, 4),
+                                    "zero_copy_decode_pcie_GBps": round(h2d_dec / zc_graph / 1e9, 2)}}
 
 
 def bench_dense_stack(timer_cls, h2d_gbs, steps=6):
@@ -584,6 +597,10 @@ def bench_moe_stack(timer_cls):
             pl[tids[j][e]] = int(host_exp[e])
     sess.set_placement(pl)
     d_st, p_st, d_h2d, p_h2d = measure()
+    sess.set_zero_copy(True)
+    timer.run(dec, 1)
+    d_zc = (timer.run(dec, 2) - t_cd) / 32
+    sess.set_zero_copy(False)
     # experts the prefill actually routes to, and how many of those are on host
     dbg = L(hp0.clone(), debug=True)
     sess.sync()
@@ -594,7 +611,8 @@ def bench_moe_stack(timer_cls):
     pf_flops = 2.0 * wl.prefill_m * (attn_bytes * 16 / 9 + k * expert_bytes * 16 / 9)  # 2 M K N per weight
     log(f"moe stack layer: decode {d_hbm * 1e3:.3f} ms ({d_st * 1e3:.3f} streamed), prefill {p_hbm * 1e3:.2f} ms "
         f"({p_st * 1e3:.2f} streamed, {n_host_act} of {n_act} active experts on host, {p_h2d / 1e6:.0f} MB "
-        f"copied -> {p_h2d / p_st / 1e9:.1f} GB/s PCIe); decode copies {d_h2d / 1e6:.1f} MB/token; "
+        f"copied -> {p_h2d / p_st / 1e9:.1f} GB/s PCIe); decode copies {d_h2d / 1e6:.1f} MB/token "
+        f"({d_zc * 1e3:.3f} ms with zero-copy reads); "
         f"x94: {94 * d_hbm * 1e3:.1f} ms/token all-HBM")
     return {"workload": "moe_stack: one 235B-A22B-shaped layer (attention 64/4 heads of 128, hidden 4096, "
                         "128 experts of SwiGLU 1536, top-8, capped-Zipf routing); 94-layer figures are 94 x the layer",
@@ -610,7 +628,10 @@ def bench_moe_stack(timer_cls):
                                        "prefill_h2d_bytes_per_layer": int(p_h2d),
                                        "prefill_pcie_GBps": round(p_h2d / p_st / 1e9, 2),
                                        "decode_tokens_per_s_94_layers": round(1.0 / (94 * d_st), 2),
-                                       "prefill_tokens_per_s_94_layers": round(wl.prefill_m / (94 * p_st), 1)}}
+                                       "prefill_tokens_per_s_94_layers": round(wl.prefill_m / (94 * p_st), 1),
+                                       "zero_copy_decode_ms_per_layer": round(d_zc * 1e3, 4),
+                                       "zero_copy_decode_pcie_GBps": round(d_h2d / d_zc / 1e9, 2),
+                                       "zero_copy_decode_tokens_per_s_94_layers": round(1.0 / (94 * d_zc), 2)}}
 
 
 def bench_placement_solver(reps: int = 3):

@@ -258,6 +258,20 @@ atsi_status atsi_moe_bucket(atsi_ctx* ctx, const int32_t* idx, int64_t M, int32_
 #define ATSI_DEBUG_SERIALIZE 2u
 atsi_status atsi_set_debug(atsi_ctx* ctx, uint32_t flags);
 
+/* Zero-copy expert reads (the paper's copy-kernel path: with host memory
+ * mapped and pinned, GPU threads read it directly; background section and
+ * Sec. 4.2).  enable = 1: in atsi_moe_ffn and atsi_moe_decoder_layer calls of
+ * at most 4 tokens, the expert kernels read the routed host-resident experts
+ * in place from their pinned host copies over PCIe, through the same launches
+ * as HBM-resident experts: no copy into a temporary slot and no wait on the
+ * host for the routing counts.  Larger calls, and every other tensor, keep
+ * the copy path.  Outputs are bit-identical to the copy path's.  Requires
+ * every registered host copy, and every one registered while enabled, to be
+ * mapped pinned host memory (e.g. hipHostMalloc'd): ATSI_E_INVALID names the
+ * first that is not.  enable = 0 restores the copy path.  Reads done in place
+ * are not counted in atsi_stats. */
+atsi_status atsi_set_zero_copy(atsi_ctx* ctx, int32_t enable);
+
 /* Wait for both streams; returns the first latched asynchronous error. */
 atsi_status atsi_sync(atsi_ctx* ctx);
 

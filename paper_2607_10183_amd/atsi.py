@@ -90,6 +90,7 @@ _SIGS = {
     "atsi_get_stats": ([_P, ctypes.POINTER(atsi_stats), ctypes.c_int32], ctypes.c_int),
     "atsi_debug_unpack": ([_P, ctypes.c_int32, _P], ctypes.c_int),
     "atsi_set_debug": ([_P, ctypes.c_uint32], ctypes.c_int),
+    "atsi_set_zero_copy": ([_P, ctypes.c_int32], ctypes.c_int),
     "atsi_solve_placement": ([ctypes.POINTER(atsi_placement_problem), _P, ctypes.POINTER(ctypes.c_double)],
                              ctypes.c_int),
 }
@@ -225,3 +226,7 @@ def atsi_solve_placement(size_bytes, r, c, budget_bytes: float, granularity_byte
 
 def atsi_set_debug(ctx: int, flags: int) -> None:
     _check(ctx, lib().atsi_set_debug(ctx, int(flags)))
+
+
+def atsi_set_zero_copy(ctx: int, enable: bool) -> None:
+    _check(ctx, lib().atsi_set_zero_copy(ctx, 1 if enable else 0))

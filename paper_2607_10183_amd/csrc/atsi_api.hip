@@ -45,6 +45,9 @@ struct Tensor {
   const uint16_t* dscales = nullptr;
   const uint8_t* hcodes = nullptr;
   const uint16_t* hscales = nullptr;
+  // device addresses of the host copy (mapped pinned memory), or null
+  const uint8_t* zcodes = nullptr;
+  const uint16_t* zscales = nullptr;
   bool on_host = false;
   size_t codes_bytes() const { return (size_t)(K / 2) * (size_t)N; }
   size_t scales_bytes() const { return (size_t)(K / kGroup) * (size_t)N * 2; }
@@ -116,6 +119,7 @@ struct atsi_ctx {
   bool layer_launched = false;    // a fused layer ran since the last atsi_sync
   bool fused_layer = false;       // batch-1 decode layers take the single persistent launch
   uint32_t debug = 0;             // ATSI_DEBUG_* flags (atsi_set_debug)
+  bool zero_copy = false;         // decode experts on host are read in place (atsi_set_zero_copy)
   int32_t* pinned = nullptr;    // pinned host copy of per-expert counts
   hipEvent_t counts_ev = nullptr;
   atsi_stats stats{};           // transfer counters (atsi_get_stats)
@@ -559,7 +563,11 @@ atsi_status get_table(atsi_ctx* c, const atsi_moe* m, atsi_ctx::MoeTable** out) 
         QView* qv[3] = {&w[i].gate, &w[i].up, &w[i].down};
         bool resident = true;
         for (int j = 0; j < 3; ++j) {
-          *qv[j] = QView{ts[j]->dcodes, ts[j]->dscales, (int)ts[j]->K, (int)ts[j]->N};
+          // a host tensor's entry is its mapped host copy in zero-copy mode
+          // (read in place by the pair-indexed decode launches only)
+          const bool z = ts[j]->on_host && c->zero_copy;
+          *qv[j] = QView{z ? ts[j]->zcodes : ts[j]->dcodes, z ? ts[j]->zscales : ts[j]->dscales, (int)ts[j]->K,
+                         (int)ts[j]->N};
           resident = resident && !ts[j]->on_host;
         }
         r[i] = resident ? 1 : 0;
@@ -744,15 +752,16 @@ atsi_status run_moe(atsi_ctx* c, const atsi_moe* m, const __half* x, int Mi, __h
                                (const __half*)m->router_w_f16, m->router_bias, Mi, H, E, k, part, idx, p,
                                dbg ? dbg->logits : nullptr, c->route_count, c->cs);
   if (e != hipSuccess) return hip_fail(c, e, "router launch");
-  // decode with every expert resident: the expert launches index routed pairs
-  // directly, and the bucketing only runs when the caller asks for its output
-  const bool by_pair = gemv && tb->n_streamed == 0;
+  // decode with every expert resident, or with host experts read in place
+  // (zero-copy): the expert launches index routed pairs directly, and the
+  // bucketing only runs when the caller asks for its output
+  const bool by_pair = gemv && (tb->n_streamed == 0 || c->zero_copy);
   const bool want_buckets = dbg && (dbg->counts || dbg->offsets || dbg->perm || dbg->inv_perm);
   if (!by_pair || want_buckets) {
     e = launch_bucket(idx, Mi, k, E, resident, bm, counts, offsets, perm, inv, order, tiles, ntiles, c->cs);
     if (e != hipSuccess) return hip_fail(c, e, "bucket launch");
   }
-  if (tb->n_streamed > 0) {
+  if (tb->n_streamed > 0 && !by_pair) {
     HIP_TRY(c, hipMemcpyAsync(c->pinned, counts, E * sizeof(int32_t), hipMemcpyDeviceToHost, c->cs));
     HIP_TRY(c, hipEventRecord(c->counts_ev, c->cs));
   }
@@ -949,6 +958,18 @@ atsi_status atsi_tensor_register(atsi_ctx* c, const atsi_qtensor* t, atsi_tid* o
   r.on_host = !has_dev;
   atsi_status st = enter(c);
   if (st) return st;
+  if (has_host) {
+    void *zc = nullptr, *zs = nullptr;
+    if (hipHostGetDevicePointer(&zc, const_cast<uint8_t*>(t->host_codes), 0) == hipSuccess &&
+        hipHostGetDevicePointer(&zs, const_cast<uint16_t*>(t->host_scales), 0) == hipSuccess) {
+      r.zcodes = static_cast<const uint8_t*>(zc);
+      r.zscales = static_cast<const uint16_t*>(zs);
+    } else {
+      (void)hipGetLastError();  // not mapped pinned memory: no zero-copy reads of this tensor
+    }
+    if (c->zero_copy && !r.zcodes)
+      return fail(c, ATSI_E_INVALID, "zero-copy mode: the host copy is not mapped pinned memory");
+  }
   c->tensors.push_back(r);
   *out = (atsi_tid)(c->tensors.size() - 1);
   if (r.on_host && r.slot_need() > c->slot_bytes) {
@@ -1237,6 +1258,24 @@ atsi_status atsi_set_debug(atsi_ctx* c, uint32_t flags) {
   if (flags & ~(uint32_t)(ATSI_DEBUG_POISON | ATSI_DEBUG_SERIALIZE))
     return fail(c, ATSI_E_INVALID, "unknown debug flags 0x%x", flags);
   c->debug = flags;
+  return ATSI_OK;
+}
+
+atsi_status atsi_set_zero_copy(atsi_ctx* c, int32_t enable) {
+  if (!c) return ATSI_E_INVALID;
+  if (enable != 0 && enable != 1) return fail(c, ATSI_E_INVALID, "enable=%d is not 0 or 1", enable);
+  if (enable)
+    for (size_t i = 0; i < c->tensors.size(); ++i) {
+      const Tensor& t = c->tensors[i];
+      if (t.hcodes && !t.zcodes)
+        return fail(c, ATSI_E_INVALID, "the host copy of tensor %zu is not mapped pinned memory", i);
+    }
+  atsi_status st = enter(c);
+  if (st) return st;
+  if (c->zero_copy != (enable != 0)) {
+    c->zero_copy = enable != 0;
+    ++c->placement_version;  // expert tables are rewritten with the new entries
+  }
   return ATSI_OK;
 }
 

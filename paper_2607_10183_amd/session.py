@@ -105,6 +105,10 @@ class Session:
         """Checking modes of the streaming engine (atsi_set_debug)."""
         atsi.atsi_set_debug(self.ctx, (atsi.DEBUG_POISON if poison else 0) | (atsi.DEBUG_SERIALIZE if serialize else 0))
 
+    def set_zero_copy(self, enable: bool = True) -> None:
+        """Decode MoE calls read host-resident experts in place (atsi_set_zero_copy)."""
+        atsi.atsi_set_zero_copy(self.ctx, enable)
+
     def set_placement(self, host_mask) -> None:
         mask = [int(v) for v in host_mask]
         atsi.atsi_set_placement(self.ctx, mask)

@@ -204,6 +204,67 @@ def test_moe_placement_invariance(sess, cfg4, M):
         assert torch.equal(outs[0], o)
 
 
+@pytest.mark.parametrize("M", [1, 4, 512])
+def test_moe_zero_copy(sess, cfg4, M):
+    """Zero-copy mode with the seeded 40 % host mask: calls of at most 4
+    tokens read the routed host experts in place (nothing is copied), larger
+    ones keep the copy path; both give the all-HBM bits."""
+    import torch
+    x = _dev(synth.activations(configs.MOE_LAYER.seed, 600 + M, M, cfg4.H))
+    host_exp = configs.moe_host_experts()
+
+    def run(mode):
+        mask = list(sess.placement)
+        for j in range(3):
+            for e in range(cfg4.E):
+                mask[cfg4.tids[j][e]] = {"hbm": 0, "mask": int(host_exp[e])}[mode]
+        sess.set_placement(mask)
+        y = cfg4.layer(x)
+        sess.sync()
+        return y
+
+    ref = run("hbm")
+    copied = run("mask")
+    try:
+        sess.set_zero_copy(True)
+        sess.stats(reset=True)
+        outs = [run("mask") for _ in range(2)]
+        st = sess.stats(reset=True)
+    finally:
+        sess.set_zero_copy(False)
+        run("hbm")
+    for y in outs:
+        assert torch.equal(ref, y)
+    assert torch.equal(ref, copied)
+    if M <= 4:
+        assert st["h2d_bytes"] == 0 and st["host_reads"] == 0
+    else:
+        assert st["h2d_bytes"] > 0
+
+
+def test_zero_copy_needs_mapped_host_copies():
+    """Zero-copy mode is refused while a host copy is ordinary (unmapped) host
+    memory, and for a tensor with such a copy registered while it is on."""
+    import torch
+    from paper_2607_10183_amd import atsi
+    from paper_2607_10183_amd.session import Session
+    codes, scales = synth.int4_codes(84, 1, 64, 256), synth.group_scales(84, 1, 64, 256)
+    dev_c = torch.from_numpy(codes).cuda()
+    dev_s = torch.from_numpy(np.ascontiguousarray(scales).view(np.int16)).cuda()
+    plain_c = torch.from_numpy(codes.copy())
+    plain_s = torch.from_numpy(np.ascontiguousarray(scales).view(np.int16).copy())
+    with Session(workspace_bytes=64 << 20, n_slots=2) as s2:
+        s2.register(codes, scales, host=True)  # pinned host copy: fine
+        s2.set_zero_copy(True)
+        with pytest.raises(atsi.AtsiError, match="ATSI_E_INVALID"):
+            s2.register_device(dev_c, dev_s, plain_c, plain_s)
+        s2.set_zero_copy(False)
+        s2.register_device(dev_c, dev_s, plain_c, plain_s)
+        with pytest.raises(atsi.AtsiError, match="ATSI_E_INVALID"):
+            s2.set_zero_copy(True)
+        assert atsi.lib().atsi_set_zero_copy(s2.ctx, 2) == 1
+
+
 def test_moe_decode_back_to_back(sess, cfg4):
     """Distinct single tokens queued back to back (decode with every expert
     resident) give bit for bit what each gives with a wait after it: the

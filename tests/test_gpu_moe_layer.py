@@ -185,6 +185,39 @@ def test_moe_layer_placement_invariance(sess, stack_layer, M):
         assert torch.equal(outs[0], o)
 
 
+@pytest.mark.parametrize("M", [1, 4])
+def test_moe_layer_zero_copy(sess, stack_layer, M):
+    """Decode of the 235B-shaped layer with the seeded 40 % of experts on host,
+    read in place (zero-copy): the all-HBM bits, and nothing copied."""
+    import torch
+    L = stack_layer
+    h0 = _dev(synth.activations(configs.MOE_STACK.seed, 800 + M, M, L.s["hidden"]))
+    host_exp = configs.moe_host_experts(frac=0.40, seed=configs.MOE_STACK.seed, layer=configs.MOE_STACK.n_layers - 1)
+
+    def run(host):
+        mask = list(sess.placement)
+        for j in range(3):
+            for e in range(L.s["n_experts"]):
+                mask[L.tids[j][e]] = int(host_exp[e]) if host else 0
+        sess.set_placement(mask)
+        h = h0.clone()
+        L.layer(h)
+        sess.sync()
+        return h
+
+    ref = run(False)
+    try:
+        sess.set_zero_copy(True)
+        sess.stats(reset=True)
+        got = run(True)
+        st = sess.stats(reset=True)
+    finally:
+        sess.set_zero_copy(False)
+        run(False)
+    assert torch.equal(ref, got)
+    assert st["h2d_bytes"] == 0
+
+
 def _sampled_layers():
     """The first layer and two seeded layers of the 94 (the last one is the
     stack_layer fixture above)."""
