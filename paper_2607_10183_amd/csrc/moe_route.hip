@@ -50,23 +50,39 @@ __device__ __forceinline__ float ld_agent(const float* p) {
   return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// 1 / sqrt(mean(x[t]^2) + eps) for one token, computed by one wavefront and
-// returned to every lane (the same arithmetic for every caller)
-__device__ __forceinline__ float token_inv_rms(const __half* __restrict__ x, int t, int H, float eps) {
+// sum of squares of row t over the wave: each lane adds its 8-input chunks
+// lane, lane + 64, ... in order; up to 8 chunks per lane are loaded in one
+// round (chunks past H count as zeros, which leaves the sums unchanged)
+__device__ __forceinline__ float row_sumsq(const __half* __restrict__ x, int t, int H) {
   const int lane = threadIdx.x & 63;
+  const __half* xr = x + (size_t)t * H;
   float q = 0.f;
-  for (int c = lane * 8; c < H; c += 64 * 8) {
-    const uint4 v = *reinterpret_cast<const uint4*>(x + (size_t)t * H + c);
-    const __half* hv = reinterpret_cast<const __half*>(&v);
+  for (int c0 = 0; c0 < H; c0 += 64 * 8 * 8) {
+    uint4 v[8];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const float f = __half2float(hv[i]);
-      q = fmaf(f, f, q);
+    for (int j = 0; j < 8; ++j) {
+      const int c = c0 + (j * 64 + lane) * 8;
+      v[j] = c < H ? *reinterpret_cast<const uint4*>(xr + c) : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const __half* hv = reinterpret_cast<const __half*>(&v[j]);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const float f = __half2float(hv[i]);
+        q = fmaf(f, f, q);
+      }
     }
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) q += __shfl_xor(q, o, 64);
-  return 1.f / sqrtf(q / (float)H + eps);
+  return q;
+}
+
+// 1 / sqrt(mean(x[t]^2) + eps) for one token, computed by one wavefront and
+// returned to every lane (the same arithmetic for every caller)
+__device__ __forceinline__ float token_inv_rms(const __half* __restrict__ x, int t, int H, float eps) {
+  return 1.f / sqrtf(row_sumsq(x, t, H) / (float)H + eps);
 }
 
 // Top k of one token's logits by (value descending, expert id ascending), by
@@ -592,19 +608,7 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const __half* x, int M, in
   const int lane = threadIdx.x & 63;
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= M) return;
-  float q = 0.f;
-  for (int c = lane * 8; c < H; c += 64 * 8) {
-    const uint4 v = *reinterpret_cast<const uint4*>(x + (size_t)t * H + c);
-    const __half* hv = reinterpret_cast<const __half*>(&v);
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const float f = __half2float(hv[i]);
-      q = fmaf(f, f, q);
-    }
-  }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) q += __shfl_xor(q, o, 64);
-  const float inv = 1.f / sqrtf(q / (float)H + eps);
+  const float inv = token_inv_rms(x, t, H, eps);
   for (int c = lane * 8; c < H; c += 64 * 8) {
     const uint4 v = *reinterpret_cast<const uint4*>(x + (size_t)t * H + c);
     const __half* hv = reinterpret_cast<const __half*>(&v);
@@ -616,36 +620,68 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const __half* x, int M, in
   }
 }
 
-// the same from an fp32 input (a residual sum that may exceed the fp16 range)
+// the same from an fp32 input (a residual sum that may exceed the fp16 range):
+// one workgroup per token, every thread loading kNv float4 of the row in one
+// round (held in registers when the row fits, else re-read), the sum of
+// squares reduced per wave and then over the four waves in a fixed order
+constexpr int kNv = 4;
 __global__ __launch_bounds__(256) void rmsnorm32_kernel(const float* __restrict__ x, int M, int H, float eps,
                                                         __half* __restrict__ y) {
-  const int lane = threadIdx.x & 63;
-  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (t >= M) return;
+  __shared__ float wsum[4];
+  const int t = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const float* xr = x + (size_t)t * H;
+  __half* yr = y + (size_t)t * H;
+  constexpr int kRound = 256 * 4 * kNv;  // inputs per round
+  float4 v[kNv];
   float q = 0.f;
-  for (int c = lane * 4; c < H; c += 64 * 4) {
-    const float4 v = *reinterpret_cast<const float4*>(x + (size_t)t * H + c);
-    q = fmaf(v.x, v.x, q);
-    q = fmaf(v.y, v.y, q);
-    q = fmaf(v.z, v.z, q);
-    q = fmaf(v.w, v.w, q);
+  for (int c0 = 0; c0 < H; c0 += kRound) {
+#pragma unroll
+    for (int j = 0; j < kNv; ++j) {
+      const int c = c0 + (j * 256 + tid) * 4;
+      v[j] = c < H ? *reinterpret_cast<const float4*>(xr + c) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int j = 0; j < kNv; ++j) {
+      q = fmaf(v[j].x, v[j].x, q);
+      q = fmaf(v[j].y, v[j].y, q);
+      q = fmaf(v[j].z, v[j].z, q);
+      q = fmaf(v[j].w, v[j].w, q);
+    }
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) q += __shfl_xor(q, o, 64);
-  const float inv = 1.f / sqrtf(q / (float)H + eps);
-  for (int c = lane * 4; c < H; c += 64 * 4) {
-    const float4 v = *reinterpret_cast<const float4*>(x + (size_t)t * H + c);
-    y[(size_t)t * H + c] = __float2half_rn(v.x * inv);
-    y[(size_t)t * H + c + 1] = __float2half_rn(v.y * inv);
-    y[(size_t)t * H + c + 2] = __float2half_rn(v.z * inv);
-    y[(size_t)t * H + c + 3] = __float2half_rn(v.w * inv);
+  if (lane == 0) wsum[wave] = q;
+  __syncthreads();
+  const float inv = 1.f / sqrtf((((wsum[0] + wsum[1]) + wsum[2]) + wsum[3]) / (float)H + eps);
+  for (int c0 = 0; c0 < H; c0 += kRound) {
+    if (H > kRound) {  // the row did not fit in one round: read this round again
+#pragma unroll
+      for (int j = 0; j < kNv; ++j) {
+        const int c = c0 + (j * 256 + tid) * 4;
+        if (c < H) v[j] = *reinterpret_cast<const float4*>(xr + c);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < kNv; ++j) {
+      const int c = c0 + (j * 256 + tid) * 4;
+      if (c < H) {
+        __half2 lo = __halves2half2(__float2half_rn(v[j].x * inv), __float2half_rn(v[j].y * inv));
+        __half2 hi = __halves2half2(__float2half_rn(v[j].z * inv), __float2half_rn(v[j].w * inv));
+        uint2 o;
+        o.x = *reinterpret_cast<const unsigned*>(&lo);
+        o.y = *reinterpret_cast<const unsigned*>(&hi);
+        *reinterpret_cast<uint2*>(yr + c) = o;
+      }
+    }
   }
 }
 
 }  // namespace
 
 hipError_t launch_rmsnorm32(const float* x, int M, int H, float eps, __half* y, hipStream_t s) {
-  hipLaunchKernelGGL(rmsnorm32_kernel, dim3((M + 3) / 4), dim3(256), 0, s, x, M, H, eps, y);
+  if (H % 4 != 0) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(rmsnorm32_kernel, dim3(M), dim3(256), 0, s, x, M, H, eps, y);
   return hipGetLastError();
 }
 
