@@ -500,7 +500,8 @@ __device__ int scan128(const int* v, int* out, int E) {
 
 // Single workgroup of 1024 threads.  Up to 16 chunks of 64 tokens are ranked
 // per pass; masks live in LDS.
-__global__ __launch_bounds__(1024) void bucket_kernel(const int32_t* __restrict__ idx, int M, int k, int E,
+constexpr int kBucketThreads = 1024;
+__global__ __launch_bounds__(kBucketThreads) void bucket_kernel(const int32_t* __restrict__ idx, int M, int k, int E,
                                                       const uint8_t* __restrict__ resident, int bm_rows,
                                                       int32_t* __restrict__ counts, int32_t* __restrict__ offsets,
                                                       int32_t* __restrict__ perm, int32_t* __restrict__ inv_perm,
@@ -517,9 +518,17 @@ __global__ __launch_bounds__(1024) void bucket_kernel(const int32_t* __restrict_
   const int pairs = M * k;
   for (int e = tid; e < E; e += blockDim.x) cnt[e] = 0;
   __syncthreads();
-  for (int i = tid; i < pairs; i += blockDim.x) {
-    const int e = idx[i];
-    if ((unsigned)e < (unsigned)E) atomicAdd(&cnt[e], 1);
+  // every load of a round of 8 is issued before its first count
+  for (int i0 = 0; i0 < pairs; i0 += 8 * kBucketThreads) {
+    int ev[8];
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+      const int i = i0 + r * kBucketThreads + tid;
+      ev[r] = i < pairs ? idx[i] : -1;
+    }
+#pragma unroll
+    for (int r = 0; r < 8; ++r)
+      if ((unsigned)ev[r] < (unsigned)E) atomicAdd(&cnt[ev[r]], 1);
   }
   __syncthreads();
   const int total = scan128(cnt, base, E);
@@ -534,11 +543,12 @@ __global__ __launch_bounds__(1024) void bucket_kernel(const int32_t* __restrict_
     for (int i = tid; i < 16 * E; i += blockDim.x) mask[i / E][i % E] = 0ull;
     __syncthreads();
     const int t = (c0 + wave) * 64 + lane;
-    if (t < M)
-      for (int j = 0; j < k; ++j) {
-        const int e = idx[(size_t)t * k + j];
-        if ((unsigned)e < (unsigned)E) atomicOr(&mask[wave][e], 1ull << lane);
-      }
+    int et[kMaxTopK];  // the token's k experts, loaded once (-1 past k or M)
+#pragma unroll
+    for (int j = 0; j < kMaxTopK; ++j) et[j] = (t < M && j < k) ? idx[(size_t)t * k + j] : -1;
+#pragma unroll
+    for (int j = 0; j < kMaxTopK; ++j)
+      if ((unsigned)et[j] < (unsigned)E) atomicOr(&mask[wave][et[j]], 1ull << lane);
     __syncthreads();
     for (int e = tid; e < E; e += blockDim.x) {
       int run = base[e];
@@ -551,8 +561,9 @@ __global__ __launch_bounds__(1024) void bucket_kernel(const int32_t* __restrict_
     __syncthreads();
     if (t < M) {
       const unsigned long long below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-      for (int j = 0; j < k; ++j) {
-        const int e = idx[(size_t)t * k + j];
+#pragma unroll
+      for (int j = 0; j < kMaxTopK; ++j) {
+        const int e = et[j];
         if ((unsigned)e >= (unsigned)E) continue;
         const int pos = pre[wave][e] + __popcll(mask[wave][e] & below);
         perm[pos] = t * k + j;
@@ -735,7 +746,8 @@ size_t router_partial_floats(int M, int H, int E) {
 hipError_t launch_bucket(const int32_t* idx, int M, int k, int E, const uint8_t* resident, int bm_rows,
                          int32_t* counts, int32_t* offsets, int32_t* perm, int32_t* inv_perm, int32_t* order,
                          int32_t* tiles, int32_t* n_tiles, hipStream_t s) {
-  hipLaunchKernelGGL(bucket_kernel, dim3(1), dim3(1024), 0, s, idx, M, k, E, resident, bm_rows, counts, offsets, perm,
+  if (k < 1 || k > kMaxTopK) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(bucket_kernel, dim3(1), dim3(kBucketThreads), 0, s, idx, M, k, E, resident, bm_rows, counts, offsets, perm,
                      inv_perm, order, tiles, n_tiles);
   return hipGetLastError();
 }
