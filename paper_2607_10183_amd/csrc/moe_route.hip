@@ -11,10 +11,10 @@
 //                   inputs of one expert; fp32 partials per slice.
 //                   A launch of at most 16 tokens routes them in its last
 //                   workgroup to finish (partials stored and loaded at agent
-//                   scope around a counter that the last one resets), and computes the
-//                   tokens' RMS-norm factors there when asked, from sums of
-//                   squares each slice's workgroup leaves beside its
-//                   partials; that workgroup's 256 threads fetch every
+//                   scope around a counter that the last one resets), and
+//                   computes the tokens' RMS-norm factors there when asked,
+//                   from sums of squares each slice's workgroup leaves beside
+//                   its partials; that workgroup's 256 threads fetch every
 //                   partial in one round of loads.
 //   router_topk     one wavefront per token: sums the K-slice partials in a
 //                   fixed order, adds the bias, selects the top k by (logit
@@ -110,8 +110,9 @@ __device__ __forceinline__ uint64_t dpp64(uint64_t x) {
   return ((uint64_t)hi << 32) | lo;
 }
 
-// the key of lane l ^ 16 (W = 16) or l ^ 32 (W = 32): the swap returns the
-// lane's own word and its partner's, the partner's second in the lower half
+// the key of lane l ^ 16 (W = 16) or l ^ 32 (W = 32): the swap of a register
+// with itself returns the lane's own word and its partner's; the partner's is
+// the second result where bit W of l is clear, else the first
 template <int W>
 __device__ __forceinline__ uint64_t swap64(uint64_t x, int lane) {
   const unsigned lo = (unsigned)x, hi = (unsigned)(x >> 32);
