@@ -112,7 +112,7 @@ __device__ __forceinline__ uint64_t dpp64(uint64_t x) {
 
 // the key of lane l ^ 16 (W = 16) or l ^ 32 (W = 32): the swap of a register
 // with itself returns the lane's own word and its partner's; the partner's is
-// the second result where bit W of l is clear, else the first
+// the second result where l & W is 0, else the first
 template <int W>
 __device__ __forceinline__ uint64_t swap64(uint64_t x, int lane) {
   const unsigned lo = (unsigned)x, hi = (unsigned)(x >> 32);
