@@ -47,7 +47,7 @@ class _Layer:
         Hq, Hkv = shape["n_heads"] * shape["head_dim"], shape["n_kv"] * shape["head_dim"]
         kn = {"q": (H, Hq), "k": (H, Hkv), "v": (H, Hkv), "o": (Hq, H)}
         self.W = {r: _qt(seed, configs.dense_uid(layer, r), kn[r][1], kn[r][0]) for r in ("q", "k", "v", "o")}
-        self.attn = {r: sess.register(*self.W[r]) for r in ("q", "k", "v", "o")}
+        self.attn = {r: sess.register(*self.W[r], hbm=True, host=True) for r in ("q", "k", "v", "o")}
         self.experts = []
         tids = [[], [], []]
         for e in range(E):
@@ -185,10 +185,11 @@ def test_moe_layer_placement_invariance(sess, stack_layer, M):
         assert torch.equal(outs[0], o)
 
 
-@pytest.mark.parametrize("M", [1, 4])
-def test_moe_layer_zero_copy(sess, stack_layer, M):
+@pytest.mark.parametrize("M,host_attn", [(1, False), (4, False), (1, True)])
+def test_moe_layer_zero_copy(sess, stack_layer, M, host_attn):
     """Decode of the 235B-shaped layer with the seeded 40 % of experts on host,
-    read in place (zero-copy): the all-HBM bits, and nothing copied."""
+    read in place (zero-copy): the all-HBM bits, and nothing copied; with the
+    attention tensors on host too, those alone are copied."""
     import torch
     L = stack_layer
     h0 = _dev(synth.activations(configs.MOE_STACK.seed, 800 + M, M, L.s["hidden"]))
@@ -199,6 +200,8 @@ def test_moe_layer_zero_copy(sess, stack_layer, M):
         for j in range(3):
             for e in range(L.s["n_experts"]):
                 mask[L.tids[j][e]] = int(host_exp[e]) if host else 0
+        for t in L.attn.values():
+            mask[t] = int(host and host_attn)
         sess.set_placement(mask)
         h = h0.clone()
         L.layer(h)
@@ -215,7 +218,8 @@ def test_moe_layer_zero_copy(sess, stack_layer, M):
         sess.set_zero_copy(False)
         run(False)
     assert torch.equal(ref, got)
-    assert st["h2d_bytes"] == 0
+    attn_bytes = sum(configs.qbytes(*sess.shapes[t]) for t in L.attn.values())
+    assert st["h2d_bytes"] == (attn_bytes if host_attn else 0)
 
 
 def _sampled_layers():
