@@ -712,8 +712,11 @@ hipError_t launch_router(const __half* x, const float* inv_r, float* inv_r_out, 
                          float* logits, unsigned* counter, hipStream_t s) {
   // K slice per workgroup: enough workgroups to cover the chip, slices of >= 64
   const int tiles = (M + kRT - 1) / kRT;
+  // a single tile may go down to one 32-input step per workgroup while the
+  // routing workgroup still gathers each logit in one round (<= 64 slices)
+  const int min_ks = (tiles == 1 && H / 32 <= 64) ? 32 : 64;
   int ks = H;
-  while (ks > 64 && (long)tiles * (H / ks) < 512 && (ks / 2) % 32 == 0 && H % (ks / 2) == 0) ks /= 2;
+  while (ks > min_ks && (long)tiles * (H / ks) < 512 && (ks / 2) % 32 == 0 && H % (ks / 2) == 0) ks /= 2;
   const int n_split = H / ks;
   RouteOut ro{counter, inv_r, inv_r_out, eps, bias, k, idx, p, logits};
   if (tiles == 1 && counter && n_split <= 512) {
@@ -740,8 +743,8 @@ hipError_t launch_router(const __half* x, const float* inv_r, float* inv_r_out, 
 
 size_t router_partial_floats(int M, int H, int E) {
   // upper bound of n_split * M * (E + 1): the logit partials, then the
-  // squares partials of the fused routing (n_split <= H / 64 + 1)
-  return (size_t)(H / 64 + 1) * M * (E + 1);
+  // squares partials of the fused routing (n_split <= H / 32 + 1)
+  return (size_t)(H / 32 + 1) * M * (E + 1);
 }
 
 hipError_t launch_bucket(const int32_t* idx, int M, int k, int E, const uint8_t* resident, int bm_rows,
