@@ -61,7 +61,9 @@ typedef int32_t atsi_tid;
 
 /* Create a context on `device`.
  * compute_stream, transfer_stream: distinct, non-null hipStream_t handles
- *   (the paper's compute stream and transfer stream, Sec. 4.2.2).
+ *   (the paper's compute stream and transfer stream, Sec. 4.2.2).  The
+ *   library creates (and destroys in atsi_destroy) one more transfer stream
+ *   of its own; host-to-device copies alternate between the two.
  * workspace: device buffer of workspace_bytes, carved into n_slots temporary
  *   buffers for streamed tensors (Sec. 4.2.1, GPU temporary buffers) and a
  *   scratch region for intermediate activations; 256-byte aligned.

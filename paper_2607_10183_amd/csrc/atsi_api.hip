@@ -120,6 +120,8 @@ struct atsi_ctx {
   bool fused_layer = false;       // batch-1 decode layers take the single persistent launch
   uint32_t debug = 0;             // ATSI_DEBUG_* flags (atsi_set_debug)
   bool zero_copy = false;         // decode experts on host are read in place (atsi_set_zero_copy)
+  hipStream_t ts2 = nullptr;      // a second transfer stream, owned: copies alternate between ts and ts2
+  unsigned copy_turn = 0;
   int32_t* pinned = nullptr;    // pinned host copy of per-expert counts
   hipEvent_t counts_ev = nullptr;
   atsi_stats stats{};           // transfer counters (atsi_get_stats)
@@ -185,6 +187,7 @@ atsi_status layout_slots(atsi_ctx* c) {
                 c->ws_bytes, c->table_floor, c->n_slots, need);
   HIP_TRY(c, hipStreamSynchronize(c->cs));
   HIP_TRY(c, hipStreamSynchronize(c->ts));
+  HIP_TRY(c, hipStreamSynchronize(c->ts2));
   c->slot_bytes = need;
   for (int i = 0; i < c->n_slots; ++i) {
     Slot& s = c->slots[i];
@@ -235,42 +238,49 @@ __global__ void poison_kernel(uint4* __restrict__ p, size_t n16) {
     p[i] = make_uint4(~0u, ~0u, ~0u, ~0u);
 }
 
-// Before a copy into `bytes` at base (slot-aligned, whole slots): poison it,
-// and in serialise mode let every launch already enqueued finish first.
-atsi_status before_copy(atsi_ctx* c, char* base, size_t bytes) {
+// The stream of the next copy: copies alternate between the two transfer
+// streams, so two are in flight at once (a copy of a few MB spends a sizeable
+// part of its time outside the transfer itself).  A copy's poison fill, copy
+// and ready event all go on its stream.
+hipStream_t copy_stream(atsi_ctx* c) { return (c->copy_turn++ & 1u) ? c->ts2 : c->ts; }
+
+// Before a copy into `bytes` at base (slot-aligned, whole slots) on stream xs:
+// poison it, and in serialise mode let every launch already enqueued finish
+// first.
+atsi_status before_copy(atsi_ctx* c, char* base, size_t bytes, hipStream_t xs) {
   if (c->debug & ATSI_DEBUG_SERIALIZE) HIP_TRY(c, hipStreamSynchronize(c->cs));
   if (c->debug & ATSI_DEBUG_POISON) {
     const size_t n16 = bytes / 16;
     const unsigned blocks = (unsigned)std::min<size_t>((n16 + 255) / 256, 4096);
-    hipLaunchKernelGGL(poison_kernel, dim3(blocks), dim3(256), 0, c->ts, reinterpret_cast<uint4*>(base), n16);
+    hipLaunchKernelGGL(poison_kernel, dim3(blocks), dim3(256), 0, xs, reinterpret_cast<uint4*>(base), n16);
     HIP_TRY(c, hipGetLastError());
   }
   return ATSI_OK;
 }
 
 // In serialise mode a copy completes before the host goes on.
-atsi_status after_copy(atsi_ctx* c) {
-  if (c->debug & ATSI_DEBUG_SERIALIZE) HIP_TRY(c, hipStreamSynchronize(c->ts));
+atsi_status after_copy(atsi_ctx* c, hipStream_t xs) {
+  if (c->debug & ATSI_DEBUG_SERIALIZE) HIP_TRY(c, hipStreamSynchronize(xs));
   return ATSI_OK;
 }
 
 // Copy host tensor t into slot s on the transfer stream: one copy when its
 // host codes and scales are contiguous (small copies cost far more than their
 // bytes), else two.  The slot must be free.
-atsi_status copy_into(atsi_ctx* c, const Tensor& t, Slot& s) {
-  atsi_status st = before_copy(c, s.base, c->slot_bytes);
+atsi_status copy_into(atsi_ctx* c, const Tensor& t, Slot& s, hipStream_t xs) {
+  atsi_status st = before_copy(c, s.base, c->slot_bytes, xs);
   if (st) return st;
   if (t.host_contiguous()) {
-    HIP_TRY(c, hipMemcpyAsync(s.base, t.hcodes, t.bytes(), hipMemcpyHostToDevice, c->ts));
+    HIP_TRY(c, hipMemcpyAsync(s.base, t.hcodes, t.bytes(), hipMemcpyHostToDevice, xs));
     c->stats.h2d_copies += 1;
   } else {
-    HIP_TRY(c, hipMemcpyAsync(s.base, t.hcodes, t.codes_bytes(), hipMemcpyHostToDevice, c->ts));
-    HIP_TRY(c, hipMemcpyAsync(s.base + t.codes_bytes(), t.hscales, t.scales_bytes(), hipMemcpyHostToDevice, c->ts));
+    HIP_TRY(c, hipMemcpyAsync(s.base, t.hcodes, t.codes_bytes(), hipMemcpyHostToDevice, xs));
+    HIP_TRY(c, hipMemcpyAsync(s.base + t.codes_bytes(), t.hscales, t.scales_bytes(), hipMemcpyHostToDevice, xs));
     c->stats.h2d_copies += 2;
   }
   c->stats.h2d_bytes += t.bytes();
   c->stats.h2d_tensors += 1;
-  return after_copy(c);
+  return after_copy(c, xs);
 }
 
 void arm(atsi_ctx* c, Slot& s, atsi_tid tid, hipEvent_t ready) {
@@ -337,8 +347,9 @@ atsi_status issue_copy(atsi_ctx* c, atsi_tid tid, bool block, const std::vector<
   *slot_out = si;
   if (si < 0) return ATSI_OK;
   Slot& s = c->slots[si];
-  if ((st = copy_into(c, c->tensors[tid], s))) return st;
-  HIP_TRY(c, hipEventRecord(s.ready, c->ts));
+  hipStream_t xs = copy_stream(c);
+  if ((st = copy_into(c, c->tensors[tid], s, xs))) return st;
+  HIP_TRY(c, hipEventRecord(s.ready, xs));
   arm(c, s, tid, s.ready);
   return ATSI_OK;
 }
@@ -379,17 +390,18 @@ atsi_status issue_run(atsi_ctx* c, const atsi_tid* tids, int n, bool* issued) {
   }
   if (first < 0) return ATSI_OK;
   Slot& s0 = c->slots[first];
-  atsi_status st = before_copy(c, s0.base, (size_t)n * c->slot_bytes);
+  hipStream_t xs = copy_stream(c);
+  atsi_status st = before_copy(c, s0.base, (size_t)n * c->slot_bytes, xs);
   if (st) return st;
   HIP_TRY(c, hipMemcpyAsync(s0.base, c->tensors[tids[0]].hcodes, (size_t)n * c->slot_bytes, hipMemcpyHostToDevice,
-                            c->ts));
+                            xs));
   c->stats.h2d_copies += 1;
   c->stats.h2d_bytes += (uint64_t)n * c->slot_bytes;
   c->stats.h2d_tensors += (uint64_t)n;
-  HIP_TRY(c, hipEventRecord(s0.ready, c->ts));
+  HIP_TRY(c, hipEventRecord(s0.ready, xs));
   for (int i = 0; i < n; ++i) arm(c, c->slots[first + i], tids[i], s0.ready);
   *issued = true;
-  return after_copy(c);
+  return after_copy(c, xs);
 }
 
 // Keep the transfer stream ahead of compute without waiting: copy queued (or
@@ -892,7 +904,8 @@ atsi_status atsi_create(int device, void* compute_stream, void* transfer_stream,
   }
   c->slots.resize(n_slots);
   if (hipHostMalloc((void**)&c->pinned, kMaxExperts * sizeof(int32_t), hipHostMallocDefault) != hipSuccess ||
-      hipEventCreateWithFlags(&c->counts_ev, hipEventDisableTiming) != hipSuccess) {
+      hipEventCreateWithFlags(&c->counts_ev, hipEventDisableTiming) != hipSuccess ||
+      hipStreamCreateWithFlags(&c->ts2, hipStreamNonBlocking) != hipSuccess) {
     fail(nullptr, ATSI_E_HIP, "pinned staging or event allocation failed");
     atsi_destroy(c);
     return ATSI_E_HIP;
@@ -921,6 +934,10 @@ atsi_status atsi_destroy(atsi_ctx* c) {
   (void)hipSetDevice(c->device);
   if (c->cs) (void)hipStreamSynchronize(c->cs);
   if (c->ts) (void)hipStreamSynchronize(c->ts);
+  if (c->ts2) {
+    (void)hipStreamSynchronize(c->ts2);
+    (void)hipStreamDestroy(c->ts2);
+  }
   for (Slot& s : c->slots) {
     if (s.ready) (void)hipEventDestroy(s.ready);
     if (s.free) (void)hipEventDestroy(s.free);
@@ -1283,6 +1300,7 @@ atsi_status atsi_sync(atsi_ctx* c) {
   if (!c) return ATSI_E_INVALID;
   hipError_t e = hipSetDevice(c->device);
   if (e == hipSuccess) e = hipStreamSynchronize(c->ts);
+  if (e == hipSuccess) e = hipStreamSynchronize(c->ts2);
   if (e == hipSuccess) e = hipStreamSynchronize(c->cs);
   if (e != hipSuccess) hip_fail(c, e, "stream synchronize");
   if (e == hipSuccess && c->layer_launched) {
