@@ -191,19 +191,29 @@ def bucket(idx: np.ndarray, n_experts: int):
 
 # ----------------------------------------------------------------------------- MoE
 
-def moe_ffn(x: np.ndarray, w_r: np.ndarray, bias, experts, k: int, x_zeta=None):
+def moe_ffn(x: np.ndarray, w_r: np.ndarray, bias, experts, k: int, x_zeta=None, route=None):
     """Routed MoE layer y[t] = sum_j p[t, j] * FFN_{idx[t, j]}(x[t]).
 
     experts[e] = (gate, up, down), each a (codes, scales) pair; only experts
     some token selected are evaluated.  Returns (y, zeta, aux) with aux holding
     logits, idx, p and per-pair expert outputs out[T][k][H].
+
+    route = (idx, p) evaluates the layer on a given selection and given
+    weights instead of the top-k of the fp64 logits: when two experts' logits
+    are within rounding of each other, either selection is a correct routing,
+    and the output is then defined by the selection actually made.  The
+    weights' own error is then not part of zeta.
     """
     xd = np.asarray(x, dtype=np.float64)
     t, hdim = xd.shape
     logits, zl = router_logits(xd, w_r, bias)
     if x_zeta is not None:
         zl = zl + x_zeta @ np.abs(np.asarray(w_r, np.float16).astype(np.float64))
-    idx, p = topk_route(logits, k)
+    if route is None:
+        idx, p = topk_route(logits, k)
+    else:
+        idx = np.asarray(route[0], dtype=np.int32).reshape(t, k)
+        p = np.asarray(route[1], dtype=np.float64).reshape(t, k)
     out = np.zeros((t, k, hdim))
     zout = np.zeros((t, k, hdim))
     for e in np.unique(idx):
@@ -214,7 +224,7 @@ def moe_ffn(x: np.ndarray, w_r: np.ndarray, bias, experts, k: int, x_zeta=None):
         zout[tok, slot] = zye
     y = np.einsum("tj,tjh->th", p, out)
     zsel = np.take_along_axis(zl, idx.astype(np.int64), axis=1)
-    zp = softmax_weight_zeta(p, zsel)
+    zp = softmax_weight_zeta(p, zsel) if route is None else np.zeros_like(p)
     zeta = np.einsum("tj,tjh->th", p, zout) + np.einsum("tj,tjh->th", zp, np.abs(out)) + np.abs(y)
     return y, zeta, {"logits": logits, "logit_zeta": zl, "idx": idx, "p": p, "out": out}
 
