@@ -179,7 +179,7 @@ def main() -> int:
     # a dense layer does the same work whatever h holds, so timed calls keep
     # updating h in place (the MoE stack below restores its inputs instead)
     def layer(c, h, M):
-        atsi.atsi_decoder_layer(sess.ctx, descs[c], h.data_ptr(), M, 0, 0)
+        atsi.atsi_decoder_layer(sess.ctx, descs[c], h.data_ptr(), M, 0, 0, None)
 
     # ------------------------------------------------------------ decode, HBM-resident (value)
     decode_s = steps_timed = n_warm = per_replay = decode_gbs = 0

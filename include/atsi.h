@@ -22,9 +22,10 @@
  * must be finite in fp16 (|scale| * 8 <= 65504).
  *
  * Ownership: the caller owns every buffer (weights in HBM, pinned host
- * weights, activations, the workspace); the library keeps borrowed pointers
- * until atsi_destroy and itself allocates only host bookkeeping and HIP
- * events.  Device pointers must be 16-byte aligned.
+ * weights, activations, the workspace, the pinned counts buffer) and every
+ * stream; the library keeps borrowed pointers until atsi_destroy and itself
+ * allocates only host bookkeeping and HIP events.  Device pointers must be
+ * 16-byte aligned.
  *
  * Streams: calls only enqueue work on the compute stream (and copies on the
  * transfer stream); they return before the GPU finishes.  Inputs must stay
@@ -61,19 +62,28 @@ typedef int32_t atsi_tid;
 
 /* Create a context on `device`.
  * compute_stream, transfer_stream: distinct, non-null hipStream_t handles
- *   (the paper's compute stream and transfer stream, Sec. 4.2.2).  The
- *   library creates (and destroys in atsi_destroy) one more transfer stream
- *   of its own; host-to-device copies alternate between the two.
+ *   (the paper's compute stream and transfer stream, Sec. 4.2.2).
+ * transfer_stream2: a second transfer stream (distinct from both), or NULL.
+ *   With it, host-to-device copies alternate between the two transfer
+ *   streams so that two copies are in flight at once; without it every copy
+ *   goes on transfer_stream.
  * workspace: device buffer of workspace_bytes, carved into n_slots temporary
  *   buffers for streamed tensors (Sec. 4.2.1, GPU temporary buffers) and a
  *   scratch region for intermediate activations; 256-byte aligned.
+ * host_counts: pinned host memory (hipHostMalloc'd) of at least 128 int32,
+ *   where an MoE call with streamed experts reads back its per-expert token
+ *   counts (expert transfers wait for routing, Sec. 4.2.2); or NULL, and then
+ *   such calls fail with ATSI_E_STATE.
  * n_slots: number of temporary buffers, 2..64.
  * On a machine without a usable GPU this returns ATSI_E_HIP and *out = NULL. */
 atsi_status atsi_create(int device, void* compute_stream, void* transfer_stream,
-                        void* workspace, size_t workspace_bytes, int n_slots,
-                        atsi_ctx** out);
+                        void* transfer_stream2, void* workspace, size_t workspace_bytes,
+                        int32_t* host_counts, int n_slots, atsi_ctx** out);
 
-/* Drain both streams and free the context (events, host bookkeeping). */
+/* Drain the context's streams and free what the context itself holds: its
+ * slot and routing events (the events that order the compute and transfer
+ * streams, Sec. 4.2.2) and host bookkeeping.  Nothing the caller passed in is
+ * freed. */
 atsi_status atsi_destroy(atsi_ctx* ctx);
 
 /* Message of the last failure on ctx (or of the last failed atsi_create when
@@ -113,7 +123,9 @@ atsi_status atsi_set_placement(atsi_ctx* ctx, const uint8_t* host_mask, int32_t 
  * stream (Sec. 4.2.2).  1 <= M <= 65536. */
 atsi_status atsi_linear(atsi_ctx* ctx, atsi_tid w, const void* x_f16, int64_t M, void* y_f16);
 
-/* Dense SwiGLU feed-forward block (the FFN of a decoder layer):
+/* Dense SwiGLU feed-forward block (the FFN of a decoder layer of the dense
+ * models of Sec. 5.1; every one of its three weight tensors is a unit of
+ * placement, Sec. 4.3.2):
  *   y = (silu(x Wg) * (x Wu)) Wd,  silu(z) = z / (1 + exp(-z)),
  * gate and up are H x I tensors, down is I x H.  gate and up run in one
  * launch with the SwiGLU product fused; the intermediate (fp16, M x I) lives
@@ -122,7 +134,9 @@ atsi_status atsi_linear(atsi_ctx* ctx, atsi_tid w, const void* x_f16, int64_t M,
 atsi_status atsi_ffn_swiglu(atsi_ctx* ctx, atsi_tid gate, atsi_tid up, atsi_tid down,
                             const void* x_f16, int64_t M, void* y_f16);
 
-/* RMS normalisation with unit gain: y[t] = x[t] / sqrt(mean_k x[t][k]^2 + eps)
+/* RMS normalisation with unit gain (the normalisation between the layers of
+ * the pre-norm models of Sec. 5.1; the paper places only weight tensors, so
+ * this glue always runs on the GPU): y[t] = x[t] / sqrt(mean_k x[t][k]^2 + eps)
  * for fp16 x, y [M][H] (device, 16-byte aligned, H % 8 == 0), fp32
  * arithmetic and one fp16 rounding; y may alias x.  The glue between the
  * layers of a stack whose hidden state is renormalised after every layer. */
@@ -145,6 +159,22 @@ typedef struct {
   int32_t renorm_out;                    /* 1: h_out = rms(h + attn + FFN) (see below), 0: plain */
 } atsi_dense_layer;
 
+/* Optional device buffers that receive a layer's intermediate activations
+ * (each may be NULL; 16-byte aligned), so that every stage can be checked on
+ * its own input:
+ *   attn    fp16 [M][n_heads*head_dim]: attention output, the input of W_O;
+ *   h_attn  fp16 [M][H]: residual stream after the attention block;
+ *   act     fp16 [M][I]: SwiGLU activation, the input of W_down (dense layers);
+ *   sum32   fp32 [M][H]: h_attn + FFN before the output renormalisation
+ *           (dense layers with renorm_out = 1).
+ * Buffers not given stay in the workspace's scratch region. */
+typedef struct {
+  void* attn;
+  void* h_attn;
+  void* act;
+  float* sum32;
+} atsi_layer_debug;
+
 /* h <- h + attn(rms(h)) Wo;  h <- h + FFN(rms(h)), in place on h[M][H].
  * With layer->renorm_out = 1 the layer's output is renormalised as well,
  * h <- rms(h + FFN(rms(h))), for stacks whose hidden state is renormalised
@@ -163,10 +193,11 @@ typedef struct {
  * runs a batch-1 layer whose tensors are all HBM-resident, of the 8B shape
  * (hidden 4096, 32 x 128 query and 8 x 128 KV heads, SwiGLU 14336), on a
  * 256-CU device, as one persistent launch with grid barriers instead (the
- * same bits; slower than the four launches on MI355X).  A barrier of that
- * launch that does not complete is reported by atsi_sync. */
+ * same bits; slower than the four launches on MI355X), unless dbg is given.
+ * A barrier of that launch that does not complete is reported by atsi_sync.
+ * dbg may be NULL. */
 atsi_status atsi_decoder_layer(atsi_ctx* ctx, const atsi_dense_layer* layer, void* h_f16, int64_t M,
-                               void* q_out_f16, void* k_out_f16);
+                               void* q_out_f16, void* k_out_f16, const atsi_layer_debug* dbg);
 
 /* Execution order of tensors, repeated cyclically (the execution plan of a
  * round, Sec. 4.2.2): the engine copies upcoming host-resident tensors into
@@ -189,11 +220,15 @@ typedef struct {
   const atsi_tid* down;
 } atsi_moe;
 
-/* Optional device buffers that receive the routing (each may be NULL):
- * logits fp32 [M][E]; idx int32 [M][k] and p fp32 [M][k] (slot j in order of
- * logit descending, expert id ascending); counts int32 [E]; offsets int32
- * [E+1] (exclusive prefix sum of counts); perm int32 [M*k] (pair ids k*t + j
- * ordered by expert, then token); inv_perm int32 [M*k] (inverse of perm). */
+/* Optional device buffers that receive the routing and the expert
+ * activations (each may be NULL): logits fp32 [M][E]; idx int32 [M][k] and p
+ * fp32 [M][k] (slot j in order of logit descending, expert id ascending);
+ * counts int32 [E]; offsets int32 [E+1] (exclusive prefix sum of counts);
+ * perm int32 [M*k] (pair ids k*t + j ordered by expert, then token); inv_perm
+ * int32 [M*k] (inverse of perm); expert_h fp16 [M*k][I] (SwiGLU activation of
+ * pair k*t + j, the input of its expert's W_down) and expert_out fp16
+ * [M*k][H] (that expert's output, the term of the combine), both 16-byte
+ * aligned, rows in pair order. */
 typedef struct {
   float* logits;
   int32_t* idx;
@@ -202,6 +237,8 @@ typedef struct {
   int32_t* offsets;
   int32_t* perm;
   int32_t* inv_perm;
+  void* expert_h;
+  void* expert_out;
 } atsi_moe_debug;
 
 /* y[t] = sum_j p[t][j] * FFN_{idx[t][j]}(x[t]) for x, y fp16 [M][H].
@@ -213,9 +250,10 @@ typedef struct {
  * is streamed after routing resolves (Sec. 4.2.2: expert transfers wait for
  * routing and move only selected experts): the host reads the per-expert
  * counts back (one event wait), copies the active host experts heaviest
- * first into temporary buffers (n_slots >= 3 needed) while the HBM-resident
- * experts already run.  Expert outputs are kept in fp16 before the fp32
- * combine.  1 <= M <= 65536.  dbg may be NULL. */
+ * first into temporary buffers (n_slots >= 3 needed, and the host_counts
+ * buffer of atsi_create) while the HBM-resident experts already run.  Expert
+ * outputs are kept in fp16 before the fp32 combine.  1 <= M <= 65536.  dbg
+ * may be NULL. */
 atsi_status atsi_moe_ffn(atsi_ctx* ctx, const atsi_moe* moe, const void* x_f16, int64_t M, void* y_f16,
                          const atsi_moe_debug* dbg);
 
@@ -227,7 +265,8 @@ atsi_status atsi_moe_ffn(atsi_ctx* ctx, const atsi_moe* moe, const void* x_f16, 
  * its per-token factor scales the router logits (before the bias) and the
  * expert gate/up products in fp32, and the combine adds the residual, so h
  * (fp16 [M][hidden], device) is updated in place.  q_out / k_out as in
- * atsi_decoder_layer; dbg as in atsi_moe_ffn.  moe->hidden must equal the
+ * atsi_decoder_layer; dbg as in atsi_moe_ffn; ldbg (attn and h_attn; act and
+ * sum32 are not used) as in atsi_decoder_layer.  moe->hidden must equal the
  * attention hidden size. */
 typedef struct {
   int32_t n_heads, n_kv_heads, head_dim;
@@ -237,7 +276,8 @@ typedef struct {
 } atsi_moe_layer;
 
 atsi_status atsi_moe_decoder_layer(atsi_ctx* ctx, const atsi_moe_layer* layer, void* h_f16, int64_t M,
-                                   void* q_out_f16, void* k_out_f16, const atsi_moe_debug* dbg);
+                                   void* q_out_f16, void* k_out_f16, const atsi_moe_debug* dbg,
+                                   const atsi_layer_debug* ldbg);
 
 /* Token-to-expert bucketing alone (the same kernel atsi_moe_ffn uses), from
  * device idx int32 [M][k] with ids in [0, n_experts): counts [E], offsets
@@ -274,7 +314,9 @@ atsi_status atsi_set_debug(atsi_ctx* ctx, uint32_t flags);
  * are not counted in atsi_stats. */
 atsi_status atsi_set_zero_copy(atsi_ctx* ctx, int32_t enable);
 
-/* Wait for both streams; returns the first latched asynchronous error. */
+/* Wait for the compute and transfer streams (the host-side synchronisation
+ * with both streams of Sec. 4.2.2); returns the first latched asynchronous
+ * error. */
 atsi_status atsi_sync(atsi_ctx* ctx);
 
 /* Transfer counters of the engine (Sec. 4.2.2 moves host tensors into GPU

@@ -46,8 +46,16 @@ class atsi_moe(ctypes.Structure):
                 ("down", ctypes.POINTER(ctypes.c_int32))]
 
 
+MOE_DEBUG_FIELDS = ("logits", "idx", "p", "counts", "offsets", "perm", "inv_perm", "expert_h", "expert_out")
+LAYER_DEBUG_FIELDS = ("attn", "h_attn", "act", "sum32")
+
+
 class atsi_moe_debug(ctypes.Structure):
-    _fields_ = [(n, ctypes.c_void_p) for n in ("logits", "idx", "p", "counts", "offsets", "perm", "inv_perm")]
+    _fields_ = [(n, ctypes.c_void_p) for n in MOE_DEBUG_FIELDS]
+
+
+class atsi_layer_debug(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in LAYER_DEBUG_FIELDS]
 
 
 class atsi_moe_layer(ctypes.Structure):
@@ -69,7 +77,8 @@ class atsi_stats(ctypes.Structure):
 
 
 _SIGS = {
-    "atsi_create": ([ctypes.c_int, _P, _P, _P, ctypes.c_size_t, ctypes.c_int, ctypes.POINTER(_P)], ctypes.c_int),
+    "atsi_create": ([ctypes.c_int, _P, _P, _P, _P, ctypes.c_size_t, _P, ctypes.c_int, ctypes.POINTER(_P)],
+                    ctypes.c_int),
     "atsi_destroy": ([_P], ctypes.c_int),
     "atsi_last_error": ([_P], ctypes.c_char_p),
     "atsi_tensor_register": ([_P, ctypes.POINTER(atsi_qtensor), ctypes.POINTER(ctypes.c_int32)], ctypes.c_int),
@@ -78,11 +87,12 @@ _SIGS = {
     "atsi_ffn_swiglu": ([_P, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _P, ctypes.c_int64, _P], ctypes.c_int),
     "atsi_swiglu_gate_up": ([_P, ctypes.c_int32, ctypes.c_int32, _P, ctypes.c_int64, _P], ctypes.c_int),
     "atsi_rmsnorm": ([_P, _P, ctypes.c_int64, ctypes.c_int64, ctypes.c_float, _P], ctypes.c_int),
-    "atsi_decoder_layer": ([_P, ctypes.POINTER(atsi_dense_layer), _P, ctypes.c_int64, _P, _P], ctypes.c_int),
+    "atsi_decoder_layer": ([_P, ctypes.POINTER(atsi_dense_layer), _P, ctypes.c_int64, _P, _P,
+                            ctypes.POINTER(atsi_layer_debug)], ctypes.c_int),
     "atsi_moe_ffn": ([_P, ctypes.POINTER(atsi_moe), _P, ctypes.c_int64, _P, ctypes.POINTER(atsi_moe_debug)],
                      ctypes.c_int),
     "atsi_moe_decoder_layer": ([_P, ctypes.POINTER(atsi_moe_layer), _P, ctypes.c_int64, _P, _P,
-                                ctypes.POINTER(atsi_moe_debug)], ctypes.c_int),
+                                ctypes.POINTER(atsi_moe_debug), ctypes.POINTER(atsi_layer_debug)], ctypes.c_int),
     "atsi_moe_bucket": ([_P, _P, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, _P, _P, _P, _P], ctypes.c_int),
     "atsi_set_schedule": ([_P, _P, ctypes.c_int32], ctypes.c_int),
     "atsi_prefetch": ([_P, ctypes.c_int32], ctypes.c_int),
@@ -120,11 +130,11 @@ def _check(ctx, status: int) -> None:
         raise AtsiError(status, msg.decode() if msg else "")
 
 
-def atsi_create(device: int, compute_stream: int, transfer_stream: int, workspace: int,
-                workspace_bytes: int, n_slots: int) -> int:
+def atsi_create(device: int, compute_stream: int, transfer_stream: int, transfer_stream2: int, workspace: int,
+                workspace_bytes: int, host_counts: int, n_slots: int) -> int:
     out = _P()
-    _check(None, lib().atsi_create(device, compute_stream, transfer_stream, workspace, workspace_bytes,
-                                   n_slots, ctypes.byref(out)))
+    _check(None, lib().atsi_create(device, compute_stream, transfer_stream, transfer_stream2 or None, workspace,
+                                   workspace_bytes, host_counts or None, n_slots, ctypes.byref(out)))
     return out.value
 
 
@@ -166,8 +176,13 @@ def atsi_swiglu_gate_up(ctx: int, gate: int, up: int, x: int, M: int, h: int) ->
     _check(ctx, lib().atsi_swiglu_gate_up(ctx, gate, up, x, M, h))
 
 
-def atsi_decoder_layer(ctx: int, layer: atsi_dense_layer, h: int, M: int, q_out: int = 0, k_out: int = 0) -> None:
-    _check(ctx, lib().atsi_decoder_layer(ctx, ctypes.byref(layer), h, M, q_out or None, k_out or None))
+def _ref(d):
+    return ctypes.byref(d) if d is not None else None
+
+
+def atsi_decoder_layer(ctx: int, layer: atsi_dense_layer, h: int, M: int, q_out: int = 0, k_out: int = 0,
+                       dbg: atsi_layer_debug | None = None) -> None:
+    _check(ctx, lib().atsi_decoder_layer(ctx, ctypes.byref(layer), h, M, q_out or None, k_out or None, _ref(dbg)))
 
 
 def atsi_moe_ffn(ctx: int, moe: atsi_moe, x: int, M: int, y: int, dbg: atsi_moe_debug | None = None) -> None:
@@ -175,9 +190,9 @@ def atsi_moe_ffn(ctx: int, moe: atsi_moe, x: int, M: int, y: int, dbg: atsi_moe_
 
 
 def atsi_moe_decoder_layer(ctx: int, layer: atsi_moe_layer, h: int, M: int, q_out: int = 0, k_out: int = 0,
-                           dbg: atsi_moe_debug | None = None) -> None:
+                           dbg: atsi_moe_debug | None = None, ldbg: atsi_layer_debug | None = None) -> None:
     _check(ctx, lib().atsi_moe_decoder_layer(ctx, ctypes.byref(layer), h, M, q_out or None, k_out or None,
-                                              ctypes.byref(dbg) if dbg is not None else None))
+                                              _ref(dbg), _ref(ldbg)))
 
 
 def atsi_moe_bucket(ctx: int, idx: int, M: int, k: int, n_experts: int, counts: int, offsets: int, perm: int,

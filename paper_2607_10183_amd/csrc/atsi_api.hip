@@ -8,6 +8,8 @@
 // waited on by the compute stream before the consumer) and `free` (recorded
 // on the compute stream after the consumer; the host checks it before the
 // slot receives another copy), so a slot is never overwritten while read.
+// Every slot records its own ready event after each copy into it, so a wait
+// on a slot's event always names that slot's latest copy.
 // Copies start as soon as a free slot allows: an explicit prefetch, or the
 // schedule (the execution order of tensors) lets the transfer stream run
 // ahead of compute by up to n_slots - 1 tensors.  A call that needs a copy
@@ -65,10 +67,10 @@ struct Tensor {
 // by one launch share its free event.
 struct Slot {
   char* base = nullptr;
-  hipEvent_t ready = nullptr;     // owned
+  hipEvent_t ready = nullptr;     // owned; recorded after every copy into this slot
   hipEvent_t free = nullptr;      // owned
-  hipEvent_t ready_ev = nullptr;  // event of the copy that fills the slot
   hipEvent_t free_ev = nullptr;   // event of the launch that last read the slot
+  uint64_t ready_rec = 0;         // number of the copy that fills the slot (slots of one run share it)
   bool armed = false;
   bool pending = false;
   int tid = -1;         // tensor whose copy the slot holds or receives
@@ -120,9 +122,10 @@ struct atsi_ctx {
   bool fused_layer = false;       // batch-1 decode layers take the single persistent launch
   uint32_t debug = 0;             // ATSI_DEBUG_* flags (atsi_set_debug)
   bool zero_copy = false;         // decode experts on host are read in place (atsi_set_zero_copy)
-  hipStream_t ts2 = nullptr;      // a second transfer stream, owned: copies alternate between ts and ts2
+  hipStream_t ts2 = nullptr;      // the caller's second transfer stream, or null: copies alternate between ts and ts2
   unsigned copy_turn = 0;
-  int32_t* pinned = nullptr;    // pinned host copy of per-expert counts
+  uint64_t copy_rec = 0;          // copies issued (numbers the ready records)
+  int32_t* pinned = nullptr;    // caller's pinned host buffer for the per-expert counts, or null
   hipEvent_t counts_ev = nullptr;
   atsi_stats stats{};           // transfer counters (atsi_get_stats)
   std::string err;
@@ -187,7 +190,7 @@ atsi_status layout_slots(atsi_ctx* c) {
                 c->ws_bytes, c->table_floor, c->n_slots, need);
   HIP_TRY(c, hipStreamSynchronize(c->cs));
   HIP_TRY(c, hipStreamSynchronize(c->ts));
-  HIP_TRY(c, hipStreamSynchronize(c->ts2));
+  if (c->ts2) HIP_TRY(c, hipStreamSynchronize(c->ts2));
   c->slot_bytes = need;
   for (int i = 0; i < c->n_slots; ++i) {
     Slot& s = c->slots[i];
@@ -242,7 +245,7 @@ __global__ void poison_kernel(uint4* __restrict__ p, size_t n16) {
 // streams, so two are in flight at once (a copy of a few MB spends a sizeable
 // part of its time outside the transfer itself).  A copy's poison fill, copy
 // and ready event all go on its stream.
-hipStream_t copy_stream(atsi_ctx* c) { return (c->copy_turn++ & 1u) ? c->ts2 : c->ts; }
+hipStream_t copy_stream(atsi_ctx* c) { return (c->ts2 && (c->copy_turn++ & 1u)) ? c->ts2 : c->ts; }
 
 // Before a copy into `bytes` at base (slot-aligned, whole slots) on stream xs:
 // poison it, and in serialise mode let every launch already enqueued finish
@@ -283,10 +286,10 @@ atsi_status copy_into(atsi_ctx* c, const Tensor& t, Slot& s, hipStream_t xs) {
   return after_copy(c, xs);
 }
 
-void arm(atsi_ctx* c, Slot& s, atsi_tid tid, hipEvent_t ready) {
+void arm(atsi_ctx* c, Slot& s, atsi_tid tid, uint64_t rec) {
   s.tid = tid;
   s.armed = true;
-  s.ready_ev = ready;
+  s.ready_rec = rec;
   s.seq = ++c->clock;
   s.last = s.seq;
 }
@@ -331,6 +334,10 @@ atsi_status pick_slot(atsi_ctx* c, const std::vector<int>& held, bool block, int
     }
     if (best < 0)
       return fail(c, ATSI_E_STATE, "one launch needs more streamed tensors than the %d slots", c->n_slots);
+    // the dropped copy may still be in flight, possibly on the other transfer
+    // stream than the copy that will replace it: let it land first, so it can
+    // never overwrite the new contents
+    HIP_TRY(c, hipEventSynchronize(c->slots[best].ready));
     c->queue.push_front(c->slots[best].tid);
     c->slots[best].armed = false;
     *out = best;
@@ -350,7 +357,7 @@ atsi_status issue_copy(atsi_ctx* c, atsi_tid tid, bool block, const std::vector<
   hipStream_t xs = copy_stream(c);
   if ((st = copy_into(c, c->tensors[tid], s, xs))) return st;
   HIP_TRY(c, hipEventRecord(s.ready, xs));
-  arm(c, s, tid, s.ready);
+  arm(c, s, tid, ++c->copy_rec);
   return ATSI_OK;
 }
 
@@ -398,8 +405,11 @@ atsi_status issue_run(atsi_ctx* c, const atsi_tid* tids, int n, bool* issued) {
   c->stats.h2d_copies += 1;
   c->stats.h2d_bytes += (uint64_t)n * c->slot_bytes;
   c->stats.h2d_tensors += (uint64_t)n;
-  HIP_TRY(c, hipEventRecord(s0.ready, xs));
-  for (int i = 0; i < n; ++i) arm(c, c->slots[first + i], tids[i], s0.ready);
+  const uint64_t rec = ++c->copy_rec;
+  for (int i = 0; i < n; ++i) {
+    HIP_TRY(c, hipEventRecord(c->slots[first + i].ready, xs));
+    arm(c, c->slots[first + i], tids[i], rec);
+  }
   *issued = true;
   return after_copy(c, xs);
 }
@@ -498,9 +508,10 @@ atsi_status acquire(atsi_ctx* c, atsi_tid tid, QView* v, std::vector<int>& held)
     if ((st = issue_copy(c, tid, true, held, &si))) return st;
   }
   Slot& s = c->slots[si];
+  // one wait per copy: slots filled by one copy (a run) share its number
   bool waited = false;
-  for (int h : held) waited = waited || c->slots[h].ready_ev == s.ready_ev;
-  if (!waited) HIP_TRY(c, hipStreamWaitEvent(c->cs, s.ready_ev, 0));
+  for (int h : held) waited = waited || c->slots[h].ready_rec == s.ready_rec;
+  if (!waited) HIP_TRY(c, hipStreamWaitEvent(c->cs, s.ready, 0));
   v->codes = reinterpret_cast<const uint8_t*>(s.base);
   v->scales = reinterpret_cast<const uint16_t*>(s.base + t.codes_bytes());
   held.push_back(si);
@@ -705,6 +716,27 @@ atsi_status check_attention(atsi_ctx* c, const atsi_tid* ids, int n_heads, int n
   return ATSI_OK;
 }
 
+// Debug buffers must be 16-byte aligned device memory.
+atsi_status check_layer_debug(atsi_ctx* c, const atsi_layer_debug* d) {
+  if (d && ((d->attn && !aligned16(d->attn)) || (d->h_attn && !aligned16(d->h_attn)) ||
+            (d->act && !aligned16(d->act)) || (d->sum32 && !aligned16(d->sum32))))
+    return fail(c, ATSI_E_INVALID, "layer debug buffers must be 16-byte aligned");
+  return ATSI_OK;
+}
+
+atsi_status check_moe_debug(atsi_ctx* c, const atsi_moe_debug* d) {
+  if (d && ((d->expert_h && !aligned16(d->expert_h)) || (d->expert_out && !aligned16(d->expert_out))))
+    return fail(c, ATSI_E_INVALID, "expert_h / expert_out must be 16-byte aligned");
+  return ATSI_OK;
+}
+
+// The residual stream after the attention block, for a caller that asked.
+atsi_status copy_h_attn(atsi_ctx* c, const atsi_layer_debug* d, const __half* hh, int M, int64_t H) {
+  if (d && d->h_attn)
+    HIP_TRY(c, hipMemcpyAsync(d->h_attn, hh, (size_t)M * H * 2, hipMemcpyDeviceToDevice, c->cs));
+  return ATSI_OK;
+}
+
 // Validate an MoE descriptor and its experts' shapes.
 atsi_status check_moe(atsi_ctx* c, const atsi_moe* m) {
   if (!m) return fail(c, ATSI_E_INVALID, "moe descriptor is NULL");
@@ -728,6 +760,16 @@ atsi_status check_moe(atsi_ctx* c, const atsi_moe* m) {
   return ATSI_OK;
 }
 
+// The SwiGLU activations of the routed pairs in pair order, for a caller that
+// asked: row i of h belongs to pair perm[i] (bucketed) or to pair i.
+atsi_status gather_expert_h(atsi_ctx* c, const atsi_moe_debug* d, const __half* h, const int32_t* perm, int rows,
+                            int I) {
+  if (!d || !d->expert_h) return ATSI_OK;
+  hipError_t e = launch_gather_rows(h, perm, rows, I, (__half*)d->expert_h, c->cs);
+  if (e != hipSuccess) return hip_fail(c, e, "expert activation gather");
+  return ATSI_OK;
+}
+
 // The routed MoE FFN (validated descriptor): y = sum_j p_j FFN_{e_j}(x) for
 // each token, plus res when res is given (y may then alias res but not x);
 // with inv_r the input is x * inv_r[t] per token (make_inv: the factors are
@@ -736,6 +778,10 @@ atsi_status check_moe(atsi_ctx* c, const atsi_moe* m) {
 atsi_status run_moe(atsi_ctx* c, const atsi_moe* m, const __half* x, int Mi, __half* y, const atsi_moe_debug* dbg,
                     float* inv_r, bool make_inv, float eps, const __half* res, Scratch& sc) {
   atsi_status st;
+  if (!c->pinned && !(Mi <= 4 && c->zero_copy))
+    for (int e = 0; e < m->n_experts; ++e)
+      if (c->tensors[m->gate[e]].on_host || c->tensors[m->up[e]].on_host || c->tensors[m->down[e]].on_host)
+        return fail(c, ATSI_E_STATE, "streamed experts need the pinned host_counts buffer given to atsi_create");
   atsi_ctx::MoeTable* tb;
   if ((st = get_table(c, m, &tb))) return st;
   const int E = m->n_experts, k = m->top_k;
@@ -754,7 +800,7 @@ atsi_status run_moe(atsi_ctx* c, const atsi_moe* m, const __half* x, int Mi, __h
   int32_t* tiles = (int32_t*)sc.take(2 * ((size_t)Mk / bm + E + 1), 4);
   int32_t* ntiles = (int32_t*)sc.take(1, 4);
   __half* h = sc.take((size_t)Mk * I);
-  __half* out = sc.take((size_t)Mk * H);
+  __half* out = dbg && dbg->expert_out ? (__half*)dbg->expert_out : sc.take((size_t)Mk * H);
   if (!part || !idx || !p || !counts || !offsets || !perm || !inv || !order || !tiles || !ntiles || !h || !out)
     return fail(c, ATSI_E_WORKSPACE, "scratch too small for a %d-token MoE layer", Mi);
   const ExpertW* table = reinterpret_cast<const ExpertW*>(c->ws + tb->off);
@@ -801,9 +847,10 @@ atsi_status run_moe(atsi_ctx* c, const atsi_moe* m, const __half* x, int Mi, __h
   const int bound = bm == 1 ? Mk : Mk / bm + std::min(E, Mk);
   if ((e = launch_expert_gateup(a, bound, gemv, c->cs)) != hipSuccess) return hip_fail(c, e, "expert gate/up launch");
   if (by_pair) {  // every expert resident: the down launch also combines
+    a.store_out = dbg && dbg->expert_out;
     if ((e = launch_expert_down_combine(a, Mi, p, res, y, c->cs)) != hipSuccess)
       return hip_fail(c, e, "expert down/combine launch");
-    return ATSI_OK;
+    return gather_expert_h(c, dbg, h, nullptr, Mk, I);
   }
   if ((e = launch_expert_down(a, bound, gemv, c->cs)) != hipSuccess) return hip_fail(c, e, "expert down launch");
 
@@ -853,19 +900,21 @@ atsi_status run_moe(atsi_ctx* c, const atsi_moe* m, const __half* x, int Mi, __h
   }
   e = launch_combine(out, p, Mi, k, H, res, y, c->cs);
   if (e != hipSuccess) return hip_fail(c, e, "combine launch");
-  return ATSI_OK;
+  return gather_expert_h(c, dbg, h, perm, Mk, I);
 }
 
 }  // namespace
 
 extern "C" {
 
-atsi_status atsi_create(int device, void* compute_stream, void* transfer_stream, void* workspace,
-                        size_t workspace_bytes, int n_slots, atsi_ctx** out) {
+atsi_status atsi_create(int device, void* compute_stream, void* transfer_stream, void* transfer_stream2,
+                        void* workspace, size_t workspace_bytes, int32_t* host_counts, int n_slots, atsi_ctx** out) {
   if (!out) return fail(nullptr, ATSI_E_INVALID, "out is NULL");
   *out = nullptr;
   if (!compute_stream || !transfer_stream || compute_stream == transfer_stream)
     return fail(nullptr, ATSI_E_INVALID, "compute and transfer streams must be distinct and non-null");
+  if (transfer_stream2 && (transfer_stream2 == compute_stream || transfer_stream2 == transfer_stream))
+    return fail(nullptr, ATSI_E_INVALID, "the second transfer stream must differ from the other two");
   if (!workspace || ((uintptr_t)workspace % kAlign) != 0)
     return fail(nullptr, ATSI_E_INVALID, "workspace must be non-null and 256-byte aligned");
   if (n_slots < 2 || n_slots > 64) return fail(nullptr, ATSI_E_INVALID, "n_slots %d outside 2..64", n_slots);
@@ -885,6 +934,8 @@ atsi_status atsi_create(int device, void* compute_stream, void* transfer_stream,
   c->ws = (char*)workspace;
   c->ws_bytes = workspace_bytes;
   c->n_slots = n_slots;
+  c->ts2 = (hipStream_t)transfer_stream2;
+  c->pinned = host_counts;
   if (const char* f = getenv("ATSI_FUSED_DECODE_LAYER")) c->fused_layer = atoi(f) == 1;
   c->table_floor = workspace_bytes / kAlign * kAlign;
   const size_t bar_bytes = align_up((kLayerBarrierWords + 1) * sizeof(unsigned));
@@ -903,10 +954,8 @@ atsi_status atsi_create(int device, void* compute_stream, void* transfer_stream,
     c->row_inv = reinterpret_cast<float*>(c->ws + c->table_floor);
   }
   c->slots.resize(n_slots);
-  if (hipHostMalloc((void**)&c->pinned, kMaxExperts * sizeof(int32_t), hipHostMallocDefault) != hipSuccess ||
-      hipEventCreateWithFlags(&c->counts_ev, hipEventDisableTiming) != hipSuccess ||
-      hipStreamCreateWithFlags(&c->ts2, hipStreamNonBlocking) != hipSuccess) {
-    fail(nullptr, ATSI_E_HIP, "pinned staging or event allocation failed");
+  if (hipEventCreateWithFlags(&c->counts_ev, hipEventDisableTiming) != hipSuccess) {
+    fail(nullptr, ATSI_E_HIP, "hipEventCreate failed");
     atsi_destroy(c);
     return ATSI_E_HIP;
   }
@@ -934,16 +983,12 @@ atsi_status atsi_destroy(atsi_ctx* c) {
   (void)hipSetDevice(c->device);
   if (c->cs) (void)hipStreamSynchronize(c->cs);
   if (c->ts) (void)hipStreamSynchronize(c->ts);
-  if (c->ts2) {
-    (void)hipStreamSynchronize(c->ts2);
-    (void)hipStreamDestroy(c->ts2);
-  }
+  if (c->ts2) (void)hipStreamSynchronize(c->ts2);
   for (Slot& s : c->slots) {
     if (s.ready) (void)hipEventDestroy(s.ready);
     if (s.free) (void)hipEventDestroy(s.free);
   }
   if (c->counts_ev) (void)hipEventDestroy(c->counts_ev);
-  if (c->pinned) (void)hipHostFree(c->pinned);
   delete c;
   return ATSI_OK;
 }
@@ -1086,13 +1131,14 @@ atsi_status atsi_swiglu_gate_up(atsi_ctx* c, atsi_tid gate, atsi_tid up, const v
 }
 
 atsi_status atsi_decoder_layer(atsi_ctx* c, const atsi_dense_layer* L, void* h, int64_t M, void* q_out,
-                               void* k_out) {
+                               void* k_out, const atsi_layer_debug* dbg) {
   if (!c) return ATSI_E_INVALID;
   if (!L) return fail(c, ATSI_E_INVALID, "layer descriptor is NULL");
   atsi_status st;
   if ((st = check_act(c, h, "h")) || (st = check_m(c, M))) return st;
   if ((q_out && !aligned16(q_out)) || (k_out && !aligned16(k_out)))
     return fail(c, ATSI_E_INVALID, "q_out / k_out must be 16-byte aligned");
+  if ((st = check_layer_debug(c, dbg))) return st;
   const atsi_tid ids[7] = {L->q, L->k, L->v, L->o, L->gate, L->up, L->down};
   for (atsi_tid t : ids)
     if ((st = check_tid(c, t))) return st;
@@ -1107,9 +1153,9 @@ atsi_status atsi_decoder_layer(atsi_ctx* c, const atsi_dense_layer* L, void* h, 
   Scratch sc(c);
   __half* qb = q_out ? (__half*)q_out : sc.take((size_t)M * Hq);
   __half* kb = k_out ? (__half*)k_out : sc.take((size_t)M * Hkv);
-  __half* oin = sc.take((size_t)M * Hq);
-  __half* hf = sc.take((size_t)M * tg.N);
-  float* y32 = L->renorm_out ? (float*)sc.take((size_t)M * H, 4) : nullptr;
+  __half* oin = dbg && dbg->attn ? (__half*)dbg->attn : sc.take((size_t)M * Hq);
+  __half* hf = dbg && dbg->act ? (__half*)dbg->act : sc.take((size_t)M * tg.N);
+  float* y32 = !L->renorm_out ? nullptr : (dbg && dbg->sum32) ? dbg->sum32 : (float*)sc.take((size_t)M * H, 4);
   if (!qb || !kb || !oin || !hf || (L->renorm_out && !y32))
     return fail(c, ATSI_E_WORKSPACE, "scratch too small for a %lld-token layer", (long long)M);
   __half* hh = (__half*)h;
@@ -1117,7 +1163,7 @@ atsi_status atsi_decoder_layer(atsi_ctx* c, const atsi_dense_layer* L, void* h, 
   const float eps = L->eps;
   bool resident = true;
   for (atsi_tid t : ids) resident = resident && !c->tensors[t].on_host;
-  if (c->fused_layer && Mi == 1 && resident && !L->renorm_out) {
+  if (c->fused_layer && Mi == 1 && resident && !L->renorm_out && !dbg) {
     // batch-1 decode with every weight in HBM: one fused launch
     LayerArgs la{};
     for (int i = 0; i < kLayerTensors; ++i) {
@@ -1149,6 +1195,7 @@ atsi_status atsi_decoder_layer(atsi_ctx* c, const atsi_dense_layer* L, void* h, 
   }
   if ((st = prefetch_call(c, ids, 7))) return st;
   if ((st = run_attention(c, ids, L->n_heads, L->n_kv_heads, L->head_dim, eps, hh, Mi, qb, kb, oin))) return st;
+  if ((st = copy_h_attn(c, dbg, hh, Mi, H))) return st;
   // 3. f = silu(rms(h) Wg) * (rms(h) Wu)
   LinOp gu = plain_op(QView{nullptr, nullptr, (int)tg.K, (int)tg.N}, hh, Mi, hf);
   gu.swiglu = 1; gu.norm = 1; gu.eps = eps;
@@ -1166,13 +1213,14 @@ atsi_status atsi_decoder_layer(atsi_ctx* c, const atsi_dense_layer* L, void* h, 
 }
 
 atsi_status atsi_moe_decoder_layer(atsi_ctx* c, const atsi_moe_layer* L, void* h, int64_t M, void* q_out,
-                                   void* k_out, const atsi_moe_debug* dbg) {
+                                   void* k_out, const atsi_moe_debug* dbg, const atsi_layer_debug* ldbg) {
   if (!c) return ATSI_E_INVALID;
   if (!L) return fail(c, ATSI_E_INVALID, "layer descriptor is NULL");
   atsi_status st;
   if ((st = check_act(c, h, "h")) || (st = check_m(c, M))) return st;
   if ((q_out && !aligned16(q_out)) || (k_out && !aligned16(k_out)))
     return fail(c, ATSI_E_INVALID, "q_out / k_out must be 16-byte aligned");
+  if ((st = check_layer_debug(c, ldbg)) || (st = check_moe_debug(c, dbg))) return st;
   const atsi_tid ids[4] = {L->q, L->k, L->v, L->o};
   if ((st = check_attention(c, ids, L->n_heads, L->n_kv_heads, L->head_dim, L->eps)) || (st = check_moe(c, L->moe)))
     return st;
@@ -1183,7 +1231,7 @@ atsi_status atsi_moe_decoder_layer(atsi_ctx* c, const atsi_moe_layer* L, void* h
   Scratch sc(c);
   __half* qb = q_out ? (__half*)q_out : sc.take((size_t)M * Hq);
   __half* kb = k_out ? (__half*)k_out : sc.take((size_t)M * Hkv);
-  __half* oin = sc.take((size_t)M * Hq);
+  __half* oin = ldbg && ldbg->attn ? (__half*)ldbg->attn : sc.take((size_t)M * Hq);
   float* inv_r = (float*)sc.take(M, 4);
   if (!qb || !kb || !oin || !inv_r)
     return fail(c, ATSI_E_WORKSPACE, "scratch too small for a %lld-token layer", (long long)M);
@@ -1192,6 +1240,7 @@ atsi_status atsi_moe_decoder_layer(atsi_ctx* c, const atsi_moe_layer* L, void* h
   // expert copies wait for routing; the attention tensors can start now
   if ((st = prefetch_call(c, ids, 4))) return st;
   if ((st = run_attention(c, ids, L->n_heads, L->n_kv_heads, L->head_dim, L->eps, hh, Mi, qb, kb, oin))) return st;
+  if ((st = copy_h_attn(c, ldbg, hh, Mi, H))) return st;
   // h = h + MoE(rms(h)): the norm is a per-token factor on the router logits
   // and the expert gate/up products (computed with the routing), the residual
   // is added by the combine
@@ -1232,7 +1281,8 @@ atsi_status atsi_moe_ffn(atsi_ctx* c, const atsi_moe* m, const void* x, int64_t 
                          const atsi_moe_debug* dbg) {
   if (!c) return ATSI_E_INVALID;
   atsi_status st;
-  if ((st = check_act(c, x, "x")) || (st = check_act(c, y, "y")) || (st = check_m(c, M)) || (st = check_moe(c, m)))
+  if ((st = check_act(c, x, "x")) || (st = check_act(c, y, "y")) || (st = check_m(c, M)) || (st = check_moe(c, m)) ||
+      (st = check_moe_debug(c, dbg)))
     return st;
   if (x == y) return fail(c, ATSI_E_INVALID, "y must not alias x");
   if ((st = enter(c))) return st;
@@ -1300,7 +1350,7 @@ atsi_status atsi_sync(atsi_ctx* c) {
   if (!c) return ATSI_E_INVALID;
   hipError_t e = hipSetDevice(c->device);
   if (e == hipSuccess) e = hipStreamSynchronize(c->ts);
-  if (e == hipSuccess) e = hipStreamSynchronize(c->ts2);
+  if (e == hipSuccess && c->ts2) e = hipStreamSynchronize(c->ts2);
   if (e == hipSuccess) e = hipStreamSynchronize(c->cs);
   if (e != hipSuccess) hip_fail(c, e, "stream synchronize");
   if (e == hipSuccess && c->layer_launched) {

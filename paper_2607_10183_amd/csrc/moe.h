@@ -41,6 +41,7 @@ struct MoeArgs {
   const int32_t* pair_expert;
   int n_pairs;
   int n_experts;               // table entries (a pair naming another expert is skipped)
+  int store_out;               // the fused down/combine launch also stores the expert outputs in out
 };
 
 // router: logits = x W_r + b (fp32 accumulation), top-k with renormalised
@@ -76,6 +77,9 @@ hipError_t launch_expert_down_combine(const MoeArgs& a, int M, const float* p, c
 // y[t] = sum_j p[t][j] * out[k*t + j] (fp32, slot order) -> fp16
 hipError_t launch_combine(const __half* out, const float* p, int M, int k, int H, const __half* res, __half* y,
                           hipStream_t s);
+// dst[perm[i]] = src[i] for rows i < rows of `cols` fp16 (dst[i] = src[i] when
+// perm is null); cols % 8 == 0
+hipError_t launch_gather_rows(const __half* src, const int32_t* perm, int rows, int cols, __half* dst, hipStream_t s);
 // write table entries e0 .. e0+n-1 (n <= 16) and their residency flags
 hipError_t launch_table_patch(ExpertW* table, uint8_t* resident, int e0, int n, const ExpertW* w, const uint8_t* r,
                               hipStream_t s);

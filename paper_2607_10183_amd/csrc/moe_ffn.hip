@@ -247,7 +247,11 @@ __global__ __launch_bounds__(kDcThreads) void expert_down_combine(MoeArgs a, con
     }
     if (lane == 0) {
 #pragma unroll
-      for (int r = 0; r < RW; ++r) outs[j][(task % SUB) * RW + r] = __half2float(__float2half_rn(g[r]));
+      for (int r = 0; r < RW; ++r) {
+        const __half o = __float2half_rn(g[r]);
+        outs[j][(task % SUB) * RW + r] = __half2float(o);
+        if (a.store_out && n0 + r < a.H) a.out[(size_t)pr * a.H + n0 + r] = o;
+      }
     }
   }
   __syncthreads();
@@ -299,6 +303,16 @@ __global__ void combine_kernel(const __half* __restrict__ out, const float* __re
 #pragma unroll
     for (int i = 0; i < 8; ++i) ho[i] = __float2half_rn(acc[i]);
     *reinterpret_cast<uint4*>(y + (size_t)t * H + (size_t)c * 8) = o;
+  }
+}
+
+__global__ void gather_rows_kernel(const uint4* __restrict__ src, const int32_t* __restrict__ perm, int rows, int c16,
+                                   uint4* __restrict__ dst) {
+  const size_t total = (size_t)rows * c16;
+  for (size_t q = (size_t)blockIdx.x * blockDim.x + threadIdx.x; q < total; q += (size_t)gridDim.x * blockDim.x) {
+    const int i = (int)(q / c16), c = (int)(q % c16);
+    const int to = perm ? perm[i] : i;
+    if ((unsigned)to < (unsigned)rows) dst[(size_t)to * c16 + c] = src[q];
   }
 }
 
@@ -359,6 +373,15 @@ hipError_t launch_combine(const __half* out, const float* p, int M, int k, int H
   const size_t total = (size_t)M * (H / 8);
   const int blocks = (int)std::min<size_t>((total + 255) / 256, 2048);
   hipLaunchKernelGGL(combine_kernel, dim3(blocks), dim3(256), 0, s, out, p, M, k, H, res, y);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather_rows(const __half* src, const int32_t* perm, int rows, int cols, __half* dst, hipStream_t s) {
+  if (rows < 1 || cols % 8) return hipErrorInvalidValue;
+  const size_t total = (size_t)rows * (cols / 8);
+  const int blocks = (int)std::min<size_t>((total + 255) / 256, 4096);
+  hipLaunchKernelGGL(gather_rows_kernel, dim3(blocks), dim3(256), 0, s, reinterpret_cast<const uint4*>(src), perm, rows,
+                     cols / 8, reinterpret_cast<uint4*>(dst));
   return hipGetLastError();
 }
 

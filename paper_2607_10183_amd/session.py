@@ -14,15 +14,20 @@ from . import atsi
 class Session:
     """One atsi context on one GPU with its own compute and transfer streams."""
 
-    def __init__(self, workspace_bytes: int = 1 << 30, n_slots: int = 4, device: int = 0):
+    def __init__(self, workspace_bytes: int = 1 << 30, n_slots: int = 4, device: int = 0,
+                 two_transfer_streams: bool = True):
         if not torch.cuda.is_available():
             raise RuntimeError("no GPU visible to torch; the atsi library has no CPU path")
         self.device = torch.device("cuda", device)
         self.cs = torch.cuda.Stream(device=self.device)
         self.ts = torch.cuda.Stream(device=self.device)
+        self.ts2 = torch.cuda.Stream(device=self.device) if two_transfer_streams else None
         self.ws = torch.empty(workspace_bytes, dtype=torch.uint8, device=self.device)
-        self.ctx = atsi.atsi_create(device, self.cs.cuda_stream, self.ts.cuda_stream, self.ws.data_ptr(),
-                                    workspace_bytes, n_slots)
+        # pinned host buffer for the per-expert counts of MoE calls with streamed experts
+        self.counts_host = torch.empty(128, dtype=torch.int32).pin_memory()
+        self.ctx = atsi.atsi_create(device, self.cs.cuda_stream, self.ts.cuda_stream,
+                                    self.ts2.cuda_stream if self.ts2 is not None else 0, self.ws.data_ptr(),
+                                    workspace_bytes, self.counts_host.data_ptr(), n_slots)
         self._keep: list = []
         self.shapes: list[tuple[int, int]] = []
         self.placement: list[int] = []  # current host mask, mirrors the library's
@@ -169,18 +174,32 @@ class Session:
 
     def decoder_layer(self, tids: dict, h: torch.Tensor, n_heads: int, n_kv: int, head_dim: int,
                       eps: float = 1e-6, q_out: torch.Tensor | None = None, k_out: torch.Tensor | None = None,
-                      renorm_out: bool = False):
+                      renorm_out: bool = False, debug: bool = False):
         """In-place pre-norm decoder layer on h[M][H]; tids maps q,k,v,o,gate,up,down to tensor ids.
-        renorm_out: the output is renormalised (h <- rms(h + FFN)), as between the layers of a stack."""
+        renorm_out: the output is renormalised (h <- rms(h + FFN)), as between the layers of a stack.
+        debug: also returns the intermediate activations {attn, h_attn, act[, sum32]}."""
         L = atsi.atsi_dense_layer(n_heads, n_kv, head_dim, eps, *[tids[r] for r in
                                                                   ("q", "k", "v", "o", "gate", "up", "down")],
                                   int(renorm_out))
-        M = h.shape[0]
+        M, H = h.shape
+        inter = self.shapes[tids["gate"]][1]
+        out, dbg = self._layer_debug(M, H, n_heads * head_dim, inter, renorm_out) if debug else ({}, None)
         self._wait_torch()
         atsi.atsi_decoder_layer(self.ctx, L, h.data_ptr(), M, q_out.data_ptr() if q_out is not None else 0,
-                                k_out.data_ptr() if k_out is not None else 0)
+                                k_out.data_ptr() if k_out is not None else 0, dbg)
         self._torch_waits()
-        return h
+        return (h, out) if debug else h
+
+    def _layer_debug(self, M: int, H: int, Hq: int, inter: int, sum32: bool):
+        with torch.cuda.stream(self.cs):
+            out = {"attn": torch.empty((M, Hq), dtype=torch.float16, device=self.device),
+                   "h_attn": torch.empty((M, H), dtype=torch.float16, device=self.device)}
+            if inter:
+                out["act"] = torch.empty((M, inter), dtype=torch.float16, device=self.device)
+            if sum32:
+                out["sum32"] = torch.empty((M, H), dtype=torch.float32, device=self.device)
+        dbg = atsi.atsi_layer_debug(*[out[n].data_ptr() if n in out else None for n in atsi.LAYER_DEBUG_FIELDS])
+        return out, dbg
 
     def moe_layer(self, router_w: torch.Tensor, gate, up, down, top_k: int,
                   router_bias: torch.Tensor | None = None) -> "MoELayer":
@@ -266,16 +285,8 @@ class MoELayer:
         with torch.cuda.stream(s.cs):
             if y is None:
                 y = torch.empty((M, self.H), dtype=torch.float16, device=s.device)
-            if debug:
-                out = {"logits": torch.empty((M, self.E), dtype=torch.float32, device=s.device),
-                       "idx": torch.empty((M, self.k), dtype=torch.int32, device=s.device),
-                       "p": torch.empty((M, self.k), dtype=torch.float32, device=s.device),
-                       "counts": torch.empty(self.E, dtype=torch.int32, device=s.device),
-                       "offsets": torch.empty(self.E + 1, dtype=torch.int32, device=s.device),
-                       "perm": torch.empty(M * self.k, dtype=torch.int32, device=s.device),
-                       "inv_perm": torch.empty(M * self.k, dtype=torch.int32, device=s.device)}
-                dbg = atsi.atsi_moe_debug(*[out[n].data_ptr() for n in
-                                            ("logits", "idx", "p", "counts", "offsets", "perm", "inv_perm")])
+        if debug:
+            out, dbg = self._debug_buffers(M)
         s._wait_torch()
         atsi.atsi_moe_ffn(s.ctx, self.desc, x.data_ptr(), M, y.data_ptr(), dbg)
         s._torch_waits()
@@ -290,9 +301,10 @@ class MoELayer:
                    "counts": torch.empty(self.E, dtype=torch.int32, device=s.device),
                    "offsets": torch.empty(self.E + 1, dtype=torch.int32, device=s.device),
                    "perm": torch.empty(M * self.k, dtype=torch.int32, device=s.device),
-                   "inv_perm": torch.empty(M * self.k, dtype=torch.int32, device=s.device)}
-        dbg = atsi.atsi_moe_debug(*[out[n].data_ptr() for n in
-                                    ("logits", "idx", "p", "counts", "offsets", "perm", "inv_perm")])
+                   "inv_perm": torch.empty(M * self.k, dtype=torch.int32, device=s.device),
+                   "expert_h": torch.empty((M * self.k, self.I), dtype=torch.float16, device=s.device),
+                   "expert_out": torch.empty((M * self.k, self.H), dtype=torch.float16, device=s.device)}
+        dbg = atsi.atsi_moe_debug(*[out[n].data_ptr() for n in atsi.MOE_DEBUG_FIELDS])
         return out, dbg
 
 
@@ -302,17 +314,23 @@ class MoEDecoderLayer:
     def __init__(self, moe: MoELayer, q: int, k: int, v: int, o: int, n_heads: int, n_kv: int, head_dim: int,
                  eps: float = 1e-6):
         self.moe = moe
+        self.n_heads, self.head_dim = n_heads, head_dim
         self.desc = atsi.atsi_moe_layer(n_heads, n_kv, head_dim, eps, q, k, v, o,
                                         __import__("ctypes").pointer(moe.desc))
 
     def __call__(self, h: torch.Tensor, q_out: torch.Tensor | None = None, k_out: torch.Tensor | None = None,
                  debug: bool = False):
-        """Updates h (fp16 [M][hidden]) in place; returns the routing buffers when debug."""
+        """Updates h (fp16 [M][hidden]) in place; returns the routing buffers and
+        the intermediate activations (attn, h_attn, expert_h, expert_out) when debug."""
         s = self.moe.sess
-        M = h.shape[0]
-        out, dbg = self.moe._debug_buffers(M) if debug else ({}, None)
+        M, H = h.shape
+        out, dbg, ldbg = {}, None, None
+        if debug:
+            out, dbg = self.moe._debug_buffers(M)
+            lo, ldbg = s._layer_debug(M, H, self.n_heads * self.head_dim, 0, False)
+            out.update(lo)
         s._wait_torch()
         atsi.atsi_moe_decoder_layer(s.ctx, self.desc, h.data_ptr(), M, q_out.data_ptr() if q_out is not None else 0,
-                                    k_out.data_ptr() if k_out is not None else 0, dbg)
+                                    k_out.data_ptr() if k_out is not None else 0, dbg, ldbg)
         s._torch_waits()
         return out if debug else None

@@ -7,6 +7,6 @@ identical bytes on both sides.
 """
 from .gen import (  # noqa: F401
     stream_key, words, uniform01, normal, to_f16,
-    int4_codes, group_scales, activations, exact_activations, exact_scales,
+    int4_codes, group_scales, activations, exact_activations, sign_activations, exact_scales,
     router_weights, permutation, scores,
 )

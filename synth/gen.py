@@ -130,6 +130,13 @@ def exact_activations(seed: int, uid: int, M: int, K: int) -> np.ndarray:
     return to_f16(v * 0.25).reshape(M, K)
 
 
+def sign_activations(seed: int, uid: int, M: int, K: int) -> np.ndarray:
+    """fp16 activations [M][K] of +1 or -1 (every row has mean square exactly 1)."""
+    key = stream_key(seed, uid, KIND_ACT)
+    v = (words(key, 0, M * K) & np.uint64(1)).astype(np.int64) * 2 - 1
+    return to_f16(v.astype(np.float64)).reshape(M, K)
+
+
 def exact_scales(N: int, K: int) -> np.ndarray:
     """fp16 scales [N][K/32], all 2**-6."""
     return np.full((N, K // 32), 2.0 ** -6, dtype=np.float16)

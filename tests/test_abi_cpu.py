@@ -45,13 +45,16 @@ def test_create_validates_before_hip(lib):
     P = ctypes.c_void_p
     out = P()
     # null out
-    assert lib.atsi_create(0, 1, 2, 256, 1 << 20, 4, None) == 1
-    # same stream twice / null stream
-    assert lib.atsi_create(0, 1, 1, 256, 1 << 20, 4, ctypes.byref(out)) == 1
-    assert lib.atsi_create(0, 0, 2, 256, 1 << 20, 4, ctypes.byref(out)) == 1
+    assert lib.atsi_create(0, 1, 2, None, 256, 1 << 20, None, 4, None) == 1
+    # same stream twice / null stream / second transfer stream equal to another
+    assert lib.atsi_create(0, 1, 1, None, 256, 1 << 20, None, 4, ctypes.byref(out)) == 1
+    assert lib.atsi_create(0, 0, 2, None, 256, 1 << 20, None, 4, ctypes.byref(out)) == 1
+    assert lib.atsi_create(0, 1, 2, 2, 256, 1 << 20, None, 4, ctypes.byref(out)) == 1
+    assert lib.atsi_create(0, 1, 2, 1, 256, 1 << 20, None, 4, ctypes.byref(out)) == 1
+    assert "second transfer stream" in atsi.atsi_last_error(None)
     # misaligned workspace, bad slot count
-    assert lib.atsi_create(0, 1, 2, 255, 1 << 20, 4, ctypes.byref(out)) == 1
-    assert lib.atsi_create(0, 1, 2, 256, 1 << 20, 1, ctypes.byref(out)) == 1
+    assert lib.atsi_create(0, 1, 2, 3, 255, 1 << 20, None, 4, ctypes.byref(out)) == 1
+    assert lib.atsi_create(0, 1, 2, 3, 256, 1 << 20, None, 1, ctypes.byref(out)) == 1
     assert "n_slots" in atsi.atsi_last_error(None)
     assert out.value is None
 
@@ -62,7 +65,7 @@ def test_create_without_gpu_fails_cleanly(lib):
         pytest.skip("a GPU is present")
     from paper_2607_10183_amd import atsi
     out = ctypes.c_void_p()
-    st = lib.atsi_create(0, 1, 2, 256, 1 << 20, 4, ctypes.byref(out))
+    st = lib.atsi_create(0, 1, 2, 3, 256, 1 << 20, None, 4, ctypes.byref(out))
     assert st == 6 and out.value is None
     assert "GPU" in atsi.atsi_last_error(None)
 

@@ -78,7 +78,9 @@ def test_dense_stack_decode_parity(stack):
             ref, zeta, _ = oracle.decoder_layer(ref, W[layer], shape.n_heads, shape.n_kv, shape.head_dim, 1e-6,
                                                 h_zeta=zeta)
             ref, zeta = oracle.rmsnorm(ref, 1e-6, zeta)
-    check(h.cpu().numpy(), ref, zeta, name=f"{N_LAYERS}-layer stack, 2 steps, M={WL.decode_m}")
+    # free-running drift over 8 layer applications (each layer's stages are
+    # checked teacher-forced elsewhere): a looser per-token norm
+    check(h.cpu().numpy(), ref, zeta, name=f"{N_LAYERS}-layer stack, 2 steps, M={WL.decode_m}", rel_l2=3e-3)
 
 
 def test_dense_stack_placement_invariance(stack):

@@ -6,7 +6,8 @@ import pytest
 import oracle
 import synth
 from synth import configs
-from tests.parity import check
+from tests import stages
+from tests.parity import assert_within_one_ulp16, bits16, check
 
 pytestmark = pytest.mark.gpu
 
@@ -58,6 +59,32 @@ def test_swiglu_gate_up_parity(sess, H, I, M):
     check(h, ref, zeta, name=f"gate/up H={H} I={I} M={M}")
 
 
+# (H, I, M): the batch-1 GEMV, the batched-decode kernel, the 128-row GEMM, the
+# 512-row-tile GEMM over the whole of K (ragged rows, a K step left half full)
+# and with K split into ranges (the reduction kernel applies the SwiGLU)
+EXACT_GATE_UP = [(4096, 14336, 1), (256, 96, 1), (4096, 1024, 4), (4096, 1024, 8), (2048, 768, 16),
+                 (512, 160, 77), (4096, 1024, 300), (128, 24576, 300), (96, 24576, 520), (4096, 4096, 512),
+                 (4096, 14336, 512)]
+
+
+@pytest.mark.parametrize("H,I,M", EXACT_GATE_UP)
+def test_swiglu_gate_up_exact_inputs(sess, H, I, M):
+    """Scales 2^-6 and activations in {-4..4}/4 make g = x Wg and u = x Wu
+    exact in fp32 on every path, so each fp16 h = silu(g) * u must be the
+    nearest-even rounding of the exact value or one of its neighbours (SiLU's
+    exp and reciprocal are the only inexact steps)."""
+    gate = (synth.int4_codes(85, H + 1, I, H), synth.exact_scales(I, H))
+    up = (synth.int4_codes(85, H + 2, I, H), synth.exact_scales(I, H))
+    tg = sess.register(*gate)
+    tu = sess.register(*up)
+    xn = synth.exact_activations(85, M, M, H)
+    h = sess.gate_up(tg, tu, _dev(xn)).cpu().numpy()
+    sess.sync()
+    g, _ = oracle.linear(xn, *gate)
+    u, _ = oracle.linear(xn, *up)
+    assert_within_one_ulp16(h, oracle.silu(g) * u, name=f"exact gate/up H={H} I={I} M={M}")
+
+
 def _layer_weights(shape, seed, layer=0):
     return {r: _qt(seed, configs.dense_uid(layer, r), shape.kn(r)[1], shape.kn(r)[0]) for r in configs.ROLES}
 
@@ -72,8 +99,13 @@ WIDE_ATTN = configs.DenseShape(hidden=4096, n_heads=64, n_kv=4, head_dim=128, in
 
 
 @pytest.mark.parametrize("shape,M", [(SMALL, 1), (SMALL, 2), (SMALL, 5), (SMALL, 64),
-                                     (configs.DenseShape(), 1), (configs.DenseShape(), 512), (WIDE_ATTN, 2048)])
+                                     (configs.DenseShape(), 1), (configs.DenseShape(), 8),
+                                     (configs.DenseShape(), 512), (WIDE_ATTN, 2048)])
 def test_decoder_layer_parity(sess, shape, M):
+    """The layer's output against the oracle layer (spec bound and
+    per-token norm), and every stage inside it teacher-forced: each projection
+    against the oracle on the GPU's own fp16 input to it, at that stage's
+    tight bound."""
     import torch
     W = _layer_weights(shape, 72)
     tids = {r: sess.register(*W[r]) for r in configs.ROLES}
@@ -81,15 +113,76 @@ def test_decoder_layer_parity(sess, shape, M):
     h = _dev(hn)
     q_out = torch.empty((M, shape.n_heads * shape.head_dim), dtype=torch.float16, device="cuda")
     k_out = torch.empty((M, shape.n_kv * shape.head_dim), dtype=torch.float16, device="cuda")
-    sess.decoder_layer(tids, h, shape.n_heads, shape.n_kv, shape.head_dim, 1e-6, q_out, k_out)
+    _, dbg = sess.decoder_layer(tids, h, shape.n_heads, shape.n_kv, shape.head_dim, 1e-6, q_out, k_out, debug=True)
     sess.sync()
-    ref, zeta, aux = oracle.decoder_layer(hn, W, shape.n_heads, shape.n_kv, shape.head_dim, 1e-6)
-    check(h.cpu().numpy(), ref, zeta, name=f"layer H={shape.hidden} M={M}")
-    a, za = oracle.rmsnorm(hn.astype(np.float64), 1e-6)
-    qr, zq = oracle.linear(a, *W["q"], za)
-    kr, zk = oracle.linear(a, *W["k"], za)
-    check(q_out.cpu().numpy(), qr, zq, name="q projection")
-    check(k_out.cpu().numpy(), kr, zk, name="k projection")
+    name = f"layer H={shape.hidden} M={M}"
+    big = M * shape.hidden > 512 * 4096
+    rows = np.arange(M) if not big else np.sort(synth.permutation(72, 5, M)[:256])
+    g = {n: t.cpu().numpy()[rows] for n, t in dict(dbg, q=q_out, k=k_out, h=h).items()}
+    stages.attention_stages(W, shape.n_heads, shape.n_kv, shape.head_dim, hn[rows], g["q"], g["k"], g["attn"],
+                            g["h_attn"], name)
+    stages.ffn_stages(W, g["h_attn"], g["act"], g["h"], name)
+    ref, zeta, aux = oracle.decoder_layer(hn if not big else hn[:64], W, shape.n_heads, shape.n_kv, shape.head_dim,
+                                          1e-6)
+    check(h.cpu().numpy()[:ref.shape[0]], ref, zeta, name=name, rel_l2=stages.COMPOSITE_ROW_L2)
+
+
+@pytest.mark.parametrize("M", [1, 8, 77])
+def test_renormalised_layer_stages(sess, M):
+    """A layer of the renormalised stack: the fp32 residual sum and its
+    renormalisation, each against the oracle on the GPU's own inputs."""
+    import torch
+    shape = configs.DenseShape()
+    W = _layer_weights(shape, 78)
+    tids = {r: sess.register(*W[r]) for r in configs.ROLES}
+    hn = synth.activations(78, 2000 + M, M, shape.hidden)
+    h = _dev(hn)
+    q_out = torch.empty((M, shape.n_heads * shape.head_dim), dtype=torch.float16, device="cuda")
+    k_out = torch.empty((M, shape.n_kv * shape.head_dim), dtype=torch.float16, device="cuda")
+    _, dbg = sess.decoder_layer(tids, h, shape.n_heads, shape.n_kv, shape.head_dim, 1e-6, q_out, k_out,
+                                renorm_out=True, debug=True)
+    sess.sync()
+    name = f"renormalised layer M={M}"
+    stages.attention_stages(W, shape.n_heads, shape.n_kv, shape.head_dim, hn, q_out, k_out, dbg["attn"],
+                            dbg["h_attn"], name)
+    stages.ffn_stages(W, dbg["h_attn"], dbg["act"], h, name, sum32=dbg["sum32"])
+
+
+EXACT_LAYER_CASES = [(SMALL, 1), (SMALL, 4), (SMALL, 64), (configs.DenseShape(), 1), (configs.DenseShape(), 4),
+                     (configs.DenseShape(), 64), (configs.DenseShape(), 512), (WIDE_ATTN, 512)]
+
+
+@pytest.mark.parametrize("shape,M", EXACT_LAYER_CASES)
+def test_layer_exact_inputs_bitexact(sess, shape, M):
+    """Inputs of +-1 (each row's mean square is exactly 1, so with eps = 0 the
+    norm factor is exactly 1) and scales 2^-6: q, k and v are exact in fp32,
+    so q, k and the grouped-query expansion of v must be the nearest-even fp16
+    rounding of the exact values bit for bit; so must the O projection plus
+    residual, whose products and partial sums then lie on a 2^-12 grid below
+    2^12 (checked).  Covers the fused norm, the expansion and residual
+    epilogues, and at 512 tokens the K-split reduction."""
+    import torch
+    hd = shape.head_dim
+    W = {r: (synth.int4_codes(80, configs.dense_uid(0, r), shape.kn(r)[1], shape.kn(r)[0]),
+             synth.exact_scales(shape.kn(r)[1], shape.kn(r)[0])) for r in configs.ROLES}
+    tids = {r: sess.register(*W[r]) for r in configs.ROLES}
+    hn = synth.sign_activations(80, M, M, shape.hidden)
+    h = _dev(hn)
+    q_out = torch.empty((M, shape.n_heads * hd), dtype=torch.float16, device="cuda")
+    k_out = torch.empty((M, shape.n_kv * hd), dtype=torch.float16, device="cuda")
+    _, dbg = sess.decoder_layer(tids, h, shape.n_heads, shape.n_kv, hd, 0.0, q_out, k_out, debug=True)
+    sess.sync()
+    x = hn.astype(np.float64)
+    q, _ = oracle.linear(x, *W["q"])
+    k, _ = oracle.linear(x, *W["k"])
+    v, _ = oracle.linear(x, *W["v"])
+    assert np.array_equal(bits16(q_out), bits16(q)), "q"
+    assert np.array_equal(bits16(k_out), bits16(k)), "k"
+    attn = oracle.gqa_stub(v.astype(np.float16), shape.n_heads, shape.n_kv, hd)
+    assert np.array_equal(bits16(dbg["attn"]), bits16(attn)), "grouped-query expansion"
+    o, zo = oracle.linear(attn.astype(np.float64), *W["o"])
+    assert np.max(zo + 1.0) < 2.0 ** 12, "partial sums would leave the exact fp32 range"
+    assert np.array_equal(bits16(dbg["h_attn"]), bits16(x + o)), "O + residual"
 
 
 @pytest.fixture(scope="module")

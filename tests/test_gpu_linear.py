@@ -5,7 +5,7 @@ import pytest
 
 import oracle
 import synth
-from tests.parity import bits16, check
+from tests.parity import bits16, check, tight_eps
 
 pytestmark = pytest.mark.gpu
 
@@ -96,7 +96,9 @@ def test_random_parity(sess, K, N, M):
     sess.sync()
     rows = np.arange(N) if N * M <= 4096 * 512 else synth.permutation(63, 9, N)[:2048]
     ref, zeta = oracle.linear(xn, codes[rows], scales[rows])
-    check(y[:, rows], ref, zeta, name=f"linear K={K} N={N} M={M}")
+    # exact products on the GEMV and the batched-decode kernel; fp16-rounded
+    # dequantised weights on the MFMA GEMM (every K here is a multiple of 128)
+    check(y[:, rows], ref, zeta, name=f"linear K={K} N={N} M={M}", tight=tight_eps(K, mfma=M > 16))
 
 
 @pytest.mark.parametrize("M", [1, 3, 16, 200])

@@ -7,6 +7,7 @@ import pytest
 import oracle
 import synth
 from synth import configs
+from tests import stages
 from tests.parity import check
 
 pytestmark = pytest.mark.gpu
@@ -81,49 +82,57 @@ class _Layer:
         return ref, zeta, aux, box
 
 
-def _decided(gpu_logits, logits, k):
-    """Tokens whose top-k set is unique: the oracle's k-th and (k+1)-th logits
-    are further apart than twice the GPU's largest logit error on that token.
-    (The router sees h after the attention half, in fp16, so its logits carry
-    that half's rounding; the logit error itself is checked against the
-    propagated magnitude.)"""
-    delta = np.abs(gpu_logits - logits).max(axis=1)
-    srt = -np.sort(-logits, axis=1)
-    return srt[:, k - 1] - srt[:, k] > 2 * delta, delta
-
-
-def _run_and_check(sess, L, M, seed, name):
+def _run_and_check(sess, L, M, seed, name, sample=False):
+    """The layer through the C ABI with every intermediate exposed; each stage
+    against the oracle on the GPU's own input to it: attention (q, k, the
+    attention output, O + residual), router logits on rms(h_attn), routing,
+    bucketing, the routed experts' SwiGLU activations and down projections,
+    and the combine with the residual.  Small calls also compare the whole
+    layer with the oracle layer on the GPU's routing.  sample: check sampled
+    rows, pairs and columns of the large stages (the routing, bucketing and
+    combine are checked in full)."""
     import torch
     s = L.s
-    hn = synth.activations(seed, 400 + M, M, s["hidden"])
+    H, E, k = s["hidden"], s["n_experts"], s["top_k"]
+    hn = synth.activations(seed, 400 + M, M, H)
     h = _dev(hn)
     q_out = torch.empty((M, s["n_heads"] * s["head_dim"]), dtype=torch.float16, device="cuda")
     k_out = torch.empty((M, s["n_kv"] * s["head_dim"]), dtype=torch.float16, device="cuda")
     dbg = L.layer(h, q_out, k_out, debug=True)
     sess.sync()
-    ref, zeta, aux, box = L.reference(hn)
-    k = s["top_k"]
-    lg = dbg["logits"].cpu().numpy().astype(np.float64)
-    check(lg, box["logits"], box["logit_zeta"], name=f"{name} logits")
-    dec, delta = _decided(lg, box["logits"], k)
-    assert dec.sum() >= int(0.6 * M), f"{name}: too many near-tied routing decisions"
-    idx = dbg["idx"].cpu().numpy()
-    # every selection is a valid top-k of the oracle logits within the logit error
-    kth = -np.sort(-box["logits"], axis=1)[:, k - 1]
-    chosen = np.take_along_axis(box["logits"], idx.astype(np.int64), axis=1)
-    assert np.all(chosen >= (kth - 2 * delta)[:, None]), f"{name}: a selection is not a valid top-k"
-    for t in np.nonzero(dec)[0]:
-        assert set(idx[t]) == set(box["idx"][t]), f"{name}: token {t} routed to other experts"
-    if dec.any():
-        check(h.cpu().numpy()[dec], ref[dec], zeta[dec], name=f"{name} h")
-    a, za = oracle.rmsnorm(hn.astype(np.float64), 1e-6)
-    qr, zq = oracle.linear(a, *L.W["q"], za)
-    kr, zk = oracle.linear(a, *L.W["k"], za)
-    check(q_out.cpu().numpy(), qr, zq, name=f"{name} q")
-    check(k_out.cpu().numpy(), kr, zk, name=f"{name} k")
-    # bucketing of the GPU's own routing is the oracle's bucketing of it
-    for key, refv in zip(("counts", "offsets", "perm", "inv_perm"), oracle.bucket(idx, s["n_experts"])):
-        assert np.array_equal(dbg[key].cpu().numpy(), refv), f"{name}: {key}"
+    g = {n: t.cpu().numpy() for n, t in dict(dbg, q=q_out, k=k_out, h=h).items()}
+    perm = synth.permutation(seed, 7, 1 << 20)
+    rows = np.sort(perm[perm < M][:256]) if sample else np.arange(M)
+    cols = np.sort(perm[perm < max(H, s["n_heads"] * s["head_dim"])][:256]) if sample else None
+    stages.attention_stages(L.W, s["n_heads"], s["n_kv"], s["head_dim"], hn[rows], g["q"][rows], g["k"][rows],
+                            g["attn"][rows], g["h_attn"][rows], name, cols=cols)
+    # the MoE half on the GPU's own residual stream after attention
+    h1 = g["h_attn"].astype(np.float64)
+    x, _ = oracle.rmsnorm(h1, 1e-6)
+    lr, zl = oracle.router_logits(x, L.wr, L.bias.astype(np.float64))
+    check(g["logits"], lr, zl, name=f"{name} logits", tight=H * 2.0 ** -24 + 2.0 ** -20)
+    idx, p = g["idx"], g["p"].astype(np.float64)
+    decided = stages.moe_routing(g["logits"].astype(np.float64), idx, p, lr, E, k, name)
+    assert decided.sum() >= int(0.6 * M), f"{name}: too many near-tied routing decisions"
+    for key, refv in zip(("counts", "offsets", "perm", "inv_perm"), oracle.bucket(idx, E)):
+        assert np.array_equal(g[key], refv), f"{name}: {key}"
+    if sample:
+        pairs = np.sort(synth.permutation(seed, 8, M * k)[:256])
+        ci = np.sort(synth.permutation(seed, 9, s["inter"])[:128])
+        ch = np.sort(synth.permutation(seed, 10, H)[:128])
+    else:
+        pairs = ci = ch = None
+    stages.moe_stages(L.experts, x, idx, p, g["expert_h"], g["expert_out"], g["h"], name, res=h1, mfma=M > 4,
+                      norm=True, pairs=pairs, cols_i=ci, cols_h=ch)
+    if not sample:
+        # the whole MoE half on the GPU's routing, and the whole layer where the
+        # routing is decided, against the oracle layer
+        yr, zr, _ = oracle.moe_ffn(x, L.wr, L.bias.astype(np.float64), L.experts, k, route=(idx, p))
+        check(g["h"], h1 + yr, zr + np.abs(h1), name=f"{name} MoE half on the GPU's routing",
+              rel_l2=stages.COMPOSITE_ROW_L2)
+        ref, zeta, _, _ = L.reference(hn)
+        if decided.any():
+            check(g["h"][decided], ref[decided], zeta[decided], name=f"{name} layer", rel_l2=stages.COMPOSITE_ROW_L2)
 
 
 @pytest.mark.parametrize("M", [1, 5, 16, 64])
@@ -151,6 +160,27 @@ def test_moe_stack_layer_parity(sess, stack_layer, M):
     sess.set_placement(mask)
     try:
         _run_and_check(sess, L, M, configs.MOE_STACK.seed, f"moe stack layer M={M}")
+    finally:
+        for j in range(3):
+            for e in range(L.s["n_experts"]):
+                mask[L.tids[j][e]] = 0
+        sess.set_placement(mask)
+
+
+def test_moe_stack_layer_prefill_2048(sess, stack_layer):
+    """The 235B-A22B-shaped layer at a 2048-token prefill chunk (expert buckets
+    of up to 2048 rows) with 40 % of its experts streamed from host: routing,
+    bucketing and the combine in full, the other stages on sampled rows,
+    routed pairs and columns."""
+    L = stack_layer
+    host_exp = configs.moe_host_experts(frac=0.40, seed=configs.MOE_STACK.seed, layer=configs.MOE_STACK.n_layers - 1)
+    mask = list(sess.placement)
+    for j in range(3):
+        for e in range(L.s["n_experts"]):
+            mask[L.tids[j][e]] = int(host_exp[e])
+    sess.set_placement(mask)
+    try:
+        _run_and_check(sess, L, 2048, configs.MOE_STACK.seed, "moe stack layer M=2048", sample=True)
     finally:
         for j in range(3):
             for e in range(L.s["n_experts"]):
