@@ -134,6 +134,21 @@ atsi_status atsi_linear(atsi_ctx* ctx, atsi_tid w, const void* x_f16, int64_t M,
 atsi_status atsi_ffn_swiglu(atsi_ctx* ctx, atsi_tid gate, atsi_tid up, atsi_tid down,
                             const void* x_f16, int64_t M, void* y_f16);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * SwiGLU feed-forward block as atsi_ffn_swiglu, but its M x I fp16
+ * intermediate lives in a static device array of the library (16 MiB, one per
+ * GPU, held until the process ends) instead of the workspace's scratch
+ * region, and no call it makes allocates.  M * I * 2 must not exceed
+ * 16 MiB (ATSI_E_WORKSPACE otherwise).  Large prefill chunks whose down
+ * projection atsi_ffn_swiglu would split along K (fp32 partial sums in the
+ * workspace) run it unsplit here.  Every call on one GPU, from any context,
+ * uses that GPU's one array: calls that overlap in time on one GPU race.
+ * Host-resident tensors still stream through the context's temporary
+ * buffers.  Same arguments, layouts and errors as atsi_ffn_swiglu. */
+atsi_status atsi_ffn_swiglu_noalloc(atsi_ctx* ctx, atsi_tid gate, atsi_tid up, atsi_tid down,
+                                    const void* x_f16, int64_t M, void* y_f16);
+
 /* RMS normalisation with unit gain (the normalisation between the layers of
  * the pre-norm models of Sec. 5.1; the paper places only weight tensors, so
  * this glue always runs on the GPU): y[t] = x[t] / sqrt(mean_k x[t][k]^2 + eps)

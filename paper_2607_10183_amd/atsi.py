@@ -85,6 +85,8 @@ _SIGS = {
     "atsi_set_placement": ([_P, _P, ctypes.c_int32], ctypes.c_int),
     "atsi_linear": ([_P, ctypes.c_int32, _P, ctypes.c_int64, _P], ctypes.c_int),
     "atsi_ffn_swiglu": ([_P, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _P, ctypes.c_int64, _P], ctypes.c_int),
+    "atsi_ffn_swiglu_noalloc": ([_P, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _P, ctypes.c_int64, _P],
+                                ctypes.c_int),
     "atsi_swiglu_gate_up": ([_P, ctypes.c_int32, ctypes.c_int32, _P, ctypes.c_int64, _P], ctypes.c_int),
     "atsi_rmsnorm": ([_P, _P, ctypes.c_int64, ctypes.c_int64, ctypes.c_float, _P], ctypes.c_int),
     "atsi_decoder_layer": ([_P, ctypes.POINTER(atsi_dense_layer), _P, ctypes.c_int64, _P, _P,
@@ -166,6 +168,10 @@ def atsi_linear(ctx: int, w: int, x: int, M: int, y: int) -> None:
 
 def atsi_ffn_swiglu(ctx: int, gate: int, up: int, down: int, x: int, M: int, y: int) -> None:
     _check(ctx, lib().atsi_ffn_swiglu(ctx, gate, up, down, x, M, y))
+
+
+def atsi_ffn_swiglu_noalloc(ctx: int, gate: int, up: int, down: int, x: int, M: int, y: int) -> None:
+    _check(ctx, lib().atsi_ffn_swiglu_noalloc(ctx, gate, up, down, x, M, y))
 
 
 def atsi_rmsnorm(ctx: int, x: int, M: int, H: int, eps: float, y: int) -> None:

@@ -21,6 +21,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -81,6 +82,38 @@ struct Slot {
 
 thread_local std::string g_create_error;
 
+// Scratch of the allocation-free SwiGLU entry point (atsi_ffn_swiglu_noalloc):
+// a file-scope device array, so each GPU the library runs on holds one copy
+// until the process ends.  Host code never uses the array's name as an
+// address: atsi_create looks up each device's copy once, with that device
+// current, and calls pass that address to the kernels.  Calls on one GPU
+// share the array (and see the last call's contents); overlapping calls on
+// one GPU race.
+constexpr size_t kStaticScratchBytes = 16u << 20;
+__device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+char* g_scratch_ptr[kMaxDevices] = {};
+
+// The device address of this GPU's scratch array (device current), or null
+// with *e set.
+char* device_scratch(int device, hipError_t* e) {
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  *e = hipSuccess;
+  if (device < 0 || device >= kMaxDevices) {
+    *e = hipErrorInvalidDevice;
+    return nullptr;
+  }
+  if (!g_scratch_ptr[device]) {
+    void* p = nullptr;
+    *e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (*e != hipSuccess) return nullptr;
+    g_scratch_ptr[device] = static_cast<char*>(p);
+  }
+  return g_scratch_ptr[device];
+}
+
 }  // namespace
 
 namespace atsi {
@@ -122,6 +155,7 @@ struct atsi_ctx {
   bool fused_layer = false;       // batch-1 decode layers take the single persistent launch
   uint32_t debug = 0;             // ATSI_DEBUG_* flags (atsi_set_debug)
   bool zero_copy = false;         // decode experts on host are read in place (atsi_set_zero_copy)
+  char* static_scratch = nullptr;  // this device's copy of the allocation-free entry point's scratch array
   hipStream_t ts2 = nullptr;      // the caller's second transfer stream, or null: copies alternate between ts and ts2
   unsigned copy_turn = 0;
   uint64_t copy_rec = 0;          // copies issued (numbers the ready records)
@@ -607,7 +641,7 @@ atsi_status get_table(atsi_ctx* c, const atsi_moe* m, atsi_ctx::MoeTable** out) 
 
 // Acquire the tensors of a fused launch (segment order; SwiGLU: gate, up),
 // launch the GEMV (M <= 4) or the GEMM, release the slots.
-atsi_status run_op(atsi_ctx* c, LinOp& op, const atsi_tid* tids, int ntids) {
+atsi_status run_op(atsi_ctx* c, LinOp& op, const atsi_tid* tids, int ntids, bool workspace_scratch = true) {
   std::vector<int> held;
   for (int i = 0; i < ntids; ++i) {
     QView v;
@@ -626,6 +660,7 @@ atsi_status run_op(atsi_ctx* c, LinOp& op, const atsi_tid* tids, int ntids) {
   // which nothing else uses until its reduction has run on the stream.
   int wide = (op.norm && !c->row_inv) ? 0 : gemm_wide_splits(op);
   float* part = nullptr;
+  if (wide > 1 && !workspace_scratch) wide = 0;  // no partial sums outside the workspace
   if (wide > 1) {
     const size_t at = align_up(c->scratch_top), need = gemm_wide_part_bytes(op, wide);
     if (at + need <= c->table_floor)
@@ -936,6 +971,11 @@ atsi_status atsi_create(int device, void* compute_stream, void* transfer_stream,
   c->n_slots = n_slots;
   c->ts2 = (hipStream_t)transfer_stream2;
   c->pinned = host_counts;
+  c->static_scratch = device_scratch(device, &e);
+  if (!c->static_scratch) {
+    delete c;
+    return fail(nullptr, ATSI_E_HIP, "hipGetSymbolAddress of the static scratch: %s", hipGetErrorString(e));
+  }
   if (const char* f = getenv("ATSI_FUSED_DECODE_LAYER")) c->fused_layer = atoi(f) == 1;
   c->table_floor = workspace_bytes / kAlign * kAlign;
   const size_t bar_bytes = align_up((kLayerBarrierWords + 1) * sizeof(unsigned));
@@ -1111,6 +1151,32 @@ atsi_status atsi_ffn_swiglu(atsi_ctx* c, atsi_tid gate, atsi_tid up, atsi_tid do
   // down: y = h Wd
   LinOp dn = plain_op(QView{nullptr, nullptr, (int)td.K, (int)td.N}, h, (int)M, (__half*)y);
   return run_op(c, dn, &order[2], 1);
+}
+
+atsi_status atsi_ffn_swiglu_noalloc(atsi_ctx* c, atsi_tid gate, atsi_tid up, atsi_tid down, const void* x,
+                                    int64_t M, void* y) {
+  if (!c) return ATSI_E_INVALID;
+  atsi_status st;
+  if ((st = check_act(c, x, "x")) || (st = check_act(c, y, "y")) || (st = check_m(c, M)) ||
+      (st = check_tid(c, gate)) || (st = check_tid(c, up)) || (st = check_tid(c, down)))
+    return st;
+  const Tensor &tg = c->tensors[gate], &tu = c->tensors[up], &td = c->tensors[down];
+  if (tg.K != tu.K || tg.N != tu.N || td.K != tg.N || td.N != tg.K)
+    return fail(c, ATSI_E_SHAPE, "SwiGLU shapes: gate/up must be H x I and down I x H");
+  if (x == y) return fail(c, ATSI_E_INVALID, "y must not alias x");
+  const size_t need = (size_t)M * (size_t)tg.N * 2;
+  if (need > kStaticScratchBytes)
+    return fail(c, ATSI_E_WORKSPACE, "the %lld x %lld SwiGLU activation (%zu B) exceeds the %zu B static scratch",
+                (long long)M, (long long)tg.N, need, kStaticScratchBytes);
+  if ((st = enter(c))) return st;
+  __half* h = reinterpret_cast<__half*>(c->static_scratch);
+  const atsi_tid order[3] = {gate, up, down};
+  if ((st = prefetch_call(c, order, 3))) return st;
+  LinOp gu = plain_op(QView{nullptr, nullptr, (int)tg.K, (int)tg.N}, (const __half*)x, (int)M, h);
+  gu.swiglu = 1;
+  if ((st = run_op(c, gu, order, 2, false))) return st;
+  LinOp dn = plain_op(QView{nullptr, nullptr, (int)td.K, (int)td.N}, h, (int)M, (__half*)y);
+  return run_op(c, dn, &order[2], 1, false);
 }
 
 atsi_status atsi_swiglu_gate_up(atsi_ctx* c, atsi_tid gate, atsi_tid up, const void* x, int64_t M, void* h) {
