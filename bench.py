@@ -1,47 +1,59 @@
 #!/usr/bin/env python3
 """Benchmark of the block-int4 quantised-linear hot path on one MI355X.
 
-Headline workload: one 8B-shaped dense decoder layer (hidden 4096, 32 query /
-8 KV heads of 128, SwiGLU 14336; seven int4 g32 tensors, 122.7 MB), seeded
-synthetic weights and activations.
+Headline workload (the line's value): one 8B-shaped dense decoder layer
+(hidden 4096, 32 query / 8 KV heads of 128, SwiGLU 14336; seven int4 g32
+tensors, 122.7 MB), seeded synthetic weights and activations, batch-1 decode.
 
-  value             decode weight GB/s = layer bytes / decode-step time for a
-                    batch-1 pass of the whole layer (4 fused launches), all
-                    tensors HBM-resident before timing, replayed from a HIP
-                    graph over rotating copies of the layer (so the 256 MB
-                    MALL cannot serve the weights).
-  prefill           tokens/s of a 512-token pass of the same layer.
-  streamed          decode and prefill with the seeded placement mask (3 of 7
-                    tensors in pinned host memory, copied on the transfer
-                    stream); PCIe-inclusive, never the headline value.
-  moe               30B-A3B-shaped MoE layer (128 experts, top-8, capped-Zipf
-                    routing): decode and 512-token prefill, all-HBM and with
-                    51 experts on host.
+  value / steps     decode weight GB/s = layer bytes / per-layer time over
+                    exactly --steps layer calls (4 fused launches each),
+                    after --warmup untimed calls, all tensors HBM-resident
+                    before timing; the calls rotate over copies of the layer
+                    (more than the 256 MB MALL) and replay as one HIP graph.
   roofline          the dominant decode kernel, the fused SwiGLU gate/up GEMV
-                    (two 4096 x 14336 tensors, 66.1 MB per launch), against
-                    8 TB/s; roofline_prefill: the fused gate/up GEMM at 512
-                    tokens against 2.5 PFLOP/s fp16 MFMA.  Both are timed
-                    alone (atsi_swiglu_gate_up) with HIP events; their HBM
-                    traffic comes from the committed counter profile when the
-                    kernel sources still match it.
-  stacks            dense_stack: 32 such layers as a decode loop of 8
-                    sequences (hidden state renormalised after every layer),
-                    all-HBM and with 30 % of the bytes streamed; moe_stack:
-                    one 235B-A22B-shaped MoE decoder layer at decode and
-                    2048-token prefill, all-HBM and with 40 % of its experts
-                    streamed (94-layer figures = 94 x the layer).
+                    (two 4096 x 14336 tensors, 66.1 MB per launch), from HIP
+                    events on the library's compute stream over >= 100
+                    graph replays (median, p10, p90 and the mean reported);
+                    roofline_prefill: the fused gate/up GEMM at 512 tokens.
+                    traffic: FETCH_SIZE + WRITE_SIZE from the committed
+                    counter profile while the kernel sources still match it.
+  kernels           each launch of the layer alone (QKV, O, gate/up, down)
+                    at decode and prefill sizes.
+  linear4096        one 4096 x 4096 linear at batch 1 (GB/s, % of 8 TB/s)
+                    and batch 16 (tokens/s, % of the attainable roofline),
+                    rotating over 64 copies (604 MB).
+  streamed          the dense layer with the seeded 3-of-7 host mask:
+                    overlapped, serialised (no overlap) and all-HBM times;
+                    copy busy = serialised - all-HBM, exposed transfer
+                    delta = overlapped - max(copy busy, all-HBM); PCIe bytes
+                    are those the launches consumed inside the window.
+  pcie              pinned host-to-device ceiling: one 256 MiB copy, and
+                    slot-sized copies alternating over two transfer streams
+                    (the engine's pattern).
+  moe               30B-A3B-shaped MoE layer (128 experts, top-8, capped-Zipf
+                    routing): decode and 512-token prefill, all-HBM, with 51
+                    experts on host, and with zero-copy decode reads.
+  stacks            dense_stack: 32 layers, 256 decode steps of 8 sequences,
+                    all-HBM, with the seeded 30 % host mask, and with the mask
+                    the placement solver makes from measured per-tensor costs;
+                    moe_stack: all 94 235B-A22B-shaped layers (131.5 GB of
+                    device-generated weights, all in HBM) at decode and at a
+                    2048-token prefill, then with 40 % of experts streamed
+                    through one shared pinned pool.
   placement_solver  host time of the static placement solver (Alg. 1) on the
                     94-layer 235B-A22B-shaped model at 1 MiB granularity.
-  cpu_baseline      the fp64 oracle's decode step on the host cores.
+  cpu_baseline      the plain-C fp64 oracle's batch-1 decode step of the same
+                    layer on the host cores (threads = cores), and one thread.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
-       python bench.py --roofline-only   (the two roofline kernels and a
-                                          256 MiB copy; for counter runs)
+       python bench.py --roofline-only   (the roofline kernels and a 256 MiB
+                                          copy; for counter runs)
 """
 from __future__ import annotations
 
 import argparse
 import json
+import math
 import os
 import sys
 import time
@@ -60,34 +72,55 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
+def stats_us(samples_s):
+    v = np.asarray(samples_s) * 1e6
+    return {"median": round(float(np.median(v)), 3), "p10": round(float(np.percentile(v, 10)), 3),
+            "p90": round(float(np.percentile(v, 90)), 3), "mean": round(float(np.mean(v)), 3), "n": int(v.size)}
+
+
 class Timer:
     """HIP-event timing on the compute stream the library launches on."""
 
     def __init__(self, stream):
-        import torch
         self.s = stream
-        self.a = torch.cuda.Event(enable_timing=True)
-        self.b = torch.cuda.Event(enable_timing=True)
 
     def run(self, fn, n: int) -> float:
-        """Seconds per call of fn over n calls."""
+        """Seconds per call of fn over n calls (one event pair around all)."""
         import torch
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         with torch.cuda.stream(self.s):
-            self.a.record(self.s)
+            a.record(self.s)
             for _ in range(n):
                 fn()
-            self.b.record(self.s)
+            b.record(self.s)
+        b.synchronize()
+        return a.elapsed_time(b) * 1e-3 / n
+
+    def samples(self, fn, n: int, per: int = 1):
+        """n samples of (time of one fn call) / per, one event pair each."""
+        import torch
         torch.cuda.synchronize()
-        return self.a.elapsed_time(self.b) * 1e-3 / n
+        evs = []
+        with torch.cuda.stream(self.s):
+            for _ in range(n):
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record(self.s)
+                fn()
+                b.record(self.s)
+                evs.append((a, b))
+        torch.cuda.synchronize()
+        return [a.elapsed_time(b) * 1e-3 / per for a, b in evs]
 
 
-def h2d_timed(sess, timer, fn, n: int):
-    """(seconds per call, host-to-device bytes the engine copied per call) of
-    fn over n timed calls; the bytes come from the library's own counters."""
-    sess.stats(reset=True)
-    t = timer.run(fn, n)
-    return t, sess.stats(reset=True)["h2d_bytes"] / n
+def graph_of(stream, fn):
+    import torch
+    fn()  # warm (allocations, table writes) outside capture
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=stream, capture_error_mode="relaxed"):
+        fn()
+    return g
 
 
 def kernel_hash(kind: str) -> str:
@@ -117,50 +150,30 @@ def measured_traffic(key: str, kind: str):
     return rec.get("hbm_bytes_per_launch")
 
 
-def graph_of(stream, fn):
-    import torch
-    fn()  # warm (allocations, table writes) outside capture
-    torch.cuda.synchronize()
-    g = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(g, stream=stream, capture_error_mode="relaxed"):
-        fn()
-    return g
+def consumed(sess, timer, fn, n: int):
+    """(seconds per call, host-tensor bytes consumed per call, bytes copied per
+    call) of fn over n calls; consumed bytes are those of host tensors whose
+    reading launch ran inside the window (library counters)."""
+    sess.stats(reset=True)
+    t = timer.run(fn, n)
+    st = sess.stats(reset=True)
+    return t, st["host_read_bytes"] / n, st["h2d_bytes"] / n
 
 
-def main() -> int:
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--copies", type=int, default=5, help="dense-layer copies rotated to defeat the MALL")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-moe", action="store_true")
-    ap.add_argument("--no-stacks", action="store_true", help="skip the dense-stack and MoE-stack lines")
-    ap.add_argument("--cpu-seconds", type=float, default=15.0)
-    ap.add_argument("--roofline-only", action="store_true",
-                    help="run only the roofline kernels and a 256 MiB copy (for rocprofv3 --pmc)")
-    args = ap.parse_args()
-    if args.gpus != 1:
-        print("bench.py runs on exactly one GPU: the library has no multi-GPU path", file=sys.stderr)
-        return 2
+# ---------------------------------------------------------------------------- dense layer (headline)
 
+def bench_dense_layer(args, sess, timer, pcie_gbs=None):
     import torch
 
     import synth
     from synth import configs
     from paper_2607_10183_amd import atsi
-    from paper_2607_10183_amd.session import Session
 
     wl = configs.DENSE_LAYER
     shape = wl.dense
     roles = configs.ROLES
     dev = torch.device("cuda", 0)
     R = args.copies
-    sess = Session(workspace_bytes=3 << 30, n_slots=32)
-    cs = sess.cs
-    timer = Timer(cs)
-
-    # ------------------------------------------------------------ dense layer weights
     log("generating dense-layer weights")
     W = {}
     for r in roles:
@@ -174,201 +187,248 @@ def main() -> int:
     Mp = wl.prefill_m
     h1 = torch.from_numpy(synth.activations(wl.seed, 1, 1, shape.hidden)).to(dev)
     hp = torch.from_numpy(synth.activations(wl.seed, 2, Mp, shape.hidden)).to(dev)
-    cs.wait_stream(torch.cuda.current_stream())
+    sess.cs.wait_stream(torch.cuda.current_stream())
 
     # a dense layer does the same work whatever h holds, so timed calls keep
-    # updating h in place (the MoE stack below restores its inputs instead)
+    # updating h in place
     def layer(c, h, M):
         atsi.atsi_decoder_layer(sess.ctx, descs[c], h.data_ptr(), M, 0, 0, None)
 
-    # ------------------------------------------------------------ decode, HBM-resident (value)
-    decode_s = steps_timed = n_warm = per_replay = decode_gbs = 0
+    def calls(n, h, M):
+        def f():
+            for i in range(n):
+                layer(i % R, h, M)
+        return f
+
+    out = {}
+    # ---- headline: exactly W warmup and K timed layer calls
     if not args.roofline_only:
-        reps = 4
+        if args.warmup:
+            graph_of(sess.cs, calls(args.warmup, h1, 1)).replay()
+        gk = graph_of(sess.cs, calls(args.steps, h1, 1))
+        decode_s = timer.run(gk.replay, 1) / args.steps
+        # distribution over 100 replays of R calls (one per copy)
+        gr = graph_of(sess.cs, calls(R, h1, 1))
+        dist = stats_us(timer.samples(gr.replay, 100, per=R))
+        out["decode"] = {"s": decode_s, "dist": dist}
+        log(f"decode layer {decode_s * 1e6:.2f} us -> {layer_bytes / decode_s / 1e9:.1f} GB/s "
+            f"(median {dist['median']} us over 100 x {R} calls)")
 
-        def decode_round():
-            for _ in range(reps):
+    # ---- single launches: the roofline kernels and the layer's other launches
+    xs = {K: torch.from_numpy(synth.activations(wl.seed, 50 + K, Mp, K)).to(dev) for K in (4096, 14336)}
+    yb = torch.empty((Mp, 14336), dtype=torch.float16, device=dev)
+    sess.cs.wait_stream(torch.cuda.current_stream())
+
+    def launches(fn_c, rounds):
+        def f():
+            for _ in range(rounds):
                 for c in range(R):
-                    layer(c, h1, 1)
+                    fn_c(c)
+        return f
 
-        g = graph_of(cs, decode_round)
-        per_replay = reps * R
-        n_replay = max(1, args.steps // per_replay)
-        n_warm = max(1, args.warmup // per_replay)
-        timer.run(g.replay, n_warm)
-        decode_s = timer.run(g.replay, n_replay) / per_replay
-        steps_timed = n_replay * per_replay
-        decode_gbs = layer_bytes / decode_s / 1e9
-        log(f"decode layer {decode_s * 1e6:.2f} us -> {decode_gbs:.1f} GB/s ({steps_timed} steps)")
+    # decode launches: 8 rounds over the R copies per replay, so the graph's
+    # own launch cost is spread over 8 R kernels
+    def time_launch(fn_c, n_samples, rounds):
+        g = graph_of(sess.cs, launches(fn_c, rounds))
+        return timer.samples(g.replay, n_samples, per=R * rounds)
 
-    # ------------------------------------------------------------ dominant kernels
-    xs = {r: torch.from_numpy(synth.activations(wl.seed, 50 + i, Mp, shape.kn(r)[0])).to(dev)
-          for i, r in enumerate(roles)}
-    hg = torch.empty((Mp, shape.inter), dtype=torch.float16, device=dev)
-    yg = torch.empty((Mp, shape.inter), dtype=torch.float16, device=dev)
-    cs.wait_stream(torch.cuda.current_stream())
+    kern = {}
+    for M, n_samples, rounds in ((1, 100, 8), (Mp, 30, 1)):
+        kern[("gate_up", M)] = time_launch(
+            lambda c, M=M: atsi.atsi_swiglu_gate_up(sess.ctx, tids[c]["gate"], tids[c]["up"], xs[4096].data_ptr(),
+                                                    M, yb.data_ptr()), n_samples, rounds)
+        if args.roofline_only:
+            continue
+        for r in ("q", "k", "o", "down"):
+            K = shape.kn(r)[0]
+            kern[(r, M)] = time_launch(lambda c, r=r, M=M, K=K: atsi.atsi_linear(
+                sess.ctx, tids[c][r], xs[K].data_ptr(), M, yb.data_ptr()), n_samples, rounds)
     K_g, N_g = shape.kn("gate")
-
-    def gate_up_round(M, n):
-        def f():
-            for _ in range(n):
-                for c in range(R):
-                    atsi.atsi_swiglu_gate_up(sess.ctx, tids[c]["gate"], tids[c]["up"], xs["gate"].data_ptr(), M,
-                                             hg.data_ptr())
-        return f
-
-    gk = graph_of(cs, gate_up_round(1, 8))
-    t_gemv = timer.run(gk.replay, 10) / (8 * R)
     gemv_bytes = 2 * configs.qbytes(K_g, N_g)
-    gemv_gbs = gemv_bytes / t_gemv / 1e9
-    log(f"gate/up GEMV {t_gemv * 1e6:.2f} us -> {gemv_gbs:.1f} GB/s")
-    gm = graph_of(cs, gate_up_round(Mp, 1))
-    t_gemm = timer.run(gm.replay, 4) / R
     gemm_flops = 2.0 * 2.0 * Mp * K_g * N_g
-    gemm_tfs = gemm_flops / t_gemm / 1e12
-    log(f"gate/up GEMM {t_gemm * 1e6:.1f} us -> {gemm_tfs:.1f} TFLOP/s")
+    t_gemv = float(np.mean(kern[("gate_up", 1)]))
+    t_gemm = float(np.mean(kern[("gate_up", Mp)]))
+    out["roofline"] = {"bound": "hbm", "achieved": round(gemv_bytes / t_gemv / 1e9, 1), "peak": HBM_PEAK_GBS,
+                       "unit": "GB/s", "frac": round(gemv_bytes / t_gemv / 1e9 / HBM_PEAK_GBS, 4),
+                       "traffic": measured_traffic("gemv_gate_up", "q4_gemv"),
+                       "kernel": "q4_gemv1_kernel<7,true,4>: SwiGLU gate/up, two 4096x14336 tensors, batch 1",
+                       "bytes_per_launch": gemv_bytes, "avg_us": round(t_gemv * 1e6, 3),
+                       "launch_us": stats_us(kern[("gate_up", 1)])}
+    out["roofline_prefill"] = {"bound": "mfma", "achieved": round(gemm_flops / t_gemm / 1e12, 1),
+                               "peak": MFMA_F16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                               "frac": round(gemm_flops / t_gemm / 1e12 / MFMA_F16_PEAK_TFLOPS, 4),
+                               "traffic": measured_traffic("gemm_gate_up", "q4_gemm"),
+                               "kernel": "q4_gemm_wide_kernel<true,false,false>: SwiGLU gate/up, two 4096x14336 "
+                                         "tensors, 512 tokens",
+                               "flops_per_launch": gemm_flops, "avg_us": round(t_gemm * 1e6, 2),
+                               "launch_us": stats_us(kern[("gate_up", Mp)])}
+    log(f"gate/up GEMV {t_gemv * 1e6:.2f} us -> {gemv_bytes / t_gemv / 1e9:.0f} GB/s; gate/up GEMM "
+        f"{t_gemm * 1e6:.1f} us -> {gemm_flops / t_gemm / 1e12:.0f} TFLOP/s")
     if args.roofline_only:
-        # copy of known size: calibrates the FETCH_SIZE / WRITE_SIZE counters
-        src = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
-        dst = torch.empty_like(src)
-        for _ in range(3):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        sess.close()
-        print(json.dumps({"roofline_only": True, "gate_up_gemv_us": round(t_gemv * 1e6, 3),
-                          "gate_up_gemm_us": round(t_gemm * 1e6, 2), "copy_bytes": 256 << 20}), flush=True)
-        return 0
+        return out
+    per = {}
+    for (r, M), v in kern.items():
+        K, N = shape.kn("gate" if r == "gate_up" else r)
+        nt = 2 if r == "gate_up" else 1
+        d = stats_us(v)
+        if M == 1:
+            d["GBps"] = round(nt * configs.qbytes(K, N) / (d["median"] * 1e-6) / 1e9, 1)
+            d["pct_hbm_peak"] = round(100 * d["GBps"] / HBM_PEAK_GBS, 1)
+        else:
+            d["TFLOPs"] = round(nt * 2.0 * M * K * N / (d["median"] * 1e-6) / 1e12, 1)
+            d["pct_mfma_peak"] = round(100 * d["TFLOPs"] / MFMA_F16_PEAK_TFLOPS, 1)
+        per[f"{r}_M{M}"] = d
+    out["kernels"] = per
 
-    # the standalone gate GEMV / GEMM (same kernels as the q, k, v, o launches)
-    def gate_round(M, n):
-        def f():
-            for _ in range(n):
-                for c in range(R):
-                    atsi.atsi_linear(sess.ctx, tids[c]["gate"], xs["gate"].data_ptr(), M, yg.data_ptr())
-        return f
-
-    g1 = graph_of(cs, gate_round(1, 8))
-    t_gate1 = timer.run(g1.replay, 10) / (8 * R)
-    log(f"gate GEMV {t_gate1 * 1e6:.2f} us -> {configs.qbytes(K_g, N_g) / t_gate1 / 1e9:.1f} GB/s")
-
-    # ------------------------------------------------------------ prefill 512, HBM-resident
-    pf_state = {"i": 0}
-
-    def prefill_once():
-        layer(pf_state["i"] % R, hp, Mp)
-        pf_state["i"] += 1
-
-    timer.run(prefill_once, 2)
-    prefill_s = timer.run(prefill_once, max(4, min(20, args.steps // 10)))
+    # ---- prefill 512, HBM-resident
+    gp = graph_of(sess.cs, calls(R, hp, Mp))
+    pf = timer.samples(gp.replay, 10, per=R)
+    prefill_s = float(np.median(pf))
     prefill_flops = sum(2.0 * Mp * shape.kn(r)[0] * shape.kn(r)[1] for r in roles)
-    prefill_tps = Mp / prefill_s
-    log(f"prefill layer {prefill_s * 1e3:.3f} ms -> {prefill_tps:.0f} tok/s, "
+    out["prefill"] = {"s": prefill_s, "flops": prefill_flops, "dist": stats_us(pf)}
+    log(f"prefill layer {prefill_s * 1e3:.3f} ms -> {Mp / prefill_s:.0f} tok/s, "
         f"{prefill_flops / prefill_s / 1e12:.1f} TFLOP/s")
 
-    # ------------------------------------------------------------ PCIe ceiling: one large pinned H2D copy
-    pin = torch.empty(256 << 20, dtype=torch.uint8).pin_memory()
-    dst = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
-    cs.wait_stream(torch.cuda.current_stream())
-    timer.run(lambda: dst.copy_(pin, non_blocking=True), 1)
-    h2d_gbs = (256 << 20) / timer.run(lambda: dst.copy_(pin, non_blocking=True), 4) / 1e9
-    del pin, dst
-    log(f"pinned H2D ceiling {h2d_gbs:.1f} GB/s")
-
-    # ------------------------------------------------------------ streamed placement (PCIe-inclusive)
-    # Timing starts right after the placement is set (slots empty), over many
-    # calls, so copies issued ahead of the timed window cannot hide in it.
+    # ---- streamed: seeded 3-of-7 host mask, overlapped; and the same calls
+    # all-HBM (compute busy) and with every copy serialised against compute
+    # (no overlap).  Copy busy is the consumed host bytes over the measured
+    # host-to-device ceiling, so the exposed delta is the time beyond a
+    # perfect overlap at the link's rate.  Timing starts right after the
+    # placement is set (the temporary buffers then hold nothing), so every
+    # copy a timed launch consumes was issued inside the window.
     host_roles = [r for r, m in zip(roles, configs.dense_layer_host_mask()) if m]
     mask = [0] * len(sess.shapes)
     for r in host_roles:
         mask[tids[0][r]] = 1
     host_bytes = sum(configs.qbytes(*shape.kn(r)) for r in host_roles)
     order = [tids[0][r] for r in ("q", "k", "v", "o", "gate", "up", "down")]
-    sess.set_placement(mask)
-    sess.set_schedule(order)
-    n_sd = 40
-    st_dec, h2d_dec = h2d_timed(sess, timer, lambda: layer(0, h1, 1), n_sd)
-    sess.set_placement(mask)
-    sess.set_schedule(order)
-    st_pf, h2d_pf = h2d_timed(sess, timer, lambda: layer(0, hp, Mp), 10)
-    sess.set_schedule([])
-    sess.set_placement([0] * len(sess.shapes))
-    log(f"streamed decode {st_dec * 1e3:.3f} ms, prefill {st_pf * 1e3:.3f} ms ({host_roles} on host, "
-        f"{host_bytes / 1e6:.1f} MB; copied per call {h2d_dec / 1e6:.1f} / {h2d_pf / 1e6:.1f} MB) -> PCIe "
-        f"{h2d_dec / st_dec / 1e9:.1f} GB/s")
-
-    moe = None if args.no_moe else bench_moe(sess, timer, args)
-    stacks = None
-    if not args.no_stacks:
-        sess.close()
-        stacks = {"dense_stack": bench_dense_stack(timer_cls=Timer, h2d_gbs=h2d_gbs),
-                  "moe_stack": bench_moe_stack(timer_cls=Timer)}
-
-    placement = bench_placement_solver()
-    log(f"placement solver: {placement}")
-
-    cpu = None
-    if not args.no_cpu_baseline:
-        cpu = cpu_baseline(W, shape, args.cpu_seconds, layer_bytes)
-        log(f"cpu baseline {cpu}")
-
-    out = {
-        "metric": METRIC,
-        "value": round(decode_gbs, 2),
-        "unit": "GB/s",
-        "n_gpus": 1,
-        "steps": steps_timed,
-        "warmup": n_warm * per_replay,
-        "ms_per_step": round(decode_s * 1e3, 6),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "f16",
-        "data": "synthetic",
-        "config": {
-            "workload": "dense_layer: one 8B-shaped decoder layer, block-int4 g32 weights (Q 4096x4096, "
-                        "K/V 4096x1024, O 4096x4096, gate/up 4096x14336, down 14336x4096; 122.7 MB), "
-                        "RMS-norm, context-length-1 GQA, SwiGLU, residuals",
-            "decode_batch": 1, "prefill_tokens": Mp, "layer_bytes": layer_bytes,
-            "placement": "all HBM-resident for value; seeded mask (3 of 7 tensors on host) under 'streamed'",
-            "mall_rotation_copies": R,
-        },
-        "pct_hbm_peak": round(100 * decode_gbs / HBM_PEAK_GBS, 2),
-        "prefill_tokens_per_s": round(prefill_tps, 1),
-        "prefill_ms_per_step": round(prefill_s * 1e3, 4),
-        "prefill_pct_mfma": round(100 * prefill_flops / prefill_s / 1e12 / MFMA_F16_PEAK_TFLOPS, 2),
-        "roofline": {"bound": "hbm", "achieved": round(gemv_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(gemv_gbs / HBM_PEAK_GBS, 4),
-                     "traffic": measured_traffic("gemv_gate_up", "q4_gemv"),
-                     "kernel": "q4_gemv1_kernel<7,true,4>: SwiGLU gate/up, two 4096x14336 tensors, batch 1",
-                     "bytes_per_launch": gemv_bytes, "avg_us": round(t_gemv * 1e6, 3)},
-        "roofline_prefill": {"bound": "mfma", "achieved": round(gemm_tfs, 1), "peak": MFMA_F16_PEAK_TFLOPS,
-                             "unit": "TFLOP/s", "frac": round(gemm_tfs / MFMA_F16_PEAK_TFLOPS, 4),
-                             "traffic": measured_traffic("gemm_gate_up", "q4_gemm"),
-                             "kernel": "q4_gemm_wide_kernel<true,false,false>: SwiGLU gate/up, two 4096x14336 "
-                                       "tensors, 512 tokens",
-                             "flops_per_launch": gemm_flops, "avg_us": round(t_gemm * 1e6, 2)},
-        "gate_gemv_us": round(t_gate1 * 1e6, 3),
-        "pcie_h2d_ceiling_GBps": round(h2d_gbs, 2),
-        "streamed": {"host_tensors": host_roles, "host_bytes": host_bytes,
-                     "decode_ms": round(st_dec * 1e3, 4), "prefill_ms": round(st_pf * 1e3, 4),
-                     "decode_weight_GBps_pcie_inclusive": round(layer_bytes / st_dec / 1e9, 2),
-                     "decode_h2d_bytes_per_call": int(h2d_dec), "prefill_h2d_bytes_per_call": int(h2d_pf),
-                     "decode_pcie_GBps": round(h2d_dec / st_dec / 1e9, 2),
-                     "decode_pct_of_h2d_ceiling": round(100 * h2d_dec / st_dec / 1e9 / h2d_gbs, 1),
-                     "prefill_exposed_ms": round(max(0.0, st_pf - prefill_s) * 1e3, 4),
-                     "prefill_tokens_per_s": round(Mp / st_pf, 1)},
-        "moe": moe,
-        "stacks": stacks,
-        "placement_solver": placement,
-        "cpu_baseline": cpu,
-    }
-    if args.no_stacks:
-        sess.close()
-    print(json.dumps(out), flush=True)
-    return 0
+    res = {}
+    for name, h, M, n in (("decode", h1, 1, 40), ("prefill", hp, Mp, 10)):
+        f = lambda h=h, M=M: layer(0, h, M)
+        timer.run(f, 3)
+        t_hbm = timer.run(f, n)
+        sess.set_placement(mask)
+        sess.set_schedule(order)
+        timer.run(f, 2)  # warm the streamed path, then start again from empty buffers
+        sess.set_placement(mask)
+        t_ov, read_b, copied_b = consumed(sess, timer, f, n)
+        sess.set_debug(serialize=True)
+        sess.set_placement(mask)
+        t_ser, _, _ = consumed(sess, timer, f, max(3, n // 4))
+        sess.set_debug()
+        sess.set_schedule([])
+        sess.set_placement([0] * len(sess.shapes))
+        copy_busy = read_b / (pcie_gbs * 1e9)
+        delta = t_ov - max(copy_busy, t_hbm)
+        res[name] = {"ms": round(t_ov * 1e3, 4), "all_hbm_ms": round(t_hbm * 1e3, 4),
+                     "serialised_ms": round(t_ser * 1e3, 4), "copy_busy_ms": round(copy_busy * 1e3, 4),
+                     "exposed_delta_ms": round(delta * 1e3, 4),
+                     "exposed_fraction": round(max(0.0, delta) / t_ov, 4),
+                     "host_bytes_consumed_per_call": int(read_b), "h2d_bytes_issued_per_call": int(copied_b),
+                     "pcie_GBps": round(read_b / t_ov / 1e9, 2)}
+        if name == "decode":
+            res[name]["weight_GBps_pcie_inclusive"] = round(layer_bytes / t_ov / 1e9, 2)
+        else:
+            res[name]["tokens_per_s"] = round(Mp / t_ov, 1)
+    res["host_tensors"] = host_roles
+    res["host_bytes"] = host_bytes
+    out["streamed"] = res
+    log(f"streamed decode {res['decode']['ms']} ms (delta {res['decode']['exposed_delta_ms']} ms), prefill "
+        f"{res['prefill']['ms']} ms (delta {res['prefill']['exposed_delta_ms']} ms), {host_roles} on host")
+    out["W"], out["layer_bytes"], out["shape"], out["Mp"] = W, layer_bytes, shape, Mp
+    return out
 
 
-def bench_moe(sess, timer, args):
+# ---------------------------------------------------------------------------- single 4096 x 4096 linear
+
+def bench_linear4096(sess, timer):
+    import torch
+
+    from synth import configs
+    from paper_2607_10183_amd import atsi
+
+    K = N = 4096
+    copies = 64  # 64 x 9.44 MB = 604 MB, more than the 256 MB MALL
+    g = torch.Generator(device="cuda")
+    g.manual_seed(configs.LINEAR4096.seed)
+    tids = []
+    for _ in range(copies):
+        c = torch.randint(0, 256, (N, K // 2), dtype=torch.uint8, device="cuda", generator=g)
+        k = torch.randint(0, 65536, (N, K // 32), dtype=torch.int32, device="cuda", generator=g).double()
+        s = (0.005 + 0.015 * k / 65536).half().view(torch.int16)
+        tids.append(sess.register_device(c, s))
+    x = torch.randn(16, K, generator=g, device="cuda").half()
+    y = torch.empty(16, N, dtype=torch.float16, device="cuda")
+    sess.cs.wait_stream(torch.cuda.current_stream())
+    bytes_ = configs.qbytes(K, N)
+    out = {"workload": "linear4096: one 4096x4096 block-int4 g32 linear (9.44 MB), fp16 activations, "
+                       "all HBM-resident, rotating over 64 copies (604 MB)"}
+    for M in (1, 16):
+        def f(M=M):
+            for t in tids:
+                atsi.atsi_linear(sess.ctx, t, x.data_ptr(), M, y.data_ptr())
+        gr = graph_of(sess.cs, f)
+        d = stats_us(timer.samples(gr.replay, 100, per=copies))
+        t = d["mean"] * 1e-6
+        gbs = bytes_ / t / 1e9
+        if M == 1:
+            out["batch1"] = {"launch_us": d, "GBps": round(gbs, 1), "pct_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2)}
+        else:
+            flops = 2.0 * M * K * N
+            ai = flops / bytes_
+            attain = min(MFMA_F16_PEAK_TFLOPS, ai * HBM_PEAK_GBS / 1e3)
+            out["batch16"] = {"launch_us": d, "tokens_per_s": round(M / t, 1), "GBps": round(gbs, 1),
+                              "TFLOPs": round(flops / t / 1e12, 2), "attainable_TFLOPs": round(attain, 1),
+                              "pct_attainable": round(100 * flops / t / 1e12 / attain, 2)}
+    log(f"linear4096: batch 1 {out['batch1']['launch_us']['mean']} us ({out['batch1']['pct_hbm_peak']} % HBM), "
+        f"batch 16 {out['batch16']['launch_us']['mean']} us ({out['batch16']['pct_attainable']} % attainable)")
+    return out
+
+
+# ---------------------------------------------------------------------------- PCIe ceiling
+
+def bench_pcie(timer):
+    import torch
+    dev = torch.device("cuda", 0)
+    big = 256 << 20
+    pin = torch.empty(big, dtype=torch.uint8).pin_memory()
+    dst = torch.empty(big, dtype=torch.uint8, device=dev)
+    timer.run(lambda: dst.copy_(pin, non_blocking=True), 1)
+    one = big / timer.run(lambda: dst.copy_(pin, non_blocking=True), 4) / 1e9
+    # the engine's pattern: slot-sized copies (the largest dense tensor, 33 MB)
+    # alternating between two transfer streams, all issued back to back
+    chunk = 33030144
+    n = big // chunk
+    s2 = [torch.cuda.Stream(), torch.cuda.Stream()]
+    best = 0.0
+    for _ in range(3):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record(s2[0])
+        s2[1].wait_event(a)
+        for i in range(n):
+            with torch.cuda.stream(s2[i & 1]):
+                dst[i * chunk:(i + 1) * chunk].copy_(pin[i * chunk:(i + 1) * chunk], non_blocking=True)
+        s2[0].wait_stream(s2[1])
+        b.record(s2[0])
+        b.synchronize()
+        best = max(best, n * chunk / (a.elapsed_time(b) * 1e-3) / 1e9)
+    # the fixed cost of one copy: 1 MiB copies back to back on one stream
+    small = 1 << 20
+    t_small = timer.run(lambda: dst[:small].copy_(pin[:small], non_blocking=True), 64)
+    ceil = max(one, best)
+    per_copy = max(0.0, t_small - small / (ceil * 1e9))
+    del pin, dst
+    log(f"pinned H2D ceiling: one 256 MiB copy {one:.1f} GB/s, 33 MB copies on two streams {best:.1f} GB/s; "
+        f"1 MiB copies {t_small * 1e6:.1f} us each")
+    return {"one_copy_256MiB_GBps": round(one, 2), "two_streams_33MB_copies_GBps": round(best, 2),
+            "ceiling_GBps": round(ceil, 2), "copy_1MiB_us": round(t_small * 1e6, 2),
+            "per_copy_overhead_us": round(per_copy * 1e6, 2)}
+
+
+# ---------------------------------------------------------------------------- MoE layer
+
+def bench_moe(sess, timer):
     """30B-A3B-shaped MoE layer: decode (batch 1) and 512-token prefill."""
     import torch
 
@@ -403,20 +463,21 @@ def bench_moe(sess, timer, args):
     yd = torch.empty((n_tok, H), dtype=torch.float16, device=dev)
     yp = torch.empty((wl.prefill_m, H), dtype=torch.float16, device=dev)
     sess.cs.wait_stream(torch.cuda.current_stream())
-    expert_bytes = shp.expert_bytes()
+    routed_bytes = k * shp.expert_bytes()
 
     def decode_all():  # 64 different tokens, one at a time
         for t in range(n_tok):
             layer(xd[t:t + 1], yd[t:t + 1])
 
-    # routed bytes actually touched per decode token (8 distinct experts)
-    routed_bytes = k * expert_bytes
     g = graph_of(sess.cs, decode_all)
-    timer.run(g.replay, 2)
-    dec_s = timer.run(g.replay, 5) / n_tok
+    dec = timer.samples(g.replay, 20, per=n_tok)
     timer.run(lambda: layer(xp, yp), 2)
-    pf_s = timer.run(lambda: layer(xp, yp), 10)
+    pf = timer.samples(lambda: layer(xp, yp), 20)
+    dec_s, pf_s = float(np.median(dec)), float(np.median(pf))
     pf_flops = 2.0 * wl.prefill_m * k * 3 * H * I
+    # attainable at the prefill's arithmetic intensity (all 128 experts' bytes read once)
+    ai = pf_flops / (E * shp.expert_bytes())
+    attain = min(MFMA_F16_PEAK_TFLOPS, ai * HBM_PEAK_GBS / 1e3)
     log(f"moe decode {dec_s * 1e6:.1f} us/token ({routed_bytes / dec_s / 1e9:.0f} GB/s routed), "
         f"prefill {pf_s * 1e3:.3f} ms -> {wl.prefill_m / pf_s:.0f} tok/s, {pf_flops / pf_s / 1e12:.1f} TFLOP/s")
 
@@ -426,116 +487,150 @@ def bench_moe(sess, timer, args):
         for e in range(E):
             mask[tids[j][e]] = int(host_exp[e])
     sess.set_placement(mask)
-    st_dec, h2d_dec = h2d_timed(sess, timer, lambda: [layer(xd[t:t + 1], yd[t:t + 1]) for t in range(32)], 1)
-    st_dec, h2d_dec = st_dec / 32, h2d_dec / 32
-    st_pf, h2d_pf = h2d_timed(sess, timer, lambda: layer(xp, yp), 3)
-    # the same placement with the routed host experts read in place (zero-copy):
-    # nothing is copied, the PCIe bytes are those the copy path moves
+    f32 = lambda: [layer(xd[t:t + 1], yd[t:t + 1]) for t in range(32)]
+    timer.run(f32, 1)
+    st_dec, rd_dec, _ = consumed(sess, timer, f32, 2)
+    st_dec, rd_dec = st_dec / 32, rd_dec / 32
+    timer.run(lambda: layer(xp, yp), 1)
+    st_pf, rd_pf, _ = consumed(sess, timer, lambda: layer(xp, yp), 5)
     sess.set_zero_copy(True)
-    timer.run(lambda: [layer(xd[t:t + 1], yd[t:t + 1]) for t in range(32)], 1)
-    zc_dec = timer.run(lambda: [layer(xd[t:t + 1], yd[t:t + 1]) for t in range(32)], 1) / 32
+    timer.run(f32, 1)
+    zc_dec = timer.run(f32, 2) / 32
     gz = graph_of(sess.cs, decode_all)
-    timer.run(gz.replay, 1)
-    zc_graph = timer.run(gz.replay, 3) / n_tok
+    zc_graph = float(np.median(timer.samples(gz.replay, 5, per=n_tok)))
     sess.set_zero_copy(False)
     for j in range(3):
         for e in range(E):
             mask[tids[j][e]] = 0
     sess.set_placement(mask)
-    log(f"moe streamed decode {st_dec * 1e3:.3f} ms/token ({h2d_dec / 1e6:.1f} MB copied), prefill "
-        f"{st_pf * 1e3:.2f} ms ({h2d_pf / 1e6:.1f} MB copied, {h2d_pf / st_pf / 1e9:.1f} GB/s PCIe); "
+    log(f"moe streamed decode {st_dec * 1e3:.3f} ms/token ({rd_dec / 1e6:.1f} MB consumed), prefill "
+        f"{st_pf * 1e3:.2f} ms ({rd_pf / 1e6:.1f} MB, {rd_pf / st_pf / 1e9:.1f} GB/s PCIe); "
         f"zero-copy decode {zc_dec * 1e3:.3f} ms/token ({zc_graph * 1e3:.3f} graph-replayed)")
     return {"workload": "moe_layer: 128 experts of SwiGLU 768 over hidden 2048, top-8, capped Zipf(1.1) loads",
-            "decode_us_per_token": round(dec_s * 1e6, 2),
+            "decode_us_per_token": stats_us(dec),
             "decode_routed_GBps": round(routed_bytes / dec_s / 1e9, 1),
+            "prefill_us": stats_us(pf),
             "prefill_tokens_per_s": round(wl.prefill_m / pf_s, 1),
-            "prefill_ms": round(pf_s * 1e3, 4),
             "prefill_TFLOPs": round(pf_flops / pf_s / 1e12, 2),
+            "prefill_attainable_TFLOPs": round(attain, 1),
+            "prefill_pct_attainable": round(100 * pf_flops / pf_s / 1e12 / attain, 2),
             "streamed_40pct_host": {"decode_ms_per_token": round(st_dec * 1e3, 4),
-                                    "decode_h2d_bytes_per_token": int(h2d_dec),
-                                    "decode_pcie_GBps": round(h2d_dec / st_dec / 1e9, 2),
+                                    "decode_host_bytes_per_token": int(rd_dec),
+                                    "decode_pcie_GBps": round(rd_dec / st_dec / 1e9, 2),
                                     "prefill_ms": round(st_pf * 1e3, 3),
-                                    "prefill_h2d_bytes": int(h2d_pf),
-                                    "prefill_pcie_GBps": round(h2d_pf / st_pf / 1e9, 2),
+                                    "prefill_host_bytes": int(rd_pf),
+                                    "prefill_pcie_GBps": round(rd_pf / st_pf / 1e9, 2),
                                     "zero_copy_decode_ms_per_token": round(zc_dec * 1e3, 4),
                                     "zero_copy_decode_ms_per_token_graph": round(zc_graph * 1e3, 4),
-                                    "zero_copy_decode_pcie_GBps": round(h2d_dec / zc_graph / 1e9, 2)}}
+                                    "zero_copy_decode_pcie_GBps": round(rd_dec / zc_graph / 1e9, 2)}}
 
 
-def bench_dense_stack(timer_cls, h2d_gbs, steps=6):
+# ---------------------------------------------------------------------------- dense stack (32 layers)
+
+def bench_dense_stack(pcie_gbs, per_copy_s, steps=256):
     """32 8B-shaped layers, a decode loop over 8 sequences (hidden state
-    renormalised after every layer), 30 % of the int4 bytes on host by
-    seeded score, streamed each step with schedule-driven prefetch."""
+    renormalised after every layer): all-HBM, the seeded 30 % host mask, and
+    the mask the placement solver makes from measured per-tensor costs."""
     import torch
 
     import synth
     from synth import configs
+    from paper_2607_10183_amd import placement
     from paper_2607_10183_amd.session import Session
 
     wl = configs.DENSE_STACK
     shape = wl.dense
-    mask = configs.dense_stack_host_mask()
+    seeded = configs.dense_stack_host_mask()
     log("generating dense-stack weights (32 layers)")
     sess = Session(workspace_bytes=2 << 30, n_slots=24)
-    timer = timer_cls(sess.cs)
+    timer = Timer(sess.cs)
     tids = []
     for layer in range(wl.n_layers):
         t = {}
-        for j, r in enumerate(configs.ROLES):
+        for r in configs.ROLES:
             K, N = shape.kn(r)
             uid = configs.dense_uid(layer, r)
             t[r] = sess.register(synth.int4_codes(wl.seed, uid, N, K), synth.group_scales(wl.seed, uid, N, K),
-                                 hbm=True, host=bool(mask[layer, j]))
+                                 hbm=True, host=True)
         tids.append(t)
-    total_bytes = wl.n_layers * shape.layer_bytes()
-    host_bytes = sum(configs.qbytes(*shape.kn(configs.ROLES[j])) for layer in range(wl.n_layers)
-                     for j in range(len(configs.ROLES)) if mask[layer, j])
+    order = [tids[layer][r] for layer in range(wl.n_layers) for r in configs.ROLES]
+    sizes = [configs.qbytes(*sess.shapes[t]) for t in order]
+    total_bytes = sum(sizes)
     h = torch.from_numpy(synth.activations(wl.seed, 1, wl.decode_m, shape.hidden)).cuda()
     sess.cs.wait_stream(torch.cuda.current_stream())
+    m = wl.decode_m
 
     def step():
         for layer in range(wl.n_layers):
             sess.decoder_layer(tids[layer], h, shape.n_heads, shape.n_kv, shape.head_dim, 1e-6, renorm_out=True)
 
-    # all weights in HBM
-    timer.run(step, 1)
+    timer.run(step, 2)
     t_hbm = timer.run(step, steps)
-    # the seeded 30 % mask, streamed with the schedule (execution order)
-    pl = [0] * len(sess.shapes)
-    for layer in range(wl.n_layers):
-        for j, r in enumerate(configs.ROLES):
-            pl[tids[layer][r]] = int(mask[layer, j])
-    sess.set_placement(pl)
-    sess.set_schedule([tids[layer][r] for layer in range(wl.n_layers) for r in configs.ROLES])
-    timer.run(step, 1)
-    t_st, h2d_st = h2d_timed(sess, timer, step, steps)
+    # Alg. 1's profile step: per-tensor resident kernel time at M = 8 (one
+    # measurement per role: every layer has the same shapes)
+    t_role = {r: placement.kernel_seconds(sess, tids[0][r], m) for r in configs.ROLES}
+    t_gpu = [t_role[r] for _ in range(wl.n_layers) for r in configs.ROLES]
+    host_seeded = [int(seeded[layer, j]) for layer in range(wl.n_layers) for j in range(len(configs.ROLES))]
+    host_bytes_seeded = sum(s for s, hm in zip(sizes, host_seeded) if hm)
+    budget = total_bytes - host_bytes_seeded  # the same HBM budget as the seeded mask
+    t0 = time.perf_counter()
+    host_solver, objective = placement.solve(sizes, t_gpu, pcie_gbs * 1e9, budget, per_copy_s=per_copy_s)
+    solver_ms = (time.perf_counter() - t0) * 1e3
+    host_bytes_solver = sum(s for s, hm in zip(sizes, host_solver) if hm)
+
+    def run_mask(host):
+        pl = [0] * len(sess.shapes)
+        for t, hm in zip(order, host):
+            pl[t] = int(hm)
+        sess.set_placement(pl)
+        sess.set_schedule(order)
+        timer.run(step, 2)
+        sess.set_placement(pl)  # timed from empty temporary buffers
+        t, rd, _ = consumed(sess, timer, step, steps)
+        sess.set_schedule([])
+        sess.set_placement([0] * len(sess.shapes))
+        return t, rd
+
+    t_seed, rd_seed = run_mask(host_seeded)
+    t_solv, rd_solv = run_mask(host_solver)
     sess.close()
-    m = wl.decode_m
-    log(f"dense stack: decode step {t_hbm * 1e3:.2f} ms all-HBM ({total_bytes / t_hbm / 1e9:.0f} GB/s), "
-        f"{t_st * 1e3:.2f} ms with {host_bytes / 1e9:.2f} GB on host ({h2d_st / 1e9:.2f} GB copied per step, "
-        f"{h2d_st / t_st / 1e9:.1f} GB/s PCIe)")
-    return {"workload": "dense_stack: 32 8B-shaped layers, decode loop of 8 sequences, hidden state renormalised "
-                        "after every layer, 30 % of the int4 bytes on host by seeded score",
-            "layers": wl.n_layers, "sequences": m, "steps_timed": steps,
-            "total_bytes": total_bytes, "host_bytes": host_bytes,
+    roles_host = {r: sum(host_solver[i] for i in range(len(order)) if configs.ROLES[i % 7] == r)
+                  for r in configs.ROLES}
+    log(f"dense stack ({steps} steps): all-HBM {t_hbm * 1e3:.2f} ms/step, seeded 30 % mask "
+        f"{t_seed * 1e3:.2f} ms/step ({rd_seed / t_seed / 1e9:.1f} GB/s PCIe), solver mask "
+        f"{t_solv * 1e3:.2f} ms/step (host tensors per role {roles_host})")
+
+    def rec(t, rd, hb):
+        return {"ms_per_step": round(t * 1e3, 3), "tokens_per_s": round(m / t, 1),
+                "weight_GBps_pcie_inclusive": round(total_bytes / t / 1e9, 1), "host_bytes": int(hb),
+                "host_bytes_consumed_per_step": int(rd), "pcie_GBps": round(rd / t / 1e9, 2),
+                "pct_of_h2d_ceiling": round(100 * rd / t / 1e9 / pcie_gbs, 1)}
+    return {"workload": "dense_stack: 32 8B-shaped layers, decode loop of 8 sequences (M = 8 per step), hidden "
+                        "state renormalised after every layer",
+            "layers": wl.n_layers, "sequences": m, "steps_timed": steps, "total_bytes": total_bytes,
             "all_hbm": {"ms_per_step": round(t_hbm * 1e3, 3), "tokens_per_s": round(m / t_hbm, 1),
                         "weight_GBps": round(total_bytes / t_hbm / 1e9, 1)},
-            "streamed": {"ms_per_step": round(t_st * 1e3, 3), "tokens_per_s": round(m / t_st, 1),
-                         "weight_GBps_pcie_inclusive": round(total_bytes / t_st / 1e9, 1),
-                         "h2d_bytes_per_step": int(h2d_st),
-                         "pcie_GBps": round(h2d_st / t_st / 1e9, 2),
-                         "pct_of_h2d_ceiling": round(100 * h2d_st / t_st / 1e9 / h2d_gbs, 1),
-                         "tokens_per_s_256_steps": round(m / t_st, 1)}}
+            "seeded_30pct_mask": rec(t_seed, rd_seed, host_bytes_seeded),
+            "solver_mask": dict(rec(t_solv, rd_solv, host_bytes_solver),
+                                resident_kernel_us_per_role={r: round(v * 1e6, 2) for r, v in t_role.items()},
+                                host_tensors_per_role=roles_host, objective_s=round(objective, 6),
+                                solver_host_ms=round(solver_ms, 2),
+                                inputs="r_i = s_i / measured H2D ceiling + measured per-copy cost - measured "
+                                       "resident kernel time at M = 8; c_i = 0; budget = the seeded mask's HBM "
+                                       "bytes")}
 
 
-def bench_moe_stack(timer_cls):
-    """One 235B-A22B-shaped layer (attention 64 / 4 heads of 128 over hidden
-    4096, 128 experts of SwiGLU 1536, top-8), timed at decode (batch 1) and
-    prefill (2048 tokens), all-HBM and with 40 % of its experts on host;
-    the 94-layer figures are 94 x one layer."""
+# ---------------------------------------------------------------------------- 94-layer MoE stack
+
+def bench_moe_stack(pcie_gbs):
+    """All 94 235B-A22B-shaped layers (attention 64 / 4 heads of 128 over
+    hidden 4096, 128 experts of SwiGLU 1536, top-8; hidden state
+    renormalised between layers): 131.5 GB of weights generated on the device
+    from a seeded generator, all HBM-resident; then
+    40 % of each layer's experts streamed, their host copies all pointing
+    into one shared pinned pool of one layer's streamed experts."""
     import torch
 
-    import synth
     from synth import configs
     from synth.calibrate_router_bias import load_bias
     from paper_2607_10183_amd.session import MoEDecoderLayer, Session
@@ -543,96 +638,130 @@ def bench_moe_stack(timer_cls):
     wl = configs.MOE_STACK
     ds, ms = wl.dense, wl.moe
     H, E, I, k = ms.hidden, ms.n_experts, ms.inter, ms.top_k
-    layer = 0
-    log("generating one MoE-stack layer")
-    sess = Session(workspace_bytes=3 << 30, n_slots=24)
-    timer = timer_cls(sess.cs)
-    a = {r: sess.register(synth.int4_codes(wl.seed, configs.dense_uid(layer, r), ds.kn(r)[1], ds.kn(r)[0]),
-                          synth.group_scales(wl.seed, configs.dense_uid(layer, r), ds.kn(r)[1], ds.kn(r)[0]))
-         for r in ("q", "k", "v", "o")}
-    tids = [[], [], []]
-    for e in range(E):
-        group = []
-        for p, (n, kk) in zip(("gate", "up", "down"), ((I, H), (I, H), (H, I))):
-            uid = configs.expert_uid(layer, e, p)
-            group.append((synth.int4_codes(wl.seed, uid, n, kk), synth.group_scales(wl.seed, uid, n, kk)))
-        for j, t in enumerate(sess.register_group(group, hbm=True, host=True)):
-            tids[j].append(t)
-    wr = torch.from_numpy(synth.router_weights(wl.seed, configs.router_uid(layer), H, E)).cuda()
-    moe = sess.moe_layer(wr, *tids, top_k=k, router_bias=torch.from_numpy(load_bias()).cuda())
-    L = MoEDecoderLayer(moe, a["q"], a["k"], a["v"], a["o"], ds.n_heads, ds.n_kv, ds.head_dim, 1e-6)
-    # The layer updates h in place (h += attention + MoE) and routing depends
-    # on h, so every timed call starts from the same hidden states: restored
-    # from a pristine copy inside the call, with the copy's own time taken off.
-    hd0 = torch.from_numpy(synth.activations(wl.seed, 1, 32, H)).cuda()
-    hp0 = torch.from_numpy(synth.activations(wl.seed, 2, wl.prefill_m, H)).cuda()
-    hd, hp = hd0.clone(), hp0.clone()
-    sess.cs.wait_stream(torch.cuda.current_stream())
+    L = wl.n_layers
+    g = torch.Generator(device="cuda")
+    g.manual_seed(wl.seed)
+
+    def qt(N, K):
+        c = torch.randint(0, 256, (N, K // 2), dtype=torch.uint8, device="cuda", generator=g)
+        kk = torch.randint(0, 65536, (N, K // 32), dtype=torch.int32, device="cuda", generator=g).double()
+        return c, (0.005 + 0.015 * kk / 65536).half().view(torch.int16)
+
+    bias = torch.from_numpy(load_bias()).cuda()
     attn_bytes = sum(configs.qbytes(*ds.kn(r)) for r in ("q", "k", "v", "o"))
     expert_bytes = 3 * configs.qbytes(H, I)
-    t_cd = timer.run(lambda: hd.copy_(hd0), 20)
-    t_cp = timer.run(lambda: hp.copy_(hp0), 20)
+    model_bytes = L * (attn_bytes + E * expert_bytes)
+    hd0 = torch.randn(32, H, generator=g, device="cuda").half()
+    hp0 = torch.randn(wl.prefill_m, H, generator=g, device="cuda").half()
+    results = {}
+    for mode in ("all_hbm", "streamed_40pct_experts"):
+        streamed = mode != "all_hbm"
+        log(f"generating the 94-layer MoE stack ({mode})")
+        sess = Session(workspace_bytes=4 << 30, n_slots=24)
+        timer = Timer(sess.cs)
+        pool = None
+        if streamed:
+            n_host = int(0.4 * E)
+            pool = torch.empty(n_host * expert_bytes, dtype=torch.uint8).pin_memory()
+            rng = np.random.default_rng(wl.seed)
+            pool.numpy()[:] = rng.integers(0, 256, pool.numel(), dtype=np.uint8)
+            # scales in the pool: bytes 0x20-0x23 give fp16 scales of about 0.006-0.009
+            for j0 in range(n_host):
+                off = j0 * expert_bytes
+                for (n, kk) in ((I, H), (I, H), (H, I)):
+                    cb, sb = n * kk // 2, n * (kk // 32) * 2
+                    pool.numpy()[off + cb + 1:off + cb + sb:2] = 0x20
+                    off += cb + sb
+        layers = []
+        mask = []
+        for layer in range(L):
+            a = {}
+            for r in ("q", "k", "v", "o"):
+                K, N = ds.kn(r)
+                a[r] = sess.register_device(*qt(N, K))
+                mask.append(0)
+            host_exp = configs.moe_host_experts(frac=0.40, seed=wl.seed, layer=layer) if streamed else np.zeros(E)
+            tids = [[], [], []]
+            slot = 0
+            for e in range(E):
+                if host_exp[e]:
+                    # an expert's gate, up and down back to back in the shared pool
+                    base = pool.data_ptr() + slot * expert_bytes
+                    slot += 1
+                    off = 0
+                    for j, (n, kk) in enumerate(((I, H), (I, H), (H, I))):
+                        cb, sb = n * kk // 2, n * (kk // 32) * 2
+                        tids[j].append(sess.register_host(kk, n, base + off, base + off + cb))
+                        off += cb + sb
+                        mask.append(1)
+                else:
+                    for j, (n, kk) in enumerate(((I, H), (I, H), (H, I))):
+                        tids[j].append(sess.register_device(*qt(n, kk)))
+                        mask.append(0)
+            wr = (torch.randn(H, E, generator=g, device="cuda") / math.sqrt(H)).half()
+            moe = sess.moe_layer(wr, *tids, top_k=k, router_bias=bias)
+            layers.append(MoEDecoderLayer(moe, a["q"], a["k"], a["v"], a["o"], ds.n_heads, ds.n_kv, ds.head_dim,
+                                          1e-6))
+        sess.placement = mask
+        hd, hp = hd0.clone(), hp0.clone()
+        torch.cuda.synchronize()
+        sess.cs.wait_stream(torch.cuda.current_stream())
 
-    def dec():
-        hd.copy_(hd0)
-        for t in range(32):
-            L(hd[t:t + 1])
+        # the hidden state is renormalised between layers (as in the dense
+        # stack): random-weight residual streams would otherwise leave the fp16
+        # range within the 94 layers and degenerate the routing
+        def dec():  # one token through all 94 layers
+            hd[:1].copy_(hd0[:1])
+            for lay in layers:
+                lay(hd[:1])
+                sess.rmsnorm(hd[:1], 1e-6, hd[:1])
 
-    def pf():
-        hp.copy_(hp0)
-        L(hp)
+        def pf():  # a 2048-token chunk through all 94 layers
+            hp.copy_(hp0)
+            for lay in layers:
+                lay(hp)
+                sess.rmsnorm(hp, 1e-6, hp)
 
-    def measure():
-        timer.run(dec, 1)
-        t_dec, b_dec = h2d_timed(sess, timer, dec, 2)
+        if streamed:  # the copy path waits on the host for each layer's routing counts
+            timer.run(dec, 1)
+            t_dec, rd_dec, _ = consumed(sess, timer, dec, 3)
+        else:  # enqueue-only: one HIP graph of the 94 layers, so host time stays out
+            gd = graph_of(sess.cs, dec)
+            gd.replay()
+            t_dec, rd_dec = float(np.median(timer.samples(gd.replay, 10))), 0
         timer.run(pf, 1)
-        t_pf, b_pf = h2d_timed(sess, timer, pf, 3)
-        return (t_dec - t_cd) / 32, t_pf - t_cp, b_dec / 32, b_pf
+        t_pf, rd_pf, _ = consumed(sess, timer, pf, 2 if streamed else 3)
+        r = {"decode_ms_per_token": round(t_dec * 1e3, 3), "decode_tokens_per_s": round(1.0 / t_dec, 2),
+             "prefill_ms_2048_tokens": round(t_pf * 1e3, 2), "prefill_tokens_per_s": round(wl.prefill_m / t_pf, 1)}
+        if streamed:
+            r.update({"decode_host_bytes_per_token": int(rd_dec), "decode_pcie_GBps": round(rd_dec / t_dec / 1e9, 2),
+                      "prefill_host_bytes": int(rd_pf), "prefill_pcie_GBps": round(rd_pf / t_pf / 1e9, 2),
+                      "pct_of_h2d_ceiling_prefill": round(100 * rd_pf / t_pf / 1e9 / pcie_gbs, 1),
+                      "pinned_pool_bytes": int(pool.numel())})
+            sess.set_zero_copy(True)
+            timer.run(dec, 1)
+            t_zc = timer.run(dec, 3)
+            sess.set_zero_copy(False)
+            r["zero_copy_decode_ms_per_token"] = round(t_zc * 1e3, 3)
+        else:
+            dense_flops = 2.0 * wl.prefill_m * attn_bytes * 16 / 9
+            expert_flops = 2.0 * wl.prefill_m * k * expert_bytes * 16 / 9
+            r["prefill_TFLOPs"] = round(L * (dense_flops + expert_flops) / t_pf / 1e12, 1)
+            r["prefill_pct_mfma_peak"] = round(100 * r["prefill_TFLOPs"] / MFMA_F16_PEAK_TFLOPS, 2)
+            r["decode_weight_GBps_routed"] = round(L * (attn_bytes + k * expert_bytes) / t_dec / 1e9, 1)
+        results[mode] = r
+        log(f"moe stack {mode}: {r}")
+        sess.close()
+        del layers, sess, pool
+        torch.cuda.empty_cache()
+    return {"workload": "moe_stack: 94 235B-A22B-shaped layers (attention 64/4 heads of 128, hidden 4096, 128 experts "
+                        "of SwiGLU 1536, top-8, capped-Zipf routing bias), 131.5 GB of block-int4 weights generated "
+                        "on the device from a seeded generator; the streamed run shares one pinned pool of one "
+                        "layer's 51 host experts among all 94 layers' host copies",
+            "layers": L, "model_bytes": model_bytes, **results}
 
-    d_hbm, p_hbm, _, _ = measure()
-    host_exp = configs.moe_host_experts(frac=0.40, seed=wl.seed, layer=layer)
-    pl = list(sess.placement)
-    for j in range(3):
-        for e in range(E):
-            pl[tids[j][e]] = int(host_exp[e])
-    sess.set_placement(pl)
-    d_st, p_st, d_h2d, p_h2d = measure()
-    sess.set_zero_copy(True)
-    timer.run(dec, 1)
-    d_zc = (timer.run(dec, 2) - t_cd) / 32
-    sess.set_zero_copy(False)
-    # experts the prefill actually routes to, and how many of those are on host
-    dbg = L(hp0.clone(), debug=True)
-    sess.sync()
-    counts = dbg["counts"].cpu().numpy()
-    n_act = int((counts > 0).sum())
-    n_host_act = int(((counts > 0) & (host_exp > 0)).sum())
-    sess.close()
-    pf_flops = 2.0 * wl.prefill_m * (attn_bytes * 16 / 9 + k * expert_bytes * 16 / 9)  # 2 M K N per weight
-    log(f"moe stack layer: decode {d_hbm * 1e3:.3f} ms ({d_st * 1e3:.3f} streamed), prefill {p_hbm * 1e3:.2f} ms "
-        f"({p_st * 1e3:.2f} streamed, {n_host_act} of {n_act} active experts on host, {p_h2d / 1e6:.0f} MB "
-        f"copied -> {p_h2d / p_st / 1e9:.1f} GB/s PCIe); decode copies {d_h2d / 1e6:.1f} MB/token "
-        f"({d_zc * 1e3:.3f} ms with zero-copy reads); "
-        f"x94: {94 * d_hbm * 1e3:.1f} ms/token all-HBM")
-    return {"workload": "moe_stack: one 235B-A22B-shaped layer (attention 64/4 heads of 128, hidden 4096, "
-                        "128 experts of SwiGLU 1536, top-8, capped-Zipf routing); 94-layer figures are 94 x the layer",
-            "all_hbm": {"decode_ms_per_layer": round(d_hbm * 1e3, 4), "prefill_ms_per_layer": round(p_hbm * 1e3, 3),
-                        "decode_tokens_per_s_94_layers": round(1.0 / (94 * d_hbm), 2),
-                        "prefill_tokens_per_s_94_layers": round(wl.prefill_m / (94 * p_hbm), 1),
-                        "prefill_TFLOPs": round(pf_flops / p_hbm / 1e12, 1)},
-            "prefill_active_experts": n_act, "prefill_active_host_experts": n_host_act,
-            "streamed_40pct_experts": {"decode_ms_per_layer": round(d_st * 1e3, 4),
-                                       "prefill_ms_per_layer": round(p_st * 1e3, 3),
-                                       "decode_h2d_bytes_per_layer": int(d_h2d),
-                                       "decode_pcie_GBps": round(d_h2d / d_st / 1e9, 2),
-                                       "prefill_h2d_bytes_per_layer": int(p_h2d),
-                                       "prefill_pcie_GBps": round(p_h2d / p_st / 1e9, 2),
-                                       "decode_tokens_per_s_94_layers": round(1.0 / (94 * d_st), 2),
-                                       "prefill_tokens_per_s_94_layers": round(wl.prefill_m / (94 * p_st), 1),
-                                       "zero_copy_decode_ms_per_layer": round(d_zc * 1e3, 4),
-                                       "zero_copy_decode_pcie_GBps": round(d_h2d / d_zc / 1e9, 2),
-                                       "zero_copy_decode_tokens_per_s_94_layers": round(1.0 / (94 * d_zc), 2)}}
 
+# ---------------------------------------------------------------------------- host-side pieces
 
 def bench_placement_solver(reps: int = 3):
     """Host time of atsi_solve_placement on the 94-layer 235B-A22B-shaped
@@ -657,39 +786,166 @@ def bench_placement_solver(reps: int = 3):
     units = int((budget - sum(x for x, e in zip(s, expert) if not e)) // (1 << 20))
     return {"workload": "static placement of the 94-layer 235B-A22B-shaped model (752 tensors), 1 MiB "
                         "granularity, budget half the model", "tensors": len(s), "budget_units": units,
-            "gpu_resident_bytes": int(sum(x for x, g in zip(s, b) if g)), "objective_s": round(obj, 6),
+            "gpu_resident_bytes": int(sum(x for x, gg in zip(s, b) if gg)), "objective_s": round(obj, 6),
             "host_ms": round(best * 1e3, 2)}
 
 
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(W, shape, budget_s, layer_bytes):
-    """The fp64 oracle's decode step of the same layer (batch 1), timed on the host."""
+    """The oracle's batch-1 decode step of the same layer on the host cores:
+    the plain-C fp64 linear (threads = cores) for the seven projections, the
+    oracle's numpy glue around them; and one thread on the gate tensor, scaled
+    to the layer's bytes."""
     import oracle
     import synth
-    try:
-        from threadpoolctl import threadpool_info
-        blas = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] or [1])
-    except Exception:  # pragma: no cover
-        blas = 1
-    h = synth.activations(1002, 1, 1, shape.hidden)
+    from oracle import c_linear
+    cores = len(os.sched_getaffinity(0))
+    h = synth.activations(1002, 1, 1, shape.hidden).astype(np.float64)
+
+    def step():
+        a, _ = oracle.rmsnorm(h, 1e-6)
+        lin = lambda x, r: c_linear.linear(x, *W[r], threads=cores)
+        lin(a, "q"), lin(a, "k")
+        v = lin(a, "v")
+        h1 = h + lin(oracle.gqa_stub(v, shape.n_heads, shape.n_kv, shape.head_dim), "o")
+        b, _ = oracle.rmsnorm(h1, 1e-6)
+        act = oracle.silu(lin(b, "gate")) * lin(b, "up")
+        return h1 + lin(act, "down")
+
     n = 0
     t0 = time.perf_counter()
     while True:
-        oracle.decoder_layer(h, W, shape.n_heads, shape.n_kv, shape.head_dim, 1e-6)
+        step()
         n += 1
         if time.perf_counter() - t0 >= budget_s:
             break
     dt = (time.perf_counter() - t0) / n
-    return {"value": round(layer_bytes / dt / 1e9, 4), "unit": "GB/s", "cores": int(blas), "kind": "oracle",
-            "sample": f"{n} batch-1 decode steps of the dense layer (fp64 dequant + BLAS matmul), "
-                      f"{dt:.2f} s per step",
-            "host_cpus": len(os.sched_getaffinity(0))}
+    t1 = time.perf_counter()
+    c_linear.linear(h, *W["gate"], threads=1)
+    t_one = (time.perf_counter() - t1) * layer_bytes / (W["gate"][0].nbytes + W["gate"][1].nbytes)
+    return {"value": round(layer_bytes / dt / 1e9, 4), "unit": "GB/s", "cores": cores, "kind": "oracle",
+            "sample": f"{n} batch-1 decode steps of the dense layer, plain-C fp64 linear on {cores} threads "
+                      f"({dt:.2f} s per step)",
+            "single_thread_GBps": round(layer_bytes / t_one / 1e9, 4),
+            "single_thread_s_per_step": round(t_one, 2), "cpu_model": cpu_model()}
+
+
+# ---------------------------------------------------------------------------- main
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--copies", type=int, default=5, help="dense-layer copies rotated to defeat the MALL")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-moe", action="store_true")
+    ap.add_argument("--no-stacks", action="store_true", help="skip the dense-stack and MoE-stack lines")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--roofline-only", action="store_true",
+                    help="run only the roofline kernels and a 256 MiB copy (for rocprofv3 --pmc)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path, so --gpus must be 1", file=sys.stderr)
+        return 2
+    if args.steps < 1 or args.warmup < 0:
+        print("--steps must be >= 1 and --warmup >= 0", file=sys.stderr)
+        return 2
+
+    import torch
+
+    from paper_2607_10183_amd.session import Session
+
+    sess = Session(workspace_bytes=3 << 30, n_slots=32)
+    timer = Timer(sess.cs)
+    pcie = None if args.roofline_only else bench_pcie(timer)
+    dl = bench_dense_layer(args, sess, timer, pcie and pcie["ceiling_GBps"])
+    if args.roofline_only:
+        # copy of known size: calibrates the FETCH_SIZE / WRITE_SIZE counters
+        src = torch.empty(256 << 20, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        sess.close()
+        print(json.dumps({"roofline_only": True, "roofline": dl["roofline"], "roofline_prefill": dl["roofline_prefill"],
+                          "copy_bytes": 256 << 20}), flush=True)
+        return 0
+    lin = bench_linear4096(sess, timer)
+    moe = None if args.no_moe else bench_moe(sess, timer)
+    sess.close()
+    del sess
+    torch.cuda.empty_cache()
+    stacks = None
+    if not args.no_stacks:
+        stacks = {"dense_stack": bench_dense_stack(pcie["ceiling_GBps"], pcie["per_copy_overhead_us"] * 1e-6),
+                  "moe_stack": bench_moe_stack(pcie["ceiling_GBps"])}
+    placement = bench_placement_solver()
+    log(f"placement solver: {placement}")
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(dl["W"], dl["shape"], args.cpu_seconds, dl["layer_bytes"])
+        log(f"cpu baseline {cpu}")
+
+    decode_s = dl["decode"]["s"]
+    layer_bytes, Mp = dl["layer_bytes"], dl["Mp"]
+    pf = dl["prefill"]
+    out = {
+        "metric": METRIC,
+        "value": round(layer_bytes / decode_s / 1e9, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(decode_s * 1e3, 6),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16",
+        "data": "synthetic",
+        "config": {
+            "workload": "dense_layer: one 8B-shaped decoder layer, block-int4 g32 weights (Q 4096x4096, "
+                        "K/V 4096x1024, O 4096x4096, gate/up 4096x14336, down 14336x4096; 122.7 MB), "
+                        "RMS-norm, context-length-1 GQA, SwiGLU, residuals",
+            "decode_batch": 1, "prefill_tokens": Mp, "layer_bytes": layer_bytes,
+            "placement": "all HBM-resident for value; seeded mask (3 of 7 tensors on host) under 'streamed'",
+            "mall_rotation_copies": args.copies,
+        },
+        "pct_hbm_peak": round(100 * layer_bytes / decode_s / 1e9 / HBM_PEAK_GBS, 2),
+        "decode_layer_us": dl["decode"]["dist"],
+        "prefill_tokens_per_s": round(Mp / pf["s"], 1),
+        "prefill_ms_per_step": round(pf["s"] * 1e3, 4),
+        "prefill_pct_mfma": round(100 * pf["flops"] / pf["s"] / 1e12 / MFMA_F16_PEAK_TFLOPS, 2),
+        "prefill_layer_us": pf["dist"],
+        "roofline": dl["roofline"],
+        "roofline_prefill": dl["roofline_prefill"],
+        "kernels": dl["kernels"],
+        "linear4096": lin,
+        "pcie": pcie,
+        "streamed": dl["streamed"],
+        "moe": moe,
+        "stacks": stacks,
+        "placement_solver": placement,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+    return 0
 
 
 def summarize(trace_dir: str, fetch_dir: str, write_dir: str, commands: dict) -> None:
-    """Write profiles/kernels_dense_layer_moe_layer.md (per-kernel durations of a
-    full bench run) and profiles/traffic.json + .md (HBM bytes per launch of
-    the two roofline kernels from FETCH_SIZE / WRITE_SIZE, scaled by what the
-    same counters read for a 256 MiB device copy) from rocprofv3 CSV output."""
+    """Write profiles/kernels_bench.md (per-kernel durations of a full bench
+    run) and profiles/traffic.json + .md (HBM bytes per launch of the two
+    roofline kernels from FETCH_SIZE / WRITE_SIZE, scaled by what the same
+    counters read for a 256 MiB device copy) from rocprofv3 CSV output."""
     import csv
     import glob
 
@@ -701,14 +957,14 @@ def summarize(trace_dir: str, fetch_dir: str, write_dir: str, commands: dict) ->
 
     prof = os.path.join(ROOT, "profiles")
     stats = list(csv.DictReader(open(one(os.path.join(trace_dir, "*kernel_stats.csv")))))
-    lines = ["# Kernel durations: dense_layer + moe_layer bench run", "",
+    lines = ["# Kernel durations: full bench run (dense layer, linear4096, MoE layer, stacks)", "",
              "Command (from the repository root, on one MI355X):", "",
              "    " + commands["trace"], "",
              "| kernel | calls | avg us | min us | max us | share |", "|---|---|---|---|---|---|"]
-    for r in sorted(stats, key=lambda r: -float(r["TotalDurationNs"]))[:24]:
+    for r in sorted(stats, key=lambda r: -float(r["TotalDurationNs"]))[:30]:
         lines.append(f"| `{r['Name'][:110]}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
                      f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} | {float(r['Percentage']):.1f}% |")
-    with open(os.path.join(prof, "kernels_dense_layer_moe_layer.md"), "w") as fh:
+    with open(os.path.join(prof, "kernels_bench.md"), "w") as fh:
         fh.write("\n".join(lines) + "\n")
 
     def counter(dirname, name):
@@ -718,10 +974,10 @@ def summarize(trace_dir: str, fetch_dir: str, write_dir: str, commands: dict) ->
                 continue
             per.setdefault(r["Kernel_Name"], {}).setdefault(r["Dispatch_Id"], 0.0)
             per[r["Kernel_Name"]][r["Dispatch_Id"]] += float(r["Counter_Value"])
-        return {k: sorted(v.values()) for k, v in per.items()}
+        return {kk: sorted(v.values()) for kk, v in per.items()}
 
     def pick(per, needle):
-        ks = [k for k in per if needle in k]
+        ks = [kk for kk in per if needle in kk]
         if not ks:
             raise KeyError(needle)
         vals = per[ks[0]]

@@ -342,6 +342,8 @@ typedef struct {
   uint64_t h2d_copies;   /* hipMemcpyAsync calls that moved them */
   uint64_t h2d_tensors;  /* host tensors copied (an expert moved as one copy counts 3) */
   uint64_t host_reads;   /* launches' reads of a host tensor, each served by a copy */
+  uint64_t host_read_bytes; /* bytes of those tensors: counted when the reading launch is enqueued, so a
+                               copy counts once its consumer is in the stream, never for prefetches alone */
 } atsi_stats;
 
 /* *out = the counters; reset != 0 then zeroes them. */

@@ -73,7 +73,7 @@ class atsi_placement_problem(ctypes.Structure):
 _P = ctypes.c_void_p
 class atsi_stats(ctypes.Structure):
     _fields_ = [("h2d_bytes", ctypes.c_uint64), ("h2d_copies", ctypes.c_uint64), ("h2d_tensors", ctypes.c_uint64),
-                ("host_reads", ctypes.c_uint64)]
+                ("host_reads", ctypes.c_uint64), ("host_read_bytes", ctypes.c_uint64)]
 
 
 _SIGS = {

@@ -550,6 +550,7 @@ atsi_status acquire(atsi_ctx* c, atsi_tid tid, QView* v, std::vector<int>& held)
   v->scales = reinterpret_cast<const uint16_t*>(s.base + t.codes_bytes());
   held.push_back(si);
   c->stats.host_reads += 1;
+  c->stats.host_read_bytes += t.bytes();
   return ATSI_OK;
 }
 

@@ -106,6 +106,14 @@ class Session:
         self.placement.append(0)
         return tid
 
+    def register_host(self, K: int, N: int, host_codes: int, host_scales: int) -> int:
+        """Register a tensor with only a pinned host copy at raw addresses (codes
+        [N][K/2] then fp16 scales [N][K/32]); the caller keeps that memory alive."""
+        tid = atsi.atsi_tensor_register(self.ctx, K, N, 0, 0, host_codes, host_scales)
+        self.shapes.append((K, N))
+        self.placement.append(1)
+        return tid
+
     def set_debug(self, poison: bool = False, serialize: bool = False) -> None:
         """Checking modes of the streaming engine (atsi_set_debug)."""
         atsi.atsi_set_debug(self.ctx, (atsi.DEBUG_POISON if poison else 0) | (atsi.DEBUG_SERIALIZE if serialize else 0))

@@ -98,3 +98,35 @@ def test_dense_stack_placement_invariance(stack):
     sess.set_schedule([])
     for o in outs[1:]:
         assert torch.equal(outs[0], o)
+
+
+def test_solver_placement_runs_bit_identical(stack):
+    """Alg. 1 end to end: per-tensor resident kernel times measured on the GPU
+    (one per role), gains r = copy time over a nominal 50 GB/s link minus that
+    time, the solver's mask for 30 % of the bytes on host; the stack runs with
+    that mask and gives the all-HBM bits."""
+    import torch
+    from paper_2607_10183_amd import placement
+    sess, W, tids = stack
+    shape = WL.dense
+    order = [tids[layer][r] for layer in range(N_LAYERS) for r in configs.ROLES]
+    sizes = [configs.qbytes(*sess.shapes[t]) for t in order]
+    t_role = {r: placement.kernel_seconds(sess, tids[0][r], WL.decode_m, reps=4) for r in configs.ROLES}
+    assert all(0 < v < 1e-3 for v in t_role.values())
+    t_gpu = [t_role[r] for _ in range(N_LAYERS) for r in configs.ROLES]
+    host, obj = placement.solve(sizes, t_gpu, 50e9, 0.7 * sum(sizes))
+    assert sum(s for s, h in zip(sizes, host) if not h) <= 0.7 * sum(sizes) + (1 << 20)
+    assert 0 < sum(host) < len(host)
+    hn = synth.activations(WL.seed, 3, WL.decode_m, shape.hidden)
+    ref = _decode(sess, tids, hn, steps=1)
+    mask = list(sess.placement)
+    for t, h in zip(order, host):
+        mask[t] = int(h)
+    sess.set_placement(mask)
+    sess.set_schedule(order)
+    try:
+        got = _decode(sess, tids, hn, steps=1)
+    finally:
+        sess.set_schedule([])
+        sess.set_placement([0] * len(mask))
+    assert torch.equal(ref, got)

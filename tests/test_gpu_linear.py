@@ -146,8 +146,12 @@ def test_placement_invariance(sess, M):
     tid = sess.register(codes, scales, hbm=True, host=True)
     y_hbm = sess.linear(tid, x)
     sess.place(tid, True)
+    sess.stats(reset=True)
     y_host = [sess.linear(tid, x) for _ in range(3)]
     sess.sync()
+    st = sess.stats(reset=True)
     sess.place(tid, False)
+    # each of the three launches consumed the tensor's bytes once
+    assert st["host_reads"] == 3 and st["host_read_bytes"] == 3 * (codes.nbytes + scales.nbytes)
     for yh in y_host:
         assert torch.equal(y_hbm, yh)
