@@ -7,9 +7,12 @@
  * (the GPU resident region, Sec. 4.2.1) or from pinned host memory (CPU
  * pinned-memory storage, Sec. 4.2.1); a host tensor is copied into a GPU
  * temporary buffer ("slot") on a transfer stream and consumed on a compute
- * stream, with events ordering the two (Sec. 4.2.2).  All compute runs on the
- * GPU: every host tensor is promoted for each use (the all-GPU runtime
- * assignment of Sec. 4.4.1), and the engine hides the copies behind compute.
+ * stream, with events ordering the two (Sec. 4.2.2).  By default every host
+ * tensor is promoted for each use (the all-GPU runtime assignment of Sec.
+ * 4.4.1) and the engine hides the copies behind compute; with a CPU backend
+ * attached (atsi_set_cpu_backend), host tensors may instead run on the host
+ * CPU (the hybrid execution of Sec. 4.3-4.4), as the runtime assignment of
+ * atsi_schedule_transfers decides.
  *
  * Weight format (the paper uses INT4 weights without fixing a layout, Sec. 5.1):
  *   codes  uint8 [N][K/2]  -- row n = output feature n; byte j of a row holds
@@ -384,6 +387,129 @@ typedef struct {
 } atsi_placement_problem;
 
 atsi_status atsi_solve_placement(const atsi_placement_problem* problem, uint8_t* on_gpu_out, double* objective_out);
+
+/* ---- Hybrid CPU-GPU execution: dynamic transfer scheduling (Sec. 4.4) ----
+ *
+ * A round runs tensors 0..n-1 in execution order.  Tensor i has a default
+ * placement b_i (on_gpu[i] = 1: GPU-resident; 0: CPU, i.e. host-placed),
+ * GPU and CPU execution times t_gpu[i], t_cpu[i], the activation-transfer
+ * (backend switch) cost c[i] at the boundary between tensors i-1 and i
+ * (c[0] unused) and the weight-transfer time w[i] (Sec. 4.4.1; for MoE
+ * experts in decode, the copy time of the activated experts).  Times are in
+ * any one unit (seconds in this library's measurements), finite and >= 0. */
+typedef struct {
+  int32_t n;
+  const uint8_t* on_gpu;
+  const double* t_gpu;
+  const double* t_cpu;
+  const double* c;
+  const double* w;
+} atsi_transfer_problem;
+
+/* Alg. 2 (Sec. 4.4.2): the runtime backend assignment rb minimising the
+ * round latency
+ *   T(rb) = sum_i t_i^{rb_i} + sum_{i>=1} c_i [rb_{i-1} != rb_i] + sum_{promoted i} delta_i,
+ *   delta_i = max(w_i - seg(j, i), 0),
+ * where a promoted tensor (b_i = CPU, rb_i = GPU) has its weights copied from
+ * the CPU-side endpoint j: the round start, or the first CPU-run tensor after
+ * the previous promotion; seg(j, i) is the default-path time strictly between
+ * j and i (execution times on the default backends plus the switches among
+ * them).  Two promoted tensors need a CPU-run tensor between them.  GPU-placed
+ * tensors always run on the GPU.  Host computation only, no context: O(n^2)
+ * time, O(n) memory.
+ * Outputs: rb_out[n] (caller-owned) = 1 where tensor i runs on the GPU;
+ * latency_out (nullable) = T(rb).  Ties go to the CPU (fewer promotions) and
+ * to the earliest endpoint, so results are deterministic.
+ * Errors (message from atsi_last_error(NULL)): ATSI_E_INVALID for NULL
+ * arrays, on_gpu values other than 0/1, negative or non-finite times;
+ * ATSI_E_SHAPE for n outside 1..65536. */
+atsi_status atsi_schedule_transfers(const atsi_transfer_problem* problem, uint8_t* rb_out, double* latency_out);
+
+/* Alg. 3 (Sec. 4.4.3): load-aware re-scheduling.  A rescheduler keeps the
+ * measurement snapshot and time of the last scheduling and the assignment it
+ * produced.  Each step compares the current snapshot with the kept one: the
+ * deviation d is the largest relative change of a measured series' total,
+ * max over (t_gpu, t_cpu, c, w) of |sum cur - sum prev| / sum prev (infinite
+ * when a series grows from zero; the paper leaves the measure open).  It
+ * re-runs atsi_schedule_transfers on the current snapshot when there is no
+ * kept snapshot, when the default placement changed, or when d >= eps and
+ * now_s - (time of the last scheduling) >= tau_tpot * tpot_s (the paper:
+ * eps = 0.15, tau = 5 x the recent TPOT); otherwise it returns the kept
+ * assignment.  Applying the assignment (BuildRuntime) is the caller's
+ * atsi_set_backends.  Host computation only.
+ * create: n tensors per round (1..65536), eps >= 0, tau_tpot >= 0, finite.
+ * step: rb_out[n] (caller-owned) = the assignment in force (1 = GPU);
+ *   rescheduled_out and deviation_out (nullable) report the decision and d.
+ *   Errors: ATSI_E_SHAPE when cur->n differs from the rescheduler's n, and
+ *   the errors of atsi_schedule_transfers; the kept state is then unchanged. */
+typedef struct atsi_rescheduler atsi_rescheduler;
+atsi_status atsi_rescheduler_create(int32_t n, double eps, double tau_tpot, atsi_rescheduler** out);
+atsi_status atsi_rescheduler_step(atsi_rescheduler* r, const atsi_transfer_problem* cur, double now_s, double tpot_s,
+                                  uint8_t* rb_out, int32_t* rescheduled_out, double* deviation_out);
+atsi_status atsi_rescheduler_destroy(atsi_rescheduler* r);
+
+/* The host-CPU backend (the CPU side of the hybrid, Sec. 4.3-4.4): a pool of
+ * worker threads (the calling thread takes part as one of them).  A pool
+ * runs one product at a time; it may serve several contexts. */
+typedef struct atsi_cpu_pool atsi_cpu_pool;
+atsi_status atsi_cpu_pool_create(int32_t threads, atsi_cpu_pool** out);
+atsi_status atsi_cpu_pool_destroy(atsi_cpu_pool* pool);
+
+/* y[M][N] = x[M][K] . W^T on the host CPU, all pointers host memory: codes
+ * and scales in the layout of this header, x and y fp16 bit patterns
+ * (row-major, y must not alias x), fp32 sums, one round-to-nearest-even to
+ * fp16.  1 <= M <= 65536, K % 32 == 0.  Errors: ATSI_E_INVALID for NULL
+ * pointers, ATSI_E_SHAPE for sizes outside the limits; the message comes
+ * from atsi_last_error(NULL).  No GPU is needed. */
+atsi_status atsi_cpu_linear(atsi_cpu_pool* pool, const uint8_t* codes, const uint16_t* scales, int64_t N,
+                            int64_t K, const uint16_t* x_f16, int64_t M, uint16_t* y_f16);
+
+/* Attach the CPU backend to a context: the pool runs CPU-assigned tensors
+ * and staging (pinned host memory, hipHostMalloc'd, 256-byte aligned,
+ * staging_bytes long) carries their activations: a CPU-run launch copies its
+ * input rows (and residual) to staging on the compute stream, waits for
+ * them, computes on the pool and copies its outputs back on the compute
+ * stream, so the calling thread blocks for the CPU part (the backend switches
+ * are the activation transfers c_i of Sec. 4.4.1).  It needs M*K*2 bytes for
+ * the input, M*N*2 per output (4 for an fp32 one, twice for a SwiGLU pair)
+ * and M*N*2 for a residual, each rounded up to 256 (ATSI_E_WORKSPACE if
+ * staging is too small).  The library uses staging until atsi_destroy or the
+ * next atsi_set_cpu_backend, which drains the compute stream first.  pool =
+ * NULL detaches the backend (ATSI_E_STATE while a tensor is assigned to the
+ * CPU). */
+atsi_status atsi_set_cpu_backend(atsi_ctx* ctx, atsi_cpu_pool* pool, void* staging, size_t staging_bytes);
+
+/* Runtime backend assignment (BuildRuntime of Alg. 3): on_cpu[i] = 1 runs
+ * tensor i on the CPU backend from its pinned host copy, 0 on the GPU (a
+ * host-placed tensor is then promoted: copied through a temporary buffer).
+ * n must equal the number of registered tensors; only host-placed tensors
+ * may run on the CPU (ATSI_E_STATE otherwise, or without a CPU backend).
+ * Within one fused launch the gate and up tensors of a SwiGLU pair must share
+ * a backend; the q, k and v projections may differ (the GPU and CPU parts of
+ * the launch overlap).  MoE expert tensors run on the GPU only.
+ * atsi_set_placement resets every tensor it places in HBM to the GPU. */
+atsi_status atsi_set_backends(atsi_ctx* ctx, const uint8_t* on_cpu, int32_t n);
+
+/* Per-tensor measurements for the snapshots of Alg. 3 (Sec. 4.4.3).  With
+ * timing on, the context records HIP events around each GPU launch, weight
+ * copy and activation transfer, and host clock time around each CPU product.
+ * atsi_get_timings drains the streams and reports, per tensor, the latest
+ * value since timing was enabled (NaN where none): a fused launch's time is
+ * shared among its tensors by their byte sizes. */
+typedef struct {
+  double t_gpu;  /* GPU execution (s) */
+  double t_cpu;  /* CPU execution (s) */
+  double d2h;    /* activation transfer into a CPU run of the tensor (s) */
+  double h2d;    /* activation transfer out of it (s) */
+  double w;      /* weight copy into a temporary buffer (s) */
+} atsi_tensor_timing;
+atsi_status atsi_set_timing(atsi_ctx* ctx, int32_t enable);
+atsi_status atsi_get_timings(atsi_ctx* ctx, int32_t n, atsi_tensor_timing* out);
+
+/* Test export: the CPU backend's fp16 conversions, out[i] = the fp16 bit
+ * pattern of in[i] rounded to nearest even, back[i] = that fp16 as fp32
+ * (either output nullable).  No GPU is needed. */
+atsi_status atsi_debug_cpu_f16(const float* in, int64_t n, uint16_t* out, float* back);
 
 /* Test export: the signed codes q[N][K] (int8, device buffer) of tensor w as
  * the library reads them, from wherever w currently lives. */

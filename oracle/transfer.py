@@ -128,10 +128,12 @@ def deviation(prev, cur) -> float:
     return d
 
 
-def should_reschedule(prev, cur, eps: float, now: float, last: float, tau: float) -> bool:
+def should_reschedule(prev, cur, eps: float, now: float, last: float, tau: float,
+                      placement_changed: bool = False) -> bool:
     """Alg. 3's test: keep the previous assignment when the deviation is below
-    eps or less than tau has passed since the last re-scheduling; with no
-    previous snapshot (the first round) schedule."""
-    if prev is None:
+    eps or less than tau has passed since the last re-scheduling.  Readings:
+    with no previous snapshot (the first round) schedule; a new default
+    placement b invalidates the previous assignment, so it schedules too."""
+    if prev is None or placement_changed:
         return True
     return not (deviation(prev, cur) < eps or now - last < tau)

@@ -70,6 +70,18 @@ class atsi_placement_problem(ctypes.Structure):
                 ("granularity_bytes", ctypes.c_double)]
 
 
+class atsi_transfer_problem(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_int32), ("on_gpu", ctypes.c_void_p), ("t_gpu", ctypes.c_void_p),
+                ("t_cpu", ctypes.c_void_p), ("c", ctypes.c_void_p), ("w", ctypes.c_void_p)]
+
+
+TIMING_FIELDS = ("t_gpu", "t_cpu", "d2h", "h2d", "w")
+
+
+class atsi_tensor_timing(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_double) for n in TIMING_FIELDS]
+
+
 _P = ctypes.c_void_p
 class atsi_stats(ctypes.Structure):
     _fields_ = [("h2d_bytes", ctypes.c_uint64), ("h2d_copies", ctypes.c_uint64), ("h2d_tensors", ctypes.c_uint64),
@@ -105,6 +117,21 @@ _SIGS = {
     "atsi_set_zero_copy": ([_P, ctypes.c_int32], ctypes.c_int),
     "atsi_solve_placement": ([ctypes.POINTER(atsi_placement_problem), _P, ctypes.POINTER(ctypes.c_double)],
                              ctypes.c_int),
+    "atsi_schedule_transfers": ([ctypes.POINTER(atsi_transfer_problem), _P, ctypes.POINTER(ctypes.c_double)],
+                                ctypes.c_int),
+    "atsi_rescheduler_create": ([ctypes.c_int32, ctypes.c_double, ctypes.c_double, ctypes.POINTER(_P)],
+                                ctypes.c_int),
+    "atsi_rescheduler_step": ([_P, ctypes.POINTER(atsi_transfer_problem), ctypes.c_double, ctypes.c_double, _P,
+                               ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_double)], ctypes.c_int),
+    "atsi_rescheduler_destroy": ([_P], ctypes.c_int),
+    "atsi_cpu_pool_create": ([ctypes.c_int32, ctypes.POINTER(_P)], ctypes.c_int),
+    "atsi_cpu_pool_destroy": ([_P], ctypes.c_int),
+    "atsi_cpu_linear": ([_P, _P, _P, ctypes.c_int64, ctypes.c_int64, _P, ctypes.c_int64, _P], ctypes.c_int),
+    "atsi_set_cpu_backend": ([_P, _P, _P, ctypes.c_size_t], ctypes.c_int),
+    "atsi_set_backends": ([_P, _P, ctypes.c_int32], ctypes.c_int),
+    "atsi_set_timing": ([_P, ctypes.c_int32], ctypes.c_int),
+    "atsi_get_timings": ([_P, ctypes.c_int32, ctypes.POINTER(atsi_tensor_timing)], ctypes.c_int),
+    "atsi_debug_cpu_f16": ([_P, ctypes.c_int64, _P, _P], ctypes.c_int),
 }
 
 _lib = None
@@ -251,3 +278,93 @@ def atsi_set_debug(ctx: int, flags: int) -> None:
 
 def atsi_set_zero_copy(ctx: int, enable: bool) -> None:
     _check(ctx, lib().atsi_set_zero_copy(ctx, 1 if enable else 0))
+
+
+class _TransferArrays:
+    """An atsi_transfer_problem and the arrays it points at (kept alive together)."""
+
+    def __init__(self, on_gpu, t_gpu, t_cpu, c, w):
+        n = len(on_gpu)
+        if not (len(t_gpu) == len(t_cpu) == len(c) == len(w) == n):
+            raise ValueError("the five series of a transfer problem must have one length")
+        D = ctypes.c_double * max(n, 1)
+        self.b = (ctypes.c_uint8 * max(n, 1))(*[int(v) for v in on_gpu])
+        self.tg, self.tc = D(*map(float, t_gpu)), D(*map(float, t_cpu))
+        self.c, self.w = D(*map(float, c)), D(*map(float, w))
+        self.p = atsi_transfer_problem(n, ctypes.cast(self.b, _P), ctypes.cast(self.tg, _P),
+                                       ctypes.cast(self.tc, _P), ctypes.cast(self.c, _P), ctypes.cast(self.w, _P))
+        self.n = n
+
+
+def atsi_schedule_transfers(on_gpu, t_gpu, t_cpu, c, w):
+    """(rb list, 1 = GPU; T) of Alg. 2 (host computation)."""
+    a = _TransferArrays(on_gpu, t_gpu, t_cpu, c, w)
+    out = (ctypes.c_uint8 * max(a.n, 1))()
+    T = ctypes.c_double()
+    _check(None, lib().atsi_schedule_transfers(ctypes.byref(a.p), ctypes.cast(out, _P), ctypes.byref(T)))
+    return [int(out[i]) for i in range(a.n)], T.value
+
+
+def atsi_rescheduler_create(n: int, eps: float, tau_tpot: float) -> int:
+    out = _P()
+    _check(None, lib().atsi_rescheduler_create(n, eps, tau_tpot, ctypes.byref(out)))
+    return out.value
+
+
+def atsi_rescheduler_step(r: int, on_gpu, t_gpu, t_cpu, c, w, now_s: float, tpot_s: float):
+    """(rb list, rescheduled bool, deviation) of one Alg. 3 step."""
+    a = _TransferArrays(on_gpu, t_gpu, t_cpu, c, w)
+    out = (ctypes.c_uint8 * max(a.n, 1))()
+    did = ctypes.c_int32()
+    d = ctypes.c_double()
+    _check(None, lib().atsi_rescheduler_step(r, ctypes.byref(a.p), float(now_s), float(tpot_s),
+                                             ctypes.cast(out, _P), ctypes.byref(did), ctypes.byref(d)))
+    return [int(out[i]) for i in range(a.n)], bool(did.value), d.value
+
+
+def atsi_rescheduler_destroy(r: int) -> None:
+    _check(None, lib().atsi_rescheduler_destroy(r))
+
+
+def atsi_cpu_pool_create(threads: int) -> int:
+    out = _P()
+    _check(None, lib().atsi_cpu_pool_create(int(threads), ctypes.byref(out)))
+    return out.value
+
+
+def atsi_cpu_pool_destroy(pool: int) -> None:
+    _check(None, lib().atsi_cpu_pool_destroy(pool))
+
+
+def atsi_cpu_linear(pool: int, codes: int, scales: int, N: int, K: int, x: int, M: int, y: int) -> None:
+    _check(None, lib().atsi_cpu_linear(pool, codes, scales, N, K, x, M, y))
+
+
+def atsi_set_cpu_backend(ctx: int, pool: int, staging: int, staging_bytes: int) -> None:
+    _check(ctx, lib().atsi_set_cpu_backend(ctx, pool or None, staging or None, staging_bytes))
+
+
+def atsi_set_backends(ctx: int, on_cpu) -> None:
+    arr = (ctypes.c_uint8 * max(1, len(on_cpu)))(*[int(v) for v in on_cpu])
+    _check(ctx, lib().atsi_set_backends(ctx, ctypes.cast(arr, _P), len(on_cpu)))
+
+
+def atsi_set_timing(ctx: int, enable: bool) -> None:
+    _check(ctx, lib().atsi_set_timing(ctx, 1 if enable else 0))
+
+
+def atsi_get_timings(ctx: int, n: int) -> list:
+    """Per-tensor dicts of the latest measured times (seconds; NaN where none)."""
+    arr = (atsi_tensor_timing * max(1, n))()
+    _check(ctx, lib().atsi_get_timings(ctx, n, arr))
+    return [{f: getattr(arr[i], f) for f in TIMING_FIELDS} for i in range(n)]
+
+
+def atsi_debug_cpu_f16(values):
+    """(fp16 bit patterns, their fp32 values) of the CPU backend's rounding."""
+    n = len(values)
+    src = (ctypes.c_float * max(1, n))(*map(float, values))
+    out = (ctypes.c_uint16 * max(1, n))()
+    back = (ctypes.c_float * max(1, n))()
+    _check(None, lib().atsi_debug_cpu_f16(ctypes.cast(src, _P), n, ctypes.cast(out, _P), ctypes.cast(back, _P)))
+    return [int(out[i]) for i in range(n)], [back[i] for i in range(n)]

@@ -24,6 +24,17 @@ FLAGS = [
 ]
 
 
+# host-only sources (the CPU backend and the schedulers): no device code
+HOST_FLAGS = ["-O3", "-fPIC", "-std=c++17", "-Wall", "-pthread"]
+
+
+def _host_cxx() -> str:
+    for p in ("/opt/rocm/llvm/bin/clang++", shutil.which("clang++") or "", shutil.which("g++") or ""):
+        if p and os.path.exists(p):
+            return p
+    raise RuntimeError("no host C++ compiler found")
+
+
 def _hipcc() -> str:
     p = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
     if not os.path.exists(p):
@@ -33,7 +44,11 @@ def _hipcc() -> str:
 
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-    cmd = [_hipcc(), *FLAGS, "-I", os.path.join(PKG, "..", "include"), "-c", src, "-o", obj]
+    inc = ["-I", os.path.join(PKG, "..", "include")]
+    if src.endswith(".cpp"):
+        cmd = [_host_cxx(), *HOST_FLAGS, *inc, "-c", src, "-o", obj]
+    else:
+        cmd = [_hipcc(), *FLAGS, *inc, "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed on {src}:\n{r.stdout}\n{r.stderr}")
@@ -42,11 +57,11 @@ def _compile(src: str) -> str:
 
 def build(verbose: bool = False) -> str:
     os.makedirs(BUILD, exist_ok=True)
-    srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")))
+    srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")) + glob.glob(os.path.join(CSRC, "*.cpp")))
     with cf.ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
         objs = list(ex.map(_compile, srcs))
     tmp = LIB + f".tmp{os.getpid()}"
-    cmd = [_hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]
+    cmd = [_hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-pthread", "-o", tmp, *objs]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stdout}\n{r.stderr}")

@@ -16,11 +16,14 @@
 // while every slot is still being read waits on the host for the oldest
 // reader to finish.
 #include <algorithm>
+#include <chrono>
+#include <cmath>
 #include <cstdarg>
 #include <deque>
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <limits>
 #include <mutex>
 #include <new>
 #include <string>
@@ -28,6 +31,7 @@
 
 #include "../../include/atsi.h"
 #include "common.h"
+#include "cpu_backend.h"
 #include "layer.h"
 #include "moe.h"
 
@@ -52,6 +56,9 @@ struct Tensor {
   const uint8_t* zcodes = nullptr;
   const uint16_t* zscales = nullptr;
   bool on_host = false;
+  bool on_cpu = false;  // runtime backend: runs on the CPU backend (a host tensor only)
+  // a host tensor that runs on the GPU is copied into a slot for each use
+  bool streamed() const { return on_host && !on_cpu; }
   size_t codes_bytes() const { return (size_t)(K / 2) * (size_t)N; }
   size_t scales_bytes() const { return (size_t)(K / kGroup) * (size_t)N * 2; }
   size_t bytes() const { return codes_bytes() + scales_bytes(); }
@@ -162,6 +169,25 @@ struct atsi_ctx {
   int32_t* pinned = nullptr;    // caller's pinned host buffer for the per-expert counts, or null
   hipEvent_t counts_ev = nullptr;
   atsi_stats stats{};           // transfer counters (atsi_get_stats)
+  // CPU backend (atsi_set_cpu_backend): the caller's pool and pinned staging
+  atsi::cpu::Pool* pool = nullptr;
+  char* staging = nullptr;
+  size_t staging_bytes = 0;
+  hipEvent_t cpu_ev = nullptr;         // a CPU launch's inputs have reached staging
+  std::vector<float> cpu_x, cpu_acc;   // re-ordered fp32 inputs, fp32 products
+  // timing (atsi_set_timing): event pairs resolved into per-tensor figures
+  struct TimeRec {
+    hipEvent_t a, b;
+    int kind;  // offset of the field in atsi_tensor_timing, in doubles
+    int n;
+    atsi_tid tid[3];
+    double share[3];
+  };
+  bool timing = false;
+  std::vector<hipEvent_t> tev;          // timing events (created when timing is first enabled)
+  size_t tev_used = 0;
+  std::vector<TimeRec> trecs;
+  std::vector<atsi_tensor_timing> timings;
   std::string err;
   atsi_status latched = ATSI_OK;
   std::string latched_msg;
@@ -211,6 +237,69 @@ bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 atsi_status check_tid(atsi_ctx* c, atsi_tid t) {
   if (t < 0 || (size_t)t >= c->tensors.size())
     return fail(c, ATSI_E_UNKNOWN_TENSOR, "unknown tensor id %d (registered: %zu)", t, c->tensors.size());
+  return ATSI_OK;
+}
+
+// ---- timing (atsi_set_timing) ----
+// Fields of atsi_tensor_timing, in doubles.
+constexpr int kTimeGpu = 0, kTimeCpu = 1, kTimeD2H = 2, kTimeH2D = 3, kTimeW = 4;
+constexpr size_t kTimingEvents = 2048;
+
+double* timing_field(atsi_ctx* c, atsi_tid t, int kind) {
+  if ((size_t)t >= c->timings.size()) {
+    const double nan = std::numeric_limits<double>::quiet_NaN();
+    c->timings.resize(c->tensors.size(), atsi_tensor_timing{nan, nan, nan, nan, nan});
+  }
+  return reinterpret_cast<double*>(&c->timings[t]) + kind;
+}
+
+// Shares of a multi-tensor operation, by byte size.
+void byte_shares(atsi_ctx* c, const atsi_tid* tids, int n, double* share) {
+  double tot = 0.0;
+  for (int i = 0; i < n; ++i) tot += (double)c->tensors[tids[i]].bytes();
+  for (int i = 0; i < n; ++i) share[i] = tot > 0.0 ? (double)c->tensors[tids[i]].bytes() / tot : 1.0 / n;
+}
+
+// Turn the recorded event pairs into per-tensor figures (drains the streams).
+atsi_status resolve_timing(atsi_ctx* c) {
+  if (c->trecs.empty()) return ATSI_OK;
+  HIP_TRY(c, hipStreamSynchronize(c->cs));
+  HIP_TRY(c, hipStreamSynchronize(c->ts));
+  if (c->ts2) HIP_TRY(c, hipStreamSynchronize(c->ts2));
+  for (const auto& r : c->trecs) {
+    float ms = 0.f;
+    HIP_TRY(c, hipEventElapsedTime(&ms, r.a, r.b));
+    for (int i = 0; i < r.n; ++i) *timing_field(c, r.tid[i], r.kind) = (double)ms * 1e-3 * r.share[i];
+  }
+  c->trecs.clear();
+  c->tev_used = 0;
+  return ATSI_OK;
+}
+
+// Start timing an operation of `kind` on tensors tids (at most 3) on stream
+// s; *rec = the record to close with time_end, or -1 with timing off.
+atsi_status time_begin(atsi_ctx* c, int kind, const atsi_tid* tids, int n, hipStream_t s, int* rec) {
+  *rec = -1;
+  if (!c->timing || n < 1) return ATSI_OK;
+  if (c->tev_used + 2 > c->tev.size()) {
+    atsi_status st = resolve_timing(c);
+    if (st) return st;
+  }
+  atsi_ctx::TimeRec r{};
+  r.a = c->tev[c->tev_used++];
+  r.b = c->tev[c->tev_used++];
+  r.kind = kind;
+  r.n = std::min(n, 3);
+  for (int i = 0; i < r.n; ++i) r.tid[i] = tids[i];
+  byte_shares(c, r.tid, r.n, r.share);
+  HIP_TRY(c, hipEventRecord(r.a, s));
+  c->trecs.push_back(r);
+  *rec = (int)c->trecs.size() - 1;
+  return ATSI_OK;
+}
+
+atsi_status time_end(atsi_ctx* c, int rec, hipStream_t s) {
+  if (rec >= 0) HIP_TRY(c, hipEventRecord(c->trecs[rec].b, s));
   return ATSI_OK;
 }
 
@@ -304,9 +393,12 @@ atsi_status after_copy(atsi_ctx* c, hipStream_t xs) {
 // Copy host tensor t into slot s on the transfer stream: one copy when its
 // host codes and scales are contiguous (small copies cost far more than their
 // bytes), else two.  The slot must be free.
-atsi_status copy_into(atsi_ctx* c, const Tensor& t, Slot& s, hipStream_t xs) {
+atsi_status copy_into(atsi_ctx* c, atsi_tid tid, Slot& s, hipStream_t xs) {
+  const Tensor& t = c->tensors[tid];
   atsi_status st = before_copy(c, s.base, c->slot_bytes, xs);
   if (st) return st;
+  int tr;
+  if ((st = time_begin(c, kTimeW, &tid, 1, xs, &tr))) return st;
   if (t.host_contiguous()) {
     HIP_TRY(c, hipMemcpyAsync(s.base, t.hcodes, t.bytes(), hipMemcpyHostToDevice, xs));
     c->stats.h2d_copies += 1;
@@ -315,6 +407,7 @@ atsi_status copy_into(atsi_ctx* c, const Tensor& t, Slot& s, hipStream_t xs) {
     HIP_TRY(c, hipMemcpyAsync(s.base + t.codes_bytes(), t.hscales, t.scales_bytes(), hipMemcpyHostToDevice, xs));
     c->stats.h2d_copies += 2;
   }
+  if ((st = time_end(c, tr, xs))) return st;
   c->stats.h2d_bytes += t.bytes();
   c->stats.h2d_tensors += 1;
   return after_copy(c, xs);
@@ -389,7 +482,7 @@ atsi_status issue_copy(atsi_ctx* c, atsi_tid tid, bool block, const std::vector<
   if (si < 0) return ATSI_OK;
   Slot& s = c->slots[si];
   hipStream_t xs = copy_stream(c);
-  if ((st = copy_into(c, c->tensors[tid], s, xs))) return st;
+  if ((st = copy_into(c, tid, s, xs))) return st;
   HIP_TRY(c, hipEventRecord(s.ready, xs));
   arm(c, s, tid, ++c->copy_rec);
   return ATSI_OK;
@@ -402,7 +495,7 @@ bool run_candidate(atsi_ctx* c, const atsi_tid* tids, int n) {
   if (n < 2) return false;
   for (int i = 0; i < n; ++i) {
     const Tensor& t = c->tensors[tids[i]];
-    if (!t.on_host || !t.host_contiguous() || t.bytes() != c->slot_bytes) return false;
+    if (!t.streamed() || !t.host_contiguous() || t.bytes() != c->slot_bytes) return false;
     if (i && c->tensors[tids[i - 1]].hcodes + c->slot_bytes != t.hcodes) return false;
   }
   return true;
@@ -434,8 +527,11 @@ atsi_status issue_run(atsi_ctx* c, const atsi_tid* tids, int n, bool* issued) {
   hipStream_t xs = copy_stream(c);
   atsi_status st = before_copy(c, s0.base, (size_t)n * c->slot_bytes, xs);
   if (st) return st;
+  int tr;
+  if ((st = time_begin(c, kTimeW, tids, n, xs, &tr))) return st;
   HIP_TRY(c, hipMemcpyAsync(s0.base, c->tensors[tids[0]].hcodes, (size_t)n * c->slot_bytes, hipMemcpyHostToDevice,
                             xs));
+  if ((st = time_end(c, tr, xs))) return st;
   c->stats.h2d_copies += 1;
   c->stats.h2d_bytes += (uint64_t)n * c->slot_bytes;
   c->stats.h2d_tensors += (uint64_t)n;
@@ -461,7 +557,7 @@ atsi_status topup(atsi_ctx* c) {
       if (c->schedule.empty() || guard++ >= c->schedule.size()) break;
       atsi_tid t = c->schedule[c->sched_pos % c->schedule.size()];
       c->sched_pos++;
-      if (c->tensors[t].on_host) c->queue.push_back(t);
+      if (c->tensors[t].streamed()) c->queue.push_back(t);
       continue;
     }
     if (c->queue.size() >= 3) {
@@ -479,7 +575,7 @@ atsi_status topup(atsi_ctx* c) {
       }
     }
     const atsi_tid t = c->queue.front();
-    if (!c->tensors[t].on_host) {
+    if (!c->tensors[t].streamed()) {
       c->queue.pop_front();
       continue;
     }
@@ -499,7 +595,7 @@ atsi_status prefetch_call(atsi_ctx* c, const atsi_tid* tids, int n) {
   if (!c->schedule.empty()) return topup(c);
   for (int i = 0; i < n; ++i) {
     const atsi_tid t = tids[i];
-    if (!c->tensors[t].on_host) continue;
+    if (!c->tensors[t].streamed()) continue;
     bool have = std::find(c->queue.begin(), c->queue.end(), t) != c->queue.end();
     for (const Slot& s : c->slots) have = have || (s.armed && s.tid == t);
     if (!have) c->queue.push_back(t);
@@ -642,11 +738,12 @@ atsi_status get_table(atsi_ctx* c, const atsi_moe* m, atsi_ctx::MoeTable** out) 
 
 // Acquire the tensors of a fused launch (segment order; SwiGLU: gate, up),
 // launch the GEMV (M <= 4) or the GEMM, release the slots.
-atsi_status run_op(atsi_ctx* c, LinOp& op, const atsi_tid* tids, int ntids, bool workspace_scratch = true) {
+atsi_status run_gpu_op(atsi_ctx* c, LinOp& op, const atsi_tid* tids, int ntids, bool workspace_scratch) {
   std::vector<int> held;
+  atsi_status st;
   for (int i = 0; i < ntids; ++i) {
     QView v;
-    atsi_status st = acquire(c, tids[i], &v, held);
+    st = acquire(c, tids[i], &v, held);
     if (st) return st;
     if (op.swiglu) {
       if (i == 0) op.seg[0].w = v; else op.seg[0].w2 = v;
@@ -659,6 +756,8 @@ atsi_status run_op(atsi_ctx* c, LinOp& op, const atsi_tid* tids, int ntids, bool
   // loop has no registers to spare for the sums); a launch with K ranges
   // needs their fp32 partial sums above the scratch this call has taken,
   // which nothing else uses until its reduction has run on the stream.
+  int tr;  // timed from after the copy waits: the launch alone
+  if ((st = time_begin(c, kTimeGpu, tids, ntids, c->cs, &tr))) return st;
   int wide = (op.norm && !c->row_inv) ? 0 : gemm_wide_splits(op);
   float* part = nullptr;
   if (wide > 1 && !workspace_scratch) wide = 0;  // no partial sums outside the workspace
@@ -677,6 +776,7 @@ atsi_status run_op(atsi_ctx* c, LinOp& op, const atsi_tid* tids, int ntids, bool
     }
     hipError_t e = launch_gemm_wide(op, wide, part, c->cs);
     if (e != hipSuccess) return hip_fail(c, e, "q4 wide gemm launch");
+    if ((st = time_end(c, tr, c->cs))) return st;
     return release(c, held);
   }
   // decode sizes: one token runs the GEMV, 2 to 16 the batched-decode kernel
@@ -703,7 +803,181 @@ atsi_status run_op(atsi_ctx* c, LinOp& op, const atsi_tid* tids, int ntids, bool
     hipError_t e = launch_gemm(op, c->cs);
     if (e != hipSuccess) return hip_fail(c, e, "q4 gemm launch");
   }
+  if ((st = time_end(c, tr, c->cs))) return st;
   return release(c, held);
+}
+
+// ---- CPU backend part of a launch ----
+// Staging regions of the CPU segments of one launch: the input rows, the
+// residual (segment 0), and one packed output block per CPU segment.
+struct CpuPlan {
+  int seg[kMaxSeg];
+  int n = 0;
+  atsi_tid tids[kMaxSeg + 1];  // the CPU tensors (a SwiGLU pair counts two)
+  int ntids = 0;
+  char* x = nullptr;
+  char* res = nullptr;
+  char* out[kMaxSeg] = {};
+  int width[kMaxSeg] = {};  // output columns per row (N, or N * expand)
+  int elem[kMaxSeg] = {};   // 2 (fp16) or 4 (fp32)
+};
+
+atsi_status cpu_plan(atsi_ctx* c, const LinOp& op, const bool* cpu, const atsi_tid* tids, CpuPlan* p) {
+  if (!c->pool || !c->staging) return fail(c, ATSI_E_STATE, "a tensor runs on the CPU but no CPU backend is attached");
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    char* r = c->staging + off;
+    off += align_up(bytes);
+    return r;
+  };
+  const size_t M = (size_t)op.M;
+  p->x = take(M * op.K * 2);
+  for (int s = 0; s < op.nseg; ++s) {
+    if (!cpu[s]) continue;
+    const Seg& sg = op.seg[s];
+    const int i = p->n++;
+    p->seg[i] = s;
+    if (op.swiglu) {
+      p->tids[p->ntids++] = tids[0];
+      p->tids[p->ntids++] = tids[1];
+    } else {
+      p->tids[p->ntids++] = tids[s];
+    }
+    p->width[i] = sg.expand > 1 ? sg.w.N * sg.expand : sg.w.N;
+    p->elem[i] = (s == 0 && op.y32) ? 4 : 2;
+    p->out[i] = take(M * p->width[i] * p->elem[i]);
+    if (s == 0 && op.res) p->res = take(M * sg.w.N * 2);
+  }
+  if (off > c->staging_bytes)
+    return fail(c, ATSI_E_WORKSPACE, "CPU backend staging of %zu B < %zu B this %d-row launch needs",
+                c->staging_bytes, off, op.M);
+  return ATSI_OK;
+}
+
+// Inputs of the CPU part to staging, on the compute stream (after everything
+// that produces them), then the event the host waits on.
+atsi_status cpu_fetch(atsi_ctx* c, const LinOp& op, const CpuPlan& p) {
+  atsi_status st;
+  int tr;
+  if ((st = time_begin(c, kTimeD2H, p.tids, p.ntids, c->cs, &tr))) return st;
+  HIP_TRY(c, hipMemcpyAsync(p.x, op.x, (size_t)op.M * op.K * 2, hipMemcpyDeviceToHost, c->cs));
+  if (p.res) {
+    const Seg& s0 = op.seg[0];
+    HIP_TRY(c, hipMemcpy2DAsync(p.res, (size_t)s0.w.N * 2, op.res, (size_t)s0.ldy * 2, (size_t)s0.w.N * 2,
+                                (size_t)op.M, hipMemcpyDeviceToHost, c->cs));
+  }
+  if ((st = time_end(c, tr, c->cs))) return st;
+  HIP_TRY(c, hipEventRecord(c->cpu_ev, c->cs));
+  return ATSI_OK;
+}
+
+// The CPU part proper: wait for the inputs, run the products on the pool,
+// apply the launch's epilogue (the same semantics as the GPU's: RMS norm of
+// the input, SwiGLU, grouped-query expansion, residual, fp32 or fp16 output)
+// and copy the outputs back on the compute stream.
+atsi_status cpu_finish(atsi_ctx* c, const LinOp& op, const CpuPlan& p) {
+  HIP_TRY(c, hipEventSynchronize(c->cpu_ev));
+  const int M = op.M, K = op.K;
+  c->cpu_x.resize((size_t)M * K);
+  atsi::cpu::prepare_x(reinterpret_cast<const uint16_t*>(p.x), M, K, c->cpu_x.data());
+  std::vector<float> inv((size_t)M, 1.f);
+  if (op.norm)
+    for (int m = 0; m < M; ++m) {
+      double ss = 0.0;
+      for (int k = 0; k < K; ++k) ss += (double)c->cpu_x[(size_t)m * K + k] * c->cpu_x[(size_t)m * K + k];
+      inv[m] = (float)(1.0 / std::sqrt(ss / K + (double)op.eps));
+    }
+  const uint16_t* res = reinterpret_cast<const uint16_t*>(p.res);
+  for (int i = 0; i < p.n; ++i) {
+    const int s = p.seg[i];
+    const Seg& sg = op.seg[s];
+    const int N = sg.w.N;
+    const atsi_tid t0 = op.swiglu ? p.tids[0] : p.tids[i];
+    const Tensor& w = c->tensors[t0];
+    c->cpu_acc.resize((size_t)(op.swiglu ? 2 : 1) * M * N);
+    float* acc = c->cpu_acc.data();
+    const auto t_start = std::chrono::steady_clock::now();
+    atsi::cpu::linear(*c->pool, w.hcodes, w.hscales, N, K, c->cpu_x.data(), M, acc);
+    if (op.swiglu) {
+      const Tensor& u = c->tensors[p.tids[1]];
+      atsi::cpu::linear(*c->pool, u.hcodes, u.hscales, N, K, c->cpu_x.data(), M, acc + (size_t)M * N);
+    }
+    uint16_t* o16 = reinterpret_cast<uint16_t*>(p.out[i]);
+    float* o32 = reinterpret_cast<float*>(p.out[i]);
+    const int W = p.width[i];
+    for (int m = 0; m < M; ++m)
+      for (int n = 0; n < N; ++n) {
+        float v = acc[(size_t)m * N + n] * inv[m];
+        if (op.swiglu) {
+          const float u = acc[(size_t)(M + m) * N + n] * inv[m];
+          v = v / (1.f + std::exp(-v)) * u;
+        }
+        if (sg.expand > 1) {
+          const int hd = op.head_dim, jh = n / hd, d = n % hd;
+          const uint16_t h = atsi::cpu::float_to_half_rn(v);
+          for (int g = 0; g < sg.expand; ++g) o16[(size_t)m * W + (size_t)(jh * sg.expand + g) * hd + d] = h;
+          continue;
+        }
+        if (s == 0 && res) v += atsi::cpu::half_to_float(res[(size_t)m * N + n]);
+        if (p.elem[i] == 4)
+          o32[(size_t)m * W + n] = v;
+        else
+          o16[(size_t)m * W + n] = atsi::cpu::float_to_half_rn(v);
+      }
+    const double secs = std::chrono::duration<double>(std::chrono::steady_clock::now() - t_start).count();
+    if (c->timing) {
+      double share[2] = {1.0, 0.0};
+      const int nt = op.swiglu ? 2 : 1;
+      const atsi_tid tt[2] = {t0, op.swiglu ? p.tids[1] : t0};
+      if (nt == 2) byte_shares(c, tt, 2, share);
+      for (int j = 0; j < nt; ++j) *timing_field(c, tt[j], kTimeCpu) = secs * share[j];
+    }
+  }
+  atsi_status st;
+  int tr;
+  if ((st = time_begin(c, kTimeH2D, p.tids, p.ntids, c->cs, &tr))) return st;
+  for (int i = 0; i < p.n; ++i) {
+    const Seg& sg = op.seg[p.seg[i]];
+    void* dst = (p.seg[i] == 0 && op.y32) ? (void*)op.y32 : (void*)sg.y;
+    const size_t row = (size_t)p.width[i] * p.elem[i];
+    HIP_TRY(c, hipMemcpy2DAsync(dst, (size_t)sg.ldy * p.elem[i], p.out[i], row, row, (size_t)M,
+                                hipMemcpyHostToDevice, c->cs));
+  }
+  return time_end(c, tr, c->cs);
+}
+
+// Run one fused launch: segments whose tensors are assigned to the CPU run
+// on the CPU backend, the rest as one GPU launch that overlaps the CPU part.
+atsi_status run_op(atsi_ctx* c, LinOp& op, const atsi_tid* tids, int ntids, bool workspace_scratch = true) {
+  bool cpu[kMaxSeg] = {};
+  int ncpu = 0;
+  for (int s = 0; s < op.nseg; ++s) {
+    const atsi_tid t = op.swiglu ? tids[0] : tids[s];
+    cpu[s] = c->tensors[t].on_cpu;
+    if (op.swiglu && c->tensors[tids[1]].on_cpu != cpu[s])
+      return fail(c, ATSI_E_STATE, "gate %d and up %d of a SwiGLU pair must share a backend", tids[0], tids[1]);
+    ncpu += cpu[s] ? 1 : 0;
+  }
+  if (ncpu == 0) return run_gpu_op(c, op, tids, ntids, workspace_scratch);
+  if (!workspace_scratch) return fail(c, ATSI_E_STATE, "this entry point runs no tensor on the CPU backend");
+  if (ncpu < op.nseg && (op.res || op.y32 || op.swiglu))
+    return fail(c, ATSI_E_STATE, "a launch with a residual or fp32 output runs on one backend");
+  CpuPlan p;
+  atsi_status st = cpu_plan(c, op, cpu, tids, &p);
+  if (st) return st;
+  if ((st = cpu_fetch(c, op, p))) return st;
+  if (ncpu < op.nseg) {
+    LinOp g = op;
+    g.nseg = 0;
+    atsi_tid gt[kMaxSeg];
+    for (int s = 0; s < op.nseg; ++s)
+      if (!cpu[s]) {
+        gt[g.nseg] = tids[s];
+        g.seg[g.nseg++] = op.seg[s];
+      }
+    if ((st = run_gpu_op(c, g, gt, g.nseg, workspace_scratch))) return st;
+  }
+  return cpu_finish(c, op, p);
 }
 
 atsi_status check_act(atsi_ctx* c, const void* p, const char* what) {
@@ -792,6 +1066,8 @@ atsi_status check_moe(atsi_ctx* c, const atsi_moe* m) {
     const Tensor &g = c->tensors[m->gate[e]], &u = c->tensors[m->up[e]], &d = c->tensors[m->down[e]];
     if (g.K != H || g.N != I || u.K != H || u.N != I || d.K != I || d.N != H)
       return fail(c, ATSI_E_SHAPE, "expert %d: gate/up must be %d x %d and down %d x %d", e, H, I, I, H);
+    if (g.on_cpu || u.on_cpu || d.on_cpu)
+      return fail(c, ATSI_E_STATE, "expert %d is assigned to the CPU backend; experts run on the GPU only", e);
   }
   return ATSI_OK;
 }
@@ -995,7 +1271,8 @@ atsi_status atsi_create(int device, void* compute_stream, void* transfer_stream,
     c->row_inv = reinterpret_cast<float*>(c->ws + c->table_floor);
   }
   c->slots.resize(n_slots);
-  if (hipEventCreateWithFlags(&c->counts_ev, hipEventDisableTiming) != hipSuccess) {
+  if (hipEventCreateWithFlags(&c->counts_ev, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&c->cpu_ev, hipEventDisableTiming) != hipSuccess) {
     fail(nullptr, ATSI_E_HIP, "hipEventCreate failed");
     atsi_destroy(c);
     return ATSI_E_HIP;
@@ -1030,6 +1307,8 @@ atsi_status atsi_destroy(atsi_ctx* c) {
     if (s.free) (void)hipEventDestroy(s.free);
   }
   if (c->counts_ev) (void)hipEventDestroy(c->counts_ev);
+  if (c->cpu_ev) (void)hipEventDestroy(c->cpu_ev);
+  for (hipEvent_t e : c->tev) (void)hipEventDestroy(e);
   delete c;
   return ATSI_OK;
 }
@@ -1101,14 +1380,19 @@ atsi_status atsi_set_placement(atsi_ctx* c, const uint8_t* host_mask, int32_t n)
   }
   atsi_status st = enter(c);
   if (st) return st;
-  std::vector<bool> old(n);
+  std::vector<bool> old(n), old_cpu(n);
   for (int32_t i = 0; i < n; ++i) {
     old[i] = c->tensors[i].on_host;
+    old_cpu[i] = c->tensors[i].on_cpu;
     c->tensors[i].on_host = host_mask[i] != 0;
+    c->tensors[i].on_cpu = c->tensors[i].on_cpu && c->tensors[i].on_host;  // HBM tensors run on the GPU
   }
   st = layout_slots(c);
   if (st) {
-    for (int32_t i = 0; i < n; ++i) c->tensors[i].on_host = old[i];
+    for (int32_t i = 0; i < n; ++i) {
+      c->tensors[i].on_host = old[i];
+      c->tensors[i].on_cpu = old_cpu[i];
+    }
     return st;
   }
   ++c->placement_version;
@@ -1375,7 +1659,7 @@ atsi_status atsi_prefetch(atsi_ctx* c, atsi_tid w) {
   atsi_status st = check_tid(c, w);
   if (st) return st;
   if ((st = enter(c))) return st;
-  if (!c->tensors[w].on_host) return ATSI_OK;
+  if (!c->tensors[w].streamed()) return ATSI_OK;
   c->queue.push_back(w);
   return topup(c);
 }
@@ -1436,6 +1720,81 @@ atsi_status atsi_sync(atsi_ctx* c) {
     c->err = c->latched_msg;
     return c->latched;
   }
+  return ATSI_OK;
+}
+
+atsi_status atsi_set_cpu_backend(atsi_ctx* c, atsi_cpu_pool* pool, void* staging, size_t staging_bytes) {
+  if (!c) return ATSI_E_INVALID;
+  if (pool && (!staging || ((uintptr_t)staging % kAlign) != 0 || staging_bytes < kAlign))
+    return fail(c, ATSI_E_INVALID, "staging must be non-null pinned host memory, 256-byte aligned, >= 256 B");
+  if (!pool)
+    for (size_t i = 0; i < c->tensors.size(); ++i)
+      if (c->tensors[i].on_cpu) return fail(c, ATSI_E_STATE, "tensor %zu is assigned to the CPU backend", i);
+  atsi_status st = enter(c);
+  if (st) return st;
+  HIP_TRY(c, hipStreamSynchronize(c->cs));  // the old staging may still be read by a copy
+  c->pool = pool ? &pool->pool : nullptr;
+  c->staging = pool ? static_cast<char*>(staging) : nullptr;
+  c->staging_bytes = pool ? staging_bytes : 0;
+  return ATSI_OK;
+}
+
+atsi_status atsi_set_backends(atsi_ctx* c, const uint8_t* on_cpu, int32_t n) {
+  if (!c) return ATSI_E_INVALID;
+  if (!on_cpu) return fail(c, ATSI_E_INVALID, "on_cpu is NULL");
+  if (n != (int32_t)c->tensors.size())
+    return fail(c, ATSI_E_INVALID, "assignment length %d != %zu registered tensors", n, c->tensors.size());
+  bool any = false;
+  for (int32_t i = 0; i < n; ++i) {
+    if (on_cpu[i] > 1) return fail(c, ATSI_E_INVALID, "on_cpu[%d]=%d is not 0 or 1", i, on_cpu[i]);
+    if (on_cpu[i] && !c->tensors[i].on_host)
+      return fail(c, ATSI_E_STATE, "tensor %d is placed in HBM; only host-placed tensors run on the CPU", i);
+    any = any || on_cpu[i];
+  }
+  if (any && !c->pool) return fail(c, ATSI_E_STATE, "no CPU backend attached (atsi_set_cpu_backend)");
+  atsi_status st = enter(c);
+  if (st) return st;
+  for (int32_t i = 0; i < n; ++i) c->tensors[i].on_cpu = on_cpu[i] != 0;
+  // copies armed or queued for tensors now on the CPU would never be read:
+  // free their slots once the copies have landed, and drop them from the queue
+  for (Slot& sl : c->slots)
+    if (sl.armed && !c->tensors[sl.tid].streamed()) {
+      HIP_TRY(c, hipEventSynchronize(sl.ready));
+      sl.armed = false;
+    }
+  c->queue.erase(std::remove_if(c->queue.begin(), c->queue.end(),
+                                [&](atsi_tid t) { return !c->tensors[t].streamed(); }),
+                 c->queue.end());
+  return ATSI_OK;
+}
+
+atsi_status atsi_set_timing(atsi_ctx* c, int32_t enable) {
+  if (!c) return ATSI_E_INVALID;
+  if (enable != 0 && enable != 1) return fail(c, ATSI_E_INVALID, "enable=%d is not 0 or 1", enable);
+  atsi_status st = enter(c);
+  if (st) return st;
+  if ((st = resolve_timing(c))) return st;
+  if (enable && c->tev.empty()) {
+    c->tev.resize(kTimingEvents, nullptr);
+    for (hipEvent_t& e : c->tev) HIP_TRY(c, hipEventCreate(&e));
+  }
+  const double nan = std::numeric_limits<double>::quiet_NaN();
+  if (enable && !c->timing) c->timings.assign(c->tensors.size(), atsi_tensor_timing{nan, nan, nan, nan, nan});
+  c->timing = enable != 0;
+  return ATSI_OK;
+}
+
+atsi_status atsi_get_timings(atsi_ctx* c, int32_t n, atsi_tensor_timing* out) {
+  if (!c) return ATSI_E_INVALID;
+  if (!out) return fail(c, ATSI_E_INVALID, "out is NULL");
+  if (n != (int32_t)c->tensors.size())
+    return fail(c, ATSI_E_INVALID, "output length %d != %zu registered tensors", n, c->tensors.size());
+  atsi_status st = enter(c);
+  if (st) return st;
+  if ((st = resolve_timing(c))) return st;
+  const double nan = std::numeric_limits<double>::quiet_NaN();
+  c->timings.resize(c->tensors.size(), atsi_tensor_timing{nan, nan, nan, nan, nan});
+  for (int32_t i = 0; i < n; ++i) out[i] = c->timings[i];
   return ATSI_OK;
 }
 

@@ -1,0 +1,182 @@
+"""The library's dynamic transfer scheduler (atsi_schedule_transfers, Alg. 2)
+and load-aware re-scheduler (atsi_rescheduler_*, Alg. 3) against the oracle,
+CPU only (host code).
+
+Several assignments can reach the optimum, so the scheduler is checked on
+what is unique -- the optimal latency -- and its assignment must be valid and
+reach that latency under the oracle's T(rb).
+"""
+import json
+import math
+import os
+import random
+
+import pytest
+
+from oracle import transfer as tr
+from paper_2607_10183_amd import atsi
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _check(b, tg, tc, c, w):
+    rb, T = atsi.atsi_schedule_transfers(b, tg, tc, c, w)
+    assert all(not (bi == 1 and ri == 0) for bi, ri in zip(b, rb)), "a GPU-placed tensor left the GPU"
+    t_rb = tr.latency(rb, b, tg, tc, c, w)
+    assert t_rb == pytest.approx(T, rel=1e-9, abs=1e-12), "reported latency is not T(rb)"
+    return rb, T
+
+
+def test_worked_round():
+    with open(os.path.join(GOLD, "transfer_worked.json")) as f:
+        g = json.load(f)
+    rb, T = _check(g["b"], g["tg"], g["tc"], g["c"], g["w"])
+    assert T == pytest.approx(g["best"]["T"], abs=1e-12)
+    assert rb in g["best"]["rb"]
+
+
+def _round(rng, n, p_cpu, w_scale):
+    b = [0 if rng.random() < p_cpu else 1 for _ in range(n)]
+    tg = [rng.uniform(0.05, 2.0) for _ in range(n)]
+    tc = [rng.uniform(0.2, 6.0) for _ in range(n)]
+    c = [rng.uniform(0.0, 0.8) for _ in range(n)]
+    w = [rng.uniform(0.0, w_scale) for _ in range(n)]
+    return b, tg, tc, c, w
+
+
+@pytest.mark.parametrize("seed", range(60))
+def test_matches_enumeration(seed):
+    rng = random.Random(seed)
+    n = rng.randint(1, 14)
+    b, tg, tc, c, w = _round(rng, n, p_cpu=rng.choice([0.3, 0.7, 1.0]), w_scale=rng.choice([1.0, 6.0, 20.0]))
+    best, _ = tr.best_by_enumeration(b, tg, tc, c, w)
+    _, T = _check(b, tg, tc, c, w)
+    assert T == pytest.approx(best, rel=1e-9, abs=1e-12)
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_ties_and_zeros(seed):
+    """Integer-valued times with many equal-latency assignments and zero
+    costs: the optimum still matches and the result is deterministic."""
+    rng = random.Random(500 + seed)
+    n = 12
+    b = [rng.choice((0, 0, 1)) for _ in range(n)]
+    tg = [float(rng.randint(0, 2)) for _ in range(n)]
+    tc = [float(rng.randint(0, 3)) for _ in range(n)]
+    c = [float(rng.randint(0, 1)) for _ in range(n)]
+    w = [float(rng.randint(0, 4)) for _ in range(n)]
+    best, _ = tr.best_by_enumeration(b, tg, tc, c, w)
+    rb1, T = _check(b, tg, tc, c, w)
+    rb2, _ = _check(b, tg, tc, c, w)
+    assert T == pytest.approx(best, abs=1e-12) and rb1 == rb2
+
+
+@pytest.mark.parametrize("n", [200, 752])
+def test_large_round_dominates(n):
+    """At model sizes (no enumeration): the optimum is no worse than keeping
+    the default placement or than any of 200 random reachable assignments."""
+    rng = random.Random(n)
+    b, tg, tc, c, w = _round(rng, n, 0.6, 8.0)
+    rb, T = _check(b, tg, tc, c, w)
+    assert T <= tr.latency(b, b, tg, tc, c, w) + 1e-9
+    for _ in range(200):
+        cand = [1 if bi == 1 else rng.choice((0, 1)) for bi in b]
+        assert T <= tr.latency(cand, b, tg, tc, c, w) + 1e-9
+
+
+def test_all_gpu_round_is_fixed():
+    rb, T = _check([1] * 5, [1.0, 2, 3, 4, 5], [9.0] * 5, [0.5] * 5, [1.0] * 5)
+    assert rb == [1] * 5 and T == pytest.approx(15.0)
+
+
+def test_rejects_bad_problems():
+    with pytest.raises(atsi.AtsiError):
+        atsi.atsi_schedule_transfers([0, 2], [1, 1], [1, 1], [0, 0], [0, 0])
+    with pytest.raises(atsi.AtsiError):
+        atsi.atsi_schedule_transfers([0], [-1.0], [1.0], [0.0], [0.0])
+    with pytest.raises(atsi.AtsiError):
+        atsi.atsi_schedule_transfers([0], [math.inf], [1.0], [0.0], [0.0])
+    with pytest.raises(atsi.AtsiError):
+        atsi.atsi_schedule_transfers([], [], [], [], [])
+
+
+# ---------------------------------------------------------------- Alg. 3
+
+def _snapshots(rng, n, steps):
+    b, tg, tc, c, w = _round(rng, n, 0.6, 6.0)
+    out = []
+    for s in range(steps):
+        f_cpu = rng.choice([1.0, 1.0, 1.05, 1.3, 1.6])   # background CPU load
+        f_link = rng.choice([1.0, 1.0, 0.9, 1.25, 2.0])  # PCIe contention
+        out.append((b, [x * rng.uniform(0.97, 1.03) for x in tg], [x * f_cpu for x in tc], c,
+                    [x * f_link for x in w]))
+    return out
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_rescheduler_follows_alg3(seed):
+    """A sequence of snapshots with load swings: the library's decisions and
+    assignments equal the oracle's decision rule driving its own scheduler."""
+    rng = random.Random(900 + seed)
+    n, eps, k = 10, 0.15, 5.0
+    r = atsi.atsi_rescheduler_create(n, eps, k)
+    try:
+        prev, last, rb_keep = None, 0.0, None
+        now = 0.0
+        decisions = []
+        for snap in _snapshots(rng, n, 40):
+            tpot = 0.04
+            now += rng.choice([0.04, 0.04, 0.2, 0.5])
+            b = snap[0]
+            series = snap[1:]
+            want = tr.should_reschedule(prev, series, eps, now, last, k * tpot)
+            rb, did, d = atsi.atsi_rescheduler_step(r, *snap, now, tpot)
+            assert did == want
+            decisions.append(did)
+            if prev is not None:
+                assert d == pytest.approx(tr.deviation(prev, series), rel=1e-12)
+            if want:
+                best, _ = tr.best_by_enumeration(b, *series)
+                assert tr.latency(rb, b, *series) == pytest.approx(best, rel=1e-9)
+                prev, last, rb_keep = series, now, rb
+            else:
+                assert rb == rb_keep
+        assert sum(decisions) > 1 and not all(decisions), "the sequence must both keep and re-schedule"
+    finally:
+        atsi.atsi_rescheduler_destroy(r)
+
+
+def test_rescheduler_thresholds_exactly():
+    """At eps and at tau exactly the rule re-schedules; just below it keeps."""
+    n = 2
+    b = [0, 0]
+    base = ([1.0, 1.0], [2.0, 2.0], [0.5, 0.5], [3.0, 1.0])
+    at_eps = ([1.0, 1.0], [2.0, 2.5], [0.5, 0.5], [3.0, 1.0])   # d = 0.125
+    below = ([1.0, 1.0], [2.0, 2.4375], [0.5, 0.5], [3.0, 1.0])  # d = 0.109375
+    tpot = 0.03125
+    for cur, dt, want in [(at_eps, 5 * tpot, True), (below, 5 * tpot, False),
+                          (at_eps, 5 * tpot - 2.0 ** -10, False), (at_eps, 40 * tpot, True)]:
+        r = atsi.atsi_rescheduler_create(n, 0.125, 5.0)
+        try:
+            _, did0, _ = atsi.atsi_rescheduler_step(r, b, *base, 1.0, tpot)
+            assert did0
+            _, did, d = atsi.atsi_rescheduler_step(r, b, *cur, 1.0 + dt, tpot)
+            assert did == want, (cur, dt)
+            assert did == tr.should_reschedule(base, cur, 0.125, 1.0 + dt, 1.0, 5 * tpot)
+        finally:
+            atsi.atsi_rescheduler_destroy(r)
+
+
+def test_rescheduler_new_placement_reschedules():
+    r = atsi.atsi_rescheduler_create(3, 0.15, 5.0)
+    try:
+        s = ([1.0] * 3, [4.0] * 3, [0.1] * 3, [0.5] * 3)
+        atsi.atsi_rescheduler_step(r, [0, 0, 0], *s, 0.0, 0.04)
+        _, did, _ = atsi.atsi_rescheduler_step(r, [0, 0, 0], *s, 10.0, 0.04)
+        assert not did
+        _, did, _ = atsi.atsi_rescheduler_step(r, [1, 0, 0], *s, 10.0, 0.04)
+        assert did == tr.should_reschedule(s, s, 0.15, 10.0, 10.0, 0.2, placement_changed=True) == True
+        with pytest.raises(atsi.AtsiError):
+            atsi.atsi_rescheduler_step(r, [0, 0], [1.0] * 2, [1.0] * 2, [0.0] * 2, [0.0] * 2, 11.0, 0.04)
+    finally:
+        atsi.atsi_rescheduler_destroy(r)
