@@ -818,6 +818,7 @@ struct CpuPlan {
   char* x = nullptr;
   char* res = nullptr;
   char* out[kMaxSeg] = {};
+  int N[kMaxSeg] = {};      // outputs of the segment's tensor
   int width[kMaxSeg] = {};  // output columns per row (N, or N * expand)
   int elem[kMaxSeg] = {};   // 2 (fp16) or 4 (fp32)
 };
@@ -843,10 +844,13 @@ atsi_status cpu_plan(atsi_ctx* c, const LinOp& op, const bool* cpu, const atsi_t
     } else {
       p->tids[p->ntids++] = tids[s];
     }
-    p->width[i] = sg.expand > 1 ? sg.w.N * sg.expand : sg.w.N;
+    // the launch's views are filled in only when a GPU part acquires them:
+    // sizes come from the registered tensor
+    p->N[i] = (int)c->tensors[op.swiglu ? tids[0] : tids[s]].N;
+    p->width[i] = sg.expand > 1 ? p->N[i] * sg.expand : p->N[i];
     p->elem[i] = (s == 0 && op.y32) ? 4 : 2;
     p->out[i] = take(M * p->width[i] * p->elem[i]);
-    if (s == 0 && op.res) p->res = take(M * sg.w.N * 2);
+    if (s == 0 && op.res) p->res = take(M * p->N[i] * 2);
   }
   if (off > c->staging_bytes)
     return fail(c, ATSI_E_WORKSPACE, "CPU backend staging of %zu B < %zu B this %d-row launch needs",
@@ -861,10 +865,10 @@ atsi_status cpu_fetch(atsi_ctx* c, const LinOp& op, const CpuPlan& p) {
   int tr;
   if ((st = time_begin(c, kTimeD2H, p.tids, p.ntids, c->cs, &tr))) return st;
   HIP_TRY(c, hipMemcpyAsync(p.x, op.x, (size_t)op.M * op.K * 2, hipMemcpyDeviceToHost, c->cs));
-  if (p.res) {
-    const Seg& s0 = op.seg[0];
-    HIP_TRY(c, hipMemcpy2DAsync(p.res, (size_t)s0.w.N * 2, op.res, (size_t)s0.ldy * 2, (size_t)s0.w.N * 2,
-                                (size_t)op.M, hipMemcpyDeviceToHost, c->cs));
+  if (p.res) {  // segment 0 is then the plan's first
+    const size_t row = (size_t)p.N[0] * 2;
+    HIP_TRY(c, hipMemcpy2DAsync(p.res, row, op.res, (size_t)op.seg[0].ldy * 2, row, (size_t)op.M,
+                                hipMemcpyDeviceToHost, c->cs));
   }
   if ((st = time_end(c, tr, c->cs))) return st;
   HIP_TRY(c, hipEventRecord(c->cpu_ev, c->cs));
@@ -891,7 +895,7 @@ atsi_status cpu_finish(atsi_ctx* c, const LinOp& op, const CpuPlan& p) {
   for (int i = 0; i < p.n; ++i) {
     const int s = p.seg[i];
     const Seg& sg = op.seg[s];
-    const int N = sg.w.N;
+    const int N = p.N[i];
     const atsi_tid t0 = op.swiglu ? p.tids[0] : p.tids[i];
     const Tensor& w = c->tensors[t0];
     c->cpu_acc.resize((size_t)(op.swiglu ? 2 : 1) * M * N);

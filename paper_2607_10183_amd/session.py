@@ -31,6 +31,9 @@ class Session:
         self._keep: list = []
         self.shapes: list[tuple[int, int]] = []
         self.placement: list[int] = []  # current host mask, mirrors the library's
+        self.backends: list[int] = []   # current runtime assignment, 1 = CPU
+        self.pool = 0
+        self.staging = None
 
     # ---------------------------------------------------------------- tensors
     def register(self, codes: np.ndarray, scales: np.ndarray, hbm: bool = True, host: bool = False) -> int:
@@ -55,6 +58,7 @@ class Session:
         tid = atsi.atsi_tensor_register(self.ctx, K, N, dc, ds, hc, hs)
         self.shapes.append((K, N))
         self.placement.append(0 if hbm else 1)
+        self.backends.append(0)
         return tid
 
     @staticmethod
@@ -92,6 +96,7 @@ class Session:
             out.append(atsi.atsi_tensor_register(self.ctx, K, N, dc, ds, hc, hs))
             self.shapes.append((K, N))
             self.placement.append(0 if hbm else 1)
+            self.backends.append(0)
         return out
 
     def register_device(self, codes_t: torch.Tensor, scales_t: torch.Tensor,
@@ -104,6 +109,7 @@ class Session:
                                         host_scales.data_ptr() if host_scales is not None else 0)
         self.shapes.append((2 * kb, N))
         self.placement.append(0)
+        self.backends.append(0)
         return tid
 
     def register_host(self, K: int, N: int, host_codes: int, host_scales: int) -> int:
@@ -112,6 +118,7 @@ class Session:
         tid = atsi.atsi_tensor_register(self.ctx, K, N, 0, 0, host_codes, host_scales)
         self.shapes.append((K, N))
         self.placement.append(1)
+        self.backends.append(0)
         return tid
 
     def set_debug(self, poison: bool = False, serialize: bool = False) -> None:
@@ -126,6 +133,30 @@ class Session:
         mask = [int(v) for v in host_mask]
         atsi.atsi_set_placement(self.ctx, mask)
         self.placement = mask
+        self.backends = [b if m else 0 for b, m in zip(self.backends, mask)]
+
+    # ---------------------------------------------------------------- hybrid CPU-GPU
+    def attach_cpu(self, threads: int, staging_bytes: int = 64 << 20) -> None:
+        """Attach the host-CPU backend: a pool of `threads` workers and a pinned
+        staging buffer for the activations of CPU-run launches."""
+        if self.pool:
+            raise RuntimeError("a CPU backend is already attached")
+        self.pool = atsi.atsi_cpu_pool_create(threads)
+        self.staging = torch.empty(staging_bytes, dtype=torch.uint8).pin_memory()
+        atsi.atsi_set_cpu_backend(self.ctx, self.pool, self.staging.data_ptr(), staging_bytes)
+
+    def set_backends(self, on_cpu) -> None:
+        """Runtime backend assignment (1 = the CPU backend; host-placed tensors only)."""
+        a = [int(v) for v in on_cpu]
+        atsi.atsi_set_backends(self.ctx, a)
+        self.backends = a
+
+    def set_timing(self, enable: bool = True) -> None:
+        atsi.atsi_set_timing(self.ctx, enable)
+
+    def timings(self) -> list:
+        """Latest per-tensor measurements (t_gpu, t_cpu, d2h, h2d, w in seconds; NaN where none)."""
+        return atsi.atsi_get_timings(self.ctx, len(self.shapes))
 
     def place(self, tid: int, host: bool) -> None:
         """Move one tensor between HBM and host, keeping the others where they are."""
@@ -258,6 +289,9 @@ class Session:
         if self.ctx:
             atsi.atsi_destroy(self.ctx)
             self.ctx = 0
+        if self.pool:
+            atsi.atsi_cpu_pool_destroy(self.pool)
+            self.pool = 0
 
     def __enter__(self):
         return self
