@@ -769,6 +769,254 @@ def bench_moe_stack(pcie_gbs):
 
 # ---------------------------------------------------------------------------- host-side pieces
 
+# ---------------------------------------------------------------------------- hybrid CPU-GPU decode (Alg. 1-3)
+
+class LoadInjector:
+    """Background load for the load-aware runs: `cpu` busy processes on the
+    host cores, or `link` a thread copying a pinned 256 MiB buffer to the
+    device back to back on a stream of its own (PCIe pressure)."""
+
+    def __init__(self, cpu: int = 0, link: bool = False):
+        self.cpu, self.link = cpu, link
+        self.procs, self.thread, self.stop = [], None, None
+
+    def __enter__(self):
+        import subprocess
+        import threading
+        import torch
+        for _ in range(self.cpu):
+            self.procs.append(subprocess.Popen([sys.executable, "-c", "while True:\n    pass"]))
+        if self.link:
+            self.stop = threading.Event()
+            src = torch.empty(256 << 20, dtype=torch.uint8).pin_memory()
+            dst = torch.empty(256 << 20, dtype=torch.uint8, device="cuda")
+            st = torch.cuda.Stream()
+
+            def pump():
+                while not self.stop.is_set():
+                    with torch.cuda.stream(st):
+                        dst.copy_(src, non_blocking=True)
+                    st.synchronize()
+            self.thread = threading.Thread(target=pump, daemon=True)
+            self.thread.start()
+        return self
+
+    def __exit__(self, *exc):
+        for p in self.procs:
+            p.kill()
+        for p in self.procs:
+            p.wait()
+        if self.thread is not None:
+            self.stop.set()
+            self.thread.join()
+        return False
+
+
+def bench_hybrid(pcie_gbs, steps=30):
+    """Hybrid decode of the 32-layer 8B-shaped stack at batch 1 (TPOT):
+    Alg. 1 places 30 % of the bytes on the host from measured per-unit GPU and
+    CPU times, Alg. 2 picks which host units to promote each round, and the
+    library runs the rest on its CPU backend.  Measured against its own
+    prediction T(rb) for three assignments: the static default (every host
+    unit on the CPU), all host units promoted, and Alg. 2's choice."""
+    import torch
+
+    import synth
+    from synth import configs
+    from paper_2607_10183_amd import hybrid
+    from paper_2607_10183_amd.session import Session
+
+    wl = configs.DENSE_STACK
+    shape = wl.dense
+    threads = min(16, os.cpu_count() or 1)
+    log(f"hybrid: generating the 32-layer stack (CPU backend on {threads} threads)")
+    sess = Session(workspace_bytes=2 << 30, n_slots=24)
+    sess.attach_cpu(threads, staging_bytes=8 << 20)
+    layers = []
+    for layer in range(wl.n_layers):
+        t = {}
+        for r in configs.ROLES:
+            K, N = shape.kn(r)
+            uid = configs.dense_uid(layer, r)
+            t[r] = sess.register(synth.int4_codes(wl.seed, uid, N, K), synth.group_scales(wl.seed, uid, N, K),
+                                 hbm=True, host=True)
+        layers.append(t)
+    units = hybrid.dense_units(layers)
+    nu, nt = len(units), len(sess.shapes)
+    ub = [float(sum(configs.qbytes(*sess.shapes[t]) for t in tids)) for _, _, tids in units]
+    order = [t for _, _, tids in units for t in tids]
+    h = torch.from_numpy(synth.activations(wl.seed, 7, 1, shape.hidden)).cuda()
+    sess.cs.wait_stream(torch.cuda.current_stream())
+
+    def step():
+        for t in layers:
+            sess.decoder_layer(t, h, shape.n_heads, shape.n_kv, shape.head_dim, 1e-6, renorm_out=True)
+
+    def wall(n):
+        sess.sync()
+        t0 = time.perf_counter()
+        for _ in range(n):
+            step()
+        sess.sync()
+        return (time.perf_counter() - t0) / n
+
+    def timed_samples(n):
+        sess.set_timing(True)
+        out = []
+        for _ in range(n):
+            step()
+            out.append(sess.timings())
+        sess.set_timing(False)
+        return out
+
+    def configure(host_units, cpu_units):
+        sess.set_backends([0] * nt)
+        sess.set_placement(hybrid.host_mask(sess, units, host_units))
+        sess.set_backends(hybrid.cpu_mask(sess, units, cpu_units))
+        sess.set_schedule(order)
+
+    # Alg. 1's profile: every unit resident, every unit on the CPU, every unit promoted
+    configure([0] * nu, [0] * nu)
+    wall(3)
+    ref_g = hybrid.median_timings(timed_samples(5), "t_gpu", units)
+    t_hbm = wall(steps)
+    configure([1] * nu, [1] * nu)
+    wall(1)
+    sm = timed_samples(3)
+    ref_c = [float(np.median(v)) for v in zip(*[hybrid.cpu_unit_raw(units, x) for x in sm])]
+    t_allcpu = wall(max(3, steps // 5))
+    launches = 4 * wl.n_layers  # q/k/v, o, gate/up, down
+    per_launch = max(0.0, (t_allcpu - sum(ref_c)) / launches)
+    share = {("q",): 1 / 3, ("k",): 1 / 3, ("v",): 1 / 3}
+    t_cpu = [rc + per_launch * share.get(roles, 1.0) for (_, roles, _), rc in zip(units, ref_c)]
+    configure([1] * nu, [0] * nu)
+    wall(2)
+    ref_w = hybrid.median_timings(timed_samples(3), "w", units)
+    w = [b / (pcie_gbs * 1e9) for b in ub]
+    t_gpu = ref_g
+
+    # Alg. 1 (static placement at 70 % of the bytes in HBM) and Alg. 2
+    budget = 0.70 * sum(ub)
+    t0 = time.perf_counter()
+    on_gpu = hybrid.static_placement(ub, t_gpu, t_cpu, budget)
+    t1 = time.perf_counter()
+    rb, T_dp = hybrid.schedule(on_gpu, t_gpu, t_cpu, w)
+    t2 = time.perf_counter()
+    host_units = [1 - g for g in on_gpu]
+    policies = {"static_default": list(on_gpu), "all_promoted": [1] * nu, "dynamic_alg2": rb}
+    # the host's speed drifts (other tenants of the CPU): the policies take
+    # turns over three rounds and each reports its median round
+    walls = {name: [] for name in policies}
+    for _ in range(3):
+        for name, r in policies.items():
+            configure(host_units, [1 - v for v in r])
+            wall(1)
+            walls[name].append(wall(max(1, steps // 3)))
+    res = {}
+    regime_ref = None
+    for name, r in policies.items():
+        configure(host_units, [1 - v for v in r])
+        wall(1)
+        t = float(np.median(walls[name]))
+        T = hybrid.predicted(on_gpu, r, t_gpu, t_cpu, w)
+        # the same assignment with per-unit timing: what its CPU units and copies took
+        smp = timed_samples(3)
+        raw_c = [float(np.median(v)) for v in zip(*[hybrid.cpu_unit_raw(units, x) for x in smp])]
+        raw_w = hybrid.median_timings(smp, "w", units)
+        raw_g = hybrid.median_timings(smp, "t_gpu", units)
+        cpu_idx = [i for i, v in enumerate(r) if v == 0]
+        prom_idx = [i for i, (g, v) in enumerate(zip(on_gpu, r)) if g == 0 and v == 1]
+        res[name] = {"ms_per_token": round(t * 1e3, 3), "tokens_per_s": round(1.0 / t, 2),
+                     "ms_per_token_rounds": [round(v * 1e3, 3) for v in walls[name]],
+                     "predicted_ms": round(T * 1e3, 3) if math.isfinite(T) else None,
+                     "promoted_units": len(prom_idx), "cpu_units": len(cpu_idx),
+                     "cpu_unit_us_vs_profile": [round(float(np.mean([raw_c[i] for i in cpu_idx])) * 1e6, 1),
+                                                round(float(np.mean([ref_c[i] for i in cpu_idx])) * 1e6, 1)]
+                     if cpu_idx else None,
+                     "copy_us_vs_model": [round(float(np.mean([raw_w[i] for i in prom_idx])) * 1e6, 1),
+                                          round(float(np.mean([w[i] for i in prom_idx])) * 1e6, 1)]
+                     if prom_idx else None}
+        if name == "dynamic_alg2":
+            # Alg. 3 starts in this regime: its execution times are the
+            # reference; a measured copy time replaces the model's w directly
+            # (copies slow down beside CPU work that shares host memory, which
+            # the model's overlap window does not see)
+            regime_ref = {"t_gpu": [a if not math.isnan(a) else b for a, b in zip(raw_g, ref_g)],
+                          "t_cpu": [a if not math.isnan(a) else b for a, b in zip(raw_c, ref_c)],
+                          "w": list(w)}
+        log(f"hybrid {name}: {t * 1e3:.2f} ms/token (predicted {res[name]['predicted_ms']} ms), "
+            f"{res[name]['promoted_units']} units promoted, {res[name]['cpu_units']} on the CPU; CPU unit us "
+            f"(measured, profile) {res[name]['cpu_unit_us_vs_profile']}, copy us (measured, model) "
+            f"{res[name]['copy_us_vs_model']}")
+    roles_host = {"+".join(rr): sum(1 for (_, r2, _), hu in zip(units, host_units) if hu and r2 == rr)
+                  for rr in hybrid.ROLE_UNITS}
+    roles_promoted = {"+".join(rr): sum(1 for (_, r2, _), hu, v in zip(units, host_units, rb) if hu and v and r2 == rr)
+                      for rr in hybrid.ROLE_UNITS}
+    profile = {"units": nu, "unit_bytes_total": int(sum(ub)), "host_bytes": int(sum(b for b, hu in zip(ub, host_units) if hu)),
+               "all_hbm_ms_per_token": round(t_hbm * 1e3, 3), "all_cpu_ms_per_token": round(t_allcpu * 1e3, 3),
+               "cpu_launch_overhead_us": round(per_launch * 1e6, 2),
+               "t_gpu_us_per_layer": {"+".join(r): round(v * 1e6, 2) for (_, r, _), v in zip(units[:6], t_gpu[:6])},
+               "t_cpu_us_per_layer": {"+".join(r): round(v * 1e6, 2) for (_, r, _), v in zip(units[:6], t_cpu[:6])},
+               "w_us_per_layer": {"+".join(r): round(v * 1e6, 2) for (_, r, _), v in zip(units[:6], w[:6])},
+               "host_units_per_role": roles_host, "promoted_units_per_role": roles_promoted,
+               "alg1_host_ms": round((t1 - t0) * 1e3, 3), "alg2_host_ms": round((t2 - t1) * 1e3, 3)}
+    ctx = {"sess": sess, "units": units, "on_gpu": on_gpu, "rb": rb, "step": step, "configure": configure,
+           "model": {"t_gpu": t_gpu, "t_cpu": t_cpu, "w": w}, "reference": regime_ref, "threads": threads}
+    return {"workload": "hybrid_decode: 32 8B-shaped layers at batch 1 (one token per step, hidden state "
+                        "renormalised after every layer); Alg. 1 puts 30 % of the bytes on the host from "
+                        "measured per-unit times; CPU units run on the library's CPU backend",
+            "threads": threads, "steps_timed": steps, "profile": profile, "policies": res}, ctx
+
+
+def bench_load_aware(ctx, phase_steps=40):
+    """Alg. 3 online: the Alg. 2 assignment kept fixed (static) against the
+    load-aware loop (eps = 15 %, tau = 5 x the recent TPOT), over phases of
+    idle, CPU load (busy processes on every host core the pool uses), PCIe
+    load (back-to-back 256 MiB host-to-device copies) and idle again."""
+    from paper_2607_10183_amd import hybrid
+
+    sess, units, on_gpu, rb0, step = ctx["sess"], ctx["units"], ctx["on_gpu"], ctx["rb"], ctx["step"]
+    phases = [("idle", {}), ("cpu_load", {"cpu": ctx["threads"]}), ("pcie_load", {"link": True}), ("idle_again", {})]
+    out = {}
+    for policy in ("static", "load_aware"):
+        ctx["configure"]([1 - g for g in on_gpu], [1 - v for v in rb0])
+        ctrl = None
+        if policy == "load_aware":
+            ctrl = hybrid.Controller(sess, units, on_gpu, hybrid.Snapshotter(units, ctx["model"], ctx["reference"]))
+            ctrl.rb = list(rb0)
+        sess.set_timing(True)
+        sess.sync()
+        rec = {}
+        recent = []
+        decide_s = 0.0
+        for name, load in phases:
+            tpots = []
+            with LoadInjector(**load):
+                for _ in range(phase_steps):
+                    t0 = time.perf_counter()
+                    step()
+                    tm = sess.timings()  # drains the streams
+                    t1 = time.perf_counter()
+                    tpots.append(t1 - t0)
+                    recent = (recent + [t1 - t0])[-8:]
+                    if ctrl is not None:
+                        ctrl.step(t1, float(np.median(recent)), tm)
+                        decide_s += time.perf_counter() - t1
+            rec[name] = {"ms_per_token_mean": round(float(np.mean(tpots)) * 1e3, 3),
+                         "ms_per_token_median": round(float(np.median(tpots)) * 1e3, 3)}
+            if ctrl is not None:
+                rec[name]["cpu_units_now"] = int(sum(1 for v in ctrl.rb if v == 0))
+        sess.set_timing(False)
+        if ctrl is not None:
+            rec["reschedules"] = ctrl.reschedules
+            rec["decision_ms_per_step"] = round(decide_s / (len(phases) * phase_steps) * 1e3, 3)
+            ctrl.close()
+        out[policy] = rec
+        log(f"load-aware {policy}: {rec}")
+    return {"workload": "the hybrid_decode stack, " + ", ".join(f"{n} ({phase_steps} tokens)" for n, _ in phases),
+            "eps": 0.15, "tau": "5 x median TPOT of the last 8 tokens", "policies": out}
+
+
 def bench_placement_solver(reps: int = 3):
     """Host time of atsi_solve_placement on the 94-layer 235B-A22B-shaped
     model: per layer q, k, v, o, the router and the gate / up / down expert
@@ -857,6 +1105,7 @@ def main() -> int:
     ap.add_argument("--no-moe", action="store_true")
     ap.add_argument("--no-stacks", action="store_true", help="skip the dense-stack and MoE-stack lines")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-hybrid", action="store_true", help="skip the hybrid CPU-GPU and load-aware lines")
     ap.add_argument("--roofline-only", action="store_true",
                     help="run only the roofline kernels and a 256 MiB copy (for rocprofv3 --pmc)")
     args = ap.parse_args()
@@ -895,6 +1144,13 @@ def main() -> int:
     if not args.no_stacks:
         stacks = {"dense_stack": bench_dense_stack(pcie["ceiling_GBps"]),
                   "moe_stack": bench_moe_stack(pcie["ceiling_GBps"])}
+    hybrid_rec = load_rec = None
+    if not args.no_hybrid:
+        hybrid_rec, hctx = bench_hybrid(pcie["ceiling_GBps"])
+        load_rec = bench_load_aware(hctx)
+        hctx["sess"].close()
+        del hctx
+        torch.cuda.empty_cache()
     placement = bench_placement_solver()
     log(f"placement solver: {placement}")
     cpu = None
@@ -941,6 +1197,8 @@ def main() -> int:
         "moe": moe,
         "stacks": stacks,
         "placement_solver": placement,
+        "hybrid": hybrid_rec,
+        "load_aware": load_rec,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

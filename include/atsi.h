@@ -425,6 +425,13 @@ typedef struct {
  * ATSI_E_SHAPE for n outside 1..65536. */
 atsi_status atsi_schedule_transfers(const atsi_transfer_problem* problem, uint8_t* rb_out, double* latency_out);
 
+/* T(rb) of Sec. 4.4.1 for a given assignment rb (1 = GPU), under the
+ * endpoint reading of atsi_schedule_transfers; *latency_out = +infinity for
+ * an assignment that reading cannot reach (two promotions with no CPU-run
+ * tensor between).  Errors: those of atsi_schedule_transfers, ATSI_E_INVALID
+ * for rb values other than 0/1 or a GPU-placed tensor assigned to the CPU. */
+atsi_status atsi_transfer_latency(const atsi_transfer_problem* problem, const uint8_t* rb, double* latency_out);
+
 /* Alg. 3 (Sec. 4.4.3): load-aware re-scheduling.  A rescheduler keeps the
  * measurement snapshot and time of the last scheduling and the assignment it
  * produced.  Each step compares the current snapshot with the kept one: the

@@ -119,6 +119,8 @@ _SIGS = {
                              ctypes.c_int),
     "atsi_schedule_transfers": ([ctypes.POINTER(atsi_transfer_problem), _P, ctypes.POINTER(ctypes.c_double)],
                                 ctypes.c_int),
+    "atsi_transfer_latency": ([ctypes.POINTER(atsi_transfer_problem), _P, ctypes.POINTER(ctypes.c_double)],
+                              ctypes.c_int),
     "atsi_rescheduler_create": ([ctypes.c_int32, ctypes.c_double, ctypes.c_double, ctypes.POINTER(_P)],
                                 ctypes.c_int),
     "atsi_rescheduler_step": ([_P, ctypes.POINTER(atsi_transfer_problem), ctypes.c_double, ctypes.c_double, _P,
@@ -303,6 +305,15 @@ def atsi_schedule_transfers(on_gpu, t_gpu, t_cpu, c, w):
     T = ctypes.c_double()
     _check(None, lib().atsi_schedule_transfers(ctypes.byref(a.p), ctypes.cast(out, _P), ctypes.byref(T)))
     return [int(out[i]) for i in range(a.n)], T.value
+
+
+def atsi_transfer_latency(on_gpu, t_gpu, t_cpu, c, w, rb) -> float:
+    """T(rb) of Sec. 4.4.1 (inf for an unreachable rb)."""
+    a = _TransferArrays(on_gpu, t_gpu, t_cpu, c, w)
+    arr = (ctypes.c_uint8 * max(a.n, 1))(*[int(v) for v in rb])
+    T = ctypes.c_double()
+    _check(None, lib().atsi_transfer_latency(ctypes.byref(a.p), ctypes.cast(arr, _P), ctypes.byref(T)))
+    return T.value
 
 
 def atsi_rescheduler_create(n: int, eps: float, tau_tpot: float) -> int:

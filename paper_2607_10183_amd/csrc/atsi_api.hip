@@ -27,6 +27,7 @@
 #include <mutex>
 #include <new>
 #include <string>
+#include <thread>
 #include <vector>
 
 #include "../../include/atsi.h"
@@ -880,7 +881,17 @@ atsi_status cpu_fetch(atsi_ctx* c, const LinOp& op, const CpuPlan& p) {
 // the input, SwiGLU, grouped-query expansion, residual, fp32 or fp16 output)
 // and copy the outputs back on the compute stream.
 atsi_status cpu_finish(atsi_ctx* c, const LinOp& op, const CpuPlan& p) {
-  HIP_TRY(c, hipEventSynchronize(c->cpu_ev));
+  // poll (a blocking wait wakes up tens of microseconds late), then block
+  {
+    hipError_t e = hipEventQuery(c->cpu_ev);
+    const auto t0 = std::chrono::steady_clock::now();
+    while (e == hipErrorNotReady && std::chrono::steady_clock::now() - t0 < std::chrono::milliseconds(20)) {
+      std::this_thread::yield();
+      e = hipEventQuery(c->cpu_ev);
+    }
+    if (e == hipErrorNotReady) e = hipEventSynchronize(c->cpu_ev);
+    if (e != hipSuccess) return hip_fail(c, e, "waiting for a CPU launch's inputs");
+  }
   const int M = op.M, K = op.K;
   c->cpu_x.resize((size_t)M * K);
   atsi::cpu::prepare_x(reinterpret_cast<const uint16_t*>(p.x), M, K, c->cpu_x.data());

@@ -17,6 +17,7 @@
 #include <immintrin.h>
 
 #include <algorithm>
+#include <chrono>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -31,6 +32,11 @@ namespace cpu {
 
 // ---------------------------------------------------------------- pool
 
+// Waiting for the next job: pause-spin briefly, then yield the core (so that
+// under oversubscription a preempted thread of this pool gets it), then sleep.
+constexpr auto kPauseSpin = std::chrono::microseconds(20);
+constexpr auto kYieldSpin = std::chrono::microseconds(2000);
+
 Pool::Pool(int threads) : n_(std::max(1, threads)) {
   for (int i = 1; i < n_; ++i) threads_.emplace_back(&Pool::worker, this, i);
 }
@@ -38,7 +44,7 @@ Pool::Pool(int threads) : n_(std::max(1, threads)) {
 Pool::~Pool() {
   {
     std::lock_guard<std::mutex> lk(mu_);
-    stop_ = true;
+    stop_.store(true);
   }
   go_.notify_all();
   for (auto& t : threads_) t.join();
@@ -47,35 +53,52 @@ Pool::~Pool() {
 void Pool::worker(int id) {
   uint64_t seen = 0;
   for (;;) {
-    const std::function<void(int)>* f;
-    {
+    const auto t0 = std::chrono::steady_clock::now();
+    int spins = 0;
+    while (gen_.load() == seen && !stop_.load()) {
+      if (++spins < 64) {
+        _mm_pause();
+        continue;
+      }
+      spins = 0;
+      const auto dt = std::chrono::steady_clock::now() - t0;
+      if (dt < kPauseSpin) continue;
+      if (dt < kYieldSpin) {
+        std::this_thread::yield();
+        continue;
+      }
       std::unique_lock<std::mutex> lk(mu_);
-      go_.wait(lk, [&] { return stop_ || gen_ != seen; });
-      if (stop_) return;
-      seen = gen_;
-      f = fn_;
+      sleepers_.fetch_add(1);
+      go_.wait(lk, [&] { return gen_.load() != seen || stop_.load(); });
+      sleepers_.fetch_sub(1);
     }
-    (*f)(id);
-    {
-      std::lock_guard<std::mutex> lk(mu_);
-      if (--pending_ == 0) done_.notify_one();
-    }
+    if (stop_.load()) return;
+    seen = gen_.load();
+    (*fn_)(id);
+    pending_.fetch_sub(1);
   }
 }
 
 void Pool::run(const std::function<void(int)>& fn) {
   std::lock_guard<std::mutex> one(run_mu_);
-  {
+  fn_ = &fn;
+  pending_.store(n_ - 1);
+  gen_.fetch_add(1);  // publishes fn_ (sequentially consistent)
+  if (sleepers_.load() > 0) {
     std::lock_guard<std::mutex> lk(mu_);
-    fn_ = &fn;
-    pending_ = n_ - 1;
-    ++gen_;
+    go_.notify_all();
   }
-  go_.notify_all();
   fn(0);
-  std::unique_lock<std::mutex> lk(mu_);
-  done_.wait(lk, [&] { return pending_ == 0; });
-  fn_ = nullptr;
+  const auto t0 = std::chrono::steady_clock::now();
+  int spins = 0;
+  while (pending_.load() != 0) {
+    if (++spins < 64) {
+      _mm_pause();
+      continue;
+    }
+    spins = 0;
+    if (std::chrono::steady_clock::now() - t0 >= kPauseSpin) std::this_thread::yield();
+  }
 }
 
 // ---------------------------------------------------------------- fp16

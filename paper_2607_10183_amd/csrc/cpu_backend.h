@@ -5,6 +5,7 @@
 
 #include <stdint.h>
 
+#include <atomic>
 #include <condition_variable>
 #include <functional>
 #include <mutex>
@@ -16,7 +17,10 @@ namespace cpu {
 
 // A fixed set of worker threads; run(fn) calls fn(0..n-1) once each, the
 // calling thread taking part as worker 0, and returns when all are done.
-// One run at a time per pool (run serialises its callers).
+// One run at a time per pool (run serialises its callers).  Workers spin on
+// the job counter for a while after each job (decode rounds hand the pool a
+// new product every few tens of microseconds) and then sleep on a condition
+// variable.
 class Pool {
  public:
   explicit Pool(int threads);
@@ -29,12 +33,13 @@ class Pool {
   int n_;
   std::vector<std::thread> threads_;
   std::mutex run_mu_;  // one run at a time
-  std::mutex mu_;
-  std::condition_variable go_, done_;
+  std::mutex mu_;      // guards sleeping
+  std::condition_variable go_;
   const std::function<void(int)>* fn_ = nullptr;
-  uint64_t gen_ = 0;
-  int pending_ = 0;
-  bool stop_ = false;
+  std::atomic<uint64_t> gen_{0};
+  std::atomic<int> pending_{0};
+  std::atomic<int> sleepers_{0};
+  std::atomic<bool> stop_{false};
 };
 
 // acc[m * ldacc + n] = sum_k q[n][k] * s[n][k / 32] * x[m][k] in fp32 for

@@ -173,6 +173,40 @@ atsi_status atsi_schedule_transfers(const atsi_transfer_problem* p, uint8_t* rb_
   return ATSI_OK;
 }
 
+atsi_status atsi_transfer_latency(const atsi_transfer_problem* p, const uint8_t* rb, double* latency_out) {
+  atsi_status st = check_problem(p);
+  if (st) return st;
+  if (!rb || !latency_out) return refuse(ATSI_E_INVALID, "rb and latency_out must be non-null");
+  const int n = p->n;
+  const uint8_t* b = p->on_gpu;
+  for (int i = 0; i < n; ++i) {
+    if (rb[i] > 1) return refuse(ATSI_E_INVALID, "rb[%d] = %d is not 0 or 1", i, rb[i]);
+    if (b[i] == kGpu && rb[i] == kCpu) return refuse(ATSI_E_INVALID, "tensor %d is placed on the GPU", i);
+  }
+  // walk the round: the default-path prefix P gives seg(j, i) = P[i] - P[j+1]
+  std::vector<double> P(n + 1, 0.0);
+  for (int i = 0; i < n; ++i)
+    P[i + 1] = P[i] + (b[i] == kGpu ? p->t_gpu[i] : p->t_cpu[i]) + ((i >= 1 && b[i - 1] != b[i]) ? p->c[i] : 0.0);
+  double T = 0.0;
+  int start = -1;        // endpoint of the next promotion: -1 round start, -2 none yet after a promotion
+  for (int i = 0; i < n; ++i) {
+    T += rb[i] == kGpu ? p->t_gpu[i] : p->t_cpu[i];
+    if (i >= 1 && rb[i - 1] != rb[i]) T += p->c[i];
+    if (b[i] == kCpu && rb[i] == kGpu) {
+      if (start == -2) {
+        *latency_out = kInf;  // two promotions with no CPU-run tensor between
+        return ATSI_OK;
+      }
+      T += std::max(p->w[i] - (P[i] - P[start + 1]), 0.0);
+      start = -2;
+    } else if (rb[i] == kCpu && start == -2) {
+      start = i;
+    }
+  }
+  *latency_out = T;
+  return ATSI_OK;
+}
+
 atsi_status atsi_rescheduler_create(int32_t n, double eps, double tau_tpot, atsi_rescheduler** out) {
   if (!out) return refuse(ATSI_E_INVALID, "out is NULL");
   *out = nullptr;

@@ -233,3 +233,62 @@ def test_timings_record_each_backend(sess):
             assert math.isnan(t["t_cpu"]), (r, t)
     # a 29 MB copy at under 64 GB/s takes at least 0.45 ms
     assert tm[tids["gate"]]["w"] > 0.45e-3
+
+
+def test_controller_rebuilds_runtime(sess):
+    """Alg. 3's loop on the GPU: the controller's decisions follow the
+    measured load (synthetic timing reads), BuildRuntime applies each new
+    assignment to the library, and the layer computed under it still matches
+    the oracle."""
+    import torch
+    from paper_2607_10183_amd import hybrid
+    shape = configs.DenseShape()
+    W = {r: _qt(98, configs.dense_uid(0, r), shape.kn(r)[1], shape.kn(r)[0]) for r in configs.ROLES}
+    tids = {r: sess.register(*W[r], hbm=True, host=True) for r in configs.ROLES}
+    units = hybrid.dense_units([tids])
+    on_gpu = [1, 1, 1, 0, 0, 0]  # o, gate+up and down on the host
+    sess.set_placement(hybrid.host_mask(sess, units, [1 - g for g in on_gpu]))
+    model = {"t_gpu": [8e-6, 2e-6, 2e-6, 7e-6, 15e-6, 13e-6], "t_cpu": [2e-4, 1e-4, 1e-4, 2.5e-4, 6e-4, 4e-4],
+             "w": [1.7e-4, 4e-5, 4e-5, 1.7e-4, 1.2e-3, 6e-4]}
+    ctrl = hybrid.Controller(sess, units, on_gpu, hybrid.Snapshotter(units, model, model))
+    nan = float("nan")
+    n = len(sess.shapes)
+
+    def reads(cpu_scale):
+        tm = [{"t_gpu": nan, "t_cpu": nan, "d2h": nan, "h2d": nan, "w": nan} for _ in range(n)]
+        for (_, roles, ts), tg, tc in zip(units, model["t_gpu"], model["t_cpu"]):
+            for t in ts:
+                tm[t].update(t_gpu=tg / len(ts), t_cpu=tc * cpu_scale / len(ts), d2h=0.0, h2d=0.0)
+        return tm
+
+    def run_and_check(tag):
+        hn = synth.activations(98, 5, 1, shape.hidden)
+        h = _dev(hn)
+        q_out = torch.empty((1, shape.n_heads * shape.head_dim), dtype=torch.float16, device="cuda")
+        k_out = torch.empty((1, shape.n_kv * shape.head_dim), dtype=torch.float16, device="cuda")
+        _, dbg = sess.decoder_layer(tids, h, shape.n_heads, shape.n_kv, shape.head_dim, 1e-6, q_out, k_out,
+                                    debug=True)
+        sess.sync()
+        stages.attention_stages(W, shape.n_heads, shape.n_kv, shape.head_dim, hn, q_out, k_out, dbg["attn"],
+                                dbg["h_attn"], tag)
+        stages.ffn_stages(W, dbg["h_attn"], dbg["act"], h, tag)
+
+    try:
+        did, _ = ctrl.step(0.0, 0.01, reads(1.0))
+        assert did and ctrl.rb is not None
+        first = list(ctrl.rb)
+        assert sess.backends == hybrid.cpu_mask(sess, units, [1 - v for v in first])
+        run_and_check(f"controller first assignment {first}")
+        did, _ = ctrl.step(0.02, 0.01, reads(1.0))          # nothing changed
+        assert not did
+        did, _ = ctrl.step(0.03, 0.01, reads(50.0))         # CPU 50x slower, but within tau = 5 x 10 ms
+        assert not did
+        did, d = ctrl.step(0.2, 0.01, reads(50.0))          # after tau: re-schedule
+        assert did and d > 0.15
+        second = list(ctrl.rb)
+        assert sum(second) >= sum(first), "a slower CPU must not move work to the CPU"
+        assert sess.backends == hybrid.cpu_mask(sess, units, [1 - v for v in second])
+        run_and_check(f"controller loaded assignment {second}")
+    finally:
+        ctrl.close()
+        _reset(sess)

@@ -21,6 +21,7 @@ GOLD = os.path.join(os.path.dirname(__file__), "golden")
 
 def _check(b, tg, tc, c, w):
     rb, T = atsi.atsi_schedule_transfers(b, tg, tc, c, w)
+    assert atsi.atsi_transfer_latency(b, tg, tc, c, w, rb) == pytest.approx(T, rel=1e-12, abs=1e-12)
     assert all(not (bi == 1 and ri == 0) for bi, ri in zip(b, rb)), "a GPU-placed tensor left the GPU"
     t_rb = tr.latency(rb, b, tg, tc, c, w)
     assert t_rb == pytest.approx(T, rel=1e-9, abs=1e-12), "reported latency is not T(rb)"
@@ -82,6 +83,22 @@ def test_large_round_dominates(n):
     for _ in range(200):
         cand = [1 if bi == 1 else rng.choice((0, 1)) for bi in b]
         assert T <= tr.latency(cand, b, tg, tc, c, w) + 1e-9
+
+
+@pytest.mark.parametrize("seed", range(10))
+def test_latency_of_every_assignment(seed):
+    """atsi_transfer_latency against the oracle's T(rb), unreachable ones included."""
+    rng = random.Random(700 + seed)
+    b, tg, tc, c, w = _round(rng, rng.randint(1, 9), 0.6, 6.0)
+    for rb in tr.assignments(b):
+        want = tr.latency(rb, b, tg, tc, c, w)
+        got = atsi.atsi_transfer_latency(b, tg, tc, c, w, rb)
+        if want == math.inf:
+            assert got == math.inf
+        else:
+            assert got == pytest.approx(want, rel=1e-12, abs=1e-12)
+    with pytest.raises(atsi.AtsiError):
+        atsi.atsi_transfer_latency([1], [1.0], [1.0], [0.0], [0.0], [0])
 
 
 def test_all_gpu_round_is_fixed():
