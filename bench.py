@@ -233,12 +233,12 @@ def bench_dense_layer(args, sess, timer, pcie_gbs=None):
         return timer.samples(g.replay, n_samples, per=R * rounds)
 
     kern = {}
-    for M, n_samples, rounds in ((1, 100, 8), (Mp, 30, 1)):
+    # under counter collection every dispatch is serialised and sampled: a few suffice
+    sizes = ((1, 10, 1), (Mp, 3, 1)) if args.roofline_only else ((1, 100, 8), (Mp, 30, 1))
+    for M, n_samples, rounds in sizes:
         kern[("gate_up", M)] = time_launch(
             lambda c, M=M: atsi.atsi_swiglu_gate_up(sess.ctx, tids[c]["gate"], tids[c]["up"], xs[4096].data_ptr(),
                                                     M, yb.data_ptr()), n_samples, rounds)
-        if args.roofline_only:
-            continue
         for r in ("q", "k", "o", "down"):
             K = shape.kn(r)[0]
             kern[(r, M)] = time_launch(lambda c, r=r, M=M, K=K: atsi.atsi_linear(
@@ -264,8 +264,6 @@ def bench_dense_layer(args, sess, timer, pcie_gbs=None):
                                "launch_us": stats_us(kern[("gate_up", Mp)])}
     log(f"gate/up GEMV {t_gemv * 1e6:.2f} us -> {gemv_bytes / t_gemv / 1e9:.0f} GB/s; gate/up GEMM "
         f"{t_gemm * 1e6:.1f} us -> {gemm_flops / t_gemm / 1e12:.0f} TFLOP/s")
-    if args.roofline_only:
-        return out
     per = {}
     for (r, M), v in kern.items():
         K, N = shape.kn("gate" if r == "gate_up" else r)
@@ -279,6 +277,13 @@ def bench_dense_layer(args, sess, timer, pcie_gbs=None):
             d["pct_mfma_peak"] = round(100 * d["TFLOPs"] / MFMA_F16_PEAK_TFLOPS, 1)
         per[f"{r}_M{M}"] = d
     out["kernels"] = per
+    if args.roofline_only:
+        # the layer's fused Q/K/V launch (norm, grouped-query expansion) once per size
+        for h, M in ((h1, 1), (hp, Mp)):
+            for c in range(R):
+                layer(c, h, M)
+        torch.cuda.synchronize()
+        return out
 
     # ---- prefill 512, HBM-resident
     gp = graph_of(sess.cs, calls(R, hp, Mp))
@@ -428,8 +433,9 @@ def bench_pcie(timer):
 
 # ---------------------------------------------------------------------------- MoE layer
 
-def bench_moe(sess, timer):
-    """30B-A3B-shaped MoE layer: decode (batch 1) and 512-token prefill."""
+def bench_moe(sess, timer, counters_only=False):
+    """30B-A3B-shaped MoE layer: decode (batch 1) and 512-token prefill.
+    counters_only: a few decode and prefill calls, no timing (for counter runs)."""
     import torch
 
     import synth
@@ -464,6 +470,13 @@ def bench_moe(sess, timer):
     yp = torch.empty((wl.prefill_m, H), dtype=torch.float16, device=dev)
     sess.cs.wait_stream(torch.cuda.current_stream())
     routed_bytes = k * shp.expert_bytes()
+    if counters_only:
+        for t in range(8):
+            layer(xd[t:t + 1], yd[t:t + 1])
+        for _ in range(3):
+            layer(xp, yp)
+        torch.cuda.synchronize()
+        return None
 
     def decode_all():  # 64 different tokens, one at a time
         for t in range(n_tok):
@@ -1107,7 +1120,9 @@ def main() -> int:
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-hybrid", action="store_true", help="skip the hybrid CPU-GPU and load-aware lines")
     ap.add_argument("--roofline-only", action="store_true",
-                    help="run only the roofline kernels and a 256 MiB copy (for rocprofv3 --pmc)")
+                    help="run only a few launches of every kernel (the dense layer's launches at batch 1 and "
+                         "512 tokens, the MoE layer at decode and prefill) and a 256 MiB copy, for "
+                         "rocprofv3 --pmc runs")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path, so --gpus must be 1", file=sys.stderr)
@@ -1125,6 +1140,7 @@ def main() -> int:
     pcie = None if args.roofline_only else bench_pcie(timer)
     dl = bench_dense_layer(args, sess, timer, pcie and pcie["ceiling_GBps"])
     if args.roofline_only:
+        bench_moe(sess, timer, counters_only=True)
         # copy of known size: calibrates the FETCH_SIZE / WRITE_SIZE counters
         src = torch.empty(256 << 20, dtype=torch.uint8, device="cuda")
         dst = torch.empty_like(src)
@@ -1278,7 +1294,90 @@ def summarize(trace_dir: str, fetch_dir: str, write_dir: str, commands: dict) ->
         fh.write("\n".join(md) + "\n")
 
 
+SQ_COUNTERS = ("SQ_WAVES", "SQ_INSTS_VALU", "SQ_INSTS_MFMA", "SQ_VALU_MFMA_BUSY_CYCLES", "SQ_INSTS_LDS",
+               "SQ_LDS_BANK_CONFLICT", "SQ_WAIT_INST_LDS", "SQ_BUSY_CYCLES")
+
+
+def summarize_counters(sq_dir: str, fetch_dir: str, write_dir: str, commands: dict) -> None:
+    """Write profiles/counters.md: per kernel and grid size (one row per
+    launch shape of the --roofline-only run), the median per dispatch of
+    HBM bytes (FETCH_SIZE, WRITE_SIZE scaled by a 256 MiB copy), matrix-core
+    and VALU instruction counts, MFMA busy cycles per CU-cycle, LDS
+    instructions and bank-conflict cycles."""
+    import csv
+    import glob
+
+    def rows(d):
+        hits = glob.glob(os.path.join(d, "*counter_collection.csv"))
+        if not hits:
+            raise FileNotFoundError(d)
+        return list(csv.DictReader(open(hits[0])))
+
+    def table(d):
+        per = {}
+        for r in rows(d):
+            grid = next((r[k] for k in r if k.lower().startswith("grid")), "")
+            key = (r["Kernel_Name"], grid)
+            per.setdefault(key, {}).setdefault(r["Counter_Name"], {}).setdefault(r["Dispatch_Id"], 0.0)
+            per[key][r["Counter_Name"]][r["Dispatch_Id"]] += float(r["Counter_Value"])
+            per[key].setdefault("dur_ns", {})[r["Dispatch_Id"]] = float(r["End_Timestamp"]) - float(r["Start_Timestamp"])
+        return {k: {c: float(np.median(list(v.values()))) for c, v in cs.items()} | {
+            "dispatches": max(len(v) for v in cs.values())} for k, cs in per.items()}
+
+    sq, fe, wr = table(sq_dir), table(fetch_dir), table(write_dir)
+    copy_f = [v["FETCH_SIZE"] for (n, _), v in fe.items() if "copyBuffer" in n]
+    copy_w = [v["WRITE_SIZE"] for (n, _), v in wr.items() if "copyBuffer" in n]
+    copy_bytes = 256 << 20
+    f_scale = copy_bytes / (max(copy_f) * 1024)
+    w_scale = copy_bytes / (max(copy_w) * 1024)
+
+    def short(name):
+        name = name.replace("(anonymous namespace)::", "").replace("atsi::", "")
+        return name.split("(")[0].replace("void ", "")[:70]
+
+    md = ["# Per-launch counters: every kernel of the dense and MoE layers", "",
+          "Commands (from the repository root, on one MI355X; one pass per run):", "",
+          *["    " + commands[k] for k in ("sq", "fetch", "write")], "",
+          f"HBM bytes = FETCH_SIZE x {f_scale:.4f} + WRITE_SIZE x {w_scale:.4f} KiB (the factors make a 256 MiB "
+          "device copy read and write 256 MiB).  Values are medians over the dispatches of each kernel and grid "
+          "size (the dispatch time is the counter run's, with every dispatch serialised).  SQ_BUSY_CYCLES sums "
+          "the 32 shader engines, so SQ_BUSY_CYCLES / 32 is the dispatch's length in shader clocks (clock = that "
+          "over the dispatch time); SQ_VALU_MFMA_BUSY_CYCLES sums the 1024 SIMDs, so MFMA busy = "
+          "SQ_VALU_MFMA_BUSY_CYCLES / (32 x SQ_BUSY_CYCLES) is the matrix cores' busy fraction at that clock.  "
+          "LDS conflict = SQ_LDS_BANK_CONFLICT / SQ_INSTS_LDS, cycles per LDS instruction.", "",
+          "| kernel | grid | dispatches | us | clock GHz | HBM MB | waves | VALU insts | MFMA insts | MFMA busy | "
+          "LDS insts | LDS conflict cyc/inst | LDS-wait cyc |", "|---|---|---|---|---|---|---|---|---|---|---|---|---|"]
+    keys = sorted(set(sq) | set(fe), key=lambda k: (short(k[0]), int(k[1] or 0)))
+    for k in keys:
+        if "copyBuffer" in k[0] or "fill" in k[0].lower():
+            continue
+        q, f, w = sq.get(k, {}), fe.get(k, {}), wr.get(k, {})
+        hbm = (f.get("FETCH_SIZE", float("nan")) * f_scale + w.get("WRITE_SIZE", float("nan")) * w_scale) * 1024
+        busy = q.get("SQ_VALU_MFMA_BUSY_CYCLES", float("nan")) / max(q.get("SQ_BUSY_CYCLES", 0.0) * 32.0, 1.0)
+        dur = q.get("dur_ns", float("nan"))
+        ghz = q.get("SQ_BUSY_CYCLES", float("nan")) / 32.0 / dur if dur == dur and dur > 0 else float("nan")
+        lds = q.get("SQ_INSTS_LDS", float("nan"))
+        conf = q.get("SQ_LDS_BANK_CONFLICT", float("nan")) / lds if lds and lds == lds else float("nan")
+        md.append(f"| `{short(k[0])}` | {k[1]} | {q.get('dispatches', f.get('dispatches', 0))} | {dur / 1e3:.1f} | "
+                  f"{ghz:.2f} | {hbm / 1e6:.2f} | "
+                  f"{q.get('SQ_WAVES', float('nan')):.0f} | {q.get('SQ_INSTS_VALU', float('nan')):.3g} | "
+                  f"{q.get('SQ_INSTS_MFMA', float('nan')):.3g} | {busy:.3f} | {lds:.3g} | {conf:.3f} | "
+                  f"{q.get('SQ_WAIT_INST_LDS', float('nan')):.3g} |")
+    with open(os.path.join(ROOT, "profiles", "counters.md"), "w") as fh:
+        fh.write("\n".join(md) + "\n")
+
+
 if __name__ == "__main__":
+    if len(sys.argv) > 1 and sys.argv[1] == "--summarize-counters":
+        # bench.py --summarize-counters SQ_DIR FETCH_DIR WRITE_DIR
+        summarize_counters(sys.argv[2], sys.argv[3], sys.argv[4], {
+            "sq": "rocprofv3 --pmc " + " ".join(SQ_COUNTERS) + " -f csv -d gpurun_out/prof_sq -o sq -- "
+                  "python -u bench.py --roofline-only",
+            "fetch": "rocprofv3 --pmc FETCH_SIZE -f csv -d gpurun_out/prof_fetch -o f -- "
+                     "python -u bench.py --roofline-only",
+            "write": "rocprofv3 --pmc WRITE_SIZE -f csv -d gpurun_out/prof_write -o w -- "
+                     "python -u bench.py --roofline-only"})
+        sys.exit(0)
     if len(sys.argv) > 1 and sys.argv[1] == "--summarize":
         # bench.py --summarize TRACE_DIR FETCH_DIR WRITE_DIR
         summarize(sys.argv[2], sys.argv[3], sys.argv[4], {
