@@ -936,6 +936,12 @@ def bench_hybrid(pcie_gbs, steps=30):
         smp = timed_samples(3)
         raw_c = [float(np.median(v)) for v in zip(*[hybrid.cpu_unit_raw(units, x) for x in smp])]
         raw_w = hybrid.median_timings(smp, "w", units)
+        # per promoted tensor: its copy time (the two tensors of a unit may be in flight together)
+        tw = [float(np.median([x[t]["w"] for x in smp if not math.isnan(x[t]["w"])]))
+              for (_, _, tids), g, v in zip(units, on_gpu, r) if g == 0 and v == 1 for t in tids
+              if any(not math.isnan(x[t]["w"]) for x in smp)]
+        tw_model = [configs.qbytes(*sess.shapes[t]) / (pcie_gbs * 1e9)
+                    for (_, _, tids), g, v in zip(units, on_gpu, r) if g == 0 and v == 1 for t in tids]
         raw_g = hybrid.median_timings(smp, "t_gpu", units)
         cpu_idx = [i for i, v in enumerate(r) if v == 0]
         prom_idx = [i for i, (g, v) in enumerate(zip(on_gpu, r)) if g == 0 and v == 1]
@@ -946,9 +952,9 @@ def bench_hybrid(pcie_gbs, steps=30):
                      "cpu_unit_us_vs_profile": [round(float(np.mean([raw_c[i] for i in cpu_idx])) * 1e6, 1),
                                                 round(float(np.mean([ref_c[i] for i in cpu_idx])) * 1e6, 1)]
                      if cpu_idx else None,
-                     "copy_us_vs_model": [round(float(np.mean([raw_w[i] for i in prom_idx])) * 1e6, 1),
-                                          round(float(np.mean([w[i] for i in prom_idx])) * 1e6, 1)]
-                     if prom_idx else None}
+                     "copy_us_per_tensor_vs_alone": [round(float(np.mean(tw)) * 1e6, 1),
+                                                     round(float(np.mean(tw_model)) * 1e6, 1)]
+                     if tw else None}
         if name == "dynamic_alg2":
             # Alg. 3 starts in this regime: its execution times are the
             # reference; a measured copy time replaces the model's w directly
@@ -959,8 +965,8 @@ def bench_hybrid(pcie_gbs, steps=30):
                           "w": list(w)}
         log(f"hybrid {name}: {t * 1e3:.2f} ms/token (predicted {res[name]['predicted_ms']} ms), "
             f"{res[name]['promoted_units']} units promoted, {res[name]['cpu_units']} on the CPU; CPU unit us "
-            f"(measured, profile) {res[name]['cpu_unit_us_vs_profile']}, copy us (measured, model) "
-            f"{res[name]['copy_us_vs_model']}")
+            f"(measured, profile) {res[name]['cpu_unit_us_vs_profile']}, copy us per tensor (measured, alone at "
+            f"the ceiling) {res[name]['copy_us_per_tensor_vs_alone']}")
     roles_host = {"+".join(rr): sum(1 for (_, r2, _), hu in zip(units, host_units) if hu and r2 == rr)
                   for rr in hybrid.ROLE_UNITS}
     roles_promoted = {"+".join(rr): sum(1 for (_, r2, _), hu, v in zip(units, host_units, rb) if hu and v and r2 == rr)
@@ -981,7 +987,7 @@ def bench_hybrid(pcie_gbs, steps=30):
             "threads": threads, "steps_timed": steps, "profile": profile, "policies": res}, ctx
 
 
-def bench_load_aware(ctx, phase_steps=40):
+def bench_load_aware(ctx, phase_steps=60):
     """Alg. 3 online: the Alg. 2 assignment kept fixed (static) against the
     load-aware loop (eps = 15 %, tau = 5 x the recent TPOT), over phases of
     idle, CPU load (busy processes on every host core the pool uses), PCIe

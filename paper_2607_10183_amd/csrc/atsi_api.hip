@@ -173,6 +173,7 @@ struct atsi_ctx {
   // CPU backend (atsi_set_cpu_backend): the caller's pool and pinned staging
   atsi::cpu::Pool* pool = nullptr;
   char* staging = nullptr;
+  char* staging_dev = nullptr;         // its device address (mapped pinned memory), or null
   size_t staging_bytes = 0;
   hipEvent_t cpu_ev = nullptr;         // a CPU launch's inputs have reached staging
   std::vector<float> cpu_x, cpu_acc;   // re-ordered fp32 inputs, fp32 products
@@ -809,6 +810,51 @@ atsi_status run_gpu_op(atsi_ctx* c, LinOp& op, const atsi_tid* tids, int ntids, 
 }
 
 // ---- CPU backend part of a launch ----
+// Activation transfers of a CPU-run launch (the paper's copy kernel): GPU
+// threads copy rows between device memory and mapped pinned staging, on the
+// compute stream, so these small transfers never queue behind weight copies
+// on the DMA engines.  rows x row_bytes, each side with its own pitch;
+// 16-byte units where rows, pitches and both bases allow, else 2-byte units.
+__global__ void stage_rows_kernel(const uint8_t* __restrict__ src, size_t spitch, uint8_t* __restrict__ dst,
+                                  size_t dpitch, size_t row_bytes, int rows, int vec16) {
+  const size_t per_row = vec16 ? row_bytes / 16 : row_bytes / 2;
+  const size_t total = per_row * (size_t)rows;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (size_t)gridDim.x * blockDim.x) {
+    const size_t r = i / per_row, col = i % per_row;
+    if (vec16)
+      *reinterpret_cast<uint4*>(dst + r * dpitch + col * 16) =
+          *reinterpret_cast<const uint4*>(src + r * spitch + col * 16);
+    else
+      *reinterpret_cast<uint16_t*>(dst + r * dpitch + col * 2) =
+          *reinterpret_cast<const uint16_t*>(src + r * spitch + col * 2);
+  }
+  __threadfence_system();  // host-side readers wait on an event recorded after the launch
+}
+
+// Copy rows on the compute stream: by the copy kernel when staging is mapped,
+// else by the DMA engines.  host_side: the staging address (host pointer).
+atsi_status stage_rows(atsi_ctx* c, const void* src, size_t spitch, void* dst, size_t dpitch, size_t row_bytes,
+                       int rows, bool to_host) {
+  if (rows <= 0 || row_bytes == 0) return ATSI_OK;
+  if (!c->staging_dev) {
+    HIP_TRY(c, hipMemcpy2DAsync(dst, dpitch, src, spitch, row_bytes, (size_t)rows,
+                                to_host ? hipMemcpyDeviceToHost : hipMemcpyHostToDevice, c->cs));
+    return ATSI_OK;
+  }
+  // the staging side is addressed through its device mapping
+  auto dev = [&](const void* h) { return c->staging_dev + (static_cast<const char*>(h) - c->staging); };
+  const uint8_t* s = static_cast<const uint8_t*>(to_host ? src : dev(src));
+  uint8_t* d = reinterpret_cast<uint8_t*>(to_host ? dev(dst) : dst);
+  const bool v16 = row_bytes % 16 == 0 && spitch % 16 == 0 && dpitch % 16 == 0 && ((uintptr_t)s % 16) == 0 &&
+                   ((uintptr_t)d % 16) == 0;
+  const size_t units = (v16 ? row_bytes / 16 : row_bytes / 2) * (size_t)rows;
+  const unsigned blocks = (unsigned)std::min<size_t>((units + 255) / 256, 1024);
+  hipLaunchKernelGGL(stage_rows_kernel, dim3(blocks), dim3(256), 0, c->cs, s, spitch, d, dpitch, row_bytes, rows,
+                     v16 ? 1 : 0);
+  HIP_TRY(c, hipGetLastError());
+  return ATSI_OK;
+}
+
 // Staging regions of the CPU segments of one launch: the input rows, the
 // residual (segment 0), and one packed output block per CPU segment.
 struct CpuPlan {
@@ -865,11 +911,11 @@ atsi_status cpu_fetch(atsi_ctx* c, const LinOp& op, const CpuPlan& p) {
   atsi_status st;
   int tr;
   if ((st = time_begin(c, kTimeD2H, p.tids, p.ntids, c->cs, &tr))) return st;
-  HIP_TRY(c, hipMemcpyAsync(p.x, op.x, (size_t)op.M * op.K * 2, hipMemcpyDeviceToHost, c->cs));
+  const size_t xrow = (size_t)op.K * 2;
+  if ((st = stage_rows(c, op.x, xrow, p.x, xrow, xrow, op.M, true))) return st;
   if (p.res) {  // segment 0 is then the plan's first
     const size_t row = (size_t)p.N[0] * 2;
-    HIP_TRY(c, hipMemcpy2DAsync(p.res, row, op.res, (size_t)op.seg[0].ldy * 2, row, (size_t)op.M,
-                                hipMemcpyDeviceToHost, c->cs));
+    if ((st = stage_rows(c, op.res, (size_t)op.seg[0].ldy * 2, p.res, row, row, op.M, true))) return st;
   }
   if ((st = time_end(c, tr, c->cs))) return st;
   HIP_TRY(c, hipEventRecord(c->cpu_ev, c->cs));
@@ -955,8 +1001,7 @@ atsi_status cpu_finish(atsi_ctx* c, const LinOp& op, const CpuPlan& p) {
     const Seg& sg = op.seg[p.seg[i]];
     void* dst = (p.seg[i] == 0 && op.y32) ? (void*)op.y32 : (void*)sg.y;
     const size_t row = (size_t)p.width[i] * p.elem[i];
-    HIP_TRY(c, hipMemcpy2DAsync(dst, (size_t)sg.ldy * p.elem[i], p.out[i], row, row, (size_t)M,
-                                hipMemcpyHostToDevice, c->cs));
+    if ((st = stage_rows(c, p.out[i], row, dst, (size_t)sg.ldy * p.elem[i], row, M, false))) return st;
   }
   return time_end(c, tr, c->cs);
 }
@@ -1751,6 +1796,14 @@ atsi_status atsi_set_cpu_backend(atsi_ctx* c, atsi_cpu_pool* pool, void* staging
   c->pool = pool ? &pool->pool : nullptr;
   c->staging = pool ? static_cast<char*>(staging) : nullptr;
   c->staging_bytes = pool ? staging_bytes : 0;
+  c->staging_dev = nullptr;
+  if (pool) {
+    void* d = nullptr;
+    if (hipHostGetDevicePointer(&d, staging, 0) == hipSuccess)
+      c->staging_dev = static_cast<char*>(d);
+    else
+      (void)hipGetLastError();  // not mapped: activation transfers go through the DMA engines
+  }
   return ATSI_OK;
 }
 

@@ -108,17 +108,29 @@ class Snapshotter:
 
     SERIES = ("t_gpu", "t_cpu", "w")
 
-    def __init__(self, units, model: dict, reference: dict):
+    def __init__(self, units, model: dict, reference: dict, window: int = 4):
         self.units = units
         self.model = {k: list(model[k]) for k in self.SERIES}
         self.reference = {k: list(reference[k]) for k in self.SERIES}
+        self.window = window
+        self.reads = []
 
-    def raw(self, tm):
-        return {"t_gpu": median_timings([tm], "t_gpu", self.units), "t_cpu": cpu_unit_raw(self.units, tm),
-                "w": median_timings([tm], "w", self.units)}
+    def raw(self, reads):
+        cpu = [cpu_unit_raw(self.units, tm) for tm in reads]
+        return {"t_gpu": median_timings(reads, "t_gpu", self.units),
+                "t_cpu": [float(np.nanmedian(v)) if not all(math.isnan(x) for x in v) else math.nan
+                          for v in zip(*cpu)],
+                "w": median_timings(reads, "w", self.units)}
+
+    def record(self, tm):
+        self.reads = (self.reads + [tm])[-self.window:]
 
     def __call__(self, tm):
-        fresh = self.raw(tm)
+        """Snapshot from the last `window` rounds' timing reads (per-unit
+        medians, so one round disturbed by the scheduler of the host does not
+        trigger a re-scheduling by itself)."""
+        self.record(tm)
+        fresh = self.raw(self.reads)
         out = {}
         for k in self.SERIES:
             f, ref, mod = fresh[k], self.reference[k], self.model[k]
@@ -136,15 +148,24 @@ class Controller:
     def __init__(self, sess, units, on_gpu, snapshotter, eps=0.15, tau_tpot=5.0):
         self.sess, self.units, self.on_gpu = sess, units, list(on_gpu)
         self.snap = snapshotter
+        self.tau_tpot = tau_tpot
         self.r = atsi.atsi_rescheduler_create(len(units), eps, tau_tpot)
         self.rb = None
+        self.t_last = None
         self.reschedules = 0
 
     def step(self, now_s, tpot_s, timings):
+        """One round's decision: (re-scheduled, deviation or None).  Within
+        tau of the last re-scheduling Alg. 3 keeps the assignment whatever the
+        deviation, so the snapshot is only recorded then."""
+        if self.t_last is not None and now_s - self.t_last < self.tau_tpot * tpot_s:
+            self.snap.record(timings)
+            return False, None
         tg, tc, c, w = self.snap(timings)
         rb, did, d = atsi.atsi_rescheduler_step(self.r, self.on_gpu, tg, tc, c, w, now_s, tpot_s)
         if did:
             self.reschedules += 1
+            self.t_last = now_s
             self.apply(rb)
         return did, d
 
