@@ -966,7 +966,9 @@ atsi_status cpu_finish(atsi_ctx* c, const LinOp& op, const CpuPlan& p) {
     uint16_t* o16 = reinterpret_cast<uint16_t*>(p.out[i]);
     float* o32 = reinterpret_cast<float*>(p.out[i]);
     const int W = p.width[i];
-    for (int m = 0; m < M; ++m)
+    // the epilogue over rows [m0, m1); split over the pool when it is large
+    auto epilogue = [&](int m0, int m1) {
+    for (int m = m0; m < m1; ++m)
       for (int n = 0; n < N; ++n) {
         float v = acc[(size_t)m * N + n] * inv[m];
         if (op.swiglu) {
@@ -985,6 +987,13 @@ atsi_status cpu_finish(atsi_ctx* c, const LinOp& op, const CpuPlan& p) {
         else
           o16[(size_t)m * W + n] = atsi::cpu::float_to_half_rn(v);
       }
+    };
+    if ((size_t)M * N < (1u << 16) || M < 2) {
+      epilogue(0, M);
+    } else {
+      const int T = c->pool->size();
+      c->pool->run([&](int t) { epilogue((int)((int64_t)M * t / T), (int)((int64_t)M * (t + 1) / T)); });
+    }
     const double secs = std::chrono::duration<double>(std::chrono::steady_clock::now() - t_start).count();
     if (c->timing) {
       double share[2] = {1.0, 0.0};
