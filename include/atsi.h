@@ -457,7 +457,10 @@ atsi_status atsi_rescheduler_destroy(atsi_rescheduler* r);
 
 /* The host-CPU backend (the CPU side of the hybrid, Sec. 4.3-4.4): a pool of
  * worker threads (the calling thread takes part as one of them).  A pool
- * runs one product at a time; it may serve several contexts. */
+ * runs one product at a time; it may serve several contexts and must outlive
+ * every context it is attached to (destroy it after atsi_destroy, or after
+ * atsi_set_cpu_backend(ctx, NULL, ...)).  Idle workers spin briefly, then
+ * yield, then sleep. */
 typedef struct atsi_cpu_pool atsi_cpu_pool;
 atsi_status atsi_cpu_pool_create(int32_t threads, atsi_cpu_pool** out);
 atsi_status atsi_cpu_pool_destroy(atsi_cpu_pool* pool);
@@ -477,7 +480,10 @@ atsi_status atsi_cpu_linear(atsi_cpu_pool* pool, const uint8_t* codes, const uin
  * input rows (and residual) to staging on the compute stream, waits for
  * them, computes on the pool and copies its outputs back on the compute
  * stream, so the calling thread blocks for the CPU part (the backend switches
- * are the activation transfers c_i of Sec. 4.4.1).  It needs M*K*2 bytes for
+ * are the activation transfers c_i of Sec. 4.4.1).  When staging is mapped
+ * pinned memory these copies are done by a small kernel (the paper's copy
+ * kernel), so they never queue behind weight copies on the DMA engines;
+ * otherwise by hipMemcpy2DAsync.  It needs M*K*2 bytes for
  * the input, M*N*2 per output (4 for an fp32 one, twice for a SwiGLU pair)
  * and M*N*2 for a residual, each rounded up to 256 (ATSI_E_WORKSPACE if
  * staging is too small).  The library uses staging until atsi_destroy or the
