@@ -1020,20 +1020,22 @@ def bench_load_aware(ctx, phase_steps=60):
         ctx["configure"]([1 - g for g in on_gpu], [1 - v for v in rb0])
         ctrl = None
         if policy == "load_aware":
-            ctrl = hybrid.Controller(sess, units, on_gpu, hybrid.Snapshotter(units, ctx["model"], ctx["reference"]))
+            ctrl = hybrid.Controller(sess, units, on_gpu,
+                                     hybrid.Snapshotter(units, ctx["model"], ctx["reference"], window=3))
             ctrl.rb = list(rb0)
         sess.sync()
         rec = {}
         recent = []
         decide_s = 0.0
         t_idx = 0
+        events = []  # (token, CPU units after the re-scheduling)
         for name, load in phases:
             tpots = []
             with LoadInjector(**load):
                 for _ in range(phase_steps):
-                    # every fourth token is measured (HIP events around each
+                    # every other token is measured (HIP events around each
                     # launch, copy and transfer) and feeds the decision
-                    measured = t_idx % 4 == 0
+                    measured = t_idx % 2 == 0
                     t_idx += 1
                     if measured:
                         sess.set_timing(True)
@@ -1048,21 +1050,27 @@ def bench_load_aware(ctx, phase_steps=60):
                     tpots.append(t1 - t0)
                     recent = (recent + [t1 - t0])[-8:]
                     if ctrl is not None and measured:
-                        ctrl.step(t1, float(np.median(recent)), tm)
+                        did, _ = ctrl.step(t1, float(np.median(recent)), tm)
                         decide_s += time.perf_counter() - t1
+                        if did:
+                            events.append([t_idx - 1, int(sum(1 for v in ctrl.rb if v == 0))])
             rec[name] = {"ms_per_token_mean": round(float(np.mean(tpots)) * 1e3, 3),
-                         "ms_per_token_median": round(float(np.median(tpots)) * 1e3, 3)}
+                         "ms_per_token_median": round(float(np.median(tpots)) * 1e3, 3),
+                         "ms_per_token": [round(v * 1e3, 1) for v in tpots]}
             if ctrl is not None:
                 rec[name]["cpu_units_now"] = int(sum(1 for v in ctrl.rb if v == 0))
         if ctrl is not None:
             rec["reschedules"] = ctrl.reschedules
-            rec["decision_ms_per_measured_token"] = round(decide_s / (len(phases) * phase_steps / 4) * 1e3, 3)
+            rec["reschedule_events"] = events
+            rec["decision_ms_per_measured_token"] = round(decide_s / (len(phases) * phase_steps / 2) * 1e3, 3)
             ctrl.close()
         out[policy] = rec
-        log(f"load-aware {policy}: {rec}")
+        log(f"load-aware {policy}: " + str({k: ({kk: vv for kk, vv in v.items() if kk != "ms_per_token"}
+                                                 if isinstance(v, dict) else v) for k, v in rec.items()}))
     return {"workload": "the hybrid_decode stack, " + ", ".join(f"{n} ({phase_steps} tokens)" for n, _ in phases),
             "eps": 0.15, "tau": "5 x median TPOT of the last 8 tokens",
-            "measurement": "every fourth token runs with per-launch timing and feeds the decision (both policies)",
+            "measurement": "every other token runs with per-launch timing and feeds the decision (both policies); "
+                           "snapshots are medians over the last three measured tokens",
             "policies": out}
 
 
@@ -1273,13 +1281,28 @@ def summarize(trace_dir: str, fetch_dir: str, write_dir: str, commands: dict) ->
 
     prof = os.path.join(ROOT, "profiles")
     stats = list(csv.DictReader(open(one(os.path.join(trace_dir, "*kernel_stats.csv")))))
-    lines = ["# Kernel durations: full bench run (dense layer, linear4096, MoE layer, stacks)", "",
+    lines = ["# Kernel durations: the default bench run (dense layer, linear4096, MoE layer, stacks, hybrid, "
+             "load-aware; HIP events of the bench itself under the tracer read slightly slower)", "",
              "Command (from the repository root, on one MI355X):", "",
              "    " + commands["trace"], "",
              "| kernel | calls | avg us | min us | max us | share |", "|---|---|---|---|---|---|"]
     for r in sorted(stats, key=lambda r: -float(r["TotalDurationNs"]))[:30]:
         lines.append(f"| `{r['Name'][:110]}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
                      f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} | {float(r['Percentage']):.1f}% |")
+    runs_path = os.path.join(trace_dir, "trace_reduced.json")
+    if os.path.exists(runs_path):
+        red = json.load(open(runs_path))
+        lines += ["", "The two roofline kernels in their measurement windows (the longest run of consecutive "
+                  "dispatches of that kernel and grid: the bench's back-to-back timed launches), from the "
+                  "same trace (`bench.py --reduce-trace`):", "",
+                  "| kernel | grid | dispatches in the run | run avg us | all calls | avg us over all calls |",
+                  "|---|---|---|---|---|---|"]
+        for needle, grid in (("q4_gemv1_kernel<7, true, 4>", "262144"),
+                             ("q4_gemm_wide_kernel<true, false, false>", "114688")):
+            for r in red:
+                if needle in r["kernel"] and r["grid"] == grid:
+                    lines.append(f"| `{needle}` | {grid} | {r['longest_run']} | {r['longest_run_avg_us']:.2f} | "
+                                 f"{r['calls']} | {r['avg_us']:.2f} |")
     with open(os.path.join(prof, "kernels_bench.md"), "w") as fh:
         fh.write("\n".join(lines) + "\n")
 
@@ -1328,6 +1351,48 @@ def summarize(trace_dir: str, fetch_dir: str, write_dir: str, commands: dict) ->
         json.dump(out, fh, indent=1)
     with open(os.path.join(prof, "traffic.md"), "w") as fh:
         fh.write("\n".join(md) + "\n")
+
+
+def reduce_trace(trace_csv: str, out_json: str) -> None:
+    """Reduce a rocprofv3 kernel trace (one row per dispatch; too large to keep)
+    to per-(kernel, grid) duration statistics, plus, for every kernel and grid,
+    its longest run of consecutive dispatches: the roofline kernels are timed
+    as long runs of back-to-back launches of one shape, so that run is the
+    bench's own measurement window."""
+    import csv
+    rows = []
+    with open(trace_csv) as fh:
+        for r in csv.DictReader(fh):
+            if "Grid_Size_X" in r:
+                grid = str(int(r["Grid_Size_X"]) * int(r["Grid_Size_Y"]) * int(r["Grid_Size_Z"]))
+            else:
+                grid = r.get("Grid_Size", "")
+            rows.append((int(r["Start_Timestamp"]), int(r["End_Timestamp"]), r["Kernel_Name"], grid))
+    rows.sort()
+    stats, runs = {}, {}
+    cur, run = None, []
+    for t0, t1, name, grid in rows + [(0, 0, None, None)]:
+        key = (name, grid)
+        if key != cur:
+            if cur is not None and cur[0] is not None and len(run) > len(runs.get(cur, [])):
+                runs[cur] = run
+            cur, run = key, []
+        if name is None:
+            break
+        d = (t1 - t0) / 1e3
+        run.append(d)
+        st = stats.setdefault(key, [0, 0.0, 1e30, 0.0])
+        st[0] += 1
+        st[1] += d
+        st[2] = min(st[2], d)
+        st[3] = max(st[3], d)
+    out = []
+    for (name, grid), (n, tot, lo, hi) in stats.items():
+        r = runs.get((name, grid), [])
+        out.append({"kernel": name, "grid": grid, "calls": n, "avg_us": tot / n, "min_us": lo, "max_us": hi,
+                    "longest_run": len(r), "longest_run_avg_us": (sum(r) / len(r)) if r else None})
+    with open(out_json, "w") as fh:
+        json.dump(out, fh)
 
 
 SQ_COUNTERS = ("SQ_WAVES", "SQ_INSTS_VALU", "SQ_INSTS_MFMA", "SQ_VALU_MFMA_BUSY_CYCLES", "SQ_INSTS_LDS",
@@ -1404,6 +1469,10 @@ def summarize_counters(sq_dir: str, fetch_dir: str, write_dir: str, commands: di
 
 
 if __name__ == "__main__":
+    if len(sys.argv) > 1 and sys.argv[1] == "--reduce-trace":
+        # bench.py --reduce-trace TRACE_CSV OUT_JSON
+        reduce_trace(sys.argv[2], sys.argv[3])
+        sys.exit(0)
     if len(sys.argv) > 1 and sys.argv[1] == "--summarize-counters":
         # bench.py --summarize-counters SQ_DIR FETCH_DIR WRITE_DIR
         summarize_counters(sys.argv[2], sys.argv[3], sys.argv[4], {
@@ -1418,7 +1487,7 @@ if __name__ == "__main__":
         # bench.py --summarize TRACE_DIR FETCH_DIR WRITE_DIR
         summarize(sys.argv[2], sys.argv[3], sys.argv[4], {
             "trace": "rocprofv3 --kernel-trace --stats -f csv -d gpurun_out/prof_trace -o bench -- "
-                     "python -u bench.py --no-cpu-baseline",
+                     "python -u bench.py",
             "fetch": "rocprofv3 --pmc FETCH_SIZE -f csv -d gpurun_out/prof_fetch -o f -- "
                      "python -u bench.py --roofline-only",
             "write": "rocprofv3 --pmc WRITE_SIZE -f csv -d gpurun_out/prof_write -o w -- "
