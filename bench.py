@@ -785,24 +785,25 @@ def bench_moe_stack(pcie_gbs):
 # ---------------------------------------------------------------------------- hybrid CPU-GPU decode (Alg. 1-3)
 
 class LoadInjector:
-    """Background load for the load-aware runs: `cpu` processes each busy
-    `duty` of the time on the host cores (6 ms busy per 10 ms at 0.6), and
-    `gpu_link` a thread alternating a 256 MiB host-to-device copy and an
-    8192^3 fp16 matrix product on a stream of its own (PCIe and compute
-    pressure on the GPU)."""
+    """Background load for the load-aware runs, each in processes of its own
+    (a thread of this process would compete with the bench for the
+    interpreter lock): `cpu` processes each busy `duty` of the time on the
+    host cores (6 ms busy per 10 ms at 0.6), and `gpu_link` one process that
+    alternates a 256 MiB host-to-device copy and an 8192^3 fp16 matrix product
+    on the GPU (PCIe and compute pressure).  The GPU load is running when the
+    context is entered and stops cleanly (a stop file) when it is left."""
 
     def __init__(self, cpu: int = 0, duty: float = 1.0, gpu_link: bool = False):
         self.cpu, self.duty, self.gpu_link = cpu, duty, gpu_link
-        self.procs, self.thread, self.stop = [], None, None
+        self.procs, self.gpu_proc, self.stop_path = [], None, None
 
     def __enter__(self):
         import subprocess
-        import threading
-        import torch
+        import tempfile
         busy, idle = 0.010 * self.duty, 0.010 * (1.0 - self.duty)
         prog = ("import time\n"
                 "while True:\n"
-                f"    t = time.perf_counter()\n"
+                "    t = time.perf_counter()\n"
                 f"    while time.perf_counter() - t < {busy}:\n"
                 "        pass\n"
                 f"    if {idle} > 0:\n"
@@ -810,21 +811,24 @@ class LoadInjector:
         for _ in range(self.cpu):
             self.procs.append(subprocess.Popen([sys.executable, "-c", prog]))
         if self.gpu_link:
-            self.stop = threading.Event()
-            src = torch.empty(256 << 20, dtype=torch.uint8).pin_memory()
-            dst = torch.empty(256 << 20, dtype=torch.uint8, device="cuda")
-            a = torch.randn(8192, 8192, device="cuda").half()
-            b = torch.randn(8192, 8192, device="cuda").half()
-            st = torch.cuda.Stream()
-
-            def pump():
-                while not self.stop.is_set():
-                    with torch.cuda.stream(st):
-                        dst.copy_(src, non_blocking=True)
-                        torch.mm(a, b)
-                    st.synchronize()
-            self.thread = threading.Thread(target=pump, daemon=True)
-            self.thread.start()
+            fd, self.stop_path = tempfile.mkstemp(prefix="atsi_load_stop_")
+            os.close(fd)
+            os.unlink(self.stop_path)
+            gprog = ("import os, sys, torch\n"
+                     "src = torch.empty(256 << 20, dtype=torch.uint8).pin_memory()\n"
+                     "dst = torch.empty(256 << 20, dtype=torch.uint8, device='cuda')\n"
+                     "a = torch.randn(8192, 8192, device='cuda').half()\n"
+                     "b = torch.randn(8192, 8192, device='cuda').half()\n"
+                     "torch.cuda.synchronize()\n"
+                     "print('ready', flush=True)\n"
+                     f"while not os.path.exists({self.stop_path!r}):\n"
+                     "    dst.copy_(src, non_blocking=True)\n"
+                     "    torch.mm(a, b)\n"
+                     "    torch.cuda.synchronize()\n")
+            self.gpu_proc = subprocess.Popen([sys.executable, "-c", gprog], stdout=subprocess.PIPE, text=True)
+            line = self.gpu_proc.stdout.readline()
+            if line.strip() != "ready":
+                raise RuntimeError("the GPU load process did not start")
         return self
 
     def __exit__(self, *exc):
@@ -832,9 +836,15 @@ class LoadInjector:
             p.kill()
         for p in self.procs:
             p.wait()
-        if self.thread is not None:
-            self.stop.set()
-            self.thread.join()
+        if self.gpu_proc is not None:
+            import subprocess
+            open(self.stop_path, "w").close()
+            try:
+                self.gpu_proc.wait(timeout=60)
+            except subprocess.TimeoutExpired:
+                self.gpu_proc.kill()
+                self.gpu_proc.wait()
+            os.unlink(self.stop_path)
         return False
 
 
