@@ -1077,7 +1077,18 @@ def bench_load_aware(ctx, phase_steps=60):
         out[policy] = rec
         log(f"load-aware {policy}: " + str({k: ({kk: vv for kk, vv in v.items() if kk != "ms_per_token"}
                                                  if isinstance(v, dict) else v) for k, v in rec.items()}))
+    # the paper's figure of merit: how much of the static policy's TPOT
+    # increase under a load the load-aware policy avoids (idle: the static
+    # policy's first idle phase)
+    base = out["static"]["idle"]["ms_per_token_mean"]
+    reduction = {}
+    for name, _ in phases[1:3]:
+        inc_s = out["static"][name]["ms_per_token_mean"] - base
+        inc_a = out["load_aware"][name]["ms_per_token_mean"] - base
+        reduction[name] = round(1.0 - inc_a / inc_s, 3) if inc_s > 0 else None
+    log(f"load-aware: TPOT-increase reduction against the static policy {reduction}")
     return {"workload": "the hybrid_decode stack, " + ", ".join(f"{n} ({phase_steps} tokens)" for n, _ in phases),
+            "tpot_increase_reduction": reduction,
             "eps": 0.15, "tau": "5 x median TPOT of the last 8 tokens",
             "measurement": "every other token runs with per-launch timing and feeds the decision (both policies); "
                            "snapshots are medians over the last three measured tokens",
