@@ -1190,7 +1190,7 @@ def main() -> int:
                          "rocprofv3 --pmc runs")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path, so --gpus must be 1", file=sys.stderr)
+        print("bench.py measures one GPU: the library has no multi-GPU path, so --gpus must be 1", file=sys.stderr)
         return 2
     if args.steps < 1 or args.warmup < 0:
         print("--steps must be >= 1 and --warmup >= 0", file=sys.stderr)

@@ -1,6 +1,6 @@
 """Acceptance checks shared by the GPU parity tests.
 
-spec gate : |y - y_ref| <= 1e-2 * zeta elementwise, zeta = |W| . |x| for one
+required gate : |y - y_ref| <= 1e-2 * zeta elementwise, zeta = |W| . |x| for one
                   linear layer (x the stage's own input) and its propagated form
                   for composite stages.
 tight gate      : the same with a smaller factor.  For one linear it follows the
@@ -15,7 +15,7 @@ row rel-L2 gate : ||y_r - y_ref_r|| / ||y_ref_r|| <= 1e-3 for every row r (token
 """
 import numpy as np
 
-NORTH_STAR = 1e-2
+REQUIRED = 1e-2
 TIGHT = 2.5e-3
 REL_L2 = 1e-3
 
@@ -40,7 +40,7 @@ def check(y, y_ref, zeta, name="", tight=TIGHT, rel_l2=REL_L2):
     err = np.abs(y - y_ref)
     assert np.all(np.isfinite(y)), f"{name}: non-finite output"
     worst = float(np.max(err / np.maximum(zeta, 1e-30))) if err.size else 0.0
-    assert np.all(err <= NORTH_STAR * zeta), f"{name}: north-star bound violated (max err/zeta {worst:.3e})"
+    assert np.all(err <= REQUIRED * zeta), f"{name}: required 1e-2 bound violated (max err/zeta {worst:.3e})"
     assert np.all(err <= tight * zeta), f"{name}: tight bound violated (max err/zeta {worst:.3e} > {tight:.3e})"
     rows_y = (y - y_ref).reshape(-1, y_ref.shape[-1]) if y_ref.ndim else (y - y_ref).reshape(1, 1)
     rows_r = y_ref.reshape(rows_y.shape)

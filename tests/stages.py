@@ -16,7 +16,7 @@ from tests.parity import check, tight_eps
 # with its SiLU-derivative term, stays the tight one for this stage.
 SWIGLU_ROW_L2 = 2e-2
 # Whole composite stages (a layer, an MoE FFN) free-running from the oracle's
-# own intermediates: per-token relative L2 at the 1e-2 of the benchmark spec; the
+# own intermediates: per-token relative L2 at the required 1e-2 bound; the
 # stages inside are gated teacher-forced.
 COMPOSITE_ROW_L2 = 1e-2
 

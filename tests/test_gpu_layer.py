@@ -102,7 +102,7 @@ WIDE_ATTN = configs.DenseShape(hidden=4096, n_heads=64, n_kv=4, head_dim=128, in
                                      (configs.DenseShape(), 1), (configs.DenseShape(), 8),
                                      (configs.DenseShape(), 512), (WIDE_ATTN, 2048)])
 def test_decoder_layer_parity(sess, shape, M):
-    """The layer's output against the oracle layer (spec bound and
+    """The layer's output against the oracle layer (required 1e-2 bound and
     per-token norm), and every stage inside it teacher-forced: each projection
     against the oracle on the GPU's own fp16 input to it, at that stage's
     tight bound."""
