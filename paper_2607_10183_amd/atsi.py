@@ -115,6 +115,7 @@ _SIGS = {
     "atsi_debug_unpack": ([_P, ctypes.c_int32, _P], ctypes.c_int),
     "atsi_set_debug": ([_P, ctypes.c_uint32], ctypes.c_int),
     "atsi_set_zero_copy": ([_P, ctypes.c_int32], ctypes.c_int),
+    "atsi_set_moe_light_rows": ([_P, ctypes.c_int32], ctypes.c_int),
     "atsi_solve_placement": ([ctypes.POINTER(atsi_placement_problem), _P, ctypes.POINTER(ctypes.c_double)],
                              ctypes.c_int),
     "atsi_schedule_transfers": ([ctypes.POINTER(atsi_transfer_problem), _P, ctypes.POINTER(ctypes.c_double)],
@@ -280,6 +281,10 @@ def atsi_set_debug(ctx: int, flags: int) -> None:
 
 def atsi_set_zero_copy(ctx: int, enable: bool) -> None:
     _check(ctx, lib().atsi_set_zero_copy(ctx, 1 if enable else 0))
+
+
+def atsi_set_moe_light_rows(ctx: int, rows: int) -> None:
+    _check(ctx, lib().atsi_set_moe_light_rows(ctx, int(rows)))
 
 
 class _TransferArrays:

@@ -163,6 +163,7 @@ struct atsi_ctx {
   bool fused_layer = false;       // batch-1 decode layers take the single persistent launch
   uint32_t debug = 0;             // ATSI_DEBUG_* flags (atsi_set_debug)
   bool zero_copy = false;         // decode experts on host are read in place (atsi_set_zero_copy)
+  int moe_light_rows = -1;        // prefill experts routed at most this many pairs take the light kernels (-1: by call size)
   char* static_scratch = nullptr;  // this device's copy of the allocation-free entry point's scratch array
   hipStream_t ts2 = nullptr;      // the caller's second transfer stream, or null: copies alternate between ts and ts2
   unsigned copy_turn = 0;
@@ -1170,6 +1171,13 @@ atsi_status run_moe(atsi_ctx* c, const atsi_moe* m, const __half* x, int Mi, __h
   const int Mk = Mi * k;
   const bool gemv = Mi <= 4;
   const int bm = expert_tile_rows(gemv);
+  // experts routed at most `light` pairs run on the light-expert kernels; by
+  // default all of them while the call routes at most 32 pairs per expert on
+  // average, none beyond (measured on MI355X at 64, 512 and 2048 tokens of
+  // the 128-expert layer)
+  int light = c->moe_light_rows;
+  if (light < 0) light = Mk <= kLightAutoPairs * E ? kMoeLightRowsMax : 0;
+  if (gemv || !light_supported(H, I) || (size_t)Mk * std::max(H, I) * 2 >= ((size_t)1 << 31)) light = 0;
   float* part = (float*)sc.take(router_partial_floats(Mi, H, E), 4);
   int32_t* idx = dbg && dbg->idx ? dbg->idx : (int32_t*)sc.take(Mk, 4);
   float* p = dbg && dbg->p ? dbg->p : (float*)sc.take(Mk, 4);
@@ -1180,9 +1188,12 @@ atsi_status run_moe(atsi_ctx* c, const atsi_moe* m, const __half* x, int Mi, __h
   int32_t* order = (int32_t*)sc.take(E, 4);
   int32_t* tiles = (int32_t*)sc.take(2 * ((size_t)Mk / bm + E + 1), 4);
   int32_t* ntiles = (int32_t*)sc.take(1, 4);
+  int32_t* ltiles = light ? (int32_t*)sc.take(2 * ((size_t)Mk / kLightTileRows + E + 1), 4) : nullptr;
+  int32_t* nltiles = light ? (int32_t*)sc.take(1, 4) : nullptr;
   __half* h = sc.take((size_t)Mk * I);
   __half* out = dbg && dbg->expert_out ? (__half*)dbg->expert_out : sc.take((size_t)Mk * H);
-  if (!part || !idx || !p || !counts || !offsets || !perm || !inv || !order || !tiles || !ntiles || !h || !out)
+  if (!part || !idx || !p || !counts || !offsets || !perm || !inv || !order || !tiles || !ntiles || !h || !out ||
+      (light && (!ltiles || !nltiles)))
     return fail(c, ATSI_E_WORKSPACE, "scratch too small for a %d-token MoE layer", Mi);
   const ExpertW* table = reinterpret_cast<const ExpertW*>(c->ws + tb->off);
   const uint8_t* resident = reinterpret_cast<const uint8_t*>(c->ws + tb->off + align_up((size_t)E * sizeof(ExpertW)));
@@ -1197,7 +1208,8 @@ atsi_status run_moe(atsi_ctx* c, const atsi_moe* m, const __half* x, int Mi, __h
   const bool by_pair = gemv && (tb->n_streamed == 0 || c->zero_copy);
   const bool want_buckets = dbg && (dbg->counts || dbg->offsets || dbg->perm || dbg->inv_perm);
   if (!by_pair || want_buckets) {
-    e = launch_bucket(idx, Mi, k, E, resident, bm, counts, offsets, perm, inv, order, tiles, ntiles, c->cs);
+    e = launch_bucket(idx, Mi, k, E, resident, bm, light, counts, offsets, perm, inv, order, tiles, ntiles, ltiles,
+                      nltiles, c->cs);
     if (e != hipSuccess) return hip_fail(c, e, "bucket launch");
   }
   if (tb->n_streamed > 0 && !by_pair) {
@@ -1216,6 +1228,7 @@ atsi_status run_moe(atsi_ctx* c, const atsi_moe* m, const __half* x, int Mi, __h
   a.out = out;
   a.inv_r = inv_r;
   a.k = k;
+  a.M = Mi;
   a.H = H;
   a.I = I;
   if (by_pair) {
@@ -1224,9 +1237,15 @@ atsi_status run_moe(atsi_ctx* c, const atsi_moe* m, const __half* x, int Mi, __h
     a.n_experts = E;
   }
   // HBM-resident experts first: they run while the host learns which
-  // streamed experts are needed.
-  const int bound = bm == 1 ? Mk : Mk / bm + std::min(E, Mk);
+  // streamed experts are needed.  Grid bounds: tiles of bm rows over experts
+  // routed more than `light` pairs, and light tiles over the others.
+  const int bound = bm == 1 ? Mk : Mk / bm + std::min(E, Mk / (light + 1));
+  const int lbound = light ? std::min(Mk / kLightTileRows + E, E * ((light + kLightTileRows - 1) / kLightTileRows)) : 0;
+  MoeArgs al = a;
+  al.tiles = ltiles;
+  al.n_tiles = nltiles;
   if ((e = launch_expert_gateup(a, bound, gemv, c->cs)) != hipSuccess) return hip_fail(c, e, "expert gate/up launch");
+  if ((e = launch_light_gateup(al, lbound, c->cs)) != hipSuccess) return hip_fail(c, e, "light expert gate/up launch");
   if (by_pair) {  // every expert resident: the down launch also combines
     a.store_out = dbg && dbg->expert_out;
     if ((e = launch_expert_down_combine(a, Mi, p, res, y, c->cs)) != hipSuccess)
@@ -1234,6 +1253,7 @@ atsi_status run_moe(atsi_ctx* c, const atsi_moe* m, const __half* x, int Mi, __h
     return gather_expert_h(c, dbg, h, nullptr, Mk, I);
   }
   if ((e = launch_expert_down(a, bound, gemv, c->cs)) != hipSuccess) return hip_fail(c, e, "expert down launch");
+  if ((e = launch_light_down(al, lbound, c->cs)) != hipSuccess) return hip_fail(c, e, "light expert down launch");
 
   if (tb->n_streamed > 0) {
     HIP_TRY(c, hipEventSynchronize(c->counts_ev));
@@ -1250,8 +1270,9 @@ atsi_status run_moe(atsi_ctx* c, const atsi_moe* m, const __half* x, int Mi, __h
     const int B = std::max(1, std::min(kBatchExp, c->n_slots / 3));
     for (size_t b0 = 0; b0 < act.size(); b0 += B) {
       std::vector<int> held;
-      MoeArgs ba = a;
+      MoeArgs ba = a, bl = a;  // tiles of bm rows / light tiles of the batch
       ba.nb = 0;
+      bl.nb = 0;
       const int nbx = (int)std::min<size_t>(B, act.size() - b0);
       for (int b = 0; b < nbx; ++b) {
         const int ex = act[b0 + b];
@@ -1259,20 +1280,28 @@ atsi_status run_moe(atsi_ctx* c, const atsi_moe* m, const __half* x, int Mi, __h
         if ((st = acquire(c, m->gate[ex], &ba.bw[b].gate, held)) || (st = acquire(c, m->up[ex], &ba.bw[b].up, held)) ||
             (st = acquire(c, m->down[ex], &ba.bw[b].down, held)))
           return st;
+        bl.bexp[b] = ex;
+        bl.bw[b] = ba.bw[b];
       }
       auto flush = [&]() -> atsi_status {
-        if (ba.nb == 0) return ATSI_OK;
-        hipError_t fe = launch_expert_gateup(ba, ba.nb, gemv, c->cs);
-        if (fe == hipSuccess) fe = launch_expert_down(ba, ba.nb, gemv, c->cs);
+        hipError_t fe = hipSuccess;
+        if (ba.nb > 0) fe = launch_expert_gateup(ba, ba.nb, gemv, c->cs);
+        if (fe == hipSuccess && bl.nb > 0) fe = launch_light_gateup(bl, bl.nb, c->cs);
+        if (fe == hipSuccess && ba.nb > 0) fe = launch_expert_down(ba, ba.nb, gemv, c->cs);
+        if (fe == hipSuccess && bl.nb > 0) fe = launch_light_down(bl, bl.nb, c->cs);
         if (fe != hipSuccess) return hip_fail(c, fe, "streamed expert launch");
         ba.nb = 0;
+        bl.nb = 0;
         return ATSI_OK;
       };
       for (int b = 0; b < nbx; ++b) {
+        // the same tiles as a resident expert with this count gets
         const int cnt = c->pinned[act[b0 + b]];
-        for (int r0 = 0; r0 < cnt; r0 += bm) {
-          if (ba.nb == kBatchTiles && (st = flush())) return st;
-          ba.btiles[ba.nb++] = make_int2(b, r0);
+        const bool lt = cnt <= light;
+        MoeArgs& dst = lt ? bl : ba;
+        for (int r0 = 0; r0 < cnt; r0 += lt ? kLightTileRows : bm) {
+          if (dst.nb == kBatchTiles && (st = flush())) return st;
+          dst.btiles[dst.nb++] = make_int2(b, r0);
         }
       }
       if ((st = flush())) return st;
@@ -1692,7 +1721,8 @@ atsi_status atsi_moe_bucket(atsi_ctx* c, const int32_t* idx, int64_t M, int32_t 
   int32_t* tiles = (int32_t*)sc.take(2 * ((size_t)M * k + E + 1), 4);
   int32_t* nt = (int32_t*)sc.take(1, 4);
   if (!order || !tiles || !nt) return fail(c, ATSI_E_WORKSPACE, "scratch too small for bucketing");
-  hipError_t e = launch_bucket(idx, (int)M, k, E, nullptr, 1, counts, offsets, perm, inv_perm, order, tiles, nt, c->cs);
+  hipError_t e = launch_bucket(idx, (int)M, k, E, nullptr, 1, 0, counts, offsets, perm, inv_perm, order, tiles, nt,
+                               nullptr, nullptr, c->cs);
   if (e != hipSuccess) return hip_fail(c, e, "bucket launch");
   return ATSI_OK;
 }
@@ -1745,6 +1775,16 @@ atsi_status atsi_set_debug(atsi_ctx* c, uint32_t flags) {
   if (flags & ~(uint32_t)(ATSI_DEBUG_POISON | ATSI_DEBUG_SERIALIZE))
     return fail(c, ATSI_E_INVALID, "unknown debug flags 0x%x", flags);
   c->debug = flags;
+  return ATSI_OK;
+}
+
+atsi_status atsi_set_moe_light_rows(atsi_ctx* c, int32_t rows) {
+  if (!c) return ATSI_E_INVALID;
+  if (rows < -1 || rows > kMoeLightRowsMax)
+    return fail(c, ATSI_E_INVALID, "rows=%d out of range -1..%d", rows, kMoeLightRowsMax);
+  atsi_status st = enter(c);
+  if (st) return st;
+  c->moe_light_rows = rows;
   return ATSI_OK;
 }
 

@@ -10,6 +10,9 @@ constexpr int kMaxExperts = 128;   // experts per layer handled by one launch
 constexpr int kMaxTopK = 16;
 constexpr int kBatchExp = 4;       // streamed experts per batch launch
 constexpr int kBatchTiles = 64;    // row tiles per batch launch
+constexpr int kLightTileRows = 16; // rows per tile of the light-expert kernels
+constexpr int kMoeLightRowsMax = 1 << 20;
+constexpr int kLightAutoPairs = 32;  // default: light kernels for every expert up to this many pairs per expert
 
 // The three weight tensors of one SwiGLU expert.
 struct ExpertW {
@@ -35,6 +38,7 @@ struct MoeArgs {
   __half* out;                 // expert outputs [M*k][H], row = pair id
   const float* inv_r;          // per-token RMS-norm factor of x, or nullptr
   int k, H, I;
+  int M;                       // tokens (rows of x)
   // decode with every expert HBM-resident (GEMV path only): tile t is routed
   // pair t, whose expert is pair_expert[t]; its rows in h and out are t, so no
   // bucketing sits between routing and the expert loads
@@ -59,16 +63,26 @@ hipError_t launch_rmsnorm32(const float* x, int M, int H, float eps, __half* y, 
 size_t router_partial_floats(int M, int H, int E);
 
 // bucketing (single workgroup): counts, offsets, perm, inv_perm, heavy-first
-// expert order and the row tiles (of bm_rows) of experts with resident[e] != 0
+// expert order and the row tiles of experts with resident[e] != 0: tiles of
+// bm_rows rows for experts routed more than light_rows pairs, tiles of
+// kLightTileRows rows (ltiles, n_ltiles; may be null when light_rows is 0)
+// for the others
 hipError_t launch_bucket(const int32_t* idx, int M, int k, int E, const uint8_t* resident, int bm_rows,
-                         int32_t* counts, int32_t* offsets, int32_t* perm, int32_t* inv_perm, int32_t* order,
-                         int32_t* tiles, int32_t* n_tiles, hipStream_t s);
+                         int light_rows, int32_t* counts, int32_t* offsets, int32_t* perm, int32_t* inv_perm,
+                         int32_t* order, int32_t* tiles, int32_t* n_tiles, int32_t* ltiles, int32_t* n_ltiles,
+                         hipStream_t s);
 
 // rows per tile of the grouped expert kernels (1 on the GEMV path)
 int expert_tile_rows(bool gemv);
 // grouped SwiGLU gate/up and grouped down; tile_bound = grid size in tiles
 hipError_t launch_expert_gateup(const MoeArgs& a, int tile_bound, bool gemv, hipStream_t s);
 hipError_t launch_expert_down(const MoeArgs& a, int tile_bound, bool gemv, hipStream_t s);
+// light experts (tiles of kLightTileRows rows from a.tiles / a.btiles): the
+// same products as the grouped GEMM, on a kernel that streams each weight once
+// per tile; shapes where light_supported(H, I) holds
+bool light_supported(int H, int I);
+hipError_t launch_light_gateup(const MoeArgs& a, int tile_bound, hipStream_t s);
+hipError_t launch_light_down(const MoeArgs& a, int tile_bound, hipStream_t s);
 // pair-indexed decode (a.pair_expert set): the down projections of all k
 // experts of each of the M tokens and the combine, in one launch; the same
 // results as launch_expert_down followed by launch_combine

@@ -130,6 +130,335 @@ __global__ __launch_bounds__(kGemmBlock, 2) void expert_down_gemm(MoeArgs a, int
     }
 }
 
+// ---------------------------------------------------------------- light experts
+
+// Most experts of a prefill call are routed only a few tokens (under a Zipf
+// load most of the 128 draw fewer than 32 of 512), and a 64-row MFMA tile
+// then spends its K loop on staging activations that are mostly padding.  For
+// such experts a tile is kLightTileRows rows, and the kernel streams each
+// weight once per tile with no LDS staging of weights or activations:
+//   * work items are (tile, block of output columns) in tile-major order; a
+//     workgroup (one per CU) takes a contiguous run of them, so it mostly
+//     stays on one tile and its activations, and a ring of loads runs on
+//     across items, so the next item's weights are in flight while an item
+//     finishes;
+//   * wavefront (ks, cg) takes K-slice ks (GS groups of 32 inputs) of the
+//     kLightSteps 16-row steps of column group cg of an item (gate/up: four
+//     steps of gate rows and the four matching steps of up rows);
+//   * the tile's activations for the K-slice stay in registers as the A
+//     operands of v_mfma_f32_16x16x32_f16 (lane n + 16 c holds token n, inputs
+//     8c .. 8c + 7 of each group, permuted to the nibble pair order);
+//   * per step a lane loads GS / 4 x 16 code bytes of its weight row (groups
+//     c, c + 4, ... of the slice: four lanes read 64 contiguous bytes) and the
+//     row's scales of the slice; a 4 x 4 transpose of words across the four
+//     16-lane rows (permlane32 and permlane16 swaps) gives every lane the code
+//     word of its 8-input chunk for each group, which becomes eight exact fp16
+//     integers;
+//   * one MFMA per group sums that group's exact products for 16 tokens x 16
+//     weight rows, and the group's fp16 scale multiplies the sums in fp32
+//     (the arithmetic of the batched-decode kernel);
+//   * each finished step's partial sums go to LDS; after a barrier the
+//     K-slices are summed in slice order and the epilogue (SwiGLU and the RMS
+//     factor, or the store by pair id) runs on every thread.
+#ifndef LIGHT_D
+#define LIGHT_D 8
+#endif
+#ifndef LIGHT_D16
+#define LIGHT_D16 2
+#endif
+constexpr int kLightSteps = 8;  // 16-row steps per wavefront and item
+constexpr int kLightMF = 4;     // MFMAs issued before their products are scaled
+constexpr int kLightWaves = 8;  // at most, per workgroup (one workgroup per CU)
+constexpr uint32_t kLightOob = 0x80000000u;  // an offset past every buffer here
+// steps of loads in flight (divides kLightSteps) for K-slices of gs groups
+constexpr int light_d(int gs) { return gs == 8 ? LIGHT_D : LIGHT_D16; }
+static_assert(kLightSteps % light_d(8) == 0 && kLightSteps % light_d(16) == 0, "the ring restarts at every item");
+
+typedef float lf4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t light_rsrc(const void* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), 0, (int)bytes, 0x00020000);
+}
+
+// 4 x 4 transpose of words across the four 16-lane rows of the wave: on entry
+// row r holds X[r][0..3] in v[0..3]; on return row r holds X[0..3][r].
+__device__ __forceinline__ void transpose_rows4(uint32_t (&v)[4]) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  // 2 x 2 blocks of rows {0, 1} and {2, 3} trade places (lane halves) ...
+  const auto a = __builtin_amdgcn_permlane32_swap(v[0], v[2], false, false);
+  const auto b = __builtin_amdgcn_permlane32_swap(v[1], v[3], false, false);
+  // ... then each block is transposed between neighbouring rows
+  const auto c = __builtin_amdgcn_permlane16_swap(a[0], b[0], false, false);
+  const auto d = __builtin_amdgcn_permlane16_swap(a[1], b[1], false, false);
+  v[0] = c[0];
+  v[1] = c[1];
+  v[2] = d[0];
+  v[3] = d[1];
+#endif
+}
+
+template <typename T>
+__device__ __forceinline__ T* uniform_ptr(T* p) {
+  const uint64_t v = reinterpret_cast<uint64_t>(p);
+  const uint64_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)v);
+  const uint64_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(v >> 32));
+  return reinterpret_cast<T*>(lo | (hi << 32));
+}
+
+// Loads through the global address space (a generic load would also count
+// against the LDS wait counter, and its wait drains every load in flight).
+template <typename T>
+__device__ __forceinline__ T ld_global(const T* p) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  return *reinterpret_cast<const __attribute__((address_space(1))) T*>(reinterpret_cast<uintptr_t>(p));
+#else
+  return *p;
+#endif
+}
+
+// One work item of a light launch, all of it uniform.  Past the workgroup's
+// items the pointers are null and every load of the ring reads zeros.
+struct LightItem {
+  const uint8_t* c0;    // codes / scales of gate (or down) and up
+  const uint16_t* s0;
+  const uint8_t* c1;
+  const uint16_t* s1;
+  int tix, cb, base, rows;
+};
+
+template <bool DOWN>
+__device__ __forceinline__ LightItem light_item(const MoeArgs& a, int i, int i1, int ncb) {
+  LightItem it;
+  if (i >= i1) {
+    it.c0 = it.c1 = nullptr;
+    it.s0 = it.s1 = nullptr;
+    it.tix = -1;
+    it.cb = it.base = it.rows = 0;
+    return it;
+  }
+  it.tix = i / ncb;
+  it.cb = i % ncb;
+  int e, row0;
+  ExpertW w;
+  if (a.nb > 0) {
+    const int2 t = a.btiles[it.tix];
+    e = a.bexp[t.x];
+    row0 = t.y;
+    w = a.bw[t.x];
+  } else {
+    e = ld_global(a.tiles + 2 * it.tix);
+    row0 = ld_global(a.tiles + 2 * it.tix + 1);
+    w = ld_global(a.table + e);
+  }
+  e = __builtin_amdgcn_readfirstlane(e);
+  row0 = __builtin_amdgcn_readfirstlane(row0);
+  it.base = __builtin_amdgcn_readfirstlane(ld_global(a.offsets + e)) + row0;
+  it.rows = min(kLightTileRows, __builtin_amdgcn_readfirstlane(ld_global(a.counts + e)) - row0);
+  const QView& w0 = DOWN ? w.down : w.gate;
+  const QView& w1 = DOWN ? w.down : w.up;
+  it.c0 = uniform_ptr(w0.codes);
+  it.s0 = uniform_ptr(w0.scales);
+  it.c1 = DOWN ? it.c0 : uniform_ptr(w1.codes);
+  it.s1 = DOWN ? it.s0 : uniform_ptr(w1.scales);
+  return it;
+}
+
+template <bool DOWN, int GS>
+__global__ __launch_bounds__(kLightWaves * 64) void expert_light(MoeArgs a, int nk, int nc, int ncb) {
+  using namespace gemv;
+  constexpr int D = light_d(GS);
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  lf4_t* red = reinterpret_cast<lf4_t*>(smem);  // [wave][step][lane]
+  __shared__ int row_dst[kLightTileRows];       // output row of tile row m (pair id / bucket row)
+  __shared__ float row_scale[kLightTileRows];   // gate/up: the token's RMS factor
+  const int ntiles = a.nb > 0 ? a.nb : __builtin_amdgcn_readfirstlane(ld_global(a.n_tiles));
+  const int total = ntiles * ncb;
+  const int per = (total + (int)gridDim.x - 1) / (int)gridDim.x;
+  const int i0 = (int)blockIdx.x * per, i1 = min(i0 + per, total);
+  if (i0 >= i1) return;
+  const int K = DOWN ? a.I : a.H, N = DOWN ? a.H : a.I, G = K / kGroup;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
+  const int ks = wave % nk, cg = wave / nk;
+  const int n = lane & 15, c = lane >> 4;
+  const int g0 = ks * GS;
+  constexpr int OUTS = DOWN ? 16 * kLightSteps : 8 * kLightSteps;  // output columns per column group
+  const uint32_t cbytes = (uint32_t)((size_t)N * K / 2), sbytes = (uint32_t)((size_t)N * G * 2);
+
+  struct Ld {
+    u32x4_t c[GS / 4];  // groups c, c + 4, ... of the slice
+    u32x4_t s[GS / 8];  // the row's scales of the slice's groups
+  };
+  // step st of item it: weight row col0 + 16 st + n (gate/up: gate rows for
+  // the first half of the steps, up rows after)
+  auto load = [&](Ld& b, const LightItem& it, int st) {
+    const bool second = !DOWN && st >= kLightSteps / 2;
+    const int row = (it.cb * nc + cg) * OUTS + 16 * (DOWN ? st : (st % (kLightSteps / 2))) + n;
+    const bool live = it.tix >= 0;
+    const bool ok = row < N && live;
+    const uint32_t co = ok ? (uint32_t)row * (uint32_t)(K / 2) + (uint32_t)(g0 + c) * 16 : kLightOob;
+    const uint32_t so = ok ? ((uint32_t)row * (uint32_t)G + (uint32_t)g0) * 2 : kLightOob;
+    const __amdgpu_buffer_rsrc_t rc = light_rsrc(second ? it.c1 : it.c0, live ? cbytes : 0);
+    const __amdgpu_buffer_rsrc_t rs = light_rsrc(second ? it.s1 : it.s0, live ? sbytes : 0);
+#pragma unroll
+    for (int q = 0; q < GS / 4; ++q)
+      b.c[q] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rc, co + 64 * q, 0, 0));
+#pragma unroll
+    for (int q = 0; q < GS / 8; ++q)
+      b.s[q] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rs, so + 16 * q, 0, 0));
+  };
+  // token row n of a tile (gate/up: its pair's id, looked up before the
+  // weight loads go out, so that waiting for it does not wait for them)
+  auto pair_of = [&](const LightItem& it) {
+    return DOWN ? 0 : ld_global(a.perm + it.base + (n < it.rows ? n : 0));
+  };
+  // A operand: lane n + 16 c holds token row n, inputs 8c .. 8c + 7 of each
+  // group of the slice (zeros past the tile's rows); the epilogue's row table
+  const __amdgpu_buffer_rsrc_t rx = DOWN ? light_rsrc(a.h, (uint32_t)((size_t)a.M * a.k * a.I * 2))
+                                         : light_rsrc(a.x, (uint32_t)((size_t)a.M * a.H * 2));
+  half8_t xa[GS];
+  auto load_rows = [&](const LightItem& it, int pr) {
+    const bool has_row = n < it.rows;
+    const uint32_t rowoff = DOWN ? (uint32_t)(it.base + n) * (uint32_t)a.I * 2 : (uint32_t)(pr / a.k) * (uint32_t)a.H * 2;
+    const uint32_t xo = rowoff + (uint32_t)(g0 * kGroup + c * 8) * 2;
+#pragma unroll
+    for (int g = 0; g < GS; ++g) {
+      const u32x4_t v = __builtin_bit_cast(
+          u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rx, has_row ? xo + (uint32_t)g * kGroup * 2 : kLightOob, 0, 0));
+      xa[g] = perm_x(v);
+    }
+    if (threadIdx.x < (unsigned)it.rows) {
+      const int m = threadIdx.x;
+      const int p = ld_global(a.perm + it.base + m);
+      row_dst[m] = DOWN ? p : it.base + m;
+      row_scale[m] = (!DOWN && a.inv_r) ? ld_global(a.inv_r + p / a.k) : 1.f;
+    }
+  };
+
+  LightItem cur = light_item<DOWN>(a, i0, i1, ncb);
+  LightItem nxt = light_item<DOWN>(a, i0 + 1, i1, ncb);
+  const int pr0 = pair_of(cur);
+  __builtin_amdgcn_sched_barrier(0);
+  Ld buf[D];
+#pragma unroll
+  for (int d = 0; d < D; ++d) load(buf[d], cur, d);
+  __builtin_amdgcn_sched_barrier(0);
+  load_rows(cur, pr0);
+
+  const UnpackMasks um = unpack_masks();
+  const lf4_t zero = {0.f, 0.f, 0.f, 0.f};
+  lf4_t* mine = red + (size_t)wave * kLightSteps * 64 + lane;
+  constexpr int SPO = DOWN ? kLightSteps : kLightSteps / 2;  // steps per set of outputs
+  const int nent = nc * SPO * 64;
+
+  for (int i = i0; i < i1; ++i) {
+#pragma unroll
+    for (int st = 0; st < kLightSteps; ++st) {
+      Ld& b = buf[st % D];
+      uint32_t t4[GS / 4][4];
+#pragma unroll
+      for (int q = 0; q < GS / 4; ++q) {
+        t4[q][0] = b.c[q].x;
+        t4[q][1] = b.c[q].y;
+        t4[q][2] = b.c[q].z;
+        t4[q][3] = b.c[q].w;
+      }
+      u32x4_t sv[GS / 8];
+#pragma unroll
+      for (int q = 0; q < GS / 8; ++q) sv[q] = b.s[q];
+      // refill: a later step of this item, or an early one of the next
+      if (st + D < kLightSteps)
+        load(b, cur, st + D);
+      else
+        load(b, nxt, st + D - kLightSteps);
+#pragma unroll
+      for (int q = 0; q < GS / 4; ++q) transpose_rows4(t4[q]);
+      lf4_t acc = zero;
+      // kLightMF MFMAs in flight before their products are scaled
+#pragma unroll
+      for (int h = 0; h < GS / kLightMF; ++h) {
+        lf4_t p[kLightMF];
+#pragma unroll
+        for (int j = 0; j < kLightMF; ++j) {
+          const int g = kLightMF * h + j;
+          p[j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(xa[g], unpack_q(t4[g >> 2][g & 3], um), zero, 0, 0, 0);
+        }
+#pragma unroll
+        for (int j = 0; j < kLightMF; ++j) {
+          const int g = kLightMF * h + j;
+          const uint32_t pair = sv[g >> 3][(g & 7) >> 1];
+          const float sc = __half2float(__ushort_as_half((uint16_t)((g & 1) ? pair >> 16 : pair)));
+#pragma unroll
+          for (int v = 0; v < 4; ++v) acc[v] = fmaf(sc, p[j][v], acc[v]);
+        }
+      }
+      mine[st * 64] = acc;
+    }
+    __syncthreads();
+
+    // slices summed in order; D[m][n] of a step sits in lane n + 16 (m / 4), item m % 4
+    for (int q = threadIdx.x; q < nent; q += blockDim.x) {
+      const int l = q & 63, sidx = (q >> 6) % SPO, cgq = (q >> 6) / SPO;
+      const int col = (cur.cb * nc + cgq) * OUTS + 16 * sidx + (l & 15);
+      if (col >= N) continue;
+      const lf4_t* r0 = red + (size_t)cgq * nk * kLightSteps * 64 + l;
+      lf4_t v = r0[sidx * 64], u = zero;
+      if constexpr (!DOWN) u = r0[(sidx + SPO) * 64];
+      for (int k2 = 1; k2 < nk; ++k2) {
+        v += r0[((size_t)k2 * kLightSteps + sidx) * 64];
+        if constexpr (!DOWN) u += r0[((size_t)k2 * kLightSteps + sidx + SPO) * 64];
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int m = 4 * (l >> 4) + j;
+        if (m >= cur.rows) break;
+        if constexpr (DOWN) {
+          a.out[(size_t)row_dst[m] * a.H + col] = __float2half_rn(v[j]);
+        } else {
+          // RMS-normalised input: scale both products by the token's factor
+          const float sc = row_scale[m];
+          a.h[(size_t)row_dst[m] * a.I + col] = __float2half_rn(silu_f(v[j] * sc) * (u[j] * sc));
+        }
+      }
+    }
+    __syncthreads();
+    if (i + 1 < i1) {
+      if (nxt.tix != cur.tix) load_rows(nxt, pair_of(nxt));
+      cur = nxt;
+      nxt = light_item<DOWN>(a, i + 2, i1, ncb);
+    }
+  }
+}
+
+// groups per K-slice: 8, or 16 where 8 would take more than kLightWaves slices
+int light_gs(int K) { return K / kGroup / 8 <= kLightWaves ? 8 : 16; }
+
+template <bool DOWN>
+hipError_t launch_light(const MoeArgs& a, int tile_bound, hipStream_t s) {
+  if (tile_bound <= 0) return hipSuccess;
+  if (!light_supported(a.H, a.I)) return hipErrorInvalidValue;
+  const int K = DOWN ? a.I : a.H, N = DOWN ? a.H : a.I;
+  const int gs = light_gs(K);
+  const int nk = K / (gs * kGroup);
+  const int nc = std::max(1, kLightWaves / nk);
+  const int outs = (DOWN ? 16 : 8) * kLightSteps * nc;
+  const int ncb = (N + outs - 1) / outs;
+  const size_t lds = (size_t)nk * nc * kLightSteps * 64 * sizeof(lf4_t);
+  if (lds + 2 * kLightTileRows * 4 > lds_limit()) return hipErrorInvalidValue;
+  // one workgroup per CU: each holds its loads in flight in registers
+  int cus = 256;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) !=
+                                               hipSuccess || cus < 1)
+    cus = 256;
+  const int grid = std::min(tile_bound * ncb, cus);
+  if (gs == 8)
+    hipLaunchKernelGGL((expert_light<DOWN, 8>), dim3(grid), dim3(nk * nc * 64), lds, s, a, nk, nc, ncb);
+  else
+    hipLaunchKernelGGL((expert_light<DOWN, 16>), dim3(grid), dim3(nk * nc * 64), lds, s, a, nk, nc, ncb);
+  return hipGetLastError();
+}
+
 // ---------------------------------------------------------------- GEMV path (one row per tile)
 
 // Sums over the wave of RW rows n0 .. n0 + RW - 1 of w1 (and of w2 when TWO)
@@ -358,6 +687,24 @@ hipError_t launch_expert_down(const MoeArgs& a, int tile_bound, bool gemv, hipSt
     hipLaunchKernelGGL(expert_down_gemm, dim3(tile_bound * tn), dim3(kGemmBlock), 0, s, a, tile_bound);
   }
   return hipGetLastError();
+}
+
+bool light_supported(int H, int I) {
+  // K-slices of 8 or 16 groups, at most kLightWaves of them
+  auto ok = [](int K) {
+    if (K % (8 * kGroup)) return false;
+    const int G = K / kGroup, gs = light_gs(K);
+    return G % gs == 0 && G / gs <= kLightWaves;
+  };
+  return ok(H) && ok(I);
+}
+
+hipError_t launch_light_gateup(const MoeArgs& a, int tile_bound, hipStream_t s) {
+  return launch_light<false>(a, tile_bound, s);
+}
+
+hipError_t launch_light_down(const MoeArgs& a, int tile_bound, hipStream_t s) {
+  return launch_light<true>(a, tile_bound, s);
 }
 
 hipError_t launch_expert_down_combine(const MoeArgs& a, int M, const float* p, const __half* res, __half* y,

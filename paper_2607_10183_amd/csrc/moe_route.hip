@@ -504,10 +504,11 @@ __device__ int scan128(const int* v, int* out, int E) {
 constexpr int kBucketThreads = 1024;
 __global__ __launch_bounds__(kBucketThreads) void bucket_kernel(const int32_t* __restrict__ idx, int M, int k, int E,
                                                       const uint8_t* __restrict__ resident, int bm_rows,
-                                                      int32_t* __restrict__ counts, int32_t* __restrict__ offsets,
-                                                      int32_t* __restrict__ perm, int32_t* __restrict__ inv_perm,
-                                                      int32_t* __restrict__ order, int32_t* __restrict__ tiles,
-                                                      int32_t* __restrict__ n_tiles) {
+                                                      int light_rows, int32_t* __restrict__ counts,
+                                                      int32_t* __restrict__ offsets, int32_t* __restrict__ perm,
+                                                      int32_t* __restrict__ inv_perm, int32_t* __restrict__ order,
+                                                      int32_t* __restrict__ tiles, int32_t* __restrict__ n_tiles,
+                                                      int32_t* __restrict__ ltiles, int32_t* __restrict__ n_ltiles) {
   __shared__ int cnt[kMaxExperts];
   __shared__ int base[kMaxExperts];
   __shared__ unsigned long long mask[16][kMaxExperts];
@@ -515,6 +516,8 @@ __global__ __launch_bounds__(kBucketThreads) void bucket_kernel(const int32_t* _
   __shared__ int ord[kMaxExperts];
   __shared__ int ntile[kMaxExperts];   // tiles of the expert at rank r
   __shared__ int tstart[kMaxExperts];
+  __shared__ int nlt[kMaxExperts];     // light tiles of the expert at rank r
+  __shared__ int lstart[kMaxExperts];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int pairs = M * k;
   for (int e = tid; e < E; e += blockDim.x) cnt[e] = 0;
@@ -588,20 +591,33 @@ __global__ __launch_bounds__(kBucketThreads) void bucket_kernel(const int32_t* _
     order[r] = e;
   }
   __syncthreads();
-  // row tiles of resident experts in heavy-first order: tile -> (expert, first row)
+  // row tiles of resident experts in heavy-first order: tile -> (expert, first
+  // row); experts routed at most light_rows pairs get tiles of kLightTileRows
+  // rows in the second list instead
   for (int r = tid; r < E; r += blockDim.x) {
     const int e = ord[r];
-    ntile[r] = (resident == nullptr || resident[e]) ? (cnt[e] + bm_rows - 1) / bm_rows : 0;
+    const bool res = resident == nullptr || resident[e];
+    const bool light = cnt[e] <= light_rows;
+    ntile[r] = (res && !light) ? (cnt[e] + bm_rows - 1) / bm_rows : 0;
+    nlt[r] = (res && light) ? (cnt[e] + kLightTileRows - 1) / kLightTileRows : 0;
   }
   __syncthreads();
   const int nt = scan128(ntile, tstart, E);
-  if (tid == 0) *n_tiles = nt;
+  const int nl = scan128(nlt, lstart, E);
+  if (tid == 0) {
+    *n_tiles = nt;
+    if (n_ltiles) *n_ltiles = nl;
+  }
   __syncthreads();
   for (int r = wave; r < E; r += blockDim.x / 64) {
     const int e = ord[r];
     for (int i = lane; i < ntile[r]; i += 64) {
       tiles[2 * (tstart[r] + i)] = e;
       tiles[2 * (tstart[r] + i) + 1] = i * bm_rows;
+    }
+    for (int i = lane; i < nlt[r]; i += 64) {
+      ltiles[2 * (lstart[r] + i)] = e;
+      ltiles[2 * (lstart[r] + i) + 1] = i * kLightTileRows;
     }
   }
 }
@@ -748,11 +764,12 @@ size_t router_partial_floats(int M, int H, int E) {
 }
 
 hipError_t launch_bucket(const int32_t* idx, int M, int k, int E, const uint8_t* resident, int bm_rows,
-                         int32_t* counts, int32_t* offsets, int32_t* perm, int32_t* inv_perm, int32_t* order,
-                         int32_t* tiles, int32_t* n_tiles, hipStream_t s) {
-  if (k < 1 || k > kMaxTopK) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(bucket_kernel, dim3(1), dim3(kBucketThreads), 0, s, idx, M, k, E, resident, bm_rows, counts, offsets, perm,
-                     inv_perm, order, tiles, n_tiles);
+                         int light_rows, int32_t* counts, int32_t* offsets, int32_t* perm, int32_t* inv_perm,
+                         int32_t* order, int32_t* tiles, int32_t* n_tiles, int32_t* ltiles, int32_t* n_ltiles,
+                         hipStream_t s) {
+  if (k < 1 || k > kMaxTopK || (light_rows > 0 && (!ltiles || !n_ltiles))) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(bucket_kernel, dim3(1), dim3(kBucketThreads), 0, s, idx, M, k, E, resident, bm_rows, light_rows,
+                     counts, offsets, perm, inv_perm, order, tiles, n_tiles, ltiles, n_ltiles);
   return hipGetLastError();
 }
 

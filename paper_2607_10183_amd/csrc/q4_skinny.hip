@@ -39,9 +39,9 @@ namespace {
 
 using namespace gemv;
 
-typedef _Float16 h8_t __attribute__((ext_vector_type(8)));
+typedef half8_t h8_t;
 typedef float f4_t __attribute__((ext_vector_type(4)));
-typedef unsigned u4_t __attribute__((ext_vector_type(4)));
+typedef u32x4_t u4_t;
 
 constexpr int kRows = 16;  // weight rows per workgroup: the MFMA's N
 constexpr uint32_t kOob = 0x80000000u;  // an offset past every buffer here
@@ -52,53 +52,6 @@ struct SkinnyMap {
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* p, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), 0, (int)bytes, 0x00020000);
-}
-
-// Masks in scalar registers and the 1024.0 pattern in a vector register, so
-// that each mask-and-or is one v_and_or_b32 (its encoding takes no literal
-// constant and reads at most one scalar register).
-struct UnpackK {
-  uint32_t lo, hi, magic;
-};
-
-__device__ __forceinline__ uint32_t sgpr_const(uint32_t v) {
-  uint32_t r;
-  asm volatile("s_mov_b32 %0, %1" : "=s"(r) : "i"(v));
-  return r;
-}
-
-__device__ __forceinline__ uint32_t vgpr_const(uint32_t v) {
-  uint32_t r;
-  asm volatile("v_mov_b32 %0, %1" : "=v"(r) : "i"(v));
-  return r;
-}
-
-__device__ __forceinline__ UnpackK unpack_consts() {
-  return UnpackK{sgpr_const(0x000F000Fu), sgpr_const(0x00F000F0u), vgpr_const(kMagic)};
-}
-
-// Eight exact fp16 integers q = u - 8 from one code word, in the pair order
-// (k0, k4), (k1, k5), (k2, k6), (k3, k7).
-__device__ __forceinline__ h8_t unpack_q(uint32_t w, const UnpackK& k) {
-  const uint32_t w8 = w >> 8;
-  const half2_t off = {(_Float16)-1032.f, (_Float16)-1032.f};
-  const half2_t sh = {(_Float16)0.0625f, (_Float16)0.0625f};
-  const half2_t off16 = {(_Float16)-72.f, (_Float16)-72.f};
-  // (1024 + u) - 1032 and (1024 + 16 u) / 16 - 72 are exact in fp16
-  const half2_t a = __builtin_bit_cast(half2_t, (w & k.lo) | k.magic) + off;
-  const half2_t b = __builtin_bit_cast(half2_t, (w & k.hi) | k.magic) * sh + off16;
-  const half2_t c = __builtin_bit_cast(half2_t, (w8 & k.lo) | k.magic) + off;
-  const half2_t d = __builtin_bit_cast(half2_t, (w8 & k.hi) | k.magic) * sh + off16;
-  const u4_t r = {__builtin_bit_cast(uint32_t, a), __builtin_bit_cast(uint32_t, b), __builtin_bit_cast(uint32_t, c),
-                  __builtin_bit_cast(uint32_t, d)};
-  return __builtin_bit_cast(h8_t, r);
-}
-
-// Eight consecutive fp16 activations reordered to the same pair order.
-__device__ __forceinline__ h8_t perm_x(u4_t d) {
-  const u4_t r = {__builtin_amdgcn_perm(d.z, d.x, 0x05040100u), __builtin_amdgcn_perm(d.z, d.x, 0x07060302u),
-                  __builtin_amdgcn_perm(d.w, d.y, 0x05040100u), __builtin_amdgcn_perm(d.w, d.y, 0x07060302u)};
-  return __builtin_bit_cast(h8_t, r);
 }
 
 // One step is four consecutive groups (128 inputs) of the wave's 16 rows.
@@ -194,7 +147,7 @@ __global__ __launch_bounds__(NW * 64) void q4_skinny_kernel(LinOp op, SkinnyMap 
     *reinterpret_cast<u4_t*>(&L.x[4 * MX * kXStride + lane * 16]) = u4_t{0u, 0u, 0u, 0u};
   const int arow = j < 4 * MX ? j : 4 * MX;
   const uint8_t* xa = &L.x[arow * kXStride + kb * 16];   // + 64 per group
-  const UnpackK uk = unpack_consts();
+  const UnpackMasks uk = unpack_masks();
 
   const f4_t zero = {0.f, 0.f, 0.f, 0.f};
   f4_t acc[NT], gram = zero;

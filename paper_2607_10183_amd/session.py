@@ -129,6 +129,11 @@ class Session:
         """Decode MoE calls read host-resident experts in place (atsi_set_zero_copy)."""
         atsi.atsi_set_zero_copy(self.ctx, enable)
 
+    def set_moe_light_rows(self, rows: int) -> None:
+        """Prefill experts routed at most `rows` pairs take the light-expert
+        kernels, the others the grouped GEMM (atsi_set_moe_light_rows)."""
+        atsi.atsi_set_moe_light_rows(self.ctx, rows)
+
     def set_placement(self, host_mask) -> None:
         mask = [int(v) for v in host_mask]
         atsi.atsi_set_placement(self.ctx, mask)

@@ -135,6 +135,39 @@ def test_moe_wide_topk_parity(sess, k, M):
 
 
 @pytest.fixture(scope="module")
+def light_setup(sess):
+    # hidden 768 and inter 512: three and two K-slices per light workgroup,
+    # and output blocks the expert's rows do not fill
+    return _Setup(sess, 85, E=16, H=768, I=512, k=4)
+
+
+@pytest.mark.parametrize("light", [0, 32, 1 << 20])
+@pytest.mark.parametrize("M", [5, 50, 300])
+def test_moe_light_experts_parity(sess, light_setup, light, M):
+    """Prefill experts on the grouped GEMM only (0), split by routed count
+    (32: the light-expert kernels take experts of at most 32 pairs, one or two
+    16-row tiles), or all on the light kernels (an expert of 200 pairs then
+    has 13 tiles, the last one ragged)."""
+    st = light_setup
+    xn = synth.activations(85, 100 + M, M, st.H)
+    sess.set_moe_light_rows(light)
+    try:
+        y, dbg = st.layer(_dev(xn), debug=True)
+        sess.sync()
+    finally:
+        sess.set_moe_light_rows(-1)
+    _check_moe(y, dbg, st, xn, f"moe light={light} M={M}")
+
+
+def test_moe_light_rows_range(sess):
+    from paper_2607_10183_amd import atsi
+    for bad in (-2, (1 << 20) + 1):
+        with pytest.raises(atsi.AtsiError, match="ATSI_E_INVALID"):
+            sess.set_moe_light_rows(bad)
+    sess.set_moe_light_rows(-1)
+
+
+@pytest.fixture(scope="module")
 def cfg4(sess):
     shp = configs.MOE_LAYER.moe
     return _Setup(sess, configs.MOE_LAYER.seed, E=shp.n_experts, H=shp.hidden, I=shp.inter, k=shp.top_k, host=True)
