@@ -332,21 +332,26 @@ atsi_status atsi_set_debug(atsi_ctx* ctx, uint32_t flags);
  * are not counted in atsi_stats. */
 atsi_status atsi_set_zero_copy(atsi_ctx* ctx, int32_t enable);
 
-/* Kernel choice for the routed experts of a prefill call (more than 4
- * tokens; the expert GEMMs of Sec. 2.2's compute-bound phase, only for
- * routed experts, Sec. 3.2).  An expert routed at most `rows` pairs in the
- * call runs on the light-expert kernels (tiles of 16 rows that stream each
- * weight once per tile, exact products scaled per group as at decode); the
- * others on the grouped GEMM (tiles of 64 rows, weights rounded to fp16 once).
- * rows = 0 sends every expert to the grouped GEMM; rows = -1 (the default)
- * sends every expert to the light kernels while the call routes at most 32
- * pairs per expert on average and none beyond.  The light kernels cover
- * hidden and intermediate sizes that are multiples of 256 up to 4096 (the
- * 16-group slices of sizes above 2048 only where they divide evenly); other
- * shapes always take the grouped GEMM.  The choice depends only on the
- * routed counts and the call size, so HBM-resident and streamed experts give
- * the same bits; the two kernels differ by rounding only.  ATSI_E_INVALID for
- * rows < -1 or rows > 2^20. */
+/* Kernel choice for the routed experts of a prefill call (more than 4 tokens;
+ * the expert GEMMs of Sec. 2.2's compute-bound phase, only for routed
+ * experts, Sec. 3.2). An expert routed at most `rows` pairs in the call runs
+ * on the light-expert kernels: tiles that stream each weight through
+ * registers once per tile, of 16 rows, or, in calls that route more than 16
+ * pairs per expert on average, of 16, 32 or 64 rows (the fewest 16-row blocks
+ * that cover its count). 16-row tiles sum each group's exact products and
+ * scale them in fp32 (the decode arithmetic); taller tiles round each weight
+ * to fp16 once, as the grouped GEMM does. The other experts run on the
+ * grouped GEMM (tiles of 64 rows staged through LDS). rows = 0 sends every
+ * expert to the grouped GEMM; rows = -1 (the default) every expert to the
+ * light kernels, except in calls of more than 16 pairs per expert on shapes
+ * that allow only 16-row tiles, which keep the grouped GEMM. The light
+ * kernels cover hidden and intermediate sizes that are multiples of 256 up to
+ * 4096 (above 2048 in 16-row tiles only, and only where 16-group slices
+ * divide the size evenly); other shapes always take the grouped GEMM. The
+ * choice depends only on the call's size and routed counts, so HBM-resident
+ * and streamed experts give the same bits; the kernels differ by rounding
+ * only.
+ * ATSI_E_INVALID for rows < -1 or rows > 2^20. */
 atsi_status atsi_set_moe_light_rows(atsi_ctx* ctx, int32_t rows);
 
 /* Wait for the compute and transfer streams (the host-side synchronisation

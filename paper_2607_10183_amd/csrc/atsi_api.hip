@@ -1171,13 +1171,19 @@ atsi_status run_moe(atsi_ctx* c, const atsi_moe* m, const __half* x, int Mi, __h
   const int Mk = Mi * k;
   const bool gemv = Mi <= 4;
   const int bm = expert_tile_rows(gemv);
-  // experts routed at most `light` pairs run on the light-expert kernels; by
-  // default all of them while the call routes at most 32 pairs per expert on
-  // average, none beyond (measured on MI355X at 64, 512 and 2048 tokens of
-  // the 128-expert layer)
-  int light = c->moe_light_rows;
-  if (light < 0) light = Mk <= kLightAutoPairs * E ? kMoeLightRowsMax : 0;
+  // experts routed at most `light` pairs run on the light-expert kernels (by
+  // default all of them: faster than the grouped GEMM at 64, 512 and 2048
+  // tokens of the 128-expert layer on MI355X)
+  int light = c->moe_light_rows < 0 ? kMoeLightRowsMax : c->moe_light_rows;
   if (gemv || !light_supported(H, I) || (size_t)Mk * std::max(H, I) * 2 >= ((size_t)1 << 31)) light = 0;
+  // taller tiles pay off once experts are routed many tokens; below that the
+  // extra launches' latency costs more than they save (MI355X: 16-row tiles
+  // only up to 16 pairs per expert on average).  Where the shape allows only
+  // 16-row tiles, large calls keep the grouped GEMM by default: heavy experts
+  // would be streamed once per 16 of their rows.
+  const bool tall = Mk > kLightTallPairs * E;
+  if (tall && c->moe_light_rows < 0 && light && light_mtmax(H, I) < 4) light = 0;
+  const int lmt = !light ? 0 : (tall ? light_mtmax(H, I) : 1);
   float* part = (float*)sc.take(router_partial_floats(Mi, H, E), 4);
   int32_t* idx = dbg && dbg->idx ? dbg->idx : (int32_t*)sc.take(Mk, 4);
   float* p = dbg && dbg->p ? dbg->p : (float*)sc.take(Mk, 4);
@@ -1189,7 +1195,7 @@ atsi_status run_moe(atsi_ctx* c, const atsi_moe* m, const __half* x, int Mi, __h
   int32_t* tiles = (int32_t*)sc.take(2 * ((size_t)Mk / bm + E + 1), 4);
   int32_t* ntiles = (int32_t*)sc.take(1, 4);
   int32_t* ltiles = light ? (int32_t*)sc.take(2 * ((size_t)Mk / kLightTileRows + E + 1), 4) : nullptr;
-  int32_t* nltiles = light ? (int32_t*)sc.take(1, 4) : nullptr;
+  int32_t* nltiles = light ? (int32_t*)sc.take(kLightClasses, 4) : nullptr;
   __half* h = sc.take((size_t)Mk * I);
   __half* out = dbg && dbg->expert_out ? (__half*)dbg->expert_out : sc.take((size_t)Mk * H);
   if (!part || !idx || !p || !counts || !offsets || !perm || !inv || !order || !tiles || !ntiles || !h || !out ||
@@ -1208,8 +1214,8 @@ atsi_status run_moe(atsi_ctx* c, const atsi_moe* m, const __half* x, int Mi, __h
   const bool by_pair = gemv && (tb->n_streamed == 0 || c->zero_copy);
   const bool want_buckets = dbg && (dbg->counts || dbg->offsets || dbg->perm || dbg->inv_perm);
   if (!by_pair || want_buckets) {
-    e = launch_bucket(idx, Mi, k, E, resident, bm, light, counts, offsets, perm, inv, order, tiles, ntiles, ltiles,
-                      nltiles, c->cs);
+    e = launch_bucket(idx, Mi, k, E, resident, bm, light, lmt, counts, offsets, perm, inv, order, tiles, ntiles,
+                      ltiles, nltiles, c->cs);
     if (e != hipSuccess) return hip_fail(c, e, "bucket launch");
   }
   if (tb->n_streamed > 0 && !by_pair) {
@@ -1229,6 +1235,7 @@ atsi_status run_moe(atsi_ctx* c, const atsi_moe* m, const __half* x, int Mi, __h
   a.inv_r = inv_r;
   a.k = k;
   a.M = Mi;
+  a.light_mtmax = lmt;
   a.H = H;
   a.I = I;
   if (by_pair) {
@@ -1245,7 +1252,12 @@ atsi_status run_moe(atsi_ctx* c, const atsi_moe* m, const __half* x, int Mi, __h
   al.tiles = ltiles;
   al.n_tiles = nltiles;
   if ((e = launch_expert_gateup(a, bound, gemv, c->cs)) != hipSuccess) return hip_fail(c, e, "expert gate/up launch");
-  if ((e = launch_light_gateup(al, lbound, c->cs)) != hipSuccess) return hip_fail(c, e, "light expert gate/up launch");
+  // one launch per light tile height the shape allows (the kernels of
+  // classes with no tiles exit at once)
+  const int cls0 = lmt ? light_class(lmt) : kLightClasses;
+  for (int q = cls0; q < kLightClasses; ++q)
+    if ((e = launch_light_gateup(al, q, lbound, c->cs)) != hipSuccess)
+      return hip_fail(c, e, "light expert gate/up launch");
   if (by_pair) {  // every expert resident: the down launch also combines
     a.store_out = dbg && dbg->expert_out;
     if ((e = launch_expert_down_combine(a, Mi, p, res, y, c->cs)) != hipSuccess)
@@ -1253,7 +1265,8 @@ atsi_status run_moe(atsi_ctx* c, const atsi_moe* m, const __half* x, int Mi, __h
     return gather_expert_h(c, dbg, h, nullptr, Mk, I);
   }
   if ((e = launch_expert_down(a, bound, gemv, c->cs)) != hipSuccess) return hip_fail(c, e, "expert down launch");
-  if ((e = launch_light_down(al, lbound, c->cs)) != hipSuccess) return hip_fail(c, e, "light expert down launch");
+  for (int q = cls0; q < kLightClasses; ++q)
+    if ((e = launch_light_down(al, q, lbound, c->cs)) != hipSuccess) return hip_fail(c, e, "light expert down launch");
 
   if (tb->n_streamed > 0) {
     HIP_TRY(c, hipEventSynchronize(c->counts_ev));
@@ -1270,9 +1283,10 @@ atsi_status run_moe(atsi_ctx* c, const atsi_moe* m, const __half* x, int Mi, __h
     const int B = std::max(1, std::min(kBatchExp, c->n_slots / 3));
     for (size_t b0 = 0; b0 < act.size(); b0 += B) {
       std::vector<int> held;
-      MoeArgs ba = a, bl = a;  // tiles of bm rows / light tiles of the batch
+      MoeArgs ba = a;  // tiles of bm rows / light tiles of each class of the batch
       ba.nb = 0;
-      bl.nb = 0;
+      MoeArgs bl[kLightClasses] = {a, a, a};
+      for (MoeArgs& q : bl) q.nb = 0;
       const int nbx = (int)std::min<size_t>(B, act.size() - b0);
       for (int b = 0; b < nbx; ++b) {
         const int ex = act[b0 + b];
@@ -1280,26 +1294,31 @@ atsi_status run_moe(atsi_ctx* c, const atsi_moe* m, const __half* x, int Mi, __h
         if ((st = acquire(c, m->gate[ex], &ba.bw[b].gate, held)) || (st = acquire(c, m->up[ex], &ba.bw[b].up, held)) ||
             (st = acquire(c, m->down[ex], &ba.bw[b].down, held)))
           return st;
-        bl.bexp[b] = ex;
-        bl.bw[b] = ba.bw[b];
+        for (MoeArgs& q : bl) {
+          q.bexp[b] = ex;
+          q.bw[b] = ba.bw[b];
+        }
       }
       auto flush = [&]() -> atsi_status {
         hipError_t fe = hipSuccess;
         if (ba.nb > 0) fe = launch_expert_gateup(ba, ba.nb, gemv, c->cs);
-        if (fe == hipSuccess && bl.nb > 0) fe = launch_light_gateup(bl, bl.nb, c->cs);
+        for (int q = 0; q < kLightClasses; ++q)
+          if (fe == hipSuccess && bl[q].nb > 0) fe = launch_light_gateup(bl[q], q, bl[q].nb, c->cs);
         if (fe == hipSuccess && ba.nb > 0) fe = launch_expert_down(ba, ba.nb, gemv, c->cs);
-        if (fe == hipSuccess && bl.nb > 0) fe = launch_light_down(bl, bl.nb, c->cs);
+        for (int q = 0; q < kLightClasses; ++q)
+          if (fe == hipSuccess && bl[q].nb > 0) fe = launch_light_down(bl[q], q, bl[q].nb, c->cs);
         if (fe != hipSuccess) return hip_fail(c, fe, "streamed expert launch");
         ba.nb = 0;
-        bl.nb = 0;
+        for (MoeArgs& q : bl) q.nb = 0;
         return ATSI_OK;
       };
       for (int b = 0; b < nbx; ++b) {
         // the same tiles as a resident expert with this count gets
         const int cnt = c->pinned[act[b0 + b]];
         const bool lt = cnt <= light;
-        MoeArgs& dst = lt ? bl : ba;
-        for (int r0 = 0; r0 < cnt; r0 += lt ? kLightTileRows : bm) {
+        const int lmtb = lt ? light_mt(cnt, lmt) : 0;
+        MoeArgs& dst = lt ? bl[light_class(lmtb)] : ba;
+        for (int r0 = 0; r0 < cnt; r0 += lt ? kLightTileRows * lmtb : bm) {
           if (dst.nb == kBatchTiles && (st = flush())) return st;
           dst.btiles[dst.nb++] = make_int2(b, r0);
         }
@@ -1721,8 +1740,8 @@ atsi_status atsi_moe_bucket(atsi_ctx* c, const int32_t* idx, int64_t M, int32_t 
   int32_t* tiles = (int32_t*)sc.take(2 * ((size_t)M * k + E + 1), 4);
   int32_t* nt = (int32_t*)sc.take(1, 4);
   if (!order || !tiles || !nt) return fail(c, ATSI_E_WORKSPACE, "scratch too small for bucketing");
-  hipError_t e = launch_bucket(idx, (int)M, k, E, nullptr, 1, 0, counts, offsets, perm, inv_perm, order, tiles, nt,
-                               nullptr, nullptr, c->cs);
+  hipError_t e = launch_bucket(idx, (int)M, k, E, nullptr, 1, 0, 0, counts, offsets, perm, inv_perm, order, tiles,
+                               nt, nullptr, nullptr, c->cs);
   if (e != hipSuccess) return hip_fail(c, e, "bucket launch");
   return ATSI_OK;
 }

@@ -10,9 +10,20 @@ constexpr int kMaxExperts = 128;   // experts per layer handled by one launch
 constexpr int kMaxTopK = 16;
 constexpr int kBatchExp = 4;       // streamed experts per batch launch
 constexpr int kBatchTiles = 64;    // row tiles per batch launch
-constexpr int kLightTileRows = 16; // rows per tile of the light-expert kernels
+constexpr int kLightTileRows = 16; // rows per token block of the light-expert kernels
 constexpr int kMoeLightRowsMax = 1 << 20;
-constexpr int kLightAutoPairs = 32;  // default: light kernels for every expert up to this many pairs per expert
+constexpr int kLightClasses = 3;     // tiles of 4, 2 and 1 token blocks, in that order in the tile list
+constexpr int kLightTallPairs = 16;  // taller light tiles only above this many pairs per expert on average
+
+// Token blocks of 16 rows per light tile of an expert routed cnt pairs: the
+// smallest of 1, 2, 4 that covers cnt, at most mtmax.
+__host__ __device__ inline int light_mt(int cnt, int mtmax) {
+  int mt = 1;
+  while (mt < mtmax && mt < 4 && mt * kLightTileRows < cnt) mt *= 2;
+  return mt;
+}
+// class of a tile of mt token blocks: 0 for 4, 1 for 2, 2 for 1
+__host__ __device__ inline int light_class(int mt) { return mt == 4 ? 0 : (mt == 2 ? 1 : 2); }
 
 // The three weight tensors of one SwiGLU expert.
 struct ExpertW {
@@ -39,6 +50,7 @@ struct MoeArgs {
   const float* inv_r;          // per-token RMS-norm factor of x, or nullptr
   int k, H, I;
   int M;                       // tokens (rows of x)
+  int light_mtmax;             // light tiles: at most this many token blocks
   // decode with every expert HBM-resident (GEMV path only): tile t is routed
   // pair t, whose expert is pair_expert[t]; its rows in h and out are t, so no
   // bucketing sits between routing and the expert loads
@@ -64,25 +76,29 @@ size_t router_partial_floats(int M, int H, int E);
 
 // bucketing (single workgroup): counts, offsets, perm, inv_perm, heavy-first
 // expert order and the row tiles of experts with resident[e] != 0: tiles of
-// bm_rows rows for experts routed more than light_rows pairs, tiles of
-// kLightTileRows rows (ltiles, n_ltiles; may be null when light_rows is 0)
-// for the others
+// bm_rows rows for experts routed more than light_rows pairs; for the others
+// light tiles of 16 * light_mt(cnt, light_mtmax) rows in ltiles, with the
+// number of tiles of each class in n_ltiles[0 .. kLightClasses) (ltiles and
+// n_ltiles may be null when light_rows is 0)
 hipError_t launch_bucket(const int32_t* idx, int M, int k, int E, const uint8_t* resident, int bm_rows,
-                         int light_rows, int32_t* counts, int32_t* offsets, int32_t* perm, int32_t* inv_perm,
-                         int32_t* order, int32_t* tiles, int32_t* n_tiles, int32_t* ltiles, int32_t* n_ltiles,
-                         hipStream_t s);
+                         int light_rows, int light_mtmax, int32_t* counts, int32_t* offsets, int32_t* perm,
+                         int32_t* inv_perm, int32_t* order, int32_t* tiles, int32_t* n_tiles, int32_t* ltiles,
+                         int32_t* n_ltiles, hipStream_t s);
 
 // rows per tile of the grouped expert kernels (1 on the GEMV path)
 int expert_tile_rows(bool gemv);
 // grouped SwiGLU gate/up and grouped down; tile_bound = grid size in tiles
 hipError_t launch_expert_gateup(const MoeArgs& a, int tile_bound, bool gemv, hipStream_t s);
 hipError_t launch_expert_down(const MoeArgs& a, int tile_bound, bool gemv, hipStream_t s);
-// light experts (tiles of kLightTileRows rows from a.tiles / a.btiles): the
-// same products as the grouped GEMM, on a kernel that streams each weight once
-// per tile; shapes where light_supported(H, I) holds
+// light experts: the tiles of one class of a.tiles (the light list, counts
+// per class at a.n_tiles) or of a.btiles (all of that class): the grouped
+// GEMM's products, on kernels that stream each weight once per tile; shapes
+// where light_supported(H, I) holds, with tiles of at most
+// light_mtmax(H, I) token blocks
 bool light_supported(int H, int I);
-hipError_t launch_light_gateup(const MoeArgs& a, int tile_bound, hipStream_t s);
-hipError_t launch_light_down(const MoeArgs& a, int tile_bound, hipStream_t s);
+int light_mtmax(int H, int I);
+hipError_t launch_light_gateup(const MoeArgs& a, int cls, int tile_bound, hipStream_t s);
+hipError_t launch_light_down(const MoeArgs& a, int cls, int tile_bound, hipStream_t s);
 // pair-indexed decode (a.pair_expert set): the down projections of all k
 // experts of each of the M tokens and the combine, in one launch; the same
 // results as launch_expert_down followed by launch_combine

@@ -132,47 +132,55 @@ __global__ __launch_bounds__(kGemmBlock, 2) void expert_down_gemm(MoeArgs a, int
 
 // ---------------------------------------------------------------- light experts
 
-// Most experts of a prefill call are routed only a few tokens (under a Zipf
-// load most of the 128 draw fewer than 32 of 512), and a 64-row MFMA tile
-// then spends its K loop on staging activations that are mostly padding.  For
-// such experts a tile is kLightTileRows rows, and the kernel streams each
-// weight once per tile with no LDS staging of weights or activations:
+// Under a Zipf load most experts of a prefill call are routed a few tokens
+// and a few many.  On the fixed 64-row MFMA tile of the grouped GEMM the
+// light ones spend their K loop staging padding, and every tile walks K in
+// short LDS-staged steps whose load latency the pipeline does not cover.
+// Here an expert's tiles have 16, 32 or 64 rows (1, 2 or 4 token blocks of
+// 16: the fewest that cover its count), one launch per tile height, and the
+// weights stream through registers once per tile:
 //   * work items are (tile, block of output columns) in tile-major order; a
 //     workgroup (one per CU) takes a contiguous run of them, so it mostly
 //     stays on one tile and its activations, and a ring of loads runs on
 //     across items, so the next item's weights are in flight while an item
 //     finishes;
 //   * wavefront (ks, cg) takes K-slice ks (GS groups of 32 inputs) of the
-//     kLightSteps 16-row steps of column group cg of an item (gate/up: four
-//     steps of gate rows and the four matching steps of up rows);
+//     light_steps(MT) 16-row steps of column group cg of an item (gate/up:
+//     steps of gate rows, then the matching steps of up rows);
 //   * the tile's activations for the K-slice stay in registers as the A
-//     operands of v_mfma_f32_16x16x32_f16 (lane n + 16 c holds token n, inputs
-//     8c .. 8c + 7 of each group, permuted to the nibble pair order);
+//     operands of v_mfma_f32_16x16x32_f16, one per token block and group
+//     (lane n + 16 c holds token row n of the block, inputs 8c .. 8c + 7 of
+//     the group, permuted to the nibble pair order);
 //   * per step a lane loads GS / 4 x 16 code bytes of its weight row (groups
 //     c, c + 4, ... of the slice: four lanes read 64 contiguous bytes) and the
 //     row's scales of the slice; a 4 x 4 transpose of words across the four
 //     16-lane rows (permlane32 and permlane16 swaps) gives every lane the code
-//     word of its 8-input chunk for each group, which becomes eight exact fp16
-//     integers;
-//   * one MFMA per group sums that group's exact products for 16 tokens x 16
-//     weight rows, and the group's fp16 scale multiplies the sums in fp32
-//     (the arithmetic of the batched-decode kernel);
+//     word of its 8-input chunk for each group;
+//   * with one token block each word becomes eight exact fp16 integers, one
+//     MFMA per group sums that group's exact products and the group's fp16
+//     scale multiplies the sums in fp32 (the batched-decode arithmetic); with
+//     two or four blocks each word becomes eight weights w = RNE16(s * q) (q
+//     exact, one rounding of the product: the grouped GEMM's operand), so the
+//     ALU work per weight does not grow with the tile's rows, and the group
+//     sums of every block accumulate in the MFMA's fp32 accumulator;
 //   * each finished step's partial sums go to LDS; after a barrier the
 //     K-slices are summed in slice order and the epilogue (SwiGLU and the RMS
 //     factor, or the store by pair id) runs on every thread.
-#ifndef LIGHT_D
-#define LIGHT_D 8
+#ifndef LIGHT_D1
+#define LIGHT_D1 8
 #endif
-#ifndef LIGHT_D16
-#define LIGHT_D16 2
+#ifndef LIGHT_D2
+#define LIGHT_D2 4
 #endif
-constexpr int kLightSteps = 8;  // 16-row steps per wavefront and item
-constexpr int kLightMF = 4;     // MFMAs issued before their products are scaled
+#ifndef LIGHT_D4
+#define LIGHT_D4 4
+#endif
 constexpr int kLightWaves = 8;  // at most, per workgroup (one workgroup per CU)
 constexpr uint32_t kLightOob = 0x80000000u;  // an offset past every buffer here
-// steps of loads in flight (divides kLightSteps) for K-slices of gs groups
-constexpr int light_d(int gs) { return gs == 8 ? LIGHT_D : LIGHT_D16; }
-static_assert(kLightSteps % light_d(8) == 0 && kLightSteps % light_d(16) == 0, "the ring restarts at every item");
+// 16-row steps per item (the partial sums of an item fill at most 16 KB of
+// LDS per wavefront) and steps of loads in flight (dividing the steps)
+__host__ __device__ constexpr int light_steps(int mt) { return mt == 4 ? 4 : 8; }
+constexpr int light_d(int gs, int mt) { return gs == 16 ? 2 : (mt == 1 ? LIGHT_D1 : (mt == 2 ? LIGHT_D2 : LIGHT_D4)); }
 
 typedef float lf4_t __attribute__((ext_vector_type(4)));
 
@@ -216,6 +224,14 @@ __device__ __forceinline__ T ld_global(const T* p) {
 #endif
 }
 
+// Eight weights w = RNE16(s * q) from one code word, in the pair order of
+// unpack_q (q exact, then one rounding of the product).
+__device__ __forceinline__ gemv::half8_t dequant_word(uint32_t w, gemv::half2_t s2, const gemv::UnpackMasks& k) {
+  const gemv::half8_t q = gemv::unpack_q(w, k);
+  const gemv::half8_t s8 = {s2.x, s2.y, s2.x, s2.y, s2.x, s2.y, s2.x, s2.y};
+  return q * s8;
+}
+
 // One work item of a light launch, all of it uniform.  Past the workgroup's
 // items the pointers are null and every load of the ring reads zeros.
 struct LightItem {
@@ -226,8 +242,8 @@ struct LightItem {
   int tix, cb, base, rows;
 };
 
-template <bool DOWN>
-__device__ __forceinline__ LightItem light_item(const MoeArgs& a, int i, int i1, int ncb) {
+template <bool DOWN, int MT>
+__device__ __forceinline__ LightItem light_item(const MoeArgs& a, int t0, int i, int i1, int ncb) {
   LightItem it;
   if (i >= i1) {
     it.c0 = it.c1 = nullptr;
@@ -246,14 +262,14 @@ __device__ __forceinline__ LightItem light_item(const MoeArgs& a, int i, int i1,
     row0 = t.y;
     w = a.bw[t.x];
   } else {
-    e = ld_global(a.tiles + 2 * it.tix);
-    row0 = ld_global(a.tiles + 2 * it.tix + 1);
+    e = ld_global(a.tiles + 2 * (t0 + it.tix));
+    row0 = ld_global(a.tiles + 2 * (t0 + it.tix) + 1);
     w = ld_global(a.table + e);
   }
   e = __builtin_amdgcn_readfirstlane(e);
   row0 = __builtin_amdgcn_readfirstlane(row0);
   it.base = __builtin_amdgcn_readfirstlane(ld_global(a.offsets + e)) + row0;
-  it.rows = min(kLightTileRows, __builtin_amdgcn_readfirstlane(ld_global(a.counts + e)) - row0);
+  it.rows = min(kLightTileRows * MT, __builtin_amdgcn_readfirstlane(ld_global(a.counts + e)) - row0);
   const QView& w0 = DOWN ? w.down : w.gate;
   const QView& w1 = DOWN ? w.down : w.up;
   it.c0 = uniform_ptr(w0.codes);
@@ -263,15 +279,22 @@ __device__ __forceinline__ LightItem light_item(const MoeArgs& a, int i, int i1,
   return it;
 }
 
-template <bool DOWN, int GS>
+template <bool DOWN, int GS, int MT>
 __global__ __launch_bounds__(kLightWaves * 64) void expert_light(MoeArgs a, int nk, int nc, int ncb) {
   using namespace gemv;
-  constexpr int D = light_d(GS);
+  constexpr int S = light_steps(MT), D = light_d(GS, MT), RT = kLightTileRows * MT;
+  static_assert(S % D == 0, "the ring restarts at every item");
   extern __shared__ __attribute__((aligned(16))) char smem[];
-  lf4_t* red = reinterpret_cast<lf4_t*>(smem);  // [wave][step][lane]
-  __shared__ int row_dst[kLightTileRows];       // output row of tile row m (pair id / bucket row)
-  __shared__ float row_scale[kLightTileRows];   // gate/up: the token's RMS factor
-  const int ntiles = a.nb > 0 ? a.nb : __builtin_amdgcn_readfirstlane(ld_global(a.n_tiles));
+  lf4_t* red = reinterpret_cast<lf4_t*>(smem);  // [wave][step][token block][lane]
+  __shared__ int row_dst[RT];                   // output row of tile row m (pair id / bucket row)
+  __shared__ float row_scale[RT];               // gate/up: the token's RMS factor
+  // this class's tiles: the light list's range for MT, or the whole batch
+  const int cls = light_class(MT);
+  int t0 = 0, ntiles = a.nb;
+  if (a.nb == 0) {
+    for (int q = 0; q < cls; ++q) t0 += __builtin_amdgcn_readfirstlane(ld_global(a.n_tiles + q));
+    ntiles = __builtin_amdgcn_readfirstlane(ld_global(a.n_tiles + cls));
+  }
   const int total = ntiles * ncb;
   const int per = (total + (int)gridDim.x - 1) / (int)gridDim.x;
   const int i0 = (int)blockIdx.x * per, i1 = min(i0 + per, total);
@@ -282,7 +305,7 @@ __global__ __launch_bounds__(kLightWaves * 64) void expert_light(MoeArgs a, int 
   const int ks = wave % nk, cg = wave / nk;
   const int n = lane & 15, c = lane >> 4;
   const int g0 = ks * GS;
-  constexpr int OUTS = DOWN ? 16 * kLightSteps : 8 * kLightSteps;  // output columns per column group
+  constexpr int OUTS = DOWN ? 16 * S : 8 * S;  // output columns per column group and item
   const uint32_t cbytes = (uint32_t)((size_t)N * K / 2), sbytes = (uint32_t)((size_t)N * G * 2);
 
   struct Ld {
@@ -292,8 +315,8 @@ __global__ __launch_bounds__(kLightWaves * 64) void expert_light(MoeArgs a, int 
   // step st of item it: weight row col0 + 16 st + n (gate/up: gate rows for
   // the first half of the steps, up rows after)
   auto load = [&](Ld& b, const LightItem& it, int st) {
-    const bool second = !DOWN && st >= kLightSteps / 2;
-    const int row = (it.cb * nc + cg) * OUTS + 16 * (DOWN ? st : (st % (kLightSteps / 2))) + n;
+    const bool second = !DOWN && st >= S / 2;
+    const int row = (it.cb * nc + cg) * OUTS + 16 * (DOWN ? st : (st % (S / 2))) + n;
     const bool live = it.tix >= 0;
     const bool ok = row < N && live;
     const uint32_t co = ok ? (uint32_t)row * (uint32_t)(K / 2) + (uint32_t)(g0 + c) * 16 : kLightOob;
@@ -307,25 +330,34 @@ __global__ __launch_bounds__(kLightWaves * 64) void expert_light(MoeArgs a, int 
     for (int q = 0; q < GS / 8; ++q)
       b.s[q] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rs, so + 16 * q, 0, 0));
   };
-  // token row n of a tile (gate/up: its pair's id, looked up before the
-  // weight loads go out, so that waiting for it does not wait for them)
-  auto pair_of = [&](const LightItem& it) {
-    return DOWN ? 0 : ld_global(a.perm + it.base + (n < it.rows ? n : 0));
-  };
-  // A operand: lane n + 16 c holds token row n, inputs 8c .. 8c + 7 of each
-  // group of the slice (zeros past the tile's rows); the epilogue's row table
+  // A operands: token block t, row 16 t + n of the tile (zeros past its
+  // rows); gate/up looks the rows' pair ids up before the ring's loads go
+  // out, so that waiting for them does not wait for those
   const __amdgpu_buffer_rsrc_t rx = DOWN ? light_rsrc(a.h, (uint32_t)((size_t)a.M * a.k * a.I * 2))
                                          : light_rsrc(a.x, (uint32_t)((size_t)a.M * a.H * 2));
-  half8_t xa[GS];
-  auto load_rows = [&](const LightItem& it, int pr) {
-    const bool has_row = n < it.rows;
-    const uint32_t rowoff = DOWN ? (uint32_t)(it.base + n) * (uint32_t)a.I * 2 : (uint32_t)(pr / a.k) * (uint32_t)a.H * 2;
-    const uint32_t xo = rowoff + (uint32_t)(g0 * kGroup + c * 8) * 2;
+  half8_t xa[MT][GS];
+  int prs[MT];
+  auto pairs_of = [&](const LightItem& it) {
 #pragma unroll
-    for (int g = 0; g < GS; ++g) {
-      const u32x4_t v = __builtin_bit_cast(
-          u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rx, has_row ? xo + (uint32_t)g * kGroup * 2 : kLightOob, 0, 0));
-      xa[g] = perm_x(v);
+    for (int t = 0; t < MT; ++t) {
+      const int m = kLightTileRows * t + n;
+      prs[t] = DOWN ? 0 : ld_global(a.perm + it.base + (m < it.rows ? m : 0));
+    }
+  };
+  auto load_rows = [&](const LightItem& it) {
+#pragma unroll
+    for (int t = 0; t < MT; ++t) {
+      const int m = kLightTileRows * t + n;
+      const bool has_row = m < it.rows;
+      const uint32_t rowoff =
+          DOWN ? (uint32_t)(it.base + m) * (uint32_t)a.I * 2 : (uint32_t)(prs[t] / a.k) * (uint32_t)a.H * 2;
+      const uint32_t xo = rowoff + (uint32_t)(g0 * kGroup + c * 8) * 2;
+#pragma unroll
+      for (int g = 0; g < GS; ++g) {
+        const u32x4_t v = __builtin_bit_cast(
+            u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rx, has_row ? xo + (uint32_t)g * kGroup * 2 : kLightOob, 0, 0));
+        xa[t][g] = perm_x(v);
+      }
     }
     if (threadIdx.x < (unsigned)it.rows) {
       const int m = threadIdx.x;
@@ -335,25 +367,25 @@ __global__ __launch_bounds__(kLightWaves * 64) void expert_light(MoeArgs a, int 
     }
   };
 
-  LightItem cur = light_item<DOWN>(a, i0, i1, ncb);
-  LightItem nxt = light_item<DOWN>(a, i0 + 1, i1, ncb);
-  const int pr0 = pair_of(cur);
+  LightItem cur = light_item<DOWN, MT>(a, t0, i0, i1, ncb);
+  LightItem nxt = light_item<DOWN, MT>(a, t0, i0 + 1, i1, ncb);
+  pairs_of(cur);
   __builtin_amdgcn_sched_barrier(0);
   Ld buf[D];
 #pragma unroll
   for (int d = 0; d < D; ++d) load(buf[d], cur, d);
   __builtin_amdgcn_sched_barrier(0);
-  load_rows(cur, pr0);
+  load_rows(cur);
 
   const UnpackMasks um = unpack_masks();
   const lf4_t zero = {0.f, 0.f, 0.f, 0.f};
-  lf4_t* mine = red + (size_t)wave * kLightSteps * 64 + lane;
-  constexpr int SPO = DOWN ? kLightSteps : kLightSteps / 2;  // steps per set of outputs
-  const int nent = nc * SPO * 64;
+  lf4_t* mine = red + (size_t)wave * S * MT * 64 + lane;
+  constexpr int SPO = DOWN ? S : S / 2;  // steps per set of outputs
+  const int nent = nc * SPO * MT * 64;
 
   for (int i = i0; i < i1; ++i) {
 #pragma unroll
-    for (int st = 0; st < kLightSteps; ++st) {
+    for (int st = 0; st < S; ++st) {
       Ld& b = buf[st % D];
       uint32_t t4[GS / 4][4];
 #pragma unroll
@@ -367,50 +399,69 @@ __global__ __launch_bounds__(kLightWaves * 64) void expert_light(MoeArgs a, int 
 #pragma unroll
       for (int q = 0; q < GS / 8; ++q) sv[q] = b.s[q];
       // refill: a later step of this item, or an early one of the next
-      if (st + D < kLightSteps)
+      if (st + D < S)
         load(b, cur, st + D);
       else
-        load(b, nxt, st + D - kLightSteps);
+        load(b, nxt, st + D - S);
 #pragma unroll
       for (int q = 0; q < GS / 4; ++q) transpose_rows4(t4[q]);
-      lf4_t acc = zero;
-      // kLightMF MFMAs in flight before their products are scaled
+      lf4_t acc[MT];
+      if constexpr (MT == 1) {
+        // one token block: exact group sums (independent MFMAs, integer
+        // weights), each scaled by its group's scale in fp32
+        acc[0] = zero;
 #pragma unroll
-      for (int h = 0; h < GS / kLightMF; ++h) {
-        lf4_t p[kLightMF];
+        for (int h = 0; h < GS / 4; ++h) {
+          lf4_t p[4];
 #pragma unroll
-        for (int j = 0; j < kLightMF; ++j) {
-          const int g = kLightMF * h + j;
-          p[j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(xa[g], unpack_q(t4[g >> 2][g & 3], um), zero, 0, 0, 0);
+          for (int j = 0; j < 4; ++j) {
+            const int g = 4 * h + j;
+            p[j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(xa[0][g], unpack_q(t4[h][j], um), zero, 0, 0, 0);
+          }
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const int g = 4 * h + j;
+            const uint32_t pair = sv[g >> 3][(g & 7) >> 1];
+            const float sc = __half2float(__ushort_as_half((uint16_t)((g & 1) ? pair >> 16 : pair)));
+#pragma unroll
+            for (int v = 0; v < 4; ++v) acc[0][v] = fmaf(sc, p[j][v], acc[0][v]);
+          }
         }
+      } else {
+        // several token blocks share each dequantised weight: w = RNE16(s q),
+        // the group sums accumulating in the MFMA
 #pragma unroll
-        for (int j = 0; j < kLightMF; ++j) {
-          const int g = kLightMF * h + j;
+        for (int t = 0; t < MT; ++t) acc[t] = zero;
+#pragma unroll
+        for (int g = 0; g < GS; ++g) {
           const uint32_t pair = sv[g >> 3][(g & 7) >> 1];
-          const float sc = __half2float(__ushort_as_half((uint16_t)((g & 1) ? pair >> 16 : pair)));
+          const uint32_t sb = (g & 1) ? pair >> 16 : pair & 0xFFFFu;
+          const half8_t wq = dequant_word(t4[g >> 2][g & 3], __builtin_bit_cast(half2_t, sb * 0x10001u), um);
 #pragma unroll
-          for (int v = 0; v < 4; ++v) acc[v] = fmaf(sc, p[j][v], acc[v]);
+          for (int t = 0; t < MT; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(xa[t][g], wq, acc[t], 0, 0, 0);
         }
       }
-      mine[st * 64] = acc;
+#pragma unroll
+      for (int t = 0; t < MT; ++t) mine[(st * MT + t) * 64] = acc[t];
     }
     __syncthreads();
 
-    // slices summed in order; D[m][n] of a step sits in lane n + 16 (m / 4), item m % 4
+    // slices summed in order; D[m][n] of a token block sits in lane
+    // n + 16 (m / 4), item m % 4
     for (int q = threadIdx.x; q < nent; q += blockDim.x) {
-      const int l = q & 63, sidx = (q >> 6) % SPO, cgq = (q >> 6) / SPO;
+      const int l = q & 63, t = (q >> 6) % MT, sidx = (q >> 6) / MT % SPO, cgq = (q >> 6) / MT / SPO;
       const int col = (cur.cb * nc + cgq) * OUTS + 16 * sidx + (l & 15);
       if (col >= N) continue;
-      const lf4_t* r0 = red + (size_t)cgq * nk * kLightSteps * 64 + l;
-      lf4_t v = r0[sidx * 64], u = zero;
-      if constexpr (!DOWN) u = r0[(sidx + SPO) * 64];
+      const lf4_t* r0 = red + (size_t)cgq * nk * S * MT * 64 + t * 64 + l;
+      lf4_t v = r0[sidx * MT * 64], u = zero;
+      if constexpr (!DOWN) u = r0[(sidx + SPO) * MT * 64];
       for (int k2 = 1; k2 < nk; ++k2) {
-        v += r0[((size_t)k2 * kLightSteps + sidx) * 64];
-        if constexpr (!DOWN) u += r0[((size_t)k2 * kLightSteps + sidx + SPO) * 64];
+        v += r0[((size_t)k2 * S + sidx) * MT * 64];
+        if constexpr (!DOWN) u += r0[((size_t)k2 * S + sidx + SPO) * MT * 64];
       }
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const int m = 4 * (l >> 4) + j;
+        const int m = kLightTileRows * t + 4 * (l >> 4) + j;
         if (m >= cur.rows) break;
         if constexpr (DOWN) {
           a.out[(size_t)row_dst[m] * a.H + col] = __float2half_rn(v[j]);
@@ -423,28 +474,28 @@ __global__ __launch_bounds__(kLightWaves * 64) void expert_light(MoeArgs a, int 
     }
     __syncthreads();
     if (i + 1 < i1) {
-      if (nxt.tix != cur.tix) load_rows(nxt, pair_of(nxt));
+      if (nxt.tix != cur.tix) {
+        pairs_of(nxt);
+        load_rows(nxt);
+      }
       cur = nxt;
-      nxt = light_item<DOWN>(a, i + 2, i1, ncb);
+      nxt = light_item<DOWN, MT>(a, t0, i + 2, i1, ncb);
     }
   }
 }
 
 // groups per K-slice: 8, or 16 where 8 would take more than kLightWaves slices
 int light_gs(int K) { return K / kGroup / 8 <= kLightWaves ? 8 : 16; }
+// token blocks per tile the kernels hold: 4 with 8-group slices, 1 with 16
+int light_mtmax_k(int K) { return light_gs(K) == 8 ? 4 : 1; }
 
-template <bool DOWN>
-hipError_t launch_light(const MoeArgs& a, int tile_bound, hipStream_t s) {
-  if (tile_bound <= 0) return hipSuccess;
-  if (!light_supported(a.H, a.I)) return hipErrorInvalidValue;
-  const int K = DOWN ? a.I : a.H, N = DOWN ? a.H : a.I;
-  const int gs = light_gs(K);
-  const int nk = K / (gs * kGroup);
-  const int nc = std::max(1, kLightWaves / nk);
-  const int outs = (DOWN ? 16 : 8) * kLightSteps * nc;
+template <bool DOWN, int GS, int MT>
+hipError_t launch_light_cfg(const MoeArgs& a, int tile_bound, int nk, int nc, hipStream_t s) {
+  const int N = DOWN ? a.H : a.I;
+  const int outs = (DOWN ? 16 : 8) * light_steps(MT) * nc;
   const int ncb = (N + outs - 1) / outs;
-  const size_t lds = (size_t)nk * nc * kLightSteps * 64 * sizeof(lf4_t);
-  if (lds + 2 * kLightTileRows * 4 > lds_limit()) return hipErrorInvalidValue;
+  const size_t lds = (size_t)nk * nc * light_steps(MT) * MT * 64 * sizeof(lf4_t);
+  if (lds + 2 * kLightTileRows * MT * 4 > lds_limit()) return hipErrorInvalidValue;
   // one workgroup per CU: each holds its loads in flight in registers
   int cus = 256;
   int dev = 0;
@@ -452,11 +503,22 @@ hipError_t launch_light(const MoeArgs& a, int tile_bound, hipStream_t s) {
                                                hipSuccess || cus < 1)
     cus = 256;
   const int grid = std::min(tile_bound * ncb, cus);
-  if (gs == 8)
-    hipLaunchKernelGGL((expert_light<DOWN, 8>), dim3(grid), dim3(nk * nc * 64), lds, s, a, nk, nc, ncb);
-  else
-    hipLaunchKernelGGL((expert_light<DOWN, 16>), dim3(grid), dim3(nk * nc * 64), lds, s, a, nk, nc, ncb);
+  hipLaunchKernelGGL((expert_light<DOWN, GS, MT>), dim3(grid), dim3(nk * nc * 64), lds, s, a, nk, nc, ncb);
   return hipGetLastError();
+}
+
+template <bool DOWN>
+hipError_t launch_light(const MoeArgs& a, int cls, int tile_bound, hipStream_t s) {
+  if (tile_bound <= 0) return hipSuccess;
+  if (!light_supported(a.H, a.I) || cls < 0 || cls >= kLightClasses) return hipErrorInvalidValue;
+  const int K = DOWN ? a.I : a.H;
+  const int gs = light_gs(K);
+  const int nk = K / (gs * kGroup);
+  const int nc = std::max(1, kLightWaves / nk);
+  if (gs == 16) return cls == 2 ? launch_light_cfg<DOWN, 16, 1>(a, tile_bound, nk, nc, s) : hipErrorInvalidValue;
+  if (cls == 0) return launch_light_cfg<DOWN, 8, 4>(a, tile_bound, nk, nc, s);
+  if (cls == 1) return launch_light_cfg<DOWN, 8, 2>(a, tile_bound, nk, nc, s);
+  return launch_light_cfg<DOWN, 8, 1>(a, tile_bound, nk, nc, s);
 }
 
 // ---------------------------------------------------------------- GEMV path (one row per tile)
@@ -699,12 +761,15 @@ bool light_supported(int H, int I) {
   return ok(H) && ok(I);
 }
 
-hipError_t launch_light_gateup(const MoeArgs& a, int tile_bound, hipStream_t s) {
-  return launch_light<false>(a, tile_bound, s);
+// the gate/up and down launches share the tile list
+int light_mtmax(int H, int I) { return std::min(light_mtmax_k(H), light_mtmax_k(I)); }
+
+hipError_t launch_light_gateup(const MoeArgs& a, int cls, int tile_bound, hipStream_t s) {
+  return launch_light<false>(a, cls, tile_bound, s);
 }
 
-hipError_t launch_light_down(const MoeArgs& a, int tile_bound, hipStream_t s) {
-  return launch_light<true>(a, tile_bound, s);
+hipError_t launch_light_down(const MoeArgs& a, int cls, int tile_bound, hipStream_t s) {
+  return launch_light<true>(a, cls, tile_bound, s);
 }
 
 hipError_t launch_expert_down_combine(const MoeArgs& a, int M, const float* p, const __half* res, __half* y,

@@ -382,8 +382,11 @@ __global__ __launch_bounds__(256) void router_partial_kernel(const __half* __res
   const int k_begin = blockIdx.y * ks, k_end = k_begin + ks;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int tr = lane & 15, kq = (lane >> 4) * 8;
-  const int kk = threadIdx.x >> 4, e8 = (threadIdx.x & 15) * 8;
-  const bool wl = e8 < E;
+  // staging roles: k row kk of the step, experts e8 .. e8 + 7 and 64 above
+  // (a wave's 2-byte LDS stores then cover 16 consecutive dwords twice,
+  // 32 banks apart: no bank conflicts)
+  const int kk = threadIdx.x & 31, e8 = (threadIdx.x >> 5) * 8;
+  const bool wl = e8 < E, wl2 = e8 + 64 < E;
   const int t = t0 + tr;
   // squares of the slice's inputs, for the norm factors of the fused routing
   const bool sq = FUSED && ro.inv_r_out && wave == 0;
@@ -392,24 +395,23 @@ __global__ __launch_bounds__(256) void router_partial_kernel(const __half* __res
   uint4 w0 = {0, 0, 0, 0}, w1 = {0, 0, 0, 0};
   half8_t a = {0, 0, 0, 0, 0, 0, 0, 0};
   auto fetch = [&](int k0) {
-    // W_r rows k0 + kk and k0 + kk + 16, 8 experts from e8; x[t][k0 + kq ..]
-    if (wl) {
-      w0 = *reinterpret_cast<const uint4*>(wr + (size_t)(k0 + kk) * E + e8);
-      w1 = *reinterpret_cast<const uint4*>(wr + (size_t)(k0 + kk + 16) * E + e8);
-    }
+    // W_r row k0 + kk, 8 experts from e8 and from e8 + 64; x[t][k0 + kq ..]
+    if (wl) w0 = *reinterpret_cast<const uint4*>(wr + (size_t)(k0 + kk) * E + e8);
+    if (wl2) w1 = *reinterpret_cast<const uint4*>(wr + (size_t)(k0 + kk) * E + e8 + 64);
     if (t < M) a = *reinterpret_cast<const half8_t*>(x + (size_t)t * H + k0 + kq);
   };
   fetch(k_begin);
   for (int k0 = k_begin; k0 < k_end; k0 += 32) {
     __syncthreads();  // the previous step's reads of Bt are done
+    const _Float16* h0 = reinterpret_cast<const _Float16*>(&w0);
+    const _Float16* h1 = reinterpret_cast<const _Float16*>(&w1);
     if (wl) {
-      const _Float16* h0 = reinterpret_cast<const _Float16*>(&w0);
-      const _Float16* h1 = reinterpret_cast<const _Float16*>(&w1);
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        Bt[(e8 + i) * 40 + kk] = h0[i];
-        Bt[(e8 + i) * 40 + kk + 16] = h1[i];
-      }
+      for (int i = 0; i < 8; ++i) Bt[(e8 + i) * 40 + kk] = h0[i];
+    }
+    if (wl2) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) Bt[(e8 + 64 + i) * 40 + kk] = h1[i];
     }
     const half8_t ac = a;
     if (k0 + 32 < k_end) fetch(k0 + 32);
@@ -504,7 +506,7 @@ __device__ int scan128(const int* v, int* out, int E) {
 constexpr int kBucketThreads = 1024;
 __global__ __launch_bounds__(kBucketThreads) void bucket_kernel(const int32_t* __restrict__ idx, int M, int k, int E,
                                                       const uint8_t* __restrict__ resident, int bm_rows,
-                                                      int light_rows, int32_t* __restrict__ counts,
+                                                      int light_rows, int light_mtmax, int32_t* __restrict__ counts,
                                                       int32_t* __restrict__ offsets, int32_t* __restrict__ perm,
                                                       int32_t* __restrict__ inv_perm, int32_t* __restrict__ order,
                                                       int32_t* __restrict__ tiles, int32_t* __restrict__ n_tiles,
@@ -518,6 +520,7 @@ __global__ __launch_bounds__(kBucketThreads) void bucket_kernel(const int32_t* _
   __shared__ int tstart[kMaxExperts];
   __shared__ int nlt[kMaxExperts];     // light tiles of the expert at rank r
   __shared__ int lstart[kMaxExperts];
+  __shared__ int lclass[kLightClasses];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int pairs = M * k;
   for (int e = tid; e < E; e += blockDim.x) cnt[e] = 0;
@@ -592,22 +595,24 @@ __global__ __launch_bounds__(kBucketThreads) void bucket_kernel(const int32_t* _
   }
   __syncthreads();
   // row tiles of resident experts in heavy-first order: tile -> (expert, first
-  // row); experts routed at most light_rows pairs get tiles of kLightTileRows
-  // rows in the second list instead
+  // row); experts routed at most light_rows pairs get light tiles in the
+  // second list instead (their class never rises along the list)
+  if (tid < kLightClasses) lclass[tid] = 0;
+  __syncthreads();
   for (int r = tid; r < E; r += blockDim.x) {
     const int e = ord[r];
     const bool res = resident == nullptr || resident[e];
     const bool light = cnt[e] <= light_rows;
+    const int lrows = kLightTileRows * light_mt(cnt[e], light_mtmax);
     ntile[r] = (res && !light) ? (cnt[e] + bm_rows - 1) / bm_rows : 0;
-    nlt[r] = (res && light) ? (cnt[e] + kLightTileRows - 1) / kLightTileRows : 0;
+    nlt[r] = (res && light) ? (cnt[e] + lrows - 1) / lrows : 0;
+    if (nlt[r]) atomicAdd(&lclass[light_class(light_mt(cnt[e], light_mtmax))], nlt[r]);
   }
   __syncthreads();
   const int nt = scan128(ntile, tstart, E);
-  const int nl = scan128(nlt, lstart, E);
-  if (tid == 0) {
-    *n_tiles = nt;
-    if (n_ltiles) *n_ltiles = nl;
-  }
+  scan128(nlt, lstart, E);
+  if (tid == 0) *n_tiles = nt;
+  if (n_ltiles && tid < kLightClasses) n_ltiles[tid] = lclass[tid];
   __syncthreads();
   for (int r = wave; r < E; r += blockDim.x / 64) {
     const int e = ord[r];
@@ -615,9 +620,10 @@ __global__ __launch_bounds__(kBucketThreads) void bucket_kernel(const int32_t* _
       tiles[2 * (tstart[r] + i)] = e;
       tiles[2 * (tstart[r] + i) + 1] = i * bm_rows;
     }
+    const int lrows = kLightTileRows * light_mt(cnt[e], light_mtmax);
     for (int i = lane; i < nlt[r]; i += 64) {
       ltiles[2 * (lstart[r] + i)] = e;
-      ltiles[2 * (lstart[r] + i) + 1] = i * kLightTileRows;
+      ltiles[2 * (lstart[r] + i) + 1] = i * lrows;
     }
   }
 }
@@ -764,12 +770,13 @@ size_t router_partial_floats(int M, int H, int E) {
 }
 
 hipError_t launch_bucket(const int32_t* idx, int M, int k, int E, const uint8_t* resident, int bm_rows,
-                         int light_rows, int32_t* counts, int32_t* offsets, int32_t* perm, int32_t* inv_perm,
-                         int32_t* order, int32_t* tiles, int32_t* n_tiles, int32_t* ltiles, int32_t* n_ltiles,
-                         hipStream_t s) {
-  if (k < 1 || k > kMaxTopK || (light_rows > 0 && (!ltiles || !n_ltiles))) return hipErrorInvalidValue;
+                         int light_rows, int light_mtmax, int32_t* counts, int32_t* offsets, int32_t* perm,
+                         int32_t* inv_perm, int32_t* order, int32_t* tiles, int32_t* n_tiles, int32_t* ltiles,
+                         int32_t* n_ltiles, hipStream_t s) {
+  if (k < 1 || k > kMaxTopK || (light_rows > 0 && (!ltiles || !n_ltiles || light_mtmax < 1)))
+    return hipErrorInvalidValue;
   hipLaunchKernelGGL(bucket_kernel, dim3(1), dim3(kBucketThreads), 0, s, idx, M, k, E, resident, bm_rows, light_rows,
-                     counts, offsets, perm, inv_perm, order, tiles, n_tiles, ltiles, n_ltiles);
+                     light_mtmax, counts, offsets, perm, inv_perm, order, tiles, n_tiles, ltiles, n_ltiles);
   return hipGetLastError();
 }
 
