@@ -16,7 +16,7 @@
 // its own arguments.
 #include "moe.h"
 #include "q4_gemm_core.h"
-#include "q4_gemv_core.h"
+#include "q4_mfma_unpack.h"
 
 namespace atsi {
 namespace {

@@ -190,33 +190,5 @@ __device__ __forceinline__ float group_dot_m(const uint4& cw, const XGroup& g, c
   return fmaf(so, 0.0625f, se - g.corr);
 }
 
-typedef _Float16 half8_t __attribute__((ext_vector_type(8)));
-typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
-
-// Eight exact fp16 integers q = u - 8 from one code word, in the pair order
-// (k0, k4), (k1, k5), (k2, k6), (k3, k7): the B operand of an MFMA that sums
-// one group's exact products.
-__device__ __forceinline__ half8_t unpack_q(uint32_t w, const UnpackMasks& k) {
-  const uint32_t w8 = w >> 8;
-  const half2_t off = {(_Float16)-1032.f, (_Float16)-1032.f};
-  const half2_t sh = {(_Float16)0.0625f, (_Float16)0.0625f};
-  const half2_t off16 = {(_Float16)-72.f, (_Float16)-72.f};
-  // (1024 + u) - 1032 and (1024 + 16 u) / 16 - 72 are exact in fp16
-  const half2_t a = __builtin_bit_cast(half2_t, (w & k.lo) | k.magic) + off;
-  const half2_t b = __builtin_bit_cast(half2_t, (w & k.hi) | k.magic) * sh + off16;
-  const half2_t c = __builtin_bit_cast(half2_t, (w8 & k.lo) | k.magic) + off;
-  const half2_t d = __builtin_bit_cast(half2_t, (w8 & k.hi) | k.magic) * sh + off16;
-  const u32x4_t r = {__builtin_bit_cast(uint32_t, a), __builtin_bit_cast(uint32_t, b), __builtin_bit_cast(uint32_t, c),
-                     __builtin_bit_cast(uint32_t, d)};
-  return __builtin_bit_cast(half8_t, r);
-}
-
-// Eight consecutive fp16 activations reordered to the same pair order.
-__device__ __forceinline__ half8_t perm_x(u32x4_t d) {
-  const u32x4_t r = {__builtin_amdgcn_perm(d.z, d.x, 0x05040100u), __builtin_amdgcn_perm(d.z, d.x, 0x07060302u),
-                     __builtin_amdgcn_perm(d.w, d.y, 0x05040100u), __builtin_amdgcn_perm(d.w, d.y, 0x07060302u)};
-  return __builtin_bit_cast(half8_t, r);
-}
-
 }  // namespace gemv
 }  // namespace atsi

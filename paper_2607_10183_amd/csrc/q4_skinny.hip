@@ -32,7 +32,7 @@
 //     product is what is kept).
 // The epilogue is the GEMV's: SwiGLU product, residual, fp32 output, KV-head
 // expansion, over up to three tensors sharing the input.
-#include "q4_gemv_core.h"
+#include "q4_mfma_unpack.h"
 
 namespace atsi {
 namespace {
