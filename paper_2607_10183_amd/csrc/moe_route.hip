@@ -521,6 +521,7 @@ __global__ __launch_bounds__(kBucketThreads) void bucket_kernel(const int32_t* _
   __shared__ int nlt[kMaxExperts];     // light tiles of the expert at rank r
   __shared__ int lstart[kMaxExperts];
   __shared__ int lclass[kLightClasses];
+  __shared__ int rpart[8][kMaxExperts];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int pairs = M * k;
   for (int e = tid; e < E; e += blockDim.x) cnt[e] = 0;
@@ -579,19 +580,26 @@ __global__ __launch_bounds__(kBucketThreads) void bucket_kernel(const int32_t* _
     }
     __syncthreads();
   }
-  // heavy-first expert order: (count descending, id ascending)
-  for (int e = tid; e < E; e += blockDim.x) {
+  // heavy-first expert order: (count descending, id ascending); eight
+  // threads per expert each count the experts ahead of it in an eighth of
+  // the others (E is a multiple of 16)
+  if (tid < 8 * E) {
+    const int e = tid % E, part = tid / E, span = E / 8;
     const int ce = cnt[e];
     int r = 0;
-    for (int f0 = 0; f0 < E; f0 += 16) {  // E is a multiple of 16
-      int cf[16];
-#pragma unroll
-      for (int j = 0; j < 16; ++j) cf[j] = cnt[f0 + j];
-#pragma unroll
-      for (int j = 0; j < 16; ++j) r += (cf[j] > ce) || (cf[j] == ce && f0 + j < e);
+    for (int f = part * span; f < (part + 1) * span; ++f) {
+      const int cf = cnt[f];
+      r += (cf > ce) || (cf == ce && f < e);
     }
-    ord[r] = e;
-    order[r] = e;
+    rpart[part][e] = r;
+  }
+  __syncthreads();
+  if (tid < E) {
+    int r = 0;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) r += rpart[q][tid];
+    ord[r] = tid;
+    order[r] = tid;
   }
   __syncthreads();
   // row tiles of resident experts in heavy-first order: tile -> (expert, first
@@ -614,16 +622,17 @@ __global__ __launch_bounds__(kBucketThreads) void bucket_kernel(const int32_t* _
   if (tid == 0) *n_tiles = nt;
   if (n_ltiles && tid < kLightClasses) n_ltiles[tid] = lclass[tid];
   __syncthreads();
-  for (int r = wave; r < E; r += blockDim.x / 64) {
-    const int e = ord[r];
-    for (int i = lane; i < ntile[r]; i += 64) {
-      tiles[2 * (tstart[r] + i)] = e;
-      tiles[2 * (tstart[r] + i) + 1] = i * bm_rows;
+  // one thread per rank writes that expert's tiles
+  for (int r = tid; r < E; r += blockDim.x) {
+    const int e = ord[r], t0 = tstart[r], l0 = lstart[r];
+    for (int i = 0; i < ntile[r]; ++i) {
+      tiles[2 * (t0 + i)] = e;
+      tiles[2 * (t0 + i) + 1] = i * bm_rows;
     }
     const int lrows = kLightTileRows * light_mt(cnt[e], light_mtmax);
-    for (int i = lane; i < nlt[r]; i += 64) {
-      ltiles[2 * (lstart[r] + i)] = e;
-      ltiles[2 * (lstart[r] + i) + 1] = i * lrows;
+    for (int i = 0; i < nlt[r]; ++i) {
+      ltiles[2 * (l0 + i)] = e;
+      ltiles[2 * (l0 + i) + 1] = i * lrows;
     }
   }
 }
