@@ -338,7 +338,8 @@ atsi_status atsi_set_zero_copy(atsi_ctx* ctx, int32_t enable);
  * on the light-expert kernels: tiles that stream each weight through
  * registers once per tile, of 16 rows, or, in calls that route more than 16
  * pairs per expert on average, of 16, 32 or 64 rows (the fewest 16-row blocks
- * that cover its count). 16-row tiles sum each group's exact products and
+ * that cover its count; at most 32 rows for hidden or intermediate sizes
+ * above 2048). 16-row tiles sum each group's exact products and
  * scale them in fp32 (the decode arithmetic); taller tiles round each weight
  * to fp16 once, as the grouped GEMM does. The other experts run on the
  * grouped GEMM (tiles of 64 rows staged through LDS). rows = 0 sends every
@@ -346,8 +347,8 @@ atsi_status atsi_set_zero_copy(atsi_ctx* ctx, int32_t enable);
  * light kernels, except in calls of more than 16 pairs per expert on shapes
  * that allow only 16-row tiles, which keep the grouped GEMM. The light
  * kernels cover hidden and intermediate sizes that are multiples of 256 up to
- * 4096 (above 2048 in 16-row tiles only, and only where 16-group slices
- * divide the size evenly); other shapes always take the grouped GEMM. The
+ * 4096 (above 2048 only where 16-group slices divide the size evenly); other
+ * shapes always take the grouped GEMM. The
  * choice depends only on the call's size and routed counts, so HBM-resident
  * and streamed experts give the same bits; the kernels differ by rounding
  * only.

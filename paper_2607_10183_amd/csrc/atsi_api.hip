@@ -1182,7 +1182,7 @@ atsi_status run_moe(atsi_ctx* c, const atsi_moe* m, const __half* x, int Mi, __h
   // 16-row tiles, large calls keep the grouped GEMM by default: heavy experts
   // would be streamed once per 16 of their rows.
   const bool tall = Mk > kLightTallPairs * E;
-  if (tall && c->moe_light_rows < 0 && light && light_mtmax(H, I) < 4) light = 0;
+  if (tall && c->moe_light_rows < 0 && light && light_mtmax(H, I) < 2) light = 0;
   const int lmt = !light ? 0 : (tall ? light_mtmax(H, I) : 1);
   float* part = (float*)sc.take(router_partial_floats(Mi, H, E), 4);
   int32_t* idx = dbg && dbg->idx ? dbg->idx : (int32_t*)sc.take(Mk, 4);
@@ -1235,7 +1235,6 @@ atsi_status run_moe(atsi_ctx* c, const atsi_moe* m, const __half* x, int Mi, __h
   a.inv_r = inv_r;
   a.k = k;
   a.M = Mi;
-  a.light_mtmax = lmt;
   a.H = H;
   a.I = I;
   if (by_pair) {

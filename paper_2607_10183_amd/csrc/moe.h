@@ -50,7 +50,6 @@ struct MoeArgs {
   const float* inv_r;          // per-token RMS-norm factor of x, or nullptr
   int k, H, I;
   int M;                       // tokens (rows of x)
-  int light_mtmax;             // light tiles: at most this many token blocks
   // decode with every expert HBM-resident (GEMV path only): tile t is routed
   // pair t, whose expert is pair_expert[t]; its rows in h and out are t, so no
   // bucketing sits between routing and the expert loads

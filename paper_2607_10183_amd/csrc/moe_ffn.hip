@@ -175,6 +175,9 @@ __global__ __launch_bounds__(kGemmBlock, 2) void expert_down_gemm(MoeArgs a, int
 #ifndef LIGHT_D4
 #define LIGHT_D4 4
 #endif
+#ifndef LIGHT_MT16
+#define LIGHT_MT16 2
+#endif
 constexpr int kLightWaves = 8;  // at most, per workgroup (one workgroup per CU)
 constexpr uint32_t kLightOob = 0x80000000u;  // an offset past every buffer here
 // 16-row steps per item (the partial sums of an item fill at most 16 KB of
@@ -486,8 +489,9 @@ __global__ __launch_bounds__(kLightWaves * 64) void expert_light(MoeArgs a, int 
 
 // groups per K-slice: 8, or 16 where 8 would take more than kLightWaves slices
 int light_gs(int K) { return K / kGroup / 8 <= kLightWaves ? 8 : 16; }
-// token blocks per tile the kernels hold: 4 with 8-group slices, 1 with 16
-int light_mtmax_k(int K) { return light_gs(K) == 8 ? 4 : 1; }
+// token blocks per tile the kernels hold: 4 with 8-group slices, 2 with 16
+// (the activations of 16 groups x 2 blocks fill 128 registers)
+int light_mtmax_k(int K) { return light_gs(K) == 8 ? 4 : LIGHT_MT16; }
 
 template <bool DOWN, int GS, int MT>
 hipError_t launch_light_cfg(const MoeArgs& a, int tile_bound, int nk, int nc, hipStream_t s) {
@@ -515,7 +519,11 @@ hipError_t launch_light(const MoeArgs& a, int cls, int tile_bound, hipStream_t s
   const int gs = light_gs(K);
   const int nk = K / (gs * kGroup);
   const int nc = std::max(1, kLightWaves / nk);
-  if (gs == 16) return cls == 2 ? launch_light_cfg<DOWN, 16, 1>(a, tile_bound, nk, nc, s) : hipErrorInvalidValue;
+  if (gs == 16) {
+    if (cls == 2) return launch_light_cfg<DOWN, 16, 1>(a, tile_bound, nk, nc, s);
+    if (cls == 1) return launch_light_cfg<DOWN, 16, 2>(a, tile_bound, nk, nc, s);
+    return hipErrorInvalidValue;
+  }
   if (cls == 0) return launch_light_cfg<DOWN, 8, 4>(a, tile_bound, nk, nc, s);
   if (cls == 1) return launch_light_cfg<DOWN, 8, 2>(a, tile_bound, nk, nc, s);
   return launch_light_cfg<DOWN, 8, 1>(a, tile_bound, nk, nc, s);
