@@ -191,23 +191,6 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t light_rsrc(const void* p, uint
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), 0, (int)bytes, 0x00020000);
 }
 
-// 4 x 4 transpose of words across the four 16-lane rows of the wave: on entry
-// row r holds X[r][0..3] in v[0..3]; on return row r holds X[0..3][r].
-__device__ __forceinline__ void transpose_rows4(uint32_t (&v)[4]) {
-#if defined(__HIP_DEVICE_COMPILE__)
-  // 2 x 2 blocks of rows {0, 1} and {2, 3} trade places (lane halves) ...
-  const auto a = __builtin_amdgcn_permlane32_swap(v[0], v[2], false, false);
-  const auto b = __builtin_amdgcn_permlane32_swap(v[1], v[3], false, false);
-  // ... then each block is transposed between neighbouring rows
-  const auto c = __builtin_amdgcn_permlane16_swap(a[0], b[0], false, false);
-  const auto d = __builtin_amdgcn_permlane16_swap(a[1], b[1], false, false);
-  v[0] = c[0];
-  v[1] = c[1];
-  v[2] = d[0];
-  v[3] = d[1];
-#endif
-}
-
 template <typename T>
 __device__ __forceinline__ T* uniform_ptr(T* p) {
   const uint64_t v = reinterpret_cast<uint64_t>(p);

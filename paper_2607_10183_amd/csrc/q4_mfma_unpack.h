@@ -1,7 +1,9 @@
-// Int4 code words as MFMA operands, shared by the batched-decode kernel and
+// Int4 code words as MFMA operands, shared by the batched-decode kernels and
 // the light-expert kernels: one 32-bit word (8 nibbles of one 8-input chunk)
-// becomes the eight fp16 B-operand values of v_mfma_f32_16x16x32_f16, and
-// eight activations are permuted to the same pair order.
+// becomes the eight fp16 B-operand values of v_mfma_f32_16x16x32_f16, eight
+// activations are permuted to the same pair order, and a 4 x 4 word
+// transpose across a wave's 16-lane rows moves code words loaded row by row
+// into the MFMA operand layout.
 #pragma once
 
 #include "q4_gemv_core.h"
@@ -35,6 +37,23 @@ __device__ __forceinline__ half8_t perm_x(u32x4_t d) {
   const u32x4_t r = {__builtin_amdgcn_perm(d.z, d.x, 0x05040100u), __builtin_amdgcn_perm(d.z, d.x, 0x07060302u),
                      __builtin_amdgcn_perm(d.w, d.y, 0x05040100u), __builtin_amdgcn_perm(d.w, d.y, 0x07060302u)};
   return __builtin_bit_cast(half8_t, r);
+}
+
+// 4 x 4 transpose of words across the four 16-lane rows of the wave: on entry
+// row r holds X[r][0..3] in v[0..3]; on return row r holds X[0..3][r].
+__device__ __forceinline__ void transpose_rows4(uint32_t (&v)[4]) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  // 2 x 2 blocks of rows {0, 1} and {2, 3} trade places (lane halves) ...
+  const auto a = __builtin_amdgcn_permlane32_swap(v[0], v[2], false, false);
+  const auto b = __builtin_amdgcn_permlane32_swap(v[1], v[3], false, false);
+  // ... then each block is transposed between neighbouring rows
+  const auto c = __builtin_amdgcn_permlane16_swap(a[0], b[0], false, false);
+  const auto d = __builtin_amdgcn_permlane16_swap(a[1], b[1], false, false);
+  v[0] = c[0];
+  v[1] = c[1];
+  v[2] = d[0];
+  v[3] = d[1];
+#endif
 }
 
 }  // namespace gemv
