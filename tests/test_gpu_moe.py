@@ -159,6 +159,23 @@ def test_moe_light_experts_parity(sess, light_setup, light, M):
     _check_moe(y, dbg, st, xn, f"moe light={light} M={M}")
 
 
+@pytest.mark.parametrize("H,I", [(256, 1024), (1024, 256), (3072, 512)])
+def test_moe_light_shapes(sess, H, I):
+    """Light tiles of every height on other slice layouts: one K-slice and
+    eight column groups (hidden 256), four slices and two groups (1024), and
+    16-group slices at hidden 3072 (six slices, tiles of at most 32 rows);
+    100 tokens route 400 pairs over 16 experts, so every tile height occurs."""
+    st = _Setup(sess, 86, E=16, H=H, I=I, k=4)
+    xn = synth.activations(86, 7, 100, H)
+    sess.set_moe_light_rows(1 << 20)
+    try:
+        y, dbg = st.layer(_dev(xn), debug=True)
+        sess.sync()
+    finally:
+        sess.set_moe_light_rows(-1)
+    _check_moe(y, dbg, st, xn, f"moe light H={H} I={I}")
+
+
 def test_moe_light_rows_range(sess):
     from paper_2607_10183_amd import atsi
     for bad in (-2, (1 << 20) + 1):
