@@ -254,6 +254,24 @@ def bench_dense_layer(args, sess, timer, pcie_gbs=None):
                        "kernel": "q4_gemv1_kernel<7,true,4>: SwiGLU gate/up, two 4096x14336 tensors, batch 1",
                        "bytes_per_launch": gemv_bytes, "avg_us": round(t_gemv * 1e6, 3),
                        "launch_us": stats_us(kern[("gate_up", 1)])}
+    if not args.roofline_only:
+        # the measured read ceiling: the library's read-only streaming probe
+        # over the same bytes per launch (R distinct buffers, rotated as the
+        # weights are), and one pass over 1 GiB
+        bufs = [torch.empty(gemv_bytes, dtype=torch.uint8, device=dev) for _ in range(R)]
+        t_probe = float(np.mean(time_launch(
+            lambda c: atsi.atsi_debug_read_probe(sess.ctx, bufs[c].data_ptr(), gemv_bytes), 100, 8)))
+        big = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        t_big = float(np.mean(timer.samples(lambda: atsi.atsi_debug_read_probe(sess.ctx, big.data_ptr(), 1 << 30), 10)))
+        del bufs, big
+        probe_gbs = gemv_bytes / t_probe / 1e9
+        out["roofline"]["measured_ceiling"] = {
+            "kernel": "read_probe_kernel<4>: read-only non-temporal 16-B buffer loads, same bytes per launch",
+            "GBps": round(probe_gbs, 1), "GBps_1GiB": round((1 << 30) / t_big / 1e9, 1),
+            "frac_of_ceiling": round(gemv_bytes / t_gemv / 1e9 / probe_gbs, 4)}
+        log(f"read probe {t_probe * 1e6:.2f} us -> {probe_gbs:.0f} GB/s over {gemv_bytes} B "
+            f"({(1 << 30) / t_big / 1e9:.0f} GB/s over 1 GiB); the gate/up GEMV reaches "
+            f"{gemv_bytes / t_gemv / 1e9 / probe_gbs:.0%} of it")
     out["roofline_prefill"] = {"bound": "mfma", "achieved": round(gemm_flops / t_gemm / 1e12, 1),
                                "peak": MFMA_F16_PEAK_TFLOPS, "unit": "TFLOP/s",
                                "frac": round(gemm_flops / t_gemm / 1e12 / MFMA_F16_PEAK_TFLOPS, 4),

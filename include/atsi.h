@@ -551,6 +551,15 @@ atsi_status atsi_debug_cpu_f16(const float* in, int64_t n, uint16_t* out, float*
  * the library reads them, from wherever w currently lives. */
 atsi_status atsi_debug_unpack(atsi_ctx* ctx, atsi_tid w, int8_t* q_out);
 
+/* Measurement export: one read-only pass over `bytes` of device memory at
+ * dev (16-byte aligned, a positive multiple of 16, below 2 GiB), enqueued on
+ * the compute stream: non-temporal 16-byte buffer loads, four per thread in
+ * flight, workgroups reading contiguous 16 KiB rounds, eight workgroups per
+ * CU.  The read ceiling the batch-1 GEMV is compared to (HBM streaming, Sec.
+ * 2.2's memory-bound decode); the data is not changed and nothing the caller
+ * sees is written.  ATSI_E_INVALID for a bad buffer. */
+atsi_status atsi_debug_read_probe(atsi_ctx* ctx, const void* dev, size_t bytes);
+
 #ifdef __cplusplus
 }
 #endif

@@ -135,6 +135,7 @@ _SIGS = {
     "atsi_set_timing": ([_P, ctypes.c_int32], ctypes.c_int),
     "atsi_get_timings": ([_P, ctypes.c_int32, ctypes.POINTER(atsi_tensor_timing)], ctypes.c_int),
     "atsi_debug_cpu_f16": ([_P, ctypes.c_int64, _P, _P], ctypes.c_int),
+    "atsi_debug_read_probe": ([_P, _P, ctypes.c_size_t], ctypes.c_int),
 }
 
 _lib = None
@@ -384,3 +385,8 @@ def atsi_debug_cpu_f16(values):
     back = (ctypes.c_float * max(1, n))()
     _check(None, lib().atsi_debug_cpu_f16(ctypes.cast(src, _P), n, ctypes.cast(out, _P), ctypes.cast(back, _P)))
     return [int(out[i]) for i in range(n)], [back[i] for i in range(n)]
+
+
+def atsi_debug_read_probe(ctx: int, dev_ptr: int, nbytes: int) -> None:
+    """One read-only streaming pass over device memory (HBM read ceiling)."""
+    _check(ctx, lib().atsi_debug_read_probe(ctx, dev_ptr, nbytes))

@@ -1933,6 +1933,18 @@ atsi_status atsi_get_timings(atsi_ctx* c, int32_t n, atsi_tensor_timing* out) {
   return ATSI_OK;
 }
 
+atsi_status atsi_debug_read_probe(atsi_ctx* c, const void* dev, size_t bytes) {
+  if (!c) return ATSI_E_INVALID;
+  if (!dev || bytes == 0 || bytes % 16 || (uintptr_t)dev % 16 || bytes >= ((size_t)1 << 31))
+    return fail(c, ATSI_E_INVALID,
+                "the probe needs a 16-byte aligned device buffer of a positive multiple of 16 bytes below 2 GiB");
+  atsi_status st = enter(c);
+  if (st) return st;
+  hipError_t e = launch_read_probe(dev, bytes, c->layer_bar + kProbeSinkWord, c->cs);
+  if (e != hipSuccess) return hip_fail(c, e, "read probe launch");
+  return ATSI_OK;
+}
+
 atsi_status atsi_debug_unpack(atsi_ctx* c, atsi_tid w, int8_t* q_out) {
   if (!c) return ATSI_E_INVALID;
   if (!q_out) return fail(c, ATSI_E_INVALID, "q_out is NULL");

@@ -106,6 +106,8 @@ int gemm_wide_splits(const LinOp& op);
 size_t gemm_wide_part_bytes(const LinOp& op, int splits);
 hipError_t launch_gemm_wide(const LinOp& op, int splits, float* part, hipStream_t s);
 hipError_t launch_unpack(const QView& w, int8_t* q, hipStream_t s);
+// read-only streaming probe over bytes (16-byte aligned, a multiple of 16)
+hipError_t launch_read_probe(const void* p, size_t bytes, unsigned* sink, hipStream_t s);
 
 // single-tensor helpers
 inline LinOp plain_op(const QView& w, const __half* x, int M, __half* y) {

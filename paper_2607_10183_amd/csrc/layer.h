@@ -13,6 +13,9 @@ enum LayerTensor { kQ = 0, kK, kV, kO, kGate, kUp, kDown, kLayerTensors };
 // flag, which stays set after a barrier that timed out)
 constexpr size_t kLayerBarrierWords = 352;
 constexpr int kLayerBarrierErrWord = 8 * 32 + 64;
+// a word of the same block the read probe may write (never read)
+constexpr int kProbeSinkWord = kLayerBarrierErrWord + 16;
+static_assert(kProbeSinkWord < (int)kLayerBarrierWords, "probe sink inside the block");
 
 struct LayerArgs {
   QView w[kLayerTensors];

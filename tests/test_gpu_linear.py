@@ -155,3 +155,19 @@ def test_placement_invariance(sess, M):
     assert st["host_reads"] == 3 and st["host_read_bytes"] == 3 * (codes.nbytes + scales.nbytes)
     for yh in y_host:
         assert torch.equal(y_hbm, yh)
+
+
+def test_read_probe_leaves_memory_and_checks_arguments(sess):
+    """The measurement probe reads device memory without changing it, and
+    refuses misaligned or ragged buffers."""
+    import torch
+    from paper_2607_10183_amd import atsi
+    buf = torch.randint(0, 256, (1 << 20,), dtype=torch.uint8, device="cuda")
+    before = buf.clone()
+    atsi.atsi_debug_read_probe(sess.ctx, buf.data_ptr(), buf.numel())
+    atsi.atsi_debug_read_probe(sess.ctx, buf.data_ptr(), 4096 + 16)  # a ragged tail of chunks
+    sess.sync()
+    assert torch.equal(buf, before)
+    for ptr, n in ((buf.data_ptr() + 8, 4096), (buf.data_ptr(), 100), (buf.data_ptr(), 0), (0, 4096)):
+        with pytest.raises(atsi.AtsiError, match="ATSI_E_INVALID"):
+            atsi.atsi_debug_read_probe(sess.ctx, ptr, n)
