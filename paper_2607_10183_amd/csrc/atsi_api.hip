@@ -1245,7 +1245,8 @@ atsi_status run_moe(atsi_ctx* c, const atsi_moe* m, const __half* x, int Mi, __h
   // HBM-resident experts first: they run while the host learns which
   // streamed experts are needed.  Grid bounds: tiles of bm rows over experts
   // routed more than `light` pairs, and light tiles over the others.
-  const int bound = bm == 1 ? Mk : Mk / bm + std::min(E, Mk / (light + 1));
+  const int heavy = std::min(E, Mk / (light + 1));  // experts that can be routed more than `light` pairs
+  const int bound = bm == 1 ? Mk : (heavy > 0 ? Mk / bm + heavy : 0);
   const int lbound = light ? std::min(Mk / kLightTileRows + E, E * ((light + kLightTileRows - 1) / kLightTileRows)) : 0;
   MoeArgs al = a;
   al.tiles = ltiles;

@@ -210,6 +210,82 @@ __device__ __forceinline__ T ld_global(const T* p) {
 #endif
 }
 
+// Wave-uniform loads through the scalar data cache, for the tables an earlier
+// launch wrote (that cache is invalidated when a launch starts).  Their wait
+// counts against the scalar/LDS counter, so it leaves the vector loads in
+// flight: waiting for a vector load here would wait for every weight load
+// issued before it.  Addresses are wave-uniform and 4-byte aligned.
+typedef int sint2_t __attribute__((ext_vector_type(2)));
+typedef int sint4_t __attribute__((ext_vector_type(4)));
+
+// Three consecutive ints in one round of loads.
+__device__ __forceinline__ sint4_t s_ld3(const int32_t* p) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  sint2_t v;
+  int w;
+  asm volatile("s_load_dwordx2 %0, %2, 0x0\n\ts_load_dword %1, %2, 0x8\n\ts_waitcnt lgkmcnt(0)"
+               : "=&s"(v), "=&s"(w)
+               : "s"(p)
+               : "memory");
+  return sint4_t{v.x, v.y, w, 0};
+#else
+  return sint4_t{p[0], p[1], p[2], 0};
+#endif
+}
+
+__device__ __forceinline__ sint2_t s_ld2(const int32_t* p) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  sint2_t v;
+  asm volatile("s_load_dwordx2 %0, %1, 0x0\n\ts_waitcnt lgkmcnt(0)" : "=&s"(v) : "s"(p) : "memory");
+  return v;
+#else
+  return sint2_t{p[0], p[1]};
+#endif
+}
+
+// One int from each of two tables, in one round of loads.
+__device__ __forceinline__ sint2_t s_ld2_pair(const int32_t* pa, const int32_t* pb) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  int va, vb;
+  asm volatile("s_load_dword %0, %2, 0x0\n\ts_load_dword %1, %3, 0x0\n\ts_waitcnt lgkmcnt(0)"
+               : "=&s"(va), "=&s"(vb)
+               : "s"(pa), "s"(pb)
+               : "memory");
+  return sint2_t{va, vb};
+#else
+  return sint2_t{*pa, *pb};
+#endif
+}
+
+// The code and scale pointers of two QViews of one ExpertW (byte offsets O0
+// and O1), and one int from each of two tables, in one round of loads.
+template <int O0, int O1>
+__device__ __forceinline__ void s_ld_item(const ExpertW* w, const int32_t* pa, const int32_t* pb, sint4_t& q0,
+                                          sint4_t& q1, int& va, int& vb) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  asm volatile(
+      "s_load_dwordx4 %0, %4, %7\n\t"
+      "s_load_dwordx4 %1, %4, %8\n\t"
+      "s_load_dword %2, %5, 0x0\n\t"
+      "s_load_dword %3, %6, 0x0\n\t"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&s"(q0), "=&s"(q1), "=&s"(va), "=&s"(vb)
+      : "s"(w), "s"(pa), "s"(pb), "i"(O0), "i"(O1)
+      : "memory");
+#else
+  const char* b = reinterpret_cast<const char*>(w);
+  q0 = *reinterpret_cast<const sint4_t*>(b + O0);
+  q1 = *reinterpret_cast<const sint4_t*>(b + O1);
+  va = *pa;
+  vb = *pb;
+#endif
+}
+
+template <typename T>
+__device__ __forceinline__ T* ptr_of(int lo, int hi) {
+  return reinterpret_cast<T*>((uint64_t)(uint32_t)lo | ((uint64_t)(uint32_t)hi << 32));
+}
+
 // Eight weights w = RNE16(s * q) from one code word, in the pair order of
 // unpack_q (q exact, then one rounding of the product).
 __device__ __forceinline__ gemv::half8_t dequant_word(uint32_t w, gemv::half2_t s2, const gemv::UnpackMasks& k) {
@@ -240,28 +316,40 @@ __device__ __forceinline__ LightItem light_item(const MoeArgs& a, int t0, int i,
   }
   it.tix = i / ncb;
   it.cb = i % ncb;
-  int e, row0;
-  ExpertW w;
+  // scalar loads only: the ring's weight loads stay in flight meanwhile
+  constexpr int O0 = DOWN ? (int)offsetof(ExpertW, down) : (int)offsetof(ExpertW, gate);
+  constexpr int O1 = DOWN ? (int)offsetof(ExpertW, down) : (int)offsetof(ExpertW, up);
+  static_assert(offsetof(QView, codes) == 0 && offsetof(QView, scales) == 8, "QView pointer layout");
+  int e, row0, off, cnt;
   if (a.nb > 0) {
+    // the batch's weights sit in the launch arguments
     const int2 t = a.btiles[it.tix];
     e = a.bexp[t.x];
     row0 = t.y;
-    w = a.bw[t.x];
+    const ExpertW& w = a.bw[t.x];
+    const QView& w0 = DOWN ? w.down : w.gate;
+    const QView& w1 = DOWN ? w.down : w.up;
+    it.c0 = uniform_ptr(w0.codes);
+    it.s0 = uniform_ptr(w0.scales);
+    it.c1 = uniform_ptr(w1.codes);
+    it.s1 = uniform_ptr(w1.scales);
+    const sint2_t oc = s_ld2_pair(uniform_ptr(a.offsets + e), uniform_ptr(a.counts + e));
+    off = oc.x;
+    cnt = oc.y;
   } else {
-    e = ld_global(a.tiles + 2 * (t0 + it.tix));
-    row0 = ld_global(a.tiles + 2 * (t0 + it.tix) + 1);
-    w = ld_global(a.table + e);
+    const sint2_t t = s_ld2(uniform_ptr(a.tiles + 2 * (t0 + it.tix)));
+    e = t.x;
+    row0 = t.y;
+    sint4_t q0, q1;
+    s_ld_item<O0, O1>(uniform_ptr(a.table + e), uniform_ptr(a.offsets + e), uniform_ptr(a.counts + e), q0, q1, off,
+                      cnt);
+    it.c0 = ptr_of<const uint8_t>(q0.x, q0.y);
+    it.s0 = ptr_of<const uint16_t>(q0.z, q0.w);
+    it.c1 = ptr_of<const uint8_t>(q1.x, q1.y);
+    it.s1 = ptr_of<const uint16_t>(q1.z, q1.w);
   }
-  e = __builtin_amdgcn_readfirstlane(e);
-  row0 = __builtin_amdgcn_readfirstlane(row0);
-  it.base = __builtin_amdgcn_readfirstlane(ld_global(a.offsets + e)) + row0;
-  it.rows = min(kLightTileRows * MT, __builtin_amdgcn_readfirstlane(ld_global(a.counts + e)) - row0);
-  const QView& w0 = DOWN ? w.down : w.gate;
-  const QView& w1 = DOWN ? w.down : w.up;
-  it.c0 = uniform_ptr(w0.codes);
-  it.s0 = uniform_ptr(w0.scales);
-  it.c1 = DOWN ? it.c0 : uniform_ptr(w1.codes);
-  it.s1 = DOWN ? it.s0 : uniform_ptr(w1.scales);
+  it.base = off + row0;
+  it.rows = min(kLightTileRows * MT, cnt - row0);
   return it;
 }
 
@@ -278,8 +366,10 @@ __global__ __launch_bounds__(kLightWaves * 64) void expert_light(MoeArgs a, int 
   const int cls = light_class(MT);
   int t0 = 0, ntiles = a.nb;
   if (a.nb == 0) {
-    for (int q = 0; q < cls; ++q) t0 += __builtin_amdgcn_readfirstlane(ld_global(a.n_tiles + q));
-    ntiles = __builtin_amdgcn_readfirstlane(ld_global(a.n_tiles + cls));
+    static_assert(kLightClasses == 3, "one round of loads reads the three class counts");
+    const sint4_t nt = s_ld3(uniform_ptr(a.n_tiles));
+    t0 = (cls > 0 ? nt.x : 0) + (cls > 1 ? nt.y : 0);
+    ntiles = cls == 0 ? nt.x : (cls == 1 ? nt.y : nt.z);
   }
   const int total = ntiles * ncb;
   const int per = (total + (int)gridDim.x - 1) / (int)gridDim.x;
@@ -330,7 +420,7 @@ __global__ __launch_bounds__(kLightWaves * 64) void expert_light(MoeArgs a, int 
       prs[t] = DOWN ? 0 : ld_global(a.perm + it.base + (m < it.rows ? m : 0));
     }
   };
-  auto load_rows = [&](const LightItem& it) {
+  auto load_x = [&](const LightItem& it) {
 #pragma unroll
     for (int t = 0; t < MT; ++t) {
       const int m = kLightTileRows * t + n;
@@ -345,23 +435,50 @@ __global__ __launch_bounds__(kLightWaves * 64) void expert_light(MoeArgs a, int 
         xa[t][g] = perm_x(v);
       }
     }
-    if (threadIdx.x < (unsigned)it.rows) {
+  };
+  // output row and RMS factor of tile row m = threadIdx.x, loaded into
+  // registers when a tile starts and stored to LDS at the end of each item's
+  // steps, so that their wait comes after the ring's loads of that item
+  int rdst = 0;
+  float rsc = 1.f;
+  auto row_info = [&](const LightItem& it) {
+    if (threadIdx.x < (unsigned)RT) {
       const int m = threadIdx.x;
-      const int p = ld_global(a.perm + it.base + m);
-      row_dst[m] = DOWN ? p : it.base + m;
-      row_scale[m] = (!DOWN && a.inv_r) ? ld_global(a.inv_r + p / a.k) : 1.f;
+      if constexpr (DOWN) {
+        rdst = ld_global(a.perm + it.base + (m < it.rows ? m : 0));
+      } else {
+        int p = prs[0];
+#pragma unroll
+        for (int t = 1; t < MT; ++t)
+          if ((m >> 4) == t) p = prs[t];
+        rdst = it.base + m;
+        rsc = a.inv_r ? ld_global(a.inv_r + p / a.k) : 1.f;
+      }
     }
   };
+  // the next item: the same tile's metadata with another column block, or a
+  // new tile's
+  auto next_item = [&](const LightItem& p, int i) {
+    if (i < i1 && i / ncb == p.tix) {
+      LightItem it = p;
+      it.cb = i % ncb;
+      return it;
+    }
+    return light_item<DOWN, MT>(a, t0, i, i1, ncb);
+  };
 
+  // the tile's activations go out before the ring's weight loads, so that
+  // the first step's wait for them leaves those in flight
   LightItem cur = light_item<DOWN, MT>(a, t0, i0, i1, ncb);
-  LightItem nxt = light_item<DOWN, MT>(a, t0, i0 + 1, i1, ncb);
   pairs_of(cur);
+  load_x(cur);
   __builtin_amdgcn_sched_barrier(0);
   Ld buf[D];
 #pragma unroll
   for (int d = 0; d < D; ++d) load(buf[d], cur, d);
   __builtin_amdgcn_sched_barrier(0);
-  load_rows(cur);
+  row_info(cur);
+  LightItem nxt = next_item(cur, i0 + 1);
 
   const UnpackMasks um = unpack_masks();
   const lf4_t zero = {0.f, 0.f, 0.f, 0.f};
@@ -430,6 +547,10 @@ __global__ __launch_bounds__(kLightWaves * 64) void expert_light(MoeArgs a, int 
 #pragma unroll
       for (int t = 0; t < MT; ++t) mine[(st * MT + t) * 64] = acc[t];
     }
+    if (threadIdx.x < (unsigned)RT) {
+      row_dst[threadIdx.x] = rdst;
+      row_scale[threadIdx.x] = rsc;
+    }
     __syncthreads();
 
     // slices summed in order; D[m][n] of a token block sits in lane
@@ -462,10 +583,11 @@ __global__ __launch_bounds__(kLightWaves * 64) void expert_light(MoeArgs a, int 
     if (i + 1 < i1) {
       if (nxt.tix != cur.tix) {
         pairs_of(nxt);
-        load_rows(nxt);
+        load_x(nxt);
+        row_info(nxt);
       }
       cur = nxt;
-      nxt = light_item<DOWN, MT>(a, t0, i + 2, i1, ncb);
+      nxt = next_item(cur, i + 2);
     }
   }
 }
