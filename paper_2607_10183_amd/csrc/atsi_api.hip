@@ -1252,12 +1252,9 @@ atsi_status run_moe(atsi_ctx* c, const atsi_moe* m, const __half* x, int Mi, __h
   al.tiles = ltiles;
   al.n_tiles = nltiles;
   if ((e = launch_expert_gateup(a, bound, gemv, c->cs)) != hipSuccess) return hip_fail(c, e, "expert gate/up launch");
-  // one launch per light tile height the shape allows (the kernels of
-  // classes with no tiles exit at once)
-  const int cls0 = lmt ? light_class(lmt) : kLightClasses;
-  for (int q = cls0; q < kLightClasses; ++q)
-    if ((e = launch_light_gateup(al, q, lbound, c->cs)) != hipSuccess)
-      return hip_fail(c, e, "light expert gate/up launch");
+  // one launch for every light tile height the shape allows
+  if (lmt && (e = launch_light_all_gateup(al, lmt, lbound, c->cs)) != hipSuccess)
+    return hip_fail(c, e, "light expert gate/up launch");
   if (by_pair) {  // every expert resident: the down launch also combines
     a.store_out = dbg && dbg->expert_out;
     if ((e = launch_expert_down_combine(a, Mi, p, res, y, c->cs)) != hipSuccess)
@@ -1265,8 +1262,8 @@ atsi_status run_moe(atsi_ctx* c, const atsi_moe* m, const __half* x, int Mi, __h
     return gather_expert_h(c, dbg, h, nullptr, Mk, I);
   }
   if ((e = launch_expert_down(a, bound, gemv, c->cs)) != hipSuccess) return hip_fail(c, e, "expert down launch");
-  for (int q = cls0; q < kLightClasses; ++q)
-    if ((e = launch_light_down(al, q, lbound, c->cs)) != hipSuccess) return hip_fail(c, e, "light expert down launch");
+  if (lmt && (e = launch_light_all_down(al, lmt, lbound, c->cs)) != hipSuccess)
+    return hip_fail(c, e, "light expert down launch");
 
   if (tb->n_streamed > 0) {
     HIP_TRY(c, hipEventSynchronize(c->counts_ev));

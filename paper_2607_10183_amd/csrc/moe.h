@@ -98,6 +98,10 @@ bool light_supported(int H, int I);
 int light_mtmax(int H, int I);
 hipError_t launch_light_gateup(const MoeArgs& a, int cls, int tile_bound, hipStream_t s);
 hipError_t launch_light_down(const MoeArgs& a, int cls, int tile_bound, hipStream_t s);
+// Every light tile height up to 16 mtmax rows in one launch (resident tile
+// list only; mtmax 1 is the one class of 16-row tiles).
+hipError_t launch_light_all_gateup(const MoeArgs& a, int mtmax, int tile_bound, hipStream_t s);
+hipError_t launch_light_all_down(const MoeArgs& a, int mtmax, int tile_bound, hipStream_t s);
 // pair-indexed decode (a.pair_expert set): the down projections of all k
 // experts of each of the M tokens and the combine, in one launch; the same
 // results as launch_expert_down followed by launch_combine

@@ -353,28 +353,15 @@ __device__ __forceinline__ LightItem light_item(const MoeArgs& a, int t0, int i,
   return it;
 }
 
+// Items i0 .. i1 - 1 of the tiles of height 16 MT listed from t0 (wave
+// uniform), with red the partial-sum LDS ([wave][step][token block][lane])
+// and row_dst / row_scale 16 MT entries of LDS each.
 template <bool DOWN, int GS, int MT>
-__global__ __launch_bounds__(kLightWaves * 64) void expert_light(MoeArgs a, int nk, int nc, int ncb) {
+__device__ __forceinline__ void light_run(const MoeArgs& a, int t0, int i0, int i1, int ncb, int nk, int nc,
+                                          lf4_t* red, int* row_dst, float* row_scale) {
   using namespace gemv;
   constexpr int S = light_steps(MT), D = light_d(GS, MT), RT = kLightTileRows * MT;
   static_assert(S % D == 0, "the ring restarts at every item");
-  extern __shared__ __attribute__((aligned(16))) char smem[];
-  lf4_t* red = reinterpret_cast<lf4_t*>(smem);  // [wave][step][token block][lane]
-  __shared__ int row_dst[RT];                   // output row of tile row m (pair id / bucket row)
-  __shared__ float row_scale[RT];               // gate/up: the token's RMS factor
-  // this class's tiles: the light list's range for MT, or the whole batch
-  const int cls = light_class(MT);
-  int t0 = 0, ntiles = a.nb;
-  if (a.nb == 0) {
-    static_assert(kLightClasses == 3, "one round of loads reads the three class counts");
-    const sint4_t nt = s_ld3(uniform_ptr(a.n_tiles));
-    t0 = (cls > 0 ? nt.x : 0) + (cls > 1 ? nt.y : 0);
-    ntiles = cls == 0 ? nt.x : (cls == 1 ? nt.y : nt.z);
-  }
-  const int total = ntiles * ncb;
-  const int per = (total + (int)gridDim.x - 1) / (int)gridDim.x;
-  const int i0 = (int)blockIdx.x * per, i1 = min(i0 + per, total);
-  if (i0 >= i1) return;
   const int K = DOWN ? a.I : a.H, N = DOWN ? a.H : a.I, G = K / kGroup;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
@@ -592,6 +579,93 @@ __global__ __launch_bounds__(kLightWaves * 64) void expert_light(MoeArgs a, int 
   }
 }
 
+// One tile height per launch: the batch's tiles, or one class of the light list.
+template <bool DOWN, int GS, int MT>
+__global__ __launch_bounds__(kLightWaves * 64) void expert_light(MoeArgs a, int nk, int nc, int ncb) {
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  __shared__ int row_dst[kLightTileRows * MT];    // output row of tile row m (pair id / bucket row)
+  __shared__ float row_scale[kLightTileRows * MT];  // gate/up: the token's RMS factor
+  const int cls = light_class(MT);
+  int t0 = 0, ntiles = a.nb;
+  if (a.nb == 0) {
+    static_assert(kLightClasses == 3, "one round of loads reads the three class counts");
+    const sint4_t nt = s_ld3(uniform_ptr(a.n_tiles));
+    t0 = (cls > 0 ? nt.x : 0) + (cls > 1 ? nt.y : 0);
+    ntiles = cls == 0 ? nt.x : (cls == 1 ? nt.y : nt.z);
+  }
+  const int total = ntiles * ncb;
+  const int per = (total + (int)gridDim.x - 1) / (int)gridDim.x;
+  const int i0 = (int)blockIdx.x * per, i1 = min(i0 + per, total);
+  if (i0 >= i1) return;
+  light_run<DOWN, GS, MT>(a, t0, i0, i1, ncb, nk, nc, reinterpret_cast<lf4_t*>(smem), row_dst, row_scale);
+}
+
+// Relative cost of one item of each tile height (light_steps 16-row steps,
+// 1, 2 or 4 token blocks), from per-item times measured on MI355X with one
+// workgroup per CU (30B-shaped layer, 512 and 2048 tokens): about 7.75 us for
+// 16-row items, 9 us for 32-row items and 6 us for 64-row items (half the
+// steps).
+__host__ __device__ constexpr int light_item_cost(int mt) { return mt == 4 ? 24 : (mt == 2 ? 36 : 31); }
+__host__ __device__ inline int light_ncb(int N, int mt, int nc, bool down) {
+  const int outs = (down ? 16 : 8) * light_steps(mt) * nc;
+  return (N + outs - 1) / outs;
+}
+
+// Every tile height of the light list in one launch (classes MTMAX and
+// below): the grid is shared among the classes in proportion to their items'
+// cost, and each workgroup runs a contiguous range of one class's items, so
+// the classes' start-up and tails overlap instead of following each other.
+template <bool DOWN, int GS, int MTMAX>
+__global__ __launch_bounds__(kLightWaves * 64) void expert_light_all(MoeArgs a, int nk, int nc) {
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  __shared__ int row_dst[kLightTileRows * MTMAX];
+  __shared__ float row_scale[kLightTileRows * MTMAX];
+  static_assert(kLightClasses == 3, "one round of loads reads the three class counts");
+  const sint4_t nt = s_ld3(uniform_ptr(a.n_tiles));
+  const int N = DOWN ? a.H : a.I, grid = (int)gridDim.x;
+  const int cls0 = light_class(MTMAX);
+  // items and cost per class (0: 64-row tiles, 1: 32, 2: 16), all uniform
+  const int n0 = cls0 <= 0 ? nt.x * light_ncb(N, 4, nc, DOWN) : 0;
+  const int n1 = cls0 <= 1 ? nt.y * light_ncb(N, 2, nc, DOWN) : 0;
+  const int n2 = nt.z * light_ncb(N, 1, nc, DOWN);
+  constexpr int w0 = light_item_cost(4), w1 = light_item_cost(2), w2 = light_item_cost(1);
+  const long long tot = (long long)n0 * w0 + (long long)n1 * w1 + (long long)n2 * w2;
+  if (tot == 0) return;
+  // workgroups per class: the proportional share rounded down (at least one
+  // for a class with items), then the rest one by one to the class whose
+  // workgroups carry the most
+  auto share = [&](int n, int w) { return n ? max(1, (int)((long long)grid * n * w / tot)) : 0; };
+  int g0 = share(n0, w0), g1 = share(n1, w1), g2 = share(n2, w2);
+  auto load_of = [](int n, int g, int w) { return g ? (n + g - 1) / g * w : 0; };
+  while (g0 + g1 + g2 > grid) {  // only where the grid is smaller than the classes need
+    if (g0 > 1 && g0 >= g1 && g0 >= g2) --g0;
+    else if (g1 > 1 && g1 >= g2) --g1;
+    else if (g2 > 1) --g2;
+    else break;
+  }
+  while (g0 + g1 + g2 < grid) {
+    const int l0 = load_of(n0, g0, w0), l1 = load_of(n1, g1, w1), l2 = load_of(n2, g2, w2);
+    if (l0 >= l1 && l0 >= l2) ++g0;
+    else if (l1 >= l2) ++g1;
+    else ++g2;
+  }
+  const int b = (int)blockIdx.x;
+  const int c = b < g0 ? 0 : (b < g0 + g1 ? 1 : 2);
+  const int lb = b - (c == 0 ? 0 : (c == 1 ? g0 : g0 + g1));
+  const int nc_items = c == 0 ? n0 : (c == 1 ? n1 : n2), gc = c == 0 ? g0 : (c == 1 ? g1 : g2);
+  if (lb >= gc) return;
+  const int per = (nc_items + gc - 1) / gc;
+  const int i0 = __builtin_amdgcn_readfirstlane(lb * per);
+  const int i1 = __builtin_amdgcn_readfirstlane(min(lb * per + per, nc_items));
+  if (i0 >= i1) return;
+  const int t0 = __builtin_amdgcn_readfirstlane((c > 0 ? nt.x : 0) + (c > 1 ? nt.y : 0));
+  lf4_t* red = reinterpret_cast<lf4_t*>(smem);
+  if constexpr (MTMAX >= 4)
+    if (c == 0) return light_run<DOWN, GS, 4>(a, t0, i0, i1, light_ncb(N, 4, nc, DOWN), nk, nc, red, row_dst, row_scale);
+  if (c == 1) return light_run<DOWN, GS, 2>(a, t0, i0, i1, light_ncb(N, 2, nc, DOWN), nk, nc, red, row_dst, row_scale);
+  light_run<DOWN, GS, 1>(a, t0, i0, i1, light_ncb(N, 1, nc, DOWN), nk, nc, red, row_dst, row_scale);
+}
+
 // groups per K-slice: 8, or 16 where 8 would take more than kLightWaves slices
 int light_gs(int K) { return K / kGroup / 8 <= kLightWaves ? 8 : 16; }
 // token blocks per tile the kernels hold: 4 with 8-group slices, 2 with 16
@@ -632,6 +706,39 @@ hipError_t launch_light(const MoeArgs& a, int cls, int tile_bound, hipStream_t s
   if (cls == 0) return launch_light_cfg<DOWN, 8, 4>(a, tile_bound, nk, nc, s);
   if (cls == 1) return launch_light_cfg<DOWN, 8, 2>(a, tile_bound, nk, nc, s);
   return launch_light_cfg<DOWN, 8, 1>(a, tile_bound, nk, nc, s);
+}
+
+template <bool DOWN, int GS, int MTMAX>
+hipError_t launch_light_all_cfg(const MoeArgs& a, int tile_bound, int nk, int nc, hipStream_t s) {
+  const int N = DOWN ? a.H : a.I;
+  size_t lds = 0;
+  for (int mt = 1; mt <= MTMAX; mt *= 2)
+    lds = std::max(lds, (size_t)nk * nc * light_steps(mt) * mt * 64 * sizeof(lf4_t));
+  if (lds + 2 * kLightTileRows * MTMAX * 4 > lds_limit()) return hipErrorInvalidValue;
+  int cus = 256;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) !=
+                                               hipSuccess || cus < 1)
+    cus = 256;
+  // at least one workgroup per class; 64-row items are the most per tile
+  const int grid = std::max(kLightClasses, std::min(tile_bound * light_ncb(N, MTMAX, nc, DOWN), cus));
+  hipLaunchKernelGGL((expert_light_all<DOWN, GS, MTMAX>), dim3(grid), dim3(nk * nc * 64), lds, s, a, nk, nc);
+  return hipGetLastError();
+}
+
+template <bool DOWN>
+hipError_t launch_light_all(const MoeArgs& a, int mtmax, int tile_bound, hipStream_t s) {
+  if (tile_bound <= 0) return hipSuccess;
+  if (mtmax == 1) return launch_light<DOWN>(a, light_class(1), tile_bound, s);
+  if (!light_supported(a.H, a.I) || a.nb != 0 || (mtmax != 2 && mtmax != 4)) return hipErrorInvalidValue;
+  const int K = DOWN ? a.I : a.H;
+  const int gs = light_gs(K);
+  if (mtmax > light_mtmax_k(K)) return hipErrorInvalidValue;
+  const int nk = K / (gs * kGroup);
+  const int nc = std::max(1, kLightWaves / nk);
+  if (gs == 16) return launch_light_all_cfg<DOWN, 16, 2>(a, tile_bound, nk, nc, s);
+  if (mtmax == 4) return launch_light_all_cfg<DOWN, 8, 4>(a, tile_bound, nk, nc, s);
+  return launch_light_all_cfg<DOWN, 8, 2>(a, tile_bound, nk, nc, s);
 }
 
 // ---------------------------------------------------------------- GEMV path (one row per tile)
@@ -883,6 +990,14 @@ hipError_t launch_light_gateup(const MoeArgs& a, int cls, int tile_bound, hipStr
 
 hipError_t launch_light_down(const MoeArgs& a, int cls, int tile_bound, hipStream_t s) {
   return launch_light<true>(a, cls, tile_bound, s);
+}
+
+hipError_t launch_light_all_gateup(const MoeArgs& a, int mtmax, int tile_bound, hipStream_t s) {
+  return launch_light_all<false>(a, mtmax, tile_bound, s);
+}
+
+hipError_t launch_light_all_down(const MoeArgs& a, int mtmax, int tile_bound, hipStream_t s) {
+  return launch_light_all<true>(a, mtmax, tile_bound, s);
 }
 
 hipError_t launch_expert_down_combine(const MoeArgs& a, int M, const float* p, const __half* res, __half* y,
