@@ -504,6 +504,10 @@ __device__ int scan128(const int* v, int* out, int E) {
 // Single workgroup of 1024 threads.  Up to 16 chunks of 64 tokens are ranked
 // per pass; masks live in LDS.
 constexpr int kBucketThreads = 1024;
+// up to this many routed pairs the scatter writes perm into LDS and copies it
+// out in order (64 KB): scattered 4-byte stores from the one workgroup took
+// most of the kernel's time
+constexpr int kBucketStage = 16384;
 __global__ __launch_bounds__(kBucketThreads) void bucket_kernel(const int32_t* __restrict__ idx, int M, int k, int E,
                                                       const uint8_t* __restrict__ resident, int bm_rows,
                                                       int light_rows, int light_mtmax, int32_t* __restrict__ counts,
@@ -522,8 +526,12 @@ __global__ __launch_bounds__(kBucketThreads) void bucket_kernel(const int32_t* _
   __shared__ int lstart[kMaxExperts];
   __shared__ int lclass[kLightClasses];
   __shared__ int rpart[8][kMaxExperts];
+  extern __shared__ int sperm[];  // perm, staged (pairs <= kBucketStage)
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int pairs = M * k;
+  const bool stage = pairs <= kBucketStage;
+  // inv_perm rows of four pairs go out as one 16-byte store where aligned
+  const bool inv4 = (k & 3) == 0 && (reinterpret_cast<uintptr_t>(inv_perm) & 15) == 0;
   for (int e = tid; e < E; e += blockDim.x) cnt[e] = 0;
   __syncthreads();
   // every load of a round of 8 is issued before its first count
@@ -569,16 +577,44 @@ __global__ __launch_bounds__(kBucketThreads) void bucket_kernel(const int32_t* _
     __syncthreads();
     if (t < M) {
       const unsigned long long below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+      int iv[kMaxTopK];
 #pragma unroll
       for (int j = 0; j < kMaxTopK; ++j) {
         const int e = et[j];
+        iv[j] = -1;
         if ((unsigned)e >= (unsigned)E) continue;
         const int pos = pre[wave][e] + __popcll(mask[wave][e] & below);
-        perm[pos] = t * k + j;
-        inv_perm[t * k + j] = pos;
+        iv[j] = pos;
+        if (stage)
+          sperm[pos] = t * k + j;
+        else
+          perm[pos] = t * k + j;
+      }
+      if (inv4) {
+#pragma unroll
+        for (int q = 0; q < kMaxTopK / 4; ++q)
+          if (4 * q < k)
+            *reinterpret_cast<int4*>(inv_perm + (size_t)t * k + 4 * q) =
+                make_int4(iv[4 * q], iv[4 * q + 1], iv[4 * q + 2], iv[4 * q + 3]);
+      } else {
+#pragma unroll
+        for (int j = 0; j < kMaxTopK; ++j)
+          if (j < k && iv[j] >= 0) inv_perm[t * k + j] = iv[j];
       }
     }
     __syncthreads();
+  }
+  if (stage) {  // staged perm out in order
+    if ((reinterpret_cast<uintptr_t>(perm) & 15) == 0) {
+      for (int i = 4 * tid; i < pairs; i += 4 * kBucketThreads) {
+        if (i + 3 < pairs)
+          *reinterpret_cast<int4*>(perm + i) = make_int4(sperm[i], sperm[i + 1], sperm[i + 2], sperm[i + 3]);
+        else
+          for (int q = i; q < pairs; ++q) perm[q] = sperm[q];
+      }
+    } else {
+      for (int i = tid; i < pairs; i += kBucketThreads) perm[i] = sperm[i];
+    }
   }
   // heavy-first expert order: (count descending, id ascending); eight
   // threads per expert each count the experts ahead of it in an eighth of
@@ -784,7 +820,8 @@ hipError_t launch_bucket(const int32_t* idx, int M, int k, int E, const uint8_t*
                          int32_t* n_ltiles, hipStream_t s) {
   if (k < 1 || k > kMaxTopK || (light_rows > 0 && (!ltiles || !n_ltiles || light_mtmax < 1)))
     return hipErrorInvalidValue;
-  hipLaunchKernelGGL(bucket_kernel, dim3(1), dim3(kBucketThreads), 0, s, idx, M, k, E, resident, bm_rows, light_rows,
+  const size_t lds = (size_t)M * k <= (size_t)kBucketStage ? (size_t)M * k * sizeof(int32_t) : 0;
+  hipLaunchKernelGGL(bucket_kernel, dim3(1), dim3(kBucketThreads), lds, s, idx, M, k, E, resident, bm_rows, light_rows,
                      light_mtmax, counts, offsets, perm, inv_perm, order, tiles, n_tiles, ltiles, n_ltiles);
   return hipGetLastError();
 }
