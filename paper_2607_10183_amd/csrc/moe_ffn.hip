@@ -601,11 +601,14 @@ __global__ __launch_bounds__(kLightWaves * 64) void expert_light(MoeArgs a, int 
 }
 
 // Relative cost of one item of each tile height (light_steps 16-row steps,
-// 1, 2 or 4 token blocks), from per-item times measured on MI355X with one
-// workgroup per CU (30B-shaped layer, 512 and 2048 tokens): about 7.75 us for
-// 16-row items, 9 us for 32-row items and 6 us for 64-row items (half the
-// steps).
-__host__ __device__ constexpr int light_item_cost(int mt) { return mt == 4 ? 24 : (mt == 2 ? 36 : 31); }
+// 1, 2 or 4 token blocks) within one launch, from per-item times measured on
+// MI355X with one workgroup per CU: with 8-group slices (hidden 2048, 512 and
+// 2048 tokens) about 7.75 us for 16-row items, 9 us for 32-row items and 6 us
+// for 64-row items (half the steps); with 16-group slices (hidden 4096, 512
+// tokens) 14.4 us for 16-row and 21 us for 32-row items.
+__host__ __device__ constexpr int light_item_cost(int gs, int mt) {
+  return gs == 16 ? (mt == 2 ? 44 : 30) : (mt == 4 ? 24 : (mt == 2 ? 36 : 31));
+}
 __host__ __device__ inline int light_ncb(int N, int mt, int nc, bool down) {
   const int outs = (down ? 16 : 8) * light_steps(mt) * nc;
   return (N + outs - 1) / outs;
@@ -628,7 +631,7 @@ __global__ __launch_bounds__(kLightWaves * 64) void expert_light_all(MoeArgs a, 
   const int n0 = cls0 <= 0 ? nt.x * light_ncb(N, 4, nc, DOWN) : 0;
   const int n1 = cls0 <= 1 ? nt.y * light_ncb(N, 2, nc, DOWN) : 0;
   const int n2 = nt.z * light_ncb(N, 1, nc, DOWN);
-  constexpr int w0 = light_item_cost(4), w1 = light_item_cost(2), w2 = light_item_cost(1);
+  constexpr int w0 = light_item_cost(GS, 4), w1 = light_item_cost(GS, 2), w2 = light_item_cost(GS, 1);
   const long long tot = (long long)n0 * w0 + (long long)n1 * w1 + (long long)n2 * w2;
   if (tot == 0) return;
   // workgroups per class: the proportional share rounded down (at least one
