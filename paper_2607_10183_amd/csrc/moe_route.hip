@@ -388,8 +388,8 @@ __global__ __launch_bounds__(256) void router_partial_kernel(const __half* __res
   const int kk = threadIdx.x & 31, e8 = (threadIdx.x >> 5) * 8;
   const bool wl = e8 < E, wl2 = e8 + 64 < E;
   const int t = t0 + tr;
-  // squares of the slice's inputs, for the norm factors of the fused routing
-  const bool sq = FUSED && ro.inv_r_out && wave == 0;
+  // squares of the slice's inputs, for the norm factors the routing makes
+  const bool sq = ro.inv_r_out && wave == 0;
   float4_t acc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
   float q = 0.f;
   uint4 w0 = {0, 0, 0, 0}, w1 = {0, 0, 0, 0};
@@ -443,13 +443,16 @@ __global__ __launch_bounds__(256) void router_partial_kernel(const __half* __res
       }
     }
   }
-  if constexpr (FUSED) {
-    if (sq) {
-      // lanes tr, tr + 16, tr + 32, tr + 48 hold token tr's four 8-input groups
-      q += __shfl_xor(q, 16, 64);
-      q += __shfl_xor(q, 32, 64);
-      if (lane < 16 && t < M) st_agent(part + (size_t)gridDim.y * M * E + (size_t)blockIdx.y * M + t, q);
+  if (sq) {
+    // lanes tr, tr + 16, tr + 32, tr + 48 hold token tr's four 8-input groups
+    q += __shfl_xor(q, 16, 64);
+    q += __shfl_xor(q, 32, 64);
+    if (lane < 16 && t < M) {
+      float* dst = part + (size_t)gridDim.y * M * E + (size_t)blockIdx.y * M + t;
+      if constexpr (FUSED) st_agent(dst, q); else *dst = q;
     }
+  }
+  if constexpr (FUSED) {
     // The last workgroup to finish routes the tile.  Every thread waits until
     // its agent-scope stores are performed, then one thread counts the
     // workgroup in; the last one resets the count for the next launch and
@@ -466,15 +469,31 @@ __global__ __launch_bounds__(256) void router_partial_kernel(const __half* __res
 }
 
 // one wave per token; E <= 128 (two candidates per lane)
+// With inv_r_out the norm factors come from the partial kernel's per-slice
+// sums of squares (summed here over the slices, lane by lane, then across the
+// wave) and are written out for the expert launches.
 __global__ __launch_bounds__(256) void router_topk_kernel(const float* __restrict__ part, int n_split,
-                                                          const float* __restrict__ inv_r,
-                                                          const float* __restrict__ bias, int M, int E, int k,
-                                                          int32_t* __restrict__ idx, float* __restrict__ p,
-                                                          float* __restrict__ logits_out) {
+                                                          const float* __restrict__ inv_r, float* __restrict__ inv_r_out,
+                                                          int H, float eps, const float* __restrict__ bias, int M,
+                                                          int E, int k, int32_t* __restrict__ idx,
+                                                          float* __restrict__ p, float* __restrict__ logits_out) {
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= M) return;
-  const float rs = inv_r ? inv_r[t] : 1.f;
-  route_token(part, n_split, M, t, inv_r != nullptr, rs, bias, E, k, idx, p, logits_out);
+  float rs = 1.f;
+  if (inv_r_out) {
+    const int lane = threadIdx.x & 63;
+    const float* sq = part + (size_t)n_split * M * E;  // [slice][token]
+    float q = 0.f;
+    for (int s = lane; s < n_split; s += 64) q += sq[(size_t)s * M + t];
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) q += __shfl_xor(q, o, 64);
+    q = __shfl(q, 0, 64);  // lane 0's sum in every lane: one factor for all experts
+    rs = 1.f / sqrtf(q / (float)H + eps);
+    if (lane == 0) inv_r_out[t] = rs;
+  } else if (inv_r) {
+    rs = inv_r[t];
+  }
+  route_token(part, n_split, M, t, inv_r_out != nullptr || inv_r != nullptr, rs, bias, E, k, idx, p, logits_out);
 }
 
 // Single workgroup of 1024 threads.  Up to 16 chunks of 64 tokens are ranked
@@ -793,18 +812,14 @@ hipError_t launch_router(const __half* x, const float* inv_r, float* inv_r_out, 
                        ro);
     return hipGetLastError();
   }
-  if (inv_r_out) {
-    hipLaunchKernelGGL(rms_inv_kernel, dim3((M + 3) / 4), dim3(256), 0, s, x, M, H, eps, inv_r_out);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    inv_r = inv_r_out;
-  }
+  // with inv_r_out the partial launch also stores per-slice sums of squares
+  // and the top-k launch makes the norm factors from them
   hipLaunchKernelGGL(router_partial_kernel<false>, dim3(tiles, n_split), dim3(256), 0, s, x, wr, M, H, E, ks, part,
                      ro);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(router_topk_kernel, dim3((M + 3) / 4), dim3(256), 0, s, part, n_split, inv_r, bias, M, E, k,
-                     idx, p, logits);
+  hipLaunchKernelGGL(router_topk_kernel, dim3((M + 3) / 4), dim3(256), 0, s, part, n_split, inv_r_out ? nullptr : inv_r,
+                     inv_r_out, H, eps, bias, M, E, k, idx, p, logits);
   return hipGetLastError();
 }
 
