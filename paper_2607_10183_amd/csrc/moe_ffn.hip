@@ -137,13 +137,15 @@ __global__ __launch_bounds__(kGemmBlock, 2) void expert_down_gemm(MoeArgs a, int
 // light ones spend their K loop staging padding, and every tile walks K in
 // short LDS-staged steps whose load latency the pipeline does not cover.
 // Here an expert's tiles have 16, 32 or 64 rows (1, 2 or 4 token blocks of
-// 16: the fewest that cover its count), one launch per tile height, and the
-// weights stream through registers once per tile:
+// 16: the fewest that cover its count), every height in one launch with a
+// code path per height, and the weights stream through registers once per
+// tile:
 //   * work items are (tile, block of output columns) in tile-major order; a
-//     workgroup (one per CU) takes a contiguous run of them, so it mostly
-//     stays on one tile and its activations, and a ring of loads runs on
-//     across items, so the next item's weights are in flight while an item
-//     finishes;
+//     workgroup (one per CU) takes a contiguous run of one height's items, so
+//     it mostly stays on one tile and its activations, and a ring of loads
+//     runs on across items, so the next item's weights are in flight while an
+//     item finishes; the item metadata comes through scalar loads, so waiting
+//     for it leaves the ring's vector loads in flight;
 //   * wavefront (ks, cg) takes K-slice ks (GS groups of 32 inputs) of the
 //     light_steps(MT) 16-row steps of column group cg of an item (gate/up:
 //     steps of gate rows, then the matching steps of up rows);
